@@ -1,0 +1,164 @@
+/*
+ * pdn.h -- C ABI of the chunkwise preconditioned delta rule on MI355X (gfx950).
+ *
+ * Computes, for every batch b and head h independently, the recurrence of
+ * "Preconditioned DeltaNet" (arXiv 2604.21100), Sec. 3.5, Eq. precond_end2end,
+ * in its three instantiations (PDN: no decay; PGDN: scalar decay; PKDA:
+ * per-key-channel decay -- the decayed forms of Sec. 3.5 and App. D):
+ *
+ *   A_t  = exp(gP_t) A_{t-1} + betaP_t (k_t * k_t)            diagonal key Gram
+ *   r_t  = log(A_t) - exp(logAScale_h)
+ *   B_t  = exp(-log(x) * r_t / (1 + |r_t|))                    in [1/x, x]
+ *   kt_t = B_t * k_t                                           write key
+ *   S_t  = alpha_t S_{t-1} + beta_t (v_t - alpha_t S_{t-1} k_t) kt_t^T
+ *   o_t  = scale * S_t q_t
+ *
+ * with S_t in R^{dv x dk} (the paper's orientation), alpha_t = exp(g_t) a
+ * scalar (PGDN) or a dk-vector acting as S Diag(alpha_t) (PKDA).  The library
+ * evaluates it with the chunkwise-parallel form of Eq. chunkwise_atk_form /
+ * App. D (UT transform T = (I + tril(Diag(beta) K Kt^T, -1))^{-1} Diag(beta),
+ * W = T K, U = T V, inter-chunk state scan, chunk output).
+ *
+ * Conventions
+ *   - Every tensor argument is a DEVICE pointer to dense row-major memory owned
+ *     by the caller.  The library never allocates or frees device memory; all
+ *     scratch lives in a caller-provided workspace (pdn_workspace_size).
+ *   - Layouts: q, k, ktilde, dq, dk: [B, T, H, dk];  v, o, dO, dv: [B, T, H, dv];
+ *     beta, betaP, gP and a scalar gate g: [B, T, H];  a per-channel gate g:
+ *     [B, T, H, dk];  logAScale: [H];  A0, A_T: [B, H, dk];
+ *     S0, S_T, dS_T, dS0: [B, H, dk, dv] holding S^T (the transpose of the
+ *     paper's S), i.e. element (b, h, i, j) is S[j][i].
+ *   - q, k, v, o, ktilde and their gradients use the problem's io dtype
+ *     (IEEE fp32 or bfloat16); every other tensor is fp32.
+ *   - Calls are asynchronous on the given HIP stream (a hipStream_t passed as
+ *     void*; NULL = the null stream).  Inputs, outputs and workspace must stay
+ *     valid until the stream work completes.
+ *   - Errors: every argument is validated on the host BEFORE any HIP call;
+ *     on a validation failure the function returns the first failing code
+ *     and writes nothing.  A failed kernel launch returns PDN_ERR_HIP and
+ *     leaves the outputs undefined.  Values are not inspected: NaN / Inf in
+ *     the inputs propagate.  No exception, abort or printf crosses the ABI.
+ *   - The library keeps no mutable global state: calls are re-entrant and may
+ *     run concurrently on different streams with distinct workspaces.
+ */
+#ifndef PDN_H
+#define PDN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PDN_ABI_VERSION 1
+
+typedef enum {
+  PDN_OK = 0,
+  PDN_ERR_NULL = 1,        /* a required pointer is NULL                       */
+  PDN_ERR_SHAPE = 2,       /* B, T, H negative or sizes overflow               */
+  PDN_ERR_DTYPE = 3,       /* unknown io dtype                                 */
+  PDN_ERR_UNSUPPORTED = 4, /* dk, dv or chunk outside the built kernels        */
+  PDN_ERR_ALIGN = 5,       /* a tensor is not 16-byte aligned                  */
+  PDN_ERR_ALIAS = 6,       /* an output overlaps an input or another output    */
+  PDN_ERR_WORKSPACE = 7,   /* workspace NULL, too small or misaligned          */
+  PDN_ERR_VALUE = 8,       /* bad scalar (x < 1, non-finite x/scale) or enum,
+                              or a gate pointer inconsistent with the gate kind */
+  PDN_ERR_HIP = 9          /* a HIP launch failed                              */
+} pdn_status;
+
+typedef enum { PDN_F32 = 0, PDN_BF16 = 1 } pdn_dtype;
+
+typedef enum {
+  PDN_GATE_NONE = 0,    /* PDN:  alpha_t = 1                        */
+  PDN_GATE_SCALAR = 1,  /* PGDN: alpha_t = exp(g_t), g [B,T,H]      */
+  PDN_GATE_CHANNEL = 2  /* PKDA: alpha_t = exp(g_t), g [B,T,H,dk]   */
+} pdn_gate;
+
+typedef enum {
+  PDN_PRECOND_SQUASH = 0,   /* write key of Eq. precond_end2end (the method) */
+  PDN_PRECOND_IDENTITY = 1, /* kt = k: plain DeltaNet / GDN / KDA            */
+  PDN_PRECOND_EXTERNAL = 2  /* kt supplied by the caller in `ktilde`         */
+} pdn_precond;
+
+typedef struct {
+  int64_t B, T, H;     /* batch, sequence length, heads; 0 is allowed      */
+  int32_t dk, dv;      /* head dims: each 64 or 128                         */
+  int32_t chunk;       /* chunk length C: 64                                */
+  pdn_dtype io;        /* dtype of q, k, v, o, ktilde and their gradients   */
+  pdn_gate gate;
+  pdn_precond precond;
+  float x;             /* squash range [1/x, x]; x >= 1 (paper: 1.5)        */
+  float scale;         /* output scale (paper: 1.0)                         */
+} pdn_problem;
+
+typedef struct {
+  const void* q;             /* [B,T,H,dk] io                                */
+  const void* k;             /* [B,T,H,dk] io  (read key)                    */
+  const void* v;             /* [B,T,H,dv] io                                */
+  const float* beta;         /* [B,T,H]                                      */
+  const float* g;            /* NULL for GATE_NONE, else [B,T,H] / [B,T,H,dk] */
+  const float* beta_p;       /* [B,T,H]; SQUASH only                         */
+  const float* g_p;          /* [B,T,H] or NULL (alpha^P = 1); SQUASH only   */
+  const float* log_a_scale;  /* [H]; mu_h = exp(.); SQUASH only              */
+  const float* A0;           /* [B,H,dk] or NULL (= 0); SQUASH only          */
+  const float* S0;           /* [B,H,dk,dv] (S^T) or NULL (= 0)              */
+  const void* ktilde;        /* [B,T,H,dk] io; EXTERNAL only                 */
+} pdn_inputs;
+
+typedef struct {
+  void* o;      /* [B,T,H,dv] io                                             */
+  float* S_T;   /* [B,H,dk,dv] final state S_T^T, or NULL                    */
+  float* A_T;   /* [B,H,dk] final preconditioner state, or NULL (SQUASH only) */
+} pdn_fwd_out;
+
+typedef struct {
+  void* dq;              /* [B,T,H,dk] io                                    */
+  void* dk;              /* [B,T,H,dk] io                                    */
+  void* dv;              /* [B,T,H,dv] io                                    */
+  float* dbeta;          /* [B,T,H]                                          */
+  float* dg;             /* [B,T,H] / [B,T,H,dk]; NULL iff GATE_NONE         */
+  float* dS0;            /* [B,H,dk,dv] or NULL                              */
+  float* dbeta_p;        /* [B,T,H] or NULL (SQUASH)                         */
+  float* dg_p;           /* [B,T,H] or NULL (SQUASH)                         */
+  float* dlog_a_scale;   /* [H] or NULL (SQUASH)                             */
+  float* dA0;            /* [B,H,dk] or NULL (SQUASH)                        */
+  void* dktilde;         /* [B,T,H,dk] io, EXTERNAL only, or NULL            */
+} pdn_bwd_out;
+
+/* Bytes of workspace pdn_chunk_fwd (with_bwd = 0) or pdn_chunk_bwd
+ * (with_bwd = 1) needs for this problem.  Host-only, no HIP call.
+ * Returns PDN_ERR_NULL / SHAPE / DTYPE / UNSUPPORTED / VALUE for a bad
+ * problem; *bytes is written only on PDN_OK. */
+pdn_status pdn_workspace_size(const pdn_problem* problem, int with_bwd,
+                              size_t* bytes);
+
+/* Forward pass (Eq. chunkwise_atk_form with the preconditioner of Eq.
+ * precond_end2end; decayed forms of App. D).  Writes o and, when non-NULL,
+ * S_T and A_T.  `ws` must be 256-byte aligned and at least
+ * pdn_workspace_size(problem, 0) bytes.  Asynchronous on `hip_stream`. */
+pdn_status pdn_chunk_fwd(const pdn_problem* problem, const pdn_inputs* in,
+                         pdn_fwd_out* out, void* ws, size_t ws_bytes,
+                         void* hip_stream);
+
+/* Backward pass: gradients of <dO, o> + <dS_T, S_T> with respect to every
+ * input of pdn_chunk_fwd (App. C, backward pseudocode).  dO is [B,T,H,dv]
+ * io; dS_T is [B,H,dk,dv] fp32 or NULL (= 0).  The forward intermediates are
+ * recomputed; `ws` must hold pdn_workspace_size(problem, 1) bytes.  The
+ * output pointers dbeta_p, dg_p, dlog_a_scale, dA0 and dS0 may be NULL to
+ * skip them. */
+pdn_status pdn_chunk_bwd(const pdn_problem* problem, const pdn_inputs* in,
+                         const void* dO, const float* dS_T, pdn_bwd_out* out,
+                         void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Static, NUL-terminated description of a status code. */
+const char* pdn_status_string(pdn_status status);
+
+/* PDN_ABI_VERSION of the built library. */
+int pdn_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PDN_H */

@@ -1,0 +1,193 @@
+"""Chunkwise preconditioned delta rule (PDN / PGDN / PKDA) on MI355X.
+
+Thin ctypes binding of libpdn.so, the C ABI declared in include/pdn.h.  The
+binding only marshals arguments: it maps torch tensors to device pointers,
+allocates outputs and the workspace when the caller does not pass them, and
+turns status codes into exceptions.  Every step of the computation runs in
+the library's HIP kernels; there is no fallback.  Importing this package
+fails loudly if the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpdn.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build the HIP library first "
+        "(python -c 'import __graft_entry__ as g; g.build()' or "
+        "python paper_2604_21100_amd/_build.py)")
+_lib = ctypes.CDLL(LIB_PATH)
+
+# ---------------------------------------------------------------- enums
+PDN_OK, PDN_ERR_NULL, PDN_ERR_SHAPE, PDN_ERR_DTYPE, PDN_ERR_UNSUPPORTED, \
+    PDN_ERR_ALIGN, PDN_ERR_ALIAS, PDN_ERR_WORKSPACE, PDN_ERR_VALUE, \
+    PDN_ERR_HIP = range(10)
+PDN_F32, PDN_BF16 = 0, 1
+PDN_GATE_NONE, PDN_GATE_SCALAR, PDN_GATE_CHANNEL = 0, 1, 2
+PDN_PRECOND_SQUASH, PDN_PRECOND_IDENTITY, PDN_PRECOND_EXTERNAL = 0, 1, 2
+
+GATES = {"none": PDN_GATE_NONE, "scalar": PDN_GATE_SCALAR,
+         "channel": PDN_GATE_CHANNEL}
+PRECONDS = {"squash": PDN_PRECOND_SQUASH, "identity": PDN_PRECOND_IDENTITY,
+            "external": PDN_PRECOND_EXTERNAL}
+
+_vp = ctypes.c_void_p
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int64), ("T", ctypes.c_int64),
+                ("H", ctypes.c_int64), ("dk", ctypes.c_int32),
+                ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
+                ("io", ctypes.c_int), ("gate", ctypes.c_int),
+                ("precond", ctypes.c_int), ("x", ctypes.c_float),
+                ("scale", ctypes.c_float)]
+
+
+class Inputs(ctypes.Structure):
+    _fields_ = [(n, _vp) for n in ("q", "k", "v", "beta", "g", "beta_p",
+                                   "g_p", "log_a_scale", "A0", "S0",
+                                   "ktilde")]
+
+
+class FwdOut(ctypes.Structure):
+    _fields_ = [("o", _vp), ("S_T", _vp), ("A_T", _vp)]
+
+
+class BwdOut(ctypes.Structure):
+    _fields_ = [(n, _vp) for n in ("dq", "dk", "dv", "dbeta", "dg", "dS0",
+                                   "dbeta_p", "dg_p", "dlog_a_scale", "dA0",
+                                   "dktilde")]
+
+
+_lib.pdn_workspace_size.argtypes = [ctypes.POINTER(Problem), ctypes.c_int,
+                                    ctypes.POINTER(ctypes.c_size_t)]
+_lib.pdn_workspace_size.restype = ctypes.c_int
+_lib.pdn_chunk_fwd.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs),
+                               ctypes.POINTER(FwdOut), _vp, ctypes.c_size_t,
+                               _vp]
+_lib.pdn_chunk_fwd.restype = ctypes.c_int
+_lib.pdn_chunk_bwd.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs),
+                               _vp, _vp, ctypes.POINTER(BwdOut), _vp,
+                               ctypes.c_size_t, _vp]
+_lib.pdn_chunk_bwd.restype = ctypes.c_int
+_lib.pdn_status_string.argtypes = [ctypes.c_int]
+_lib.pdn_status_string.restype = ctypes.c_char_p
+_lib.pdn_abi_version.argtypes = []
+_lib.pdn_abi_version.restype = ctypes.c_int
+
+EXPORTED = ("pdn_workspace_size", "pdn_chunk_fwd", "pdn_chunk_bwd",
+            "pdn_status_string", "pdn_abi_version")
+
+
+class PdnError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {pdn_status_string(status)} "
+                         f"(status {status})")
+
+
+def pdn_status_string(status: int) -> str:
+    return _lib.pdn_status_string(int(status)).decode()
+
+
+def pdn_abi_version() -> int:
+    return _lib.pdn_abi_version()
+
+
+def make_problem(B, T, H, dk, dv, *, io="bf16", gate="none",
+                 precond="squash", x=1.5, scale=1.0, chunk=64) -> Problem:
+    return Problem(B, T, H, dk, dv, chunk,
+                   PDN_BF16 if io == "bf16" else PDN_F32,
+                   GATES[gate] if isinstance(gate, str) else int(gate),
+                   PRECONDS[precond] if isinstance(precond, str)
+                   else int(precond), x, scale)
+
+
+def pdn_workspace_size(problem: Problem, with_bwd: bool = False) -> int:
+    n = ctypes.c_size_t(0)
+    st = _lib.pdn_workspace_size(ctypes.byref(problem), int(with_bwd),
+                                 ctypes.byref(n))
+    if st != PDN_OK:
+        raise PdnError(st, "pdn_workspace_size")
+    return n.value
+
+
+# ------------------------------------------------------- raw pointer calls
+def pdn_chunk_fwd_raw(problem: Problem, inputs: Inputs, out: FwdOut, ws: int,
+                      ws_bytes: int, stream: int) -> int:
+    """Direct call with raw pointers; returns the status code."""
+    return _lib.pdn_chunk_fwd(ctypes.byref(problem), ctypes.byref(inputs),
+                              ctypes.byref(out), ws, ws_bytes, stream)
+
+
+def pdn_chunk_bwd_raw(problem: Problem, inputs: Inputs, dO: int, dS_T: int,
+                      out: BwdOut, ws: int, ws_bytes: int,
+                      stream: int) -> int:
+    return _lib.pdn_chunk_bwd(ctypes.byref(problem), ctypes.byref(inputs), dO,
+                              dS_T, ctypes.byref(out), ws, ws_bytes, stream)
+
+
+# ------------------------------------------------------- torch marshalling
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libpdn must be contiguous")
+    return t.data_ptr()
+
+
+def _io_of(t):
+    import torch
+    if t.dtype == torch.bfloat16:
+        return "bf16"
+    if t.dtype == torch.float32:
+        return "f32"
+    raise TypeError(f"q/k/v must be float32 or bfloat16, got {t.dtype}")
+
+
+def _stream(stream, device):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return s.cuda_stream
+
+
+def _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde):
+    return Inputs(*[_ptr(t) for t in (q, k, v, beta, g, beta_p, g_p,
+                                      log_a_scale, A0, S0, ktilde)])
+
+
+def pdn_chunk_fwd(q, k, v, beta, *, g=None, gate="none", precond="squash",
+                  beta_p=None, g_p=None, log_a_scale=None, A0=None, S0=None,
+                  ktilde=None, x=1.5, scale=1.0, chunk=64, o=None, S_T=None,
+                  A_T=None, want_state=True, workspace=None, stream=None):
+    """Forward pass on torch device tensors in the ABI layouts of pdn.h.
+
+    Returns (o, S_T, A_T); S_T / A_T are None when not requested.  Outputs and
+    the workspace are allocated with torch when not given."""
+    import torch
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    io = _io_of(q)
+    prob = make_problem(B, T, H, dk, dv, io=io, gate=gate, precond=precond,
+                        x=x, scale=scale, chunk=chunk)
+    dev = q.device
+    if o is None:
+        o = torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
+    if S_T is None and want_state:
+        S_T = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev)
+    if A_T is None and want_state and precond == "squash":
+        A_T = torch.empty((B, H, dk), dtype=torch.float32, device=dev)
+    nbytes = pdn_workspace_size(prob, False)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    inp = _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde)
+    out = FwdOut(_ptr(o), _ptr(S_T), _ptr(A_T))
+    st = pdn_chunk_fwd_raw(prob, inp, out, _ptr(workspace),
+                           workspace.numel(), _stream(stream, dev))
+    if st != PDN_OK:
+        raise PdnError(st, "pdn_chunk_fwd")
+    return o, S_T, A_T

@@ -1,0 +1,234 @@
+// C ABI of libpdn: argument validation (host only, before any HIP call),
+// workspace sizing and kernel sequencing.  See include/pdn.h.
+#include "../../include/pdn.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <vector>
+
+#include "pdn_internal.hpp"
+
+namespace {
+
+using pdn::kChunk;
+
+struct Range {
+  uintptr_t lo, hi;  // [lo, hi)
+};
+
+bool overlap(const Range& a, const Range& b) {
+  return a.lo < b.hi && b.lo < a.hi;
+}
+
+// checked multiply of non-negative sizes
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+  if (a < 0 || b < 0) return false;
+  if (a != 0 && b > INT64_MAX / a) return false;
+  *out = a * b;
+  return true;
+}
+
+struct Sizes {
+  int64_t BH, NT, tok;        // tok = B*T*H
+  int64_t nq, nv, nscal, ngate, nS, nA;
+  int esz;
+};
+
+pdn_status check_problem(const pdn_problem* p, Sizes* sz) {
+  if (!p) return PDN_ERR_NULL;
+  if (p->B < 0 || p->T < 0 || p->H < 0) return PDN_ERR_SHAPE;
+  if (p->io != PDN_F32 && p->io != PDN_BF16) return PDN_ERR_DTYPE;
+  if ((p->dk != 64 && p->dk != 128) || (p->dv != 64 && p->dv != 128)) return PDN_ERR_UNSUPPORTED;
+  if (p->chunk != kChunk) return PDN_ERR_UNSUPPORTED;
+  if (p->gate != PDN_GATE_NONE && p->gate != PDN_GATE_SCALAR && p->gate != PDN_GATE_CHANNEL)
+    return PDN_ERR_VALUE;
+  if (p->precond != PDN_PRECOND_SQUASH && p->precond != PDN_PRECOND_IDENTITY &&
+      p->precond != PDN_PRECOND_EXTERNAL)
+    return PDN_ERR_VALUE;
+  if (!std::isfinite(p->x) || !(p->x >= 1.0f) || !std::isfinite(p->scale)) return PDN_ERR_VALUE;
+  Sizes s{};
+  int64_t bt;
+  if (!mul_ok(p->B, p->H, &s.BH) || !mul_ok(p->B, p->T, &bt) || !mul_ok(bt, p->H, &s.tok))
+    return PDN_ERR_SHAPE;
+  s.NT = (p->T + kChunk - 1) / kChunk;
+  int64_t tpad;
+  if (!mul_ok(s.NT, kChunk, &tpad)) return PDN_ERR_SHAPE;
+  // every element count used below must fit in int64 (with a generous margin
+  // for the workspace's byte counts)
+  int64_t tmp;
+  if (!mul_ok(s.tok, 128, &s.nq) || !mul_ok(s.BH, tpad, &tmp) || !mul_ok(tmp, 128 * 8, &tmp) ||
+      !mul_ok(s.BH, 128 * 128 * 4, &tmp))
+    return PDN_ERR_SHAPE;
+  if (s.NT > (int64_t)1 << 30 || s.BH * s.NT > (int64_t)INT32_MAX) return PDN_ERR_SHAPE;
+  s.nq = s.tok * p->dk;
+  s.nv = s.tok * p->dv;
+  s.nscal = s.tok;
+  s.ngate = p->gate == PDN_GATE_NONE ? 0 : (p->gate == PDN_GATE_SCALAR ? s.tok : s.tok * p->dk);
+  s.nS = s.BH * p->dk * p->dv;
+  s.nA = s.BH * p->dk;
+  s.esz = p->io == PDN_BF16 ? 2 : 4;
+  *sz = s;
+  return PDN_OK;
+}
+
+Range rng(const void* p, int64_t bytes) {
+  const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+  return Range{a, a + static_cast<uintptr_t>(bytes)};
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Buf {
+  const void* p;
+  int64_t bytes;
+};
+
+// outputs must not overlap inputs, each other or the workspace; the workspace
+// must not overlap inputs
+pdn_status check_aliasing(const std::vector<Buf>& ins, const std::vector<Buf>& outs, Buf ws) {
+  for (size_t i = 0; i < outs.size(); ++i) {
+    if (!outs[i].p || outs[i].bytes == 0) continue;
+    const Range ro = rng(outs[i].p, outs[i].bytes);
+    for (const Buf& in : ins)
+      if (in.p && in.bytes && overlap(ro, rng(in.p, in.bytes))) return PDN_ERR_ALIAS;
+    for (size_t j = i + 1; j < outs.size(); ++j)
+      if (outs[j].p && outs[j].bytes && overlap(ro, rng(outs[j].p, outs[j].bytes))) return PDN_ERR_ALIAS;
+    if (ws.p && ws.bytes && overlap(ro, rng(ws.p, ws.bytes))) return PDN_ERR_ALIAS;
+  }
+  if (ws.p && ws.bytes)
+    for (const Buf& in : ins)
+      if (in.p && in.bytes && overlap(rng(ws.p, ws.bytes), rng(in.p, in.bytes))) return PDN_ERR_ALIAS;
+  return PDN_OK;
+}
+
+pdn_status check_inputs(const pdn_problem* p, const pdn_inputs* in, const Sizes& s,
+                        std::vector<Buf>* bufs) {
+  if (!in) return PDN_ERR_NULL;
+  const bool empty = s.tok == 0;
+  // per-token tensors are only dereferenced when there are tokens
+  if (!empty) {
+    if (!in->q || !in->k || !in->v || !in->beta) return PDN_ERR_NULL;
+    if (p->gate != PDN_GATE_NONE && !in->g) return PDN_ERR_NULL;
+    if (p->precond == PDN_PRECOND_SQUASH && (!in->beta_p || !in->log_a_scale)) return PDN_ERR_NULL;
+    if (p->precond == PDN_PRECOND_EXTERNAL && !in->ktilde) return PDN_ERR_NULL;
+  }
+  if (p->gate == PDN_GATE_NONE && in->g) return PDN_ERR_VALUE;
+  const int64_t e = s.esz;
+  std::vector<Buf> b = {
+      {in->q, s.nq * e}, {in->k, s.nq * e}, {in->v, s.nv * e}, {in->beta, s.nscal * 4},
+      {in->g, s.ngate * 4}, {in->S0, s.nS * 4},
+  };
+  if (p->precond == PDN_PRECOND_SQUASH) {
+    b.push_back({in->beta_p, s.nscal * 4});
+    b.push_back({in->g_p, s.nscal * 4});
+    b.push_back({in->log_a_scale, p->H * 4});
+    b.push_back({in->A0, s.nA * 4});
+  }
+  if (p->precond == PDN_PRECOND_EXTERNAL) b.push_back({in->ktilde, s.nq * e});
+  for (const Buf& x : b)
+    if (x.p && !aligned16(x.p)) return PDN_ERR_ALIGN;
+  *bufs = b;
+  return PDN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pdn_status_string(pdn_status st) {
+  switch (st) {
+    case PDN_OK: return "ok";
+    case PDN_ERR_NULL: return "a required pointer is NULL";
+    case PDN_ERR_SHAPE: return "invalid or overflowing shape";
+    case PDN_ERR_DTYPE: return "unknown io dtype";
+    case PDN_ERR_UNSUPPORTED: return "head dimension or chunk size not supported (dk, dv in {64, 128}; chunk 64)";
+    case PDN_ERR_ALIGN: return "a tensor is not 16-byte aligned";
+    case PDN_ERR_ALIAS: return "an output overlaps an input, another output or the workspace";
+    case PDN_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case PDN_ERR_VALUE: return "invalid scalar, enum or gate pointer";
+    case PDN_ERR_HIP: return "HIP launch failed";
+  }
+  return "unknown status";
+}
+
+int pdn_abi_version(void) { return PDN_ABI_VERSION; }
+
+pdn_status pdn_workspace_size(const pdn_problem* p, int with_bwd, size_t* bytes) {
+  if (!bytes) return PDN_ERR_NULL;
+  Sizes s;
+  const pdn_status st = check_problem(p, &s);
+  if (st != PDN_OK) return st;
+  (void)with_bwd;
+  const pdn::WsLayout L = pdn::fwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, s.esz, p->gate,
+                                             p->precond);
+  *bytes = L.total;
+  return PDN_OK;
+}
+
+pdn_status pdn_chunk_fwd(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out* out, void* ws,
+                         size_t ws_bytes, void* hip_stream) {
+  Sizes s;
+  pdn_status st = check_problem(p, &s);
+  if (st != PDN_OK) return st;
+  std::vector<Buf> ins;
+  if ((st = check_inputs(p, in, s, &ins)) != PDN_OK) return st;
+  if (!out) return PDN_ERR_NULL;
+  if (s.tok > 0 && !out->o) return PDN_ERR_NULL;
+  if (p->precond != PDN_PRECOND_SQUASH && out->A_T) return PDN_ERR_VALUE;
+  const std::vector<Buf> outs = {{out->o, s.nv * s.esz}, {out->S_T, s.nS * 4}, {out->A_T, s.nA * 4}};
+  for (const Buf& x : outs)
+    if (x.p && !aligned16(x.p)) return PDN_ERR_ALIGN;
+  const pdn::WsLayout L = pdn::fwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, s.esz, p->gate,
+                                             p->precond);
+  const bool need_ws = s.tok > 0;
+  // the whole declared workspace range must be disjoint from inputs/outputs;
+  // its size is checked last
+  if ((st = check_aliasing(ins, outs, Buf{ws, need_ws ? static_cast<int64_t>(ws_bytes) : 0})) != PDN_OK)
+    return st;
+  if (need_ws && (!ws || ws_bytes < L.total || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0))
+    return PDN_ERR_WORKSPACE;
+
+  pdn::FwdArgs a{};
+  a.B = p->B; a.T = p->T; a.H = p->H; a.BH = s.BH;
+  a.NT = static_cast<int>(s.NT);
+  a.Tpad = s.NT * kChunk;
+  a.dk = p->dk; a.dv = p->dv;
+  a.gate = p->gate; a.precond = p->precond;
+  a.lnx = std::log(p->x);
+  a.scale = p->scale;
+  a.q = in->q; a.k = in->k; a.v = in->v; a.ktilde = in->ktilde;
+  a.beta = in->beta; a.g = in->g; a.beta_p = in->beta_p; a.g_p = in->g_p;
+  a.log_a_scale = in->log_a_scale; a.A0 = in->A0; a.S0 = in->S0;
+  a.o = out->o; a.S_T = out->S_T; a.A_T = out->A_T;
+  char* w = static_cast<char*>(ws);
+  if (need_ws) {
+    if (p->precond == PDN_PRECOND_SQUASH) {
+      a.sumL = reinterpret_cast<float*>(w + L.sumL);
+      a.sumD = reinterpret_cast<float*>(w + L.sumD);
+      a.Abound = reinterpret_cast<float*>(w + L.Abound);
+    }
+    a.KtG = w + L.KtG;
+    a.Tm = w + L.Tm;
+    a.Pm = w + L.Pm;
+    if (p->gate != PDN_GATE_NONE) a.G = reinterpret_cast<float*>(w + L.G);
+  }
+  if (s.BH == 0) return PDN_OK;
+  const hipError_t e = pdn::launch_forward(a, p->io == PDN_BF16, static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? PDN_OK : PDN_ERR_HIP;
+}
+
+pdn_status pdn_chunk_bwd(const pdn_problem* p, const pdn_inputs* in, const void* dO,
+                         const float* dS_T, pdn_bwd_out* out, void* ws, size_t ws_bytes,
+                         void* hip_stream) {
+  Sizes s;
+  pdn_status st = check_problem(p, &s);
+  if (st != PDN_OK) return st;
+  std::vector<Buf> ins;
+  if ((st = check_inputs(p, in, s, &ins)) != PDN_OK) return st;
+  (void)dO; (void)dS_T; (void)out; (void)ws; (void)ws_bytes; (void)hip_stream;
+  return PDN_ERR_UNSUPPORTED;
+}
+
+}  // extern "C"

@@ -1,0 +1,155 @@
+"""The C ABI on the host: the library loads, exports every function the
+header declares, and rejects bad arguments before touching the GPU.  No call
+here reaches a kernel launch (every call fails validation or only sizes the
+workspace), so these run without a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pdn.h")
+
+pdn = pytest.importorskip("paper_2604_21100_amd",
+                          reason="libpdn.so not built")
+
+A = 1 << 20   # fake, 256-byte aligned addresses; never dereferenced
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pdn_\w+)\s*\(", text)))
+
+
+def test_header_symbols_exported():
+    names = header_functions()
+    assert set(names) == set(pdn.EXPORTED)
+    lib = ctypes.CDLL(pdn.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert pdn.pdn_abi_version() == 1
+
+
+def test_status_strings():
+    for st in range(10):
+        assert pdn.pdn_status_string(st)
+    assert pdn.pdn_status_string(0) == "ok"
+
+
+def _prob(**kw):
+    base = dict(B=2, T=130, H=3, dk=128, dv=64, io="bf16", gate="scalar",
+                precond="squash")
+    base.update(kw)
+    return pdn.make_problem(**base)
+
+
+def _inputs(**kw):
+    names = [f[0] for f in pdn.Inputs._fields_]
+    vals = dict(q=A * 1, k=A * 2, v=A * 3, beta=A * 4, g=A * 5, beta_p=A * 6,
+                g_p=A * 7, log_a_scale=A * 8, A0=None, S0=None, ktilde=None)
+    vals.update(kw)
+    return pdn.Inputs(*[vals[n] for n in names])
+
+
+def _fwd(prob, inp=None, out=None, ws=A * 64, ws_bytes=None):
+    if inp is None:
+        inp = _inputs()
+    if out is None:
+        out = pdn.FwdOut(A * 20, A * 21, A * 22)
+    if ws_bytes is None:
+        try:
+            ws_bytes = pdn.pdn_workspace_size(prob) - 1   # always too small
+        except pdn.PdnError:
+            ws_bytes = 0
+    return pdn.pdn_chunk_fwd_raw(prob, inp, out, ws, ws_bytes, 0)
+
+
+def test_workspace_size_monotone_and_validated():
+    a = pdn.pdn_workspace_size(_prob(T=64))
+    b = pdn.pdn_workspace_size(_prob(T=65))
+    c = pdn.pdn_workspace_size(_prob(T=130, gate="channel"))
+    assert 0 < a < b < c
+    assert pdn.pdn_workspace_size(_prob(B=0)) == 0
+    with pytest.raises(pdn.PdnError) as e:
+        pdn.pdn_workspace_size(_prob(dk=96))
+    assert e.value.status == pdn.PDN_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dk=96), pdn.PDN_ERR_UNSUPPORTED),
+    (dict(dv=256), pdn.PDN_ERR_UNSUPPORTED),
+    (dict(chunk=32), pdn.PDN_ERR_UNSUPPORTED),
+    (dict(B=-1), pdn.PDN_ERR_SHAPE),
+    (dict(T=-5), pdn.PDN_ERR_SHAPE),
+    (dict(B=1 << 40, T=1 << 30), pdn.PDN_ERR_SHAPE),
+    (dict(x=0.9), pdn.PDN_ERR_VALUE),
+    (dict(x=float("nan")), pdn.PDN_ERR_VALUE),
+    (dict(scale=float("inf")), pdn.PDN_ERR_VALUE),
+    (dict(gate=7), pdn.PDN_ERR_VALUE),
+    (dict(precond=5), pdn.PDN_ERR_VALUE),
+])
+def test_problem_validation(kw, code):
+    assert _fwd(_prob(**kw)) == code
+
+
+def test_bad_dtype():
+    p = _prob()
+    p.io = 9
+    assert _fwd(p) == pdn.PDN_ERR_DTYPE
+
+
+@pytest.mark.parametrize("field", ["q", "k", "v", "beta", "g", "beta_p",
+                                   "log_a_scale"])
+def test_null_required_pointer(field):
+    assert _fwd(_prob(), _inputs(**{field: None})) == pdn.PDN_ERR_NULL
+
+
+def test_null_pointer_cases():
+    assert pdn.pdn_chunk_fwd_raw(_prob(), _inputs(), pdn.FwdOut(None, None, None),
+                                 A * 64, 16, 0) == pdn.PDN_ERR_NULL
+    assert _fwd(_prob(precond="external")) == pdn.PDN_ERR_NULL   # no ktilde
+    # g_p may be NULL (alpha^P = 1): the failure is then the workspace size
+    assert _fwd(_prob(), _inputs(g_p=None)) == pdn.PDN_ERR_WORKSPACE
+
+
+def test_gate_pointer_must_match_kind():
+    assert _fwd(_prob(gate="none")) == pdn.PDN_ERR_VALUE   # g given
+
+
+def test_misaligned():
+    assert _fwd(_prob(), _inputs(q=A + 2)) == pdn.PDN_ERR_ALIGN
+    assert _fwd(_prob(), out=pdn.FwdOut(A * 20 + 8, None, None)) == pdn.PDN_ERR_ALIGN
+
+
+def test_workspace_checks():
+    p = _prob()
+    n = pdn.pdn_workspace_size(p)
+    assert _fwd(p, ws=None, ws_bytes=n - 1) == pdn.PDN_ERR_WORKSPACE
+    assert _fwd(p, ws_bytes=n - 1) == pdn.PDN_ERR_WORKSPACE
+    # a misaligned workspace of sufficient size is only checked on hosts
+    # where a launch cannot happen
+    if not os.path.exists("/dev/kfd"):
+        assert _fwd(p, ws=A * 64 + 16, ws_bytes=n) == pdn.PDN_ERR_WORKSPACE
+
+
+def test_aliasing():
+    # the workspace is one byte short in every call, so even a missed alias
+    # could not reach a launch
+    p = _prob()
+    # o overlaps v
+    assert _fwd(p, out=pdn.FwdOut(A * 3 + 256, None, None)) == pdn.PDN_ERR_ALIAS
+    # S_T overlaps o
+    assert _fwd(p, out=pdn.FwdOut(A * 20, A * 20 + 512, None)) == pdn.PDN_ERR_ALIAS
+    # workspace overlaps q
+    assert _fwd(p, ws=A * 1 - 256) == pdn.PDN_ERR_ALIAS
+    # A_T only exists for the squash preconditioner
+    assert _fwd(_prob(precond="identity"), _inputs(beta_p=None)) == pdn.PDN_ERR_VALUE
+
+
+def test_backward_validates_first():
+    p = _prob(dk=96)
+    st = pdn.pdn_chunk_bwd_raw(p, _inputs(), A * 30, None,
+                               pdn.BwdOut(*([None] * 11)), A * 64, 0, 0)
+    assert st == pdn.PDN_ERR_UNSUPPORTED
