@@ -141,6 +141,22 @@ pdn_status pdn_chunk_fwd(const pdn_problem* problem, const pdn_inputs* in,
                          pdn_fwd_out* out, void* ws, size_t ws_bytes,
                          void* hip_stream);
 
+/* pdn_chunk_fwd that also records caller-created HIP events (hipEvent_t
+ * handles passed as void*) on `hip_stream` at the stage boundaries, for
+ * timing individual kernels:
+ *   stage_events[0]  before the preconditioner scan (k1_*; empty unless
+ *                    SQUASH)
+ *   stage_events[1]  after it / before the per-chunk prep kernel (k2)
+ *   stage_events[2]  after k2 / before the inter-chunk scan + output (k3)
+ *   stage_events[3]  after k3
+ * n_events must be 4 (else PDN_ERR_VALUE).  The events stay owned by the
+ * caller; results are identical to pdn_chunk_fwd. */
+#define PDN_FWD_STAGE_EVENTS 4
+pdn_status pdn_chunk_fwd_events(const pdn_problem* problem, const pdn_inputs* in,
+                                pdn_fwd_out* out, void* ws, size_t ws_bytes,
+                                void* hip_stream, void* const* stage_events,
+                                int n_events);
+
 /* Backward pass: gradients of <dO, o> + <dS_T, S_T> with respect to every
  * input of pdn_chunk_fwd (App. C, backward pseudocode).  dO is [B,T,H,dv]
  * io; dS_T is [B,H,dk,dv] fp32 or NULL (= 0).  The forward intermediates are

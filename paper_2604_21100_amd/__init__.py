@@ -70,6 +70,10 @@ _lib.pdn_chunk_fwd.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs),
                                ctypes.POINTER(FwdOut), _vp, ctypes.c_size_t,
                                _vp]
 _lib.pdn_chunk_fwd.restype = ctypes.c_int
+_lib.pdn_chunk_fwd_events.argtypes = [
+    ctypes.POINTER(Problem), ctypes.POINTER(Inputs), ctypes.POINTER(FwdOut),
+    _vp, ctypes.c_size_t, _vp, ctypes.POINTER(_vp), ctypes.c_int]
+_lib.pdn_chunk_fwd_events.restype = ctypes.c_int
 _lib.pdn_chunk_bwd.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs),
                                _vp, _vp, ctypes.POINTER(BwdOut), _vp,
                                ctypes.c_size_t, _vp]
@@ -79,8 +83,9 @@ _lib.pdn_status_string.restype = ctypes.c_char_p
 _lib.pdn_abi_version.argtypes = []
 _lib.pdn_abi_version.restype = ctypes.c_int
 
-EXPORTED = ("pdn_workspace_size", "pdn_chunk_fwd", "pdn_chunk_bwd",
-            "pdn_status_string", "pdn_abi_version")
+EXPORTED = ("pdn_workspace_size", "pdn_chunk_fwd", "pdn_chunk_fwd_events",
+            "pdn_chunk_bwd", "pdn_status_string", "pdn_abi_version")
+FWD_STAGES = ("precond", "chunk_prep", "chunk_scan")
 
 
 class PdnError(RuntimeError):
@@ -124,6 +129,16 @@ def pdn_chunk_fwd_raw(problem: Problem, inputs: Inputs, out: FwdOut, ws: int,
                               ctypes.byref(out), ws, ws_bytes, stream)
 
 
+def pdn_chunk_fwd_events_raw(problem: Problem, inputs: Inputs, out: FwdOut,
+                             ws: int, ws_bytes: int, stream: int,
+                             events) -> int:
+    """pdn_chunk_fwd_events with raw hipEvent_t handles (ints)."""
+    arr = (_vp * len(events))(*events)
+    return _lib.pdn_chunk_fwd_events(ctypes.byref(problem),
+                                     ctypes.byref(inputs), ctypes.byref(out),
+                                     ws, ws_bytes, stream, arr, len(events))
+
+
 def pdn_chunk_bwd_raw(problem: Problem, inputs: Inputs, dO: int, dS_T: int,
                       out: BwdOut, ws: int, ws_bytes: int,
                       stream: int) -> int:
@@ -163,11 +178,14 @@ def _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde):
 def pdn_chunk_fwd(q, k, v, beta, *, g=None, gate="none", precond="squash",
                   beta_p=None, g_p=None, log_a_scale=None, A0=None, S0=None,
                   ktilde=None, x=1.5, scale=1.0, chunk=64, o=None, S_T=None,
-                  A_T=None, want_state=True, workspace=None, stream=None):
+                  A_T=None, want_state=True, workspace=None, stream=None,
+                  stage_events=None):
     """Forward pass on torch device tensors in the ABI layouts of pdn.h.
 
     Returns (o, S_T, A_T); S_T / A_T are None when not requested.  Outputs and
-    the workspace are allocated with torch when not given."""
+    the workspace are allocated with torch when not given.  stage_events: 4
+    recorded-at-stage-boundary torch.cuda.Event objects (see
+    pdn_chunk_fwd_events), or None."""
     import torch
     B, T, H, dk = q.shape
     dv = v.shape[-1]
@@ -186,8 +204,21 @@ def pdn_chunk_fwd(q, k, v, beta, *, g=None, gate="none", precond="squash",
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     inp = _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde)
     out = FwdOut(_ptr(o), _ptr(S_T), _ptr(A_T))
-    st = pdn_chunk_fwd_raw(prob, inp, out, _ptr(workspace),
-                           workspace.numel(), _stream(stream, dev))
+    if stage_events is None:
+        st = pdn_chunk_fwd_raw(prob, inp, out, _ptr(workspace),
+                               workspace.numel(), _stream(stream, dev))
+    else:
+        st = pdn_chunk_fwd_events_raw(
+            prob, inp, out, _ptr(workspace), workspace.numel(),
+            _stream(stream, dev), [_event_handle(e) for e in stage_events])
     if st != PDN_OK:
         raise PdnError(st, "pdn_chunk_fwd")
     return o, S_T, A_T
+
+
+def _event_handle(ev):
+    """Raw hipEvent_t of a torch.cuda.Event (created on first use)."""
+    if ev.cuda_event == 0:
+        import torch
+        ev.record(torch.cuda.current_stream())   # forces creation
+    return ev.cuda_event

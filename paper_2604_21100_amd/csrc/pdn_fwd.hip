@@ -574,8 +574,10 @@ static hipError_t launch_k2_prec(const FwdArgs& a, hipStream_t s) {
 }
 
 template <typename T, int DK>
-static hipError_t launch_all(const FwdArgs& a, hipStream_t s) {
+static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* ev) {
   hipError_t e;
+  auto mark = [&](int i) { return ev ? hipEventRecord(ev[i], s) : hipSuccess; };
+  if ((e = mark(0)) != hipSuccess) return e;
   if (a.precond == kSquash) {
     hipLaunchKernelGGL((k1_precond_summary<T, DK>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(DK),
                        0, s, a);
@@ -583,12 +585,14 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s) {
     hipLaunchKernelGGL((k1_precond_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
+  if ((e = mark(1)) != hipSuccess) return e;
   switch (a.gate) {
     case kGateNone: e = launch_k2_prec<T, DK, kGateNone>(a, s); break;
     case kGateScalar: e = launch_k2_prec<T, DK, kGateScalar>(a, s); break;
     default: e = launch_k2_prec<T, DK, kGateChannel>(a, s); break;
   }
   if (e != hipSuccess) return e;
+  if ((e = mark(2)) != hipSuccess) return e;
   const int64_t nslab = a.dv / BV;
   const unsigned grid = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
   switch (a.gate) {
@@ -599,10 +603,17 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s) {
     default:
       hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel>), dim3(grid), dim3(256), 0, s, a); break;
   }
-  return hipGetLastError();
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return mark(3);
 }
 
-hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t s) {
+hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev) {
+  if (a.BH == 0 || a.T == 0) {
+    // nothing to time: the stage events still mark the (empty) stages
+    if (ev)
+      for (int i = 0; i < 4; ++i)
+        if (hipEventRecord(ev[i], s) != hipSuccess) return hipErrorInvalidValue;
+  }
   if (a.BH == 0) return hipSuccess;
   if (a.T == 0) {
     const int64_t nS = a.BH * a.dk * a.dv, nA = a.BH * a.dk;
@@ -612,9 +623,9 @@ hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t s) {
     return hipGetLastError();
   }
   if (io_bf16) {
-    return a.dk == 64 ? launch_all<bf16, 64>(a, s) : launch_all<bf16, 128>(a, s);
+    return a.dk == 64 ? launch_all<bf16, 64>(a, s, ev) : launch_all<bf16, 128>(a, s, ev);
   }
-  return a.dk == 64 ? launch_all<float, 64>(a, s) : launch_all<float, 128>(a, s);
+  return a.dk == 64 ? launch_all<float, 64>(a, s, ev) : launch_all<float, 128>(a, s, ev);
 }
 
 }  // namespace pdn

@@ -167,8 +167,9 @@ pdn_status pdn_workspace_size(const pdn_problem* p, int with_bwd, size_t* bytes)
   return PDN_OK;
 }
 
-pdn_status pdn_chunk_fwd(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out* out, void* ws,
-                         size_t ws_bytes, void* hip_stream) {
+static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out* out,
+                                 void* ws, size_t ws_bytes, void* hip_stream,
+                                 hipEvent_t const* ev) {
   Sizes s;
   pdn_status st = check_problem(p, &s);
   if (st != PDN_OK) return st;
@@ -214,9 +215,25 @@ pdn_status pdn_chunk_fwd(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out
     a.Pm = w + L.Pm;
     if (p->gate != PDN_GATE_NONE) a.G = reinterpret_cast<float*>(w + L.G);
   }
-  if (s.BH == 0) return PDN_OK;
-  const hipError_t e = pdn::launch_forward(a, p->io == PDN_BF16, static_cast<hipStream_t>(hip_stream));
+  const hipError_t e =
+      pdn::launch_forward(a, p->io == PDN_BF16, static_cast<hipStream_t>(hip_stream), ev);
   return e == hipSuccess ? PDN_OK : PDN_ERR_HIP;
+}
+
+pdn_status pdn_chunk_fwd(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out* out, void* ws,
+                         size_t ws_bytes, void* hip_stream) {
+  return chunk_fwd_impl(p, in, out, ws, ws_bytes, hip_stream, nullptr);
+}
+
+pdn_status pdn_chunk_fwd_events(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out* out,
+                                void* ws, size_t ws_bytes, void* hip_stream,
+                                void* const* stage_events, int n_events) {
+  if (!stage_events) return PDN_ERR_NULL;
+  if (n_events != PDN_FWD_STAGE_EVENTS) return PDN_ERR_VALUE;
+  for (int i = 0; i < n_events; ++i)
+    if (!stage_events[i]) return PDN_ERR_NULL;
+  return chunk_fwd_impl(p, in, out, ws, ws_bytes, hip_stream,
+                        reinterpret_cast<hipEvent_t const*>(stage_events));
 }
 
 pdn_status pdn_chunk_bwd(const pdn_problem* p, const pdn_inputs* in, const void* dO,

@@ -55,6 +55,9 @@ struct WsLayout {
 
 WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precond);
 
-hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t stream);
+// ev: NULL or 4 events recorded at the stage boundaries (see
+// pdn_chunk_fwd_events)
+hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t stream,
+                          hipEvent_t const* ev = nullptr);
 
 }  // namespace pdn
