@@ -78,6 +78,17 @@ __device__ __forceinline__ void st8(float* p, const Frag8<float>& f) {
   *reinterpret_cast<floatx4*>(p + 4) = f.hi;
 }
 
+// base + a 32-bit byte offset: lets the backend use the scalar-base +
+// vector-offset global addressing form (no 64-bit per-lane arithmetic)
+template <typename T>
+__device__ __forceinline__ const T* at_bytes(const T* base, uint32_t byte_off) {
+  return reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + byte_off);
+}
+template <typename T>
+__device__ __forceinline__ T* at_bytes(T* base, uint32_t byte_off) {
+  return reinterpret_cast<T*>(reinterpret_cast<char*>(base) + byte_off);
+}
+
 // acc += A_frag * B_frag over one 32-deep slab
 __device__ __forceinline__ void mma(floatx4& acc, const Frag8<bf16>& a, const Frag8<bf16>& b) {
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, acc, 0, 0, 0);

@@ -24,26 +24,62 @@ namespace pdn {
 constexpr int C = kChunk;
 
 // ---------------------------------------------------------------- K1
+// The chunk's affine summary: A_end = exp(sum gP) A_start + L with
+// L = sum_r betaP_r exp(GP_end - GP_r) k_r^2, GP the in-chunk prefix of gP.
+// Rows are weighted in parallel, then reduced per channel.
 template <typename T, int DK>
-__global__ __launch_bounds__(DK) void k1_precond_summary(FwdArgs a) {
+__global__ __launch_bounds__(256) void k1_precond_summary(FwdArgs a) {
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int VPR = DK / VEC;       // 16-byte vectors per row
+  constexpr int RPP = 256 / VPR;      // rows per pass
+  __shared__ float sW[C];
+  __shared__ __attribute__((aligned(16))) float sRed[RPP * DK];
   const int64_t blk = blockIdx.x;
   const int64_t bh = blk / a.NT;
   const int i = static_cast<int>(blk % a.NT);
   const int64_t b = bh / a.H, h = bh % a.H;
-  const int c = threadIdx.x;
+  const int tid = threadIdx.x;
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
-  const T* k = static_cast<const T*>(a.k);
-  float L = 0.f, D = 0.f;
-  for (int r = 0; r < n; ++r) {
+  if (tid < 64) {
+    const int r = tid;
     const int64_t sidx = (b * a.T + t0 + r) * a.H + h;
-    const float gp = a.g_p ? a.g_p[sidx] : 0.f;
-    const float kv = to_f(k[sidx * DK + c]);
-    L = fast_exp(gp) * L + a.beta_p[sidx] * kv * kv;
-    D += gp;
+    float gp = (r < n && a.g_p) ? a.g_p[sidx] : 0.f;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const float y = __shfl_up(gp, off, 64);
+      if (r >= off) gp += y;
+    }
+    const float gend = __shfl(gp, 63, 64);
+    sW[r] = r < n ? a.beta_p[sidx] * fast_exp(gend - gp) : 0.f;
+    if (r == 0) a.sumD[bh * a.NT + i] = gend;
   }
-  a.sumL[(bh * a.NT + i) * DK + c] = L;
-  if (c == 0) a.sumD[bh * a.NT + i] = D;
+  __syncthreads();
+  const T* k = static_cast<const T*>(a.k);
+  const int cg = tid % VPR, r0 = tid / VPR;
+  float acc[VEC];
+#pragma unroll
+  for (int s = 0; s < VEC; ++s) acc[s] = 0.f;
+  for (int r = r0; r < n; r += RPP) {
+    const T* src = k + ((b * a.T + t0 + r) * a.H + h) * DK + cg * VEC;
+    float4 raw = *reinterpret_cast<const float4*>(src);
+    const T* e = reinterpret_cast<const T*>(&raw);
+    const float wr = sW[r];
+#pragma unroll
+    for (int s = 0; s < VEC; ++s) {
+      const float kv = to_f(e[s]);
+      acc[s] += wr * kv * kv;
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < VEC; ++s) sRed[r0 * DK + cg * VEC + s] = acc[s];
+  __syncthreads();
+  if (tid < DK) {
+    float L = 0.f;
+#pragma unroll
+    for (int r = 0; r < RPP; ++r) L += sRed[r * DK + tid];
+    a.sumL[(bh * a.NT + i) * DK + tid] = L;
+  }
 }
 
 template <int DK>
@@ -86,7 +122,8 @@ struct K2Smem {
   static constexpr size_t kGc = GATE == kGateChannel ? sizeof(float) * C * (DK + 4) : 0;
   static constexpr size_t kY = sizeof(float) * 4 * 16 * 17;
   static constexpr size_t kScal = sizeof(float) * 5 * C;
-  static constexpr size_t kTotal = kR1 + kR2 + kR3 + kGc + kY + kScal;
+  static constexpr size_t kSeg = sizeof(float) * 2 * 256;   // preconditioner segment carries
+  static constexpr size_t kTotal = kR1 + kR2 + kR3 + kGc + kY + kScal + kSeg;
 };
 
 template <typename T, int DK, int GATE, int PREC>
@@ -106,6 +143,8 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   float* sEgp = sBp + C;
   float* sG = sEgp + C;
   float* sGraw = sG + C;
+  float* sSegE = sGraw + C;
+  float* sSegP = sSegE + 256;
 
   const int64_t blk = blockIdx.x;
   const int64_t bh = blk / a.NT;
@@ -183,14 +222,29 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         gout[(int64_t)r * DK] = acc;
       }
     }
-    if (PREC == kSquash) {
-      float A = a.Abound[(bh * (a.NT + 1) + i) * DK + c];
-      const float mu = fast_exp(a.log_a_scale[h]);
-      for (int r = 0; r < C; ++r) {
-        const float kv = to_f(sK[r * LDK + c]);
-        A = sEgp[r] * A + sBp[r] * kv * kv;
-        sKt[r * LDK + c] = from_f<T>(squash_gain(A, mu, a.lnx) * kv);
-      }
+  }
+  if (PREC == kSquash) {
+    // the in-chunk prefix A_r = a_r A_{r-1} + bP_r k_r^2 in NSEG row segments:
+    // pass 1 reduces each segment to (prod a, partial sum), the segments are
+    // chained from the chunk-start state, pass 2 re-walks its rows
+    constexpr int NSEG = 256 / DK, SEG = C / NSEG;
+    const int c = tid % DK, sg = tid / DK;
+    float E = 1.f, Pp = 0.f;
+    for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
+      const float kv = to_f(sK[r * LDK + c]);
+      E *= sEgp[r];
+      Pp = sEgp[r] * Pp + sBp[r] * kv * kv;
+    }
+    sSegE[sg * DK + c] = E;
+    sSegP[sg * DK + c] = Pp;
+    __syncthreads();
+    float A = a.Abound[(bh * (a.NT + 1) + i) * DK + c];
+    for (int q = 0; q < sg; ++q) A = sSegE[q * DK + c] * A + sSegP[q * DK + c];
+    const float mu = fast_exp(a.log_a_scale[h]);
+    for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
+      const float kv = to_f(sK[r * LDK + c]);
+      A = sEgp[r] * A + sBp[r] * kv * kv;
+      sKt[r * LDK + c] = from_f<T>(squash_gain(A, mu, a.lnx) * kv);
     }
   }
   __syncthreads();
@@ -340,14 +394,261 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
 // ---------------------------------------------------------------- K3
 constexpr int BV = 32;  // value columns per workgroup
 
+// One thread's share of a chunk's C x BV value (or output) slab, as 16-byte
+// vectors: vector j of thread tid covers row idx / kSegs, elements
+// [(idx % kSegs) * kVec, + kVec) with idx = tid + 256 j.
+template <typename T>
+struct SlabMap {
+  static constexpr int kVec = 16 / static_cast<int>(sizeof(T));
+  static constexpr int kSegs = BV / kVec;
+  static constexpr int kPer = C * kSegs / 256;
+};
+
+// Operands one wave needs for one chunk, loaded two chunks ahead of use.
+// A-operand rows: token 16w + lr of the chunk; decayed write keys: rows
+// c = 16*(w*CT + ct) + lr.  Gate values are kept raw (log-domain) and the
+// value slab raw: nothing here is consumed at load time, so the loads stay
+// in flight across the compute of the chunks before it.
+//
+// Rows past the end of the sequence (last chunk only) are loaded from the
+// last valid row instead of being zeroed: their T columns and rows are zero
+// (beta = 0 on padded rows), so they cannot reach any stored output.
+template <typename T, int DK, int GATE>
+struct ScanFrags {
+  static constexpr int KK = DK / 32, CT = DK / 64;
+  Frag8<T> K[KK], Q[KK], Tm[2], P[2], G[CT][2];
+  float4 v[SlabMap<T>::kPer];                      // value slab share
+  float g[GATE == kGateScalar ? 4 : 1];            // G of rows 16w + 4lg + ii
+  float gC[GATE == kGateChannel ? CT : 1][GATE == kGateNone ? 1 : 4];  // G at the chunk end
+  float gk[GATE == kGateChannel ? KK : 1][GATE == kGateChannel ? 8 : 1];  // G of the A rows
+};
+
+struct ScanCtx {
+  int64_t b, h, bh;
+  int v0, w, lr, lg, tid;
+};
+
+// Each chunk's loads are a wave-uniform (scalar) base plus a 32-bit lane
+// byte offset, so the loop does almost no per-lane address arithmetic.
+template <typename T, int DK, int GATE>
+__device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdArgs& a, int i,
+                                          const ScanCtx& x) {
+  constexpr int KK = DK / 32, CT = DK / 64;
+  constexpr uint32_t E = sizeof(T);
+  using SM = SlabMap<T>;
+  const int64_t t0 = static_cast<int64_t>(i) * C;
+  const int last = static_cast<int>(min<int64_t>(C, a.T - t0)) - 1;
+  const int64_t HD = a.H * (int64_t)DK, HV = a.H * (int64_t)a.dv;
+  const T* kb = static_cast<const T*>(a.k) + (x.b * a.T + t0) * HD + x.h * DK;
+  const T* qb = static_cast<const T*>(a.q) + (x.b * a.T + t0) * HD + x.h * DK;
+  const T* vb = static_cast<const T*>(a.v) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0;
+  const T* tb = static_cast<const T*>(a.Tm) + (x.bh * a.NT + i) * (int64_t)(C * C);
+  const T* pb = static_cast<const T*>(a.Pm) + (x.bh * a.NT + i) * (int64_t)(C * C);
+  const T* gb = static_cast<const T*>(a.KtG) + (x.bh * a.NT + i) * (int64_t)(DK * C);
+  const uint32_t rr = static_cast<uint32_t>(min(16 * x.w + x.lr, last));
+  const uint32_t okq = (rr * static_cast<uint32_t>(HD) + 8 * x.lg) * E;
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    f.K[kk] = ld8(at_bytes(kb, okq + kk * 32 * E));
+    f.Q[kk] = ld8(at_bytes(qb, okq + kk * 32 * E));
+  }
+  const int ra = 16 * x.w + x.lr;
+  const uint32_t otp = static_cast<uint32_t>(ra * C + 8 * x.lg) * E;
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2) {
+    f.Tm[k2] = ld8(at_bytes(tb, otp + k2 * 32 * E));
+    f.P[k2] = ld8(at_bytes(pb, otp + k2 * 32 * E));
+  }
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2)
+      f.G[ct][k2] = ld8(at_bytes(gb, static_cast<uint32_t>((16 * (x.w * CT + ct) + x.lr) * C + 8 * x.lg + k2 * 32) * E));
+#pragma unroll
+  for (int j = 0; j < SM::kPer; ++j) {
+    const int idx = x.tid + 256 * j;
+    const uint32_t row = static_cast<uint32_t>(min(idx / SM::kSegs, last));
+    const uint32_t off = (row * static_cast<uint32_t>(HV) + (idx % SM::kSegs) * SM::kVec) * E;
+    f.v[j] = *reinterpret_cast<const float4*>(at_bytes(vb, off));
+  }
+  if (GATE == kGateScalar) {
+    const float* gs = a.G + x.bh * a.Tpad + t0;
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii)
+      f.g[ii] = *at_bytes(gs, static_cast<uint32_t>(16 * x.w + 4 * x.lg + ii) * 4u);
+    f.gC[0][0] = gs[C - 1];
+  }
+  if (GATE == kGateChannel) {
+    const float* gr = a.G + (x.bh * a.Tpad + t0) * DK + static_cast<uint32_t>(ra * DK + 8 * x.lg);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int s = 0; s < 8; ++s) f.gk[kk][s] = gr[kk * 32 + s];
+    const float* ge = a.G + (x.bh * a.Tpad + t0 + C - 1) * DK;
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) f.gC[ct][ii] = ge[16 * (x.w * CT + ct) + 4 * x.lg + ii];
+  }
+}
+
+// Workgroup barrier that only orders LDS: outstanding global loads (the
+// next chunks' prefetch) stay in flight.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// value slab share -> sVt[v][t] (transposed)
+template <typename T>
+__device__ __forceinline__ void stage_values(const float4 (&v)[SlabMap<T>::kPer], T* sVt,
+                                             int tid) {
+  using SM = SlabMap<T>;
+  constexpr int LDE = C + 8;
+#pragma unroll
+  for (int j = 0; j < SM::kPer; ++j) {
+    const int idx = tid + 256 * j;
+    const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
+    const T* e = reinterpret_cast<const T*>(&v[j]);
+#pragma unroll
+    for (int s = 0; s < SM::kVec; ++s) sVt[(c0 + s) * LDE + row] = e[s];
+  }
+}
+
+// sO[v][t] -> o rows of chunk i (coalesced 16-byte stores); n valid rows
+template <typename T>
+__device__ __forceinline__ void flush_output(const FwdArgs& a, int i, int n, const T* sO,
+                                             const ScanCtx& x) {
+  using SM = SlabMap<T>;
+  constexpr int LDE = C + 8;
+  const int64_t t0 = static_cast<int64_t>(i) * C;
+  const int64_t HV = a.H * (int64_t)a.dv;
+  T* ob = static_cast<T*>(a.o) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0;
+#pragma unroll
+  for (int j = 0; j < SM::kPer; ++j) {
+    const int idx = x.tid + 256 * j;
+    const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
+    float4 pk;
+    T* e = reinterpret_cast<T*>(&pk);
+#pragma unroll
+    for (int s = 0; s < SM::kVec; ++s) e[s] = sO[(c0 + s) * LDE + row];
+    if (row < n)
+      *reinterpret_cast<float4*>(at_bytes(ob, (static_cast<uint32_t>(row) * static_cast<uint32_t>(HV) + c0) *
+                                                  static_cast<uint32_t>(sizeof(T)))) = pk;
+  }
+}
+
+// One chunk step.  On entry sVt holds this chunk's values and sO the previous
+// chunk's output (flushed first).  FULL: C valid tokens, so the step has no
+// per-row branches (a conditional store would make the compiler wait for the
+// prefetched loads); the ragged last chunk takes FULL = false.
+template <bool FULL, typename T, int DK, int GATE>
+__device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float4* vnext,
+                                          floatx4 (&st)[DK / 64][2], const FwdArgs& a, int i,
+                                          const ScanCtx& x, T* sH, T* sX, T* sE, T* sVt, T* sO) {
+  constexpr int KK = DK / 32, CT = DK / 64;
+  constexpr int LDH = DK + 8, LDE = C + 8;
+  const int w = x.w, lr = x.lr, lg = x.lg;
+  if (i > 0) flush_output<T>(a, i - 1, C, sO, x);   // only full chunks precede this one
+  float lam[4];
+#pragma unroll
+  for (int ii = 0; ii < 4; ++ii) lam[ii] = GATE == kGateScalar ? fast_exp(f.g[ii]) : 1.f;
+  if (GATE == kGateChannel) {
+    // Lam = exp(G) per (token, channel) on the read key and the query
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const float e = fast_exp(f.gk[kk][s]);
+        f.K[kk].set(s, f.K[kk].get(s) * e);
+        f.Q[kk].set(s, f.Q[kk].get(s) * e);
+      }
+  }
+  // ---- (Lam K) S^T and (Lam Q) S^T;  X = V - (Lam K) S^T
+  Frag8<T> bH[2][KK];
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) bH[vt][kk] = ld8(sH + (16 * vt + lr) * LDH + kk * 32 + 8 * lg);
+  typename Vec4<T>::type vv[2];
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt)
+    vv[vt] = *reinterpret_cast<const typename Vec4<T>::type*>(sVt + (16 * vt + lr) * LDE + 16 * w + 4 * lg);
+  floatx4 accX[2], accO[2];
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt) {
+    accX[vt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    accO[vt] = accX[vt];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      mma(accX[vt], f.K[kk], bH[vt][kk]);
+      mma(accO[vt], f.Q[kk], bH[vt][kk]);
+    }
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      accX[vt][ii] = to_f(vv[vt][ii]) - lam[ii] * accX[vt][ii];
+      accO[vt][ii] *= lam[ii];
+    }
+    st4<T>(sX + (16 * vt + lr) * LDE + 16 * w + 4 * lg, accX[vt][0], accX[vt][1], accX[vt][2],
+           accX[vt][3]);
+  }
+  lds_barrier();
+  // ---- E = T X
+  Frag8<T> bX[2][2];
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) bX[vt][k2] = ld8(sX + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg);
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt) {
+    floatx4 accE = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) mma(accE, f.Tm[k2], bX[vt][k2]);
+    st4<T>(sE + (16 * vt + lr) * LDE + 16 * w + 4 * lg, accE[0], accE[1], accE[2], accE[3]);
+  }
+  lds_barrier();
+  // ---- O = scale [ (Lam Q) S^T + P E ];  S^T <- Diag(gamma_C) S^T + (Kt Gamma)^T E
+  Frag8<T> fE[2][2];
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) fE[vt][k2] = ld8(sE + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg);
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt) {
+    // P is causal: for rows < 32 its second slab is zero
+    mma(accO[vt], f.P[0], fE[vt][0]);
+    mma(accO[vt], f.P[1], fE[vt][1]);
+    st4<T>(sO + (16 * vt + lr) * LDE + 16 * w + 4 * lg, a.scale * accO[vt][0], a.scale * accO[vt][1],
+           a.scale * accO[vt][2], a.scale * accO[vt][3]);
+  }
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int vt = 0; vt < 2; ++vt) {
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        float gam = 1.f;
+        if (GATE == kGateScalar) gam = fast_exp(f.gC[0][0]);
+        if (GATE == kGateChannel) gam = fast_exp(f.gC[ct][ii]);
+        st[ct][vt][ii] *= gam;
+      }
+      mma(st[ct][vt], f.G[ct][0], fE[vt][0]);
+      mma(st[ct][vt], f.G[ct][1], fE[vt][1]);
+      st4<T>(sH + (16 * vt + lr) * LDH + 16 * (w * CT + ct) + 4 * lg, st[ct][vt][0], st[ct][vt][1],
+             st[ct][vt][2], st[ct][vt][3]);
+    }
+  if (vnext) stage_values<T>(*reinterpret_cast<const float4(*)[SlabMap<T>::kPer]>(vnext), sVt, x.tid);
+  lds_barrier();
+}
+
 template <typename T, int DK, int GATE>
 __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   constexpr int CT = DK / 64;       // state row tiles per wave
-  constexpr int KK = DK / 32;       // contraction slabs over d_k
   constexpr int LDH = DK + 8, LDE = C + 8;
-  __shared__ __attribute__((aligned(16))) T sH[BV * LDH];  // bf16/fp32 copy of S^T slab, [v][c]
-  __shared__ __attribute__((aligned(16))) T sX[BV * LDE];  // X = V - Lam K S^T, [v][t]
-  __shared__ __attribute__((aligned(16))) T sE[BV * LDE];  // E = T X, [v][t]
+  __shared__ __attribute__((aligned(16))) T sH[BV * LDH];   // io copy of the S^T slab, [v][c]
+  __shared__ __attribute__((aligned(16))) T sX[BV * LDE];   // X = V - Lam K S^T, [v][t]
+  __shared__ __attribute__((aligned(16))) T sE[BV * LDE];   // E = T X, [v][t]
+  __shared__ __attribute__((aligned(16))) T sVt[BV * LDE];  // this chunk's values, [v][t]
+  __shared__ __attribute__((aligned(16))) T sO[BV * LDE];   // last chunk's output, [v][t]
 
   const int nslab = a.dv / BV;
   const int64_t bid = blockIdx.x;
@@ -356,17 +657,17 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   const int slab = static_cast<int>(j8 % nslab);
   const int64_t bh = (j8 / nslab) * 8 + xcd;  // slabs of one head share an XCD (and its L2)
   if (bh >= a.BH) return;
-  const int64_t b = bh / a.H, h = bh % a.H;
-  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 15, lg = l >> 4;
-  const int v0 = slab * BV;
+  ScanCtx x;
+  x.bh = bh;
+  x.b = bh / a.H;
+  x.h = bh % a.H;
+  x.tid = threadIdx.x;
+  x.w = x.tid >> 6;
+  x.lr = x.tid & 15;
+  x.lg = (x.tid & 63) >> 4;
+  x.v0 = slab * BV;
+  const int w = x.w, lr = x.lr, lg = x.lg;
   const int DV = a.dv;
-  const T* qp = static_cast<const T*>(a.q);
-  const T* kp = static_cast<const T*>(a.k);
-  const T* vp = static_cast<const T*>(a.v);
-  T* op = static_cast<T*>(a.o);
-  const T* Tm = static_cast<const T*>(a.Tm);
-  const T* Pm = static_cast<const T*>(a.Pm);
-  const T* KtG = static_cast<const T*>(a.KtG);
 
   // state slab: rows c = 16*(w*CT+ct) + 4*lg + ii, column v0 + 16*vt + lr
   floatx4 st[CT][2];
@@ -377,7 +678,7 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
         const int c = 16 * (w * CT + ct) + 4 * lg + ii;
-        st[ct][vt][ii] = a.S0 ? a.S0[(bh * DK + c) * DV + v0 + 16 * vt + lr] : 0.f;
+        st[ct][vt][ii] = a.S0 ? a.S0[(bh * DK + c) * DV + x.v0 + 16 * vt + lr] : 0.f;
       }
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
@@ -385,136 +686,44 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
     for (int vt = 0; vt < 2; ++vt)
       st4<T>(sH + (16 * vt + lr) * LDH + 16 * (w * CT + ct) + 4 * lg, st[ct][vt][0],
              st[ct][vt][1], st[ct][vt][2], st[ct][vt][3]);
+
+  // software pipeline, three deep: chunk i+2's operands load while chunk i
+  // computes.  The loop covers the full chunks, three per trip, with no exit
+  // in the middle and unconditional prefetches (past the end they re-read
+  // the last chunk), so every path into the loop header has the same loads
+  // in flight and the compiler's wait counts stay exact.  A ragged last chunk
+  // runs after it.
+  ScanFrags<T, DK, GATE> f0, f1, f2;
+  const int last = a.NT - 1;
+  const int NF = static_cast<int>(a.T / C);   // full chunks
+  scan_load(f0, a, 0, x);
+  scan_load(f1, a, min(1, last), x);
+  stage_values<T>(f0.v, sVt, x.tid);
   __syncthreads();
-
-  const int rr = 16 * w + lr;  // A-operand row (token in chunk) of this lane
-  for (int i = 0; i < a.NT; ++i) {
-    const int64_t t0 = static_cast<int64_t>(i) * C;
-    const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
-    // ---- operand fragments for this wave
-    Frag8<T> fK[KK], fQ[KK], fT[2], fP[2], fG[CT][2];
-    const bool rok = rr < n;
-    const int64_t rowoff = ((b * a.T + t0 + rr) * a.H + h) * DK;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      if (rok) {
-        fK[kk] = ld8(kp + rowoff + kk * 32 + 8 * lg);
-        fQ[kk] = ld8(qp + rowoff + kk * 32 + 8 * lg);
-      } else {
-        fK[kk] = frag_zero<T>();
-        fQ[kk] = frag_zero<T>();
-      }
-    }
-    const int64_t cc = (bh * a.NT + i) * (int64_t)(C * C);
-#pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
-      fT[k2] = ld8(Tm + cc + rr * C + k2 * 32 + 8 * lg);
-      fP[k2] = ld8(Pm + cc + rr * C + k2 * 32 + 8 * lg);
-    }
-    const int64_t kg = (bh * a.NT + i) * (int64_t)(DK * C);
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2)
-        fG[ct][k2] = ld8(KtG + kg + (16 * (w * CT + ct) + lr) * C + k2 * 32 + 8 * lg);
-    // values in accumulator layout: rows 16w + 4lg + ii, column v0 + 16vt + lr
-    float vv[2][4], lam[4];
-#pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-      const int t = 16 * w + 4 * lg + ii;
-      lam[ii] = 1.f;
-      if (GATE == kGateScalar) lam[ii] = fast_exp(a.G[bh * a.Tpad + t0 + t]);
-#pragma unroll
-      for (int vt = 0; vt < 2; ++vt)
-        vv[vt][ii] = t < n ? to_f(vp[((b * a.T + t0 + t) * a.H + h) * DV + v0 + 16 * vt + lr]) : 0.f;
-    }
-    if (GATE == kGateChannel) {
-      // Lam = exp(G) per (token, channel) on the read key and the query
-      const float* gr = a.G + (bh * a.Tpad + t0 + rr) * DK;
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          const float e = fast_exp(gr[kk * 32 + 8 * lg + s]);
-          fK[kk].set(s, fK[kk].get(s) * e);
-          fQ[kk].set(s, fQ[kk].get(s) * e);
-        }
-    }
-
-    // ---- (Lam K) S^T and (Lam Q) S^T
-    floatx4 accX[2], accO[2];
-#pragma unroll
-    for (int vt = 0; vt < 2; ++vt) {
-      accX[vt] = floatx4{0.f, 0.f, 0.f, 0.f};
-      accO[vt] = accX[vt];
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        const Frag8<T> bH = ld8(sH + (16 * vt + lr) * LDH + kk * 32 + 8 * lg);
-        mma(accX[vt], fK[kk], bH);
-        mma(accO[vt], fQ[kk], bH);
-      }
-#pragma unroll
-      for (int ii = 0; ii < 4; ++ii) {
-        accX[vt][ii] = vv[vt][ii] - lam[ii] * accX[vt][ii];
-        accO[vt][ii] *= lam[ii];
-      }
-      st4<T>(sX + (16 * vt + lr) * LDE + 16 * w + 4 * lg, accX[vt][0], accX[vt][1], accX[vt][2],
-             accX[vt][3]);
-    }
-    __syncthreads();
-
-    // ---- E = T X
-    floatx4 accE[2];
-#pragma unroll
-    for (int vt = 0; vt < 2; ++vt) {
-      accE[vt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2)
-        mma(accE[vt], fT[k2], ld8(sX + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg));
-      st4<T>(sE + (16 * vt + lr) * LDE + 16 * w + 4 * lg, accE[vt][0], accE[vt][1], accE[vt][2],
-             accE[vt][3]);
-    }
-    __syncthreads();
-
-    // ---- O = scale [ (Lam Q) S^T + P E ];  S^T <- Diag(gamma_C) S^T + (Kt Gamma)^T E
-    Frag8<T> fE[2][2];
-#pragma unroll
-    for (int vt = 0; vt < 2; ++vt)
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) fE[vt][k2] = ld8(sE + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg);
-#pragma unroll
-    for (int vt = 0; vt < 2; ++vt) {
-      mma(accO[vt], fP[0], fE[vt][0]);
-      if (w >= 2) mma(accO[vt], fP[1], fE[vt][1]);
-#pragma unroll
-      for (int ii = 0; ii < 4; ++ii) {
-        const int t = 16 * w + 4 * lg + ii;
-        if (t < n) op[((b * a.T + t0 + t) * a.H + h) * DV + v0 + 16 * vt + lr] = from_f<T>(a.scale * accO[vt][ii]);
-      }
-    }
-    float gam[CT][4];
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-      for (int ii = 0; ii < 4; ++ii) {
-        gam[ct][ii] = 1.f;
-        if (GATE == kGateScalar) gam[ct][ii] = fast_exp(a.G[bh * a.Tpad + t0 + C - 1]);
-        if (GATE == kGateChannel)
-          gam[ct][ii] = fast_exp(a.G[(bh * a.Tpad + t0 + C - 1) * DK + 16 * (w * CT + ct) + 4 * lg + ii]);
-      }
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-      for (int vt = 0; vt < 2; ++vt) {
-#pragma unroll
-        for (int ii = 0; ii < 4; ++ii) st[ct][vt][ii] *= gam[ct][ii];
-        mma(st[ct][vt], fG[ct][0], fE[vt][0]);
-        mma(st[ct][vt], fG[ct][1], fE[vt][1]);
-        st4<T>(sH + (16 * vt + lr) * LDH + 16 * (w * CT + ct) + 4 * lg, st[ct][vt][0], st[ct][vt][1],
-               st[ct][vt][2], st[ct][vt][3]);
-      }
-    __syncthreads();
+  int i = 0;
+  for (; i + 2 < NF; i += 3) {
+    scan_load(f2, a, i + 2, x);
+    scan_step<true>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_load(f0, a, min(i + 3, last), x);
+    scan_step<true>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
+    scan_load(f1, a, min(i + 4, last), x);
+    scan_step<true>(f2, f0.v, st, a, i + 2, x, sH, sX, sE, sVt, sO);
   }
+  // f0, f1 hold chunks i, i + 1 (clamped to the last chunk)
+  if (NF - i == 2) {
+    scan_load(f2, a, min(i + 2, last), x);
+    scan_step<true>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<true>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
+    i += 2;
+    if (i < a.NT) scan_step<false>(f2, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+  } else if (NF - i == 1) {
+    scan_step<true>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    i += 1;
+    if (i < a.NT) scan_step<false>(f1, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+  } else if (i < a.NT) {
+    scan_step<false>(f0, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+  }
+  flush_output<T>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
   if (a.S_T) {
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
@@ -523,7 +732,7 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) {
           const int c = 16 * (w * CT + ct) + 4 * lg + ii;
-          a.S_T[(bh * DK + c) * DV + v0 + 16 * vt + lr] = st[ct][vt][ii];
+          a.S_T[(bh * DK + c) * DV + x.v0 + 16 * vt + lr] = st[ct][vt][ii];
         }
   }
 }
@@ -579,7 +788,7 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
   auto mark = [&](int i) { return ev ? hipEventRecord(ev[i], s) : hipSuccess; };
   if ((e = mark(0)) != hipSuccess) return e;
   if (a.precond == kSquash) {
-    hipLaunchKernelGGL((k1_precond_summary<T, DK>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(DK),
+    hipLaunchKernelGGL((k1_precond_summary<T, DK>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
                        0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((k1_precond_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, a);
