@@ -222,3 +222,56 @@ def _event_handle(ev):
         import torch
         ev.record(torch.cuda.current_stream())   # forces creation
     return ev.cuda_event
+
+
+def pdn_chunk_bwd(q, k, v, beta, dO, *, g=None, gate="none", precond="squash",
+                  beta_p=None, g_p=None, log_a_scale=None, A0=None, S0=None,
+                  ktilde=None, dS_T=None, x=1.5, scale=1.0, chunk=64,
+                  outputs=None, want_optional=True, workspace=None,
+                  stream=None):
+    """Backward pass on torch device tensors (layouts of pdn.h).
+
+    Returns a dict with dq, dk, dv, dbeta and, when present, dg, dS0 and the
+    preconditioner gradients dbeta_p, dg_p, dlog_a_scale, dA0 (squash) or
+    dktilde (external).  Outputs and the workspace are allocated with torch
+    when not given (``outputs``: dict of preallocated tensors)."""
+    import torch
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    io = _io_of(q)
+    prob = make_problem(B, T, H, dk, dv, io=io, gate=gate, precond=precond,
+                        x=x, scale=scale, chunk=chunk)
+    dev = q.device
+    f32 = torch.float32
+    out = dict(outputs or {})
+
+    def need(name, shape, dtype):
+        if name not in out:
+            out[name] = torch.empty(shape, dtype=dtype, device=dev)
+
+    need("dq", (B, T, H, dk), q.dtype)
+    need("dk", (B, T, H, dk), q.dtype)
+    need("dv", (B, T, H, dv), q.dtype)
+    need("dbeta", (B, T, H), f32)
+    if gate != "none":
+        need("dg", tuple(g.shape), f32)
+    if want_optional:
+        need("dS0", (B, H, dk, dv), f32)
+        if precond == "squash":
+            need("dbeta_p", (B, T, H), f32)
+            need("dg_p", (B, T, H), f32)
+            need("dlog_a_scale", (H,), f32)
+            need("dA0", (B, H, dk), f32)
+        if precond == "external":
+            need("dktilde", (B, T, H, dk), q.dtype)
+    nbytes = pdn_workspace_size(prob, True)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    inp = _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde)
+    bo = BwdOut(*[_ptr(out.get(n)) for n, _ in BwdOut._fields_])
+    st = pdn_chunk_bwd_raw(prob, inp, _ptr(dO), _ptr(dS_T), bo,
+                           _ptr(workspace), workspace.numel(),
+                           _stream(stream, dev))
+    if st != PDN_OK:
+        raise PdnError(st, "pdn_chunk_bwd")
+    return out

@@ -13,7 +13,7 @@ ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libpdn.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 
-SOURCES = ["pdn_host.cpp", "pdn_fwd.hip"]
+SOURCES = ["pdn_host.cpp", "pdn_fwd.hip", "pdn_bwd.hip"]
 
 # Packed-fp32 VALU ops are disabled for all device code (they have produced
 # silent wrong results on this hardware generation); hipcc's host pass warns

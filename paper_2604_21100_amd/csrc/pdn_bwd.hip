@@ -1,0 +1,929 @@
+// Backward kernels of the chunkwise preconditioned delta rule for gfx950
+// (PDN and PGDN: no gate or a scalar gate).
+//
+// The gradient is the exact adjoint of the chunkwise forward (Eq.
+// chunkwise_atk_form with the decayed forms of App. D).  Per chunk, with
+// lam_r = exp(G_r) (G the in-chunk prefix of the log-decay), w_r =
+// exp(G_{C-1} - G_r), Gam_rt = exp(G_r - G_t) (r >= t), S^T the chunk-start
+// state (dk x dv), M = (I + At)^{-1}, T = M Diag(beta):
+//   X  = V - Diag(lam) K S^T            E = T X
+//   O  = scale [ Diag(lam) Q S^T + (Gam o Q Kt^T)_causal E ]
+//   S'^T = lam_C S^T + Kt^T Diag(w) E
+//   At = strict_lower(Diag(beta) (Gam o K Kt^T))
+// and the adjoint, given dO and dS'^T (the state adjoint from the right):
+//   dE  = (Gam o Q Kt^T)_causal^T dO_s + Diag(w) Kt dS'^T      dO_s = scale dO
+//   dX  = T^T dE                      dV = dX
+//   dS^T = lam_C dS'^T + Q^T Diag(lam) dO_s - K^T Diag(lam) dX
+//   dQ  = Diag(lam) dO_s S + dSqk Kt  dK = -Diag(lam) dX S + dSkk Kt
+//   dKt = dSqk^T Q + Diag(w) E dS' + dSkk^T K
+//   dSqk = Gam o (dO_s E^T)_causal,   dM = dE X^T Diag(beta),
+//   dL = -M^T dM M^T,  dAt = strict_lower(dL),  dSkk = Gam o Diag(beta) dAt
+//   dbeta_t = (M^T dE X^T)_tt + sum_{s<t} dAt_ts (Gam o K Kt^T)_ts
+// plus the gate terms (gradients of lam, w, lam_C and Gam, reverse-summed
+// over the chunk) and the preconditioner's reverse scan.
+//
+//   r1_state_adjoint   sequential over chunks (reverse): dS^T carry, dE, dX
+//   p1_chunk_cc        per chunk: the C x C adjoint algebra (dSqk, dSkk,
+//                      dbeta, gate terms of Gam)
+//   p2_chunk_grads     per chunk: dq, dk, dkt, dg
+//   pc_*               preconditioner: reverse scan over tokens of the
+//                      diagonal Gram recurrence (dk, dbetaP, dgP, dlogAScale,
+//                      dA0)
+#include "pdn_device.hpp"
+#include "pdn_internal.hpp"
+
+namespace pdn {
+
+constexpr int C = kChunk;
+constexpr int BVB = 32;  // value columns per workgroup in the reverse scan
+
+template <typename T>
+struct Slab {
+  static constexpr int kVec = 16 / static_cast<int>(sizeof(T));
+  static constexpr int kSegs = BVB / kVec;
+  static constexpr int kPer = C * kSegs / 256;
+};
+
+__device__ __forceinline__ void lds_barrier_b() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// [v][t] LDS slab -> rows of a [rows][ld] tensor (16-byte stores), rows < n
+template <typename T>
+__device__ __forceinline__ void slab_to_rows(T* dst, int64_t ld, const T* src, int lds, int nrows,
+                                             int n, int tid) {
+  using SM = Slab<T>;
+  for (int idx = tid; idx < nrows * SM::kSegs; idx += 256) {
+    const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
+    float4 pk;
+    T* e = reinterpret_cast<T*>(&pk);
+#pragma unroll
+    for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = src[(c0 + s2) * lds + row];
+    if (row < n) *reinterpret_cast<float4*>(dst + row * ld + c0) = pk;
+  }
+}
+
+// ------------------------------------------------------------ r1
+template <typename T, int DK>
+struct RevFrags {
+  static constexpr int KK = DK / 32, CT = DK / 64;
+  Frag8<T> Pt[2], Kw[KK], Tt[2], Ql[CT][2], Kn[CT][2];
+  float4 dO[Slab<T>::kPer];
+  float gC;
+};
+
+struct RevCtx {
+  int64_t b, h, bh;
+  int v0, w, lr, lg, tid;
+};
+
+template <typename T, int DK, int GATE>
+__device__ __forceinline__ void rev_load(RevFrags<T, DK>& f, const BwdArgs& ba, int i,
+                                         const RevCtx& x) {
+  constexpr int KK = DK / 32, CT = DK / 64;
+  constexpr uint32_t E = sizeof(T);
+  using SM = Slab<T>;
+  const FwdArgs& a = ba.f;
+  const int64_t t0 = static_cast<int64_t>(i) * C;
+  const int last = static_cast<int>(min<int64_t>(C, a.T - t0)) - 1;
+  const int64_t cc = (x.bh * a.NT + i) * (int64_t)(C * C);
+  const int64_t ck = (x.bh * a.NT + i) * (int64_t)(DK * C);
+  const T* pt = static_cast<const T*>(a.PtT) + cc;
+  const T* tt = static_cast<const T*>(a.TtT) + cc;
+  const T* kw = static_cast<const T*>(a.Kw) + (x.bh * a.Tpad + t0) * DK;
+  const T* ql = static_cast<const T*>(a.QlT) + ck;
+  const T* kn = static_cast<const T*>(a.KnT) + ck;
+  const int ra = 16 * x.w + x.lr;
+  const uint32_t ocr = static_cast<uint32_t>(ra * C + 8 * x.lg) * E;
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2) {
+    f.Pt[k2] = ld8(at_bytes(pt, ocr + k2 * 32 * E));
+    f.Tt[k2] = ld8(at_bytes(tt, ocr + k2 * 32 * E));
+  }
+  const uint32_t okw = static_cast<uint32_t>(ra * DK + 8 * x.lg) * E;
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) f.Kw[kk] = ld8(at_bytes(kw, okw + kk * 32 * E));
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      const uint32_t o = static_cast<uint32_t>((16 * (x.w * CT + ct) + x.lr) * C + 8 * x.lg + k2 * 32) * E;
+      f.Ql[ct][k2] = ld8(at_bytes(ql, o));
+      f.Kn[ct][k2] = ld8(at_bytes(kn, o));
+    }
+  const int64_t HV = a.H * (int64_t)a.dv;
+  const T* dob = static_cast<const T*>(ba.dO) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0;
+#pragma unroll
+  for (int j = 0; j < SM::kPer; ++j) {
+    const int idx = x.tid + 256 * j;
+    const uint32_t row = static_cast<uint32_t>(min(idx / SM::kSegs, last));
+    const uint32_t off = (row * static_cast<uint32_t>(HV) + (idx % SM::kSegs) * SM::kVec) * E;
+    f.dO[j] = *reinterpret_cast<const float4*>(at_bytes(dob, off));
+  }
+  f.gC = GATE == kGateScalar ? a.G[x.bh * a.Tpad + t0 + C - 1] : 0.f;
+}
+
+// scale * dO of one chunk -> sDO[v][r]; rows past the sequence end are zero
+template <typename T>
+__device__ __forceinline__ void rev_stage_dO(const float4 (&v)[Slab<T>::kPer], T* sDO, int n,
+                                             float scale, int tid) {
+  using SM = Slab<T>;
+  constexpr int LDE = C + 8;
+#pragma unroll
+  for (int j = 0; j < SM::kPer; ++j) {
+    const int idx = tid + 256 * j;
+    const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
+    const T* e = reinterpret_cast<const T*>(&v[j]);
+#pragma unroll
+    for (int s2 = 0; s2 < SM::kVec; ++s2)
+      sDO[(c0 + s2) * LDE + row] = from_f<T>(row < n ? scale * to_f(e[s2]) : 0.f);
+  }
+}
+
+template <bool FULL, typename T, int DK, int GATE>
+__device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, const RevFrags<T, DK>& fnext, bool stage_next,
+                                         floatx4 (&st)[DK / 64][2], const BwdArgs& ba, int i,
+                                         const RevCtx& x, T* sH, T* sDOc, T* sDOn, T* sE, T* sX) {
+  constexpr int KK = DK / 32, CT = DK / 64;
+  constexpr int LDH = DK + 8, LDE = C + 8;
+  const FwdArgs& a = ba.f;
+  const int w = x.w, lr = x.lr, lg = x.lg;
+  const int64_t t0 = static_cast<int64_t>(i) * C;
+  const int n = FULL ? C : static_cast<int>(min<int64_t>(C, a.T - t0));
+  // state adjoint entering this chunk from the right, rows c, slab columns
+  {
+    T* dst = static_cast<T*>(ba.dHs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0;
+    using SM = Slab<T>;
+    for (int idx = x.tid; idx < DK * SM::kSegs; idx += 256) {
+      const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
+      float4 pk;
+      T* e = reinterpret_cast<T*>(&pk);
+#pragma unroll
+      for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = sH[(c0 + s2) * LDH + row];
+      *reinterpret_cast<float4*>(dst + row * a.dv + c0) = pk;
+    }
+  }
+  // ---- dE = P^T dO_s + Diag(w) Kt dS'^T   (rows t of this wave)
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Pt[k2], ld8(sDOc + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg));
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) mma(acc, f.Kw[kk], ld8(sH + (16 * vt + lr) * LDH + kk * 32 + 8 * lg));
+    st4<T>(sE + (16 * vt + lr) * LDE + 16 * w + 4 * lg, acc[0], acc[1], acc[2], acc[3]);
+  }
+  lds_barrier_b();
+  // ---- dX = T^T dE
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Tt[k2], ld8(sE + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg));
+    st4<T>(sX + (16 * vt + lr) * LDE + 16 * w + 4 * lg, acc[0], acc[1], acc[2], acc[3]);
+  }
+  {
+    const int64_t r0 = (x.bh * a.Tpad + t0) * a.dv + x.v0;
+    slab_to_rows<T>(static_cast<T*>(ba.dEr) + r0, a.dv, sE, LDE, C, C, x.tid);
+  }
+  lds_barrier_b();
+  {
+    const int64_t r0 = (x.bh * a.Tpad + t0) * a.dv + x.v0;
+    slab_to_rows<T>(static_cast<T*>(ba.dXr) + r0, a.dv, sX, LDE, C, C, x.tid);
+    const int64_t HV = a.H * (int64_t)a.dv;
+    slab_to_rows<T>(static_cast<T*>(ba.dv) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0, HV, sX, LDE, C,
+                    n, x.tid);
+  }
+  // ---- dS^T <- lam_C dS'^T + (Diag(lam) Q)^T dO_s - (Diag(lam) K)^T dX
+  const float gam = GATE == kGateScalar ? fast_exp(f.gC) : 1.f;
+  Frag8<T> bD[2][2], bX[2][2];
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      bD[vt][k2] = ld8(sDOc + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg);
+      bX[vt][k2] = ld8(sX + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg);
+    }
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int vt = 0; vt < 2; ++vt) {
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) st[ct][vt][ii] *= gam;
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        mma(st[ct][vt], f.Ql[ct][k2], bD[vt][k2]);
+        mma(st[ct][vt], f.Kn[ct][k2], bX[vt][k2]);
+      }
+      st4<T>(sH + (16 * vt + lr) * LDH + 16 * (w * CT + ct) + 4 * lg, st[ct][vt][0], st[ct][vt][1],
+             st[ct][vt][2], st[ct][vt][3]);
+    }
+  if (stage_next) rev_stage_dO<T>(fnext.dO, sDOn, C, a.scale, x.tid);  // earlier chunks are full
+  lds_barrier_b();
+}
+
+template <typename T, int DK, int GATE>
+__global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
+  constexpr int CT = DK / 64;
+  constexpr int LDH = DK + 8, LDE = C + 8;
+  __shared__ __attribute__((aligned(16))) T sH[BVB * LDH];
+  __shared__ __attribute__((aligned(16))) T sDO[2][BVB * LDE];
+  __shared__ __attribute__((aligned(16))) T sE[BVB * LDE];
+  __shared__ __attribute__((aligned(16))) T sX[BVB * LDE];
+  const FwdArgs& a = ba.f;
+  const int nslab = a.dv / BVB;
+  const int64_t bid = blockIdx.x;
+  const int xcd = static_cast<int>(bid & 7);
+  const int64_t j8 = bid >> 3;
+  const int slab = static_cast<int>(j8 % nslab);
+  const int64_t bh = (j8 / nslab) * 8 + xcd;
+  if (bh >= a.BH) return;
+  RevCtx x;
+  x.bh = bh;
+  x.b = bh / a.H;
+  x.h = bh % a.H;
+  x.tid = threadIdx.x;
+  x.w = x.tid >> 6;
+  x.lr = x.tid & 15;
+  x.lg = (x.tid & 63) >> 4;
+  x.v0 = slab * BVB;
+  const int w = x.w, lr = x.lr, lg = x.lg;
+  const int DV = a.dv;
+  floatx4 st[CT][2];
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int c = 16 * (w * CT + ct) + 4 * lg + ii;
+        st[ct][vt][ii] = ba.dS_T ? ba.dS_T[(bh * DK + c) * DV + x.v0 + 16 * vt + lr] : 0.f;
+      }
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int vt = 0; vt < 2; ++vt)
+      st4<T>(sH + (16 * vt + lr) * LDH + 16 * (w * CT + ct) + 4 * lg, st[ct][vt][0], st[ct][vt][1],
+             st[ct][vt][2], st[ct][vt][3]);
+  // reverse order: the (possibly ragged) last chunk first, then the full
+  // chunks two per trip with a branch-free body; dO slabs double-buffered
+  const int NT = a.NT;
+  RevFrags<T, DK> fA, fB;
+  rev_load<T, DK, GATE>(fA, ba, NT - 1, x);
+  rev_load<T, DK, GATE>(fB, ba, max(NT - 2, 0), x);
+  rev_stage_dO<T>(fA.dO, sDO[0], static_cast<int>(a.T - static_cast<int64_t>(NT - 1) * C), a.scale, x.tid);
+  __syncthreads();
+  rev_step<false, T, DK, GATE>(fA, fB, NT > 1, st, ba, NT - 1, x, sH, sDO[0], sDO[1], sE, sX);
+  int i = NT - 2, buf = 1;
+  for (; i >= 1; i -= 2) {
+    rev_load<T, DK, GATE>(fA, ba, i - 1, x);
+    rev_step<true, T, DK, GATE>(fB, fA, true, st, ba, i, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX);
+    buf ^= 1;
+    rev_load<T, DK, GATE>(fB, ba, max(i - 2, 0), x);
+    rev_step<true, T, DK, GATE>(fA, fB, true, st, ba, i - 1, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX);
+    buf ^= 1;
+  }
+  if (i == 0) rev_step<true, T, DK, GATE>(fB, fA, false, st, ba, 0, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX);
+  if (ba.dS0) {
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) {
+          const int c = 16 * (w * CT + ct) + 4 * lg + ii;
+          ba.dS0[(bh * DK + c) * DV + x.v0 + 16 * vt + lr] = st[ct][vt][ii];
+        }
+  }
+}
+
+// ------------------------------------------------------------ p1
+template <typename T, int DD>
+__device__ __forceinline__ void load_rows(T* dst, int ldd, const T* src, int64_t lds, int nvalid,
+                                          int tid, float scale = 1.f) {
+  constexpr int VEC = 16 / sizeof(T), VPR = DD / VEC;
+  for (int idx = tid; idx < C * VPR; idx += 256) {
+    const int r = idx / VPR, cv = idx % VPR;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < nvalid) v = *reinterpret_cast<const float4*>(src + r * lds + cv * VEC);
+    if (scale != 1.f) {
+      T* e = reinterpret_cast<T*>(&v);
+#pragma unroll
+      for (int s2 = 0; s2 < VEC; ++s2) e[s2] = from_f<T>(scale * to_f(e[s2]));
+    }
+    *reinterpret_cast<float4*>(dst + r * ldd + cv * VEC) = v;
+  }
+}
+
+// rows [C][DD] of src -> dst[DD][C + 8] (transposed)
+template <typename T, int DD>
+__device__ __forceinline__ void load_rows_t(T* dst, const T* src, int64_t lds, int nvalid, int tid) {
+  constexpr int VEC = 16 / sizeof(T), VPR = DD / VEC, LDT = C + 8;
+  for (int idx = tid; idx < C * VPR; idx += 256) {
+    const int r = idx / VPR, cv = idx % VPR;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < nvalid) v = *reinterpret_cast<const float4*>(src + r * lds + cv * VEC);
+    const T* e = reinterpret_cast<const T*>(&v);
+#pragma unroll
+    for (int s2 = 0; s2 < VEC; ++s2) dst[(cv * VEC + s2) * LDT + r] = e[s2];
+  }
+}
+
+template <typename T, int DK, int DV>
+struct P1Smem {
+  static constexpr int LDR = (DK > DV ? DK : DV) + 8;
+  static constexpr size_t kRows = sizeof(T) * 2 * C * LDR;
+  static constexpr int LDF = C + 4;
+  static constexpr size_t kF = sizeof(float) * 4 * C * LDF;
+  static constexpr size_t kTotal = kRows + kF + sizeof(float) * 4 * C;
+};
+
+template <typename T, int DK, int DV, int GATE>
+__global__ __launch_bounds__(256) void p1_chunk_cc(BwdArgs ba) {
+  using SM = P1Smem<T, DK, DV>;
+  constexpr int LDR = SM::LDR, LDF = SM::LDF;
+  __shared__ __attribute__((aligned(16))) char smem[SM::kTotal];
+  T* R0 = reinterpret_cast<T*>(smem);
+  T* R1 = R0 + C * LDR;
+  float* sM = reinterpret_cast<float*>(smem + SM::kRows);
+  float* sMt = sM + C * LDF;
+  float* sW1 = sMt + C * LDF;
+  float* sW2 = sW1 + C * LDF;
+  float* sG = sW2 + C * LDF;
+  float* sBeta = sG + C;
+  float* sDbT = sBeta + C;
+
+  const FwdArgs& a = ba.f;
+  const int64_t blk = blockIdx.x;
+  const int64_t bh = blk / a.NT;
+  const int i = static_cast<int>(blk % a.NT);
+  const int64_t b = bh / a.H, h = bh % a.H;
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 15, lg = l >> 4;
+  const int64_t t0 = static_cast<int64_t>(i) * C;
+  const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
+  const int64_t HV = a.H * (int64_t)DV, HD = a.H * (int64_t)DK;
+  const int64_t cc = (bh * a.NT + i) * (int64_t)(C * C);
+
+  // ---- dO_s, E rows; M, M^T; gate prefix and beta
+  load_rows<T, DV>(R0, LDR, static_cast<const T*>(ba.dO) + (b * a.T + t0) * HV + h * DV, HV, n, tid,
+                   a.scale);
+  const int64_t rv = (bh * a.Tpad + t0) * DV;
+  load_rows<T, DV>(R1, LDR, static_cast<const T*>(a.Er) + rv, DV, C, tid);
+  for (int idx = tid; idx < C * C; idx += 256) {
+    const int r = idx / C, t = idx % C;
+    const float m = a.Mi[cc + idx];
+    sM[r * LDF + t] = m;
+    sMt[t * LDF + r] = m;
+  }
+  if (tid < C) {
+    sG[tid] = GATE == kGateScalar ? a.G[bh * a.Tpad + t0 + tid] : 0.f;
+    sBeta[tid] = tid < n ? a.beta[(b * a.T + t0 + tid) * a.H + h] : 0.f;
+  }
+  __syncthreads();
+
+  // ---- dP = dO_s E^T (causal), row block w
+  floatx4 dP[4], dT[4], Sqk[4], Skk[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    dP[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    dT[j] = dP[j];
+    Sqk[j] = dP[j];
+    Skk[j] = dP[j];
+    if (j <= w) mma_tile<DV>(dP[j], R0 + (16 * w) * LDR, LDR, R1 + (16 * j) * LDR, LDR, lr, lg);
+  }
+  __syncthreads();
+  // ---- dT = dE X^T
+  load_rows<T, DV>(R0, LDR, static_cast<const T*>(ba.dEr) + rv, DV, C, tid);
+  load_rows<T, DV>(R1, LDR, static_cast<const T*>(a.Xr) + rv, DV, C, tid);
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j) mma_tile<DV>(dT[j], R0 + (16 * w) * LDR, LDR, R1 + (16 * j) * LDR, LDR, lr, lg);
+  __syncthreads();
+  // ---- S_qk = Q Kt^T, then S_kk = K Kt^T (row block w, causal part)
+  load_rows<T, DK>(R0, LDR, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK, HD, n, tid);
+  load_rows<T, DK>(R1, LDR, static_cast<const T*>(a.Ktr) + (bh * a.Tpad + t0) * DK, DK, C, tid);
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if (j <= w) mma_tile<DK>(Sqk[j], R0 + (16 * w) * LDR, LDR, R1 + (16 * j) * LDR, LDR, lr, lg);
+  __syncthreads();
+  load_rows<T, DK>(R0, LDR, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK, HD, n, tid);
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if (j <= w) mma_tile<DK>(Skk[j], R0 + (16 * w) * LDR, LDR, R1 + (16 * j) * LDR, LDR, lr, lg);
+  // ---- dSqk; dM = dT Diag(beta) -> sW1; M o dT -> sW2 (column sums: dbeta via T)
+  T* dSqk = static_cast<T*>(ba.dSqk) + cc;
+  T* dSqkT = static_cast<T*>(ba.dSqkT) + cc;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    floatx4 ds;
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      const int r = 16 * w + 4 * lg + ii, t = 16 * j + lr;
+      const float gm = (r >= t) ? (GATE == kGateScalar ? fast_exp(sG[r] - sG[t]) : 1.f) : 0.f;
+      ds[ii] = gm * dP[j][ii];
+      sW1[r * LDF + t] = dT[j][ii] * sBeta[t];
+      sW2[r * LDF + t] = dT[j][ii] * sM[r * LDF + t];
+      // keep the masked C x C products for the Gam gradient
+      dP[j][ii] = ds[ii] * Sqk[j][ii];   // (Gam o dP) o S_qk, causal
+    }
+    st_tile<T>(dSqk + (16 * w) * C + 16 * j, C, ds, lr, lg);
+    st_tile_t<T>(dSqkT + (16 * j) * C + 16 * w, C, ds, lr, lg);
+  }
+  __syncthreads();
+  if (tid < C) {
+    float sdb = 0.f;
+    for (int r = 0; r < C; ++r) sdb += sW2[r * LDF + tid];
+    sDbT[tid] = sdb;
+  }
+  __syncthreads();
+  // ---- Y = dM M^T -> sW2 as Y^T
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    floatx4 y = {0.f, 0.f, 0.f, 0.f};
+    mma_tile<C>(y, sW1 + (16 * w) * LDF, LDF, sM + (16 * j) * LDF, LDF, lr, lg);
+    st_tile_t<float>(sW2 + (16 * j) * LDF + 16 * w, LDF, y, lr, lg);
+  }
+  __syncthreads();
+  // ---- dL = -M^T Y;  dAt = strict_lower(dL);  dSkk = Gam o Diag(beta) dAt
+  T* dSkk = static_cast<T*>(ba.dSkk) + cc;
+  T* dSkkT = static_cast<T*>(ba.dSkkT) + cc;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    floatx4 dl = {0.f, 0.f, 0.f, 0.f};
+    mma_tile<C>(dl, sMt + (16 * w) * LDF, LDF, sW2 + (16 * j) * LDF, LDF, lr, lg);
+    floatx4 ds;
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      const int r = 16 * w + 4 * lg + ii, t = 16 * j + lr;
+      const float gm = (r > t) ? (GATE == kGateScalar ? fast_exp(sG[r] - sG[t]) : 1.f) : 0.f;
+      const float dA = (r > t) ? -dl[ii] : 0.f;
+      ds[ii] = gm * sBeta[r] * dA;
+      // row sums: dbeta via At (dAt o Gam o S_kk) and the Gam gradient
+      sW1[r * LDF + t] = dA * gm * Skk[j][ii];
+      Skk[j][ii] = ds[ii] * Skk[j][ii] + dP[j][ii];   // (dSkk o S_kk) + (dSqk o S_qk)
+    }
+    st_tile<T>(dSkk + (16 * w) * C + 16 * j, C, ds, lr, lg);
+    st_tile_t<T>(dSkkT + (16 * j) * C + 16 * w, C, ds, lr, lg);
+  }
+  __syncthreads();   // sW1 complete; sMt free
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) sMt[(16 * w + 4 * lg + ii) * LDF + 16 * j + lr] = Skk[j][ii];
+  __syncthreads();
+  if (tid < C) {
+    const int r = tid;
+    float dbA = 0.f, rs = 0.f, cs = 0.f;
+    for (int t = 0; t < C; ++t) {
+      dbA += sW1[r * LDF + t];
+      rs += sMt[r * LDF + t];
+      cs += sMt[t * LDF + r];
+    }
+    // Gam_rt = exp(G_r - G_t): d/dG_r of sum R_rt = row sum, d/dG_t = -column sum
+    ba.dGp[bh * a.Tpad + t0 + r] = GATE == kGateScalar ? rs - cs : 0.f;
+    if (r < n) ba.dbeta[(b * a.T + t0 + r) * a.H + h] = sDbT[r] + dbA;
+  }
+}
+
+// ------------------------------------------------------------ p2
+template <typename T, int DK, int DV>
+struct P2Smem {
+  static constexpr int LDR = DV + 8;   // rows of dO_s, dX, E
+  static constexpr int LDS = DV + 8;   // rows of S^T, dS'^T ([dk][dv])
+  static constexpr size_t kPh1 = sizeof(T) * (3 * C * LDR + 2 * DK * LDS);
+  static constexpr int LDT = C + 8;    // [dk][C] transposed rows and [C][C]
+  static constexpr size_t kPh2 = sizeof(T) * (3 * DK * LDT + 4 * C * LDT);
+  static constexpr size_t kMain = kPh1 > kPh2 ? kPh1 : kPh2;
+  static constexpr size_t kTotal = kMain + sizeof(float) * (6 * C + 4);
+};
+
+template <typename T, int DK, int DV, int GATE>
+__global__ __launch_bounds__(256) void p2_chunk_grads(BwdArgs ba) {
+  using SM = P2Smem<T, DK, DV>;
+  constexpr int LDR = SM::LDR, LDS = SM::LDS, LDT = SM::LDT;
+  constexpr int NJ = DK / 16;   // column tiles over d_k
+  __shared__ __attribute__((aligned(16))) char smem[SM::kTotal];
+  // phase 1
+  T* sDO = reinterpret_cast<T*>(smem);
+  T* sDX = sDO + C * LDR;
+  T* sE = sDX + C * LDR;
+  T* sS = sE + C * LDR;
+  T* sdS = sS + DK * LDS;
+  // phase 2 (reuses the same memory)
+  T* sKtT = reinterpret_cast<T*>(smem);
+  T* sQT = sKtT + DK * LDT;
+  T* sKT = sQT + DK * LDT;
+  T* sdSqk = sKT + DK * LDT;
+  T* sdSkk = sdSqk + C * LDT;
+  T* sdSqkT = sdSkk + C * LDT;
+  T* sdSkkT = sdSqkT + C * LDT;
+  float* sG = reinterpret_cast<float*>(smem + SM::kMain);
+  float* sDl = sG + C;      // d lam_r partials
+  float* sDw = sDl + C;     // d w_r partials
+  float* sDG = sDw + C;
+  float* sRed = sDG + C;    // 4 wave partials of sum(dS' o S)
+
+  const FwdArgs& a = ba.f;
+  const int64_t blk = blockIdx.x;
+  const int64_t bh = blk / a.NT;
+  const int i = static_cast<int>(blk % a.NT);
+  const int64_t b = bh / a.H, h = bh % a.H;
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 15, lg = l >> 4;
+  const int64_t t0 = static_cast<int64_t>(i) * C;
+  const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
+  const int64_t HV = a.H * (int64_t)DV, HD = a.H * (int64_t)DK;
+  const int64_t cc = (bh * a.NT + i) * (int64_t)(C * C);
+
+  // ---- phase 1: A1 = dO_s S, A2 = dX S, A3 = E dS'   (C x dk, row block w)
+  load_rows<T, DV>(sDO, LDR, static_cast<const T*>(ba.dO) + (b * a.T + t0) * HV + h * DV, HV, n, tid,
+                   a.scale);
+  const int64_t rv = (bh * a.Tpad + t0) * DV;
+  load_rows<T, DV>(sDX, LDR, static_cast<const T*>(ba.dXr) + rv, DV, C, tid);
+  load_rows<T, DV>(sE, LDR, static_cast<const T*>(a.Er) + rv, DV, C, tid);
+  {
+    constexpr int VEC = 16 / sizeof(T), VPR = DV / VEC;
+    const int64_t cs = (bh * a.NT + i) * (int64_t)DK * DV;
+    const T* Hs = static_cast<const T*>(a.Hs) + cs;
+    const T* dHs = static_cast<const T*>(ba.dHs) + cs;
+    for (int idx = tid; idx < DK * VPR; idx += 256) {
+      const int c = idx / VPR, cv = idx % VPR;
+      *reinterpret_cast<float4*>(sS + c * LDS + cv * VEC) = *reinterpret_cast<const float4*>(Hs + c * DV + cv * VEC);
+      *reinterpret_cast<float4*>(sdS + c * LDS + cv * VEC) = *reinterpret_cast<const float4*>(dHs + c * DV + cv * VEC);
+    }
+  }
+  if (tid < C) sG[tid] = GATE == kGateScalar ? a.G[bh * a.Tpad + t0 + tid] : 0.f;
+  __syncthreads();
+  floatx4 A1[NJ], A2[NJ], A3[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    A1[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    A2[j] = A1[j];
+    A3[j] = A1[j];
+    mma_tile<DV>(A1[j], sDO + (16 * w) * LDR, LDR, sS + (16 * j) * LDS, LDS, lr, lg);
+    mma_tile<DV>(A2[j], sDX + (16 * w) * LDR, LDR, sS + (16 * j) * LDS, LDS, lr, lg);
+    mma_tile<DV>(A3[j], sE + (16 * w) * LDR, LDR, sdS + (16 * j) * LDS, LDS, lr, lg);
+  }
+  // sum(dS' o S) for the gradient of lam_C
+  {
+    float part = 0.f;
+    for (int idx = tid; idx < DK * DV; idx += 256) {
+      const int c = idx / DV, v = idx % DV;
+      part += to_f(sS[c * LDS + v]) * to_f(sdS[c * LDS + v]);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) part += __shfl_xor(part, off, 64);
+    if (l == 0) sRed[w] = part;
+  }
+  __syncthreads();
+  // ---- phase 2: transposed Kt, Q, K and the C x C adjoints
+  load_rows_t<T, DK>(sKtT, static_cast<const T*>(a.Ktr) + (bh * a.Tpad + t0) * DK, DK, C, tid);
+  load_rows_t<T, DK>(sQT, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK, HD, n, tid);
+  load_rows_t<T, DK>(sKT, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK, HD, n, tid);
+  load_rows<T, C>(sdSqk, LDT, static_cast<const T*>(ba.dSqk) + cc, C, C, tid);
+  load_rows<T, C>(sdSkk, LDT, static_cast<const T*>(ba.dSkk) + cc, C, C, tid);
+  load_rows<T, C>(sdSqkT, LDT, static_cast<const T*>(ba.dSqkT) + cc, C, C, tid);
+  load_rows<T, C>(sdSkkT, LDT, static_cast<const T*>(ba.dSkkT) + cc, C, C, tid);
+  __syncthreads();
+  float lam[4], wr[4];
+#pragma unroll
+  for (int ii = 0; ii < 4; ++ii) {
+    const int r = 16 * w + 4 * lg + ii;
+    lam[ii] = GATE == kGateScalar ? fast_exp(sG[r]) : 1.f;
+    wr[ii] = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[r]) : 1.f;
+  }
+  // gate partials: dlam_r = Q_r . A1_r - K_r . A2_r ;  dw_r = Kt_r . A3_r
+  float pl[4] = {0.f, 0.f, 0.f, 0.f}, pw[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int c = 16 * j + lr;
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      const int r = 16 * w + 4 * lg + ii;
+      pl[ii] += to_f(sQT[c * LDT + r]) * A1[j][ii] - to_f(sKT[c * LDT + r]) * A2[j][ii];
+      pw[ii] += to_f(sKtT[c * LDT + r]) * A3[j][ii];
+    }
+  }
+#pragma unroll
+  for (int ii = 0; ii < 4; ++ii)
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      pl[ii] += __shfl_xor(pl[ii], off, 64);
+      pw[ii] += __shfl_xor(pw[ii], off, 64);
+    }
+  if (lr == 0) {
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      sDl[16 * w + 4 * lg + ii] = pl[ii];
+      sDw[16 * w + 4 * lg + ii] = pw[ii];
+    }
+  }
+  // ---- dQ, dK (read key), dKt
+  T* dq = static_cast<T*>(ba.dq) + (b * a.T + t0) * HD + h * DK;
+  float* dKm = ba.dKm + (bh * a.Tpad + t0) * DK;
+  float* dKt = ba.dKt + (bh * a.Tpad + t0) * DK;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    floatx4 aq, ak, at;
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      aq[ii] = lam[ii] * A1[j][ii];
+      ak[ii] = -lam[ii] * A2[j][ii];
+      at[ii] = wr[ii] * A3[j][ii];
+    }
+    mma_tile<C>(aq, sdSqk + (16 * w) * LDT, LDT, sKtT + (16 * j) * LDT, LDT, lr, lg);
+    mma_tile<C>(ak, sdSkk + (16 * w) * LDT, LDT, sKtT + (16 * j) * LDT, LDT, lr, lg);
+    mma_tile<C>(at, sdSqkT + (16 * w) * LDT, LDT, sQT + (16 * j) * LDT, LDT, lr, lg);
+    mma_tile<C>(at, sdSkkT + (16 * w) * LDT, LDT, sKT + (16 * j) * LDT, LDT, lr, lg);
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      const int r = 16 * w + 4 * lg + ii, c = 16 * j + lr;
+      if (r < n) dq[r * HD + c] = from_f<T>(aq[ii]);
+      dKm[r * DK + c] = ak[ii];
+      dKt[r * DK + c] = at[ii];
+    }
+  }
+  __syncthreads();
+  // ---- gate: dG_r, then the reverse in-chunk cumsum -> dg
+  if (GATE == kGateScalar && w == 0) {
+    const int r = l;
+    const float lamr = fast_exp(sG[r]);
+    const float wrr = fast_exp(sG[C - 1] - sG[r]);
+    float wdw = wrr * sDw[r];
+    float dG = ba.dGp[bh * a.Tpad + t0 + r] + lamr * sDl[r] - wdw;
+    // lam_C and the w_r all depend on G_{C-1}
+    float tot = wdw;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) tot += __shfl_xor(tot, off, 64);
+    if (r == C - 1) dG += tot + fast_exp(sG[C - 1]) * (sRed[0] + sRed[1] + sRed[2] + sRed[3]);
+    // dg_j = sum_{r >= j} dG_r
+    float x = dG;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const float y = __shfl_down(x, off, 64);
+      if (r + off < 64) x += y;
+    }
+    if (r < n) ba.dg[(b * a.T + t0 + r) * a.H + h] = x;
+  }
+}
+
+// ------------------------------------------------------------ preconditioner
+// Reverse scan of A_t = aP_t A_{t-1} + bP_t k_t^2, kt_t = B(A_t) k_t over the
+// tokens.  With D_t the adjoint of A_t: D_t = inj_t + aP_{t+1} D_{t+1},
+// inj_t = (dB/dA)(A_t) (dkt_t o k_t).  Chunk-parallel in three passes:
+// pc_chunk<false> computes each chunk's local adjoint (zero carry), pc_carry
+// chains the chunks (adjoint entering each chunk from the right), and
+// pc_chunk<true> recomputes with the carry and writes dk, dbetaP, dgP and the
+// partial d mu.
+template <typename T, int DK, bool FINAL>
+__global__ __launch_bounds__(DK) void pc_chunk(BwdArgs ba) {
+  __shared__ float sA[C * DK];
+  __shared__ float sKv[C * DK];
+  __shared__ float sEgp[C], sBp[C];
+  __shared__ float sRb[C * DK / 64 * 2];   // per-row wave partials: [row][wave][2]
+  __shared__ float sMu[DK / 64];
+  const FwdArgs& a = ba.f;
+  const int64_t blk = blockIdx.x;
+  const int64_t bh = blk / a.NT;
+  const int i = static_cast<int>(blk % a.NT);
+  const int64_t b = bh / a.H, h = bh % a.H;
+  const int c = threadIdx.x, wv = c >> 6, l = c & 63;
+  const int64_t t0 = static_cast<int64_t>(i) * C;
+  const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
+  const T* kp = static_cast<const T*>(a.k);
+  if (c < C) {
+    const bool ok = c < n;
+    const int64_t sidx = (b * a.T + t0 + c) * a.H + h;
+    sEgp[c] = (ok && a.g_p) ? fast_exp(a.g_p[sidx]) : 1.f;
+    sBp[c] = ok ? a.beta_p[sidx] : 0.f;
+  }
+  __syncthreads();
+  const float A_start = a.Abound[(bh * (a.NT + 1) + i) * DK + c];
+  float A = A_start;
+  for (int r = 0; r < C; ++r) {
+    const float kr = r < n ? to_f(kp[((b * a.T + t0 + r) * a.H + h) * DK + c]) : 0.f;
+    A = sEgp[r] * A + sBp[r] * kr * kr;
+    sA[r * DK + c] = A;
+    sKv[r * DK + c] = kr;
+  }
+  const float mu = fast_exp(a.log_a_scale[h]);
+  const float lnx = a.lnx;
+  const float* dkt = ba.dKt + (bh * a.Tpad + t0) * DK + c;
+  float D = FINAL ? ba.pcC[(bh * (a.NT + 1) + i + 1) * DK + c] : 0.f;   // adjoint entering from the right
+  float aNext = 1.f;   // aP of the token after r (its factor on D)
+  float muPart = 0.f;
+  for (int r = C - 1; r >= 0; --r) {
+    const float Ar = sA[r * DK + c];
+    const float kvr = sKv[r * DK + c];
+    const float dk_t = dkt[r * DK];
+    const float Bv = squash_gain(Ar, mu, lnx);
+    float inj = 0.f, dr = 0.f;
+    if (Ar > 0.f) {
+      const float rr = fast_log(Ar) - mu;
+      const float ds = -lnx * Bv * dk_t * kvr;
+      const float den = 1.f + fabsf(rr);
+      dr = ds / (den * den);
+      inj = dr / Ar;
+    }
+    D = inj + aNext * D;
+    aNext = sEgp[r];
+    if (FINAL) {
+      muPart -= dr;
+      if (r < n) {
+        const float Aprev = r > 0 ? sA[(r - 1) * DK + c] : A_start;
+        const float dkk = ba.dKm[(bh * a.Tpad + t0 + r) * DK + c] + Bv * dk_t + 2.f * sBp[r] * kvr * D;
+        static_cast<T*>(ba.dk)[((b * a.T + t0 + r) * a.H + h) * DK + c] = from_f<T>(dkk);
+        // per-row sums over channels: dbetaP_r = sum D k^2, dgP_r = aP_r sum D A_{r-1}
+        float s1 = D * kvr * kvr, s2 = D * Aprev;
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+          s1 += __shfl_xor(s1, off, 64);
+          s2 += __shfl_xor(s2, off, 64);
+        }
+        if (l == 0) {
+          sRb[(r * (DK / 64) + wv) * 2] = s1;
+          sRb[(r * (DK / 64) + wv) * 2 + 1] = s2;
+        }
+      }
+    }
+  }
+  if (!FINAL) {
+    // the adjoint this chunk sends to the left, with zero carry: aP_0 D_0
+    ba.pcL[(bh * a.NT + i) * DK + c] = aNext * D;
+  } else {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) muPart += __shfl_xor(muPart, off, 64);
+    if (l == 0) sMu[wv] = muPart;
+    __syncthreads();
+    if (c < n) {
+      float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+      for (int q = 0; q < DK / 64; ++q) {
+        s1 += sRb[(c * (DK / 64) + q) * 2];
+        s2 += sRb[(c * (DK / 64) + q) * 2 + 1];
+      }
+      const int64_t sidx = (b * a.T + t0 + c) * a.H + h;
+      if (ba.dbeta_p) ba.dbeta_p[sidx] = s1;
+      if (ba.dg_p) ba.dg_p[sidx] = sEgp[c] * s2;
+    }
+    if (c == 0) {
+      float m = 0.f;
+#pragma unroll
+      for (int q = 0; q < DK / 64; ++q) m += sMu[q];
+      ba.pcMu[bh * a.NT + i] = m;
+    }
+  }
+}
+
+// carry_{i-1} = L_i + exp(sumD_i) carry_i, from the last chunk (carry 0)
+template <int DK>
+__global__ __launch_bounds__(DK) void pc_carry(BwdArgs ba) {
+  const FwdArgs& a = ba.f;
+  const int64_t bh = blockIdx.x;
+  const int c = threadIdx.x;
+  float carry = 0.f;
+  ba.pcC[(bh * (a.NT + 1) + a.NT) * DK + c] = 0.f;
+  for (int i = a.NT - 1; i >= 0; --i) {
+    ba.pcC[(bh * (a.NT + 1) + i + 1) * DK + c] = carry;
+    carry = ba.pcL[(bh * a.NT + i) * DK + c] + fast_exp(a.sumD[bh * a.NT + i]) * carry;
+  }
+  if (ba.dA0) ba.dA0[bh * DK + c] = carry;
+}
+
+// d logAScale_h = mu_h * sum over batches and chunks of the partial d mu
+__global__ void pc_mu(BwdArgs ba) {
+  const FwdArgs& a = ba.f;
+  const int64_t h = blockIdx.x;
+  float s = 0.f;
+  for (int64_t idx = threadIdx.x; idx < a.B * a.NT; idx += blockDim.x) {
+    const int64_t b = idx / a.NT, i = idx % a.NT;
+    s += ba.pcMu[(b * a.H + h) * a.NT + i];
+  }
+  __shared__ float red[256];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if (static_cast<int>(threadIdx.x) < off) red[threadIdx.x] += red[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) ba.dlog_a_scale[h] = fast_exp(a.log_a_scale[h]) * red[0];
+}
+
+// identity / external write key: dk = dKm (+ dKt), dktilde = dKt
+template <typename T, int DK>
+__global__ __launch_bounds__(256) void combine_dk(BwdArgs ba) {
+  const FwdArgs& a = ba.f;
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t tot = a.B * a.T * a.H * DK;
+  if (idx >= tot) return;
+  const int c = static_cast<int>(idx % DK);
+  const int64_t tok = idx / DK;
+  const int64_t h = tok % a.H, t = (tok / a.H) % a.T, b = tok / (a.H * a.T);
+  const int64_t w = ((b * a.H + h) * a.Tpad + t) * DK + c;
+  const float km = ba.dKm[w], kt = ba.dKt[w];
+  if (a.precond == kIdentity) {
+    static_cast<T*>(ba.dk)[idx] = from_f<T>(km + kt);
+  } else {
+    static_cast<T*>(ba.dk)[idx] = from_f<T>(km);
+    if (ba.dktilde) static_cast<T*>(ba.dktilde)[idx] = from_f<T>(kt);
+  }
+}
+
+// ------------------------------------------------------------ host side
+static size_t align256b(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond) {
+  BwdWsLayout L{};
+  L.f = fwd_ws_layout(BH, NT, dk, esz, gate, precond);
+  size_t off = L.f.total;
+  auto take = [&](size_t bytes) { const size_t o = off; off = align256b(off + bytes); return o; };
+  const size_t bh = static_cast<size_t>(BH), nt = static_cast<size_t>(NT), tp = nt * C;
+  L.Hs = take(bh * nt * dk * dv * esz);
+  L.Xr = take(bh * tp * dv * esz);
+  L.Er = take(bh * tp * dv * esz);
+  L.PtT = take(bh * nt * C * C * esz);
+  L.TtT = take(bh * nt * C * C * esz);
+  L.Mi = take(bh * nt * C * C * 4);
+  L.Ktr = take(bh * tp * dk * esz);
+  L.Kw = take(bh * tp * dk * esz);
+  L.QlT = take(bh * nt * dk * C * esz);
+  L.KnT = take(bh * nt * dk * C * esz);
+  L.dHs = take(bh * nt * dk * dv * esz);
+  L.dEr = take(bh * tp * dv * esz);
+  L.dXr = take(bh * tp * dv * esz);
+  L.dSqk = take(bh * nt * C * C * esz);
+  L.dSqkT = take(bh * nt * C * C * esz);
+  L.dSkk = take(bh * nt * C * C * esz);
+  L.dSkkT = take(bh * nt * C * C * esz);
+  L.dGp = take(bh * tp * 4);
+  L.dKt = take(bh * tp * dk * 4);
+  L.dKm = take(bh * tp * dk * 4);
+  L.pcL = take(bh * nt * dk * 4);
+  L.pcC = take(bh * (nt + 1) * dk * 4);
+  L.pcMu = take(bh * nt * 4);
+  L.total = off;
+  return L;
+}
+
+hipError_t launch_forward_parts(const FwdArgs& a, int io_bf16, hipStream_t s, bool bwd);
+
+template <typename T, int DK, int DV, int GATE>
+static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s) {
+  const FwdArgs& a = ba.f;
+  hipError_t e;
+  const int64_t nslab = DV / BVB;
+  const unsigned grid_scan = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
+  const unsigned grid_chunk = static_cast<unsigned>(a.BH * a.NT);
+  hipLaunchKernelGGL((r1_state_adjoint<T, DK, GATE>), dim3(grid_scan), dim3(256), 0, s, ba);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL((p1_chunk_cc<T, DK, DV, GATE>), dim3(grid_chunk), dim3(256), 0, s, ba);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL((p2_chunk_grads<T, DK, DV, GATE>), dim3(grid_chunk), dim3(256), 0, s, ba);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (a.precond == kSquash) {
+    hipLaunchKernelGGL((pc_chunk<T, DK, false>), dim3(grid_chunk), dim3(DK), 0, s, ba);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL((pc_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, ba);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL((pc_chunk<T, DK, true>), dim3(grid_chunk), dim3(DK), 0, s, ba);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (ba.dlog_a_scale) {
+      hipLaunchKernelGGL(pc_mu, dim3(static_cast<unsigned>(a.H)), dim3(256), 0, s, ba);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+  } else {
+    const int64_t tot = a.B * a.T * a.H * DK;
+    hipLaunchKernelGGL((combine_dk<T, DK>), dim3(static_cast<unsigned>((tot + 255) / 256)), dim3(256), 0,
+                       s, ba);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// fp32 io: head dims 64 only (LDS); the host validates this
+static hipError_t launch_bwd_f32(const BwdArgs& ba, hipStream_t s) {
+  return ba.f.gate == kGateScalar ? launch_bwd_typed<float, 64, 64, kGateScalar>(ba, s)
+                                  : launch_bwd_typed<float, 64, 64, kGateNone>(ba, s);
+}
+
+template <typename T>
+static hipError_t launch_bwd_dims(const BwdArgs& ba, hipStream_t s) {
+  const FwdArgs& a = ba.f;
+  const bool sc = a.gate == kGateScalar;
+  if (a.dk == 128 && a.dv == 128)
+    return sc ? launch_bwd_typed<T, 128, 128, kGateScalar>(ba, s) : launch_bwd_typed<T, 128, 128, kGateNone>(ba, s);
+  if (a.dk == 128 && a.dv == 64)
+    return sc ? launch_bwd_typed<T, 128, 64, kGateScalar>(ba, s) : launch_bwd_typed<T, 128, 64, kGateNone>(ba, s);
+  if (a.dk == 64 && a.dv == 128)
+    return sc ? launch_bwd_typed<T, 64, 128, kGateScalar>(ba, s) : launch_bwd_typed<T, 64, 128, kGateNone>(ba, s);
+  return sc ? launch_bwd_typed<T, 64, 64, kGateScalar>(ba, s) : launch_bwd_typed<T, 64, 64, kGateNone>(ba, s);
+}
+
+hipError_t launch_backward(const BwdArgs& ba, int io_bf16, hipStream_t s) {
+  hipError_t e = launch_forward_parts(ba.f, io_bf16, s, true);
+  if (e != hipSuccess) return e;
+  return io_bf16 ? launch_bwd_dims<bf16>(ba, s) : launch_bwd_f32(ba, s);
+}
+
+}  // namespace pdn

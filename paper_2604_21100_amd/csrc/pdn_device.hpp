@@ -116,6 +116,33 @@ __device__ __forceinline__ void st4(T* p, float a, float b, float c, float d) {
   *reinterpret_cast<typename Vec4<T>::type*>(p) = v;
 }
 
+// One 16x16 output tile of A Bt^T over a contraction of K (multiple of 32):
+// A points at row 0 of the tile's rows (row-major, leading dim lda), Bt at
+// row 0 of its columns stored as rows (row-major, leading dim ldb).  Every
+// operand used this way is staged as [output index][contraction index], so
+// each fragment is one contiguous 8-element read.
+template <int K, typename T>
+__device__ __forceinline__ void mma_tile(floatx4& acc, const T* A, int lda, const T* Bt, int ldb,
+                                         int lr, int lg) {
+#pragma unroll
+  for (int kk = 0; kk < K / 32; ++kk)
+    mma(acc, ld8(A + lr * lda + kk * 32 + 8 * lg), ld8(Bt + lr * ldb + kk * 32 + 8 * lg));
+}
+
+// accumulator tile -> memory, row-major (4 scalar stores) or transposed
+// (one 4-vector store)
+template <typename T>
+__device__ __forceinline__ void st_tile(T* out, int ld, const floatx4& acc, int lr, int lg,
+                                        float scale = 1.f) {
+#pragma unroll
+  for (int ii = 0; ii < 4; ++ii) out[(4 * lg + ii) * ld + lr] = from_f<T>(scale * acc[ii]);
+}
+template <typename T>
+__device__ __forceinline__ void st_tile_t(T* out, int ld, const floatx4& acc, int lr, int lg,
+                                          float scale = 1.f) {
+  st4<T>(out + lr * ld + 4 * lg, scale * acc[0], scale * acc[1], scale * acc[2], scale * acc[3]);
+}
+
 __device__ __forceinline__ float fast_exp(float x) { return __expf(x); }
 __device__ __forceinline__ float fast_log(float x) { return __logf(x); }
 

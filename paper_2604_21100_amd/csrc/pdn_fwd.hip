@@ -126,7 +126,10 @@ struct K2Smem {
   static constexpr size_t kTotal = kR1 + kR2 + kR3 + kGc + kY + kScal + kSeg;
 };
 
-template <typename T, int DK, int GATE, int PREC>
+// BWD: also write the operand layouts the backward kernels read (P^T, T^T,
+// M, write-key rows, w-scaled write-key rows, (Diag(lam) Q)^T and
+// -(Diag(lam) K)^T); scalar gate or no gate only.
+template <typename T, int DK, int GATE, int PREC, bool BWD>
 __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   using SM = K2Smem<T, DK, GATE>;
   constexpr int LDK = SM::LDK, LDA = SM::LDA;
@@ -295,10 +298,32 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         const int r = 16 * w + 4 * lg + ii;
         float fac = 1.f;
         if (GATE == kGateScalar) fac = fast_exp(sG[r] - sG[t]);
-        const float pv = (j <= w && r >= t) ? accP[j][ii] * fac : 0.f;
+        accP[j][ii] = (j <= w && r >= t) ? accP[j][ii] * fac : 0.f;
         accA[j][ii] = (j <= w && r > t) ? sBeta[r] * accA[j][ii] * fac : 0.f;
-        P[r * C + t] = from_f<T>(pv);
+        P[r * C + t] = from_f<T>(accP[j][ii]);
       }
+      if (BWD) {
+        T* PtT = static_cast<T*>(a.PtT) + (bh * a.NT + i) * (int64_t)(C * C);
+        st_tile_t<T>(PtT + (16 * j) * C + 16 * w, C, accP[j], lr, lg);
+      }
+    }
+  }
+  if (BWD) {
+    // (Diag(lam) Q)^T and -(Diag(lam) K)^T per chunk, [dk][C]
+    T* QlT = static_cast<T*>(a.QlT) + (bh * a.NT + i) * (int64_t)(DK * C);
+    T* KnT = static_cast<T*>(a.KnT) + (bh * a.NT + i) * (int64_t)(DK * C);
+    for (int idx = tid; idx < DK * (C / 8); idx += 256) {
+      const int c = idx / (C / 8), r0 = (idx % (C / 8)) * 8;
+      Frag8<T> fq, fk;
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) {
+        const int r = r0 + s2;
+        const float lam = GATE == kGateScalar ? fast_exp(sG[r]) : 1.f;
+        fq.set(s2, lam * to_f(sQ[r * LDK + c]));
+        fk.set(s2, -lam * to_f(sK[r * LDK + c]));
+      }
+      st8(QlT + c * C + r0, fq);
+      st8(KnT + c * C + r0, fk);
     }
   }
   __syncthreads();  // sK / sQ are free from here on
@@ -370,6 +395,40 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         f.set(s, lower ? sX[r * LDA + t] * sBeta[t] : 0.f);
       }
       st8(Tout + r * C + t0v, f);
+    }
+  }
+  if (BWD) {
+    const int64_t cc = (bh * a.NT + i) * (int64_t)(C * C);
+    float* Mo = a.Mi + cc;
+    T* TtT = static_cast<T*>(a.TtT) + cc;
+    for (int idx = tid; idx < C * C / 8; idx += 256) {
+      const int r = idx / (C / 8), t0v = (idx % (C / 8)) * 8;
+      Frag8<float> fm;
+      Frag8<T> ft;
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) {
+        const int t = t0v + s2;
+        const bool lower = (t >> 4) < (r >> 4) || ((t >> 4) == (r >> 4) && t <= r);
+        fm.set(s2, lower ? sX[r * LDA + t] : 0.f);
+        // T^T[r][t] = T[t][r] = M[t][r] beta_r
+        const bool upper = (r >> 4) < (t >> 4) || ((r >> 4) == (t >> 4) && r <= t);
+        ft.set(s2, upper ? sX[t * LDA + r] * sBeta[r] : 0.f);
+      }
+      st8(Mo + r * C + t0v, fm);
+      st8(TtT + r * C + t0v, ft);
+    }
+    // write-key rows and w-scaled write-key rows
+    T* Kr = static_cast<T*>(a.Ktr) + (bh * a.Tpad + t0) * DK;
+    T* Kwr = static_cast<T*>(a.Kw) + (bh * a.Tpad + t0) * DK;
+    for (int idx = tid; idx < C * (DK / 8); idx += 256) {
+      const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
+      const Frag8<T> fk = ld8(sKt + r * LDK + c0);
+      Frag8<T> fw;
+      const float wr = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[r]) : 1.f;
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) fw.set(s2, wr * fk.get(s2));
+      st8(Kr + r * DK + c0, fk);
+      st8(Kwr + r * DK + c0, fw);
     }
   }
   // ---- decayed write keys, transposed per chunk: (Kt * Lam_C / Lam_t)^T
@@ -520,6 +579,7 @@ __device__ __forceinline__ void flush_output(const FwdArgs& a, int i, int n, con
                                              const ScanCtx& x) {
   using SM = SlabMap<T>;
   constexpr int LDE = C + 8;
+  if (!a.o) return;
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int64_t HV = a.H * (int64_t)a.dv;
   T* ob = static_cast<T*>(a.o) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0;
@@ -541,7 +601,23 @@ __device__ __forceinline__ void flush_output(const FwdArgs& a, int i, int n, con
 // chunk's output (flushed first).  FULL: C valid tokens, so the step has no
 // per-row branches (a conditional store would make the compiler wait for the
 // prefetched loads); the ragged last chunk takes FULL = false.
-template <bool FULL, typename T, int DK, int GATE>
+// [v][t] (or [v][c]) LDS slab -> rows of a [rows][ld] global tensor: columns
+// x.v0 .. x.v0 + BV of rows 0 .. nrows-1, 16-byte stores
+template <typename T>
+__device__ __forceinline__ void flush_slab_t(T* dst, int64_t ld, const T* src, int lds, int nrows,
+                                             int tid) {
+  using SM = SlabMap<T>;
+  for (int idx = tid; idx < nrows * SM::kSegs; idx += 256) {
+    const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
+    float4 pk;
+    T* e = reinterpret_cast<T*>(&pk);
+#pragma unroll
+    for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = src[(c0 + s2) * lds + row];
+    *reinterpret_cast<float4*>(dst + row * ld + c0) = pk;
+  }
+}
+
+template <bool FULL, bool SAVE, typename T, int DK, int GATE>
 __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float4* vnext,
                                           floatx4 (&st)[DK / 64][2], const FwdArgs& a, int i,
                                           const ScanCtx& x, T* sH, T* sX, T* sE, T* sVt, T* sO) {
@@ -549,6 +625,9 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
   constexpr int LDH = DK + 8, LDE = C + 8;
   const int w = x.w, lr = x.lr, lg = x.lg;
   if (i > 0) flush_output<T>(a, i - 1, C, sO, x);   // only full chunks precede this one
+  if (SAVE)  // chunk-start state S^T of this chunk, rows c, columns of the slab
+    flush_slab_t<T>(static_cast<T*>(a.Hs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv, sH,
+                    LDH, DK, x.tid);
   float lam[4];
 #pragma unroll
   for (int ii = 0; ii < 4; ++ii) lam[ii] = GATE == kGateScalar ? fast_exp(f.g[ii]) : 1.f;
@@ -606,6 +685,11 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
     st4<T>(sE + (16 * vt + lr) * LDE + 16 * w + 4 * lg, accE[0], accE[1], accE[2], accE[3]);
   }
   lds_barrier();
+  if (SAVE) {  // X and E rows of this chunk (whole chunk: padded rows included)
+    const int64_t r0 = (x.bh * a.Tpad + static_cast<int64_t>(i) * C) * a.dv + x.v0;
+    flush_slab_t<T>(static_cast<T*>(a.Xr) + r0, a.dv, sX, LDE, C, x.tid);
+    flush_slab_t<T>(static_cast<T*>(a.Er) + r0, a.dv, sE, LDE, C, x.tid);
+  }
   // ---- O = scale [ (Lam Q) S^T + P E ];  S^T <- Diag(gamma_C) S^T + (Kt Gamma)^T E
   Frag8<T> fE[2][2];
 #pragma unroll
@@ -640,7 +724,9 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
   lds_barrier();
 }
 
-template <typename T, int DK, int GATE>
+// SAVE: also write the chunk-start states and the X, E rows (backward
+// recompute); the output is skipped when a.o is NULL.
+template <typename T, int DK, int GATE, bool SAVE>
 __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   constexpr int CT = DK / 64;       // state row tiles per wave
   constexpr int LDH = DK + 8, LDE = C + 8;
@@ -703,25 +789,25 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   int i = 0;
   for (; i + 2 < NF; i += 3) {
     scan_load(f2, a, i + 2, x);
-    scan_step<true>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
     scan_load(f0, a, min(i + 3, last), x);
-    scan_step<true>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
     scan_load(f1, a, min(i + 4, last), x);
-    scan_step<true>(f2, f0.v, st, a, i + 2, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE>(f2, f0.v, st, a, i + 2, x, sH, sX, sE, sVt, sO);
   }
   // f0, f1 hold chunks i, i + 1 (clamped to the last chunk)
   if (NF - i == 2) {
     scan_load(f2, a, min(i + 2, last), x);
-    scan_step<true>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
-    scan_step<true>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
     i += 2;
-    if (i < a.NT) scan_step<false>(f2, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+    if (i < a.NT) scan_step<false, SAVE>(f2, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
   } else if (NF - i == 1) {
-    scan_step<true>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
     i += 1;
-    if (i < a.NT) scan_step<false>(f1, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+    if (i < a.NT) scan_step<false, SAVE>(f1, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
   } else if (i < a.NT) {
-    scan_step<false>(f0, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<false, SAVE>(f0, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
   }
   flush_output<T>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
   if (a.S_T) {
@@ -766,19 +852,19 @@ WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precon
   return L;
 }
 
-template <typename T, int DK, int GATE, int PREC>
+template <typename T, int DK, int GATE, int PREC, bool BWD>
 static hipError_t launch_k2(const FwdArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((k2_chunk_prep<T, DK, GATE, PREC>), dim3(static_cast<unsigned>(a.BH * a.NT)),
+  hipLaunchKernelGGL((k2_chunk_prep<T, DK, GATE, PREC, BWD>), dim3(static_cast<unsigned>(a.BH * a.NT)),
                      dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
-template <typename T, int DK, int GATE>
+template <typename T, int DK, int GATE, bool BWD = false>
 static hipError_t launch_k2_prec(const FwdArgs& a, hipStream_t s) {
   switch (a.precond) {
-    case kSquash: return launch_k2<T, DK, GATE, kSquash>(a, s);
-    case kIdentity: return launch_k2<T, DK, GATE, kIdentity>(a, s);
-    default: return launch_k2<T, DK, GATE, kExternal>(a, s);
+    case kSquash: return launch_k2<T, DK, GATE, kSquash, BWD>(a, s);
+    case kIdentity: return launch_k2<T, DK, GATE, kIdentity, BWD>(a, s);
+    default: return launch_k2<T, DK, GATE, kExternal, BWD>(a, s);
   }
 }
 
@@ -806,14 +892,44 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
   const unsigned grid = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
   switch (a.gate) {
     case kGateNone:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone>), dim3(grid), dim3(256), 0, s, a); break;
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, false>), dim3(grid), dim3(256), 0, s, a); break;
     case kGateScalar:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar>), dim3(grid), dim3(256), 0, s, a); break;
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, false>), dim3(grid), dim3(256), 0, s, a); break;
     default:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel>), dim3(grid), dim3(256), 0, s, a); break;
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, false>), dim3(grid), dim3(256), 0, s, a); break;
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return mark(3);
+}
+
+// the backward's forward recompute: k1 (squash), k2 in backward mode and k3
+// saving chunk states and X, E rows (no output); scalar gate or none
+template <typename T, int DK>
+static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s) {
+  hipError_t e;
+  if (a.precond == kSquash) {
+    hipLaunchKernelGGL((k1_precond_summary<T, DK>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
+                       0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL((k1_precond_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  e = a.gate == kGateScalar ? launch_k2_prec<T, DK, kGateScalar, true>(a, s)
+                            : launch_k2_prec<T, DK, kGateNone, true>(a, s);
+  if (e != hipSuccess) return e;
+  const int64_t nslab = a.dv / BV;
+  const unsigned grid = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
+  if (a.gate == kGateScalar)
+    hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, true>), dim3(grid), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, true>), dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_forward_parts(const FwdArgs& a, int io_bf16, hipStream_t s, bool bwd) {
+  (void)bwd;
+  if (io_bf16) return a.dk == 64 ? launch_recompute<bf16, 64>(a, s) : launch_recompute<bf16, 128>(a, s);
+  return launch_recompute<float, 64>(a, s);
 }
 
 hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev) {

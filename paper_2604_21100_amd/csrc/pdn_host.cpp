@@ -133,6 +133,14 @@ pdn_status check_inputs(const pdn_problem* p, const pdn_inputs* in, const Sizes&
   return PDN_OK;
 }
 
+// the backward covers the no-gate and scalar-gate forms; fp32 io at head
+// dims 64
+pdn_status check_bwd_support(const pdn_problem* p) {
+  if (p->gate == PDN_GATE_CHANNEL) return PDN_ERR_UNSUPPORTED;
+  if (p->io == PDN_F32 && (p->dk != 64 || p->dv != 64)) return PDN_ERR_UNSUPPORTED;
+  return PDN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -160,7 +168,12 @@ pdn_status pdn_workspace_size(const pdn_problem* p, int with_bwd, size_t* bytes)
   Sizes s;
   const pdn_status st = check_problem(p, &s);
   if (st != PDN_OK) return st;
-  (void)with_bwd;
+  if (with_bwd) {
+    const pdn_status sb = check_bwd_support(p);
+    if (sb != PDN_OK) return sb;
+    *bytes = pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond).total;
+    return PDN_OK;
+  }
   const pdn::WsLayout L = pdn::fwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, s.esz, p->gate,
                                              p->precond);
   *bytes = L.total;
@@ -244,8 +257,81 @@ pdn_status pdn_chunk_bwd(const pdn_problem* p, const pdn_inputs* in, const void*
   if (st != PDN_OK) return st;
   std::vector<Buf> ins;
   if ((st = check_inputs(p, in, s, &ins)) != PDN_OK) return st;
-  (void)dO; (void)dS_T; (void)out; (void)ws; (void)ws_bytes; (void)hip_stream;
-  return PDN_ERR_UNSUPPORTED;
+  if ((st = check_bwd_support(p)) != PDN_OK) return st;
+  if (!out) return PDN_ERR_NULL;
+  const bool tok = s.tok > 0;
+  if (tok && (!dO || !out->dq || !out->dk || !out->dv || !out->dbeta)) return PDN_ERR_NULL;
+  if (tok && p->gate != PDN_GATE_NONE && !out->dg) return PDN_ERR_NULL;
+  if (p->gate == PDN_GATE_NONE && out->dg) return PDN_ERR_VALUE;
+  const bool sq = p->precond == PDN_PRECOND_SQUASH;
+  if (!sq && (out->dbeta_p || out->dg_p || out->dlog_a_scale || out->dA0)) return PDN_ERR_VALUE;
+  if (p->precond != PDN_PRECOND_EXTERNAL && out->dktilde) return PDN_ERR_VALUE;
+  ins.push_back({dO, s.nv * s.esz});
+  ins.push_back({dS_T, s.nS * 4});
+  const int64_t e = s.esz;
+  const std::vector<Buf> outs = {
+      {out->dq, s.nq * e},        {out->dk, s.nq * e},          {out->dv, s.nv * e},
+      {out->dbeta, s.nscal * 4},  {out->dg, s.ngate * 4},       {out->dS0, s.nS * 4},
+      {out->dbeta_p, s.nscal * 4}, {out->dg_p, s.nscal * 4},    {out->dlog_a_scale, p->H * 4},
+      {out->dA0, s.nA * 4},       {out->dktilde, s.nq * e}};
+  for (const Buf& x : outs)
+    if (x.p && !aligned16(x.p)) return PDN_ERR_ALIGN;
+  for (const Buf& x : ins)
+    if (x.p && !aligned16(x.p)) return PDN_ERR_ALIGN;
+  const pdn::BwdWsLayout L =
+      pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond);
+  if ((st = check_aliasing(ins, outs, Buf{ws, tok ? static_cast<int64_t>(ws_bytes) : 0})) != PDN_OK)
+    return st;
+  if (tok && (!ws || ws_bytes < L.total || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0))
+    return PDN_ERR_WORKSPACE;
+  if (s.BH == 0) return PDN_OK;
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  if (!tok) {
+    // T == 0: the state passes through unchanged
+    pdn::FwdArgs f{};
+    f.BH = s.BH; f.dk = p->dk; f.dv = p->dv;
+    f.S0 = dS_T; f.S_T = out->dS0; f.A0 = nullptr; f.A_T = out->dA0;
+    const hipError_t he = pdn::launch_forward(f, p->io == PDN_BF16, stream);
+    return he == hipSuccess ? PDN_OK : PDN_ERR_HIP;
+  }
+  pdn::BwdArgs a{};
+  pdn::FwdArgs& f = a.f;
+  f.B = p->B; f.T = p->T; f.H = p->H; f.BH = s.BH;
+  f.NT = static_cast<int>(s.NT);
+  f.Tpad = s.NT * kChunk;
+  f.dk = p->dk; f.dv = p->dv;
+  f.gate = p->gate; f.precond = p->precond;
+  f.lnx = std::log(p->x);
+  f.scale = p->scale;
+  f.q = in->q; f.k = in->k; f.v = in->v; f.ktilde = in->ktilde;
+  f.beta = in->beta; f.g = in->g; f.beta_p = in->beta_p; f.g_p = in->g_p;
+  f.log_a_scale = in->log_a_scale; f.A0 = in->A0; f.S0 = in->S0;
+  f.o = nullptr; f.S_T = nullptr; f.A_T = nullptr;
+  char* w = static_cast<char*>(ws);
+  if (sq) {
+    f.sumL = reinterpret_cast<float*>(w + L.f.sumL);
+    f.sumD = reinterpret_cast<float*>(w + L.f.sumD);
+    f.Abound = reinterpret_cast<float*>(w + L.f.Abound);
+  }
+  f.KtG = w + L.f.KtG; f.Tm = w + L.f.Tm; f.Pm = w + L.f.Pm;
+  if (p->gate != PDN_GATE_NONE) f.G = reinterpret_cast<float*>(w + L.f.G);
+  f.Hs = w + L.Hs; f.Xr = w + L.Xr; f.Er = w + L.Er; f.PtT = w + L.PtT; f.TtT = w + L.TtT;
+  f.Mi = reinterpret_cast<float*>(w + L.Mi);
+  f.Ktr = w + L.Ktr; f.Kw = w + L.Kw; f.QlT = w + L.QlT; f.KnT = w + L.KnT;
+  a.dO = dO; a.dS_T = dS_T;
+  a.dq = out->dq; a.dk = out->dk; a.dv = out->dv; a.dbeta = out->dbeta; a.dg = out->dg;
+  a.dS0 = out->dS0; a.dbeta_p = out->dbeta_p; a.dg_p = out->dg_p; a.dlog_a_scale = out->dlog_a_scale;
+  a.dA0 = out->dA0; a.dktilde = out->dktilde;
+  a.dHs = w + L.dHs; a.dEr = w + L.dEr; a.dXr = w + L.dXr;
+  a.dSqk = w + L.dSqk; a.dSqkT = w + L.dSqkT; a.dSkk = w + L.dSkk; a.dSkkT = w + L.dSkkT;
+  a.dGp = reinterpret_cast<float*>(w + L.dGp);
+  a.dKt = reinterpret_cast<float*>(w + L.dKt);
+  a.dKm = reinterpret_cast<float*>(w + L.dKm);
+  a.pcL = reinterpret_cast<float*>(w + L.pcL);
+  a.pcC = reinterpret_cast<float*>(w + L.pcC);
+  a.pcMu = reinterpret_cast<float*>(w + L.pcMu);
+  const hipError_t he = pdn::launch_backward(a, p->io == PDN_BF16, stream);
+  return he == hipSuccess ? PDN_OK : PDN_ERR_HIP;
 }
 
 }  // extern "C"

@@ -47,6 +47,51 @@ struct FwdArgs {
   void* Tm;       // [BH, NT, C, C]  T = (I + At)^{-1} Diag(beta), io dtype
   void* Pm;       // [BH, NT, C, C]  causal (Q*Lam)(Kt/Lam)^T, io dtype
   float* G;       // [BH, Tpad] or [BH, Tpad, dk] in-chunk log-decay prefix
+  // backward only (NULL in the forward): forward intermediates kept for the
+  // adjoint kernels.  lam_r = exp(G_r), w_r = exp(G_{C-1} - G_r).
+  void* Hs;       // [BH, NT, dk, dv] io  chunk-start states S^T
+  void* Xr;       // [BH, Tpad, dv] io    X = V - (Lam K) S^T rows
+  void* Er;       // [BH, Tpad, dv] io    E = T X rows
+  void* PtT;      // [BH, NT, C, C] io    P^T
+  void* TtT;      // [BH, NT, C, C] io    T^T
+  float* Mi;      // [BH, NT, C, C] fp32  M = (I + At)^{-1} (T = M Diag(beta))
+  void* Ktr;      // [BH, Tpad, dk] io    write key rows
+  void* Kw;       // [BH, Tpad, dk] io    w_r * write key rows
+  void* QlT;      // [BH, NT, dk, C] io   (Diag(lam) Q)^T per chunk
+  void* KnT;      // [BH, NT, dk, C] io   -(Diag(lam) K)^T per chunk
+};
+
+// Backward-only arguments and workspace (the forward recompute uses f).
+struct BwdArgs {
+  FwdArgs f;
+  const void* dO;       // [B, T, H, dv] io
+  const float* dS_T;    // [B, H, dk, dv] or NULL
+  // outputs
+  void* dq;
+  void* dk;
+  void* dv;
+  float* dbeta;
+  float* dg;
+  float* dS0;
+  float* dbeta_p;
+  float* dg_p;
+  float* dlog_a_scale;
+  float* dA0;
+  void* dktilde;
+  // workspace
+  void* dHs;      // [BH, NT, dk, dv] io  state adjoint entering each chunk from the right
+  void* dEr;      // [BH, Tpad, dv] io    dE rows
+  void* dXr;      // [BH, Tpad, dv] io    dX rows (= dV, padded to whole chunks)
+  void* dSqk;     // [BH, NT, C, C] io    d(Q Kt^T), masked and decayed
+  void* dSqkT;    // transposed
+  void* dSkk;     // [BH, NT, C, C] io    d(K Kt^T)
+  void* dSkkT;
+  float* dGp;     // [BH, Tpad] fp32      gate-prefix gradient from the C x C terms
+  float* dKt;     // [BH, Tpad, dk] fp32  gradient of the write key
+  float* dKm;     // [BH, Tpad, dk] fp32  gradient of the read key (main recurrence)
+  float* pcL;     // [BH, NT, dk]         preconditioner: in-chunk adjoint at chunk start
+  float* pcC;     // [BH, NT + 1, dk]     preconditioner: adjoint carried into each chunk
+  float* pcMu;    // [BH, NT]             preconditioner: partial d mu
 };
 
 struct WsLayout {
@@ -54,6 +99,16 @@ struct WsLayout {
 };
 
 WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precond);
+
+struct BwdWsLayout {
+  WsLayout f;
+  size_t Hs, Xr, Er, PtT, TtT, Mi, Ktr, Kw, QlT, KnT;
+  size_t dHs, dEr, dXr, dSqk, dSqkT, dSkk, dSkkT, dGp, dKt, dKm, pcL, pcC, pcMu, total;
+};
+
+BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond);
+
+hipError_t launch_backward(const BwdArgs& a, int io_bf16, hipStream_t stream);
 
 // ev: NULL or 4 events recorded at the stage boundaries (see
 // pdn_chunk_fwd_events)
