@@ -3,17 +3,22 @@
 
 Default workload: the 1B-scale Preconditioned Gated DeltaNet layer (bf16 q/k/v,
 fp32 state, B=4, T=4096, H=16, d_k=d_v=128, chunk 64, scalar gate, squash
-preconditioner with x=1.5).  One step is one pass of the forward hot path
-(preconditioner scan, per-chunk UT transform, inter-chunk state scan with the
-chunk output) over the whole batch, with inputs resident in HBM.
+preconditioner with x=1.5).  One step is one pass of the whole hot path over
+the batch, with inputs resident in HBM: the forward (preconditioner scan,
+per-chunk UT transform, inter-chunk state scan with the chunk output) and then
+the backward for an upstream gradient dO (recompute of the forward
+intermediates, reverse state-adjoint scan, per-chunk adjoint algebra, the
+preconditioner's reverse scan).  --pass fwd times the forward alone.
 
 Prints ONE JSON line: tokens/s (B*T per step time), the roofline of the
 dominant kernel measured live with HIP events on the launch stream, and the
-float64 CPU oracle timed on a bounded sample on the host's cores.
+float64 CPU oracle (forward and adjoint) timed on a bounded sample on the
+host's cores.
 """
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -35,45 +40,100 @@ PEAK_FP32_TFLOPS = 157.3       # dense fp32 matrix
 def algorithmic_per_token_head(spec):
     """Algorithmic FLOPs and bytes per token-head (one (b, t, h)).
 
-    Whole forward (dense per-chunk products as the paper writes them):
-        FLOP = 6 C dk + 4 C dv + 6 dk dv + C^2 / 3
-    and the compulsory bytes of each kernel (inputs read once, outputs written
-    once).  Returns (flop_total, {stage: (flop, bytes)})."""
+    Dense per-chunk products as the paper writes them:
+        forward  FLOP = 6 C dk + 4 C dv + 6 dk dv + C^2 / 3
+        backward FLOP = 12 C dk + 8 C dv + 12 dk dv + 4 C^2
+    (the backward's recompute of forward intermediates is executed work, not
+    algorithmic, and is not in the totals).  Per kernel stage: its share of
+    those FLOPs (the recompute stages: the products they execute) and its
+    compulsory bytes (what that kernel must read and write, each once).
+    Returns (flop_fwd, flop_bwd, {stage: (flop, bytes)})."""
     C, dk, dv = spec.chunk, spec.dk, spec.dv
     e = 2 if spec.io == "bf16" else 4
-    gate_b = {"none": 0, "scalar": 4, "channel": 4 * dk}[spec.gate]
-    flop = 6 * C * dk + 4 * C * dv + 6 * dk * dv + C * C / 3.0
+    gb = {"none": 0, "scalar": 4, "channel": 4 * dk}[spec.gate]
+    st = e * dk * dv / C                       # one chunk-start state, per token
+    flop_fwd = 6 * C * dk + 4 * C * dv + 6 * dk * dv + C * C / 3.0
+    flop_bwd = 12 * C * dk + 8 * C * dv + 12 * dk * dv + 4 * C * C
+    precond = (3 * dk, e * dk + 8 + 4 * dk / C)
     stages = {
         # k1: read k, betaP, gP; write the per-chunk summaries
-        "precond": (3 * dk, e * dk + 8 + 4 * dk / C),
+        "precond": precond,
         # k2: read q, k, beta, g, betaP, gP, chunk-start A; write the decayed
         # write keys (dk), T and P (C each) and the gate prefix
         "chunk_prep": (4 * C * dk + C * C / 3.0,
-                       2 * e * dk + 12 + gate_b + 4 * dk / C
-                       + e * (dk + 2 * C) + gate_b),
+                       2 * e * dk + 12 + gb + 4 * dk / C
+                       + e * (dk + 2 * C) + gb),
         # k3: read q, k, v, T, P, decayed write keys, gate prefix; write o
         "chunk_scan": (6 * dk * dv + 4 * C * dv,
-                       e * (2 * dk + dv) + e * (2 * C + dk) + gate_b + e * dv),
+                       e * (2 * dk + dv) + e * (2 * C + dk) + gb + e * dv),
+        "bwd_precond_recompute": precond,
+        # k2 (backward): as k2, plus P^T, T^T (C each, io), M (C, fp32) and
+        # the write-key, decayed write-key, decayed query and key rows (dk
+        # each, io)
+        "bwd_chunk_prep": (4 * C * dk + C * C / 3.0,
+                           2 * e * dk + 12 + gb + 4 * dk / C
+                           + e * (dk + 2 * C) + gb
+                           + 2 * e * C + 4 * C + 4 * e * dk),
+        # k3 (saving): read k, v, T, decayed write keys, gate prefix; write
+        # the chunk-start states and the X, E rows
+        "bwd_state_save_scan": (4 * dk * dv + 2 * C * dv,
+                                e * (dk + dv) + e * (C + dk) + gb
+                                + st + 2 * e * dv),
+        # r1: read P^T, T^T, w*Kt, (lam Q)^T, -(lam K)^T, dO; write the state
+        # adjoints, dE, dX rows and dv
+        "bwd_state_adjoint_scan": (4 * C * dv + 6 * dk * dv,
+                                   2 * e * C + 3 * e * dk + e * dv + 4 / C
+                                   + st + 3 * e * dv),
+        # p1: read dO, E, dE, X, M, beta, gate prefix, q, kt, k; write the
+        # four masked C x C adjoints (and transposes), dbeta, dG partial
+        "bwd_chunk_cc": (4 * C * dv + 4 * C * dk + 4 * C * C,
+                         4 * e * dv + 4 * C + 4 + gb + 3 * e * dk
+                         + 4 * e * C + 8),
+        # p2: read dO, dX, E, S, dS', gate prefix, kt, q, k, the C x C
+        # adjoints, dG partial; write dq, dk (read key, fp32), dkt (fp32), dg
+        "bwd_chunk_grads": (6 * dk * dv + 8 * C * dk,
+                            3 * e * dv + 2 * st + gb + 3 * e * dk + 4 * e * C
+                            + 4 + e * dk + 8 * dk + 4),
+        # pc: read k, dk (read key), dkt, betaP, gP, chunk-start A; write dk,
+        # dbetaP, dgP
+        "bwd_precond_reverse": (10 * dk,
+                                e * dk + 8 * dk + 8 + 4 * dk / C + e * dk + 8),
     }
-    return flop, stages
+    return flop_fwd, flop_bwd, stages
+
+
+KERNELS = {
+    "precond": "k1_precond_summary+k1_precond_carry",
+    "chunk_prep": "k2_chunk_prep",
+    "chunk_scan": "k3_chunk_scan",
+    "bwd_precond_recompute": "k1_precond_summary+k1_precond_carry",
+    "bwd_chunk_prep": "k2_chunk_prep (backward mode)",
+    "bwd_state_save_scan": "k3_chunk_scan (saving mode)",
+    "bwd_state_adjoint_scan": "r1_state_adjoint",
+    "bwd_chunk_cc": "p1_chunk_cc",
+    "bwd_chunk_grads": "p2_chunk_grads",
+    "bwd_precond_reverse": "pc_chunk+pc_carry+pc_chunk+pc_mu",
+}
 
 
 def _oracle_job(args):
     from threadpoolctl import threadpool_limits
     from oracle import abi as oabi
-    sample, kw, heads = args
+    sample, kw, heads, bwd = args
     with threadpool_limits(1):
         t0 = time.perf_counter()
         oabi.forward(sample, heads=heads, **kw)
+        if bwd:
+            oabi.backward(sample, heads=heads, **kw)
         return time.perf_counter() - t0
 
 
-def cpu_baseline(spec, inp, target_s=15.0):
-    """Time the float64 oracle (token recurrence, as it stands) on a bounded
-    sample: every head of the first nb batches over a prefix of Ts tokens,
-    heads spread over worker processes.  nb and Ts are sized from a
-    calibration run to about target_s of CPU time.  Returns the cpu_baseline
-    object."""
+def cpu_baseline(spec, inp, bwd, target_s=15.0):
+    """Time the float64 oracle as it stands (token recurrence forward, and
+    for bwd its adjoint as well) on a bounded sample: every head of the first
+    nb batches over a prefix of Ts tokens, heads spread over worker
+    processes.  nb and Ts are sized from a calibration run to about target_s
+    of CPU time.  Returns the cpu_baseline object."""
     from concurrent.futures import ProcessPoolExecutor
     ncpu = len(os.sched_getaffinity(0))
     kw = dict(gate=spec.gate, precond="squash", x=spec.x, scale=spec.scale)
@@ -81,7 +141,7 @@ def cpu_baseline(spec, inp, target_s=15.0):
     def sample_of(nb, Ts):
         s = {}
         for key, a in inp.items():
-            if a is None or key == "dO":
+            if a is None or (key == "dO" and not bwd):
                 s[key] = None
             elif key == "log_a_scale":
                 s[key] = a
@@ -96,13 +156,13 @@ def cpu_baseline(spec, inp, target_s=15.0):
         groups = [g for g in (heads[i::workers] for i in range(workers)) if g]
         smp = sample_of(nb, Ts)
         t0 = time.perf_counter()
-        list(ex.map(_oracle_job, [(smp, kw, g) for g in groups]))
+        list(ex.map(_oracle_job, [(smp, kw, g, bwd) for g in groups]))
         return time.perf_counter() - t0, len(heads) * Ts
 
     workers = max(1, min(16, ncpu, spec.B * spec.H))
     with ProcessPoolExecutor(max_workers=workers) as ex:
         run(ex, workers, 1, min(spec.T, 8))               # start the workers
-        Tc = min(spec.T, 256)
+        Tc = min(spec.T, 128)
         nbc = max(1, min(spec.B, -(-workers // spec.H)))
         tc, nc = run(ex, workers, nbc, Tc)
         rate = nc / tc                                     # token-heads / s
@@ -110,16 +170,40 @@ def cpu_baseline(spec, inp, target_s=15.0):
         nb = int(min(spec.B, max(1, round(want / (spec.H * spec.T)))))
         Ts = int(min(spec.T, max(Tc, want / (nb * spec.H))))
         wall, token_heads = run(ex, workers, nb, Ts)
+    what = "forward + adjoint" if bwd else "forward"
     return {
         "value": (token_heads / spec.H) / wall,
         "unit": "tokens/s",
         "cores": workers,
         "kind": "oracle",
-        "sample": (f"float64 token-recurrence oracle, forward, batches 0..{nb - 1}"
-                   f" x all {spec.H} heads, first {Ts} of {spec.T} tokens "
-                   f"({token_heads} token-heads in {wall:.1f} s on {workers} "
-                   f"worker processes x 1 thread); value = token-heads/s / H"),
+        "sample": (f"float64 token-recurrence oracle, {what}, batches "
+                   f"0..{nb - 1} x all {spec.H} heads, first {Ts} of {spec.T} "
+                   f"tokens ({token_heads} token-heads in {wall:.1f} s on "
+                   f"{workers} worker processes x 1 thread); value = "
+                   f"token-heads/s / H"),
     }
+
+
+def roofline_of(stage, ms, stages, token_heads):
+    """Roofline object for one kernel stage from its measured average time."""
+    dflop, dbytes = stages[stage]
+    sec = ms / 1e3
+    if dflop / dbytes >= PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
+        ach = dflop * token_heads / sec / 1e12
+        roof = {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s"}
+    else:
+        ach = dbytes * token_heads / sec / 1e9
+        roof = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS,
+                "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = KERNELS[stage]
+    roof["stage"] = stage
+    roof["avg_ms"] = ms
+    roof["alg_bytes_per_launch"] = dbytes * token_heads
+    roof["alg_flop_per_launch"] = dflop * token_heads
+    return roof
 
 
 def main(argv=None):
@@ -129,6 +213,8 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
                     choices=sorted(pi.WORKLOADS))
+    ap.add_argument("--pass", dest="passes", default="fwdbwd",
+                    choices=("fwd", "fwdbwd"))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -141,11 +227,19 @@ def main(argv=None):
               "in DESIGN.md but not built)", file=sys.stderr)
         return 2
 
+    bwd = args.passes == "fwdbwd"
     spec = pi.WORKLOADS[args.workload]
+    if bwd and spec.gate == "channel":
+        print("bench.py: the backward supports no gate or a scalar gate; "
+              "use --pass fwd for the per-channel gate", file=sys.stderr)
+        return 2
+    if bwd and not spec.with_do:
+        # dO is the last draw: every other input is unchanged
+        spec = dataclasses.replace(spec, with_do=True)
     seed = pi.WORKLOAD_SEEDS[args.workload]
     inp = pi.generate(spec, seed)
     # the CPU leg runs before the GPU is touched (its worker processes fork)
-    cpu = None if args.no_cpu_baseline else cpu_baseline(spec, inp,
+    cpu = None if args.no_cpu_baseline else cpu_baseline(spec, inp, bwd,
                                                          args.cpu_seconds)
 
     import torch
@@ -155,84 +249,103 @@ def main(argv=None):
     io_dt = torch.bfloat16 if spec.io == "bf16" else torch.float32
     d = {}
     for key, a in inp.items():
-        if a is None or key == "dO":
+        if a is None:
             d[key] = None
             continue
         t = torch.from_numpy(np.ascontiguousarray(a))
-        d[key] = (t.to(io_dt) if key in ("q", "k", "v") else t).to(dev)
+        d[key] = (t.to(io_dt) if key in ("q", "k", "v", "dO") else t).to(dev)
     B, T, H, dk, dv = spec.B, spec.T, spec.H, spec.dk, spec.dv
     o = torch.empty((B, T, H, dv), dtype=io_dt, device=dev)
     S_T = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev)
     A_T = torch.empty((B, H, dk), dtype=torch.float32, device=dev)
     prob = pdn.make_problem(B, T, H, dk, dv, io=spec.io, gate=spec.gate,
                             x=spec.x, scale=spec.scale)
-    ws = torch.empty(pdn.pdn_workspace_size(prob), dtype=torch.uint8,
-                     device=dev)
+    ws = torch.empty(pdn.pdn_workspace_size(prob, with_bwd=bwd),
+                     dtype=torch.uint8, device=dev)
+    grads = None
+    if bwd:
+        f32 = dict(dtype=torch.float32, device=dev)
+        grads = {
+            "dq": torch.empty((B, T, H, dk), dtype=io_dt, device=dev),
+            "dk": torch.empty((B, T, H, dk), dtype=io_dt, device=dev),
+            "dv": torch.empty((B, T, H, dv), dtype=io_dt, device=dev),
+            "dbeta": torch.empty((B, T, H), **f32),
+            "dg": torch.empty((B, T, H), **f32) if spec.gate == "scalar"
+            else None,
+            "dS0": torch.empty((B, H, dk, dv), **f32),
+            "dbeta_p": torch.empty((B, T, H), **f32),
+            "dg_p": torch.empty((B, T, H), **f32),
+            "dlog_a_scale": torch.empty((H,), **f32),
+            "dA0": torch.empty((B, H, dk), **f32),
+        }
     calib = None
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20) // 4
         calib = (torch.empty(n, dtype=torch.float32, device=dev).uniform_(),
                  torch.empty(n, dtype=torch.float32, device=dev))
     stream = torch.cuda.current_stream(dev)
+    fwd_stages = list(pdn.FWD_STAGES)
+    bwd_stages = list(pdn.BWD_STAGES) if bwd else []
 
-    def step(events=None):
+    def step(fev=None, bev=None):
         pdn.pdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], g=d["g"],
                           gate=spec.gate, beta_p=d["beta_p"], g_p=d["g_p"],
                           log_a_scale=d["log_a_scale"], A0=d["A0"],
                           S0=d["S0"], x=spec.x, scale=spec.scale, o=o,
                           S_T=S_T, A_T=A_T, workspace=ws, stream=stream,
-                          stage_events=events)
+                          stage_events=fev)
+        if bwd:
+            pdn.pdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], d["dO"],
+                              g=d["g"], gate=spec.gate, beta_p=d["beta_p"],
+                              g_p=d["g_p"], log_a_scale=d["log_a_scale"],
+                              A0=d["A0"], S0=d["S0"], x=spec.x,
+                              scale=spec.scale, outputs=grads, workspace=ws,
+                              stream=stream, stage_events=bev)
         if calib is not None:
             calib[1].copy_(calib[0])
 
     for _ in range(args.warmup):
         step()
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)]
-          for _ in range(K)]
+    mk = lambda n: [torch.cuda.Event(enable_timing=True) for _ in range(n)]  # noqa: E731
+    fev = [mk(len(fwd_stages) + 1) for _ in range(K)]
+    bev = [mk(len(bwd_stages) + 1) for _ in range(K)] if bwd else [None] * K
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record(stream)
     for i in range(K):
-        step(ev[i])
+        step(fev[i], bev[i])
     end.record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / K
     stage_ms = {}
-    for si, name in enumerate(pdn.FWD_STAGES):
-        stage_ms[name] = sum(ev[i][si].elapsed_time(ev[i][si + 1])
+    for si, name in enumerate(fwd_stages):
+        stage_ms[name] = sum(fev[i][si].elapsed_time(fev[i][si + 1])
                              for i in range(K)) / K
+    for si, name in enumerate(bwd_stages):
+        stage_ms[name] = sum(bev[i][si].elapsed_time(bev[i][si + 1])
+                             for i in range(K)) / K
+    fwd_ms = sum(fev[i][0].elapsed_time(fev[i][-1]) for i in range(K)) / K
+    bwd_ms = (sum(bev[i][0].elapsed_time(bev[i][-1]) for i in range(K)) / K
+              if bwd else None)
 
     tokens = B * T
     token_heads = B * T * H
-    flop_tok, stages = algorithmic_per_token_head(spec)
+    flop_fwd, flop_bwd, stages = algorithmic_per_token_head(spec)
     dom = max(stage_ms, key=stage_ms.get)
-    dflop, dbytes = stages[dom]
-    dom_s = stage_ms[dom] / 1e3
-    if dflop / dbytes >= PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
-        ach = dflop * token_heads / dom_s / 1e12
-        roof = {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s"}
-    else:
-        ach = dbytes * token_heads / dom_s / 1e9
-        roof = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS,
-                "unit": "GB/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
-    roof["kernel"] = {"precond": "k1_precond_summary+k1_precond_carry",
-                      "chunk_prep": "k2_chunk_prep",
-                      "chunk_scan": "k3_chunk_scan"}[dom]
-    roof["avg_ms"] = stage_ms[dom]
-    roof["alg_bytes_per_launch"] = dbytes * token_heads
-    roof["alg_flop_per_launch"] = dflop * token_heads
+    roof = roofline_of(dom, stage_ms[dom], stages, token_heads)
+    kernels = {k: roofline_of(k, v, stages, token_heads)["frac"]
+               for k, v in stage_ms.items()}
 
+    flop_step = flop_fwd + (flop_bwd if bwd else 0.0)
     step_s = ms_per_step / 1e3
-    tflops = flop_tok * token_heads / step_s / 1e12
+    tflops = flop_step * token_heads / step_s / 1e12
     peak_tf = PEAK_BF16_TFLOPS if spec.io == "bf16" else PEAK_FP32_TFLOPS
+    variant = {"scalar": "PGDN", "channel": "PKDA"}.get(spec.gate, "PDN")
     line = {
         "metric": "tokens/s of chunkwise PDN fwd(+bwd) at 1B layer shape; "
                   "% bf16 MFMA peak",
@@ -247,15 +360,20 @@ def main(argv=None):
         "vs_baseline": None,
         "dtype": spec.io,
         "data": "synthetic",
-        "config": {"workload": args.workload, "variant": "PGDN" if spec.gate == "scalar" else ("PKDA" if spec.gate == "channel" else "PDN"),
-                   "pass": "forward", "B": B, "T": T, "H": H, "dk": dk,
-                   "dv": dv, "chunk": spec.chunk, "gate": spec.gate,
+        "config": {"workload": args.workload, "variant": variant,
+                   "pass": "forward+backward" if bwd else "forward",
+                   "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
+                   "chunk": spec.chunk, "gate": spec.gate,
                    "precond": "squash", "x": spec.x, "global_batch": B,
                    "seq_len": T, "parallelism": "none (1 GPU)"},
         "tflops": tflops,
         "mfma_frac": tflops / peak_tf,
-        "alg_flop_per_token_head": flop_tok,
+        "alg_flop_per_token_head": flop_step,
+        "fwd_ms": fwd_ms,
+        "fwd_tokens_per_s": tokens / (fwd_ms / 1e3),
+        "bwd_ms": bwd_ms,
         "stage_ms": stage_ms,
+        "stage_roofline_frac": kernels,
         "wall_s_timed": t_wall,
         "roofline": roof,
         "cpu_baseline": cpu,

@@ -167,6 +167,22 @@ pdn_status pdn_chunk_bwd(const pdn_problem* problem, const pdn_inputs* in,
                          const void* dO, const float* dS_T, pdn_bwd_out* out,
                          void* ws, size_t ws_bytes, void* hip_stream);
 
+/* pdn_chunk_bwd that also records caller-created HIP events on `hip_stream`
+ * at its stage boundaries (n_events must be PDN_BWD_STAGE_EVENTS):
+ *   [0] start  [1] after the preconditioner recompute (k1_*)
+ *   [2] after the per-chunk prep recompute (k2, backward mode)
+ *   [3] after the state-saving forward scan (k3)
+ *   [4] after the reverse state-adjoint scan (r1)
+ *   [5] after the per-chunk C x C adjoint algebra (p1)
+ *   [6] after the per-chunk q/k/kt/gate gradients (p2)
+ *   [7] after the preconditioner's reverse scan (pc_*) or the key combine
+ * Results are identical to pdn_chunk_bwd. */
+#define PDN_BWD_STAGE_EVENTS 8
+pdn_status pdn_chunk_bwd_events(const pdn_problem* problem, const pdn_inputs* in,
+                                const void* dO, const float* dS_T, pdn_bwd_out* out,
+                                void* ws, size_t ws_bytes, void* hip_stream,
+                                void* const* stage_events, int n_events);
+
 /* Static, NUL-terminated description of a status code. */
 const char* pdn_status_string(pdn_status status);
 

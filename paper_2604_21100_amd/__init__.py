@@ -20,7 +20,36 @@ if not os.path.exists(LIB_PATH):
         f"{LIB_PATH} is missing: build the HIP library first "
         "(python -c 'import __graft_entry__ as g; g.build()' or "
         "python paper_2604_21100_amd/_build.py)")
+
+# The library and torch must share one HIP runtime.  torch ships its own
+# libamdhip64 / libhsa-runtime64 under the same sonames as the system ROCm
+# that libpdn.so is linked against: if libpdn.so were loaded first, torch
+# would later map a second pair, and two HSA runtimes in one process make
+# every HIP call undefined.  Loading torch first makes libpdn.so bind to the
+# runtime already in the process.
+try:
+    import torch  # noqa: F401
+except ImportError:   # no torch: the C ABI alone, nothing else maps HIP
+    torch = None
 _lib = ctypes.CDLL(LIB_PATH)
+
+
+def loaded_hip_runtimes():
+    """Paths of the HIP runtime libraries mapped into this process."""
+    try:
+        with open("/proc/self/maps") as f:
+            maps = f.read()
+    except OSError:
+        return []
+    return sorted({ln.split()[-1] for ln in maps.splitlines()
+                   if "libamdhip64" in ln and "/" in ln})
+
+
+if len(loaded_hip_runtimes()) > 1:
+    raise ImportError(
+        "two HIP runtimes are mapped into this process "
+        f"({loaded_hip_runtimes()}); import torch before anything that "
+        "loads the system ROCm runtime")
 
 # ---------------------------------------------------------------- enums
 PDN_OK, PDN_ERR_NULL, PDN_ERR_SHAPE, PDN_ERR_DTYPE, PDN_ERR_UNSUPPORTED, \
@@ -78,14 +107,25 @@ _lib.pdn_chunk_bwd.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs),
                                _vp, _vp, ctypes.POINTER(BwdOut), _vp,
                                ctypes.c_size_t, _vp]
 _lib.pdn_chunk_bwd.restype = ctypes.c_int
+_lib.pdn_chunk_bwd_events.argtypes = [
+    ctypes.POINTER(Problem), ctypes.POINTER(Inputs), _vp, _vp,
+    ctypes.POINTER(BwdOut), _vp, ctypes.c_size_t, _vp, ctypes.POINTER(_vp),
+    ctypes.c_int]
+_lib.pdn_chunk_bwd_events.restype = ctypes.c_int
 _lib.pdn_status_string.argtypes = [ctypes.c_int]
 _lib.pdn_status_string.restype = ctypes.c_char_p
 _lib.pdn_abi_version.argtypes = []
 _lib.pdn_abi_version.restype = ctypes.c_int
 
 EXPORTED = ("pdn_workspace_size", "pdn_chunk_fwd", "pdn_chunk_fwd_events",
-            "pdn_chunk_bwd", "pdn_status_string", "pdn_abi_version")
+            "pdn_chunk_bwd", "pdn_chunk_bwd_events", "pdn_status_string",
+            "pdn_abi_version")
+FWD_STAGE_EVENTS = 4   # PDN_FWD_STAGE_EVENTS
+BWD_STAGE_EVENTS = 8   # PDN_BWD_STAGE_EVENTS
 FWD_STAGES = ("precond", "chunk_prep", "chunk_scan")
+BWD_STAGES = ("bwd_precond_recompute", "bwd_chunk_prep", "bwd_state_save_scan",
+              "bwd_state_adjoint_scan", "bwd_chunk_cc", "bwd_chunk_grads",
+              "bwd_precond_reverse")
 
 
 class PdnError(RuntimeError):
@@ -228,7 +268,7 @@ def pdn_chunk_bwd(q, k, v, beta, dO, *, g=None, gate="none", precond="squash",
                   beta_p=None, g_p=None, log_a_scale=None, A0=None, S0=None,
                   ktilde=None, dS_T=None, x=1.5, scale=1.0, chunk=64,
                   outputs=None, want_optional=True, workspace=None,
-                  stream=None):
+                  stream=None, stage_events=None):
     """Backward pass on torch device tensors (layouts of pdn.h).
 
     Returns a dict with dq, dk, dv, dbeta and, when present, dg, dS0 and the
@@ -269,9 +309,17 @@ def pdn_chunk_bwd(q, k, v, beta, dO, *, g=None, gate="none", precond="squash",
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     inp = _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde)
     bo = BwdOut(*[_ptr(out.get(n)) for n, _ in BwdOut._fields_])
-    st = pdn_chunk_bwd_raw(prob, inp, _ptr(dO), _ptr(dS_T), bo,
-                           _ptr(workspace), workspace.numel(),
-                           _stream(stream, dev))
+    if stage_events is None:
+        st = pdn_chunk_bwd_raw(prob, inp, _ptr(dO), _ptr(dS_T), bo,
+                               _ptr(workspace), workspace.numel(),
+                               _stream(stream, dev))
+    else:
+        evs = [_event_handle(e) for e in stage_events]
+        arr = (_vp * len(evs))(*evs)
+        st = _lib.pdn_chunk_bwd_events(
+            ctypes.byref(prob), ctypes.byref(inp), _ptr(dO), _ptr(dS_T),
+            ctypes.byref(bo), _ptr(workspace), workspace.numel(),
+            _stream(stream, dev), arr, len(evs))
     if st != PDN_OK:
         raise PdnError(st, "pdn_chunk_bwd")
     return out

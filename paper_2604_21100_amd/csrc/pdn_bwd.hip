@@ -866,21 +866,25 @@ BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate,
   return L;
 }
 
-hipError_t launch_forward_parts(const FwdArgs& a, int io_bf16, hipStream_t s, bool bwd);
+hipError_t launch_forward_parts(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev);
 
 template <typename T, int DK, int DV, int GATE>
-static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s) {
+static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s, hipEvent_t const* ev) {
   const FwdArgs& a = ba.f;
   hipError_t e;
+  auto mark = [&](int i) { return ev ? hipEventRecord(ev[i], s) : hipSuccess; };
   const int64_t nslab = DV / BVB;
   const unsigned grid_scan = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
   const unsigned grid_chunk = static_cast<unsigned>(a.BH * a.NT);
   hipLaunchKernelGGL((r1_state_adjoint<T, DK, GATE>), dim3(grid_scan), dim3(256), 0, s, ba);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = mark(4)) != hipSuccess) return e;
   hipLaunchKernelGGL((p1_chunk_cc<T, DK, DV, GATE>), dim3(grid_chunk), dim3(256), 0, s, ba);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = mark(5)) != hipSuccess) return e;
   hipLaunchKernelGGL((p2_chunk_grads<T, DK, DV, GATE>), dim3(grid_chunk), dim3(256), 0, s, ba);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = mark(6)) != hipSuccess) return e;
   if (a.precond == kSquash) {
     hipLaunchKernelGGL((pc_chunk<T, DK, false>), dim3(grid_chunk), dim3(DK), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -898,32 +902,32 @@ static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s) {
                        s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  return hipSuccess;
+  return mark(7);
 }
 
 // fp32 io: head dims 64 only (LDS); the host validates this
-static hipError_t launch_bwd_f32(const BwdArgs& ba, hipStream_t s) {
-  return ba.f.gate == kGateScalar ? launch_bwd_typed<float, 64, 64, kGateScalar>(ba, s)
-                                  : launch_bwd_typed<float, 64, 64, kGateNone>(ba, s);
+static hipError_t launch_bwd_f32(const BwdArgs& ba, hipStream_t s, hipEvent_t const* ev) {
+  return ba.f.gate == kGateScalar ? launch_bwd_typed<float, 64, 64, kGateScalar>(ba, s, ev)
+                                  : launch_bwd_typed<float, 64, 64, kGateNone>(ba, s, ev);
 }
 
 template <typename T>
-static hipError_t launch_bwd_dims(const BwdArgs& ba, hipStream_t s) {
+static hipError_t launch_bwd_dims(const BwdArgs& ba, hipStream_t s, hipEvent_t const* ev) {
   const FwdArgs& a = ba.f;
   const bool sc = a.gate == kGateScalar;
   if (a.dk == 128 && a.dv == 128)
-    return sc ? launch_bwd_typed<T, 128, 128, kGateScalar>(ba, s) : launch_bwd_typed<T, 128, 128, kGateNone>(ba, s);
+    return sc ? launch_bwd_typed<T, 128, 128, kGateScalar>(ba, s, ev) : launch_bwd_typed<T, 128, 128, kGateNone>(ba, s, ev);
   if (a.dk == 128 && a.dv == 64)
-    return sc ? launch_bwd_typed<T, 128, 64, kGateScalar>(ba, s) : launch_bwd_typed<T, 128, 64, kGateNone>(ba, s);
+    return sc ? launch_bwd_typed<T, 128, 64, kGateScalar>(ba, s, ev) : launch_bwd_typed<T, 128, 64, kGateNone>(ba, s, ev);
   if (a.dk == 64 && a.dv == 128)
-    return sc ? launch_bwd_typed<T, 64, 128, kGateScalar>(ba, s) : launch_bwd_typed<T, 64, 128, kGateNone>(ba, s);
-  return sc ? launch_bwd_typed<T, 64, 64, kGateScalar>(ba, s) : launch_bwd_typed<T, 64, 64, kGateNone>(ba, s);
+    return sc ? launch_bwd_typed<T, 64, 128, kGateScalar>(ba, s, ev) : launch_bwd_typed<T, 64, 128, kGateNone>(ba, s, ev);
+  return sc ? launch_bwd_typed<T, 64, 64, kGateScalar>(ba, s, ev) : launch_bwd_typed<T, 64, 64, kGateNone>(ba, s, ev);
 }
 
-hipError_t launch_backward(const BwdArgs& ba, int io_bf16, hipStream_t s) {
-  hipError_t e = launch_forward_parts(ba.f, io_bf16, s, true);
+hipError_t launch_backward(const BwdArgs& ba, int io_bf16, hipStream_t s, hipEvent_t const* ev) {
+  hipError_t e = launch_forward_parts(ba.f, io_bf16, s, ev);
   if (e != hipSuccess) return e;
-  return io_bf16 ? launch_bwd_dims<bf16>(ba, s) : launch_bwd_f32(ba, s);
+  return io_bf16 ? launch_bwd_dims<bf16>(ba, s, ev) : launch_bwd_f32(ba, s, ev);
 }
 
 }  // namespace pdn

@@ -489,7 +489,9 @@ struct ScanCtx {
 
 // Each chunk's loads are a wave-uniform (scalar) base plus a 32-bit lane
 // byte offset, so the loop does almost no per-lane address arithmetic.
-template <typename T, int DK, int GATE>
+// OUT = false (state-saving scan of the backward): the query and P tiles are
+// not needed and not loaded.
+template <bool OUT, typename T, int DK, int GATE>
 __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdArgs& a, int i,
                                           const ScanCtx& x) {
   constexpr int KK = DK / 32, CT = DK / 64;
@@ -509,14 +511,14 @@ __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdAr
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
     f.K[kk] = ld8(at_bytes(kb, okq + kk * 32 * E));
-    f.Q[kk] = ld8(at_bytes(qb, okq + kk * 32 * E));
+    if (OUT) f.Q[kk] = ld8(at_bytes(qb, okq + kk * 32 * E));
   }
   const int ra = 16 * x.w + x.lr;
   const uint32_t otp = static_cast<uint32_t>(ra * C + 8 * x.lg) * E;
 #pragma unroll
   for (int k2 = 0; k2 < 2; ++k2) {
     f.Tm[k2] = ld8(at_bytes(tb, otp + k2 * 32 * E));
-    f.P[k2] = ld8(at_bytes(pb, otp + k2 * 32 * E));
+    if (OUT) f.P[k2] = ld8(at_bytes(pb, otp + k2 * 32 * E));
   }
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
@@ -624,7 +626,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
   constexpr int KK = DK / 32, CT = DK / 64;
   constexpr int LDH = DK + 8, LDE = C + 8;
   const int w = x.w, lr = x.lr, lg = x.lg;
-  if (i > 0) flush_output<T>(a, i - 1, C, sO, x);   // only full chunks precede this one
+  if (!SAVE && i > 0) flush_output<T>(a, i - 1, C, sO, x);   // only full chunks precede this one
   if (SAVE)  // chunk-start state S^T of this chunk, rows c, columns of the slab
     flush_slab_t<T>(static_cast<T*>(a.Hs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv, sH,
                     LDH, DK, x.tid);
@@ -639,7 +641,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
       for (int s = 0; s < 8; ++s) {
         const float e = fast_exp(f.gk[kk][s]);
         f.K[kk].set(s, f.K[kk].get(s) * e);
-        f.Q[kk].set(s, f.Q[kk].get(s) * e);
+        if (!SAVE) f.Q[kk].set(s, f.Q[kk].get(s) * e);
       }
   }
   // ---- (Lam K) S^T and (Lam Q) S^T;  X = V - (Lam K) S^T
@@ -660,12 +662,12 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       mma(accX[vt], f.K[kk], bH[vt][kk]);
-      mma(accO[vt], f.Q[kk], bH[vt][kk]);
+      if (!SAVE) mma(accO[vt], f.Q[kk], bH[vt][kk]);
     }
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
       accX[vt][ii] = to_f(vv[vt][ii]) - lam[ii] * accX[vt][ii];
-      accO[vt][ii] *= lam[ii];
+      if (!SAVE) accO[vt][ii] *= lam[ii];
     }
     st4<T>(sX + (16 * vt + lr) * LDE + 16 * w + 4 * lg, accX[vt][0], accX[vt][1], accX[vt][2],
            accX[vt][3]);
@@ -697,7 +699,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) fE[vt][k2] = ld8(sE + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg);
 #pragma unroll
-  for (int vt = 0; vt < 2; ++vt) {
+  for (int vt = 0; vt < 2 && !SAVE; ++vt) {
     // P is causal: for rows < 32 its second slab is zero
     mma(accO[vt], f.P[0], fE[vt][0]);
     mma(accO[vt], f.P[1], fE[vt][1]);
@@ -724,8 +726,8 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
   lds_barrier();
 }
 
-// SAVE: also write the chunk-start states and the X, E rows (backward
-// recompute); the output is skipped when a.o is NULL.
+// SAVE: the backward's recompute: write the chunk-start states and the X, E
+// rows instead of the output (queries and P are neither loaded nor used).
 template <typename T, int DK, int GATE, bool SAVE>
 __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   constexpr int CT = DK / 64;       // state row tiles per wave
@@ -782,22 +784,22 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   ScanFrags<T, DK, GATE> f0, f1, f2;
   const int last = a.NT - 1;
   const int NF = static_cast<int>(a.T / C);   // full chunks
-  scan_load(f0, a, 0, x);
-  scan_load(f1, a, min(1, last), x);
+  scan_load<!SAVE>(f0, a, 0, x);
+  scan_load<!SAVE>(f1, a, min(1, last), x);
   stage_values<T>(f0.v, sVt, x.tid);
   __syncthreads();
   int i = 0;
   for (; i + 2 < NF; i += 3) {
-    scan_load(f2, a, i + 2, x);
+    scan_load<!SAVE>(f2, a, i + 2, x);
     scan_step<true, SAVE>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
-    scan_load(f0, a, min(i + 3, last), x);
+    scan_load<!SAVE>(f0, a, min(i + 3, last), x);
     scan_step<true, SAVE>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
-    scan_load(f1, a, min(i + 4, last), x);
+    scan_load<!SAVE>(f1, a, min(i + 4, last), x);
     scan_step<true, SAVE>(f2, f0.v, st, a, i + 2, x, sH, sX, sE, sVt, sO);
   }
   // f0, f1 hold chunks i, i + 1 (clamped to the last chunk)
   if (NF - i == 2) {
-    scan_load(f2, a, min(i + 2, last), x);
+    scan_load<!SAVE>(f2, a, min(i + 2, last), x);
     scan_step<true, SAVE>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
     scan_step<true, SAVE>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
     i += 2;
@@ -809,7 +811,7 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   } else if (i < a.NT) {
     scan_step<false, SAVE>(f0, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
   }
-  flush_output<T>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
+  if (!SAVE) flush_output<T>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
   if (a.S_T) {
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
@@ -905,8 +907,10 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
 // the backward's forward recompute: k1 (squash), k2 in backward mode and k3
 // saving chunk states and X, E rows (no output); scalar gate or none
 template <typename T, int DK>
-static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s) {
+static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s, hipEvent_t const* ev) {
   hipError_t e;
+  auto mark = [&](int i) { return ev ? hipEventRecord(ev[i], s) : hipSuccess; };
+  if ((e = mark(0)) != hipSuccess) return e;
   if (a.precond == kSquash) {
     hipLaunchKernelGGL((k1_precond_summary<T, DK>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
                        0, s, a);
@@ -914,22 +918,24 @@ static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s) {
     hipLaunchKernelGGL((k1_precond_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
+  if ((e = mark(1)) != hipSuccess) return e;
   e = a.gate == kGateScalar ? launch_k2_prec<T, DK, kGateScalar, true>(a, s)
                             : launch_k2_prec<T, DK, kGateNone, true>(a, s);
   if (e != hipSuccess) return e;
+  if ((e = mark(2)) != hipSuccess) return e;
   const int64_t nslab = a.dv / BV;
   const unsigned grid = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
   if (a.gate == kGateScalar)
     hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, true>), dim3(grid), dim3(256), 0, s, a);
   else
     hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, true>), dim3(grid), dim3(256), 0, s, a);
-  return hipGetLastError();
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return mark(3);
 }
 
-hipError_t launch_forward_parts(const FwdArgs& a, int io_bf16, hipStream_t s, bool bwd) {
-  (void)bwd;
-  if (io_bf16) return a.dk == 64 ? launch_recompute<bf16, 64>(a, s) : launch_recompute<bf16, 128>(a, s);
-  return launch_recompute<float, 64>(a, s);
+hipError_t launch_forward_parts(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev) {
+  if (io_bf16) return a.dk == 64 ? launch_recompute<bf16, 64>(a, s, ev) : launch_recompute<bf16, 128>(a, s, ev);
+  return launch_recompute<float, 64>(a, s, ev);
 }
 
 hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev) {

@@ -249,9 +249,9 @@ pdn_status pdn_chunk_fwd_events(const pdn_problem* p, const pdn_inputs* in, pdn_
                         reinterpret_cast<hipEvent_t const*>(stage_events));
 }
 
-pdn_status pdn_chunk_bwd(const pdn_problem* p, const pdn_inputs* in, const void* dO,
-                         const float* dS_T, pdn_bwd_out* out, void* ws, size_t ws_bytes,
-                         void* hip_stream) {
+static pdn_status chunk_bwd_impl(const pdn_problem* p, const pdn_inputs* in, const void* dO,
+                                 const float* dS_T, pdn_bwd_out* out, void* ws, size_t ws_bytes,
+                                 void* hip_stream, hipEvent_t const* ev) {
   Sizes s;
   pdn_status st = check_problem(p, &s);
   if (st != PDN_OK) return st;
@@ -284,8 +284,13 @@ pdn_status pdn_chunk_bwd(const pdn_problem* p, const pdn_inputs* in, const void*
     return st;
   if (tok && (!ws || ws_bytes < L.total || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0))
     return PDN_ERR_WORKSPACE;
-  if (s.BH == 0) return PDN_OK;
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  if (s.BH == 0 || !tok) {
+    if (ev)  // nothing to time: the stage events still mark the empty stages
+      for (int k = 0; k < PDN_BWD_STAGE_EVENTS; ++k)
+        if (hipEventRecord(ev[k], stream) != hipSuccess) return PDN_ERR_HIP;
+  }
+  if (s.BH == 0) return PDN_OK;
   if (!tok) {
     // T == 0: the state passes through unchanged
     pdn::FwdArgs f{};
@@ -330,8 +335,25 @@ pdn_status pdn_chunk_bwd(const pdn_problem* p, const pdn_inputs* in, const void*
   a.pcL = reinterpret_cast<float*>(w + L.pcL);
   a.pcC = reinterpret_cast<float*>(w + L.pcC);
   a.pcMu = reinterpret_cast<float*>(w + L.pcMu);
-  const hipError_t he = pdn::launch_backward(a, p->io == PDN_BF16, stream);
+  const hipError_t he = pdn::launch_backward(a, p->io == PDN_BF16, stream, ev);
   return he == hipSuccess ? PDN_OK : PDN_ERR_HIP;
+}
+
+pdn_status pdn_chunk_bwd(const pdn_problem* p, const pdn_inputs* in, const void* dO,
+                         const float* dS_T, pdn_bwd_out* out, void* ws, size_t ws_bytes,
+                         void* hip_stream) {
+  return chunk_bwd_impl(p, in, dO, dS_T, out, ws, ws_bytes, hip_stream, nullptr);
+}
+
+pdn_status pdn_chunk_bwd_events(const pdn_problem* p, const pdn_inputs* in, const void* dO,
+                                const float* dS_T, pdn_bwd_out* out, void* ws, size_t ws_bytes,
+                                void* hip_stream, void* const* stage_events, int n_events) {
+  if (!stage_events) return PDN_ERR_NULL;
+  if (n_events != PDN_BWD_STAGE_EVENTS) return PDN_ERR_VALUE;
+  for (int i = 0; i < n_events; ++i)
+    if (!stage_events[i]) return PDN_ERR_NULL;
+  return chunk_bwd_impl(p, in, dO, dS_T, out, ws, ws_bytes, hip_stream,
+                        reinterpret_cast<hipEvent_t const*>(stage_events));
 }
 
 }  // extern "C"

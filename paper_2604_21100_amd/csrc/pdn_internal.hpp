@@ -108,7 +108,10 @@ struct BwdWsLayout {
 
 BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond);
 
-hipError_t launch_backward(const BwdArgs& a, int io_bf16, hipStream_t stream);
+// ev: NULL or 8 events recorded at the stage boundaries (see
+// pdn_chunk_bwd_events)
+hipError_t launch_backward(const BwdArgs& a, int io_bf16, hipStream_t stream,
+                           hipEvent_t const* ev = nullptr);
 
 // ev: NULL or 4 events recorded at the stage boundaries (see
 // pdn_chunk_fwd_events)

@@ -153,3 +153,55 @@ def test_backward_validates_first():
     st = pdn.pdn_chunk_bwd_raw(p, _inputs(), A * 30, None,
                                pdn.BwdOut(*([None] * 11)), A * 64, 0, 0)
     assert st == pdn.PDN_ERR_UNSUPPORTED
+
+
+def test_stage_event_arguments_validated():
+    """The event variants reject a missing or wrong-length event array
+    before anything else (no HIP call is reached)."""
+    vp = ctypes.c_void_p
+    p = _prob()
+    lib = pdn._lib
+    out = pdn.FwdOut(A * 20, A * 21, A * 22)
+    ev_f = (vp * pdn.FWD_STAGE_EVENTS)(*([A * 40] * pdn.FWD_STAGE_EVENTS))
+    assert lib.pdn_chunk_fwd_events(
+        ctypes.byref(p), ctypes.byref(_inputs()), ctypes.byref(out), A * 64, 0,
+        None, None, pdn.FWD_STAGE_EVENTS) == pdn.PDN_ERR_NULL
+    assert lib.pdn_chunk_fwd_events(
+        ctypes.byref(p), ctypes.byref(_inputs()), ctypes.byref(out), A * 64, 0,
+        None, ev_f, pdn.FWD_STAGE_EVENTS - 1) == pdn.PDN_ERR_VALUE
+    bo = pdn.BwdOut(*([None] * 11))
+    ev_b = (vp * pdn.BWD_STAGE_EVENTS)(*([A * 40] * pdn.BWD_STAGE_EVENTS))
+    assert lib.pdn_chunk_bwd_events(
+        ctypes.byref(p), ctypes.byref(_inputs()), A * 30, None,
+        ctypes.byref(bo), A * 64, 0, None, None,
+        pdn.BWD_STAGE_EVENTS) == pdn.PDN_ERR_NULL
+    assert lib.pdn_chunk_bwd_events(
+        ctypes.byref(p), ctypes.byref(_inputs()), A * 30, None,
+        ctypes.byref(bo), A * 64, 0, None, ev_b, 7) == pdn.PDN_ERR_VALUE
+    ev_b[3] = None
+    assert lib.pdn_chunk_bwd_events(
+        ctypes.byref(p), ctypes.byref(_inputs()), A * 30, None,
+        ctypes.byref(bo), A * 64, 0, None, ev_b,
+        pdn.BWD_STAGE_EVENTS) == pdn.PDN_ERR_NULL
+    # with valid event pointers, problem validation still comes first
+    ev_b[3] = A * 40
+    assert lib.pdn_chunk_bwd_events(
+        ctypes.byref(_prob(dk=96)), ctypes.byref(_inputs()), A * 30, None,
+        ctypes.byref(bo), A * 64, 0, None, ev_b,
+        pdn.BWD_STAGE_EVENTS) == pdn.PDN_ERR_UNSUPPORTED
+    assert len(pdn.BWD_STAGES) == pdn.BWD_STAGE_EVENTS - 1
+    assert len(pdn.FWD_STAGES) == pdn.FWD_STAGE_EVENTS - 1
+
+
+def test_one_hip_runtime_in_process():
+    """Importing the package first must not map a second HIP runtime when
+    torch is imported afterwards (two HSA runtimes in one process break
+    every GPU call)."""
+    import subprocess
+    import sys
+    code = ("import paper_2604_21100_amd as p, torch; "
+            "print(len(p.loaded_hip_runtimes()))")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT,
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.strip() == "1", r.stdout
