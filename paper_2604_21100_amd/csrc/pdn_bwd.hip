@@ -12,19 +12,23 @@
 //   At = strict_lower(Diag(beta) (Gam o K Kt^T))
 // and the adjoint, given dO and dS'^T (the state adjoint from the right):
 //   dE  = (Gam o Q Kt^T)_causal^T dO_s + Diag(w) Kt dS'^T      dO_s = scale dO
-//   dX  = T^T dE                      dV = dX
+//   Z   = M^T dE                      dX = T^T dE = Diag(beta) Z,  dV = dX
 //   dS^T = lam_C dS'^T + Q^T Diag(lam) dO_s - K^T Diag(lam) dX
 //   dQ  = Diag(lam) dO_s S + dSqk Kt  dK = -Diag(lam) dX S + dSkk Kt
 //   dKt = dSqk^T Q + Diag(w) E dS' + dSkk^T K
-//   dSqk = Gam o (dO_s E^T)_causal,   dM = dE X^T Diag(beta),
-//   dL = -M^T dM M^T,  dAt = strict_lower(dL),  dSkk = Gam o Diag(beta) dAt
-//   dbeta_t = (M^T dE X^T)_tt + sum_{s<t} dAt_ts (Gam o K Kt^T)_ts
+//   dSqk = Gam o (dO_s E^T)_causal
+// The inverse's adjoint collapses: with dM = dE X^T Diag(beta) the gradient
+// of L = (I + At)^{-1} is dL = -M^T dM M^T = -(M^T dE)(M Diag(beta) X)^T =
+// -Z E^T, one C x C product of stored rows, so
+//   dAt = strict_lower(-Z E^T),  dSkk = Gam o Diag(beta) dAt
+//   dbeta_t = sum_v Z_tv X_tv + sum_{s<t} dAt_ts (Gam o K Kt^T)_ts
 // plus the gate terms (gradients of lam, w, lam_C and Gam, reverse-summed
 // over the chunk) and the preconditioner's reverse scan.
 //
-//   r1_state_adjoint   sequential over chunks (reverse): dS^T carry, dE, dX
-//   p1_chunk_cc        per chunk: the C x C adjoint algebra (dSqk, dSkk,
-//                      dbeta, gate terms of Gam)
+//   r1_state_adjoint   sequential over chunks (reverse): dS^T carry, dE, Z,
+//                      dX (= dv)
+//   p1_chunk_cc        per chunk: the C x C adjoints (dSqk, dSkk, dbeta,
+//                      gate terms of Gam)
 //   p2_chunk_grads     per chunk: dq, dk, dkt, dg
 //   pc_*               preconditioner: reverse scan over tokens of the
 //                      diagonal Gram recurrence (dk, dbetaP, dgP, dlogAScale,
@@ -67,9 +71,10 @@ __device__ __forceinline__ void slab_to_rows(T* dst, int64_t ld, const T* src, i
 template <typename T, int DK>
 struct RevFrags {
   static constexpr int KK = DK / 32, CT = DK / 64;
-  Frag8<T> Pt[2], Kw[KK], Tt[2], Ql[CT][2], Kn[CT][2];
+  Frag8<T> Pt[2], Kw[KK], Mt[2], Ql[CT][2], Kn[CT][2];
   float4 dO[Slab<T>::kPer];
   float gC;
+  float beta[4];   // beta of rows 16w + 4lg + ii (raw: past the end masked at use)
 };
 
 struct RevCtx {
@@ -89,7 +94,7 @@ __device__ __forceinline__ void rev_load(RevFrags<T, DK>& f, const BwdArgs& ba, 
   const int64_t cc = (x.bh * a.NT + i) * (int64_t)(C * C);
   const int64_t ck = (x.bh * a.NT + i) * (int64_t)(DK * C);
   const T* pt = static_cast<const T*>(a.PtT) + cc;
-  const T* tt = static_cast<const T*>(a.TtT) + cc;
+  const T* mt = static_cast<const T*>(a.MtT) + cc;
   const T* kw = static_cast<const T*>(a.Kw) + (x.bh * a.Tpad + t0) * DK;
   const T* ql = static_cast<const T*>(a.QlT) + ck;
   const T* kn = static_cast<const T*>(a.KnT) + ck;
@@ -98,7 +103,7 @@ __device__ __forceinline__ void rev_load(RevFrags<T, DK>& f, const BwdArgs& ba, 
 #pragma unroll
   for (int k2 = 0; k2 < 2; ++k2) {
     f.Pt[k2] = ld8(at_bytes(pt, ocr + k2 * 32 * E));
-    f.Tt[k2] = ld8(at_bytes(tt, ocr + k2 * 32 * E));
+    f.Mt[k2] = ld8(at_bytes(mt, ocr + k2 * 32 * E));
   }
   const uint32_t okw = static_cast<uint32_t>(ra * DK + 8 * x.lg) * E;
 #pragma unroll
@@ -121,6 +126,9 @@ __device__ __forceinline__ void rev_load(RevFrags<T, DK>& f, const BwdArgs& ba, 
     f.dO[j] = *reinterpret_cast<const float4*>(at_bytes(dob, off));
   }
   f.gC = GATE == kGateScalar ? a.G[x.bh * a.Tpad + t0 + C - 1] : 0.f;
+  const float* bb = a.beta + (x.b * a.T + t0) * a.H + x.h;
+#pragma unroll
+  for (int ii = 0; ii < 4; ++ii) f.beta[ii] = bb[min(16 * x.w + 4 * x.lg + ii, last) * a.H];
 }
 
 // scale * dO of one chunk -> sDO[v][r]; rows past the sequence end are zero
@@ -143,7 +151,8 @@ __device__ __forceinline__ void rev_stage_dO(const float4 (&v)[Slab<T>::kPer], T
 template <bool FULL, typename T, int DK, int GATE>
 __device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, const RevFrags<T, DK>& fnext, bool stage_next,
                                          floatx4 (&st)[DK / 64][2], const BwdArgs& ba, int i,
-                                         const RevCtx& x, T* sH, T* sDOc, T* sDOn, T* sE, T* sX) {
+                                         const RevCtx& x, T* sH, T* sDOc, T* sDOn, T* sE, T* sX,
+                                         T* sZ) {
   constexpr int KK = DK / 32, CT = DK / 64;
   constexpr int LDH = DK + 8, LDE = C + 8;
   const FwdArgs& a = ba.f;
@@ -174,22 +183,23 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, const RevFrags<T, D
     st4<T>(sE + (16 * vt + lr) * LDE + 16 * w + 4 * lg, acc[0], acc[1], acc[2], acc[3]);
   }
   lds_barrier_b();
-  // ---- dX = T^T dE
+  // ---- Z = M^T dE;  dX = Diag(beta) Z   (rows t = 16w + 4lg + ii)
+  float bt[4];
+#pragma unroll
+  for (int ii = 0; ii < 4; ++ii) bt[ii] = (FULL || 16 * w + 4 * lg + ii < n) ? f.beta[ii] : 0.f;
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt) {
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Tt[k2], ld8(sE + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg));
-    st4<T>(sX + (16 * vt + lr) * LDE + 16 * w + 4 * lg, acc[0], acc[1], acc[2], acc[3]);
-  }
-  {
-    const int64_t r0 = (x.bh * a.Tpad + t0) * a.dv + x.v0;
-    slab_to_rows<T>(static_cast<T*>(ba.dEr) + r0, a.dv, sE, LDE, C, C, x.tid);
+    for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Mt[k2], ld8(sE + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg));
+    st4<T>(sZ + (16 * vt + lr) * LDE + 16 * w + 4 * lg, acc[0], acc[1], acc[2], acc[3]);
+    st4<T>(sX + (16 * vt + lr) * LDE + 16 * w + 4 * lg, bt[0] * acc[0], bt[1] * acc[1], bt[2] * acc[2],
+           bt[3] * acc[3]);
   }
   lds_barrier_b();
   {
     const int64_t r0 = (x.bh * a.Tpad + t0) * a.dv + x.v0;
-    slab_to_rows<T>(static_cast<T*>(ba.dXr) + r0, a.dv, sX, LDE, C, C, x.tid);
+    slab_to_rows<T>(static_cast<T*>(ba.Zr) + r0, a.dv, sZ, LDE, C, C, x.tid);
     const int64_t HV = a.H * (int64_t)a.dv;
     slab_to_rows<T>(static_cast<T*>(ba.dv) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0, HV, sX, LDE, C,
                     n, x.tid);
@@ -230,6 +240,7 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
   __shared__ __attribute__((aligned(16))) T sDO[2][BVB * LDE];
   __shared__ __attribute__((aligned(16))) T sE[BVB * LDE];
   __shared__ __attribute__((aligned(16))) T sX[BVB * LDE];
+  __shared__ __attribute__((aligned(16))) T sZ[BVB * LDE];
   const FwdArgs& a = ba.f;
   const int nslab = a.dv / BVB;
   const int64_t bid = blockIdx.x;
@@ -273,17 +284,17 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
   rev_load<T, DK, GATE>(fB, ba, max(NT - 2, 0), x);
   rev_stage_dO<T>(fA.dO, sDO[0], static_cast<int>(a.T - static_cast<int64_t>(NT - 1) * C), a.scale, x.tid);
   __syncthreads();
-  rev_step<false, T, DK, GATE>(fA, fB, NT > 1, st, ba, NT - 1, x, sH, sDO[0], sDO[1], sE, sX);
+  rev_step<false, T, DK, GATE>(fA, fB, NT > 1, st, ba, NT - 1, x, sH, sDO[0], sDO[1], sE, sX, sZ);
   int i = NT - 2, buf = 1;
   for (; i >= 1; i -= 2) {
     rev_load<T, DK, GATE>(fA, ba, i - 1, x);
-    rev_step<true, T, DK, GATE>(fB, fA, true, st, ba, i, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX);
+    rev_step<true, T, DK, GATE>(fB, fA, true, st, ba, i, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
     buf ^= 1;
     rev_load<T, DK, GATE>(fB, ba, max(i - 2, 0), x);
-    rev_step<true, T, DK, GATE>(fA, fB, true, st, ba, i - 1, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX);
+    rev_step<true, T, DK, GATE>(fA, fB, true, st, ba, i - 1, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
     buf ^= 1;
   }
-  if (i == 0) rev_step<true, T, DK, GATE>(fB, fA, false, st, ba, 0, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX);
+  if (i == 0) rev_step<true, T, DK, GATE>(fB, fA, false, st, ba, 0, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
   if (ba.dS0) {
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
@@ -329,29 +340,33 @@ __device__ __forceinline__ void load_rows_t(T* dst, const T* src, int64_t lds, i
   }
 }
 
-template <typename T, int DK, int DV>
-struct P1Smem {
-  static constexpr int LDR = (DK > DV ? DK : DV) + 8;
-  static constexpr size_t kRows = sizeof(T) * 2 * C * LDR;
-  static constexpr int LDF = C + 4;
-  static constexpr size_t kF = sizeof(float) * 4 * C * LDF;
-  static constexpr size_t kTotal = kRows + kF + sizeof(float) * 4 * C;
-};
+// Rows [C][DD] of a workspace tensor -> LDS rows [C][DD + 8] (16-byte copies)
+template <typename T, int DD>
+__device__ __forceinline__ void stage_rows(T* dst, const T* src, int tid) {
+  constexpr int VEC = 16 / sizeof(T), VPR = DD / VEC, LD = DD + 8;
+  for (int idx = tid; idx < C * VPR; idx += 256) {
+    const int r = idx / VPR, cv = idx % VPR;
+    *reinterpret_cast<float4*>(dst + r * LD + cv * VEC) = *reinterpret_cast<const float4*>(src + r * DD + cv * VEC);
+  }
+}
 
+// Per chunk: four C x C products of stored rows,
+//   dP = dO E^T,  dLn = Z E^T (dL = -dLn),  Sqk = Q Kt^T,  Skk = K Kt^T,
+// and their elementwise adjoint algebra.  Wave w owns rows 16w .. 16w + 15
+// (output tiles j <= w: every product is causal or strictly causal), so its
+// A operands (dO, Z, Q, K and the X rows of the beta dot product) are
+// private and load straight from memory into fragments; the shared B
+// operands (E and Kt rows) are staged once in LDS.  Rows past the sequence
+// end re-read the last row; their dP rows are masked, every other product
+// of them meets a zero factor (Z and beta vanish there).
 template <typename T, int DK, int DV, int GATE>
 __global__ __launch_bounds__(256) void p1_chunk_cc(BwdArgs ba) {
-  using SM = P1Smem<T, DK, DV>;
-  constexpr int LDR = SM::LDR, LDF = SM::LDF;
-  __shared__ __attribute__((aligned(16))) char smem[SM::kTotal];
-  T* R0 = reinterpret_cast<T*>(smem);
-  T* R1 = R0 + C * LDR;
-  float* sM = reinterpret_cast<float*>(smem + SM::kRows);
-  float* sMt = sM + C * LDF;
-  float* sW1 = sMt + C * LDF;
-  float* sW2 = sW1 + C * LDF;
-  float* sG = sW2 + C * LDF;
-  float* sBeta = sG + C;
-  float* sDbT = sBeta + C;
+  constexpr int LDE = DV + 8, LDK = DK + 8;
+  constexpr int KV = DV / 32, KD = DK / 32;
+  constexpr uint32_t E = sizeof(T);
+  __shared__ __attribute__((aligned(16))) T sE[C * LDE];
+  __shared__ __attribute__((aligned(16))) T sKt[C * LDK];
+  __shared__ float sG[C], sBeta[C], sDb[2][C], sRs[C], sCs[4][C];
 
   const FwdArgs& a = ba.f;
   const int64_t blk = blockIdx.x;
@@ -363,127 +378,127 @@ __global__ __launch_bounds__(256) void p1_chunk_cc(BwdArgs ba) {
   const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
   const int64_t HV = a.H * (int64_t)DV, HD = a.H * (int64_t)DK;
   const int64_t cc = (bh * a.NT + i) * (int64_t)(C * C);
+  const int64_t rv = (bh * a.Tpad + t0) * DV, rk = (bh * a.Tpad + t0) * DK;
 
-  // ---- dO_s, E rows; M, M^T; gate prefix and beta
-  load_rows<T, DV>(R0, LDR, static_cast<const T*>(ba.dO) + (b * a.T + t0) * HV + h * DV, HV, n, tid,
-                   a.scale);
-  const int64_t rv = (bh * a.Tpad + t0) * DV;
-  load_rows<T, DV>(R1, LDR, static_cast<const T*>(a.Er) + rv, DV, C, tid);
-  for (int idx = tid; idx < C * C; idx += 256) {
-    const int r = idx / C, t = idx % C;
-    const float m = a.Mi[cc + idx];
-    sM[r * LDF + t] = m;
-    sMt[t * LDF + r] = m;
+  // ---- A operands of row 16w + lr (wave-private), issued first
+  const int ra = 16 * w + lr;
+  const uint32_t rc = static_cast<uint32_t>(min(ra, n - 1));
+  Frag8<T> fO[KV], fZ[KV], fX[KV], fQ[KD], fK[KD];
+  {
+    const T* dob = static_cast<const T*>(ba.dO) + (b * a.T + t0) * HV + h * DV;
+    const T* zb = static_cast<const T*>(ba.Zr) + rv;
+    const T* xb = static_cast<const T*>(a.Xr) + rv;
+    const T* qb = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
+    const T* kb = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
+#pragma unroll
+    for (int kk = 0; kk < KV; ++kk) {
+      fO[kk] = ld8(at_bytes(dob, (rc * static_cast<uint32_t>(HV) + 32 * kk + 8 * lg) * E));
+      fZ[kk] = ld8(at_bytes(zb, (static_cast<uint32_t>(ra * DV) + 32 * kk + 8 * lg) * E));
+      fX[kk] = ld8(at_bytes(xb, (static_cast<uint32_t>(ra * DV) + 32 * kk + 8 * lg) * E));
+    }
+#pragma unroll
+    for (int kk = 0; kk < KD; ++kk) {
+      fQ[kk] = ld8(at_bytes(qb, (rc * static_cast<uint32_t>(HD) + 32 * kk + 8 * lg) * E));
+      fK[kk] = ld8(at_bytes(kb, (rc * static_cast<uint32_t>(HD) + 32 * kk + 8 * lg) * E));
+    }
   }
+  // ---- shared B operands and per-row scalars
+  stage_rows<T, DV>(sE, static_cast<const T*>(a.Er) + rv, tid);
+  stage_rows<T, DK>(sKt, static_cast<const T*>(a.Ktr) + rk, tid);
   if (tid < C) {
     sG[tid] = GATE == kGateScalar ? a.G[bh * a.Tpad + t0 + tid] : 0.f;
     sBeta[tid] = tid < n ? a.beta[(b * a.T + t0 + tid) * a.H + h] : 0.f;
   }
   __syncthreads();
 
-  // ---- dP = dO_s E^T (causal), row block w
-  floatx4 dP[4], dT[4], Sqk[4], Skk[4];
+  // ---- dbeta through T: sum_v Z_rv X_rv for row ra
+  {
+    float dz = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KV; ++kk)
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) dz += fZ[kk].get(s2) * fX[kk].get(s2);
+    dz += __shfl_xor(dz, 16, 64);
+    dz += __shfl_xor(dz, 32, 64);
+    if (lg == 0) sDb[0][ra] = dz;
+  }
+  // ---- the four products, tiles j <= w
+  floatx4 dP[4], dL[4], Sqk[4], Skk[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     dP[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    dT[j] = dP[j];
+    dL[j] = dP[j];
     Sqk[j] = dP[j];
     Skk[j] = dP[j];
-    if (j <= w) mma_tile<DV>(dP[j], R0 + (16 * w) * LDR, LDR, R1 + (16 * j) * LDR, LDR, lr, lg);
+    if (j <= w) {
+#pragma unroll
+      for (int kk = 0; kk < KV; ++kk) {
+        const Frag8<T> fe = ld8(sE + (16 * j + lr) * LDE + 32 * kk + 8 * lg);
+        mma(dP[j], fO[kk], fe);
+        mma(dL[j], fZ[kk], fe);
+      }
+#pragma unroll
+      for (int kk = 0; kk < KD; ++kk) {
+        const Frag8<T> fk = ld8(sKt + (16 * j + lr) * LDK + 32 * kk + 8 * lg);
+        mma(Sqk[j], fQ[kk], fk);
+        mma(Skk[j], fK[kk], fk);
+      }
+    }
   }
-  __syncthreads();
-  // ---- dT = dE X^T
-  load_rows<T, DV>(R0, LDR, static_cast<const T*>(ba.dEr) + rv, DV, C, tid);
-  load_rows<T, DV>(R1, LDR, static_cast<const T*>(a.Xr) + rv, DV, C, tid);
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < 4; ++j) mma_tile<DV>(dT[j], R0 + (16 * w) * LDR, LDR, R1 + (16 * j) * LDR, LDR, lr, lg);
-  __syncthreads();
-  // ---- S_qk = Q Kt^T, then S_kk = K Kt^T (row block w, causal part)
-  load_rows<T, DK>(R0, LDR, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK, HD, n, tid);
-  load_rows<T, DK>(R1, LDR, static_cast<const T*>(a.Ktr) + (bh * a.Tpad + t0) * DK, DK, C, tid);
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-    if (j <= w) mma_tile<DK>(Sqk[j], R0 + (16 * w) * LDR, LDR, R1 + (16 * j) * LDR, LDR, lr, lg);
-  __syncthreads();
-  load_rows<T, DK>(R0, LDR, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK, HD, n, tid);
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-    if (j <= w) mma_tile<DK>(Skk[j], R0 + (16 * w) * LDR, LDR, R1 + (16 * j) * LDR, LDR, lr, lg);
-  // ---- dSqk; dM = dT Diag(beta) -> sW1; M o dT -> sW2 (column sums: dbeta via T)
+  // ---- elementwise: dSqk, dSkk (and transposes), row / column sums
   T* dSqk = static_cast<T*>(ba.dSqk) + cc;
   T* dSqkT = static_cast<T*>(ba.dSqkT) + cc;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    floatx4 ds;
-#pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-      const int r = 16 * w + 4 * lg + ii, t = 16 * j + lr;
-      const float gm = (r >= t) ? (GATE == kGateScalar ? fast_exp(sG[r] - sG[t]) : 1.f) : 0.f;
-      ds[ii] = gm * dP[j][ii];
-      sW1[r * LDF + t] = dT[j][ii] * sBeta[t];
-      sW2[r * LDF + t] = dT[j][ii] * sM[r * LDF + t];
-      // keep the masked C x C products for the Gam gradient
-      dP[j][ii] = ds[ii] * Sqk[j][ii];   // (Gam o dP) o S_qk, causal
-    }
-    st_tile<T>(dSqk + (16 * w) * C + 16 * j, C, ds, lr, lg);
-    st_tile_t<T>(dSqkT + (16 * j) * C + 16 * w, C, ds, lr, lg);
-  }
-  __syncthreads();
-  if (tid < C) {
-    float sdb = 0.f;
-    for (int r = 0; r < C; ++r) sdb += sW2[r * LDF + tid];
-    sDbT[tid] = sdb;
-  }
-  __syncthreads();
-  // ---- Y = dM M^T -> sW2 as Y^T
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    floatx4 y = {0.f, 0.f, 0.f, 0.f};
-    mma_tile<C>(y, sW1 + (16 * w) * LDF, LDF, sM + (16 * j) * LDF, LDF, lr, lg);
-    st_tile_t<float>(sW2 + (16 * j) * LDF + 16 * w, LDF, y, lr, lg);
-  }
-  __syncthreads();
-  // ---- dL = -M^T Y;  dAt = strict_lower(dL);  dSkk = Gam o Diag(beta) dAt
   T* dSkk = static_cast<T*>(ba.dSkk) + cc;
   T* dSkkT = static_cast<T*>(ba.dSkkT) + cc;
+  float dbA[4] = {0.f, 0.f, 0.f, 0.f}, rs[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    floatx4 dl = {0.f, 0.f, 0.f, 0.f};
-    mma_tile<C>(dl, sMt + (16 * w) * LDF, LDF, sW2 + (16 * j) * LDF, LDF, lr, lg);
-    floatx4 ds;
+    floatx4 dq, dk;
+    float cs = 0.f;
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
       const int r = 16 * w + 4 * lg + ii, t = 16 * j + lr;
-      const float gm = (r > t) ? (GATE == kGateScalar ? fast_exp(sG[r] - sG[t]) : 1.f) : 0.f;
-      const float dA = (r > t) ? -dl[ii] : 0.f;
-      ds[ii] = gm * sBeta[r] * dA;
-      // row sums: dbeta via At (dAt o Gam o S_kk) and the Gam gradient
-      sW1[r * LDF + t] = dA * gm * Skk[j][ii];
-      Skk[j][ii] = ds[ii] * Skk[j][ii] + dP[j][ii];   // (dSkk o S_kk) + (dSqk o S_qk)
+      const bool ca = r >= t && r < n, sl = r > t;
+      const float gm = GATE == kGateScalar ? fast_exp(r >= t ? sG[r] - sG[t] : 0.f) : 1.f;
+      dq[ii] = ca ? gm * a.scale * dP[j][ii] : 0.f;
+      const float dA = sl ? -dL[j][ii] : 0.f;       // strict_lower(dL)
+      dk[ii] = gm * sBeta[r] * dA;
+      dbA[ii] += dA * gm * Skk[j][ii];              // dbeta through At
+      // (dSkk o S_kk) + (dSqk o S_qk): its row minus column sums give dG
+      const float R = dk[ii] * Skk[j][ii] + dq[ii] * Sqk[j][ii];
+      rs[ii] += R;
+      cs += R;
     }
-    st_tile<T>(dSkk + (16 * w) * C + 16 * j, C, ds, lr, lg);
-    st_tile_t<T>(dSkkT + (16 * j) * C + 16 * w, C, ds, lr, lg);
+    st_tile<T>(dSqk + (16 * w) * C + 16 * j, C, dq, lr, lg);
+    st_tile_t<T>(dSqkT + (16 * j) * C + 16 * w, C, dq, lr, lg);
+    st_tile<T>(dSkk + (16 * w) * C + 16 * j, C, dk, lr, lg);
+    st_tile_t<T>(dSkkT + (16 * j) * C + 16 * w, C, dk, lr, lg);
+    // column t = 16j + lr: sum over this wave's 16 rows
+    cs += __shfl_xor(cs, 16, 64);
+    cs += __shfl_xor(cs, 32, 64);
+    if (lg == 0) sCs[w][16 * j + lr] = cs;
   }
-  __syncthreads();   // sW1 complete; sMt free
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+  for (int ii = 0; ii < 4; ++ii)
 #pragma unroll
-    for (int ii = 0; ii < 4; ++ii) sMt[(16 * w + 4 * lg + ii) * LDF + 16 * j + lr] = Skk[j][ii];
+    for (int off = 1; off < 16; off <<= 1) {
+      dbA[ii] += __shfl_xor(dbA[ii], off, 64);
+      rs[ii] += __shfl_xor(rs[ii], off, 64);
+    }
+  if (lr == 0) {
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      sDb[1][16 * w + 4 * lg + ii] = dbA[ii];
+      sRs[16 * w + 4 * lg + ii] = rs[ii];
+    }
+  }
   __syncthreads();
   if (tid < C) {
     const int r = tid;
-    float dbA = 0.f, rs = 0.f, cs = 0.f;
-    for (int t = 0; t < C; ++t) {
-      dbA += sW1[r * LDF + t];
-      rs += sMt[r * LDF + t];
-      cs += sMt[t * LDF + r];
-    }
     // Gam_rt = exp(G_r - G_t): d/dG_r of sum R_rt = row sum, d/dG_t = -column sum
-    ba.dGp[bh * a.Tpad + t0 + r] = GATE == kGateScalar ? rs - cs : 0.f;
-    if (r < n) ba.dbeta[(b * a.T + t0 + r) * a.H + h] = sDbT[r] + dbA;
+    const float cs = sCs[0][r] + sCs[1][r] + sCs[2][r] + sCs[3][r];
+    ba.dGp[bh * a.Tpad + t0 + r] = GATE == kGateScalar ? sRs[r] - cs : 0.f;
+    if (r < n) ba.dbeta[(b * a.T + t0 + r) * a.H + h] = sDb[0][r] + sDb[1][r];
   }
 }
 
@@ -540,7 +555,7 @@ __global__ __launch_bounds__(256) void p2_chunk_grads(BwdArgs ba) {
   load_rows<T, DV>(sDO, LDR, static_cast<const T*>(ba.dO) + (b * a.T + t0) * HV + h * DV, HV, n, tid,
                    a.scale);
   const int64_t rv = (bh * a.Tpad + t0) * DV;
-  load_rows<T, DV>(sDX, LDR, static_cast<const T*>(ba.dXr) + rv, DV, C, tid);
+  load_rows<T, DV>(sDX, LDR, static_cast<const T*>(ba.dv) + (b * a.T + t0) * HV + h * DV, HV, n, tid);
   load_rows<T, DV>(sE, LDR, static_cast<const T*>(a.Er) + rv, DV, C, tid);
   {
     constexpr int VEC = 16 / sizeof(T), VPR = DV / VEC;
@@ -676,104 +691,220 @@ __global__ __launch_bounds__(256) void p2_chunk_grads(BwdArgs ba) {
 // chains the chunks (adjoint entering each chunk from the right), and
 // pc_chunk<true> recomputes with the carry and writes dk, dbetaP, dgP and the
 // partial d mu.
+// Sum of 16 per-row values over the 64 lanes of a wave, scattered: lane l
+// ends with the total of row pc_row(l) (lanes differing only in bits 0-1
+// hold the same total).  Halving exchanges (8+4+2+1 values) then two plain
+// xor steps: 17 shuffles instead of 16 x 6.
+__device__ __forceinline__ int pc_row(int l) {
+  return ((l >> 5) & 1) * 8 + ((l >> 4) & 1) * 4 + ((l >> 3) & 1) * 2 + ((l >> 2) & 1);
+}
+
+__device__ __forceinline__ float pc_reduce16(float (&v)[16], int l) {
+#pragma unroll
+  for (int half = 8, m = 32; half >= 1; half >>= 1, m >>= 1) {
+    const bool hi = (l & m) != 0;
+#pragma unroll
+    for (int i = 0; i < half; ++i) {
+      const float keep = hi ? v[half + i] : v[i];
+      const float give = hi ? v[i] : v[half + i];
+      v[i] = keep + __shfl_xor(give, m, 64);
+    }
+  }
+  float x = v[0];
+  x += __shfl_xor(x, 2, 64);
+  x += __shfl_xor(x, 1, 64);
+  return x;
+}
+
+// One block per (b, h, chunk).  The chunk's 64 tokens are cut into four
+// segments of G = 16; wave w takes key channels 64 (w % NCH) .. + 63 of
+// segment w / NCH, one channel per lane.  Both recurrences are first-order
+// linear with a per-token factor aP_r shared by all channels, so each
+// segment scans from zero and a short composition through LDS supplies the
+// exact value entering it:
+//   forward  A_r = Ahat_r + (prod_{s0 <= j <= r} aP_j) A_in
+//   reverse  D_r = Dhat_r + (prod_{r < j <= s0 + G - 1} aP_j) kappa
+// (s0 the segment's first token, A_in the preconditioner state before it,
+// kappa the adjoint entering it from the right, already times aP of the
+// next token).  The products are exp of differences of the in-chunk prefix
+// of gP.  Loop bodies are branch-free and, for full chunks (FULL), store
+// without row guards, so each segment's 16 rows form one basic block.
+constexpr int PCG = 16;   // tokens per segment
+constexpr int PCS = C / PCG;
+
+template <bool FULL, typename T, int DK, bool FINAL>
+__device__ __forceinline__ void pc_body(const BwdArgs& ba, int64_t bh, int i, int n, const float* sEgp,
+                                        const float* sBp, const float* sGp, float (*sEnd)[DK],
+                                        float (*sRow)[DK / 64][C], float* sMu) {
+  constexpr int NCH = DK / 64;
+  const FwdArgs& a = ba.f;
+  const int64_t b = bh / a.H, h = bh % a.H;
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+  const int ch = w % NCH, sg = w / NCH;
+  const int c = 64 * ch + l;
+  const int s0 = PCG * sg;
+  const int64_t t0 = static_cast<int64_t>(i) * C;
+  const int64_t kst = a.H * static_cast<int64_t>(DK);
+  const T* kcol = static_cast<const T*>(a.k) + ((b * a.T + t0) * a.H + h) * DK + c;
+  const float* dkt = ba.dKt + (bh * a.Tpad + t0 + s0) * DK + c;
+  const float* dkm = ba.dKm + (bh * a.Tpad + t0 + s0) * DK + c;
+  // loads: keys (rows past the end re-read the last row and are zeroed
+  // below), write-key and read-key gradients (workspace rows cover the
+  // padded chunk)
+  float kv[PCG], gk[PCG], km[PCG];
+#pragma unroll
+  for (int j = 0; j < PCG; ++j) kv[j] = to_f(kcol[(FULL ? s0 + j : min(s0 + j, n - 1)) * kst]);
+#pragma unroll
+  for (int j = 0; j < PCG; ++j) gk[j] = dkt[j * DK];
+  if (FINAL) {
+#pragma unroll
+    for (int j = 0; j < PCG; ++j) km[j] = dkm[j * DK];
+  }
+  const float A_start = a.Abound[(bh * (a.NT + 1) + i) * DK + c];
+  const float kap_chunk = FINAL ? ba.pcC[(bh * (a.NT + 1) + i + 1) * DK + c] : 0.f;
+  if (!FULL) {
+#pragma unroll
+    for (int j = 0; j < PCG; ++j) kv[j] = s0 + j < n ? kv[j] : 0.f;
+  }
+  // prefix of gP before this segment (sGp[r] = sum_{j <= r} gP_j)
+  const float gbase = sg > 0 ? sGp[s0 - 1] : 0.f;
+  // ---- forward: local scan from zero, then the exact state entering
+  float A[PCG];
+  {
+    float x = 0.f;
+#pragma unroll
+    for (int j = 0; j < PCG; ++j) {
+      x = sEgp[s0 + j] * x + sBp[s0 + j] * kv[j] * kv[j];
+      A[j] = x;
+    }
+  }
+  sEnd[sg][c] = A[PCG - 1];
+  __syncthreads();
+  float A_in = A_start;
+  for (int q = 0; q < sg; ++q) {
+    const float pe = fast_exp(sGp[PCG * q + PCG - 1] - (q > 0 ? sGp[PCG * q - 1] : 0.f));
+    A_in = sEnd[q][c] + pe * A_in;
+  }
+#pragma unroll
+  for (int j = 0; j < PCG; ++j) A[j] += fast_exp(sGp[s0 + j] - gbase) * A_in;
+  // ---- reverse: local adjoint from zero; the gain terms need no D
+  const float mu = fast_exp(a.log_a_scale[h]);
+  const float lnx = a.lnx;
+  float Dh[PCG], base[PCG];
+  float muPart = 0.f;
+  {
+    float D = 0.f, aNext = 1.f;
+#pragma unroll
+    for (int j = PCG - 1; j >= 0; --j) {
+      const float Ar = A[j];
+      // B(A) = exp(-lnx s(rho)), rho = log A - mu, s = rho / (1 + |rho|):
+      // dB/dA = -lnx B / ((1 + |rho|)^2 A); zero where A <= 0 (B = x there)
+      const bool pos = Ar > 0.f;
+      const float rr = fast_log(fmaxf(Ar, 1e-30f)) - mu;
+      const float qd = fast_rcp(1.f + fabsf(rr));
+      const float Bv = fast_exp(-lnx * (pos ? rr * qd : -1.f));
+      const float dr = pos ? -lnx * Bv * gk[j] * kv[j] * qd * qd : 0.f;
+      D = dr * fast_rcp(fmaxf(Ar, 1e-30f)) + aNext * D;
+      aNext = sEgp[s0 + j];
+      Dh[j] = D;
+      if (FINAL) {
+        muPart -= dr;
+        base[j] = km[j] + Bv * gk[j];
+      }
+    }
+    __syncthreads();   // every thread is done with sEnd (forward)
+    sEnd[sg][c] = aNext * D;   // aP_{s0} Dhat_{s0}: what this segment sends left
+  }
+  __syncthreads();
+  // adjoint entering this segment from the right
+  float kap = kap_chunk;
+  for (int q = PCS - 1; q > sg; --q) {
+    const float pe = fast_exp(sGp[PCG * q + PCG - 1] - sGp[PCG * q - 1]);
+    kap = sEnd[q][c] + pe * kap;
+  }
+  const float gend = sGp[s0 + PCG - 1];
+  if (!FINAL) {
+    if (sg == 0) {
+      // the adjoint this chunk sends to the left, with zero carry: aP_0 D_0
+      ba.pcL[(bh * a.NT + i) * DK + c] = sEnd[0][c] + fast_exp(gend) * kap;
+    }
+    return;
+  }
+  // ---- outputs: dk = dKm + B dkt + 2 bP k D;  row sums D k^2, D A_{r-1}
+  T* dkout = static_cast<T*>(ba.dk) + ((b * a.T + t0 + s0) * a.H + h) * DK + c;
+  float s1[PCG], s2[PCG];
+#pragma unroll
+  for (int j = 0; j < PCG; ++j) {
+    const float D = Dh[j] + fast_exp(gend - sGp[s0 + j]) * kap;
+    const float dkk = base[j] + 2.f * sBp[s0 + j] * kv[j] * D;
+    if (FULL || s0 + j < n) dkout[j * kst] = from_f<T>(dkk);
+    s1[j] = D * kv[j] * kv[j];
+    s2[j] = D * (j > 0 ? A[j - 1] : A_in);
+  }
+  const float t1 = pc_reduce16(s1, l);
+  const float t2 = pc_reduce16(s2, l);
+  if ((l & 3) == 0) {
+    sRow[0][ch][s0 + pc_row(l)] = t1;
+    sRow[1][ch][s0 + pc_row(l)] = t2;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) muPart += __shfl_xor(muPart, off, 64);
+  if (l == 0) sMu[w] = muPart;
+  __syncthreads();
+  if (tid < n) {
+    float u1 = 0.f, u2 = 0.f;
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) {
+      u1 += sRow[0][q][tid];
+      u2 += sRow[1][q][tid];
+    }
+    const int64_t sidx = (b * a.T + t0 + tid) * a.H + h;
+    if (ba.dbeta_p) ba.dbeta_p[sidx] = u1;
+    if (ba.dg_p) ba.dg_p[sidx] = sEgp[tid] * u2;
+  }
+  if (tid == 0) {
+    float m = 0.f;
+#pragma unroll
+    for (int q = 0; q < PCS * NCH; ++q) m += sMu[q];
+    ba.pcMu[bh * a.NT + i] = m;
+  }
+}
+
 template <typename T, int DK, bool FINAL>
-__global__ __launch_bounds__(DK) void pc_chunk(BwdArgs ba) {
-  __shared__ float sA[C * DK];
-  __shared__ float sKv[C * DK];
-  __shared__ float sEgp[C], sBp[C];
-  __shared__ float sRb[C * DK / 64 * 2];   // per-row wave partials: [row][wave][2]
-  __shared__ float sMu[DK / 64];
+__global__ __launch_bounds__(DK * PCS) void pc_chunk(BwdArgs ba) {
+  __shared__ float sEgp[C], sBp[C], sGp[C];
+  __shared__ float sEnd[PCS][DK];          // per-segment end values (A, then adjoint)
+  __shared__ float sRow[2][DK / 64][C];    // per-channel-half row sums: D k^2, D A_{r-1}
+  __shared__ float sMu[PCS * DK / 64];
   const FwdArgs& a = ba.f;
   const int64_t blk = blockIdx.x;
   const int64_t bh = blk / a.NT;
   const int i = static_cast<int>(blk % a.NT);
   const int64_t b = bh / a.H, h = bh % a.H;
-  const int c = threadIdx.x, wv = c >> 6, l = c & 63;
+  const int tid = threadIdx.x;
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
-  const T* kp = static_cast<const T*>(a.k);
-  if (c < C) {
-    const bool ok = c < n;
-    const int64_t sidx = (b * a.T + t0 + c) * a.H + h;
-    sEgp[c] = (ok && a.g_p) ? fast_exp(a.g_p[sidx]) : 1.f;
-    sBp[c] = ok ? a.beta_p[sidx] : 0.f;
+  if (tid < C) {
+    // per-token factors; padded tokens: aP = 1 (gP = 0), bP = 0.  sGp is the
+    // in-chunk inclusive prefix of gP (one wave, shuffle scan)
+    const bool ok = tid < n;
+    const int64_t sidx = (b * a.T + t0 + min(tid, n - 1)) * a.H + h;
+    const float gp = (ok && a.g_p) ? a.g_p[sidx] : 0.f;
+    sEgp[tid] = fast_exp(gp);
+    sBp[tid] = ok ? a.beta_p[sidx] : 0.f;
+    float x = gp;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const float y = __shfl_up(x, off, 64);
+      if (tid >= off) x += y;
+    }
+    sGp[tid] = x;
   }
   __syncthreads();
-  const float A_start = a.Abound[(bh * (a.NT + 1) + i) * DK + c];
-  float A = A_start;
-  for (int r = 0; r < C; ++r) {
-    const float kr = r < n ? to_f(kp[((b * a.T + t0 + r) * a.H + h) * DK + c]) : 0.f;
-    A = sEgp[r] * A + sBp[r] * kr * kr;
-    sA[r * DK + c] = A;
-    sKv[r * DK + c] = kr;
-  }
-  const float mu = fast_exp(a.log_a_scale[h]);
-  const float lnx = a.lnx;
-  const float* dkt = ba.dKt + (bh * a.Tpad + t0) * DK + c;
-  float D = FINAL ? ba.pcC[(bh * (a.NT + 1) + i + 1) * DK + c] : 0.f;   // adjoint entering from the right
-  float aNext = 1.f;   // aP of the token after r (its factor on D)
-  float muPart = 0.f;
-  for (int r = C - 1; r >= 0; --r) {
-    const float Ar = sA[r * DK + c];
-    const float kvr = sKv[r * DK + c];
-    const float dk_t = dkt[r * DK];
-    const float Bv = squash_gain(Ar, mu, lnx);
-    float inj = 0.f, dr = 0.f;
-    if (Ar > 0.f) {
-      const float rr = fast_log(Ar) - mu;
-      const float ds = -lnx * Bv * dk_t * kvr;
-      const float den = 1.f + fabsf(rr);
-      dr = ds / (den * den);
-      inj = dr / Ar;
-    }
-    D = inj + aNext * D;
-    aNext = sEgp[r];
-    if (FINAL) {
-      muPart -= dr;
-      if (r < n) {
-        const float Aprev = r > 0 ? sA[(r - 1) * DK + c] : A_start;
-        const float dkk = ba.dKm[(bh * a.Tpad + t0 + r) * DK + c] + Bv * dk_t + 2.f * sBp[r] * kvr * D;
-        static_cast<T*>(ba.dk)[((b * a.T + t0 + r) * a.H + h) * DK + c] = from_f<T>(dkk);
-        // per-row sums over channels: dbetaP_r = sum D k^2, dgP_r = aP_r sum D A_{r-1}
-        float s1 = D * kvr * kvr, s2 = D * Aprev;
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) {
-          s1 += __shfl_xor(s1, off, 64);
-          s2 += __shfl_xor(s2, off, 64);
-        }
-        if (l == 0) {
-          sRb[(r * (DK / 64) + wv) * 2] = s1;
-          sRb[(r * (DK / 64) + wv) * 2 + 1] = s2;
-        }
-      }
-    }
-  }
-  if (!FINAL) {
-    // the adjoint this chunk sends to the left, with zero carry: aP_0 D_0
-    ba.pcL[(bh * a.NT + i) * DK + c] = aNext * D;
-  } else {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) muPart += __shfl_xor(muPart, off, 64);
-    if (l == 0) sMu[wv] = muPart;
-    __syncthreads();
-    if (c < n) {
-      float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-      for (int q = 0; q < DK / 64; ++q) {
-        s1 += sRb[(c * (DK / 64) + q) * 2];
-        s2 += sRb[(c * (DK / 64) + q) * 2 + 1];
-      }
-      const int64_t sidx = (b * a.T + t0 + c) * a.H + h;
-      if (ba.dbeta_p) ba.dbeta_p[sidx] = s1;
-      if (ba.dg_p) ba.dg_p[sidx] = sEgp[c] * s2;
-    }
-    if (c == 0) {
-      float m = 0.f;
-#pragma unroll
-      for (int q = 0; q < DK / 64; ++q) m += sMu[q];
-      ba.pcMu[bh * a.NT + i] = m;
-    }
-  }
+  if (n == C)
+    pc_body<true, T, DK, FINAL>(ba, bh, i, n, sEgp, sBp, sGp, sEnd, sRow, sMu);
+  else
+    pc_body<false, T, DK, FINAL>(ba, bh, i, n, sEgp, sBp, sGp, sEnd, sRow, sMu);
 }
 
 // carry_{i-1} = L_i + exp(sumD_i) carry_i, from the last chunk (carry 0)
@@ -843,15 +974,13 @@ BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate,
   L.Xr = take(bh * tp * dv * esz);
   L.Er = take(bh * tp * dv * esz);
   L.PtT = take(bh * nt * C * C * esz);
-  L.TtT = take(bh * nt * C * C * esz);
-  L.Mi = take(bh * nt * C * C * 4);
+  L.MtT = take(bh * nt * C * C * esz);
   L.Ktr = take(bh * tp * dk * esz);
   L.Kw = take(bh * tp * dk * esz);
   L.QlT = take(bh * nt * dk * C * esz);
   L.KnT = take(bh * nt * dk * C * esz);
   L.dHs = take(bh * nt * dk * dv * esz);
-  L.dEr = take(bh * tp * dv * esz);
-  L.dXr = take(bh * tp * dv * esz);
+  L.Zr = take(bh * tp * dv * esz);
   L.dSqk = take(bh * nt * C * C * esz);
   L.dSqkT = take(bh * nt * C * C * esz);
   L.dSkk = take(bh * nt * C * C * esz);
@@ -886,11 +1015,11 @@ static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s, hipEvent_t 
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = mark(6)) != hipSuccess) return e;
   if (a.precond == kSquash) {
-    hipLaunchKernelGGL((pc_chunk<T, DK, false>), dim3(grid_chunk), dim3(DK), 0, s, ba);
+    hipLaunchKernelGGL((pc_chunk<T, DK, false>), dim3(grid_chunk), dim3(DK * PCS), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((pc_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((pc_chunk<T, DK, true>), dim3(grid_chunk), dim3(DK), 0, s, ba);
+    hipLaunchKernelGGL((pc_chunk<T, DK, true>), dim3(grid_chunk), dim3(DK * PCS), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ba.dlog_a_scale) {
       hipLaunchKernelGGL(pc_mu, dim3(static_cast<unsigned>(a.H)), dim3(256), 0, s, ba);

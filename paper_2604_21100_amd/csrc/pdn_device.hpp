@@ -145,16 +145,15 @@ __device__ __forceinline__ void st_tile_t(T* out, int ld, const floatx4& acc, in
 
 __device__ __forceinline__ float fast_exp(float x) { return __expf(x); }
 __device__ __forceinline__ float fast_log(float x) { return __logf(x); }
+// hardware reciprocal (1 ulp)
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
 // Stable preconditioner gain B = exp(-log(x) * r / (1 + |r|)), r = log(A) - mu;
 // A <= 0 (a key channel that has been zero so far) takes the r -> -inf limit,
-// B = x.
+// B = x.  Branch-free (a select), so unrolled callers keep one basic block.
 __device__ __forceinline__ float squash_gain(float A, float mu, float lnx) {
-  float s = -1.f;
-  if (A > 0.f) {
-    const float r = fast_log(A) - mu;
-    s = r / (1.f + fabsf(r));
-  }
+  const float r = fast_log(fmaxf(A, 1e-30f)) - mu;
+  const float s = A > 0.f ? r * fast_rcp(1.f + fabsf(r)) : -1.f;
   return fast_exp(-lnx * s);
 }
 

@@ -126,8 +126,8 @@ struct K2Smem {
   static constexpr size_t kTotal = kR1 + kR2 + kR3 + kGc + kY + kScal + kSeg;
 };
 
-// BWD: also write the operand layouts the backward kernels read (P^T, T^T,
-// M, write-key rows, w-scaled write-key rows, (Diag(lam) Q)^T and
+// BWD: also write the operand layouts the backward kernels read (P^T, M^T,
+// write-key rows, w-scaled write-key rows, (Diag(lam) Q)^T and
 // -(Diag(lam) K)^T); scalar gate or no gate only.
 template <typename T, int DK, int GATE, int PREC, bool BWD>
 __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
@@ -399,23 +399,18 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   }
   if (BWD) {
     const int64_t cc = (bh * a.NT + i) * (int64_t)(C * C);
-    float* Mo = a.Mi + cc;
-    T* TtT = static_cast<T*>(a.TtT) + cc;
+    T* MtT = static_cast<T*>(a.MtT) + cc;
     for (int idx = tid; idx < C * C / 8; idx += 256) {
       const int r = idx / (C / 8), t0v = (idx % (C / 8)) * 8;
-      Frag8<float> fm;
       Frag8<T> ft;
 #pragma unroll
       for (int s2 = 0; s2 < 8; ++s2) {
         const int t = t0v + s2;
-        const bool lower = (t >> 4) < (r >> 4) || ((t >> 4) == (r >> 4) && t <= r);
-        fm.set(s2, lower ? sX[r * LDA + t] : 0.f);
-        // T^T[r][t] = T[t][r] = M[t][r] beta_r
+        // M^T[r][t] = M[t][r]; M is lower triangular (block-lower in sX)
         const bool upper = (r >> 4) < (t >> 4) || ((r >> 4) == (t >> 4) && r <= t);
-        ft.set(s2, upper ? sX[t * LDA + r] * sBeta[r] : 0.f);
+        ft.set(s2, upper ? sX[t * LDA + r] : 0.f);
       }
-      st8(Mo + r * C + t0v, fm);
-      st8(TtT + r * C + t0v, ft);
+      st8(MtT + r * C + t0v, ft);
     }
     // write-key rows and w-scaled write-key rows
     T* Kr = static_cast<T*>(a.Ktr) + (bh * a.Tpad + t0) * DK;

@@ -320,14 +320,13 @@ static pdn_status chunk_bwd_impl(const pdn_problem* p, const pdn_inputs* in, con
   }
   f.KtG = w + L.f.KtG; f.Tm = w + L.f.Tm; f.Pm = w + L.f.Pm;
   if (p->gate != PDN_GATE_NONE) f.G = reinterpret_cast<float*>(w + L.f.G);
-  f.Hs = w + L.Hs; f.Xr = w + L.Xr; f.Er = w + L.Er; f.PtT = w + L.PtT; f.TtT = w + L.TtT;
-  f.Mi = reinterpret_cast<float*>(w + L.Mi);
+  f.Hs = w + L.Hs; f.Xr = w + L.Xr; f.Er = w + L.Er; f.PtT = w + L.PtT; f.MtT = w + L.MtT;
   f.Ktr = w + L.Ktr; f.Kw = w + L.Kw; f.QlT = w + L.QlT; f.KnT = w + L.KnT;
   a.dO = dO; a.dS_T = dS_T;
   a.dq = out->dq; a.dk = out->dk; a.dv = out->dv; a.dbeta = out->dbeta; a.dg = out->dg;
   a.dS0 = out->dS0; a.dbeta_p = out->dbeta_p; a.dg_p = out->dg_p; a.dlog_a_scale = out->dlog_a_scale;
   a.dA0 = out->dA0; a.dktilde = out->dktilde;
-  a.dHs = w + L.dHs; a.dEr = w + L.dEr; a.dXr = w + L.dXr;
+  a.dHs = w + L.dHs; a.Zr = w + L.Zr;
   a.dSqk = w + L.dSqk; a.dSqkT = w + L.dSqkT; a.dSkk = w + L.dSkk; a.dSkkT = w + L.dSkkT;
   a.dGp = reinterpret_cast<float*>(w + L.dGp);
   a.dKt = reinterpret_cast<float*>(w + L.dKt);

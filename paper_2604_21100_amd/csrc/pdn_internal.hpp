@@ -53,8 +53,7 @@ struct FwdArgs {
   void* Xr;       // [BH, Tpad, dv] io    X = V - (Lam K) S^T rows
   void* Er;       // [BH, Tpad, dv] io    E = T X rows
   void* PtT;      // [BH, NT, C, C] io    P^T
-  void* TtT;      // [BH, NT, C, C] io    T^T
-  float* Mi;      // [BH, NT, C, C] fp32  M = (I + At)^{-1} (T = M Diag(beta))
+  void* MtT;      // [BH, NT, C, C] io    M^T, M = (I + At)^{-1} (T = M Diag(beta))
   void* Ktr;      // [BH, Tpad, dk] io    write key rows
   void* Kw;       // [BH, Tpad, dk] io    w_r * write key rows
   void* QlT;      // [BH, NT, dk, C] io   (Diag(lam) Q)^T per chunk
@@ -80,8 +79,7 @@ struct BwdArgs {
   void* dktilde;
   // workspace
   void* dHs;      // [BH, NT, dk, dv] io  state adjoint entering each chunk from the right
-  void* dEr;      // [BH, Tpad, dv] io    dE rows
-  void* dXr;      // [BH, Tpad, dv] io    dX rows (= dV, padded to whole chunks)
+  void* Zr;       // [BH, Tpad, dv] io    Z = M^T dE rows (dX = dV = Diag(beta) Z)
   void* dSqk;     // [BH, NT, C, C] io    d(Q Kt^T), masked and decayed
   void* dSqkT;    // transposed
   void* dSkk;     // [BH, NT, C, C] io    d(K Kt^T)
@@ -102,8 +100,8 @@ WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precon
 
 struct BwdWsLayout {
   WsLayout f;
-  size_t Hs, Xr, Er, PtT, TtT, Mi, Ktr, Kw, QlT, KnT;
-  size_t dHs, dEr, dXr, dSqk, dSqkT, dSkk, dSkkT, dGp, dKt, dKm, pcL, pcC, pcMu, total;
+  size_t Hs, Xr, Er, PtT, MtT, Ktr, Kw, QlT, KnT;
+  size_t dHs, Zr, dSqk, dSqkT, dSkk, dSkkT, dGp, dKt, dKm, pcL, pcC, pcMu, total;
 };
 
 BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond);
