@@ -6,9 +6,12 @@ fp32 state, B=4, T=4096, H=16, d_k=d_v=128, chunk 64, scalar gate, squash
 preconditioner with x=1.5).  One step is one pass of the whole hot path over
 the batch, with inputs resident in HBM: the forward (preconditioner scan,
 per-chunk UT transform, inter-chunk state scan with the chunk output) and then
-the backward for an upstream gradient dO (recompute of the forward
-intermediates, reverse state-adjoint scan, per-chunk adjoint algebra, the
-preconditioner's reverse scan).  --pass fwd times the forward alone.
+the backward for an upstream gradient dO (reverse state-adjoint scan,
+per-chunk adjoint algebra, the preconditioner's reverse scan).  The step uses
+the training pair: pdn_chunk_fwd_train leaves the forward intermediates in the
+workspace and pdn_chunk_bwd_train reads them (--recompute times pdn_chunk_fwd
++ pdn_chunk_bwd, whose backward recomputes them).  --pass fwd times the
+inference forward pdn_chunk_fwd alone.
 
 Prints ONE JSON line: tokens/s (B*T per step time), the roofline of the
 dominant kernel measured live with HIP events on the launch stream, and the
@@ -37,17 +40,18 @@ PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3       # dense fp32 matrix
 
 
-def algorithmic_per_token_head(spec):
+def algorithmic_per_token_head(spec, train=False):
     """Algorithmic FLOPs and bytes per token-head (one (b, t, h)).
 
     Dense per-chunk products as the paper writes them:
         forward  FLOP = 6 C dk + 4 C dv + 6 dk dv + C^2 / 3
         backward FLOP = 12 C dk + 8 C dv + 12 dk dv + 4 C^2
     (the backward's recompute of forward intermediates is executed work, not
-    algorithmic, and is not in the totals).  Per kernel stage: its share of
-    those FLOPs (the recompute stages: the products they execute) and its
-    compulsory bytes (what that kernel must read and write, each once).
-    Returns (flop_fwd, flop_bwd, {stage: (flop, bytes)})."""
+    algorithmic, and is not in the totals).  Per kernel stage: the products
+    that kernel performs and its compulsory bytes (what it must read and
+    write, each once).  train: the forward also writes the intermediates the
+    backward reads (training pair).  Returns (flop_fwd, flop_bwd,
+    {stage: (flop, bytes)})."""
     C, dk, dv = spec.chunk, spec.dk, spec.dv
     e = 2 if spec.io == "bf16" else 4
     gb = {"none": 0, "scalar": 4, "channel": 4 * dk}[spec.gate]
@@ -55,49 +59,47 @@ def algorithmic_per_token_head(spec):
     flop_fwd = 6 * C * dk + 4 * C * dv + 6 * dk * dv + C * C / 3.0
     flop_bwd = 12 * C * dk + 8 * C * dv + 12 * dk * dv + 4 * C * C
     precond = (3 * dk, e * dk + 8 + 4 * dk / C)
+    # k2: read q, k, beta, g, betaP, gP, chunk-start A; write the decayed
+    # write keys (dk), T and P (C each) and the gate prefix
+    prep = (4 * C * dk + C * C / 3.0,
+            2 * e * dk + 12 + gb + 4 * dk / C + e * (dk + 2 * C) + gb)
+    # k2 (backward mode): also P^T and M^T (C each) and the write-key,
+    # decayed write-key, decayed query and key rows (dk each)
+    prep_b = (prep[0], prep[1] + 2 * e * C + 4 * e * dk)
+    # k3: read q, k, v, T, P, decayed write keys, gate prefix; write o
+    scan = (6 * dk * dv + 4 * C * dv,
+            e * (2 * dk + dv) + e * (2 * C + dk) + gb + e * dv)
+    # k3 (saving, no output): read k, v, T, decayed write keys, gate prefix;
+    # write the chunk-start states and the X, E rows
+    save = (4 * dk * dv + 2 * C * dv,
+            e * (dk + dv) + e * (C + dk) + gb + st + 2 * e * dv)
     stages = {
-        # k1: read k, betaP, gP; write the per-chunk summaries
         "precond": precond,
-        # k2: read q, k, beta, g, betaP, gP, chunk-start A; write the decayed
-        # write keys (dk), T and P (C each) and the gate prefix
-        "chunk_prep": (4 * C * dk + C * C / 3.0,
-                       2 * e * dk + 12 + gb + 4 * dk / C
-                       + e * (dk + 2 * C) + gb),
-        # k3: read q, k, v, T, P, decayed write keys, gate prefix; write o
-        "chunk_scan": (6 * dk * dv + 4 * C * dv,
-                       e * (2 * dk + dv) + e * (2 * C + dk) + gb + e * dv),
+        "chunk_prep": prep_b if train else prep,
+        # training forward: the output and the saved states and rows
+        "chunk_scan": ((scan[0], scan[1] + st + 2 * e * dv) if train
+                       else scan),
         "bwd_precond_recompute": precond,
-        # k2 (backward): as k2, plus P^T, T^T (C each, io), M (C, fp32) and
-        # the write-key, decayed write-key, decayed query and key rows (dk
-        # each, io)
-        "bwd_chunk_prep": (4 * C * dk + C * C / 3.0,
-                           2 * e * dk + 12 + gb + 4 * dk / C
-                           + e * (dk + 2 * C) + gb
-                           + 2 * e * C + 4 * C + 4 * e * dk),
-        # k3 (saving): read k, v, T, decayed write keys, gate prefix; write
-        # the chunk-start states and the X, E rows
-        "bwd_state_save_scan": (4 * dk * dv + 2 * C * dv,
-                                e * (dk + dv) + e * (C + dk) + gb
-                                + st + 2 * e * dv),
-        # r1: read P^T, T^T, w*Kt, (lam Q)^T, -(lam K)^T, dO; write the state
-        # adjoints, dE, dX rows and dv
+        "bwd_chunk_prep": prep_b,
+        "bwd_state_save_scan": save,
+        # r1: read P^T, M^T, w*Kt, (lam Q)^T, -(lam K)^T, dO, beta; write the
+        # state adjoints, the Z rows and dv
         "bwd_state_adjoint_scan": (4 * C * dv + 6 * dk * dv,
-                                   2 * e * C + 3 * e * dk + e * dv + 4 / C
-                                   + st + 3 * e * dv),
-        # p1: read dO, E, dE, X, M, beta, gate prefix, q, kt, k; write the
-        # four masked C x C adjoints (and transposes), dbeta, dG partial
-        "bwd_chunk_cc": (4 * C * dv + 4 * C * dk + 4 * C * C,
-                         4 * e * dv + 4 * C + 4 + gb + 3 * e * dk
-                         + 4 * e * C + 8),
-        # p2: read dO, dX, E, S, dS', gate prefix, kt, q, k, the C x C
-        # adjoints, dG partial; write dq, dk (read key, fp32), dkt (fp32), dg
+                                   2 * e * C + 3 * e * dk + e * dv + 4
+                                   + 4 / C + st + 2 * e * dv),
+        # p1: read dO, E, Z, X, q, kt, k, beta, gate prefix; write the four
+        # masked C x C adjoints (and transposes), dbeta, dG partial
+        "bwd_chunk_cc": (4 * C * dv + 4 * C * dk,
+                         4 * e * dv + 3 * e * dk + 4 + gb + 4 * e * C + 8),
+        # p2: read dO, dX, E, S, dS', kt, q, k, the C x C adjoints, gate
+        # prefix, dG partial; write dq, dk (read key) and dkt (io), dg
         "bwd_chunk_grads": (6 * dk * dv + 8 * C * dk,
-                            3 * e * dv + 2 * st + gb + 3 * e * dk + 4 * e * C
-                            + 4 + e * dk + 8 * dk + 4),
+                            3 * e * dv + 2 * st + 3 * e * dk + 4 * e * C
+                            + gb + 4 + 3 * e * dk + 4),
         # pc: read k, dk (read key), dkt, betaP, gP, chunk-start A; write dk,
         # dbetaP, dgP
         "bwd_precond_reverse": (10 * dk,
-                                e * dk + 8 * dk + 8 + 4 * dk / C + e * dk + 8),
+                                3 * e * dk + 8 + 4 * dk / C + e * dk + 8),
     }
     return flop_fwd, flop_bwd, stages
 
@@ -106,6 +108,8 @@ KERNELS = {
     "precond": "k1_precond_summary+k1_precond_carry",
     "chunk_prep": "k2_chunk_prep",
     "chunk_scan": "k3_chunk_scan",
+    "chunk_prep_train": "k2_chunk_prep (backward mode)",
+    "chunk_scan_train": "k3_chunk_scan (saving mode, with output)",
     "bwd_precond_recompute": "k1_precond_summary+k1_precond_carry",
     "bwd_chunk_prep": "k2_chunk_prep (backward mode)",
     "bwd_state_save_scan": "k3_chunk_scan (saving mode)",
@@ -184,7 +188,7 @@ def cpu_baseline(spec, inp, bwd, target_s=15.0):
     }
 
 
-def roofline_of(stage, ms, stages, token_heads):
+def roofline_of(stage, ms, stages, token_heads, train=False):
     """Roofline object for one kernel stage from its measured average time."""
     dflop, dbytes = stages[stage]
     sec = ms / 1e3
@@ -198,7 +202,8 @@ def roofline_of(stage, ms, stages, token_heads):
                 "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = None
-    roof["kernel"] = KERNELS[stage]
+    roof["kernel"] = KERNELS[stage + ("_train" if train and stage in
+                                     ("chunk_prep", "chunk_scan") else "")]
     roof["stage"] = stage
     roof["avg_ms"] = ms
     roof["alg_bytes_per_launch"] = dbytes * token_heads
@@ -215,6 +220,9 @@ def main(argv=None):
                     choices=sorted(pi.WORKLOADS))
     ap.add_argument("--pass", dest="passes", default="fwdbwd",
                     choices=("fwd", "fwdbwd"))
+    ap.add_argument("--recompute", action="store_true",
+                    help="fwd+bwd with pdn_chunk_fwd + pdn_chunk_bwd (the "
+                         "backward recomputes the forward intermediates)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -287,20 +295,22 @@ def main(argv=None):
     fwd_stages = list(pdn.FWD_STAGES)
     bwd_stages = list(pdn.BWD_STAGES) if bwd else []
 
+    train = bwd and not args.recompute
+
     def step(fev=None, bev=None):
         pdn.pdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], g=d["g"],
                           gate=spec.gate, beta_p=d["beta_p"], g_p=d["g_p"],
                           log_a_scale=d["log_a_scale"], A0=d["A0"],
                           S0=d["S0"], x=spec.x, scale=spec.scale, o=o,
                           S_T=S_T, A_T=A_T, workspace=ws, stream=stream,
-                          stage_events=fev)
+                          stage_events=fev, train=train)
         if bwd:
             pdn.pdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], d["dO"],
                               g=d["g"], gate=spec.gate, beta_p=d["beta_p"],
                               g_p=d["g_p"], log_a_scale=d["log_a_scale"],
                               A0=d["A0"], S0=d["S0"], x=spec.x,
                               scale=spec.scale, outputs=grads, workspace=ws,
-                              stream=stream, stage_events=bev)
+                              stream=stream, stage_events=bev, saved=train)
         if calib is not None:
             calib[1].copy_(calib[0])
 
@@ -327,6 +337,8 @@ def main(argv=None):
         stage_ms[name] = sum(fev[i][si].elapsed_time(fev[i][si + 1])
                              for i in range(K)) / K
     for si, name in enumerate(bwd_stages):
+        if train and si < 3:
+            continue   # the recompute stages are empty in the training pair
         stage_ms[name] = sum(bev[i][si].elapsed_time(bev[i][si + 1])
                              for i in range(K)) / K
     fwd_ms = sum(fev[i][0].elapsed_time(fev[i][-1]) for i in range(K)) / K
@@ -335,10 +347,10 @@ def main(argv=None):
 
     tokens = B * T
     token_heads = B * T * H
-    flop_fwd, flop_bwd, stages = algorithmic_per_token_head(spec)
+    flop_fwd, flop_bwd, stages = algorithmic_per_token_head(spec, train)
     dom = max(stage_ms, key=stage_ms.get)
-    roof = roofline_of(dom, stage_ms[dom], stages, token_heads)
-    kernels = {k: roofline_of(k, v, stages, token_heads)["frac"]
+    roof = roofline_of(dom, stage_ms[dom], stages, token_heads, train)
+    kernels = {k: roofline_of(k, v, stages, token_heads, train)["frac"]
                for k, v in stage_ms.items()}
 
     flop_step = flop_fwd + (flop_bwd if bwd else 0.0)
@@ -361,7 +373,9 @@ def main(argv=None):
         "dtype": spec.io,
         "data": "synthetic",
         "config": {"workload": args.workload, "variant": variant,
-                   "pass": "forward+backward" if bwd else "forward",
+                   "pass": ("forward+backward (training pair)" if train
+                            else "forward+backward (backward recomputes)"
+                            if bwd else "forward"),
                    "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
                    "chunk": spec.chunk, "gate": spec.gate,
                    "precond": "squash", "x": spec.x, "global_batch": B,

@@ -183,6 +183,35 @@ pdn_status pdn_chunk_bwd_events(const pdn_problem* problem, const pdn_inputs* in
                                 void* ws, size_t ws_bytes, void* hip_stream,
                                 void* const* stage_events, int n_events);
 
+/* Training pair.  pdn_chunk_fwd_train computes exactly what pdn_chunk_fwd
+ * computes and also leaves in `ws` the forward intermediates the backward
+ * reads (per-chunk solve factors, chunk-start states, the X and E rows, the
+ * write-key rows, ...), so that pdn_chunk_bwd_train can skip the
+ * recompute of the forward that pdn_chunk_bwd performs.  This trades memory
+ * for time: `ws` must hold at least pdn_workspace_size(problem, 1, &bytes) bytes
+ * (the backward's workspace) for both calls.
+ *
+ * Contract: pdn_chunk_bwd_train must receive the same problem, the same
+ * input pointers with unchanged contents and the same `ws` as the preceding
+ * pdn_chunk_fwd_train, with no other call writing `ws` in between (the
+ * library cannot detect a violation; results are then undefined, but every
+ * access stays inside the declared buffers).  pdn_chunk_bwd_train leaves the
+ * saved intermediates intact, so it may be called again for another dO.
+ * The backward's restrictions apply to both calls (no per-channel gate; fp32
+ * io only with d_k = d_v = 64: PDN_ERR_UNSUPPORTED).
+ *
+ * stage_events: NULL with n_events = 0, or PDN_FWD_STAGE_EVENTS /
+ * PDN_BWD_STAGE_EVENTS caller-created events recorded as in the _events
+ * variants (the backward's recompute stages are then empty). */
+pdn_status pdn_chunk_fwd_train(const pdn_problem* problem, const pdn_inputs* in,
+                               pdn_fwd_out* out, void* ws, size_t ws_bytes,
+                               void* hip_stream, void* const* stage_events,
+                               int n_events);
+pdn_status pdn_chunk_bwd_train(const pdn_problem* problem, const pdn_inputs* in,
+                               const void* dO, const float* dS_T, pdn_bwd_out* out,
+                               void* ws, size_t ws_bytes, void* hip_stream,
+                               void* const* stage_events, int n_events);
+
 /* Static, NUL-terminated description of a status code. */
 const char* pdn_status_string(pdn_status status);
 

@@ -112,14 +112,23 @@ _lib.pdn_chunk_bwd_events.argtypes = [
     ctypes.POINTER(BwdOut), _vp, ctypes.c_size_t, _vp, ctypes.POINTER(_vp),
     ctypes.c_int]
 _lib.pdn_chunk_bwd_events.restype = ctypes.c_int
+_lib.pdn_chunk_fwd_train.argtypes = [
+    ctypes.POINTER(Problem), ctypes.POINTER(Inputs), ctypes.POINTER(FwdOut),
+    _vp, ctypes.c_size_t, _vp, ctypes.POINTER(_vp), ctypes.c_int]
+_lib.pdn_chunk_fwd_train.restype = ctypes.c_int
+_lib.pdn_chunk_bwd_train.argtypes = [
+    ctypes.POINTER(Problem), ctypes.POINTER(Inputs), _vp, _vp,
+    ctypes.POINTER(BwdOut), _vp, ctypes.c_size_t, _vp, ctypes.POINTER(_vp),
+    ctypes.c_int]
+_lib.pdn_chunk_bwd_train.restype = ctypes.c_int
 _lib.pdn_status_string.argtypes = [ctypes.c_int]
 _lib.pdn_status_string.restype = ctypes.c_char_p
 _lib.pdn_abi_version.argtypes = []
 _lib.pdn_abi_version.restype = ctypes.c_int
 
 EXPORTED = ("pdn_workspace_size", "pdn_chunk_fwd", "pdn_chunk_fwd_events",
-            "pdn_chunk_bwd", "pdn_chunk_bwd_events", "pdn_status_string",
-            "pdn_abi_version")
+            "pdn_chunk_bwd", "pdn_chunk_bwd_events", "pdn_chunk_fwd_train",
+            "pdn_chunk_bwd_train", "pdn_status_string", "pdn_abi_version")
 FWD_STAGE_EVENTS = 4   # PDN_FWD_STAGE_EVENTS
 BWD_STAGE_EVENTS = 8   # PDN_BWD_STAGE_EVENTS
 FWD_STAGES = ("precond", "chunk_prep", "chunk_scan")
@@ -219,13 +228,15 @@ def pdn_chunk_fwd(q, k, v, beta, *, g=None, gate="none", precond="squash",
                   beta_p=None, g_p=None, log_a_scale=None, A0=None, S0=None,
                   ktilde=None, x=1.5, scale=1.0, chunk=64, o=None, S_T=None,
                   A_T=None, want_state=True, workspace=None, stream=None,
-                  stage_events=None):
+                  stage_events=None, train=False):
     """Forward pass on torch device tensors in the ABI layouts of pdn.h.
 
     Returns (o, S_T, A_T); S_T / A_T are None when not requested.  Outputs and
     the workspace are allocated with torch when not given.  stage_events: 4
     recorded-at-stage-boundary torch.cuda.Event objects (see
-    pdn_chunk_fwd_events), or None."""
+    pdn_chunk_fwd_events), or None.  train=True runs pdn_chunk_fwd_train:
+    the workspace (then of the backward's size, and required) keeps the
+    intermediates pdn_chunk_bwd(..., saved=True) reads."""
     import torch
     B, T, H, dk = q.shape
     dv = v.shape[-1]
@@ -239,12 +250,22 @@ def pdn_chunk_fwd(q, k, v, beta, *, g=None, gate="none", precond="squash",
         S_T = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev)
     if A_T is None and want_state and precond == "squash":
         A_T = torch.empty((B, H, dk), dtype=torch.float32, device=dev)
-    nbytes = pdn_workspace_size(prob, False)
+    nbytes = pdn_workspace_size(prob, train)
     if workspace is None:
+        if train:
+            raise ValueError("train=True needs the caller's workspace (it "
+                             "carries the intermediates to the backward)")
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     inp = _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde)
     out = FwdOut(_ptr(o), _ptr(S_T), _ptr(A_T))
-    if stage_events is None:
+    if train:
+        evs = [_event_handle(e) for e in (stage_events or [])]
+        arr = (_vp * len(evs))(*evs) if evs else None
+        st = _lib.pdn_chunk_fwd_train(
+            ctypes.byref(prob), ctypes.byref(inp), ctypes.byref(out),
+            _ptr(workspace), workspace.numel(), _stream(stream, dev), arr,
+            len(evs))
+    elif stage_events is None:
         st = pdn_chunk_fwd_raw(prob, inp, out, _ptr(workspace),
                                workspace.numel(), _stream(stream, dev))
     else:
@@ -268,13 +289,15 @@ def pdn_chunk_bwd(q, k, v, beta, dO, *, g=None, gate="none", precond="squash",
                   beta_p=None, g_p=None, log_a_scale=None, A0=None, S0=None,
                   ktilde=None, dS_T=None, x=1.5, scale=1.0, chunk=64,
                   outputs=None, want_optional=True, workspace=None,
-                  stream=None, stage_events=None):
+                  stream=None, stage_events=None, saved=False):
     """Backward pass on torch device tensors (layouts of pdn.h).
 
     Returns a dict with dq, dk, dv, dbeta and, when present, dg, dS0 and the
     preconditioner gradients dbeta_p, dg_p, dlog_a_scale, dA0 (squash) or
     dktilde (external).  Outputs and the workspace are allocated with torch
-    when not given (``outputs``: dict of preallocated tensors)."""
+    when not given (``outputs``: dict of preallocated tensors).  saved=True
+    runs pdn_chunk_bwd_train on the intermediates a preceding
+    pdn_chunk_fwd(..., train=True) left in ``workspace``."""
     import torch
     B, T, H, dk = q.shape
     dv = v.shape[-1]
@@ -306,10 +329,19 @@ def pdn_chunk_bwd(q, k, v, beta, dO, *, g=None, gate="none", precond="squash",
             need("dktilde", (B, T, H, dk), q.dtype)
     nbytes = pdn_workspace_size(prob, True)
     if workspace is None:
+        if saved:
+            raise ValueError("saved=True needs the training forward's workspace")
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     inp = _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde)
     bo = BwdOut(*[_ptr(out.get(n)) for n, _ in BwdOut._fields_])
-    if stage_events is None:
+    if saved:
+        evs = [_event_handle(e) for e in (stage_events or [])]
+        arr = (_vp * len(evs))(*evs) if evs else None
+        st = _lib.pdn_chunk_bwd_train(
+            ctypes.byref(prob), ctypes.byref(inp), _ptr(dO), _ptr(dS_T),
+            ctypes.byref(bo), _ptr(workspace), workspace.numel(),
+            _stream(stream, dev), arr, len(evs))
+    elif stage_events is None:
         st = pdn_chunk_bwd_raw(prob, inp, _ptr(dO), _ptr(dS_T), bo,
                                _ptr(workspace), workspace.numel(),
                                _stream(stream, dev))

@@ -503,42 +503,41 @@ __global__ __launch_bounds__(256) void p1_chunk_cc(BwdArgs ba) {
 }
 
 // ------------------------------------------------------------ p2
+// Per chunk: dq, the read- and write-key gradients and dg.
+//   phase 1  A1 = dO_s S, A2 = dX S, A3 = E dS'        (C x dk, over dv)
+//   phase 2  dq = Diag(lam) A1 + dSqk Kt, dK = -Diag(lam) A2 + dSkk Kt,
+//            dKt = Diag(w) A3 + dSqk^T Q + dSkk^T K    (over the chunk)
+// Wave w owns rows 16w .. 16w + 15.  Its A operands (dO, dX, E rows and
+// the rows of the four C x C adjoints) are private and load straight into
+// fragments once; the shared B operands (the chunk-start state and its
+// adjoint as rows [c][v], and Kt, Q, K transposed to [c][t]) are staged in
+// LDS for HC key columns at a time, so the block fits twice per CU.
 template <typename T, int DK, int DV>
 struct P2Smem {
-  static constexpr int LDR = DV + 8;   // rows of dO_s, dX, E
-  static constexpr int LDS = DV + 8;   // rows of S^T, dS'^T ([dk][dv])
-  static constexpr size_t kPh1 = sizeof(T) * (3 * C * LDR + 2 * DK * LDS);
-  static constexpr int LDT = C + 8;    // [dk][C] transposed rows and [C][C]
-  static constexpr size_t kPh2 = sizeof(T) * (3 * DK * LDT + 4 * C * LDT);
-  static constexpr size_t kMain = kPh1 > kPh2 ? kPh1 : kPh2;
-  static constexpr size_t kTotal = kMain + sizeof(float) * (6 * C + 4);
+  static constexpr int HC = 64;          // key columns per pass
+  static constexpr int LDV = DV + 8;     // staged state rows [c][v]
+  static constexpr int LDT = C + 8;      // transposed rows [c][t]
+  static constexpr size_t kH = sizeof(T) * 2 * HC * LDV;
+  static constexpr size_t kT = sizeof(T) * 3 * HC * LDT;
+  static constexpr size_t kTotal = kH + kT + sizeof(float) * (3 * C + 4);
 };
 
 template <typename T, int DK, int DV, int GATE>
-__global__ __launch_bounds__(256) void p2_chunk_grads(BwdArgs ba) {
+__global__ __launch_bounds__(256, 2) void p2_chunk_grads(BwdArgs ba) {
   using SM = P2Smem<T, DK, DV>;
-  constexpr int LDR = SM::LDR, LDS = SM::LDS, LDT = SM::LDT;
-  constexpr int NJ = DK / 16;   // column tiles over d_k
+  constexpr int HC = SM::HC, LDV = SM::LDV, LDT = SM::LDT;
+  constexpr int KV = DV / 32, NPASS = DK / HC;
+  constexpr uint32_t E = sizeof(T);
   __shared__ __attribute__((aligned(16))) char smem[SM::kTotal];
-  // phase 1
-  T* sDO = reinterpret_cast<T*>(smem);
-  T* sDX = sDO + C * LDR;
-  T* sE = sDX + C * LDR;
-  T* sS = sE + C * LDR;
-  T* sdS = sS + DK * LDS;
-  // phase 2 (reuses the same memory)
-  T* sKtT = reinterpret_cast<T*>(smem);
-  T* sQT = sKtT + DK * LDT;
-  T* sKT = sQT + DK * LDT;
-  T* sdSqk = sKT + DK * LDT;
-  T* sdSkk = sdSqk + C * LDT;
-  T* sdSqkT = sdSkk + C * LDT;
-  T* sdSkkT = sdSqkT + C * LDT;
-  float* sG = reinterpret_cast<float*>(smem + SM::kMain);
+  T* sS = reinterpret_cast<T*>(smem);        // S^T rows c0 .. c0 + HC - 1
+  T* sdS = sS + HC * LDV;                    // dS'^T rows
+  T* sKtT = reinterpret_cast<T*>(smem + SM::kH);
+  T* sQT = sKtT + HC * LDT;
+  T* sKT = sQT + HC * LDT;
+  float* sG = reinterpret_cast<float*>(smem + SM::kH + SM::kT);
   float* sDl = sG + C;      // d lam_r partials
   float* sDw = sDl + C;     // d w_r partials
-  float* sDG = sDw + C;
-  float* sRed = sDG + C;    // 4 wave partials of sum(dS' o S)
+  float* sRed = sDw + C;    // 4 wave partials of sum(dS' o S)
 
   const FwdArgs& a = ba.f;
   const int64_t blk = blockIdx.x;
@@ -550,74 +549,118 @@ __global__ __launch_bounds__(256) void p2_chunk_grads(BwdArgs ba) {
   const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
   const int64_t HV = a.H * (int64_t)DV, HD = a.H * (int64_t)DK;
   const int64_t cc = (bh * a.NT + i) * (int64_t)(C * C);
+  const int64_t rv = (bh * a.Tpad + t0) * DV, rk = (bh * a.Tpad + t0) * DK;
+  const int64_t cs = (bh * a.NT + i) * (int64_t)DK * DV;
 
-  // ---- phase 1: A1 = dO_s S, A2 = dX S, A3 = E dS'   (C x dk, row block w)
-  load_rows<T, DV>(sDO, LDR, static_cast<const T*>(ba.dO) + (b * a.T + t0) * HV + h * DV, HV, n, tid,
-                   a.scale);
-  const int64_t rv = (bh * a.Tpad + t0) * DV;
-  load_rows<T, DV>(sDX, LDR, static_cast<const T*>(ba.dv) + (b * a.T + t0) * HV + h * DV, HV, n, tid);
-  load_rows<T, DV>(sE, LDR, static_cast<const T*>(a.Er) + rv, DV, C, tid);
+  // ---- wave-private A operands, row ra (token rows past the end re-read
+  // the last row: their outputs are not stored and their gate terms are
+  // masked below)
+  const int ra = 16 * w + lr;
+  const uint32_t rc = static_cast<uint32_t>(min(ra, n - 1));
+  Frag8<T> fO[KV], fX[KV], fE[KV], fSq[2], fSk[2], fSqT[2], fSkT[2];
   {
-    constexpr int VEC = 16 / sizeof(T), VPR = DV / VEC;
-    const int64_t cs = (bh * a.NT + i) * (int64_t)DK * DV;
-    const T* Hs = static_cast<const T*>(a.Hs) + cs;
-    const T* dHs = static_cast<const T*>(ba.dHs) + cs;
-    for (int idx = tid; idx < DK * VPR; idx += 256) {
-      const int c = idx / VPR, cv = idx % VPR;
-      *reinterpret_cast<float4*>(sS + c * LDS + cv * VEC) = *reinterpret_cast<const float4*>(Hs + c * DV + cv * VEC);
-      *reinterpret_cast<float4*>(sdS + c * LDS + cv * VEC) = *reinterpret_cast<const float4*>(dHs + c * DV + cv * VEC);
+    const T* dob = static_cast<const T*>(ba.dO) + (b * a.T + t0) * HV + h * DV;
+    const T* dxb = static_cast<const T*>(ba.dv) + (b * a.T + t0) * HV + h * DV;
+    const T* eb = static_cast<const T*>(a.Er) + rv;
+#pragma unroll
+    for (int kk = 0; kk < KV; ++kk) {
+      const uint32_t o = (rc * static_cast<uint32_t>(HV) + 32 * kk + 8 * lg) * E;
+      fO[kk] = ld8(at_bytes(dob, o));
+      fX[kk] = ld8(at_bytes(dxb, o));
+      fE[kk] = ld8(at_bytes(eb, (static_cast<uint32_t>(ra * DV) + 32 * kk + 8 * lg) * E));
+    }
+    const uint32_t oc = static_cast<uint32_t>(ra * C + 8 * lg) * E;
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      fSq[k2] = ld8(at_bytes(static_cast<const T*>(ba.dSqk) + cc, oc + 32 * k2 * E));
+      fSk[k2] = ld8(at_bytes(static_cast<const T*>(ba.dSkk) + cc, oc + 32 * k2 * E));
+      fSqT[k2] = ld8(at_bytes(static_cast<const T*>(ba.dSqkT) + cc, oc + 32 * k2 * E));
+      fSkT[k2] = ld8(at_bytes(static_cast<const T*>(ba.dSkkT) + cc, oc + 32 * k2 * E));
     }
   }
   if (tid < C) sG[tid] = GATE == kGateScalar ? a.G[bh * a.Tpad + t0 + tid] : 0.f;
-  __syncthreads();
-  floatx4 A1[NJ], A2[NJ], A3[NJ];
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    A1[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    A2[j] = A1[j];
-    A3[j] = A1[j];
-    mma_tile<DV>(A1[j], sDO + (16 * w) * LDR, LDR, sS + (16 * j) * LDS, LDS, lr, lg);
-    mma_tile<DV>(A2[j], sDX + (16 * w) * LDR, LDR, sS + (16 * j) * LDS, LDS, lr, lg);
-    mma_tile<DV>(A3[j], sE + (16 * w) * LDR, LDR, sdS + (16 * j) * LDS, LDS, lr, lg);
-  }
-  // sum(dS' o S) for the gradient of lam_C
-  {
-    float part = 0.f;
-    for (int idx = tid; idx < DK * DV; idx += 256) {
-      const int c = idx / DV, v = idx % DV;
-      part += to_f(sS[c * LDS + v]) * to_f(sdS[c * LDS + v]);
-    }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) part += __shfl_xor(part, off, 64);
-    if (l == 0) sRed[w] = part;
-  }
-  __syncthreads();
-  // ---- phase 2: transposed Kt, Q, K and the C x C adjoints
-  load_rows_t<T, DK>(sKtT, static_cast<const T*>(a.Ktr) + (bh * a.Tpad + t0) * DK, DK, C, tid);
-  load_rows_t<T, DK>(sQT, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK, HD, n, tid);
-  load_rows_t<T, DK>(sKT, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK, HD, n, tid);
-  load_rows<T, C>(sdSqk, LDT, static_cast<const T*>(ba.dSqk) + cc, C, C, tid);
-  load_rows<T, C>(sdSkk, LDT, static_cast<const T*>(ba.dSkk) + cc, C, C, tid);
-  load_rows<T, C>(sdSqkT, LDT, static_cast<const T*>(ba.dSqkT) + cc, C, C, tid);
-  load_rows<T, C>(sdSkkT, LDT, static_cast<const T*>(ba.dSkkT) + cc, C, C, tid);
-  __syncthreads();
-  float lam[4], wr[4];
-#pragma unroll
-  for (int ii = 0; ii < 4; ++ii) {
-    const int r = 16 * w + 4 * lg + ii;
-    lam[ii] = GATE == kGateScalar ? fast_exp(sG[r]) : 1.f;
-    wr[ii] = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[r]) : 1.f;
-  }
-  // gate partials: dlam_r = Q_r . A1_r - K_r . A2_r ;  dw_r = Kt_r . A3_r
+
   float pl[4] = {0.f, 0.f, 0.f, 0.f}, pw[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    const int c = 16 * j + lr;
+  float red = 0.f;
+  T* dq = static_cast<T*>(ba.dq) + (b * a.T + t0) * HD + h * DK;
+  T* dKm = static_cast<T*>(ba.dKm) + rk;
+  T* dKt = static_cast<T*>(ba.dKt) + rk;
+#pragma unroll 1
+  for (int p = 0; p < NPASS; ++p) {
+    const int c0 = p * HC;
+    if (p > 0) __syncthreads();   // the previous pass is done with the LDS
+    {
+      constexpr int VEC = 16 / sizeof(T), VPR = DV / VEC;
+      const T* Hs = static_cast<const T*>(a.Hs) + cs + c0 * DV;
+      const T* dHs = static_cast<const T*>(ba.dHs) + cs + c0 * DV;
+      for (int idx = tid; idx < HC * VPR; idx += 256) {
+        const int c = idx / VPR, cv = idx % VPR;
+        *reinterpret_cast<float4*>(sS + c * LDV + cv * VEC) =
+            *reinterpret_cast<const float4*>(Hs + c * DV + cv * VEC);
+        *reinterpret_cast<float4*>(sdS + c * LDV + cv * VEC) =
+            *reinterpret_cast<const float4*>(dHs + c * DV + cv * VEC);
+      }
+    }
+    load_rows_t<T, HC>(sKtT, static_cast<const T*>(a.Ktr) + rk + c0, DK, C, tid);
+    load_rows_t<T, HC>(sQT, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
+    load_rows_t<T, HC>(sKT, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
+    __syncthreads();
+    float lam[4], wr[4];
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
       const int r = 16 * w + 4 * lg + ii;
-      pl[ii] += to_f(sQT[c * LDT + r]) * A1[j][ii] - to_f(sKT[c * LDT + r]) * A2[j][ii];
-      pw[ii] += to_f(sKtT[c * LDT + r]) * A3[j][ii];
+      lam[ii] = GATE == kGateScalar ? fast_exp(sG[r]) : 1.f;
+      wr[ii] = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[r]) : 1.f;
+    }
+    // sum(dS' o S) over this pass's rows
+    for (int idx = tid; idx < HC * DV; idx += 256) {
+      const int c = idx / DV, v = idx % DV;
+      red += to_f(sS[c * LDV + v]) * to_f(sdS[c * LDV + v]);
+    }
+#pragma unroll
+    for (int j = 0; j < HC / 16; ++j) {
+      // ---- phase 1
+      floatx4 A1 = {0.f, 0.f, 0.f, 0.f}, A2 = A1, A3 = A1;
+#pragma unroll
+      for (int kk = 0; kk < KV; ++kk) {
+        const Frag8<T> fh = ld8(sS + (16 * j + lr) * LDV + 32 * kk + 8 * lg);
+        const Frag8<T> fd = ld8(sdS + (16 * j + lr) * LDV + 32 * kk + 8 * lg);
+        mma(A1, fO[kk], fh);
+        mma(A2, fX[kk], fh);
+        mma(A3, fE[kk], fd);
+      }
+      // gate partials: dlam_r = Q_r . A1_r - K_r . A2_r ;  dw_r = Kt_r . A3_r
+      const int c = 16 * j + lr;
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int r = 16 * w + 4 * lg + ii;
+        A1[ii] *= a.scale;
+        pl[ii] += to_f(sQT[c * LDT + r]) * A1[ii] - to_f(sKT[c * LDT + r]) * A2[ii];
+        pw[ii] += to_f(sKtT[c * LDT + r]) * A3[ii];
+      }
+      // ---- phase 2
+      floatx4 aq, ak, at;
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        aq[ii] = lam[ii] * A1[ii];
+        ak[ii] = -lam[ii] * A2[ii];
+        at[ii] = wr[ii] * A3[ii];
+      }
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        const Frag8<T> fk = ld8(sKtT + (16 * j + lr) * LDT + 32 * k2 + 8 * lg);
+        mma(aq, fSq[k2], fk);
+        mma(ak, fSk[k2], fk);
+        mma(at, fSqT[k2], ld8(sQT + (16 * j + lr) * LDT + 32 * k2 + 8 * lg));
+        mma(at, fSkT[k2], ld8(sKT + (16 * j + lr) * LDT + 32 * k2 + 8 * lg));
+      }
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int r = 16 * w + 4 * lg + ii, cg = c0 + c;
+        if (r < n) dq[r * HD + cg] = from_f<T>(aq[ii]);
+        dKm[r * DK + cg] = from_f<T>(ak[ii]);
+        dKt[r * DK + cg] = from_f<T>(at[ii]);
+      }
     }
   }
 #pragma unroll
@@ -630,35 +673,14 @@ __global__ __launch_bounds__(256) void p2_chunk_grads(BwdArgs ba) {
   if (lr == 0) {
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
-      sDl[16 * w + 4 * lg + ii] = pl[ii];
-      sDw[16 * w + 4 * lg + ii] = pw[ii];
+      const int r = 16 * w + 4 * lg + ii;
+      sDl[r] = r < n ? pl[ii] : 0.f;
+      sDw[r] = r < n ? pw[ii] : 0.f;
     }
   }
-  // ---- dQ, dK (read key), dKt
-  T* dq = static_cast<T*>(ba.dq) + (b * a.T + t0) * HD + h * DK;
-  float* dKm = ba.dKm + (bh * a.Tpad + t0) * DK;
-  float* dKt = ba.dKt + (bh * a.Tpad + t0) * DK;
 #pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    floatx4 aq, ak, at;
-#pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-      aq[ii] = lam[ii] * A1[j][ii];
-      ak[ii] = -lam[ii] * A2[j][ii];
-      at[ii] = wr[ii] * A3[j][ii];
-    }
-    mma_tile<C>(aq, sdSqk + (16 * w) * LDT, LDT, sKtT + (16 * j) * LDT, LDT, lr, lg);
-    mma_tile<C>(ak, sdSkk + (16 * w) * LDT, LDT, sKtT + (16 * j) * LDT, LDT, lr, lg);
-    mma_tile<C>(at, sdSqkT + (16 * w) * LDT, LDT, sQT + (16 * j) * LDT, LDT, lr, lg);
-    mma_tile<C>(at, sdSkkT + (16 * w) * LDT, LDT, sKT + (16 * j) * LDT, LDT, lr, lg);
-#pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-      const int r = 16 * w + 4 * lg + ii, c = 16 * j + lr;
-      if (r < n) dq[r * HD + c] = from_f<T>(aq[ii]);
-      dKm[r * DK + c] = ak[ii];
-      dKt[r * DK + c] = at[ii];
-    }
-  }
+  for (int off = 32; off > 0; off >>= 1) red += __shfl_xor(red, off, 64);
+  if (l == 0) sRed[w] = red;
   __syncthreads();
   // ---- gate: dG_r, then the reverse in-chunk cumsum -> dg
   if (GATE == kGateScalar && w == 0) {
@@ -746,8 +768,8 @@ __device__ __forceinline__ void pc_body(const BwdArgs& ba, int64_t bh, int i, in
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int64_t kst = a.H * static_cast<int64_t>(DK);
   const T* kcol = static_cast<const T*>(a.k) + ((b * a.T + t0) * a.H + h) * DK + c;
-  const float* dkt = ba.dKt + (bh * a.Tpad + t0 + s0) * DK + c;
-  const float* dkm = ba.dKm + (bh * a.Tpad + t0 + s0) * DK + c;
+  const T* dkt = static_cast<const T*>(ba.dKt) + (bh * a.Tpad + t0 + s0) * DK + c;
+  const T* dkm = static_cast<const T*>(ba.dKm) + (bh * a.Tpad + t0 + s0) * DK + c;
   // loads: keys (rows past the end re-read the last row and are zeroed
   // below), write-key and read-key gradients (workspace rows cover the
   // padded chunk)
@@ -755,10 +777,10 @@ __device__ __forceinline__ void pc_body(const BwdArgs& ba, int64_t bh, int i, in
 #pragma unroll
   for (int j = 0; j < PCG; ++j) kv[j] = to_f(kcol[(FULL ? s0 + j : min(s0 + j, n - 1)) * kst]);
 #pragma unroll
-  for (int j = 0; j < PCG; ++j) gk[j] = dkt[j * DK];
+  for (int j = 0; j < PCG; ++j) gk[j] = to_f(dkt[j * DK]);
   if (FINAL) {
 #pragma unroll
-    for (int j = 0; j < PCG; ++j) km[j] = dkm[j * DK];
+    for (int j = 0; j < PCG; ++j) km[j] = to_f(dkm[j * DK]);
   }
   const float A_start = a.Abound[(bh * (a.NT + 1) + i) * DK + c];
   const float kap_chunk = FINAL ? ba.pcC[(bh * (a.NT + 1) + i + 1) * DK + c] : 0.f;
@@ -952,7 +974,7 @@ __global__ __launch_bounds__(256) void combine_dk(BwdArgs ba) {
   const int64_t tok = idx / DK;
   const int64_t h = tok % a.H, t = (tok / a.H) % a.T, b = tok / (a.H * a.T);
   const int64_t w = ((b * a.H + h) * a.Tpad + t) * DK + c;
-  const float km = ba.dKm[w], kt = ba.dKt[w];
+  const float km = to_f(static_cast<const T*>(ba.dKm)[w]), kt = to_f(static_cast<const T*>(ba.dKt)[w]);
   if (a.precond == kIdentity) {
     static_cast<T*>(ba.dk)[idx] = from_f<T>(km + kt);
   } else {
@@ -986,8 +1008,8 @@ BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate,
   L.dSkk = take(bh * nt * C * C * esz);
   L.dSkkT = take(bh * nt * C * C * esz);
   L.dGp = take(bh * tp * 4);
-  L.dKt = take(bh * tp * dk * 4);
-  L.dKm = take(bh * tp * dk * 4);
+  L.dKt = take(bh * tp * dk * esz);
+  L.dKm = take(bh * tp * dk * esz);
   L.pcL = take(bh * nt * dk * 4);
   L.pcC = take(bh * (nt + 1) * dk * 4);
   L.pcMu = take(bh * nt * 4);
@@ -1053,8 +1075,14 @@ static hipError_t launch_bwd_dims(const BwdArgs& ba, hipStream_t s, hipEvent_t c
   return sc ? launch_bwd_typed<T, 64, 64, kGateScalar>(ba, s, ev) : launch_bwd_typed<T, 64, 64, kGateNone>(ba, s, ev);
 }
 
-hipError_t launch_backward(const BwdArgs& ba, int io_bf16, hipStream_t s, hipEvent_t const* ev) {
-  hipError_t e = launch_forward_parts(ba.f, io_bf16, s, ev);
+hipError_t launch_backward(const BwdArgs& ba, int io_bf16, hipStream_t s, hipEvent_t const* ev,
+                           bool recompute) {
+  hipError_t e = hipSuccess;
+  if (recompute) {
+    e = launch_forward_parts(ba.f, io_bf16, s, ev);
+  } else if (ev) {   // no recompute: its stages are empty
+    for (int k = 0; k < 4 && e == hipSuccess; ++k) e = hipEventRecord(ev[k], s);
+  }
   if (e != hipSuccess) return e;
   return io_bf16 ? launch_bwd_dims<bf16>(ba, s, ev) : launch_bwd_f32(ba, s, ev);
 }

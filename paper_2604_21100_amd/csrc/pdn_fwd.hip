@@ -614,14 +614,14 @@ __device__ __forceinline__ void flush_slab_t(T* dst, int64_t ld, const T* src, i
   }
 }
 
-template <bool FULL, bool SAVE, typename T, int DK, int GATE>
+template <bool FULL, bool SAVE, bool OUT, typename T, int DK, int GATE>
 __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float4* vnext,
                                           floatx4 (&st)[DK / 64][2], const FwdArgs& a, int i,
                                           const ScanCtx& x, T* sH, T* sX, T* sE, T* sVt, T* sO) {
   constexpr int KK = DK / 32, CT = DK / 64;
   constexpr int LDH = DK + 8, LDE = C + 8;
   const int w = x.w, lr = x.lr, lg = x.lg;
-  if (!SAVE && i > 0) flush_output<T>(a, i - 1, C, sO, x);   // only full chunks precede this one
+  if (OUT && i > 0) flush_output<T>(a, i - 1, C, sO, x);   // only full chunks precede this one
   if (SAVE)  // chunk-start state S^T of this chunk, rows c, columns of the slab
     flush_slab_t<T>(static_cast<T*>(a.Hs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv, sH,
                     LDH, DK, x.tid);
@@ -636,7 +636,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
       for (int s = 0; s < 8; ++s) {
         const float e = fast_exp(f.gk[kk][s]);
         f.K[kk].set(s, f.K[kk].get(s) * e);
-        if (!SAVE) f.Q[kk].set(s, f.Q[kk].get(s) * e);
+        if (OUT) f.Q[kk].set(s, f.Q[kk].get(s) * e);
       }
   }
   // ---- (Lam K) S^T and (Lam Q) S^T;  X = V - (Lam K) S^T
@@ -657,12 +657,12 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       mma(accX[vt], f.K[kk], bH[vt][kk]);
-      if (!SAVE) mma(accO[vt], f.Q[kk], bH[vt][kk]);
+      if (OUT) mma(accO[vt], f.Q[kk], bH[vt][kk]);
     }
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
       accX[vt][ii] = to_f(vv[vt][ii]) - lam[ii] * accX[vt][ii];
-      if (!SAVE) accO[vt][ii] *= lam[ii];
+      if (OUT) accO[vt][ii] *= lam[ii];
     }
     st4<T>(sX + (16 * vt + lr) * LDE + 16 * w + 4 * lg, accX[vt][0], accX[vt][1], accX[vt][2],
            accX[vt][3]);
@@ -694,7 +694,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) fE[vt][k2] = ld8(sE + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg);
 #pragma unroll
-  for (int vt = 0; vt < 2 && !SAVE; ++vt) {
+  for (int vt = 0; vt < 2 && OUT; ++vt) {
     // P is causal: for rows < 32 its second slab is zero
     mma(accO[vt], f.P[0], fE[vt][0]);
     mma(accO[vt], f.P[1], fE[vt][1]);
@@ -721,9 +721,10 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
   lds_barrier();
 }
 
-// SAVE: the backward's recompute: write the chunk-start states and the X, E
-// rows instead of the output (queries and P are neither loaded nor used).
-template <typename T, int DK, int GATE, bool SAVE>
+// SAVE: also write the chunk-start states and the X, E rows the backward
+// reads.  OUT: compute and write the output (without it, queries and P are
+// neither loaded nor used: the backward's recompute).
+template <typename T, int DK, int GATE, bool SAVE, bool OUT>
 __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   constexpr int CT = DK / 64;       // state row tiles per wave
   constexpr int LDH = DK + 8, LDE = C + 8;
@@ -779,34 +780,34 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   ScanFrags<T, DK, GATE> f0, f1, f2;
   const int last = a.NT - 1;
   const int NF = static_cast<int>(a.T / C);   // full chunks
-  scan_load<!SAVE>(f0, a, 0, x);
-  scan_load<!SAVE>(f1, a, min(1, last), x);
+  scan_load<OUT>(f0, a, 0, x);
+  scan_load<OUT>(f1, a, min(1, last), x);
   stage_values<T>(f0.v, sVt, x.tid);
   __syncthreads();
   int i = 0;
   for (; i + 2 < NF; i += 3) {
-    scan_load<!SAVE>(f2, a, i + 2, x);
-    scan_step<true, SAVE>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
-    scan_load<!SAVE>(f0, a, min(i + 3, last), x);
-    scan_step<true, SAVE>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
-    scan_load<!SAVE>(f1, a, min(i + 4, last), x);
-    scan_step<true, SAVE>(f2, f0.v, st, a, i + 2, x, sH, sX, sE, sVt, sO);
+    scan_load<OUT>(f2, a, i + 2, x);
+    scan_step<true, SAVE, OUT>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_load<OUT>(f0, a, min(i + 3, last), x);
+    scan_step<true, SAVE, OUT>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
+    scan_load<OUT>(f1, a, min(i + 4, last), x);
+    scan_step<true, SAVE, OUT>(f2, f0.v, st, a, i + 2, x, sH, sX, sE, sVt, sO);
   }
   // f0, f1 hold chunks i, i + 1 (clamped to the last chunk)
   if (NF - i == 2) {
-    scan_load<!SAVE>(f2, a, min(i + 2, last), x);
-    scan_step<true, SAVE>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
-    scan_step<true, SAVE>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
+    scan_load<OUT>(f2, a, min(i + 2, last), x);
+    scan_step<true, SAVE, OUT>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE, OUT>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
     i += 2;
-    if (i < a.NT) scan_step<false, SAVE>(f2, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+    if (i < a.NT) scan_step<false, SAVE, OUT>(f2, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
   } else if (NF - i == 1) {
-    scan_step<true, SAVE>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE, OUT>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
     i += 1;
-    if (i < a.NT) scan_step<false, SAVE>(f1, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+    if (i < a.NT) scan_step<false, SAVE, OUT>(f1, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
   } else if (i < a.NT) {
-    scan_step<false, SAVE>(f0, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<false, SAVE, OUT>(f0, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
   }
-  if (!SAVE) flush_output<T>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
+  if (OUT) flush_output<T>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
   if (a.S_T) {
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
@@ -865,7 +866,9 @@ static hipError_t launch_k2_prec(const FwdArgs& a, hipStream_t s) {
   }
 }
 
-template <typename T, int DK>
+// SAVE: the training forward (k2 in backward mode, k3 also saving the
+// chunk states and X, E rows); scalar gate or none
+template <typename T, int DK, bool SAVE>
 static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* ev) {
   hipError_t e;
   auto mark = [&](int i) { return ev ? hipEventRecord(ev[i], s) : hipSuccess; };
@@ -879,9 +882,12 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
   }
   if ((e = mark(1)) != hipSuccess) return e;
   switch (a.gate) {
-    case kGateNone: e = launch_k2_prec<T, DK, kGateNone>(a, s); break;
-    case kGateScalar: e = launch_k2_prec<T, DK, kGateScalar>(a, s); break;
-    default: e = launch_k2_prec<T, DK, kGateChannel>(a, s); break;
+    case kGateNone: e = launch_k2_prec<T, DK, kGateNone, SAVE>(a, s); break;
+    case kGateScalar: e = launch_k2_prec<T, DK, kGateScalar, SAVE>(a, s); break;
+    default:
+      if constexpr (SAVE) e = hipErrorInvalidValue;
+      else e = launch_k2_prec<T, DK, kGateChannel>(a, s);
+      break;
   }
   if (e != hipSuccess) return e;
   if ((e = mark(2)) != hipSuccess) return e;
@@ -889,11 +895,13 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
   const unsigned grid = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
   switch (a.gate) {
     case kGateNone:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, false>), dim3(grid), dim3(256), 0, s, a); break;
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, SAVE, true>), dim3(grid), dim3(256), 0, s, a); break;
     case kGateScalar:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, false>), dim3(grid), dim3(256), 0, s, a); break;
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, SAVE, true>), dim3(grid), dim3(256), 0, s, a); break;
     default:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, false>), dim3(grid), dim3(256), 0, s, a); break;
+      if constexpr (SAVE) return hipErrorInvalidValue;
+      else hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, false, true>), dim3(grid), dim3(256), 0, s, a);
+      break;
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return mark(3);
@@ -921,9 +929,9 @@ static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s, hipEvent_t c
   const int64_t nslab = a.dv / BV;
   const unsigned grid = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
   if (a.gate == kGateScalar)
-    hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, true>), dim3(grid), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, true, false>), dim3(grid), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, true>), dim3(grid), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, true, false>), dim3(grid), dim3(256), 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return mark(3);
 }
@@ -933,7 +941,7 @@ hipError_t launch_forward_parts(const FwdArgs& a, int io_bf16, hipStream_t s, hi
   return launch_recompute<float, 64>(a, s, ev);
 }
 
-hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev) {
+hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev, bool train) {
   if (a.BH == 0 || a.T == 0) {
     // nothing to time: the stage events still mark the (empty) stages
     if (ev)
@@ -948,10 +956,14 @@ hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent
                        a, nS, nA);
     return hipGetLastError();
   }
-  if (io_bf16) {
-    return a.dk == 64 ? launch_all<bf16, 64>(a, s, ev) : launch_all<bf16, 128>(a, s, ev);
+  if (train) {   // the host admits fp32 io only with d_k = d_v = 64 here
+    if (io_bf16) return a.dk == 64 ? launch_all<bf16, 64, true>(a, s, ev) : launch_all<bf16, 128, true>(a, s, ev);
+    return launch_all<float, 64, true>(a, s, ev);
   }
-  return a.dk == 64 ? launch_all<float, 64>(a, s, ev) : launch_all<float, 128>(a, s, ev);
+  if (io_bf16) {
+    return a.dk == 64 ? launch_all<bf16, 64, false>(a, s, ev) : launch_all<bf16, 128, false>(a, s, ev);
+  }
+  return a.dk == 64 ? launch_all<float, 64, false>(a, s, ev) : launch_all<float, 128, false>(a, s, ev);
 }
 
 }  // namespace pdn

@@ -180,14 +180,36 @@ pdn_status pdn_workspace_size(const pdn_problem* p, int with_bwd, size_t* bytes)
   return PDN_OK;
 }
 
+// Forward intermediates the backward kernels read: the forward workspace
+// plus the residual arrays of the backward layout.
+static void set_forward_ws(pdn::FwdArgs& a, const pdn::WsLayout& L, const pdn_problem* p, char* w) {
+  if (p->precond == PDN_PRECOND_SQUASH) {
+    a.sumL = reinterpret_cast<float*>(w + L.sumL);
+    a.sumD = reinterpret_cast<float*>(w + L.sumD);
+    a.Abound = reinterpret_cast<float*>(w + L.Abound);
+  }
+  a.KtG = w + L.KtG;
+  a.Tm = w + L.Tm;
+  a.Pm = w + L.Pm;
+  if (p->gate != PDN_GATE_NONE) a.G = reinterpret_cast<float*>(w + L.G);
+}
+
+static void set_residuals(pdn::FwdArgs& f, const pdn::BwdWsLayout& L, char* w) {
+  f.Hs = w + L.Hs; f.Xr = w + L.Xr; f.Er = w + L.Er; f.PtT = w + L.PtT; f.MtT = w + L.MtT;
+  f.Ktr = w + L.Ktr; f.Kw = w + L.Kw; f.QlT = w + L.QlT; f.KnT = w + L.KnT;
+}
+
+// train: the training forward (also leaves the backward's intermediates in
+// the workspace, which then has the backward's size)
 static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out* out,
                                  void* ws, size_t ws_bytes, void* hip_stream,
-                                 hipEvent_t const* ev) {
+                                 hipEvent_t const* ev, bool train) {
   Sizes s;
   pdn_status st = check_problem(p, &s);
   if (st != PDN_OK) return st;
   std::vector<Buf> ins;
   if ((st = check_inputs(p, in, s, &ins)) != PDN_OK) return st;
+  if (train && (st = check_bwd_support(p)) != PDN_OK) return st;
   if (!out) return PDN_ERR_NULL;
   if (s.tok > 0 && !out->o) return PDN_ERR_NULL;
   if (p->precond != PDN_PRECOND_SQUASH && out->A_T) return PDN_ERR_VALUE;
@@ -196,12 +218,15 @@ static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn
     if (x.p && !aligned16(x.p)) return PDN_ERR_ALIGN;
   const pdn::WsLayout L = pdn::fwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, s.esz, p->gate,
                                              p->precond);
+  const pdn::BwdWsLayout LB =
+      pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond);
+  const size_t need_bytes = train ? LB.total : L.total;
   const bool need_ws = s.tok > 0;
   // the whole declared workspace range must be disjoint from inputs/outputs;
   // its size is checked last
   if ((st = check_aliasing(ins, outs, Buf{ws, need_ws ? static_cast<int64_t>(ws_bytes) : 0})) != PDN_OK)
     return st;
-  if (need_ws && (!ws || ws_bytes < L.total || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0))
+  if (need_ws && (!ws || ws_bytes < need_bytes || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0))
     return PDN_ERR_WORKSPACE;
 
   pdn::FwdArgs a{};
@@ -218,24 +243,17 @@ static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn
   a.o = out->o; a.S_T = out->S_T; a.A_T = out->A_T;
   char* w = static_cast<char*>(ws);
   if (need_ws) {
-    if (p->precond == PDN_PRECOND_SQUASH) {
-      a.sumL = reinterpret_cast<float*>(w + L.sumL);
-      a.sumD = reinterpret_cast<float*>(w + L.sumD);
-      a.Abound = reinterpret_cast<float*>(w + L.Abound);
-    }
-    a.KtG = w + L.KtG;
-    a.Tm = w + L.Tm;
-    a.Pm = w + L.Pm;
-    if (p->gate != PDN_GATE_NONE) a.G = reinterpret_cast<float*>(w + L.G);
+    set_forward_ws(a, L, p, w);
+    if (train) set_residuals(a, LB, w);
   }
   const hipError_t e =
-      pdn::launch_forward(a, p->io == PDN_BF16, static_cast<hipStream_t>(hip_stream), ev);
+      pdn::launch_forward(a, p->io == PDN_BF16, static_cast<hipStream_t>(hip_stream), ev, train);
   return e == hipSuccess ? PDN_OK : PDN_ERR_HIP;
 }
 
 pdn_status pdn_chunk_fwd(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out* out, void* ws,
                          size_t ws_bytes, void* hip_stream) {
-  return chunk_fwd_impl(p, in, out, ws, ws_bytes, hip_stream, nullptr);
+  return chunk_fwd_impl(p, in, out, ws, ws_bytes, hip_stream, nullptr, false);
 }
 
 pdn_status pdn_chunk_fwd_events(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out* out,
@@ -246,12 +264,13 @@ pdn_status pdn_chunk_fwd_events(const pdn_problem* p, const pdn_inputs* in, pdn_
   for (int i = 0; i < n_events; ++i)
     if (!stage_events[i]) return PDN_ERR_NULL;
   return chunk_fwd_impl(p, in, out, ws, ws_bytes, hip_stream,
-                        reinterpret_cast<hipEvent_t const*>(stage_events));
+                        reinterpret_cast<hipEvent_t const*>(stage_events), false);
 }
 
+// saved: the forward intermediates are in ws already (training forward)
 static pdn_status chunk_bwd_impl(const pdn_problem* p, const pdn_inputs* in, const void* dO,
                                  const float* dS_T, pdn_bwd_out* out, void* ws, size_t ws_bytes,
-                                 void* hip_stream, hipEvent_t const* ev) {
+                                 void* hip_stream, hipEvent_t const* ev, bool saved) {
   Sizes s;
   pdn_status st = check_problem(p, &s);
   if (st != PDN_OK) return st;
@@ -313,15 +332,8 @@ static pdn_status chunk_bwd_impl(const pdn_problem* p, const pdn_inputs* in, con
   f.log_a_scale = in->log_a_scale; f.A0 = in->A0; f.S0 = in->S0;
   f.o = nullptr; f.S_T = nullptr; f.A_T = nullptr;
   char* w = static_cast<char*>(ws);
-  if (sq) {
-    f.sumL = reinterpret_cast<float*>(w + L.f.sumL);
-    f.sumD = reinterpret_cast<float*>(w + L.f.sumD);
-    f.Abound = reinterpret_cast<float*>(w + L.f.Abound);
-  }
-  f.KtG = w + L.f.KtG; f.Tm = w + L.f.Tm; f.Pm = w + L.f.Pm;
-  if (p->gate != PDN_GATE_NONE) f.G = reinterpret_cast<float*>(w + L.f.G);
-  f.Hs = w + L.Hs; f.Xr = w + L.Xr; f.Er = w + L.Er; f.PtT = w + L.PtT; f.MtT = w + L.MtT;
-  f.Ktr = w + L.Ktr; f.Kw = w + L.Kw; f.QlT = w + L.QlT; f.KnT = w + L.KnT;
+  set_forward_ws(f, L.f, p, w);
+  set_residuals(f, L, w);
   a.dO = dO; a.dS_T = dS_T;
   a.dq = out->dq; a.dk = out->dk; a.dv = out->dv; a.dbeta = out->dbeta; a.dg = out->dg;
   a.dS0 = out->dS0; a.dbeta_p = out->dbeta_p; a.dg_p = out->dg_p; a.dlog_a_scale = out->dlog_a_scale;
@@ -329,19 +341,19 @@ static pdn_status chunk_bwd_impl(const pdn_problem* p, const pdn_inputs* in, con
   a.dHs = w + L.dHs; a.Zr = w + L.Zr;
   a.dSqk = w + L.dSqk; a.dSqkT = w + L.dSqkT; a.dSkk = w + L.dSkk; a.dSkkT = w + L.dSkkT;
   a.dGp = reinterpret_cast<float*>(w + L.dGp);
-  a.dKt = reinterpret_cast<float*>(w + L.dKt);
-  a.dKm = reinterpret_cast<float*>(w + L.dKm);
+  a.dKt = w + L.dKt;
+  a.dKm = w + L.dKm;
   a.pcL = reinterpret_cast<float*>(w + L.pcL);
   a.pcC = reinterpret_cast<float*>(w + L.pcC);
   a.pcMu = reinterpret_cast<float*>(w + L.pcMu);
-  const hipError_t he = pdn::launch_backward(a, p->io == PDN_BF16, stream, ev);
+  const hipError_t he = pdn::launch_backward(a, p->io == PDN_BF16, stream, ev, !saved);
   return he == hipSuccess ? PDN_OK : PDN_ERR_HIP;
 }
 
 pdn_status pdn_chunk_bwd(const pdn_problem* p, const pdn_inputs* in, const void* dO,
                          const float* dS_T, pdn_bwd_out* out, void* ws, size_t ws_bytes,
                          void* hip_stream) {
-  return chunk_bwd_impl(p, in, dO, dS_T, out, ws, ws_bytes, hip_stream, nullptr);
+  return chunk_bwd_impl(p, in, dO, dS_T, out, ws, ws_bytes, hip_stream, nullptr, false);
 }
 
 pdn_status pdn_chunk_bwd_events(const pdn_problem* p, const pdn_inputs* in, const void* dO,
@@ -352,7 +364,34 @@ pdn_status pdn_chunk_bwd_events(const pdn_problem* p, const pdn_inputs* in, cons
   for (int i = 0; i < n_events; ++i)
     if (!stage_events[i]) return PDN_ERR_NULL;
   return chunk_bwd_impl(p, in, dO, dS_T, out, ws, ws_bytes, hip_stream,
-                        reinterpret_cast<hipEvent_t const*>(stage_events));
+                        reinterpret_cast<hipEvent_t const*>(stage_events), false);
+}
+
+// stage_events: NULL (n_events 0) or n_events == n events, all non-NULL
+static pdn_status check_events(void* const* ev, int n_events, int n) {
+  if (!ev) return n_events == 0 ? PDN_OK : PDN_ERR_NULL;
+  if (n_events != n) return PDN_ERR_VALUE;
+  for (int i = 0; i < n_events; ++i)
+    if (!ev[i]) return PDN_ERR_NULL;
+  return PDN_OK;
+}
+
+pdn_status pdn_chunk_fwd_train(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out* out,
+                               void* ws, size_t ws_bytes, void* hip_stream,
+                               void* const* stage_events, int n_events) {
+  const pdn_status st = check_events(stage_events, n_events, PDN_FWD_STAGE_EVENTS);
+  if (st != PDN_OK) return st;
+  return chunk_fwd_impl(p, in, out, ws, ws_bytes, hip_stream,
+                        reinterpret_cast<hipEvent_t const*>(stage_events), true);
+}
+
+pdn_status pdn_chunk_bwd_train(const pdn_problem* p, const pdn_inputs* in, const void* dO,
+                               const float* dS_T, pdn_bwd_out* out, void* ws, size_t ws_bytes,
+                               void* hip_stream, void* const* stage_events, int n_events) {
+  const pdn_status st = check_events(stage_events, n_events, PDN_BWD_STAGE_EVENTS);
+  if (st != PDN_OK) return st;
+  return chunk_bwd_impl(p, in, dO, dS_T, out, ws, ws_bytes, hip_stream,
+                        reinterpret_cast<hipEvent_t const*>(stage_events), true);
 }
 
 }  // extern "C"

@@ -85,8 +85,8 @@ struct BwdArgs {
   void* dSkk;     // [BH, NT, C, C] io    d(K Kt^T)
   void* dSkkT;
   float* dGp;     // [BH, Tpad] fp32      gate-prefix gradient from the C x C terms
-  float* dKt;     // [BH, Tpad, dk] fp32  gradient of the write key
-  float* dKm;     // [BH, Tpad, dk] fp32  gradient of the read key (main recurrence)
+  void* dKt;      // [BH, Tpad, dk] io    gradient of the write key
+  void* dKm;      // [BH, Tpad, dk] io    gradient of the read key (main recurrence)
   float* pcL;     // [BH, NT, dk]         preconditioner: in-chunk adjoint at chunk start
   float* pcC;     // [BH, NT + 1, dk]     preconditioner: adjoint carried into each chunk
   float* pcMu;    // [BH, NT]             preconditioner: partial d mu
@@ -107,13 +107,15 @@ struct BwdWsLayout {
 BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond);
 
 // ev: NULL or 8 events recorded at the stage boundaries (see
-// pdn_chunk_bwd_events)
+// pdn_chunk_bwd_events).  recompute = false: the forward intermediates are
+// already in the workspace (left there by the training forward).
 hipError_t launch_backward(const BwdArgs& a, int io_bf16, hipStream_t stream,
-                           hipEvent_t const* ev = nullptr);
+                           hipEvent_t const* ev = nullptr, bool recompute = true);
 
 // ev: NULL or 4 events recorded at the stage boundaries (see
-// pdn_chunk_fwd_events)
+// pdn_chunk_fwd_events).  train: also leave the backward's intermediates in
+// the workspace (a's backward fields set).
 hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t stream,
-                          hipEvent_t const* ev = nullptr);
+                          hipEvent_t const* ev = nullptr, bool train = false);
 
 }  // namespace pdn

@@ -205,3 +205,43 @@ def test_one_hip_runtime_in_process():
                        capture_output=True, text=True, timeout=300)
     assert r.returncode == 0, r.stderr
     assert r.stdout.strip() == "1", r.stdout
+
+
+def test_training_pair_validation():
+    """The training forward needs the backward's workspace and support; no
+    call reaches a launch (the workspace is always short)."""
+    vp = ctypes.c_void_p
+    lib = pdn._lib
+    out = pdn.FwdOut(A * 20, A * 21, A * 22)
+    p = _prob()
+    need_f = pdn.pdn_workspace_size(p, False)
+    need_b = pdn.pdn_workspace_size(p, True)
+    assert need_b > need_f
+    # enough for the plain forward, one byte short for the training forward
+    assert lib.pdn_chunk_fwd_train(
+        ctypes.byref(p), ctypes.byref(_inputs()), ctypes.byref(out), A * 64,
+        need_b - 1, None, None, 0) == pdn.PDN_ERR_WORKSPACE
+    # the backward's restrictions apply
+    pc = _prob(gate="channel")
+    assert lib.pdn_chunk_fwd_train(
+        ctypes.byref(pc), ctypes.byref(_inputs()), ctypes.byref(out), A * 64,
+        0, None, None, 0) == pdn.PDN_ERR_UNSUPPORTED
+    pf = _prob(io="f32", dk=128, dv=64)
+    assert lib.pdn_chunk_fwd_train(
+        ctypes.byref(pf), ctypes.byref(_inputs()), ctypes.byref(out), A * 64,
+        0, None, None, 0) == pdn.PDN_ERR_UNSUPPORTED
+    # event arrays: NULL needs n_events 0; a wrong count is rejected
+    ev = (vp * 4)(*([A * 40] * 4))
+    assert lib.pdn_chunk_fwd_train(
+        ctypes.byref(p), ctypes.byref(_inputs()), ctypes.byref(out), A * 64,
+        0, None, None, 4) == pdn.PDN_ERR_NULL
+    assert lib.pdn_chunk_fwd_train(
+        ctypes.byref(p), ctypes.byref(_inputs()), ctypes.byref(out), A * 64,
+        0, None, ev, 3) == pdn.PDN_ERR_VALUE
+    bo = pdn.BwdOut(*([None] * 11))
+    assert lib.pdn_chunk_bwd_train(
+        ctypes.byref(p), ctypes.byref(_inputs()), A * 30, None,
+        ctypes.byref(bo), A * 64, 0, None, ev, 4) == pdn.PDN_ERR_VALUE
+    assert lib.pdn_chunk_bwd_train(
+        ctypes.byref(pc), ctypes.byref(_inputs()), A * 30, None,
+        ctypes.byref(bo), A * 64, 0, None, None, 0) == pdn.PDN_ERR_UNSUPPORTED
