@@ -87,15 +87,12 @@ def algorithmic_per_token_head(spec, train=False):
         "bwd_state_adjoint_scan": (4 * C * dv + 6 * dk * dv,
                                    2 * e * C + 3 * e * dk + e * dv + 4
                                    + 4 / C + st + 2 * e * dv),
-        # p1: read dO, E, Z, X, q, kt, k, beta, gate prefix; write the four
-        # masked C x C adjoints (and transposes), dbeta, dG partial
-        "bwd_chunk_cc": (4 * C * dv + 4 * C * dk,
-                         4 * e * dv + 3 * e * dk + 4 + gb + 4 * e * C + 8),
-        # p2: read dO, dX, E, S, dS', kt, q, k, the C x C adjoints, gate
-        # prefix, dG partial; write dq, dk (read key) and dkt (io), dg
-        "bwd_chunk_grads": (6 * dk * dv + 8 * C * dk,
-                            3 * e * dv + 2 * st + 3 * e * dk + 4 * e * C
-                            + gb + 4 + 3 * e * dk + 4),
+        # p12: read dO, Z, V, E, q, k, kt, the chunk-start state and its
+        # adjoint, beta, gate prefix; write dq, dk (read key) and dkt (io),
+        # dbeta, dg
+        "bwd_chunk_grads": (4 * C * dv + 12 * C * dk + 6 * dk * dv,
+                            4 * e * dv + 3 * e * dk + 2 * st + 4 + gb
+                            + 3 * e * dk + 8),
         # pc: read k, dk (read key), dkt, betaP, gP, chunk-start A; write dk,
         # dbetaP, dgP
         "bwd_precond_reverse": (10 * dk,
@@ -114,8 +111,7 @@ KERNELS = {
     "bwd_chunk_prep": "k2_chunk_prep (backward mode)",
     "bwd_state_save_scan": "k3_chunk_scan (saving mode)",
     "bwd_state_adjoint_scan": "r1_state_adjoint",
-    "bwd_chunk_cc": "p1_chunk_cc",
-    "bwd_chunk_grads": "p2_chunk_grads",
+    "bwd_chunk_grads": "p12_chunk_grads",
     "bwd_precond_reverse": "pc_chunk+pc_carry+pc_chunk+pc_mu",
 }
 

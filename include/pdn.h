@@ -173,11 +173,10 @@ pdn_status pdn_chunk_bwd(const pdn_problem* problem, const pdn_inputs* in,
  *   [2] after the per-chunk prep recompute (k2, backward mode)
  *   [3] after the state-saving forward scan (k3)
  *   [4] after the reverse state-adjoint scan (r1)
- *   [5] after the per-chunk C x C adjoint algebra (p1)
- *   [6] after the per-chunk q/k/kt/gate gradients (p2)
- *   [7] after the preconditioner's reverse scan (pc_*) or the key combine
+ *   [5] after the per-chunk adjoints and gradients (p12)
+ *   [6] after the preconditioner's reverse scan (pc_*) or the key combine
  * Results are identical to pdn_chunk_bwd. */
-#define PDN_BWD_STAGE_EVENTS 8
+#define PDN_BWD_STAGE_EVENTS 7
 pdn_status pdn_chunk_bwd_events(const pdn_problem* problem, const pdn_inputs* in,
                                 const void* dO, const float* dS_T, pdn_bwd_out* out,
                                 void* ws, size_t ws_bytes, void* hip_stream,

@@ -130,11 +130,10 @@ EXPORTED = ("pdn_workspace_size", "pdn_chunk_fwd", "pdn_chunk_fwd_events",
             "pdn_chunk_bwd", "pdn_chunk_bwd_events", "pdn_chunk_fwd_train",
             "pdn_chunk_bwd_train", "pdn_status_string", "pdn_abi_version")
 FWD_STAGE_EVENTS = 4   # PDN_FWD_STAGE_EVENTS
-BWD_STAGE_EVENTS = 8   # PDN_BWD_STAGE_EVENTS
+BWD_STAGE_EVENTS = 7   # PDN_BWD_STAGE_EVENTS
 FWD_STAGES = ("precond", "chunk_prep", "chunk_scan")
 BWD_STAGES = ("bwd_precond_recompute", "bwd_chunk_prep", "bwd_state_save_scan",
-              "bwd_state_adjoint_scan", "bwd_chunk_cc", "bwd_chunk_grads",
-              "bwd_precond_reverse")
+              "bwd_state_adjoint_scan", "bwd_chunk_grads", "bwd_precond_reverse")
 
 
 class PdnError(RuntimeError):

@@ -22,14 +22,15 @@
 // -Z E^T, one C x C product of stored rows, so
 //   dAt = strict_lower(-Z E^T),  dSkk = Gam o Diag(beta) dAt
 //   dbeta_t = sum_v Z_tv X_tv + sum_{s<t} dAt_ts (Gam o K Kt^T)_ts
+// with sum_v Z_tv X_tv = Z_t . V_t - lam_t K_t . (Z S)_t, where Z S is the
+// product p2 forms anyway (dX S = Diag(beta) Z S), so X is never stored.
 // plus the gate terms (gradients of lam, w, lam_C and Gam, reverse-summed
 // over the chunk) and the preconditioner's reverse scan.
 //
 //   r1_state_adjoint   sequential over chunks (reverse): dS^T carry, dE, Z,
 //                      dX (= dv)
-//   p1_chunk_cc        per chunk: the C x C adjoints (dSqk, dSkk, dbeta,
-//                      gate terms of Gam)
-//   p2_chunk_grads     per chunk: dq, dk, dkt, dg
+//   p12_chunk_grads    per chunk: the C x C adjoints (dSqk, dSkk), dq, the
+//                      read- and write-key gradients, dbeta, dg
 //   pc_*               preconditioner: reverse scan over tokens of the
 //                      diagonal Gram recurrence (dk, dbetaP, dgP, dlogAScale,
 //                      dA0)
@@ -350,23 +351,67 @@ __device__ __forceinline__ void stage_rows(T* dst, const T* src, int tid) {
   }
 }
 
-// Per chunk: four C x C products of stored rows,
-//   dP = dO E^T,  dLn = Z E^T (dL = -dLn),  Sqk = Q Kt^T,  Skk = K Kt^T,
-// and their elementwise adjoint algebra.  Wave w owns rows 16w .. 16w + 15
-// (output tiles j <= w: every product is causal or strictly causal), so its
-// A operands (dO, Z, Q, K and the X rows of the beta dot product) are
-// private and load straight from memory into fragments; the shared B
-// operands (E and Kt rows) are staged once in LDS.  Rows past the sequence
-// end re-read the last row; their dP rows are masked, every other product
-// of them meets a zero factor (Z and beta vanish there).
+// ------------------------------------------------------------ p12
+// Per chunk, every gradient after the reverse scan except the
+// preconditioner's, in one pass over the chunk's rows:
+//   phase A  dP = dO E^T, dLn = Z E^T (dL = -dLn), Sqk = Q Kt^T,
+//            Skk = K Kt^T and their elementwise adjoint algebra: dSqk,
+//            dSkk, the At term of dbeta, Z . V, the Gam terms of dG
+//   phase B  (HC key columns at a time)
+//            A1 = dO_s S, A2' = Z S, A3 = E dS'       (C x dk, over dv;
+//            dX S = Diag(beta) A2')
+//            dq = Diag(lam) A1 + dSqk Kt,  dK = -Diag(lam beta) A2' + dSkk Kt,
+//            dKt = Diag(w) A3 + dSqk^T Q + dSkk^T K
+//   then     dbeta's T term -lam K . A2', dG and its reverse cumsum -> dg
+// Wave w owns rows 16w .. 16w + 15.  Its A operands (dO, Z, E, V, Q, K rows)
+// are private and load straight into fragments; shared B operands (E and Kt
+// rows; the chunk-start state and its adjoint as rows [c][v]; Kt, Q, K
+// transposed to [c][t]) are staged in LDS.  The C x C adjoints pass from
+// the C accumulator layout to A fragments (rows and, across waves,
+// transposed rows) through LDS once, then stay in registers.  Token rows
+// past the sequence end re-read the last row: their dP rows are masked,
+// their other products meet a zero factor (Z and beta vanish there), and
+// their outputs are not stored.
+template <typename T, int DK, int DV>
+struct P12Smem {
+  static constexpr int HC = 64;                 // key columns per phase-B pass
+  static constexpr int LDE = DV + 8, LDK = DK + 8, LDV = DV + 8, LDT = C + 8;
+  static constexpr size_t kA = sizeof(T) * (C * LDE + C * LDK + 4 * C * LDT);
+  static constexpr size_t kB = sizeof(T) * (2 * HC * LDV + 3 * HC * LDT);
+  static constexpr size_t kMain = kA > kB ? kA : kB;
+  static constexpr size_t kTotal = kMain + sizeof(float) * (12 * C + 4);
+};
+
 template <typename T, int DK, int DV, int GATE>
-__global__ __launch_bounds__(256) void p1_chunk_cc(BwdArgs ba) {
-  constexpr int LDE = DV + 8, LDK = DK + 8;
-  constexpr int KV = DV / 32, KD = DK / 32;
+__global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
+  using SM = P12Smem<T, DK, DV>;
+  constexpr int HC = SM::HC, LDE = SM::LDE, LDK = SM::LDK, LDV = SM::LDV, LDT = SM::LDT;
+  constexpr int KV = DV / 32, KD = DK / 32, NPASS = DK / HC;
   constexpr uint32_t E = sizeof(T);
-  __shared__ __attribute__((aligned(16))) T sE[C * LDE];
-  __shared__ __attribute__((aligned(16))) T sKt[C * LDK];
-  __shared__ float sG[C], sBeta[C], sDb[2][C], sRs[C], sCs[4][C];
+  __shared__ __attribute__((aligned(16))) char smem[SM::kTotal];
+  // phase A
+  T* sE = reinterpret_cast<T*>(smem);
+  T* sKt = sE + C * LDE;
+  T* sSq = sKt + C * LDK;     // dSqk rows [r][t]
+  T* sSk = sSq + C * LDT;     // dSkk rows
+  T* sSqT = sSk + C * LDT;    // dSqk^T rows [t][r]
+  T* sSkT = sSqT + C * LDT;   // dSkk^T rows
+  // phase B (reuses the same memory)
+  T* sS = reinterpret_cast<T*>(smem);   // S^T rows c0 .. c0 + HC - 1
+  T* sdS = sS + HC * LDV;               // dS'^T rows
+  T* sKtT = sdS + HC * LDV;
+  T* sQT = sKtT + HC * LDT;
+  T* sKT = sQT + HC * LDT;
+  float* sG = reinterpret_cast<float*>(smem + SM::kMain);
+  float* sBeta = sG + C;
+  float* sDb = sBeta + C;    // At term of dbeta
+  float* sZV = sDb + C;      // Z_r . V_r
+  float* sRs = sZV + C;      // row sums of the Gam products, then dG from them
+  float* sCs = sRs + C;      // [4][C] their column sums per wave
+  float* sDl = sCs + 4 * C;  // d lam_r
+  float* sDw = sDl + C;      // d w_r
+  float* sKZ = sDw + C;      // K_r . A2'_r
+  float* sRed = sKZ + C;     // 4 wave partials of sum(dS' o S)
 
   const FwdArgs& a = ba.f;
   const int64_t blk = blockIdx.x;
@@ -377,210 +422,154 @@ __global__ __launch_bounds__(256) void p1_chunk_cc(BwdArgs ba) {
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
   const int64_t HV = a.H * (int64_t)DV, HD = a.H * (int64_t)DK;
-  const int64_t cc = (bh * a.NT + i) * (int64_t)(C * C);
   const int64_t rv = (bh * a.Tpad + t0) * DV, rk = (bh * a.Tpad + t0) * DK;
+  const int64_t cs = (bh * a.NT + i) * (int64_t)DK * DV;
 
-  // ---- A operands of row 16w + lr (wave-private), issued first
+  // ---- A operands of row ra (wave-private)
   const int ra = 16 * w + lr;
   const uint32_t rc = static_cast<uint32_t>(min(ra, n - 1));
-  Frag8<T> fO[KV], fZ[KV], fX[KV], fQ[KD], fK[KD];
+  Frag8<T> fO[KV], fZ[KV], fE[KV];
+  Frag8<T> fV[KV], fQ[KD], fK[KD];    // phase A only
+  const T* dob = static_cast<const T*>(ba.dO) + (b * a.T + t0) * HV + h * DV;
+  const T* eb = static_cast<const T*>(a.Er) + rv;
   {
-    const T* dob = static_cast<const T*>(ba.dO) + (b * a.T + t0) * HV + h * DV;
+    const T* vb = static_cast<const T*>(a.v) + (b * a.T + t0) * HV + h * DV;
     const T* zb = static_cast<const T*>(ba.Zr) + rv;
-    const T* xb = static_cast<const T*>(a.Xr) + rv;
     const T* qb = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
     const T* kb = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
 #pragma unroll
-    for (int kk = 0; kk < KV; ++kk) {
-      fO[kk] = ld8(at_bytes(dob, (rc * static_cast<uint32_t>(HV) + 32 * kk + 8 * lg) * E));
-      fZ[kk] = ld8(at_bytes(zb, (static_cast<uint32_t>(ra * DV) + 32 * kk + 8 * lg) * E));
-      fX[kk] = ld8(at_bytes(xb, (static_cast<uint32_t>(ra * DV) + 32 * kk + 8 * lg) * E));
+    for (int kk = 0; kk < KD; ++kk) {
+      const uint32_t o = (rc * static_cast<uint32_t>(HD) + 32 * kk + 8 * lg) * E;
+      fQ[kk] = ld8(at_bytes(qb, o));
+      fK[kk] = ld8(at_bytes(kb, o));
     }
 #pragma unroll
-    for (int kk = 0; kk < KD; ++kk) {
-      fQ[kk] = ld8(at_bytes(qb, (rc * static_cast<uint32_t>(HD) + 32 * kk + 8 * lg) * E));
-      fK[kk] = ld8(at_bytes(kb, (rc * static_cast<uint32_t>(HD) + 32 * kk + 8 * lg) * E));
+    for (int kk = 0; kk < KV; ++kk) {
+      const uint32_t o = (rc * static_cast<uint32_t>(HV) + 32 * kk + 8 * lg) * E;
+      const uint32_t ow = (static_cast<uint32_t>(ra * DV) + 32 * kk + 8 * lg) * E;
+      fO[kk] = ld8(at_bytes(dob, o));
+      fV[kk] = ld8(at_bytes(vb, o));
+      fZ[kk] = ld8(at_bytes(zb, ow));
     }
   }
-  // ---- shared B operands and per-row scalars
-  stage_rows<T, DV>(sE, static_cast<const T*>(a.Er) + rv, tid);
+  // ---- phase A: shared B operands (E, Kt rows) and per-row scalars
+  stage_rows<T, DV>(sE, eb, tid);
   stage_rows<T, DK>(sKt, static_cast<const T*>(a.Ktr) + rk, tid);
   if (tid < C) {
     sG[tid] = GATE == kGateScalar ? a.G[bh * a.Tpad + t0 + tid] : 0.f;
     sBeta[tid] = tid < n ? a.beta[(b * a.T + t0 + tid) * a.H + h] : 0.f;
   }
   __syncthreads();
-
-  // ---- dbeta through T: sum_v Z_rv X_rv for row ra
   {
-    float dz = 0.f;
+    // Z_r . V_r for row ra (Z vanishes on rows past the end)
+    float zv = 0.f;
 #pragma unroll
     for (int kk = 0; kk < KV; ++kk)
 #pragma unroll
-      for (int s2 = 0; s2 < 8; ++s2) dz += fZ[kk].get(s2) * fX[kk].get(s2);
-    dz += __shfl_xor(dz, 16, 64);
-    dz += __shfl_xor(dz, 32, 64);
-    if (lg == 0) sDb[0][ra] = dz;
+      for (int s2 = 0; s2 < 8; ++s2) zv += fZ[kk].get(s2) * fV[kk].get(s2);
+    zv += __shfl_xor(zv, 16, 64);
+    zv += __shfl_xor(zv, 32, 64);
+    if (lg == 0) sZV[ra] = zv;
   }
-  // ---- the four products, tiles j <= w
-  floatx4 dP[4], dL[4], Sqk[4], Skk[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    dP[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    dL[j] = dP[j];
-    Sqk[j] = dP[j];
-    Skk[j] = dP[j];
-    if (j <= w) {
-#pragma unroll
-      for (int kk = 0; kk < KV; ++kk) {
-        const Frag8<T> fe = ld8(sE + (16 * j + lr) * LDE + 32 * kk + 8 * lg);
-        mma(dP[j], fO[kk], fe);
-        mma(dL[j], fZ[kk], fe);
-      }
-#pragma unroll
-      for (int kk = 0; kk < KD; ++kk) {
-        const Frag8<T> fk = ld8(sKt + (16 * j + lr) * LDK + 32 * kk + 8 * lg);
-        mma(Sqk[j], fQ[kk], fk);
-        mma(Skk[j], fK[kk], fk);
-      }
-    }
-  }
-  // ---- elementwise: dSqk, dSkk (and transposes), row / column sums
-  T* dSqk = static_cast<T*>(ba.dSqk) + cc;
-  T* dSqkT = static_cast<T*>(ba.dSqkT) + cc;
-  T* dSkk = static_cast<T*>(ba.dSkk) + cc;
-  T* dSkkT = static_cast<T*>(ba.dSkkT) + cc;
-  float dbA[4] = {0.f, 0.f, 0.f, 0.f}, rs[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    floatx4 dq, dk;
-    float cs = 0.f;
-#pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-      const int r = 16 * w + 4 * lg + ii, t = 16 * j + lr;
-      const bool ca = r >= t && r < n, sl = r > t;
-      const float gm = GATE == kGateScalar ? fast_exp(r >= t ? sG[r] - sG[t] : 0.f) : 1.f;
-      dq[ii] = ca ? gm * a.scale * dP[j][ii] : 0.f;
-      const float dA = sl ? -dL[j][ii] : 0.f;       // strict_lower(dL)
-      dk[ii] = gm * sBeta[r] * dA;
-      dbA[ii] += dA * gm * Skk[j][ii];              // dbeta through At
-      // (dSkk o S_kk) + (dSqk o S_qk): its row minus column sums give dG
-      const float R = dk[ii] * Skk[j][ii] + dq[ii] * Sqk[j][ii];
-      rs[ii] += R;
-      cs += R;
-    }
-    st_tile<T>(dSqk + (16 * w) * C + 16 * j, C, dq, lr, lg);
-    st_tile_t<T>(dSqkT + (16 * j) * C + 16 * w, C, dq, lr, lg);
-    st_tile<T>(dSkk + (16 * w) * C + 16 * j, C, dk, lr, lg);
-    st_tile_t<T>(dSkkT + (16 * j) * C + 16 * w, C, dk, lr, lg);
-    // column t = 16j + lr: sum over this wave's 16 rows
-    cs += __shfl_xor(cs, 16, 64);
-    cs += __shfl_xor(cs, 32, 64);
-    if (lg == 0) sCs[w][16 * j + lr] = cs;
-  }
-#pragma unroll
-  for (int ii = 0; ii < 4; ++ii)
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) {
-      dbA[ii] += __shfl_xor(dbA[ii], off, 64);
-      rs[ii] += __shfl_xor(rs[ii], off, 64);
-    }
-  if (lr == 0) {
-#pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-      sDb[1][16 * w + 4 * lg + ii] = dbA[ii];
-      sRs[16 * w + 4 * lg + ii] = rs[ii];
-    }
-  }
-  __syncthreads();
-  if (tid < C) {
-    const int r = tid;
-    // Gam_rt = exp(G_r - G_t): d/dG_r of sum R_rt = row sum, d/dG_t = -column sum
-    const float cs = sCs[0][r] + sCs[1][r] + sCs[2][r] + sCs[3][r];
-    ba.dGp[bh * a.Tpad + t0 + r] = GATE == kGateScalar ? sRs[r] - cs : 0.f;
-    if (r < n) ba.dbeta[(b * a.T + t0 + r) * a.H + h] = sDb[0][r] + sDb[1][r];
-  }
-}
-
-// ------------------------------------------------------------ p2
-// Per chunk: dq, the read- and write-key gradients and dg.
-//   phase 1  A1 = dO_s S, A2 = dX S, A3 = E dS'        (C x dk, over dv)
-//   phase 2  dq = Diag(lam) A1 + dSqk Kt, dK = -Diag(lam) A2 + dSkk Kt,
-//            dKt = Diag(w) A3 + dSqk^T Q + dSkk^T K    (over the chunk)
-// Wave w owns rows 16w .. 16w + 15.  Its A operands (dO, dX, E rows and
-// the rows of the four C x C adjoints) are private and load straight into
-// fragments once; the shared B operands (the chunk-start state and its
-// adjoint as rows [c][v], and Kt, Q, K transposed to [c][t]) are staged in
-// LDS for HC key columns at a time, so the block fits twice per CU.
-template <typename T, int DK, int DV>
-struct P2Smem {
-  static constexpr int HC = 64;          // key columns per pass
-  static constexpr int LDV = DV + 8;     // staged state rows [c][v]
-  static constexpr int LDT = C + 8;      // transposed rows [c][t]
-  static constexpr size_t kH = sizeof(T) * 2 * HC * LDV;
-  static constexpr size_t kT = sizeof(T) * 3 * HC * LDT;
-  static constexpr size_t kTotal = kH + kT + sizeof(float) * (3 * C + 4);
-};
-
-template <typename T, int DK, int DV, int GATE>
-__global__ __launch_bounds__(256, 2) void p2_chunk_grads(BwdArgs ba) {
-  using SM = P2Smem<T, DK, DV>;
-  constexpr int HC = SM::HC, LDV = SM::LDV, LDT = SM::LDT;
-  constexpr int KV = DV / 32, NPASS = DK / HC;
-  constexpr uint32_t E = sizeof(T);
-  __shared__ __attribute__((aligned(16))) char smem[SM::kTotal];
-  T* sS = reinterpret_cast<T*>(smem);        // S^T rows c0 .. c0 + HC - 1
-  T* sdS = sS + HC * LDV;                    // dS'^T rows
-  T* sKtT = reinterpret_cast<T*>(smem + SM::kH);
-  T* sQT = sKtT + HC * LDT;
-  T* sKT = sQT + HC * LDT;
-  float* sG = reinterpret_cast<float*>(smem + SM::kH + SM::kT);
-  float* sDl = sG + C;      // d lam_r partials
-  float* sDw = sDl + C;     // d w_r partials
-  float* sRed = sDw + C;    // 4 wave partials of sum(dS' o S)
-
-  const FwdArgs& a = ba.f;
-  const int64_t blk = blockIdx.x;
-  const int64_t bh = blk / a.NT;
-  const int i = static_cast<int>(blk % a.NT);
-  const int64_t b = bh / a.H, h = bh % a.H;
-  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 15, lg = l >> 4;
-  const int64_t t0 = static_cast<int64_t>(i) * C;
-  const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
-  const int64_t HV = a.H * (int64_t)DV, HD = a.H * (int64_t)DK;
-  const int64_t cc = (bh * a.NT + i) * (int64_t)(C * C);
-  const int64_t rv = (bh * a.Tpad + t0) * DV, rk = (bh * a.Tpad + t0) * DK;
-  const int64_t cs = (bh * a.NT + i) * (int64_t)DK * DV;
-
-  // ---- wave-private A operands, row ra (token rows past the end re-read
-  // the last row: their outputs are not stored and their gate terms are
-  // masked below)
-  const int ra = 16 * w + lr;
-  const uint32_t rc = static_cast<uint32_t>(min(ra, n - 1));
-  Frag8<T> fO[KV], fX[KV], fE[KV], fSq[2], fSk[2], fSqT[2], fSkT[2];
   {
-    const T* dob = static_cast<const T*>(ba.dO) + (b * a.T + t0) * HV + h * DV;
-    const T* dxb = static_cast<const T*>(ba.dv) + (b * a.T + t0) * HV + h * DV;
-    const T* eb = static_cast<const T*>(a.Er) + rv;
+    // the Gram products first (Q and K rows die here), then dP and dL tile
+    // by tile straight into the elementwise algebra
+    floatx4 Sqk[4], Skk[4];
 #pragma unroll
-    for (int kk = 0; kk < KV; ++kk) {
-      const uint32_t o = (rc * static_cast<uint32_t>(HV) + 32 * kk + 8 * lg) * E;
-      fO[kk] = ld8(at_bytes(dob, o));
-      fX[kk] = ld8(at_bytes(dxb, o));
-      fE[kk] = ld8(at_bytes(eb, (static_cast<uint32_t>(ra * DV) + 32 * kk + 8 * lg) * E));
+    for (int j = 0; j < 4; ++j) {
+      Sqk[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+      Skk[j] = Sqk[j];
+      if (j <= w) {
+#pragma unroll
+        for (int kk = 0; kk < KD; ++kk) {
+          const Frag8<T> fk = ld8(sKt + (16 * j + lr) * LDK + 32 * kk + 8 * lg);
+          mma(Sqk[j], fQ[kk], fk);
+          mma(Skk[j], fK[kk], fk);
+        }
+      }
     }
-    const uint32_t oc = static_cast<uint32_t>(ra * C + 8 * lg) * E;
+    float dbA[4] = {0.f, 0.f, 0.f, 0.f}, rs[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
-      fSq[k2] = ld8(at_bytes(static_cast<const T*>(ba.dSqk) + cc, oc + 32 * k2 * E));
-      fSk[k2] = ld8(at_bytes(static_cast<const T*>(ba.dSkk) + cc, oc + 32 * k2 * E));
-      fSqT[k2] = ld8(at_bytes(static_cast<const T*>(ba.dSqkT) + cc, oc + 32 * k2 * E));
-      fSkT[k2] = ld8(at_bytes(static_cast<const T*>(ba.dSkkT) + cc, oc + 32 * k2 * E));
+    for (int j = 0; j < 4; ++j) {
+      floatx4 dP = {0.f, 0.f, 0.f, 0.f}, dL = dP;
+      if (j <= w) {
+#pragma unroll
+        for (int kk = 0; kk < KV; ++kk) {
+          const Frag8<T> fe = ld8(sE + (16 * j + lr) * LDE + 32 * kk + 8 * lg);
+          mma(dP, fO[kk], fe);
+          mma(dL, fZ[kk], fe);
+        }
+      }
+      floatx4 dq, dk;
+      float csum = 0.f;
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int r = 16 * w + 4 * lg + ii, t = 16 * j + lr;
+        const bool ca = r >= t && r < n, sl = r > t;
+        const float gm = GATE == kGateScalar ? fast_exp(r >= t ? sG[r] - sG[t] : 0.f) : 1.f;
+        dq[ii] = ca ? gm * a.scale * dP[ii] : 0.f;
+        const float dA = sl ? -dL[ii] : 0.f;          // strict_lower(dL)
+        dk[ii] = gm * sBeta[r] * dA;
+        dbA[ii] += dA * gm * Skk[j][ii];              // dbeta through At
+        // (dSkk o S_kk) + (dSqk o S_qk): row minus column sums give dG
+        const float R = dk[ii] * Skk[j][ii] + dq[ii] * Sqk[j][ii];
+        rs[ii] += R;
+        csum += R;
+      }
+      st_tile<T>(sSq + (16 * w) * LDT + 16 * j, LDT, dq, lr, lg);
+      st_tile_t<T>(sSqT + (16 * j) * LDT + 16 * w, LDT, dq, lr, lg);
+      st_tile<T>(sSk + (16 * w) * LDT + 16 * j, LDT, dk, lr, lg);
+      st_tile_t<T>(sSkT + (16 * j) * LDT + 16 * w, LDT, dk, lr, lg);
+      csum += __shfl_xor(csum, 16, 64);
+      csum += __shfl_xor(csum, 32, 64);
+      if (lg == 0) sCs[w * C + 16 * j + lr] = csum;
+    }
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii)
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) {
+        dbA[ii] += __shfl_xor(dbA[ii], off, 64);
+        rs[ii] += __shfl_xor(rs[ii], off, 64);
+      }
+    if (lr == 0) {
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        sDb[16 * w + 4 * lg + ii] = dbA[ii];
+        sRs[16 * w + 4 * lg + ii] = rs[ii];
+      }
     }
   }
-  if (tid < C) sG[tid] = GATE == kGateScalar ? a.G[bh * a.Tpad + t0 + tid] : 0.f;
+  // E rows of this wave (phase B's A operand of A3)
+#pragma unroll
+  for (int kk = 0; kk < KV; ++kk)
+    fE[kk] = ld8(at_bytes(eb, (static_cast<uint32_t>(ra * DV) + 32 * kk + 8 * lg) * E));
+  __syncthreads();
+  // the C x C adjoints as A fragments of this wave's rows (k = 32 k2 + 8 lg)
+  Frag8<T> fSq[2], fSk[2], fSqT[2], fSkT[2];
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2) {
+    const int o = ra * LDT + 32 * k2 + 8 * lg;
+    fSq[k2] = ld8(sSq + o);
+    fSk[k2] = ld8(sSk + o);
+    fSqT[k2] = ld8(sSqT + o);
+    fSkT[k2] = ld8(sSkT + o);
+  }
+  if (tid < C) {
+    // Gam_rt = exp(G_r - G_t): d/dG_r of sum R_rt = row sum, d/dG_t = -column sum
+    sRs[tid] = GATE == kGateScalar ? sRs[tid] - (sCs[tid] + sCs[C + tid] + sCs[2 * C + tid] + sCs[3 * C + tid])
+                                   : 0.f;
+  }
+  float lam[4], wr[4], bt[4];
+#pragma unroll
+  for (int ii = 0; ii < 4; ++ii) {
+    const int r = 16 * w + 4 * lg + ii;
+    lam[ii] = GATE == kGateScalar ? fast_exp(sG[r]) : 1.f;
+    wr[ii] = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[r]) : 1.f;
+    bt[ii] = sBeta[r];
+  }
 
-  float pl[4] = {0.f, 0.f, 0.f, 0.f}, pw[4] = {0.f, 0.f, 0.f, 0.f};
+  // ---- phase B
+  float pq[4] = {0.f, 0.f, 0.f, 0.f}, pk[4] = {0.f, 0.f, 0.f, 0.f}, pw[4] = {0.f, 0.f, 0.f, 0.f};
   float red = 0.f;
   T* dq = static_cast<T*>(ba.dq) + (b * a.T + t0) * HD + h * DK;
   T* dKm = static_cast<T*>(ba.dKm) + rk;
@@ -588,7 +577,7 @@ __global__ __launch_bounds__(256, 2) void p2_chunk_grads(BwdArgs ba) {
 #pragma unroll 1
   for (int p = 0; p < NPASS; ++p) {
     const int c0 = p * HC;
-    if (p > 0) __syncthreads();   // the previous pass is done with the LDS
+    __syncthreads();   // phase A (or the previous pass) is done with the LDS
     {
       constexpr int VEC = 16 / sizeof(T), VPR = DV / VEC;
       const T* Hs = static_cast<const T*>(a.Hs) + cs + c0 * DV;
@@ -605,45 +594,37 @@ __global__ __launch_bounds__(256, 2) void p2_chunk_grads(BwdArgs ba) {
     load_rows_t<T, HC>(sQT, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
     load_rows_t<T, HC>(sKT, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
     __syncthreads();
-    float lam[4], wr[4];
-#pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-      const int r = 16 * w + 4 * lg + ii;
-      lam[ii] = GATE == kGateScalar ? fast_exp(sG[r]) : 1.f;
-      wr[ii] = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[r]) : 1.f;
-    }
     // sum(dS' o S) over this pass's rows
     for (int idx = tid; idx < HC * DV; idx += 256) {
       const int c = idx / DV, v = idx % DV;
       red += to_f(sS[c * LDV + v]) * to_f(sdS[c * LDV + v]);
     }
-#pragma unroll
+#pragma unroll 1
     for (int j = 0; j < HC / 16; ++j) {
-      // ---- phase 1
       floatx4 A1 = {0.f, 0.f, 0.f, 0.f}, A2 = A1, A3 = A1;
 #pragma unroll
       for (int kk = 0; kk < KV; ++kk) {
         const Frag8<T> fh = ld8(sS + (16 * j + lr) * LDV + 32 * kk + 8 * lg);
         const Frag8<T> fd = ld8(sdS + (16 * j + lr) * LDV + 32 * kk + 8 * lg);
         mma(A1, fO[kk], fh);
-        mma(A2, fX[kk], fh);
+        mma(A2, fZ[kk], fh);
         mma(A3, fE[kk], fd);
       }
-      // gate partials: dlam_r = Q_r . A1_r - K_r . A2_r ;  dw_r = Kt_r . A3_r
+      // row partials: Q_r . A1_r, K_r . A2'_r (gate and dbeta), Kt_r . A3_r
       const int c = 16 * j + lr;
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
         const int r = 16 * w + 4 * lg + ii;
         A1[ii] *= a.scale;
-        pl[ii] += to_f(sQT[c * LDT + r]) * A1[ii] - to_f(sKT[c * LDT + r]) * A2[ii];
+        pq[ii] += to_f(sQT[c * LDT + r]) * A1[ii];
+        pk[ii] += to_f(sKT[c * LDT + r]) * A2[ii];
         pw[ii] += to_f(sKtT[c * LDT + r]) * A3[ii];
       }
-      // ---- phase 2
       floatx4 aq, ak, at;
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
         aq[ii] = lam[ii] * A1[ii];
-        ak[ii] = -lam[ii] * A2[ii];
+        ak[ii] = -lam[ii] * bt[ii] * A2[ii];
         at[ii] = wr[ii] * A3[ii];
       }
 #pragma unroll
@@ -667,28 +648,36 @@ __global__ __launch_bounds__(256, 2) void p2_chunk_grads(BwdArgs ba) {
   for (int ii = 0; ii < 4; ++ii)
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) {
-      pl[ii] += __shfl_xor(pl[ii], off, 64);
+      pq[ii] += __shfl_xor(pq[ii], off, 64);
+      pk[ii] += __shfl_xor(pk[ii], off, 64);
       pw[ii] += __shfl_xor(pw[ii], off, 64);
     }
   if (lr == 0) {
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
       const int r = 16 * w + 4 * lg + ii;
-      sDl[r] = r < n ? pl[ii] : 0.f;
+      // dlam_r = Q_r . A1_r - beta_r K_r . A2'_r ;  dw_r = Kt_r . A3_r
+      sDl[r] = r < n ? pq[ii] - sBeta[r] * pk[ii] : 0.f;
       sDw[r] = r < n ? pw[ii] : 0.f;
+      sKZ[r] = pk[ii];
     }
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) red += __shfl_xor(red, off, 64);
   if (l == 0) sRed[w] = red;
   __syncthreads();
+  // ---- dbeta = At term + Z . V - lam K . A2'
+  if (tid < n) {
+    const float lamr = GATE == kGateScalar ? fast_exp(sG[tid]) : 1.f;
+    ba.dbeta[(b * a.T + t0 + tid) * a.H + h] = sDb[tid] + sZV[tid] - lamr * sKZ[tid];
+  }
   // ---- gate: dG_r, then the reverse in-chunk cumsum -> dg
   if (GATE == kGateScalar && w == 0) {
     const int r = l;
     const float lamr = fast_exp(sG[r]);
     const float wrr = fast_exp(sG[C - 1] - sG[r]);
     float wdw = wrr * sDw[r];
-    float dG = ba.dGp[bh * a.Tpad + t0 + r] + lamr * sDl[r] - wdw;
+    float dG = sRs[r] + lamr * sDl[r] - wdw;
     // lam_C and the w_r all depend on G_{C-1}
     float tot = wdw;
 #pragma unroll
@@ -993,7 +982,6 @@ BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate,
   auto take = [&](size_t bytes) { const size_t o = off; off = align256b(off + bytes); return o; };
   const size_t bh = static_cast<size_t>(BH), nt = static_cast<size_t>(NT), tp = nt * C;
   L.Hs = take(bh * nt * dk * dv * esz);
-  L.Xr = take(bh * tp * dv * esz);
   L.Er = take(bh * tp * dv * esz);
   L.PtT = take(bh * nt * C * C * esz);
   L.MtT = take(bh * nt * C * C * esz);
@@ -1003,11 +991,6 @@ BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate,
   L.KnT = take(bh * nt * dk * C * esz);
   L.dHs = take(bh * nt * dk * dv * esz);
   L.Zr = take(bh * tp * dv * esz);
-  L.dSqk = take(bh * nt * C * C * esz);
-  L.dSqkT = take(bh * nt * C * C * esz);
-  L.dSkk = take(bh * nt * C * C * esz);
-  L.dSkkT = take(bh * nt * C * C * esz);
-  L.dGp = take(bh * tp * 4);
   L.dKt = take(bh * tp * dk * esz);
   L.dKm = take(bh * tp * dk * esz);
   L.pcL = take(bh * nt * dk * 4);
@@ -1030,12 +1013,9 @@ static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s, hipEvent_t 
   hipLaunchKernelGGL((r1_state_adjoint<T, DK, GATE>), dim3(grid_scan), dim3(256), 0, s, ba);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = mark(4)) != hipSuccess) return e;
-  hipLaunchKernelGGL((p1_chunk_cc<T, DK, DV, GATE>), dim3(grid_chunk), dim3(256), 0, s, ba);
+  hipLaunchKernelGGL((p12_chunk_grads<T, DK, DV, GATE>), dim3(grid_chunk), dim3(256), 0, s, ba);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = mark(5)) != hipSuccess) return e;
-  hipLaunchKernelGGL((p2_chunk_grads<T, DK, DV, GATE>), dim3(grid_chunk), dim3(256), 0, s, ba);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  if ((e = mark(6)) != hipSuccess) return e;
   if (a.precond == kSquash) {
     hipLaunchKernelGGL((pc_chunk<T, DK, false>), dim3(grid_chunk), dim3(DK * PCS), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1053,7 +1033,7 @@ static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s, hipEvent_t 
                        s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  return mark(7);
+  return mark(6);
 }
 
 // fp32 io: head dims 64 only (LDS); the host validates this

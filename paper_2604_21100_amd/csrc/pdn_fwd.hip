@@ -682,9 +682,8 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
     st4<T>(sE + (16 * vt + lr) * LDE + 16 * w + 4 * lg, accE[0], accE[1], accE[2], accE[3]);
   }
   lds_barrier();
-  if (SAVE) {  // X and E rows of this chunk (whole chunk: padded rows included)
+  if (SAVE) {  // E rows of this chunk (whole chunk: padded rows included)
     const int64_t r0 = (x.bh * a.Tpad + static_cast<int64_t>(i) * C) * a.dv + x.v0;
-    flush_slab_t<T>(static_cast<T*>(a.Xr) + r0, a.dv, sX, LDE, C, x.tid);
     flush_slab_t<T>(static_cast<T*>(a.Er) + r0, a.dv, sE, LDE, C, x.tid);
   }
   // ---- O = scale [ (Lam Q) S^T + P E ];  S^T <- Diag(gamma_C) S^T + (Kt Gamma)^T E
@@ -721,7 +720,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
   lds_barrier();
 }
 
-// SAVE: also write the chunk-start states and the X, E rows the backward
+// SAVE: also write the chunk-start states and the E rows the backward
 // reads.  OUT: compute and write the output (without it, queries and P are
 // neither loaded nor used: the backward's recompute).
 template <typename T, int DK, int GATE, bool SAVE, bool OUT>

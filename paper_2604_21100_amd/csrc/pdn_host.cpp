@@ -195,7 +195,7 @@ static void set_forward_ws(pdn::FwdArgs& a, const pdn::WsLayout& L, const pdn_pr
 }
 
 static void set_residuals(pdn::FwdArgs& f, const pdn::BwdWsLayout& L, char* w) {
-  f.Hs = w + L.Hs; f.Xr = w + L.Xr; f.Er = w + L.Er; f.PtT = w + L.PtT; f.MtT = w + L.MtT;
+  f.Hs = w + L.Hs; f.Er = w + L.Er; f.PtT = w + L.PtT; f.MtT = w + L.MtT;
   f.Ktr = w + L.Ktr; f.Kw = w + L.Kw; f.QlT = w + L.QlT; f.KnT = w + L.KnT;
 }
 
@@ -339,8 +339,6 @@ static pdn_status chunk_bwd_impl(const pdn_problem* p, const pdn_inputs* in, con
   a.dS0 = out->dS0; a.dbeta_p = out->dbeta_p; a.dg_p = out->dg_p; a.dlog_a_scale = out->dlog_a_scale;
   a.dA0 = out->dA0; a.dktilde = out->dktilde;
   a.dHs = w + L.dHs; a.Zr = w + L.Zr;
-  a.dSqk = w + L.dSqk; a.dSqkT = w + L.dSqkT; a.dSkk = w + L.dSkk; a.dSkkT = w + L.dSkkT;
-  a.dGp = reinterpret_cast<float*>(w + L.dGp);
   a.dKt = w + L.dKt;
   a.dKm = w + L.dKm;
   a.pcL = reinterpret_cast<float*>(w + L.pcL);

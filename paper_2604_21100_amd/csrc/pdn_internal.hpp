@@ -50,7 +50,6 @@ struct FwdArgs {
   // backward only (NULL in the forward): forward intermediates kept for the
   // adjoint kernels.  lam_r = exp(G_r), w_r = exp(G_{C-1} - G_r).
   void* Hs;       // [BH, NT, dk, dv] io  chunk-start states S^T
-  void* Xr;       // [BH, Tpad, dv] io    X = V - (Lam K) S^T rows
   void* Er;       // [BH, Tpad, dv] io    E = T X rows
   void* PtT;      // [BH, NT, C, C] io    P^T
   void* MtT;      // [BH, NT, C, C] io    M^T, M = (I + At)^{-1} (T = M Diag(beta))
@@ -80,11 +79,6 @@ struct BwdArgs {
   // workspace
   void* dHs;      // [BH, NT, dk, dv] io  state adjoint entering each chunk from the right
   void* Zr;       // [BH, Tpad, dv] io    Z = M^T dE rows (dX = dV = Diag(beta) Z)
-  void* dSqk;     // [BH, NT, C, C] io    d(Q Kt^T), masked and decayed
-  void* dSqkT;    // transposed
-  void* dSkk;     // [BH, NT, C, C] io    d(K Kt^T)
-  void* dSkkT;
-  float* dGp;     // [BH, Tpad] fp32      gate-prefix gradient from the C x C terms
   void* dKt;      // [BH, Tpad, dk] io    gradient of the write key
   void* dKm;      // [BH, Tpad, dk] io    gradient of the read key (main recurrence)
   float* pcL;     // [BH, NT, dk]         preconditioner: in-chunk adjoint at chunk start
@@ -100,8 +94,8 @@ WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precon
 
 struct BwdWsLayout {
   WsLayout f;
-  size_t Hs, Xr, Er, PtT, MtT, Ktr, Kw, QlT, KnT;
-  size_t dHs, Zr, dSqk, dSqkT, dSkk, dSkkT, dGp, dKt, dKm, pcL, pcC, pcMu, total;
+  size_t Hs, Er, PtT, MtT, Ktr, Kw, QlT, KnT;
+  size_t dHs, Zr, dKt, dKm, pcL, pcC, pcMu, total;
 };
 
 BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond);

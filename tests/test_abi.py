@@ -177,7 +177,7 @@ def test_stage_event_arguments_validated():
         pdn.BWD_STAGE_EVENTS) == pdn.PDN_ERR_NULL
     assert lib.pdn_chunk_bwd_events(
         ctypes.byref(p), ctypes.byref(_inputs()), A * 30, None,
-        ctypes.byref(bo), A * 64, 0, None, ev_b, 7) == pdn.PDN_ERR_VALUE
+        ctypes.byref(bo), A * 64, 0, None, ev_b, 6) == pdn.PDN_ERR_VALUE
     ev_b[3] = None
     assert lib.pdn_chunk_bwd_events(
         ctypes.byref(p), ctypes.byref(_inputs()), A * 30, None,
