@@ -702,29 +702,15 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
 // chains the chunks (adjoint entering each chunk from the right), and
 // pc_chunk<true> recomputes with the carry and writes dk, dbetaP, dgP and the
 // partial d mu.
-// Sum of 16 per-row values over the 64 lanes of a wave, scattered: lane l
-// ends with the total of row pc_row(l) (lanes differing only in bits 0-1
-// hold the same total).  Halving exchanges (8+4+2+1 values) then two plain
-// xor steps: 17 shuffles instead of 16 x 6.
-__device__ __forceinline__ int pc_row(int l) {
-  return ((l >> 5) & 1) * 8 + ((l >> 4) & 1) * 4 + ((l >> 3) & 1) * 2 + ((l >> 2) & 1);
-}
-
-__device__ __forceinline__ float pc_reduce16(float (&v)[16], int l) {
+// Sum of each of 16 per-row values over the 64 lanes of a wave (butterfly:
+// every lane ends with all 16 totals).  Static indices only: a per-lane
+// choice between array elements gets merged into a runtime index by the
+// compiler, which then lowers it to compare / select chains.
+__device__ __forceinline__ void pc_wave_sum16(float (&v)[16]) {
 #pragma unroll
-  for (int half = 8, m = 32; half >= 1; half >>= 1, m >>= 1) {
-    const bool hi = (l & m) != 0;
+  for (int off = 1; off < 64; off <<= 1)
 #pragma unroll
-    for (int i = 0; i < half; ++i) {
-      const float keep = hi ? v[half + i] : v[i];
-      const float give = hi ? v[i] : v[half + i];
-      v[i] = keep + __shfl_xor(give, m, 64);
-    }
-  }
-  float x = v[0];
-  x += __shfl_xor(x, 2, 64);
-  x += __shfl_xor(x, 1, 64);
-  return x;
+    for (int j = 0; j < 16; ++j) v[j] += __shfl_xor(v[j], off, 64);
 }
 
 // One block per (b, h, chunk).  The chunk's 64 tokens are cut into four
@@ -737,90 +723,118 @@ __device__ __forceinline__ float pc_reduce16(float (&v)[16], int l) {
 //   reverse  D_r = Dhat_r + (prod_{r < j <= s0 + G - 1} aP_j) kappa
 // (s0 the segment's first token, A_in the preconditioner state before it,
 // kappa the adjoint entering it from the right, already times aP of the
-// next token).  The products are exp of differences of the in-chunk prefix
-// of gP.  Loop bodies are branch-free and, for full chunks (FULL), store
-// without row guards, so each segment's 16 rows form one basic block.
+// next token).  The per-token products come from the in-chunk prefix of gP.
+// The chunk's key, write-key-gradient and read-key-gradient rows are staged
+// in LDS with 16-byte loads (one channel per lane would mean 2-byte
+// accesses), and dk leaves the same way.  Loop bodies are branch-free.
 constexpr int PCG = 16;   // tokens per segment
 constexpr int PCS = C / PCG;
 
-template <bool FULL, typename T, int DK, bool FINAL>
-__device__ __forceinline__ void pc_body(const BwdArgs& ba, int64_t bh, int i, int n, const float* sEgp,
-                                        const float* sBp, const float* sGp, float (*sEnd)[DK],
-                                        float (*sRow)[DK / 64][C], float* sMu) {
+template <typename T, int DK>
+__device__ __forceinline__ void pc_stage(T* dst, const T* src, int64_t ld, int nvalid, int tid) {
+  constexpr int VEC = 16 / sizeof(T), VPR = DK / VEC;
+  for (int idx = tid; idx < C * VPR; idx += DK * PCS) {
+    const int r = idx / VPR, cv = idx % VPR;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < nvalid) v = *reinterpret_cast<const float4*>(src + r * ld + cv * VEC);
+    *reinterpret_cast<float4*>(dst + r * DK + cv * VEC) = v;
+  }
+}
+
+template <typename T, int DK, bool FINAL>
+__global__ __launch_bounds__(DK * PCS) void pc_chunk(BwdArgs ba) {
   constexpr int NCH = DK / 64;
+  __shared__ float sEgp[C], sBp[C], sGp[C], sFf[C], sBf[C];
+  __shared__ float sEnd[PCS][DK];          // per-segment end values (A, then adjoint)
+  __shared__ float sRow[2][NCH][C];        // per-channel-half row sums: D k^2, D A_{r-1}
+  __shared__ float sMu[PCS * NCH];
+  __shared__ __attribute__((aligned(16))) T sKr[C * DK];   // key rows (zero past the end)
+  __shared__ __attribute__((aligned(16))) T sGr[C * DK];   // write-key gradient rows
+  __shared__ __attribute__((aligned(16))) T sMr[FINAL ? C * DK : 8];   // read-key gradient rows, then dk
   const FwdArgs& a = ba.f;
+  const int64_t blk = blockIdx.x;
+  const int64_t bh = blk / a.NT;
+  const int i = static_cast<int>(blk % a.NT);
   const int64_t b = bh / a.H, h = bh % a.H;
-  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+  const int tid = threadIdx.x, l = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int ch = w % NCH, sg = w / NCH;
   const int c = 64 * ch + l;
   const int s0 = PCG * sg;
   const int64_t t0 = static_cast<int64_t>(i) * C;
+  const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
   const int64_t kst = a.H * static_cast<int64_t>(DK);
-  const T* kcol = static_cast<const T*>(a.k) + ((b * a.T + t0) * a.H + h) * DK + c;
-  const T* dkt = static_cast<const T*>(ba.dKt) + (bh * a.Tpad + t0 + s0) * DK + c;
-  const T* dkm = static_cast<const T*>(ba.dKm) + (bh * a.Tpad + t0 + s0) * DK + c;
-  // loads: keys (rows past the end re-read the last row and are zeroed
-  // below), write-key and read-key gradients (workspace rows cover the
-  // padded chunk)
-  float kv[PCG], gk[PCG], km[PCG];
-#pragma unroll
-  for (int j = 0; j < PCG; ++j) kv[j] = to_f(kcol[(FULL ? s0 + j : min(s0 + j, n - 1)) * kst]);
-#pragma unroll
-  for (int j = 0; j < PCG; ++j) gk[j] = to_f(dkt[j * DK]);
-  if (FINAL) {
-#pragma unroll
-    for (int j = 0; j < PCG; ++j) km[j] = to_f(dkm[j * DK]);
-  }
+  const T* krow = static_cast<const T*>(a.k) + ((b * a.T + t0) * a.H + h) * DK;
+  pc_stage<T, DK>(sKr, krow, kst, n, tid);
+  pc_stage<T, DK>(sGr, static_cast<const T*>(ba.dKt) + (bh * a.Tpad + t0) * DK, DK, C, tid);
+  if (FINAL) pc_stage<T, DK>(sMr, static_cast<const T*>(ba.dKm) + (bh * a.Tpad + t0) * DK, DK, C, tid);
   const float A_start = a.Abound[(bh * (a.NT + 1) + i) * DK + c];
   const float kap_chunk = FINAL ? ba.pcC[(bh * (a.NT + 1) + i + 1) * DK + c] : 0.f;
-  if (!FULL) {
+  if (tid < C) {
+    // per-token factors; padded tokens: aP = 1 (gP = 0), bP = 0.  sGp is the
+    // in-chunk inclusive prefix of gP (one wave, shuffle scan)
+    const bool ok = tid < n;
+    const int64_t sidx = (b * a.T + t0 + min(tid, n - 1)) * a.H + h;
+    const float gp = (ok && a.g_p) ? a.g_p[sidx] : 0.f;
+    sEgp[tid] = fast_exp(gp);
+    sBp[tid] = ok ? a.beta_p[sidx] : 0.f;
+    float x = gp;
 #pragma unroll
-    for (int j = 0; j < PCG; ++j) kv[j] = s0 + j < n ? kv[j] : 0.f;
+    for (int off = 1; off < 64; off <<= 1) {
+      const float y = __shfl_up(x, off, 64);
+      if (tid >= off) x += y;
+    }
+    sGp[tid] = x;
+    // per-token factors of the segment composition:
+    //   forward  prod_{s0 <= j <= r} aP_j,   reverse  prod_{r < j < s0 + G} aP_j
+    const int q0 = tid & ~(PCG - 1);
+    const float gb = __shfl(x, q0 - 1, 64), ge = __shfl(x, q0 + PCG - 1, 64);
+    sFf[tid] = fast_exp(x - (q0 > 0 ? gb : 0.f));
+    sBf[tid] = fast_exp(ge - x);
   }
-  // prefix of gP before this segment (sGp[r] = sum_{j <= r} gP_j)
-  const float gbase = sg > 0 ? sGp[s0 - 1] : 0.f;
+  __syncthreads();
   // ---- forward: local scan from zero, then the exact state entering
   float A[PCG];
   {
     float x = 0.f;
 #pragma unroll
     for (int j = 0; j < PCG; ++j) {
-      x = sEgp[s0 + j] * x + sBp[s0 + j] * kv[j] * kv[j];
+      const float kv = to_f(sKr[(s0 + j) * DK + c]);
+      x = sEgp[s0 + j] * x + sBp[s0 + j] * kv * kv;
       A[j] = x;
     }
   }
   sEnd[sg][c] = A[PCG - 1];
   __syncthreads();
   float A_in = A_start;
-  for (int q = 0; q < sg; ++q) {
-    const float pe = fast_exp(sGp[PCG * q + PCG - 1] - (q > 0 ? sGp[PCG * q - 1] : 0.f));
-    A_in = sEnd[q][c] + pe * A_in;
-  }
+  for (int q = 0; q < sg; ++q) A_in = sEnd[q][c] + sFf[PCG * q + PCG - 1] * A_in;   // segment product
 #pragma unroll
-  for (int j = 0; j < PCG; ++j) A[j] += fast_exp(sGp[s0 + j] - gbase) * A_in;
+  for (int j = 0; j < PCG; ++j) A[j] += sFf[s0 + j] * A_in;
   // ---- reverse: local adjoint from zero; the gain terms need no D
   const float mu = fast_exp(a.log_a_scale[h]);
   const float lnx = a.lnx;
-  float Dh[PCG], base[PCG];
+  float Dh[PCG];
   float muPart = 0.f;
   {
     float D = 0.f, aNext = 1.f;
 #pragma unroll
     for (int j = PCG - 1; j >= 0; --j) {
       const float Ar = A[j];
+      const float kv = to_f(sKr[(s0 + j) * DK + c]);
+      const float gk = to_f(sGr[(s0 + j) * DK + c]);
       // B(A) = exp(-lnx s(rho)), rho = log A - mu, s = rho / (1 + |rho|):
       // dB/dA = -lnx B / ((1 + |rho|)^2 A); zero where A <= 0 (B = x there)
       const bool pos = Ar > 0.f;
       const float rr = fast_log(fmaxf(Ar, 1e-30f)) - mu;
       const float qd = fast_rcp(1.f + fabsf(rr));
       const float Bv = fast_exp(-lnx * (pos ? rr * qd : -1.f));
-      const float dr = pos ? -lnx * Bv * gk[j] * kv[j] * qd * qd : 0.f;
+      const float dr = pos ? -lnx * Bv * gk * kv * qd * qd : 0.f;
       D = dr * fast_rcp(fmaxf(Ar, 1e-30f)) + aNext * D;
       aNext = sEgp[s0 + j];
       Dh[j] = D;
-      if (FINAL) {
+      if (FINAL) {   // dk's terms without D, in place of dKm (same thread)
         muPart -= dr;
-        base[j] = km[j] + Bv * gk[j];
+        sMr[(s0 + j) * DK + c] = from_f<T>(to_f(sMr[(s0 + j) * DK + c]) + Bv * gk);
       }
     }
     __syncthreads();   // every thread is done with sEnd (forward)
@@ -829,39 +843,50 @@ __device__ __forceinline__ void pc_body(const BwdArgs& ba, int64_t bh, int i, in
   __syncthreads();
   // adjoint entering this segment from the right
   float kap = kap_chunk;
-  for (int q = PCS - 1; q > sg; --q) {
-    const float pe = fast_exp(sGp[PCG * q + PCG - 1] - sGp[PCG * q - 1]);
-    kap = sEnd[q][c] + pe * kap;
-  }
-  const float gend = sGp[s0 + PCG - 1];
+  for (int q = PCS - 1; q > sg; --q) kap = sEnd[q][c] + sFf[PCG * q + PCG - 1] * kap;
   if (!FINAL) {
     if (sg == 0) {
       // the adjoint this chunk sends to the left, with zero carry: aP_0 D_0
-      ba.pcL[(bh * a.NT + i) * DK + c] = sEnd[0][c] + fast_exp(gend) * kap;
+      ba.pcL[(bh * a.NT + i) * DK + c] = sEnd[0][c] + sFf[PCG - 1] * kap;
     }
     return;
   }
-  // ---- outputs: dk = dKm + B dkt + 2 bP k D;  row sums D k^2, D A_{r-1}
-  T* dkout = static_cast<T*>(ba.dk) + ((b * a.T + t0 + s0) * a.H + h) * DK + c;
-  float s1[PCG], s2[PCG];
+  // ---- outputs: dk = dKm + B dkt + 2 bP k D (to LDS, in place of dKm);
+  // row sums D k^2, D A_{r-1}
+  float sr[PCG];
 #pragma unroll
   for (int j = 0; j < PCG; ++j) {
-    const float D = Dh[j] + fast_exp(gend - sGp[s0 + j]) * kap;
-    const float dkk = base[j] + 2.f * sBp[s0 + j] * kv[j] * D;
-    if (FULL || s0 + j < n) dkout[j * kst] = from_f<T>(dkk);
-    s1[j] = D * kv[j] * kv[j];
-    s2[j] = D * (j > 0 ? A[j - 1] : A_in);
+    const float kv = to_f(sKr[(s0 + j) * DK + c]);
+    const float D = Dh[j] + sBf[s0 + j] * kap;
+    T* p = sMr + (s0 + j) * DK + c;
+    *p = from_f<T>(to_f(*p) + 2.f * sBp[s0 + j] * kv * D);
+    Dh[j] = D;
+    sr[j] = D * kv * kv;
   }
-  const float t1 = pc_reduce16(s1, l);
-  const float t2 = pc_reduce16(s2, l);
-  if ((l & 3) == 0) {
-    sRow[0][ch][s0 + pc_row(l)] = t1;
-    sRow[1][ch][s0 + pc_row(l)] = t2;
-  }
+  pc_wave_sum16(sr);
+#pragma unroll
+  for (int j = 0; j < PCG; ++j)
+    if (l == j) sRow[0][ch][s0 + j] = sr[j];
+#pragma unroll
+  for (int j = 0; j < PCG; ++j) sr[j] = Dh[j] * (j > 0 ? A[j - 1] : A_in);
+  pc_wave_sum16(sr);
+#pragma unroll
+  for (int j = 0; j < PCG; ++j)
+    if (l == j) sRow[1][ch][s0 + j] = sr[j];
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) muPart += __shfl_xor(muPart, off, 64);
   if (l == 0) sMu[w] = muPart;
   __syncthreads();
+  {
+    // dk rows of the valid tokens, 16-byte stores
+    constexpr int VEC = 16 / sizeof(T), VPR = DK / VEC;
+    T* dko = static_cast<T*>(ba.dk) + ((b * a.T + t0) * a.H + h) * DK;
+    for (int idx = tid; idx < n * VPR; idx += DK * PCS) {
+      const int r = idx / VPR, cv = idx % VPR;
+      *reinterpret_cast<float4*>(dko + r * kst + cv * VEC) =
+          *reinterpret_cast<const float4*>(sMr + r * DK + cv * VEC);
+    }
+  }
   if (tid < n) {
     float u1 = 0.f, u2 = 0.f;
 #pragma unroll
@@ -879,43 +904,6 @@ __device__ __forceinline__ void pc_body(const BwdArgs& ba, int64_t bh, int i, in
     for (int q = 0; q < PCS * NCH; ++q) m += sMu[q];
     ba.pcMu[bh * a.NT + i] = m;
   }
-}
-
-template <typename T, int DK, bool FINAL>
-__global__ __launch_bounds__(DK * PCS) void pc_chunk(BwdArgs ba) {
-  __shared__ float sEgp[C], sBp[C], sGp[C];
-  __shared__ float sEnd[PCS][DK];          // per-segment end values (A, then adjoint)
-  __shared__ float sRow[2][DK / 64][C];    // per-channel-half row sums: D k^2, D A_{r-1}
-  __shared__ float sMu[PCS * DK / 64];
-  const FwdArgs& a = ba.f;
-  const int64_t blk = blockIdx.x;
-  const int64_t bh = blk / a.NT;
-  const int i = static_cast<int>(blk % a.NT);
-  const int64_t b = bh / a.H, h = bh % a.H;
-  const int tid = threadIdx.x;
-  const int64_t t0 = static_cast<int64_t>(i) * C;
-  const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
-  if (tid < C) {
-    // per-token factors; padded tokens: aP = 1 (gP = 0), bP = 0.  sGp is the
-    // in-chunk inclusive prefix of gP (one wave, shuffle scan)
-    const bool ok = tid < n;
-    const int64_t sidx = (b * a.T + t0 + min(tid, n - 1)) * a.H + h;
-    const float gp = (ok && a.g_p) ? a.g_p[sidx] : 0.f;
-    sEgp[tid] = fast_exp(gp);
-    sBp[tid] = ok ? a.beta_p[sidx] : 0.f;
-    float x = gp;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const float y = __shfl_up(x, off, 64);
-      if (tid >= off) x += y;
-    }
-    sGp[tid] = x;
-  }
-  __syncthreads();
-  if (n == C)
-    pc_body<true, T, DK, FINAL>(ba, bh, i, n, sEgp, sBp, sGp, sEnd, sRow, sMu);
-  else
-    pc_body<false, T, DK, FINAL>(ba, bh, i, n, sEgp, sBp, sGp, sEnd, sRow, sMu);
 }
 
 // carry_{i-1} = L_i + exp(sumD_i) carry_i, from the last chunk (carry 0)
