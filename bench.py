@@ -22,7 +22,10 @@ from __future__ import annotations
 
 import argparse
 import dataclasses
+import glob
+import hashlib
 import json
+import re
 import os
 import sys
 import time
@@ -70,14 +73,14 @@ def algorithmic_per_token_head(spec, train=False):
     scan = (6 * dk * dv + 4 * C * dv,
             e * (2 * dk + dv) + e * (2 * C + dk) + gb + e * dv)
     # k3 (saving, no output): read k, v, T, decayed write keys, gate prefix;
-    # write the chunk-start states and the X, E rows
+    # write the chunk-start states and the E rows
     save = (4 * dk * dv + 2 * C * dv,
-            e * (dk + dv) + e * (C + dk) + gb + st + 2 * e * dv)
+            e * (dk + dv) + e * (C + dk) + gb + st + e * dv)
     stages = {
         "precond": precond,
         "chunk_prep": prep_b if train else prep,
-        # training forward: the output and the saved states and rows
-        "chunk_scan": ((scan[0], scan[1] + st + 2 * e * dv) if train
+        # training forward: the output, the saved states and E rows
+        "chunk_scan": ((scan[0], scan[1] + st + e * dv) if train
                        else scan),
         "bwd_precond_recompute": precond,
         "bwd_chunk_prep": prep_b,
@@ -182,6 +185,35 @@ def cpu_baseline(spec, inp, bwd, target_s=15.0):
                    f"{workers} worker processes x 1 thread); value = "
                    f"token-heads/s / H"),
     }
+
+
+def sources_sha256():
+    """Hash of the HIP / host sources of the library (the kernels whose
+    traffic a profile summary records)."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2604_21100_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode())
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, mode, stage):
+    """HBM bytes per launch of a stage's kernels, from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary of this workload (lines
+    `traffic: <mode> <stage> <bytes>`), or None when there is none or the
+    kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"sources-sha256: ([0-9a-f]{64})", text)
+    if not m or m.group(1) != sources_sha256():
+        return None
+    m = re.search(rf"^traffic: {re.escape(mode)} {re.escape(stage)} (\d+)\s*$",
+                  text, re.M)
+    return int(m.group(1)) if m else None
 
 
 def roofline_of(stage, ms, stages, token_heads, train=False):
@@ -346,6 +378,8 @@ def main(argv=None):
     flop_fwd, flop_bwd, stages = algorithmic_per_token_head(spec, train)
     dom = max(stage_ms, key=stage_ms.get)
     roof = roofline_of(dom, stage_ms[dom], stages, token_heads, train)
+    mode = "train" if train else ("recompute" if bwd else "forward")
+    roof["traffic"] = measured_traffic(args.workload, mode, dom)
     kernels = {k: roofline_of(k, v, stages, token_heads, train)["frac"]
                for k, v in stage_ms.items()}
 
