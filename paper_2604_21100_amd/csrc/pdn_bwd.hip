@@ -63,7 +63,7 @@ __device__ __forceinline__ void slab_to_rows(T* dst, int64_t ld, const T* src, i
     float4 pk;
     T* e = reinterpret_cast<T*>(&pk);
 #pragma unroll
-    for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = src[(c0 + s2) * lds + row];
+    for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = *sw(src, lds, c0 + s2, row);
     if (row < n) *reinterpret_cast<float4*>(dst + row * ld + c0) = pk;
   }
 }
@@ -73,7 +73,7 @@ template <typename T, int DK>
 struct RevFrags {
   static constexpr int KK = DK / 32, CT = DK / 64;
   Frag8<T> Pt[2], Kw[KK], Mt[2], Ql[CT][2], Kn[CT][2];
-  float4 dO[Slab<T>::kPer];
+  float4 dO[Slab<T>::kPer];   // dO slab of the chunk before this one
   float gC;
   float beta[4];   // beta of rows 16w + 4lg + ii (raw: past the end masked at use)
 };
@@ -82,6 +82,27 @@ struct RevCtx {
   int64_t b, h, bh;
   int v0, w, lr, lg, tid;
 };
+
+// dO slab of chunk i (rows past the sequence end re-read its last row; the
+// staging zeroes them)
+template <typename T>
+__device__ __forceinline__ void rev_load_dO(float4 (&d)[Slab<T>::kPer], const BwdArgs& ba, int i,
+                                            const RevCtx& x) {
+  using SM = Slab<T>;
+  constexpr uint32_t E = sizeof(T);
+  const FwdArgs& a = ba.f;
+  const int64_t t0 = static_cast<int64_t>(i) * C;
+  const int last = static_cast<int>(min<int64_t>(C, a.T - t0)) - 1;
+  const int64_t HV = a.H * (int64_t)a.dv;
+  const T* dob = static_cast<const T*>(ba.dO) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0;
+#pragma unroll
+  for (int j = 0; j < SM::kPer; ++j) {
+    const int idx = x.tid + 256 * j;
+    const uint32_t row = static_cast<uint32_t>(min(idx / SM::kSegs, last));
+    const uint32_t off = (row * static_cast<uint32_t>(HV) + (idx % SM::kSegs) * SM::kVec) * E;
+    d[j] = *reinterpret_cast<const float4*>(at_bytes(dob, off));
+  }
+}
 
 template <typename T, int DK, int GATE>
 __device__ __forceinline__ void rev_load(RevFrags<T, DK>& f, const BwdArgs& ba, int i,
@@ -117,15 +138,9 @@ __device__ __forceinline__ void rev_load(RevFrags<T, DK>& f, const BwdArgs& ba, 
       f.Ql[ct][k2] = ld8(at_bytes(ql, o));
       f.Kn[ct][k2] = ld8(at_bytes(kn, o));
     }
-  const int64_t HV = a.H * (int64_t)a.dv;
-  const T* dob = static_cast<const T*>(ba.dO) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0;
-#pragma unroll
-  for (int j = 0; j < SM::kPer; ++j) {
-    const int idx = x.tid + 256 * j;
-    const uint32_t row = static_cast<uint32_t>(min(idx / SM::kSegs, last));
-    const uint32_t off = (row * static_cast<uint32_t>(HV) + (idx % SM::kSegs) * SM::kVec) * E;
-    f.dO[j] = *reinterpret_cast<const float4*>(at_bytes(dob, off));
-  }
+  // the dO slab staged at the end of this chunk's step: that of the chunk
+  // before it (reverse order), so it has two steps to arrive
+  rev_load_dO<T>(f.dO, ba, max(i - 1, 0), x);
   f.gC = GATE == kGateScalar ? a.G[x.bh * a.Tpad + t0 + C - 1] : 0.f;
   const float* bb = a.beta + (x.b * a.T + t0) * a.H + x.h;
 #pragma unroll
@@ -142,15 +157,16 @@ __device__ __forceinline__ void rev_stage_dO(const float4 (&v)[Slab<T>::kPer], T
   for (int j = 0; j < SM::kPer; ++j) {
     const int idx = tid + 256 * j;
     const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
-    const T* e = reinterpret_cast<const T*>(&v[j]);
+    const float4 raw = pin_here(v[j]);
+    const T* e = reinterpret_cast<const T*>(&raw);
 #pragma unroll
     for (int s2 = 0; s2 < SM::kVec; ++s2)
-      sDO[(c0 + s2) * LDE + row] = from_f<T>(row < n ? scale * to_f(e[s2]) : 0.f);
+      *sw(sDO, LDE, c0 + s2, row) = from_f<T>(row < n ? scale * to_f(e[s2]) : 0.f);
   }
 }
 
 template <bool FULL, typename T, int DK, int GATE>
-__device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, const RevFrags<T, DK>& fnext, bool stage_next,
+__device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, bool stage_next,
                                          floatx4 (&st)[DK / 64][2], const BwdArgs& ba, int i,
                                          const RevCtx& x, T* sH, T* sDOc, T* sDOn, T* sE, T* sX,
                                          T* sZ) {
@@ -169,7 +185,7 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, const RevFrags<T, D
       float4 pk;
       T* e = reinterpret_cast<T*>(&pk);
 #pragma unroll
-      for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = sH[(c0 + s2) * LDH + row];
+      for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = *sw(sH, LDH, c0 + s2, row);
       *reinterpret_cast<float4*>(dst + row * a.dv + c0) = pk;
     }
   }
@@ -178,10 +194,10 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, const RevFrags<T, D
   for (int vt = 0; vt < 2; ++vt) {
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Pt[k2], ld8(sDOc + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg));
+    for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Pt[k2], ld8(sw(sDOc, LDE, 16 * vt + lr, k2 * 32 + 8 * lg)));
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) mma(acc, f.Kw[kk], ld8(sH + (16 * vt + lr) * LDH + kk * 32 + 8 * lg));
-    st4<T>(sE + (16 * vt + lr) * LDE + 16 * w + 4 * lg, acc[0], acc[1], acc[2], acc[3]);
+    for (int kk = 0; kk < KK; ++kk) mma(acc, f.Kw[kk], ld8(sw(sH, LDH, 16 * vt + lr, kk * 32 + 8 * lg)));
+    st4<T>(sw(sE, LDE, 16 * vt + lr, 16 * w + 4 * lg), acc[0], acc[1], acc[2], acc[3]);
   }
   lds_barrier_b();
   // ---- Z = M^T dE;  dX = Diag(beta) Z   (rows t = 16w + 4lg + ii)
@@ -192,9 +208,9 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, const RevFrags<T, D
   for (int vt = 0; vt < 2; ++vt) {
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Mt[k2], ld8(sE + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg));
-    st4<T>(sZ + (16 * vt + lr) * LDE + 16 * w + 4 * lg, acc[0], acc[1], acc[2], acc[3]);
-    st4<T>(sX + (16 * vt + lr) * LDE + 16 * w + 4 * lg, bt[0] * acc[0], bt[1] * acc[1], bt[2] * acc[2],
+    for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Mt[k2], ld8(sw(sE, LDE, 16 * vt + lr, k2 * 32 + 8 * lg)));
+    st4<T>(sw(sZ, LDE, 16 * vt + lr, 16 * w + 4 * lg), acc[0], acc[1], acc[2], acc[3]);
+    st4<T>(sw(sX, LDE, 16 * vt + lr, 16 * w + 4 * lg), bt[0] * acc[0], bt[1] * acc[1], bt[2] * acc[2],
            bt[3] * acc[3]);
   }
   lds_barrier_b();
@@ -212,8 +228,8 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, const RevFrags<T, D
   for (int vt = 0; vt < 2; ++vt)
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
-      bD[vt][k2] = ld8(sDOc + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg);
-      bX[vt][k2] = ld8(sX + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg);
+      bD[vt][k2] = ld8(sw(sDOc, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
+      bX[vt][k2] = ld8(sw(sX, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
     }
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
@@ -226,10 +242,10 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, const RevFrags<T, D
         mma(st[ct][vt], f.Ql[ct][k2], bD[vt][k2]);
         mma(st[ct][vt], f.Kn[ct][k2], bX[vt][k2]);
       }
-      st4<T>(sH + (16 * vt + lr) * LDH + 16 * (w * CT + ct) + 4 * lg, st[ct][vt][0], st[ct][vt][1],
+      st4<T>(sw(sH, LDH, 16 * vt + lr, 16 * (w * CT + ct) + 4 * lg), st[ct][vt][0], st[ct][vt][1],
              st[ct][vt][2], st[ct][vt][3]);
     }
-  if (stage_next) rev_stage_dO<T>(fnext.dO, sDOn, C, a.scale, x.tid);  // earlier chunks are full
+  if (stage_next) rev_stage_dO<T>(f.dO, sDOn, C, a.scale, x.tid);  // earlier chunks are full
   lds_barrier_b();
 }
 
@@ -275,27 +291,29 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
   for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
     for (int vt = 0; vt < 2; ++vt)
-      st4<T>(sH + (16 * vt + lr) * LDH + 16 * (w * CT + ct) + 4 * lg, st[ct][vt][0], st[ct][vt][1],
+      st4<T>(sw(sH, LDH, 16 * vt + lr, 16 * (w * CT + ct) + 4 * lg), st[ct][vt][0], st[ct][vt][1],
              st[ct][vt][2], st[ct][vt][3]);
   // reverse order: the (possibly ragged) last chunk first, then the full
   // chunks two per trip with a branch-free body; dO slabs double-buffered
   const int NT = a.NT;
   RevFrags<T, DK> fA, fB;
+  float4 dlast[Slab<T>::kPer];
+  rev_load_dO<T>(dlast, ba, NT - 1, x);
   rev_load<T, DK, GATE>(fA, ba, NT - 1, x);
   rev_load<T, DK, GATE>(fB, ba, max(NT - 2, 0), x);
-  rev_stage_dO<T>(fA.dO, sDO[0], static_cast<int>(a.T - static_cast<int64_t>(NT - 1) * C), a.scale, x.tid);
+  rev_stage_dO<T>(dlast, sDO[0], static_cast<int>(a.T - static_cast<int64_t>(NT - 1) * C), a.scale, x.tid);
   __syncthreads();
-  rev_step<false, T, DK, GATE>(fA, fB, NT > 1, st, ba, NT - 1, x, sH, sDO[0], sDO[1], sE, sX, sZ);
+  rev_step<false, T, DK, GATE>(fA, NT > 1, st, ba, NT - 1, x, sH, sDO[0], sDO[1], sE, sX, sZ);
   int i = NT - 2, buf = 1;
   for (; i >= 1; i -= 2) {
     rev_load<T, DK, GATE>(fA, ba, i - 1, x);
-    rev_step<true, T, DK, GATE>(fB, fA, true, st, ba, i, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
+    rev_step<true, T, DK, GATE>(fB, true, st, ba, i, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
     buf ^= 1;
     rev_load<T, DK, GATE>(fB, ba, max(i - 2, 0), x);
-    rev_step<true, T, DK, GATE>(fA, fB, true, st, ba, i - 1, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
+    rev_step<true, T, DK, GATE>(fA, true, st, ba, i - 1, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
     buf ^= 1;
   }
-  if (i == 0) rev_step<true, T, DK, GATE>(fB, fA, false, st, ba, 0, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
+  if (i == 0) rev_step<true, T, DK, GATE>(fB, false, st, ba, 0, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
   if (ba.dS0) {
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
@@ -374,10 +392,11 @@ __device__ __forceinline__ void stage_rows(T* dst, const T* src, int tid) {
 // their outputs are not stored.
 template <typename T, int DK, int DV>
 struct P12Smem {
-  static constexpr int HC = 64;                 // key columns per phase-B pass
+  static constexpr int HC = 32;                 // key columns per phase-B pass
   static constexpr int LDE = DV + 8, LDK = DK + 8, LDV = DV + 8, LDT = C + 8;
+  static constexpr int LDO = HC + 16;           // output staging rows (bank-spread)
   static constexpr size_t kA = sizeof(T) * (C * LDE + C * LDK + 4 * C * LDT);
-  static constexpr size_t kB = sizeof(T) * (2 * HC * LDV + 3 * HC * LDT);
+  static constexpr size_t kB = sizeof(T) * (2 * HC * LDV + 3 * HC * LDT + 4 * 3 * 16 * LDO);
   static constexpr size_t kMain = kA > kB ? kA : kB;
   static constexpr size_t kTotal = kMain + sizeof(float) * (12 * C + 4);
 };
@@ -386,6 +405,7 @@ template <typename T, int DK, int DV, int GATE>
 __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   using SM = P12Smem<T, DK, DV>;
   constexpr int HC = SM::HC, LDE = SM::LDE, LDK = SM::LDK, LDV = SM::LDV, LDT = SM::LDT;
+  constexpr int LDO = SM::LDO;
   constexpr int KV = DV / 32, KD = DK / 32, NPASS = DK / HC;
   constexpr uint32_t E = sizeof(T);
   __shared__ __attribute__((aligned(16))) char smem[SM::kTotal];
@@ -402,6 +422,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   T* sKtT = sdS + HC * LDV;
   T* sQT = sKtT + HC * LDT;
   T* sKT = sQT + HC * LDT;
+  T* sOut = sKT + HC * LDT;             // per wave: dq, dK, dKt rows [3][16][LDO]
   float* sG = reinterpret_cast<float*>(smem + SM::kMain);
   float* sBeta = sG + C;
   float* sDb = sBeta + C;    // At term of dbeta
@@ -539,10 +560,9 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       }
     }
   }
-  // E rows of this wave (phase B's A operand of A3)
+  // E rows of this wave (phase B's A operand of A3), from the staged copy
 #pragma unroll
-  for (int kk = 0; kk < KV; ++kk)
-    fE[kk] = ld8(at_bytes(eb, (static_cast<uint32_t>(ra * DV) + 32 * kk + 8 * lg) * E));
+  for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sE + ra * LDE + 32 * kk + 8 * lg);
   __syncthreads();
   // the C x C adjoints as A fragments of this wave's rows (k = 32 k2 + 8 lg)
   Frag8<T> fSq[2], fSk[2], fSqT[2], fSkT[2];
@@ -635,12 +655,28 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
         mma(at, fSqT[k2], ld8(sQT + (16 * j + lr) * LDT + 32 * k2 + 8 * lg));
         mma(at, fSkT[k2], ld8(sKT + (16 * j + lr) * LDT + 32 * k2 + 8 * lg));
       }
+      // to this wave's output rows in LDS (rows 4 lg + ii, column c)
+      T* so = sOut + w * 3 * 16 * LDO;
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
-        const int r = 16 * w + 4 * lg + ii, cg = c0 + c;
-        if (r < n) dq[r * HD + cg] = from_f<T>(aq[ii]);
-        dKm[r * DK + cg] = from_f<T>(ak[ii]);
-        dKt[r * DK + cg] = from_f<T>(at[ii]);
+        so[(4 * lg + ii) * LDO + c] = from_f<T>(aq[ii]);
+        so[(16 + 4 * lg + ii) * LDO + c] = from_f<T>(ak[ii]);
+        so[(32 + 4 * lg + ii) * LDO + c] = from_f<T>(at[ii]);
+      }
+    }
+    {
+      // this wave's 16 rows x HC columns of dq, dK, dKt: 16-byte stores
+      // (the wave reads back only what it wrote: no barrier needed)
+      constexpr int VEC = 16 / sizeof(T), SPR = HC / VEC;
+      const T* so = sOut + w * 3 * 16 * LDO;
+      for (int idx = l; idx < 16 * SPR; idx += 64) {
+        const int rr = idx / SPR, sgc = (idx % SPR) * VEC, r = 16 * w + rr;
+        const float4 vq = *reinterpret_cast<const float4*>(so + rr * LDO + sgc);
+        const float4 vk = *reinterpret_cast<const float4*>(so + (16 + rr) * LDO + sgc);
+        const float4 vt = *reinterpret_cast<const float4*>(so + (32 + rr) * LDO + sgc);
+        if (r < n) *reinterpret_cast<float4*>(dq + r * HD + c0 + sgc) = vq;
+        *reinterpret_cast<float4*>(dKm + r * DK + c0 + sgc) = vk;
+        *reinterpret_cast<float4*>(dKt + r * DK + c0 + sgc) = vt;
       }
     }
   }

@@ -104,6 +104,29 @@ __device__ __forceinline__ void mma4(floatx4& acc, float a, float b) {
   acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
 }
 
+// Address of element (row, col) of an LDS slab [rows][ld] whose rows are
+// also read across (a transposed column: one element from each of many
+// rows).  With row strides of 72 or 136 elements, rows 8 apart fall on the
+// same banks; XOR-ing the column by 16 * ((row >> 3) & 3) spreads them over
+// distinct banks and keeps every aligned run of 16 elements contiguous, so
+// 4- and 8-element vector accesses stay whole.
+template <typename T>
+__device__ __forceinline__ T* sw(T* base, int ld, int row, int col) {
+  return base + row * ld + (col ^ (((row >> 3) & 3) << 4));
+}
+template <typename T>
+__device__ __forceinline__ const T* sw(const T* base, int ld, int row, int col) {
+  return base + row * ld + (col ^ (((row >> 3) & 3) << 4));
+}
+
+// Pins a prefetched 16-byte value to this point of the program: the empty
+// volatile asm "redefines" it, so unpacking it cannot be hoisted up to its
+// load (the wait for the load would then drain every later prefetch too).
+__device__ __forceinline__ float4 pin_here(float4 v) {
+  asm volatile("" : "+v"(v.x), "+v"(v.y), "+v"(v.z), "+v"(v.w));
+  return v;
+}
+
 // 4 consecutive elements (8 / 16 bytes), used to stage accumulator columns
 template <typename T> struct Vec4;
 template <> struct Vec4<bf16> { typedef bf16x4 type; };

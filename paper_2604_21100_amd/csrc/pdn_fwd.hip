@@ -564,9 +564,10 @@ __device__ __forceinline__ void stage_values(const float4 (&v)[SlabMap<T>::kPer]
   for (int j = 0; j < SM::kPer; ++j) {
     const int idx = tid + 256 * j;
     const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
-    const T* e = reinterpret_cast<const T*>(&v[j]);
+    const float4 raw = pin_here(v[j]);
+    const T* e = reinterpret_cast<const T*>(&raw);
 #pragma unroll
-    for (int s = 0; s < SM::kVec; ++s) sVt[(c0 + s) * LDE + row] = e[s];
+    for (int s = 0; s < SM::kVec; ++s) *sw(sVt, LDE, c0 + s, row) = e[s];
   }
 }
 
@@ -587,7 +588,7 @@ __device__ __forceinline__ void flush_output(const FwdArgs& a, int i, int n, con
     float4 pk;
     T* e = reinterpret_cast<T*>(&pk);
 #pragma unroll
-    for (int s = 0; s < SM::kVec; ++s) e[s] = sO[(c0 + s) * LDE + row];
+    for (int s = 0; s < SM::kVec; ++s) e[s] = *sw(sO, LDE, c0 + s, row);
     if (row < n)
       *reinterpret_cast<float4*>(at_bytes(ob, (static_cast<uint32_t>(row) * static_cast<uint32_t>(HV) + c0) *
                                                   static_cast<uint32_t>(sizeof(T)))) = pk;
@@ -609,7 +610,7 @@ __device__ __forceinline__ void flush_slab_t(T* dst, int64_t ld, const T* src, i
     float4 pk;
     T* e = reinterpret_cast<T*>(&pk);
 #pragma unroll
-    for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = src[(c0 + s2) * lds + row];
+    for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = *sw(src, lds, c0 + s2, row);
     *reinterpret_cast<float4*>(dst + row * ld + c0) = pk;
   }
 }
@@ -644,11 +645,11 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt)
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) bH[vt][kk] = ld8(sH + (16 * vt + lr) * LDH + kk * 32 + 8 * lg);
+    for (int kk = 0; kk < KK; ++kk) bH[vt][kk] = ld8(sw(sH, LDH, 16 * vt + lr, kk * 32 + 8 * lg));
   typename Vec4<T>::type vv[2];
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt)
-    vv[vt] = *reinterpret_cast<const typename Vec4<T>::type*>(sVt + (16 * vt + lr) * LDE + 16 * w + 4 * lg);
+    vv[vt] = *reinterpret_cast<const typename Vec4<T>::type*>(sw(sVt, LDE, 16 * vt + lr, 16 * w + 4 * lg));
   floatx4 accX[2], accO[2];
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt) {
@@ -664,7 +665,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
       accX[vt][ii] = to_f(vv[vt][ii]) - lam[ii] * accX[vt][ii];
       if (OUT) accO[vt][ii] *= lam[ii];
     }
-    st4<T>(sX + (16 * vt + lr) * LDE + 16 * w + 4 * lg, accX[vt][0], accX[vt][1], accX[vt][2],
+    st4<T>(sw(sX, LDE, 16 * vt + lr, 16 * w + 4 * lg), accX[vt][0], accX[vt][1], accX[vt][2],
            accX[vt][3]);
   }
   lds_barrier();
@@ -673,13 +674,13 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt)
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) bX[vt][k2] = ld8(sX + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg);
+    for (int k2 = 0; k2 < 2; ++k2) bX[vt][k2] = ld8(sw(sX, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt) {
     floatx4 accE = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) mma(accE, f.Tm[k2], bX[vt][k2]);
-    st4<T>(sE + (16 * vt + lr) * LDE + 16 * w + 4 * lg, accE[0], accE[1], accE[2], accE[3]);
+    st4<T>(sw(sE, LDE, 16 * vt + lr, 16 * w + 4 * lg), accE[0], accE[1], accE[2], accE[3]);
   }
   lds_barrier();
   if (SAVE) {  // E rows of this chunk (whole chunk: padded rows included)
@@ -691,13 +692,13 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt)
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) fE[vt][k2] = ld8(sE + (16 * vt + lr) * LDE + k2 * 32 + 8 * lg);
+    for (int k2 = 0; k2 < 2; ++k2) fE[vt][k2] = ld8(sw(sE, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
 #pragma unroll
   for (int vt = 0; vt < 2 && OUT; ++vt) {
     // P is causal: for rows < 32 its second slab is zero
     mma(accO[vt], f.P[0], fE[vt][0]);
     mma(accO[vt], f.P[1], fE[vt][1]);
-    st4<T>(sO + (16 * vt + lr) * LDE + 16 * w + 4 * lg, a.scale * accO[vt][0], a.scale * accO[vt][1],
+    st4<T>(sw(sO, LDE, 16 * vt + lr, 16 * w + 4 * lg), a.scale * accO[vt][0], a.scale * accO[vt][1],
            a.scale * accO[vt][2], a.scale * accO[vt][3]);
   }
 #pragma unroll
@@ -713,7 +714,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
       }
       mma(st[ct][vt], f.G[ct][0], fE[vt][0]);
       mma(st[ct][vt], f.G[ct][1], fE[vt][1]);
-      st4<T>(sH + (16 * vt + lr) * LDH + 16 * (w * CT + ct) + 4 * lg, st[ct][vt][0], st[ct][vt][1],
+      st4<T>(sw(sH, LDH, 16 * vt + lr, 16 * (w * CT + ct) + 4 * lg), st[ct][vt][0], st[ct][vt][1],
              st[ct][vt][2], st[ct][vt][3]);
     }
   if (vnext) stage_values<T>(*reinterpret_cast<const float4(*)[SlabMap<T>::kPer]>(vnext), sVt, x.tid);
@@ -727,6 +728,7 @@ template <typename T, int DK, int GATE, bool SAVE, bool OUT>
 __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   constexpr int CT = DK / 64;       // state row tiles per wave
   constexpr int LDH = DK + 8, LDE = C + 8;
+  // [v][.] slabs, addressed through sw() (bank-spread)
   __shared__ __attribute__((aligned(16))) T sH[BV * LDH];   // io copy of the S^T slab, [v][c]
   __shared__ __attribute__((aligned(16))) T sX[BV * LDE];   // X = V - Lam K S^T, [v][t]
   __shared__ __attribute__((aligned(16))) T sE[BV * LDE];   // E = T X, [v][t]
@@ -767,7 +769,7 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
     for (int vt = 0; vt < 2; ++vt)
-      st4<T>(sH + (16 * vt + lr) * LDH + 16 * (w * CT + ct) + 4 * lg, st[ct][vt][0],
+      st4<T>(sw(sH, LDH, 16 * vt + lr, 16 * (w * CT + ct) + 4 * lg), st[ct][vt][0],
              st[ct][vt][1], st[ct][vt][2], st[ct][vt][3]);
 
   // software pipeline, three deep: chunk i+2's operands load while chunk i
