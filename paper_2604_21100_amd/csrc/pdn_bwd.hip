@@ -328,24 +328,7 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
 }
 
 // ------------------------------------------------------------ p1
-template <typename T, int DD>
-__device__ __forceinline__ void load_rows(T* dst, int ldd, const T* src, int64_t lds, int nvalid,
-                                          int tid, float scale = 1.f) {
-  constexpr int VEC = 16 / sizeof(T), VPR = DD / VEC;
-  for (int idx = tid; idx < C * VPR; idx += 256) {
-    const int r = idx / VPR, cv = idx % VPR;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < nvalid) v = *reinterpret_cast<const float4*>(src + r * lds + cv * VEC);
-    if (scale != 1.f) {
-      T* e = reinterpret_cast<T*>(&v);
-#pragma unroll
-      for (int s2 = 0; s2 < VEC; ++s2) e[s2] = from_f<T>(scale * to_f(e[s2]));
-    }
-    *reinterpret_cast<float4*>(dst + r * ldd + cv * VEC) = v;
-  }
-}
-
-// rows [C][DD] of src -> dst[DD][C + 8] (transposed)
+// rows [C][DD] of src -> dst[DD][C + 8] (transposed; read back through sw())
 template <typename T, int DD>
 __device__ __forceinline__ void load_rows_t(T* dst, const T* src, int64_t lds, int nvalid, int tid) {
   constexpr int VEC = 16 / sizeof(T), VPR = DD / VEC, LDT = C + 8;
@@ -355,17 +338,18 @@ __device__ __forceinline__ void load_rows_t(T* dst, const T* src, int64_t lds, i
     if (r < nvalid) v = *reinterpret_cast<const float4*>(src + r * lds + cv * VEC);
     const T* e = reinterpret_cast<const T*>(&v);
 #pragma unroll
-    for (int s2 = 0; s2 < VEC; ++s2) dst[(cv * VEC + s2) * LDT + r] = e[s2];
+    for (int s2 = 0; s2 < VEC; ++s2) *sw(dst, LDT, cv * VEC + s2, r) = e[s2];
   }
 }
 
-// Rows [C][DD] of a workspace tensor -> LDS rows [C][DD + 8] (16-byte copies)
+// Rows [C][DD] of a workspace tensor -> LDS rows [C][DD + 8] (16-byte copies,
+// bank-spread addressing: read back through sw())
 template <typename T, int DD>
 __device__ __forceinline__ void stage_rows(T* dst, const T* src, int tid) {
   constexpr int VEC = 16 / sizeof(T), VPR = DD / VEC, LD = DD + 8;
   for (int idx = tid; idx < C * VPR; idx += 256) {
     const int r = idx / VPR, cv = idx % VPR;
-    *reinterpret_cast<float4*>(dst + r * LD + cv * VEC) = *reinterpret_cast<const float4*>(src + r * DD + cv * VEC);
+    *reinterpret_cast<float4*>(sw(dst, LD, r, cv * VEC)) = *reinterpret_cast<const float4*>(src + r * DD + cv * VEC);
   }
 }
 
@@ -503,7 +487,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       if (j <= w) {
 #pragma unroll
         for (int kk = 0; kk < KD; ++kk) {
-          const Frag8<T> fk = ld8(sKt + (16 * j + lr) * LDK + 32 * kk + 8 * lg);
+          const Frag8<T> fk = ld8(sw(sKt, LDK, 16 * j + lr, 32 * kk + 8 * lg));
           mma(Sqk[j], fQ[kk], fk);
           mma(Skk[j], fK[kk], fk);
         }
@@ -516,7 +500,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       if (j <= w) {
 #pragma unroll
         for (int kk = 0; kk < KV; ++kk) {
-          const Frag8<T> fe = ld8(sE + (16 * j + lr) * LDE + 32 * kk + 8 * lg);
+          const Frag8<T> fe = ld8(sw(sE, LDE, 16 * j + lr, 32 * kk + 8 * lg));
           mma(dP, fO[kk], fe);
           mma(dL, fZ[kk], fe);
         }
@@ -537,10 +521,13 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
         rs[ii] += R;
         csum += R;
       }
-      st_tile<T>(sSq + (16 * w) * LDT + 16 * j, LDT, dq, lr, lg);
-      st_tile_t<T>(sSqT + (16 * j) * LDT + 16 * w, LDT, dq, lr, lg);
-      st_tile<T>(sSk + (16 * w) * LDT + 16 * j, LDT, dk, lr, lg);
-      st_tile_t<T>(sSkT + (16 * j) * LDT + 16 * w, LDT, dk, lr, lg);
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        *sw(sSq, LDT, 16 * w + 4 * lg + ii, 16 * j + lr) = from_f<T>(dq[ii]);
+        *sw(sSk, LDT, 16 * w + 4 * lg + ii, 16 * j + lr) = from_f<T>(dk[ii]);
+      }
+      st4<T>(sw(sSqT, LDT, 16 * j + lr, 16 * w + 4 * lg), dq[0], dq[1], dq[2], dq[3]);
+      st4<T>(sw(sSkT, LDT, 16 * j + lr, 16 * w + 4 * lg), dk[0], dk[1], dk[2], dk[3]);
       csum += __shfl_xor(csum, 16, 64);
       csum += __shfl_xor(csum, 32, 64);
       if (lg == 0) sCs[w * C + 16 * j + lr] = csum;
@@ -562,17 +549,17 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   }
   // E rows of this wave (phase B's A operand of A3), from the staged copy
 #pragma unroll
-  for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sE + ra * LDE + 32 * kk + 8 * lg);
+  for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, ra, 32 * kk + 8 * lg));
   __syncthreads();
   // the C x C adjoints as A fragments of this wave's rows (k = 32 k2 + 8 lg)
   Frag8<T> fSq[2], fSk[2], fSqT[2], fSkT[2];
 #pragma unroll
   for (int k2 = 0; k2 < 2; ++k2) {
-    const int o = ra * LDT + 32 * k2 + 8 * lg;
-    fSq[k2] = ld8(sSq + o);
-    fSk[k2] = ld8(sSk + o);
-    fSqT[k2] = ld8(sSqT + o);
-    fSkT[k2] = ld8(sSkT + o);
+    const int o = 32 * k2 + 8 * lg;
+    fSq[k2] = ld8(sw(sSq, LDT, ra, o));
+    fSk[k2] = ld8(sw(sSk, LDT, ra, o));
+    fSqT[k2] = ld8(sw(sSqT, LDT, ra, o));
+    fSkT[k2] = ld8(sw(sSkT, LDT, ra, o));
   }
   if (tid < C) {
     // Gam_rt = exp(G_r - G_t): d/dG_r of sum R_rt = row sum, d/dG_t = -column sum
@@ -604,9 +591,9 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       const T* dHs = static_cast<const T*>(ba.dHs) + cs + c0 * DV;
       for (int idx = tid; idx < HC * VPR; idx += 256) {
         const int c = idx / VPR, cv = idx % VPR;
-        *reinterpret_cast<float4*>(sS + c * LDV + cv * VEC) =
+        *reinterpret_cast<float4*>(sw(sS, LDV, c, cv * VEC)) =
             *reinterpret_cast<const float4*>(Hs + c * DV + cv * VEC);
-        *reinterpret_cast<float4*>(sdS + c * LDV + cv * VEC) =
+        *reinterpret_cast<float4*>(sw(sdS, LDV, c, cv * VEC)) =
             *reinterpret_cast<const float4*>(dHs + c * DV + cv * VEC);
       }
     }
@@ -617,15 +604,15 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
     // sum(dS' o S) over this pass's rows
     for (int idx = tid; idx < HC * DV; idx += 256) {
       const int c = idx / DV, v = idx % DV;
-      red += to_f(sS[c * LDV + v]) * to_f(sdS[c * LDV + v]);
+      red += to_f(*sw(sS, LDV, c, v)) * to_f(*sw(sdS, LDV, c, v));
     }
 #pragma unroll 1
     for (int j = 0; j < HC / 16; ++j) {
       floatx4 A1 = {0.f, 0.f, 0.f, 0.f}, A2 = A1, A3 = A1;
 #pragma unroll
       for (int kk = 0; kk < KV; ++kk) {
-        const Frag8<T> fh = ld8(sS + (16 * j + lr) * LDV + 32 * kk + 8 * lg);
-        const Frag8<T> fd = ld8(sdS + (16 * j + lr) * LDV + 32 * kk + 8 * lg);
+        const Frag8<T> fh = ld8(sw(sS, LDV, 16 * j + lr, 32 * kk + 8 * lg));
+        const Frag8<T> fd = ld8(sw(sdS, LDV, 16 * j + lr, 32 * kk + 8 * lg));
         mma(A1, fO[kk], fh);
         mma(A2, fZ[kk], fh);
         mma(A3, fE[kk], fd);
@@ -636,9 +623,9 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       for (int ii = 0; ii < 4; ++ii) {
         const int r = 16 * w + 4 * lg + ii;
         A1[ii] *= a.scale;
-        pq[ii] += to_f(sQT[c * LDT + r]) * A1[ii];
-        pk[ii] += to_f(sKT[c * LDT + r]) * A2[ii];
-        pw[ii] += to_f(sKtT[c * LDT + r]) * A3[ii];
+        pq[ii] += to_f(*sw(sQT, LDT, c, r)) * A1[ii];
+        pk[ii] += to_f(*sw(sKT, LDT, c, r)) * A2[ii];
+        pw[ii] += to_f(*sw(sKtT, LDT, c, r)) * A3[ii];
       }
       floatx4 aq, ak, at;
 #pragma unroll
@@ -649,11 +636,11 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       }
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
-        const Frag8<T> fk = ld8(sKtT + (16 * j + lr) * LDT + 32 * k2 + 8 * lg);
+        const Frag8<T> fk = ld8(sw(sKtT, LDT, 16 * j + lr, 32 * k2 + 8 * lg));
         mma(aq, fSq[k2], fk);
         mma(ak, fSk[k2], fk);
-        mma(at, fSqT[k2], ld8(sQT + (16 * j + lr) * LDT + 32 * k2 + 8 * lg));
-        mma(at, fSkT[k2], ld8(sKT + (16 * j + lr) * LDT + 32 * k2 + 8 * lg));
+        mma(at, fSqT[k2], ld8(sw(sQT, LDT, 16 * j + lr, 32 * k2 + 8 * lg)));
+        mma(at, fSkT[k2], ld8(sw(sKT, LDT, 16 * j + lr, 32 * k2 + 8 * lg)));
       }
       // to this wave's output rows in LDS (rows 4 lg + ii, column c)
       T* so = sOut + w * 3 * 16 * LDO;
