@@ -196,8 +196,8 @@ pdn_status pdn_chunk_bwd_events(const pdn_problem* problem, const pdn_inputs* in
  * library cannot detect a violation; results are then undefined, but every
  * access stays inside the declared buffers).  pdn_chunk_bwd_train leaves the
  * saved intermediates intact, so it may be called again for another dO.
- * The backward's restrictions apply to both calls (no per-channel gate; fp32
- * io only with d_k = d_v = 64: PDN_ERR_UNSUPPORTED).
+ * The backward's restriction applies to both calls (fp32 io only with
+ * d_k = d_v = 64: PDN_ERR_UNSUPPORTED).
  *
  * stage_events: NULL with n_events = 0, or PDN_FWD_STAGE_EVENTS /
  * PDN_BWD_STAGE_EVENTS caller-created events recorded as in the _events

@@ -1,5 +1,5 @@
 // Backward kernels of the chunkwise preconditioned delta rule for gfx950
-// (PDN and PGDN: no gate or a scalar gate).
+// (PDN, PGDN and PKDA: no gate, a scalar or a per-channel gate).
 //
 // The gradient is the exact adjoint of the chunkwise forward (Eq.
 // chunkwise_atk_form with the decayed forms of App. D).  Per chunk, with
@@ -31,6 +31,8 @@
 //                      dX (= dv)
 //   p12_chunk_grads    per chunk: the C x C adjoints (dSqk, dSkk), dq, the
 //                      read- and write-key gradients, dbeta, dg
+//   p12c_chunk_grads   the same for the per-channel gate (decay inside the
+//                      key contractions; dg per channel)
 //   pc_*               preconditioner: reverse scan over tokens of the
 //                      diagonal Gram recurrence (dk, dbetaP, dgP, dlogAScale,
 //                      dA0)
@@ -69,12 +71,14 @@ __device__ __forceinline__ void slab_to_rows(T* dst, int64_t ld, const T* src, i
 }
 
 // ------------------------------------------------------------ r1
-template <typename T, int DK>
+template <typename T, int DK, int GATE>
 struct RevFrags {
   static constexpr int KK = DK / 32, CT = DK / 64;
   Frag8<T> Pt[2], Kw[KK], Mt[2], Ql[CT][2], Kn[CT][2];
   float4 dO[Slab<T>::kPer];   // dO slab of the chunk before this one
-  float gC;
+  // log decay at the chunk end: scalar, or per channel of the state rows
+  // c = 16 (w CT + ct) + 4 lg + ii this lane holds
+  float gC[GATE == kGateChannel ? CT : 1][GATE == kGateChannel ? 4 : 1];
   float beta[4];   // beta of rows 16w + 4lg + ii (raw: past the end masked at use)
 };
 
@@ -105,7 +109,7 @@ __device__ __forceinline__ void rev_load_dO(float4 (&d)[Slab<T>::kPer], const Bw
 }
 
 template <typename T, int DK, int GATE>
-__device__ __forceinline__ void rev_load(RevFrags<T, DK>& f, const BwdArgs& ba, int i,
+__device__ __forceinline__ void rev_load(RevFrags<T, DK, GATE>& f, const BwdArgs& ba, int i,
                                          const RevCtx& x) {
   constexpr int KK = DK / 32, CT = DK / 64;
   constexpr uint32_t E = sizeof(T);
@@ -141,7 +145,14 @@ __device__ __forceinline__ void rev_load(RevFrags<T, DK>& f, const BwdArgs& ba, 
   // the dO slab staged at the end of this chunk's step: that of the chunk
   // before it (reverse order), so it has two steps to arrive
   rev_load_dO<T>(f.dO, ba, max(i - 1, 0), x);
-  f.gC = GATE == kGateScalar ? a.G[x.bh * a.Tpad + t0 + C - 1] : 0.f;
+  if (GATE == kGateScalar) f.gC[0][0] = a.G[x.bh * a.Tpad + t0 + C - 1];
+  if (GATE == kGateChannel) {
+    const float* gl = a.G + (x.bh * a.Tpad + t0 + C - 1) * DK;
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) f.gC[ct][ii] = gl[16 * (x.w * CT + ct) + 4 * x.lg + ii];
+  }
   const float* bb = a.beta + (x.b * a.T + t0) * a.H + x.h;
 #pragma unroll
   for (int ii = 0; ii < 4; ++ii) f.beta[ii] = bb[min(16 * x.w + 4 * x.lg + ii, last) * a.H];
@@ -166,7 +177,7 @@ __device__ __forceinline__ void rev_stage_dO(const float4 (&v)[Slab<T>::kPer], T
 }
 
 template <bool FULL, typename T, int DK, int GATE>
-__device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, bool stage_next,
+__device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE>& f, bool stage_next,
                                          floatx4 (&st)[DK / 64][2], const BwdArgs& ba, int i,
                                          const RevCtx& x, T* sH, T* sDOc, T* sDOn, T* sE, T* sX,
                                          T* sZ) {
@@ -221,8 +232,8 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, bool stage_next,
     slab_to_rows<T>(static_cast<T*>(ba.dv) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0, HV, sX, LDE, C,
                     n, x.tid);
   }
-  // ---- dS^T <- lam_C dS'^T + (Diag(lam) Q)^T dO_s - (Diag(lam) K)^T dX
-  const float gam = GATE == kGateScalar ? fast_exp(f.gC) : 1.f;
+  // ---- dS^T <- Diag(lam_C) dS'^T + (Lam o Q)^T dO_s - (Lam o K)^T dX
+  const float gam = GATE == kGateScalar ? fast_exp(f.gC[0][0]) : 1.f;
   Frag8<T> bD[2][2], bX[2][2];
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt)
@@ -236,7 +247,9 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK>& f, bool stage_next,
 #pragma unroll
     for (int vt = 0; vt < 2; ++vt) {
 #pragma unroll
-      for (int ii = 0; ii < 4; ++ii) st[ct][vt][ii] *= gam;
+      for (int ii = 0; ii < 4; ++ii) {
+        st[ct][vt][ii] *= GATE == kGateChannel ? fast_exp(f.gC[ct][ii]) : gam;
+      }
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
         mma(st[ct][vt], f.Ql[ct][k2], bD[vt][k2]);
@@ -296,7 +309,7 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
   // reverse order: the (possibly ragged) last chunk first, then the full
   // chunks two per trip with a branch-free body; dO slabs double-buffered
   const int NT = a.NT;
-  RevFrags<T, DK> fA, fB;
+  RevFrags<T, DK, GATE> fA, fB;
   float4 dlast[Slab<T>::kPer];
   rev_load_dO<T>(dlast, ba, NT - 1, x);
   rev_load<T, DK, GATE>(fA, ba, NT - 1, x);
@@ -717,6 +730,320 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   }
 }
 
+// ------------------------------------------------------------ p12c
+// p12 for the per-channel gate (PKDA).  The decay now sits inside the key
+// contractions: with Lam_r = exp(G_r) per channel, the chunk forward reads
+// Lam o Q, Lam o K, Kt / Lam and Kt o (Lam_C / Lam), so
+//   dq  = Lam o (dO_s S + dSqk (Kt / Lam))
+//   dK  = Diag(beta) Lam o (-Z S + dAt (Kt / Lam))          (read key)
+//   dKt = (dSqk^T (Lam o Q) + (Diag(beta) dAt)^T (Lam o K)) / Lam
+//         + (Lam_C / Lam) o E dS'
+// with dSqk = causal(dO_s E^T) and dAt = strict_lower(-Z E^T) carrying no
+// decay.  A decay ratio exp(G_r - G_t) (r >= t) is split at a reference
+// row per 16-row output block (its first row for dq and dK, its last for
+// dKt), so every factor applied to an operand or an output is at most 1
+// except inside the block itself; operand entries that only meet zeros of
+// the causal masks are set to zero rather than scaled.  The gate gradient
+// needs no C x C product: every place Lam enters is a product with one of
+// the outputs, so per channel
+//   dG_r = q_r dq_r + k_r dK_r - kt_r dKt_r
+//          + [r = C - 1] (sum_t kt_t (Lam_C / Lam_t) (E dS')_t
+//                         + Lam_C sum_v S dS')
+// and dg is its reverse in-chunk cumsum.  dbeta_r = Z_r . V_r +
+// sum_c k_rc (dK_rc / beta_r) takes the bracket before the beta factor.
+template <typename T, int DK, int DV>
+struct P12cSmem {
+  static constexpr int HC = 32;
+  static constexpr int LDE = DV + 8, LDV = DV + 8, LDT = C + 8, LDO = HC + 16, LDG = C + 4;
+  static constexpr size_t kA = sizeof(T) * (C * LDE + 4 * C * LDT);
+  static constexpr size_t kStage = sizeof(T) * (2 * HC * LDV + 3 * HC * LDT + 4 * 3 * 16 * LDO);
+  static constexpr size_t kB = kStage + sizeof(float) * (HC * LDG + C * (HC + 1));
+  static constexpr size_t kMain = kA > kB ? kA : kB;
+  static constexpr size_t kTotal = kMain + sizeof(float) * (3 * C + 4 * HC + HC + 8 * HC);
+};
+
+template <typename T, int DK, int DV>
+__global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
+  using SM = P12cSmem<T, DK, DV>;
+  constexpr int HC = SM::HC, LDE = SM::LDE, LDV = SM::LDV, LDT = SM::LDT, LDO = SM::LDO, LDG = SM::LDG;
+  constexpr int KV = DV / 32, NPASS = DK / HC;
+  constexpr uint32_t E = sizeof(T);
+  __shared__ __attribute__((aligned(16))) char smem[SM::kTotal];
+  // phase A
+  T* sE = reinterpret_cast<T*>(smem);
+  T* sSq = sE + C * LDE;      // dSqk rows [r][t]
+  T* sSk = sSq + C * LDT;     // dAt rows
+  T* sSqT = sSk + C * LDT;    // dSqk^T rows [t][r]
+  T* sSkT = sSqT + C * LDT;   // (Diag(beta) dAt)^T rows
+  // phase B
+  T* sS = reinterpret_cast<T*>(smem);
+  T* sdS = sS + HC * LDV;
+  T* sKtT = sdS + HC * LDV;
+  T* sQT = sKtT + HC * LDT;
+  T* sKT = sQT + HC * LDT;
+  T* sOut = sKT + HC * LDT;
+  float* sGT = reinterpret_cast<float*>(smem + SM::kStage);   // G^T [c][t]
+  float* sDG = sGT + HC * LDG;                                  // dG [t][c]
+  float* sBeta = reinterpret_cast<float*>(smem + SM::kMain);
+  float* sZV = sBeta + C;
+  float* sDb = sZV + C;
+  float* sXc = sDb + C;       // [4][HC] per-wave column sums of the last-row term
+  float* sRedC = sXc + 4 * HC;   // [HC] sum_v S dS' per channel
+  float* sSeg = sRedC + HC;      // [8][HC] segment totals of the cumsum
+
+  const FwdArgs& a = ba.f;
+  const int64_t blk = blockIdx.x;
+  const int64_t bh = blk / a.NT;
+  const int i = static_cast<int>(blk % a.NT);
+  const int64_t b = bh / a.H, h = bh % a.H;
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 15, lg = l >> 4;
+  const int64_t t0 = static_cast<int64_t>(i) * C;
+  const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
+  const int64_t HV = a.H * (int64_t)DV, HD = a.H * (int64_t)DK;
+  const int64_t rv = (bh * a.Tpad + t0) * DV, rk = (bh * a.Tpad + t0) * DK;
+  const int64_t cs = (bh * a.NT + i) * (int64_t)DK * DV;
+
+  const int ra = 16 * w + lr;
+  const uint32_t rc = static_cast<uint32_t>(min(ra, n - 1));
+  Frag8<T> fO[KV], fZ[KV], fE[KV];
+  const T* dob = static_cast<const T*>(ba.dO) + (b * a.T + t0) * HV + h * DV;
+  {
+    Frag8<T> fV[KV];
+    const T* vb = static_cast<const T*>(a.v) + (b * a.T + t0) * HV + h * DV;
+    const T* zb = static_cast<const T*>(ba.Zr) + rv;
+#pragma unroll
+    for (int kk = 0; kk < KV; ++kk) {
+      const uint32_t o = (rc * static_cast<uint32_t>(HV) + 32 * kk + 8 * lg) * E;
+      const uint32_t ow = (static_cast<uint32_t>(ra * DV) + 32 * kk + 8 * lg) * E;
+      fO[kk] = ld8(at_bytes(dob, o));
+      fV[kk] = ld8(at_bytes(vb, o));
+      fZ[kk] = ld8(at_bytes(zb, ow));
+    }
+    // Z_r . V_r (Z vanishes on rows past the end)
+    float zv = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KV; ++kk)
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) zv += fZ[kk].get(s2) * fV[kk].get(s2);
+    zv += __shfl_xor(zv, 16, 64);
+    zv += __shfl_xor(zv, 32, 64);
+    if (lg == 0) sZV[ra] = zv;
+  }
+  stage_rows<T, DV>(sE, static_cast<const T*>(a.Er) + rv, tid);
+  if (tid < C) sBeta[tid] = tid < n ? a.beta[(b * a.T + t0 + tid) * a.H + h] : 0.f;
+  __syncthreads();
+  // ---- phase A: dSqk = causal(dO_s E^T), dAt = strict_lower(-Z E^T)
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    floatx4 dP = {0.f, 0.f, 0.f, 0.f}, dL = dP;
+    if (j <= w) {
+#pragma unroll
+      for (int kk = 0; kk < KV; ++kk) {
+        const Frag8<T> fe = ld8(sw(sE, LDE, 16 * j + lr, 32 * kk + 8 * lg));
+        mma(dP, fO[kk], fe);
+        mma(dL, fZ[kk], fe);
+      }
+    }
+    floatx4 dq, dA, dAb;
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      const int r = 16 * w + 4 * lg + ii, t = 16 * j + lr;
+      dq[ii] = (r >= t && r < n) ? a.scale * dP[ii] : 0.f;
+      dA[ii] = r > t ? -dL[ii] : 0.f;
+      dAb[ii] = sBeta[r] * dA[ii];
+      *sw(sSq, LDT, r, t) = from_f<T>(dq[ii]);
+      *sw(sSk, LDT, r, t) = from_f<T>(dA[ii]);
+    }
+    st4<T>(sw(sSqT, LDT, 16 * j + lr, 16 * w + 4 * lg), dq[0], dq[1], dq[2], dq[3]);
+    st4<T>(sw(sSkT, LDT, 16 * j + lr, 16 * w + 4 * lg), dAb[0], dAb[1], dAb[2], dAb[3]);
+  }
+#pragma unroll
+  for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, ra, 32 * kk + 8 * lg));
+  __syncthreads();
+  Frag8<T> fSq[2], fSk[2], fSqT[2], fSkT[2];
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2) {
+    const int o = 32 * k2 + 8 * lg;
+    fSq[k2] = ld8(sw(sSq, LDT, ra, o));
+    fSk[k2] = ld8(sw(sSk, LDT, ra, o));
+    fSqT[k2] = ld8(sw(sSqT, LDT, ra, o));
+    fSkT[k2] = ld8(sw(sSkT, LDT, ra, o));
+  }
+  float bt[4];
+#pragma unroll
+  for (int ii = 0; ii < 4; ++ii) bt[ii] = sBeta[16 * w + 4 * lg + ii];
+
+  // ---- phase B
+  float pdb[4] = {0.f, 0.f, 0.f, 0.f};
+  T* dq = static_cast<T*>(ba.dq) + (b * a.T + t0) * HD + h * DK;
+  T* dKm = static_cast<T*>(ba.dKm) + rk;
+  T* dKt = static_cast<T*>(ba.dKt) + rk;
+  const float* Gc = a.G + rk;   // in-chunk log-decay prefix rows [t][c]
+#pragma unroll 1
+  for (int p = 0; p < NPASS; ++p) {
+    const int c0 = p * HC;
+    __syncthreads();   // phase A (or the previous pass) is done with the LDS
+    {
+      constexpr int VEC = 16 / sizeof(T), VPR = DV / VEC;
+      const T* Hs = static_cast<const T*>(a.Hs) + cs + c0 * DV;
+      const T* dHs = static_cast<const T*>(ba.dHs) + cs + c0 * DV;
+      for (int idx = tid; idx < HC * VPR; idx += 256) {
+        const int c = idx / VPR, cv = idx % VPR;
+        *reinterpret_cast<float4*>(sw(sS, LDV, c, cv * VEC)) =
+            *reinterpret_cast<const float4*>(Hs + c * DV + cv * VEC);
+        *reinterpret_cast<float4*>(sw(sdS, LDV, c, cv * VEC)) =
+            *reinterpret_cast<const float4*>(dHs + c * DV + cv * VEC);
+      }
+      for (int idx = tid; idx < C * (HC / 4); idx += 256) {
+        const int t = idx / (HC / 4), c4 = (idx % (HC / 4)) * 4;
+        const float4 gv = *reinterpret_cast<const float4*>(Gc + t * DK + c0 + c4);
+        sGT[(c4 + 0) * LDG + t] = gv.x;
+        sGT[(c4 + 1) * LDG + t] = gv.y;
+        sGT[(c4 + 2) * LDG + t] = gv.z;
+        sGT[(c4 + 3) * LDG + t] = gv.w;
+      }
+    }
+    load_rows_t<T, HC>(sKtT, static_cast<const T*>(a.Ktr) + rk + c0, DK, C, tid);
+    load_rows_t<T, HC>(sQT, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
+    load_rows_t<T, HC>(sKT, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
+    __syncthreads();
+    {
+      // sum_v S dS' per channel of the pass: 8 lanes per channel
+      const int c = tid >> 3, part = tid & 7;
+      float red = 0.f;
+      for (int v = part * (DV / 8); v < (part + 1) * (DV / 8); ++v)
+        red += to_f(*sw(sS, LDV, c, v)) * to_f(*sw(sdS, LDV, c, v));
+      red += __shfl_xor(red, 1, 64);
+      red += __shfl_xor(red, 2, 64);
+      red += __shfl_xor(red, 4, 64);
+      if (part == 0) sRedC[c] = red;
+    }
+#pragma unroll 1
+    for (int j = 0; j < HC / 16; ++j) {
+      const int c = 16 * j + lr;
+      const float* gcol = sGT + c * LDG;
+      floatx4 A1 = {0.f, 0.f, 0.f, 0.f}, A2 = A1, A3 = A1;
+#pragma unroll
+      for (int kk = 0; kk < KV; ++kk) {
+        const Frag8<T> fh = ld8(sw(sS, LDV, c, 32 * kk + 8 * lg));
+        const Frag8<T> fd = ld8(sw(sdS, LDV, c, 32 * kk + 8 * lg));
+        mma(A1, fO[kk], fh);
+        mma(A2, fZ[kk], fh);
+        mma(A3, fE[kk], fd);
+      }
+      // intra-chunk products with the decay split at the block's reference rows
+      const float gref = gcol[16 * w], gref2 = gcol[16 * w + 15];
+      floatx4 aqi = {0.f, 0.f, 0.f, 0.f}, aki = aqi, ati = aqi;
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        const int tb = 32 * k2 + 8 * lg;
+        const float4 g0 = *reinterpret_cast<const float4*>(gcol + tb);
+        const float4 g1 = *reinterpret_cast<const float4*>(gcol + tb + 4);
+        const float gt[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+        Frag8<T> fk = ld8(sw(sKtT, LDT, c, tb));
+        Frag8<T> fq = ld8(sw(sQT, LDT, c, tb));
+        Frag8<T> fr = ld8(sw(sKT, LDT, c, tb));
+#pragma unroll
+        for (int s2 = 0; s2 < 8; ++s2) {
+          const int t = tb + s2;
+          // columns t > 16w + 15 meet only zeros of dSqk / dAt rows of this block;
+          // rows r < 16w only zeros of their transposes
+          const float e1 = t < 16 * w + 16 ? fast_exp(gref - gt[s2]) : 0.f;
+          const float e2 = t >= 16 * w ? fast_exp(gt[s2] - gref2) : 0.f;
+          fk.set(s2, e1 * fk.get(s2));
+          fq.set(s2, e2 * fq.get(s2));
+          fr.set(s2, e2 * fr.get(s2));
+        }
+        mma(aqi, fSq[k2], fk);
+        mma(aki, fSk[k2], fk);
+        mma(ati, fSqT[k2], fq);
+        mma(ati, fSkT[k2], fr);
+      }
+      const float gend = gcol[C - 1];
+      const float4 g4 = *reinterpret_cast<const float4*>(gcol + 16 * w + 4 * lg);
+      const float gr4[4] = {g4.x, g4.y, g4.z, g4.w};
+      const typename Vec4<T>::type q4 = *reinterpret_cast<const typename Vec4<T>::type*>(sw(sQT, LDT, c, 16 * w + 4 * lg));
+      const typename Vec4<T>::type k4 = *reinterpret_cast<const typename Vec4<T>::type*>(sw(sKT, LDT, c, 16 * w + 4 * lg));
+      const typename Vec4<T>::type t4 = *reinterpret_cast<const typename Vec4<T>::type*>(sw(sKtT, LDT, c, 16 * w + 4 * lg));
+      floatx4 oq, ok, ot;
+      float xk = 0.f;
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int r = 16 * w + 4 * lg + ii;
+        const float lam = fast_exp(gr4[ii]);
+        const float wr = fast_exp(gend - gr4[ii]);
+        const float akp = fast_exp(gr4[ii] - gref) * aki[ii] - lam * A2[ii];
+        oq[ii] = lam * a.scale * A1[ii] + fast_exp(gr4[ii] - gref) * aqi[ii];
+        ok[ii] = bt[ii] * akp;
+        const float wa3 = wr * A3[ii];
+        ot[ii] = wa3 + fast_exp(gref2 - gr4[ii]) * ati[ii];
+        const float qv = to_f(q4[ii]), kv = to_f(k4[ii]), tv = to_f(t4[ii]);
+        pdb[ii] += kv * akp;
+        xk += tv * wa3;
+        sDG[r * (HC + 1) + c] = qv * oq[ii] + kv * ok[ii] - tv * ot[ii];
+      }
+      xk += __shfl_xor(xk, 16, 64);
+      xk += __shfl_xor(xk, 32, 64);
+      if (lg == 0) sXc[w * HC + c] = xk;
+      T* so = sOut + w * 3 * 16 * LDO;
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        so[(4 * lg + ii) * LDO + c] = from_f<T>(oq[ii]);
+        so[(16 + 4 * lg + ii) * LDO + c] = from_f<T>(ok[ii]);
+        so[(32 + 4 * lg + ii) * LDO + c] = from_f<T>(ot[ii]);
+      }
+    }
+    {
+      constexpr int VEC = 16 / sizeof(T), SPR = HC / VEC;
+      const T* so = sOut + w * 3 * 16 * LDO;
+      for (int idx = l; idx < 16 * SPR; idx += 64) {
+        const int rr = idx / SPR, sgc = (idx % SPR) * VEC, r = 16 * w + rr;
+        const float4 vq = *reinterpret_cast<const float4*>(so + rr * LDO + sgc);
+        const float4 vk = *reinterpret_cast<const float4*>(so + (16 + rr) * LDO + sgc);
+        const float4 vt = *reinterpret_cast<const float4*>(so + (32 + rr) * LDO + sgc);
+        if (r < n) *reinterpret_cast<float4*>(dq + r * HD + c0 + sgc) = vq;
+        *reinterpret_cast<float4*>(dKm + r * DK + c0 + sgc) = vk;
+        *reinterpret_cast<float4*>(dKt + r * DK + c0 + sgc) = vt;
+      }
+    }
+    __syncthreads();
+    {
+      // dg_j = sum_{r >= j} dG_r + the last-row term, per channel: eight
+      // segments of 8 rows, then the totals of the later segments
+      const int c = tid & (HC - 1), sg = tid / HC;
+      float x = 0.f;
+      float v[8];
+#pragma unroll
+      for (int q = 7; q >= 0; --q) {
+        x += sDG[(8 * sg + q) * (HC + 1) + c];
+        v[q] = x;
+      }
+      sSeg[sg * HC + c] = x;
+      __syncthreads();
+      float add = fast_exp(sGT[c * LDG + C - 1]) * sRedC[c];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) add += sXc[q * HC + c];
+      for (int q = sg + 1; q < 8; ++q) add += sSeg[q * HC + c];
+      float* dg = ba.dg + ((b * a.T + t0) * a.H + h) * DK + c0 + c;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int r = 8 * sg + q;
+        if (r < n) dg[r * HD] = v[q] + add;
+      }
+    }
+  }
+#pragma unroll
+  for (int ii = 0; ii < 4; ++ii)
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) pdb[ii] += __shfl_xor(pdb[ii], off, 64);
+  if (lr == 0) {
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) sDb[16 * w + 4 * lg + ii] = pdb[ii];
+  }
+  __syncthreads();
+  if (tid < n) ba.dbeta[(b * a.T + t0 + tid) * a.H + h] = sDb[tid] + sZV[tid];
+}
+
 // ------------------------------------------------------------ preconditioner
 // Reverse scan of A_t = aP_t A_{t-1} + bP_t k_t^2, kt_t = B(A_t) k_t over the
 // tokens.  With D_t the adjoint of A_t: D_t = inj_t + aP_{t+1} D_{t+1},
@@ -1024,7 +1351,10 @@ static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s, hipEvent_t 
   hipLaunchKernelGGL((r1_state_adjoint<T, DK, GATE>), dim3(grid_scan), dim3(256), 0, s, ba);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = mark(4)) != hipSuccess) return e;
-  hipLaunchKernelGGL((p12_chunk_grads<T, DK, DV, GATE>), dim3(grid_chunk), dim3(256), 0, s, ba);
+  if constexpr (GATE == kGateChannel)
+    hipLaunchKernelGGL((p12c_chunk_grads<T, DK, DV>), dim3(grid_chunk), dim3(256), 0, s, ba);
+  else
+    hipLaunchKernelGGL((p12_chunk_grads<T, DK, DV, GATE>), dim3(grid_chunk), dim3(256), 0, s, ba);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = mark(5)) != hipSuccess) return e;
   if (a.precond == kSquash) {
@@ -1047,23 +1377,27 @@ static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s, hipEvent_t 
   return mark(6);
 }
 
+template <typename T, int DK, int DV>
+static hipError_t launch_bwd_gate(const BwdArgs& ba, hipStream_t s, hipEvent_t const* ev) {
+  switch (ba.f.gate) {
+    case kGateNone: return launch_bwd_typed<T, DK, DV, kGateNone>(ba, s, ev);
+    case kGateScalar: return launch_bwd_typed<T, DK, DV, kGateScalar>(ba, s, ev);
+    default: return launch_bwd_typed<T, DK, DV, kGateChannel>(ba, s, ev);
+  }
+}
+
 // fp32 io: head dims 64 only (LDS); the host validates this
 static hipError_t launch_bwd_f32(const BwdArgs& ba, hipStream_t s, hipEvent_t const* ev) {
-  return ba.f.gate == kGateScalar ? launch_bwd_typed<float, 64, 64, kGateScalar>(ba, s, ev)
-                                  : launch_bwd_typed<float, 64, 64, kGateNone>(ba, s, ev);
+  return launch_bwd_gate<float, 64, 64>(ba, s, ev);
 }
 
 template <typename T>
 static hipError_t launch_bwd_dims(const BwdArgs& ba, hipStream_t s, hipEvent_t const* ev) {
   const FwdArgs& a = ba.f;
-  const bool sc = a.gate == kGateScalar;
-  if (a.dk == 128 && a.dv == 128)
-    return sc ? launch_bwd_typed<T, 128, 128, kGateScalar>(ba, s, ev) : launch_bwd_typed<T, 128, 128, kGateNone>(ba, s, ev);
-  if (a.dk == 128 && a.dv == 64)
-    return sc ? launch_bwd_typed<T, 128, 64, kGateScalar>(ba, s, ev) : launch_bwd_typed<T, 128, 64, kGateNone>(ba, s, ev);
-  if (a.dk == 64 && a.dv == 128)
-    return sc ? launch_bwd_typed<T, 64, 128, kGateScalar>(ba, s, ev) : launch_bwd_typed<T, 64, 128, kGateNone>(ba, s, ev);
-  return sc ? launch_bwd_typed<T, 64, 64, kGateScalar>(ba, s, ev) : launch_bwd_typed<T, 64, 64, kGateNone>(ba, s, ev);
+  if (a.dk == 128 && a.dv == 128) return launch_bwd_gate<T, 128, 128>(ba, s, ev);
+  if (a.dk == 128 && a.dv == 64) return launch_bwd_gate<T, 128, 64>(ba, s, ev);
+  if (a.dk == 64 && a.dv == 128) return launch_bwd_gate<T, 64, 128>(ba, s, ev);
+  return launch_bwd_gate<T, 64, 64>(ba, s, ev);
 }
 
 hipError_t launch_backward(const BwdArgs& ba, int io_bf16, hipStream_t s, hipEvent_t const* ev,

@@ -127,8 +127,8 @@ struct K2Smem {
 };
 
 // BWD: also write the operand layouts the backward kernels read (P^T, M^T,
-// write-key rows, w-scaled write-key rows, (Diag(lam) Q)^T and
-// -(Diag(lam) K)^T); scalar gate or no gate only.
+// write-key rows, write-key rows decayed to the chunk end, (Lam o Q)^T and
+// -(Lam o K)^T; Lam the scalar or per-channel in-chunk decay).
 template <typename T, int DK, int GATE, int PREC, bool BWD>
 __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   using SM = K2Smem<T, DK, GATE>;
@@ -309,7 +309,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     }
   }
   if (BWD) {
-    // (Diag(lam) Q)^T and -(Diag(lam) K)^T per chunk, [dk][C]
+    // (Lam o Q)^T and -(Lam o K)^T per chunk, [dk][C]
     T* QlT = static_cast<T*>(a.QlT) + (bh * a.NT + i) * (int64_t)(DK * C);
     T* KnT = static_cast<T*>(a.KnT) + (bh * a.NT + i) * (int64_t)(DK * C);
     for (int idx = tid; idx < DK * (C / 8); idx += 256) {
@@ -318,7 +318,9 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
 #pragma unroll
       for (int s2 = 0; s2 < 8; ++s2) {
         const int r = r0 + s2;
-        const float lam = GATE == kGateScalar ? fast_exp(sG[r]) : 1.f;
+        float lam = 1.f;
+        if (GATE == kGateScalar) lam = fast_exp(sG[r]);
+        if (GATE == kGateChannel) lam = fast_exp(sGc[r * (DK + 4) + c]);
         fq.set(s2, lam * to_f(sQ[r * LDK + c]));
         fk.set(s2, -lam * to_f(sK[r * LDK + c]));
       }
@@ -421,7 +423,11 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       Frag8<T> fw;
       const float wr = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[r]) : 1.f;
 #pragma unroll
-      for (int s2 = 0; s2 < 8; ++s2) fw.set(s2, wr * fk.get(s2));
+      for (int s2 = 0; s2 < 8; ++s2) {
+        float f = wr;
+        if (GATE == kGateChannel) f = fast_exp(sGc[(C - 1) * (DK + 4) + c0 + s2] - sGc[r * (DK + 4) + c0 + s2]);
+        fw.set(s2, f * fk.get(s2));
+      }
       st8(Kr + r * DK + c0, fk);
       st8(Kwr + r * DK + c0, fw);
     }
@@ -868,7 +874,7 @@ static hipError_t launch_k2_prec(const FwdArgs& a, hipStream_t s) {
 }
 
 // SAVE: the training forward (k2 in backward mode, k3 also saving the
-// chunk states and X, E rows); scalar gate or none
+// chunk states and E rows)
 template <typename T, int DK, bool SAVE>
 static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* ev) {
   hipError_t e;
@@ -885,10 +891,7 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
   switch (a.gate) {
     case kGateNone: e = launch_k2_prec<T, DK, kGateNone, SAVE>(a, s); break;
     case kGateScalar: e = launch_k2_prec<T, DK, kGateScalar, SAVE>(a, s); break;
-    default:
-      if constexpr (SAVE) e = hipErrorInvalidValue;
-      else e = launch_k2_prec<T, DK, kGateChannel>(a, s);
-      break;
+    default: e = launch_k2_prec<T, DK, kGateChannel, SAVE>(a, s); break;
   }
   if (e != hipSuccess) return e;
   if ((e = mark(2)) != hipSuccess) return e;
@@ -900,8 +903,7 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
     case kGateScalar:
       hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, SAVE, true>), dim3(grid), dim3(256), 0, s, a); break;
     default:
-      if constexpr (SAVE) return hipErrorInvalidValue;
-      else hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, false, true>), dim3(grid), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, SAVE, true>), dim3(grid), dim3(256), 0, s, a);
       break;
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -909,7 +911,7 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
 }
 
 // the backward's forward recompute: k1 (squash), k2 in backward mode and k3
-// saving chunk states and X, E rows (no output); scalar gate or none
+// saving chunk states and E rows (no output)
 template <typename T, int DK>
 static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s, hipEvent_t const* ev) {
   hipError_t e;
@@ -923,16 +925,23 @@ static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s, hipEvent_t c
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if ((e = mark(1)) != hipSuccess) return e;
-  e = a.gate == kGateScalar ? launch_k2_prec<T, DK, kGateScalar, true>(a, s)
-                            : launch_k2_prec<T, DK, kGateNone, true>(a, s);
+  switch (a.gate) {
+    case kGateNone: e = launch_k2_prec<T, DK, kGateNone, true>(a, s); break;
+    case kGateScalar: e = launch_k2_prec<T, DK, kGateScalar, true>(a, s); break;
+    default: e = launch_k2_prec<T, DK, kGateChannel, true>(a, s); break;
+  }
   if (e != hipSuccess) return e;
   if ((e = mark(2)) != hipSuccess) return e;
   const int64_t nslab = a.dv / BV;
   const unsigned grid = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
-  if (a.gate == kGateScalar)
-    hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, true, false>), dim3(grid), dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, true, false>), dim3(grid), dim3(256), 0, s, a);
+  switch (a.gate) {
+    case kGateNone:
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, true, false>), dim3(grid), dim3(256), 0, s, a); break;
+    case kGateScalar:
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, true, false>), dim3(grid), dim3(256), 0, s, a); break;
+    default:
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, true, false>), dim3(grid), dim3(256), 0, s, a); break;
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return mark(3);
 }

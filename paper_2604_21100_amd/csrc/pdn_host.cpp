@@ -136,7 +136,6 @@ pdn_status check_inputs(const pdn_problem* p, const pdn_inputs* in, const Sizes&
 // the backward covers the no-gate and scalar-gate forms; fp32 io at head
 // dims 64
 pdn_status check_bwd_support(const pdn_problem* p) {
-  if (p->gate == PDN_GATE_CHANNEL) return PDN_ERR_UNSUPPORTED;
   if (p->io == PDN_F32 && (p->dk != 64 || p->dv != 64)) return PDN_ERR_UNSUPPORTED;
   return PDN_OK;
 }

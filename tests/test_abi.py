@@ -221,11 +221,12 @@ def test_training_pair_validation():
     assert lib.pdn_chunk_fwd_train(
         ctypes.byref(p), ctypes.byref(_inputs()), ctypes.byref(out), A * 64,
         need_b - 1, None, None, 0) == pdn.PDN_ERR_WORKSPACE
-    # the backward's restrictions apply
+    # the backward's restriction applies (fp32 io: d = 64 only); a
+    # per-channel gate is accepted and then wants the backward's workspace
     pc = _prob(gate="channel")
     assert lib.pdn_chunk_fwd_train(
         ctypes.byref(pc), ctypes.byref(_inputs()), ctypes.byref(out), A * 64,
-        0, None, None, 0) == pdn.PDN_ERR_UNSUPPORTED
+        pdn.pdn_workspace_size(pc, True) - 1, None, None, 0) == pdn.PDN_ERR_WORKSPACE
     pf = _prob(io="f32", dk=128, dv=64)
     assert lib.pdn_chunk_fwd_train(
         ctypes.byref(pf), ctypes.byref(_inputs()), ctypes.byref(out), A * 64,
@@ -243,5 +244,5 @@ def test_training_pair_validation():
         ctypes.byref(p), ctypes.byref(_inputs()), A * 30, None,
         ctypes.byref(bo), A * 64, 0, None, ev, 4) == pdn.PDN_ERR_VALUE
     assert lib.pdn_chunk_bwd_train(
-        ctypes.byref(pc), ctypes.byref(_inputs()), A * 30, None,
+        ctypes.byref(pf), ctypes.byref(_inputs()), A * 30, None,
         ctypes.byref(bo), A * 64, 0, None, None, 0) == pdn.PDN_ERR_UNSUPPORTED

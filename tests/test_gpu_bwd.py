@@ -86,6 +86,12 @@ SMALL = [
     ("f32", "scalar", "squash", 64, 64),
     ("f32", "none", "identity", 64, 64),
     ("f32", "scalar", "external", 64, 64),
+    ("bf16", "channel", "squash", 128, 128),
+    ("bf16", "channel", "identity", 128, 64),
+    ("bf16", "channel", "external", 64, 128),
+    ("bf16", "channel", "squash", 64, 64),
+    ("f32", "channel", "squash", 64, 64),
+    ("f32", "channel", "identity", 64, 64),
 ]
 
 
@@ -119,12 +125,19 @@ def test_bwd_beta_range_and_squash_coverage():
     compare(spec, pi.generate(spec, 31), tag="beta02/aniso")
 
 
-def test_bwd_rejects_channel_gate():
-    import paper_2604_21100_amd as pdn
-    p = pdn.make_problem(1, 64, 1, 64, 64, gate="channel")
-    with pytest.raises(pdn.PdnError) as e:
-        pdn.pdn_workspace_size(p, True)
-    assert e.value.status == pdn.PDN_ERR_UNSUPPORTED
+@pytest.mark.parametrize("T", [1, 65, 130])
+def test_bwd_channel_gate_sequence_lengths(T):
+    spec = pi.small_spec(T=T, B=1, H=2, gate="channel", dk=128, dv=128,
+                         with_do=True)
+    compare(spec, pi.generate(spec, 500 + T), tag=f"channel T={T}")
+
+
+def test_bwd_strong_channel_gate():
+    """Per-channel log-decays 15x the default (products of decay ratios
+    across a chunk span many orders of magnitude), with anisotropic keys."""
+    spec = pi.small_spec(gate="channel", dk=128, dv=128, with_do=True,
+                         gate_strength=1.5, key_aniso=1.0)
+    compare(spec, pi.generate(spec, 33), tag="strong channel gate")
 
 
 def test_bwd_deterministic():
@@ -134,6 +147,17 @@ def test_bwd_deterministic():
     b = run_bwd(spec, inp)
     for key in a:
         assert np.array_equal(a[key], b[key]), key
+
+
+def test_bwd_pkda_workload_sampled_heads():
+    """The PKDA layer (B=2, T=8192, H=16, d=128, per-channel gate, N(0, 0.1)
+    initial state) with an upstream dO ~ N(0, 1) drawn after the forward
+    inputs: two heads recomputed by the oracle adjoint end to end."""
+    import dataclasses
+    name = "pkda_bf16_b2_t8192_h16_d128"
+    spec = dataclasses.replace(pi.WORKLOADS[name], with_do=True)
+    inp = pi.generate(spec, pi.WORKLOAD_SEEDS[name])
+    compare(spec, inp, heads=[(0, 3), (1, 12)], tag=name + "+bwd")
 
 
 def test_bwd_full_workload_sampled_heads():

@@ -21,6 +21,8 @@ CASES = [
     ("bf16", "none", "external", 64, 64, 65),
     ("f32", "scalar", "squash", 64, 64, 200),
     ("bf16", "scalar", "squash", 128, 128, 1),
+    ("bf16", "channel", "squash", 128, 128, 200),
+    ("f32", "channel", "identity", 64, 64, 130),
 ]
 
 
