@@ -239,6 +239,90 @@ def roofline_of(stage, ms, stages, token_heads, train=False):
     return roof
 
 
+def sweep(args):
+    """Execution time against sequence length at batch 1, 8 heads, head
+    dimension 128 (the kernel profiling setup of Sec. 5, efficiency
+    analysis): for a scalar (PGDN) and a per-channel (PKDA) gate, each with
+    the preconditioner (squash), with a given distinct write key and no
+    preconditioner recurrence (external) and with the write key equal to the
+    read key (identity: GDN / KDA).  Forward (pdn_chunk_fwd) and forward +
+    backward (the training pair), HIP events around `steps` calls."""
+    import torch
+    import paper_2604_21100_amd as pdn
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    rows = []
+    for T in [int(t) for t in args.sweep_t.split(",")]:
+        for gate in ("scalar", "channel"):
+            spec = pi.Spec(1, T, 8, 128, 128, gate=gate, with_do=True)
+            inp = pi.generate(spec, 4000 + T)
+            rng = np.random.default_rng(4100 + T)
+            inp["ktilde"] = pi.round_bf16(
+                inp["k"] * rng.uniform(1 / 1.5, 1.5, inp["k"].shape))
+            d = {}
+            for key, a in inp.items():
+                if a is None:
+                    d[key] = None
+                    continue
+                t = torch.from_numpy(np.ascontiguousarray(a))
+                d[key] = (t.to(torch.bfloat16) if key in
+                          ("q", "k", "v", "dO", "ktilde") else t).to(dev)
+            for precond in ("squash", "external", "identity"):
+                sq = precond == "squash"
+                kw = dict(g=d["g"], gate=gate, precond=precond,
+                          beta_p=d["beta_p"] if sq else None,
+                          g_p=d["g_p"] if sq else None,
+                          log_a_scale=d["log_a_scale"] if sq else None,
+                          S0=d["S0"], x=spec.x, scale=spec.scale,
+                          ktilde=d["ktilde"] if precond == "external" else None)
+                prob = pdn.make_problem(1, T, 8, 128, 128, gate=gate,
+                                        precond=precond)
+                ws = torch.empty(pdn.pdn_workspace_size(prob, True),
+                                 dtype=torch.uint8, device=dev)
+                o = torch.empty_like(d["v"])
+                grads = pdn.pdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"],
+                                          d["dO"], workspace=ws, **kw)
+
+                def fwd():
+                    pdn.pdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], o=o,
+                                      workspace=ws, stream=stream, **kw)
+
+                def fwdbwd():
+                    pdn.pdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], o=o,
+                                      workspace=ws, stream=stream, train=True,
+                                      **kw)
+                    pdn.pdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"],
+                                      d["dO"], outputs=grads, workspace=ws,
+                                      stream=stream, saved=True, **kw)
+
+                def timed(fn):
+                    for _ in range(args.warmup):
+                        fn()
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    torch.cuda.synchronize()
+                    e0.record(stream)
+                    for _ in range(args.steps):
+                        fn()
+                    e1.record(stream)
+                    torch.cuda.synchronize()
+                    return e0.elapsed_time(e1) / args.steps
+
+                row = {"T": T, "gate": gate, "precond": precond,
+                       "fwd_ms": timed(fwd), "fwdbwd_ms": timed(fwdbwd)}
+                row["fwd_tokens_per_s"] = T / (row["fwd_ms"] / 1e3)
+                row["fwdbwd_tokens_per_s"] = T / (row["fwdbwd_ms"] / 1e3)
+                rows.append(row)
+                print(json.dumps(row), flush=True)
+                del ws, grads
+    print(f"{'T':>6} {'gate':8} {'precond':9} {'fwd ms':>8} {'fwd+bwd ms':>11}",
+          file=sys.stderr)
+    for r in rows:
+        print(f"{r['T']:>6} {r['gate']:8} {r['precond']:9} {r['fwd_ms']:8.3f} "
+              f"{r['fwdbwd_ms']:11.3f}", file=sys.stderr)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -253,6 +337,12 @@ def main(argv=None):
                          "backward recomputes the forward intermediates)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--sweep", action="store_true",
+                    help="kernel time against sequence length at B=1, H=8, "
+                         "d=128 for the scalar and per-channel gates with "
+                         "the preconditioner, with a given write key and "
+                         "with k~ = k (one JSON line per point)")
+    ap.add_argument("--sweep-t", default="1024,2048,4096,8192,16384,32768")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also launch one device copy of this many MiB per "
                          "step (reference kernel for HBM counter scaling)")
@@ -263,12 +353,10 @@ def main(argv=None):
               "in DESIGN.md but not built)", file=sys.stderr)
         return 2
 
+    if args.sweep:
+        return sweep(args)
     bwd = args.passes == "fwdbwd"
     spec = pi.WORKLOADS[args.workload]
-    if bwd and spec.gate == "channel":
-        print("bench.py: the backward supports no gate or a scalar gate; "
-              "use --pass fwd for the per-channel gate", file=sys.stderr)
-        return 2
     if bwd and not spec.with_do:
         # dO is the last draw: every other input is unchanged
         spec = dataclasses.replace(spec, with_do=True)
@@ -306,8 +394,9 @@ def main(argv=None):
             "dk": torch.empty((B, T, H, dk), dtype=io_dt, device=dev),
             "dv": torch.empty((B, T, H, dv), dtype=io_dt, device=dev),
             "dbeta": torch.empty((B, T, H), **f32),
-            "dg": torch.empty((B, T, H), **f32) if spec.gate == "scalar"
-            else None,
+            "dg": (torch.empty((B, T, H), **f32) if spec.gate == "scalar"
+                   else torch.empty((B, T, H, dk), **f32)
+                   if spec.gate == "channel" else None),
             "dS0": torch.empty((B, H, dk, dv), **f32),
             "dbeta_p": torch.empty((B, T, H), **f32),
             "dg_p": torch.empty((B, T, H), **f32),
@@ -380,6 +469,8 @@ def main(argv=None):
     roof = roofline_of(dom, stage_ms[dom], stages, token_heads, train)
     mode = "train" if train else ("recompute" if bwd else "forward")
     roof["traffic"] = measured_traffic(args.workload, mode, dom)
+    if spec.gate == "channel":
+        roof["kernel"] = roof["kernel"].replace("p12_", "p12c_")
     kernels = {k: roofline_of(k, v, stages, token_heads, train)["frac"]
                for k, v in stage_ms.items()}
 
