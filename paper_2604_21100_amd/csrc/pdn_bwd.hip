@@ -1063,65 +1063,69 @@ __device__ __forceinline__ void pc_wave_sum16(float (&v)[16]) {
     for (int j = 0; j < 16; ++j) v[j] += __shfl_xor(v[j], off, 64);
 }
 
-// One block per (b, h, chunk).  The chunk's 64 tokens are cut into four
-// segments of G = 16; wave w takes key channels 64 (w % NCH) .. + 63 of
-// segment w / NCH, one channel per lane.  Both recurrences are first-order
-// linear with a per-token factor aP_r shared by all channels, so each
-// segment scans from zero and a short composition through LDS supplies the
-// exact value entering it:
+// One block per (b, h, chunk), one wave per segment of G = 16 tokens; lane l
+// holds the CPL = d_k / 64 adjacent key channels CPL l .. CPL l + CPL - 1 of
+// every token row of its segment, so each row of k, dkt, dk is one
+// contiguous wave access (256 bytes for d_k = 128 in bf16) straight from
+// HBM, all of a segment's rows in flight at once, and a token's sums over
+// channels are reductions within one wave.  Both recurrences are
+// first-order linear with a per-token factor aP_r shared by all channels,
+// so each segment scans from zero and a short composition through LDS
+// supplies the exact value entering it:
 //   forward  A_r = Ahat_r + (prod_{s0 <= j <= r} aP_j) A_in
 //   reverse  D_r = Dhat_r + (prod_{r < j <= s0 + G - 1} aP_j) kappa
 // (s0 the segment's first token, A_in the preconditioner state before it,
 // kappa the adjoint entering it from the right, already times aP of the
 // next token).  The per-token products come from the in-chunk prefix of gP.
-// The chunk's key, write-key-gradient and read-key-gradient rows are staged
-// in LDS with 16-byte loads (one channel per lane would mean 2-byte
-// accesses), and dk leaves the same way.  Loop bodies are branch-free.
+// Loop bodies are branch-free.
 constexpr int PCG = 16;   // tokens per segment
 constexpr int PCS = C / PCG;
 
-template <typename T, int DK>
-__device__ __forceinline__ void pc_stage(T* dst, const T* src, int64_t ld, int nvalid, int tid) {
-  constexpr int VEC = 16 / sizeof(T), VPR = DK / VEC;
-  for (int idx = tid; idx < C * VPR; idx += DK * PCS) {
-    const int r = idx / VPR, cv = idx % VPR;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < nvalid) v = *reinterpret_cast<const float4*>(src + r * ld + cv * VEC);
-    *reinterpret_cast<float4*>(dst + r * DK + cv * VEC) = v;
-  }
-}
+template <typename T, int N>
+struct alignas(sizeof(T) * N) PcPack {
+  T x[N];
+};
 
 template <typename T, int DK, bool FINAL>
-__global__ __launch_bounds__(DK * PCS) void pc_chunk(BwdArgs ba) {
-  constexpr int NCH = DK / 64;
-  __shared__ float sEgp[C], sBp[C], sGp[C], sFf[C], sBf[C];
+__global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
+  constexpr int CPL = DK / 64;
+  using Pk = PcPack<T, CPL>;
+  __shared__ float sEgp[C], sBp[C], sFf[C], sBf[C];
   __shared__ float sEnd[PCS][DK];          // per-segment end values (A, then adjoint)
-  __shared__ float sRow[2][NCH][C];        // per-channel-half row sums: D k^2, D A_{r-1}
-  __shared__ float sMu[PCS * NCH];
-  __shared__ __attribute__((aligned(16))) T sKr[C * DK];   // key rows (zero past the end)
-  __shared__ __attribute__((aligned(16))) T sGr[C * DK];   // write-key gradient rows
-  __shared__ __attribute__((aligned(16))) T sMr[FINAL ? C * DK : 8];   // read-key gradient rows, then dk
+  __shared__ float sMu[PCS];
   const FwdArgs& a = ba.f;
   const int64_t blk = blockIdx.x;
   const int64_t bh = blk / a.NT;
   const int i = static_cast<int>(blk % a.NT);
   const int64_t b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, l = tid & 63;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
-  const int ch = w % NCH, sg = w / NCH;
-  const int c = 64 * ch + l;
-  const int s0 = PCG * sg;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // segment, wave-uniform
+  const int s0 = PCG * w, c0 = CPL * l;
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
   const int64_t kst = a.H * static_cast<int64_t>(DK);
-  const T* krow = static_cast<const T*>(a.k) + ((b * a.T + t0) * a.H + h) * DK;
-  pc_stage<T, DK>(sKr, krow, kst, n, tid);
-  pc_stage<T, DK>(sGr, static_cast<const T*>(ba.dKt) + (bh * a.Tpad + t0) * DK, DK, C, tid);
-  if (FINAL) pc_stage<T, DK>(sMr, static_cast<const T*>(ba.dKm) + (bh * a.Tpad + t0) * DK, DK, C, tid);
-  const float A_start = a.Abound[(bh * (a.NT + 1) + i) * DK + c];
-  const float kap_chunk = FINAL ? ba.pcC[(bh * (a.NT + 1) + i + 1) * DK + c] : 0.f;
+  const T* krow = static_cast<const T*>(a.k) + ((b * a.T + t0) * a.H + h) * DK + c0;
+  const T* grow = static_cast<const T*>(ba.dKt) + (bh * a.Tpad + t0) * DK + c0;
+  const T* mrow = static_cast<const T*>(ba.dKm) + (bh * a.Tpad + t0) * DK + c0;
+  // every row of the segment in flight first; rows past the sequence end
+  // re-read the last row (keys are zeroed at use, dkt and dkm rows there are
+  // zero)
+  Pk kr[PCG], gr[PCG], mr[FINAL ? PCG : 1];
+#pragma unroll
+  for (int j = 0; j < PCG; ++j) {
+    const int rr = min(s0 + j, n - 1);
+    kr[j] = *reinterpret_cast<const Pk*>(krow + rr * kst);
+    gr[j] = *reinterpret_cast<const Pk*>(grow + (s0 + j) * DK);
+    if (FINAL) mr[j] = *reinterpret_cast<const Pk*>(mrow + (s0 + j) * DK);
+  }
+  float A_start[CPL], kap_chunk[CPL];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) {
+    A_start[q] = a.Abound[(bh * (a.NT + 1) + i) * DK + c0 + q];
+    kap_chunk[q] = FINAL ? ba.pcC[(bh * (a.NT + 1) + i + 1) * DK + c0 + q] : 0.f;
+  }
   if (tid < C) {
-    // per-token factors; padded tokens: aP = 1 (gP = 0), bP = 0.  sGp is the
+    // per-token factors; padded tokens: aP = 1 (gP = 0), bP = 0; x is the
     // in-chunk inclusive prefix of gP (one wave, shuffle scan)
     const bool ok = tid < n;
     const int64_t sidx = (b * a.T + t0 + min(tid, n - 1)) * a.H + h;
@@ -1134,124 +1138,132 @@ __global__ __launch_bounds__(DK * PCS) void pc_chunk(BwdArgs ba) {
       const float y = __shfl_up(x, off, 64);
       if (tid >= off) x += y;
     }
-    sGp[tid] = x;
-    // per-token factors of the segment composition:
+    // segment composition factors:
     //   forward  prod_{s0 <= j <= r} aP_j,   reverse  prod_{r < j < s0 + G} aP_j
     const int q0 = tid & ~(PCG - 1);
     const float gb = __shfl(x, q0 - 1, 64), ge = __shfl(x, q0 + PCG - 1, 64);
     sFf[tid] = fast_exp(x - (q0 > 0 ? gb : 0.f));
     sBf[tid] = fast_exp(ge - x);
   }
+#pragma unroll
+  for (int j = 0; j < PCG; ++j)
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+      if (s0 + j >= n) kr[j].x[q] = from_f<T>(0.f);   // keys past the end are zero
   __syncthreads();
   // ---- forward: local scan from zero, then the exact state entering
-  float A[PCG];
-  {
+  float A[CPL][PCG];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) {
     float x = 0.f;
 #pragma unroll
     for (int j = 0; j < PCG; ++j) {
-      const float kv = to_f(sKr[(s0 + j) * DK + c]);
+      const float kv = to_f(kr[j].x[q]);
       x = sEgp[s0 + j] * x + sBp[s0 + j] * kv * kv;
-      A[j] = x;
+      A[q][j] = x;
     }
+    sEnd[w][c0 + q] = x;
   }
-  sEnd[sg][c] = A[PCG - 1];
   __syncthreads();
-  float A_in = A_start;
-  for (int q = 0; q < sg; ++q) A_in = sEnd[q][c] + sFf[PCG * q + PCG - 1] * A_in;   // segment product
+  float A_in[CPL];
 #pragma unroll
-  for (int j = 0; j < PCG; ++j) A[j] += sFf[s0 + j] * A_in;
+  for (int q = 0; q < CPL; ++q) {
+    float x = A_start[q];
+    for (int s = 0; s < w; ++s) x = sEnd[s][c0 + q] + sFf[PCG * s + PCG - 1] * x;   // segment product
+    A_in[q] = x;
+#pragma unroll
+    for (int j = 0; j < PCG; ++j) A[q][j] += sFf[s0 + j] * x;
+  }
   // ---- reverse: local adjoint from zero; the gain terms need no D
   const float mu = fast_exp(a.log_a_scale[h]);
   const float lnx = a.lnx;
-  float Dh[PCG];
-  float muPart = 0.f;
-  {
+  float Dh[CPL][PCG];
+  float muPart = 0.f, send[CPL];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) {
     float D = 0.f, aNext = 1.f;
 #pragma unroll
     for (int j = PCG - 1; j >= 0; --j) {
-      const float Ar = A[j];
-      const float kv = to_f(sKr[(s0 + j) * DK + c]);
-      const float gk = to_f(sGr[(s0 + j) * DK + c]);
+      const float Ar = A[q][j];
+      const float gk = to_f(gr[j].x[q]);
       // B(A) = exp(-lnx s(rho)), rho = log A - mu, s = rho / (1 + |rho|):
       // dB/dA = -lnx B / ((1 + |rho|)^2 A); zero where A <= 0 (B = x there)
       const bool pos = Ar > 0.f;
       const float rr = fast_log(fmaxf(Ar, 1e-30f)) - mu;
       const float qd = fast_rcp(1.f + fabsf(rr));
       const float Bv = fast_exp(-lnx * (pos ? rr * qd : -1.f));
-      const float dr = pos ? -lnx * Bv * gk * kv * qd * qd : 0.f;
+      const float dr = pos ? -lnx * Bv * gk * to_f(kr[j].x[q]) * qd * qd : 0.f;
       D = dr * fast_rcp(fmaxf(Ar, 1e-30f)) + aNext * D;
       aNext = sEgp[s0 + j];
-      Dh[j] = D;
-      if (FINAL) {   // dk's terms without D, in place of dKm (same thread)
+      Dh[q][j] = D;
+      if (FINAL) {   // dk's terms without D, in place of dKm
         muPart -= dr;
-        sMr[(s0 + j) * DK + c] = from_f<T>(to_f(sMr[(s0 + j) * DK + c]) + Bv * gk);
+        mr[j].x[q] = from_f<T>(to_f(mr[j].x[q]) + Bv * gk);
       }
     }
-    __syncthreads();   // every thread is done with sEnd (forward)
-    sEnd[sg][c] = aNext * D;   // aP_{s0} Dhat_{s0}: what this segment sends left
+    send[q] = aNext * D;   // aP_{s0} Dhat_{s0}: what this segment sends left
   }
+  __syncthreads();   // every wave is done with sEnd (forward)
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) sEnd[w][c0 + q] = send[q];
   __syncthreads();
   // adjoint entering this segment from the right
-  float kap = kap_chunk;
-  for (int q = PCS - 1; q > sg; --q) kap = sEnd[q][c] + sFf[PCG * q + PCG - 1] * kap;
+  float kap[CPL];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) {
+    float x = kap_chunk[q];
+    for (int s = PCS - 1; s > w; --s) x = sEnd[s][c0 + q] + sFf[PCG * s + PCG - 1] * x;
+    kap[q] = x;
+  }
   if (!FINAL) {
-    if (sg == 0) {
-      // the adjoint this chunk sends to the left, with zero carry: aP_0 D_0
-      ba.pcL[(bh * a.NT + i) * DK + c] = sEnd[0][c] + sFf[PCG - 1] * kap;
-    }
+    // the adjoint this chunk sends to the left, with zero carry: aP_0 D_0
+    if (w == 0)
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) ba.pcL[(bh * a.NT + i) * DK + c0 + q] = sEnd[0][c0 + q] + sFf[PCG - 1] * kap[q];
     return;
   }
-  // ---- outputs: dk = dKm + B dkt + 2 bP k D (to LDS, in place of dKm);
-  // row sums D k^2, D A_{r-1}
+  // ---- outputs: dk = dKm + B dkt + 2 bP k D; per token the sums over
+  // channels of D k^2 and D A_{r-1}
   float sr[PCG];
+  T* dko = static_cast<T*>(ba.dk) + ((b * a.T + t0) * a.H + h) * DK + c0;
 #pragma unroll
   for (int j = 0; j < PCG; ++j) {
-    const float kv = to_f(sKr[(s0 + j) * DK + c]);
-    const float D = Dh[j] + sBf[s0 + j] * kap;
-    T* p = sMr + (s0 + j) * DK + c;
-    *p = from_f<T>(to_f(*p) + 2.f * sBp[s0 + j] * kv * D);
-    Dh[j] = D;
-    sr[j] = D * kv * kv;
+    Pk o;
+    sr[j] = 0.f;
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      const float kv = to_f(kr[j].x[q]);
+      const float D = Dh[q][j] + sBf[s0 + j] * kap[q];
+      o.x[q] = from_f<T>(to_f(mr[j].x[q]) + 2.f * sBp[s0 + j] * kv * D);
+      sr[j] += D * kv * kv;
+      Dh[q][j] = D;
+    }
+    if (s0 + j < n) *reinterpret_cast<Pk*>(dko + (s0 + j) * kst) = o;
+  }
+  const int64_t sidx = (b * a.T + t0 + s0 + min(l, PCG - 1)) * a.H + h;
+  const bool tok = l < PCG && s0 + l < n;
+  pc_wave_sum16(sr);
+#pragma unroll
+  for (int j = 0; j < PCG; ++j)
+    if (l == j && tok && ba.dbeta_p) ba.dbeta_p[sidx] = sr[j];
+#pragma unroll
+  for (int j = 0; j < PCG; ++j) {
+    sr[j] = 0.f;
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) sr[j] += Dh[q][j] * (j > 0 ? A[q][j - 1] : A_in[q]);
   }
   pc_wave_sum16(sr);
 #pragma unroll
   for (int j = 0; j < PCG; ++j)
-    if (l == j) sRow[0][ch][s0 + j] = sr[j];
-#pragma unroll
-  for (int j = 0; j < PCG; ++j) sr[j] = Dh[j] * (j > 0 ? A[j - 1] : A_in);
-  pc_wave_sum16(sr);
-#pragma unroll
-  for (int j = 0; j < PCG; ++j)
-    if (l == j) sRow[1][ch][s0 + j] = sr[j];
+    if (l == j && tok && ba.dg_p) ba.dg_p[sidx] = sEgp[s0 + j] * sr[j];
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) muPart += __shfl_xor(muPart, off, 64);
   if (l == 0) sMu[w] = muPart;
   __syncthreads();
-  {
-    // dk rows of the valid tokens, 16-byte stores
-    constexpr int VEC = 16 / sizeof(T), VPR = DK / VEC;
-    T* dko = static_cast<T*>(ba.dk) + ((b * a.T + t0) * a.H + h) * DK;
-    for (int idx = tid; idx < n * VPR; idx += DK * PCS) {
-      const int r = idx / VPR, cv = idx % VPR;
-      *reinterpret_cast<float4*>(dko + r * kst + cv * VEC) =
-          *reinterpret_cast<const float4*>(sMr + r * DK + cv * VEC);
-    }
-  }
-  if (tid < n) {
-    float u1 = 0.f, u2 = 0.f;
-#pragma unroll
-    for (int q = 0; q < NCH; ++q) {
-      u1 += sRow[0][q][tid];
-      u2 += sRow[1][q][tid];
-    }
-    const int64_t sidx = (b * a.T + t0 + tid) * a.H + h;
-    if (ba.dbeta_p) ba.dbeta_p[sidx] = u1;
-    if (ba.dg_p) ba.dg_p[sidx] = sEgp[tid] * u2;
-  }
   if (tid == 0) {
     float m = 0.f;
 #pragma unroll
-    for (int q = 0; q < PCS * NCH; ++q) m += sMu[q];
+    for (int s = 0; s < PCS; ++s) m += sMu[s];
     ba.pcMu[bh * a.NT + i] = m;
   }
 }
@@ -1358,11 +1370,11 @@ static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s, hipEvent_t 
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = mark(5)) != hipSuccess) return e;
   if (a.precond == kSquash) {
-    hipLaunchKernelGGL((pc_chunk<T, DK, false>), dim3(grid_chunk), dim3(DK * PCS), 0, s, ba);
+    hipLaunchKernelGGL((pc_chunk<T, DK, false>), dim3(grid_chunk), dim3(64 * PCS), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((pc_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((pc_chunk<T, DK, true>), dim3(grid_chunk), dim3(DK * PCS), 0, s, ba);
+    hipLaunchKernelGGL((pc_chunk<T, DK, true>), dim3(grid_chunk), dim3(64 * PCS), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ba.dlog_a_scale) {
       hipLaunchKernelGGL(pc_mu, dim3(static_cast<unsigned>(a.H)), dim3(256), 0, s, ba);
