@@ -43,7 +43,7 @@ PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3       # dense fp32 matrix
 
 
-def algorithmic_per_token_head(spec, train=False):
+def algorithmic_per_token_head(spec, train=False, precond="squash"):
     """Algorithmic FLOPs and bytes per token-head (one (b, t, h)).
 
     Dense per-chunk products as the paper writes them:
@@ -61,7 +61,7 @@ def algorithmic_per_token_head(spec, train=False):
     st = e * dk * dv / C                       # one chunk-start state, per token
     flop_fwd = 6 * C * dk + 4 * C * dv + 6 * dk * dv + C * C / 3.0
     flop_bwd = 12 * C * dk + 8 * C * dv + 12 * dk * dv + 4 * C * C
-    precond = (3 * dk, e * dk + 8 + 4 * dk / C)
+    pre = (3 * dk, e * dk + 8 + 4 * dk / C)
     # k2: read q, k, beta, g, betaP, gP, chunk-start A; write the decayed
     # write keys (dk), T and P (C each) and the gate prefix
     prep = (4 * C * dk + C * C / 3.0,
@@ -76,13 +76,20 @@ def algorithmic_per_token_head(spec, train=False):
     # write the chunk-start states and the E rows
     save = (4 * dk * dv + 2 * C * dv,
             e * (dk + dv) + e * (C + dk) + gb + st + e * dv)
+    if precond == "atq":
+        # linear attention read through the preconditioned query: no
+        # interaction matrix or solve; the prep kernel also writes the
+        # preconditioned query rows, the scan reads them instead of q and k
+        flop_fwd = 2 * C * dk + 2 * C * dv + 4 * dk * dv
+        prep = (2 * C * dk, prep[1] + e * dk)
+        scan = (4 * dk * dv + 2 * C * dv, scan[1] - e * dk)
     stages = {
-        "precond": precond,
+        "precond": pre,
         "chunk_prep": prep_b if train else prep,
         # training forward: the output, the saved states and E rows
         "chunk_scan": ((scan[0], scan[1] + st + e * dv) if train
                        else scan),
-        "bwd_precond_recompute": precond,
+        "bwd_precond_recompute": pre,
         "bwd_chunk_prep": prep_b,
         "bwd_state_save_scan": save,
         # r1: read P^T, M^T, w*Kt, (lam Q)^T, -(lam K)^T, dO, beta; write the
@@ -131,7 +138,7 @@ def _oracle_job(args):
         return time.perf_counter() - t0
 
 
-def cpu_baseline(spec, inp, bwd, target_s=15.0):
+def cpu_baseline(spec, inp, bwd, target_s=15.0, precond="squash", ridge=1.0):
     """Time the float64 oracle as it stands (token recurrence forward, and
     for bwd its adjoint as well) on a bounded sample: every head of the first
     nb batches over a prefix of Ts tokens, heads spread over worker
@@ -139,7 +146,9 @@ def cpu_baseline(spec, inp, bwd, target_s=15.0):
     of CPU time.  Returns the cpu_baseline object."""
     from concurrent.futures import ProcessPoolExecutor
     ncpu = len(os.sched_getaffinity(0))
-    kw = dict(gate=spec.gate, precond="squash", x=spec.x, scale=spec.scale)
+    kw = dict(gate=spec.gate, precond=precond, x=spec.x, scale=spec.scale)
+    if precond != "squash":
+        kw["ridge"] = ridge
 
     def sample_of(nb, Ts):
         s = {}
@@ -332,6 +341,14 @@ def main(argv=None):
                     choices=sorted(pi.WORKLOADS))
     ap.add_argument("--pass", dest="passes", default="fwdbwd",
                     choices=("fwd", "fwdbwd"))
+    ap.add_argument("--precond", default="squash",
+                    choices=("squash", "diag_sm", "atq"),
+                    help="write-key / query preconditioner: the method's "
+                         "squash (default), the Sherman-Morrison write key "
+                         "(diag_sm) or apply-to-query linear attention (atq); "
+                         "the latter two are forward only")
+    ap.add_argument("--ridge", type=float, default=0.1,
+                    help="ridge lambda of diag_sm / atq")
     ap.add_argument("--recompute", action="store_true",
                     help="fwd+bwd with pdn_chunk_fwd + pdn_chunk_bwd (the "
                          "backward recomputes the forward intermediates)")
@@ -356,6 +373,10 @@ def main(argv=None):
     if args.sweep:
         return sweep(args)
     bwd = args.passes == "fwdbwd"
+    if bwd and args.precond != "squash":
+        print(f"bench.py: --precond {args.precond} is forward only; use "
+              "--pass fwd", file=sys.stderr)
+        return 2
     spec = pi.WORKLOADS[args.workload]
     if bwd and not spec.with_do:
         # dO is the last draw: every other input is unchanged
@@ -363,8 +384,9 @@ def main(argv=None):
     seed = pi.WORKLOAD_SEEDS[args.workload]
     inp = pi.generate(spec, seed)
     # the CPU leg runs before the GPU is touched (its worker processes fork)
-    cpu = None if args.no_cpu_baseline else cpu_baseline(spec, inp, bwd,
-                                                         args.cpu_seconds)
+    sq = args.precond == "squash"
+    cpu = None if args.no_cpu_baseline else cpu_baseline(
+        spec, inp, bwd, args.cpu_seconds, args.precond, args.ridge)
 
     import torch
     import paper_2604_21100_amd as pdn
@@ -383,7 +405,8 @@ def main(argv=None):
     S_T = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev)
     A_T = torch.empty((B, H, dk), dtype=torch.float32, device=dev)
     prob = pdn.make_problem(B, T, H, dk, dv, io=spec.io, gate=spec.gate,
-                            x=spec.x, scale=spec.scale)
+                            precond=args.precond, x=spec.x, scale=spec.scale,
+                            ridge=args.ridge)
     ws = torch.empty(pdn.pdn_workspace_size(prob, with_bwd=bwd),
                      dtype=torch.uint8, device=dev)
     grads = None
@@ -416,11 +439,13 @@ def main(argv=None):
 
     def step(fev=None, bev=None):
         pdn.pdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], g=d["g"],
-                          gate=spec.gate, beta_p=d["beta_p"], g_p=d["g_p"],
-                          log_a_scale=d["log_a_scale"], A0=d["A0"],
-                          S0=d["S0"], x=spec.x, scale=spec.scale, o=o,
-                          S_T=S_T, A_T=A_T, workspace=ws, stream=stream,
-                          stage_events=fev, train=train)
+                          gate=spec.gate, precond=args.precond,
+                          beta_p=d["beta_p"], g_p=d["g_p"],
+                          log_a_scale=d["log_a_scale"] if sq else None,
+                          A0=d["A0"], S0=d["S0"], x=spec.x, scale=spec.scale,
+                          ridge=args.ridge, o=o, S_T=S_T, A_T=A_T,
+                          workspace=ws, stream=stream, stage_events=fev,
+                          train=train)
         if bwd:
             pdn.pdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], d["dO"],
                               g=d["g"], gate=spec.gate, beta_p=d["beta_p"],
@@ -464,11 +489,13 @@ def main(argv=None):
 
     tokens = B * T
     token_heads = B * T * H
-    flop_fwd, flop_bwd, stages = algorithmic_per_token_head(spec, train)
+    flop_fwd, flop_bwd, stages = algorithmic_per_token_head(spec, train,
+                                                            args.precond)
     dom = max(stage_ms, key=stage_ms.get)
     roof = roofline_of(dom, stage_ms[dom], stages, token_heads, train)
     mode = "train" if train else ("recompute" if bwd else "forward")
-    roof["traffic"] = measured_traffic(args.workload, mode, dom)
+    roof["traffic"] = (measured_traffic(args.workload, mode, dom) if sq
+                       else None)
     if spec.gate == "channel":
         roof["kernel"] = roof["kernel"].replace("p12_", "p12c_")
     kernels = {k: roofline_of(k, v, stages, token_heads, train)["frac"]
@@ -479,6 +506,11 @@ def main(argv=None):
     tflops = flop_step * token_heads / step_s / 1e12
     peak_tf = PEAK_BF16_TFLOPS if spec.io == "bf16" else PEAK_FP32_TFLOPS
     variant = {"scalar": "PGDN", "channel": "PKDA"}.get(spec.gate, "PDN")
+    if args.precond == "atq":
+        variant = {"scalar": "P-Mamba-2", "channel": "PGLA"}.get(spec.gate,
+                                                                 "PLA")
+    elif args.precond == "diag_sm":
+        variant += " (Sherman-Morrison write key)"
     line = {
         "metric": "tokens/s of chunkwise PDN fwd(+bwd) at 1B layer shape; "
                   "% bf16 MFMA peak",
@@ -499,7 +531,9 @@ def main(argv=None):
                             if bwd else "forward"),
                    "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
                    "chunk": spec.chunk, "gate": spec.gate,
-                   "precond": "squash", "x": spec.x, "global_batch": B,
+                   "precond": args.precond, "x": spec.x,
+                   **({"ridge": args.ridge} if not sq else {}),
+                   "global_batch": B,
                    "seq_len": T, "parallelism": "none (1 GPU)"},
         "tflops": tflops,
         "mfma_frac": tflops / peak_tf,

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define PDN_ABI_VERSION 1
+#define PDN_ABI_VERSION 2
 
 typedef enum {
   PDN_OK = 0,
@@ -62,8 +62,9 @@ typedef enum {
   PDN_ERR_ALIGN = 5,       /* a tensor is not 16-byte aligned                  */
   PDN_ERR_ALIAS = 6,       /* an output overlaps an input or another output    */
   PDN_ERR_WORKSPACE = 7,   /* workspace NULL, too small or misaligned          */
-  PDN_ERR_VALUE = 8,       /* bad scalar (x < 1, non-finite x/scale) or enum,
-                              or a gate pointer inconsistent with the gate kind */
+  PDN_ERR_VALUE = 8,       /* bad scalar (x < 1, non-finite x/scale, ridge <= 0
+                              for DIAG_SM / ATQ) or enum, or a gate pointer
+                              inconsistent with the gate kind               */
   PDN_ERR_HIP = 9          /* a HIP launch failed                              */
 } pdn_status;
 
@@ -78,7 +79,20 @@ typedef enum {
 typedef enum {
   PDN_PRECOND_SQUASH = 0,   /* write key of Eq. precond_end2end (the method) */
   PDN_PRECOND_IDENTITY = 1, /* kt = k: plain DeltaNet / GDN / KDA            */
-  PDN_PRECOND_EXTERNAL = 2  /* kt supplied by the caller in `ktilde`         */
+  PDN_PRECOND_EXTERNAL = 2, /* kt supplied by the caller in `ktilde`         */
+  /* Unstable ATK (App. D, "ATK (unstable) preconditioner recurrence"; the
+   * Sherman-Morrison form of Sec. 3.4): with the same A recurrence and
+   * P_t = Diag(A_{t-1} + ridge)^{-1} (the state BEFORE token t),
+   *   kt_t = P_t k_t / (1 + k_t^T P_t k_t)
+   * and the delta rule above.  Forward only.                               */
+  PDN_PRECOND_DIAG_SM = 3,
+  /* Preconditioned linear attention, apply-to-query (Sec. 3.3 chunkwise PLA
+   * form; App. D, "ATQ preconditioner recurrence"; P-Mamba-2 with a scalar
+   * gate, PGLA with a per-channel gate): no delta rule,
+   *   S_t = alpha_t S_{t-1} + beta_t v_t k_t^T
+   *   o_t = scale * S_t (q_t / (A_t + ridge))          (A_t: current state)
+   * ktilde is unused (write key = read key).  Forward only.                */
+  PDN_PRECOND_ATQ = 4
 } pdn_precond;
 
 typedef struct {
@@ -90,6 +104,8 @@ typedef struct {
   pdn_precond precond;
   float x;             /* squash range [1/x, x]; x >= 1 (paper: 1.5)        */
   float scale;         /* output scale (paper: 1.0)                         */
+  float ridge;         /* DIAG_SM and ATQ: the ridge lambda > 0 added to A
+                          before the elementwise inverse; ignored otherwise */
 } pdn_problem;
 
 typedef struct {
@@ -98,10 +114,10 @@ typedef struct {
   const void* v;             /* [B,T,H,dv] io                                */
   const float* beta;         /* [B,T,H]                                      */
   const float* g;            /* NULL for GATE_NONE, else [B,T,H] / [B,T,H,dk] */
-  const float* beta_p;       /* [B,T,H]; SQUASH only                         */
-  const float* g_p;          /* [B,T,H] or NULL (alpha^P = 1); SQUASH only   */
+  const float* beta_p;       /* [B,T,H]; SQUASH, DIAG_SM, ATQ               */
+  const float* g_p;          /* [B,T,H] or NULL (alpha^P = 1); as beta_p     */
   const float* log_a_scale;  /* [H]; mu_h = exp(.); SQUASH only              */
-  const float* A0;           /* [B,H,dk] or NULL (= 0); SQUASH only          */
+  const float* A0;           /* [B,H,dk] or NULL (= 0); as beta_p            */
   const float* S0;           /* [B,H,dk,dv] (S^T) or NULL (= 0)              */
   const void* ktilde;        /* [B,T,H,dk] io; EXTERNAL only                 */
 } pdn_inputs;
@@ -109,7 +125,8 @@ typedef struct {
 typedef struct {
   void* o;      /* [B,T,H,dv] io                                             */
   float* S_T;   /* [B,H,dk,dv] final state S_T^T, or NULL                    */
-  float* A_T;   /* [B,H,dk] final preconditioner state, or NULL (SQUASH only) */
+  float* A_T;   /* [B,H,dk] final preconditioner state, or NULL (SQUASH,
+                   DIAG_SM, ATQ)                                             */
 } pdn_fwd_out;
 
 typedef struct {
@@ -162,7 +179,8 @@ pdn_status pdn_chunk_fwd_events(const pdn_problem* problem, const pdn_inputs* in
  * io; dS_T is [B,H,dk,dv] fp32 or NULL (= 0).  The forward intermediates are
  * recomputed; `ws` must hold pdn_workspace_size(problem, 1) bytes.  The
  * output pointers dbeta_p, dg_p, dlog_a_scale, dA0 and dS0 may be NULL to
- * skip them. */
+ * skip them.  SQUASH, IDENTITY and EXTERNAL only (DIAG_SM, ATQ:
+ * PDN_ERR_UNSUPPORTED). */
 pdn_status pdn_chunk_bwd(const pdn_problem* problem, const pdn_inputs* in,
                          const void* dO, const float* dS_T, pdn_bwd_out* out,
                          void* ws, size_t ws_bytes, void* hip_stream);
@@ -196,8 +214,8 @@ pdn_status pdn_chunk_bwd_events(const pdn_problem* problem, const pdn_inputs* in
  * library cannot detect a violation; results are then undefined, but every
  * access stays inside the declared buffers).  pdn_chunk_bwd_train leaves the
  * saved intermediates intact, so it may be called again for another dO.
- * The backward's restriction applies to both calls (fp32 io only with
- * d_k = d_v = 64: PDN_ERR_UNSUPPORTED).
+ * The backward's restrictions apply to both calls (fp32 io only with
+ * d_k = d_v = 64; no DIAG_SM or ATQ: PDN_ERR_UNSUPPORTED).
  *
  * stage_events: NULL with n_events = 0, or PDN_FWD_STAGE_EVENTS /
  * PDN_BWD_STAGE_EVENTS caller-created events recorded as in the _events

@@ -68,6 +68,39 @@ def preconditioner_scan(k, beta_p, g_p, mu, x, A0=None):
     return kt, A_all, A
 
 
+def gram_states(k, beta_p, g_p, A0=None):
+    """The diagonal key-Gram recurrence alone (Eq. diag_gram with the decay
+    and gain of Eq. precond_end2end):
+
+        A_t = alpha^P_t A_{t-1} + beta^P_t (k_t * k_t)
+
+    Returns (A_prev (N,T,dk) with A_prev[:, t] = A_{t-1}, A_all (N,T,dk)
+    with A_all[:, t] = A_t, A_T (N,dk))."""
+    k = _f64(k)
+    N, T, dk = k.shape
+    beta_p = _f64(beta_p)
+    A = np.zeros((N, dk)) if A0 is None else _f64(A0).copy()
+    A_prev = np.empty_like(k)
+    A_all = np.empty_like(k)
+    for t in range(T):
+        A_prev[:, t] = A
+        a_p = 1.0 if g_p is None else np.exp(_f64(g_p)[:, t])[:, None]
+        A = a_p * A + beta_p[:, t, None] * (k[:, t] * k[:, t])
+        A_all[:, t] = A
+    return A_prev, A_all, A
+
+
+def sm_write_key(k, A_prev, lam):
+    """Write key of the diagonal Sherman-Morrison ("unstable ATK") form, App.
+    D "ATK (unstable) preconditioner recurrence":
+
+        kt_t = P_t k_t / (1 + k_t^T P_t k_t),  P_t = Diag(A_{t-1} + lam)^{-1}
+    """
+    k, A_prev = _f64(k), _f64(A_prev)
+    pk = k / (A_prev + lam)
+    return pk / (1.0 + np.sum(k * pk, axis=-1, keepdims=True))
+
+
 # --------------------------------------------------------------------------
 # Main recurrence with distinct read key k and write key kt.
 # --------------------------------------------------------------------------
@@ -117,14 +150,45 @@ def delta_rule(q, k, kt, v, beta, g=None, gate="none", S0=None, scale=1.0,
     return o, S
 
 
+def linear_attention(q, k, v, beta, g=None, gate="none", S0=None, scale=1.0):
+    """(Gated) linear attention, one token at a time:
+
+        S_t = alpha_t S_{t-1} + beta_t v_t k_t^T
+        o_t = scale * S_t q_t
+
+    (Sec. 2's linear attention; with a scalar alpha the Mamba-2 form, with
+    a per-channel alpha acting as S Diag(alpha) the GLA form of App. E "ATQ
+    vs ATK").  The apply-to-query modes pass the preconditioned query as q.
+
+    Returns (o (N,T,dv), S_T (N,dv,dk))."""
+    q, k, v, beta = map(_f64, (q, k, v, beta))
+    g = _f64(g)
+    N, T, dk = k.shape
+    dv = v.shape[2]
+    S = np.zeros((N, dv, dk)) if S0 is None else _f64(S0).copy()
+    o = np.empty((N, T, dv))
+    for t in range(T):
+        alpha = None if gate == "none" else np.exp(g[:, t])
+        S = decay_state(S, alpha, gate) + beta[:, t, None, None] * (
+            v[:, t, :, None] * k[:, t, None, :])
+        o[:, t] = scale * np.einsum("nvk,nk->nv", S, q[:, t])
+    return o, S
+
+
 def pdn_forward(q, k, v, beta, *, g=None, gate="none", precond="squash",
                 beta_p=None, g_p=None, mu=None, x=1.5, kt_ext=None, S0=None,
-                A0=None, scale=1.0):
-    """End-to-end token recurrence for PDN / PGDN / PKDA.
+                A0=None, scale=1.0, ridge=1.0):
+    """End-to-end token recurrence for PDN / PGDN / PKDA and the other
+    preconditioner realisations.
 
     precond = "squash"    write key from Eq. precond_end2end
               "identity"  kt = k (plain DeltaNet / GDN / KDA)
               "external"  kt supplied by the caller (any write key)
+              "diag_sm"   Sherman-Morrison write key from A_{t-1} + ridge
+                          (sm_write_key), then the delta rule
+              "atq"       linear attention read through the preconditioned
+                          query q_t / (A_t + ridge) (App. D "ATQ
+                          preconditioner recurrence"); kt = k
     Returns dict(o, S_T, A_T, kt)."""
     k = _f64(k)
     N = k.shape[0]
@@ -137,6 +201,14 @@ def pdn_forward(q, k, v, beta, *, g=None, gate="none", precond="squash",
         kt = k
     elif precond == "external":
         kt = _f64(kt_ext)
+    elif precond == "diag_sm":
+        A_prev, _, A_T = gram_states(k, beta_p, g_p, A0)
+        kt = sm_write_key(k, A_prev, ridge)
+    elif precond == "atq":
+        _, A_all, A_T = gram_states(k, beta_p, g_p, A0)
+        qt = _f64(q) / (A_all + ridge)
+        o, S_T = linear_attention(qt, k, v, beta, g, gate, S0, scale)
+        return dict(o=o, S_T=S_T, A_T=A_T, kt=k)
     else:
         raise ValueError(precond)
     o, S_T = delta_rule(q, k, kt, v, beta, g, gate, S0, scale)

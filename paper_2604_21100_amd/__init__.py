@@ -57,12 +57,17 @@ PDN_OK, PDN_ERR_NULL, PDN_ERR_SHAPE, PDN_ERR_DTYPE, PDN_ERR_UNSUPPORTED, \
     PDN_ERR_HIP = range(10)
 PDN_F32, PDN_BF16 = 0, 1
 PDN_GATE_NONE, PDN_GATE_SCALAR, PDN_GATE_CHANNEL = 0, 1, 2
-PDN_PRECOND_SQUASH, PDN_PRECOND_IDENTITY, PDN_PRECOND_EXTERNAL = 0, 1, 2
+PDN_PRECOND_SQUASH, PDN_PRECOND_IDENTITY, PDN_PRECOND_EXTERNAL, \
+    PDN_PRECOND_DIAG_SM, PDN_PRECOND_ATQ = 0, 1, 2, 3, 4
 
 GATES = {"none": PDN_GATE_NONE, "scalar": PDN_GATE_SCALAR,
          "channel": PDN_GATE_CHANNEL}
 PRECONDS = {"squash": PDN_PRECOND_SQUASH, "identity": PDN_PRECOND_IDENTITY,
-            "external": PDN_PRECOND_EXTERNAL}
+            "external": PDN_PRECOND_EXTERNAL, "diag_sm": PDN_PRECOND_DIAG_SM,
+            "atq": PDN_PRECOND_ATQ}
+# modes driven by the diagonal key-Gram recurrence (they take beta_p, g_p,
+# A0 and return A_T)
+GRAM_PRECONDS = ("squash", "diag_sm", "atq")
 
 _vp = ctypes.c_void_p
 
@@ -73,7 +78,7 @@ class Problem(ctypes.Structure):
                 ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
                 ("io", ctypes.c_int), ("gate", ctypes.c_int),
                 ("precond", ctypes.c_int), ("x", ctypes.c_float),
-                ("scale", ctypes.c_float)]
+                ("scale", ctypes.c_float), ("ridge", ctypes.c_float)]
 
 
 class Inputs(ctypes.Structure):
@@ -126,6 +131,12 @@ _lib.pdn_status_string.restype = ctypes.c_char_p
 _lib.pdn_abi_version.argtypes = []
 _lib.pdn_abi_version.restype = ctypes.c_int
 
+ABI_VERSION = 2   # PDN_ABI_VERSION: the struct layouts mirrored above
+if _lib.pdn_abi_version() != ABI_VERSION:
+    raise ImportError(f"{LIB_PATH} implements ABI version "
+                      f"{_lib.pdn_abi_version()}, this binding mirrors "
+                      f"version {ABI_VERSION}: rebuild the library")
+
 EXPORTED = ("pdn_workspace_size", "pdn_chunk_fwd", "pdn_chunk_fwd_events",
             "pdn_chunk_bwd", "pdn_chunk_bwd_events", "pdn_chunk_fwd_train",
             "pdn_chunk_bwd_train", "pdn_status_string", "pdn_abi_version")
@@ -152,12 +163,13 @@ def pdn_abi_version() -> int:
 
 
 def make_problem(B, T, H, dk, dv, *, io="bf16", gate="none",
-                 precond="squash", x=1.5, scale=1.0, chunk=64) -> Problem:
+                 precond="squash", x=1.5, scale=1.0, chunk=64,
+                 ridge=1.0) -> Problem:
     return Problem(B, T, H, dk, dv, chunk,
                    PDN_BF16 if io == "bf16" else PDN_F32,
                    GATES[gate] if isinstance(gate, str) else int(gate),
                    PRECONDS[precond] if isinstance(precond, str)
-                   else int(precond), x, scale)
+                   else int(precond), x, scale, ridge)
 
 
 def pdn_workspace_size(problem: Problem, with_bwd: bool = False) -> int:
@@ -225,9 +237,9 @@ def _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde):
 
 def pdn_chunk_fwd(q, k, v, beta, *, g=None, gate="none", precond="squash",
                   beta_p=None, g_p=None, log_a_scale=None, A0=None, S0=None,
-                  ktilde=None, x=1.5, scale=1.0, chunk=64, o=None, S_T=None,
-                  A_T=None, want_state=True, workspace=None, stream=None,
-                  stage_events=None, train=False):
+                  ktilde=None, x=1.5, scale=1.0, chunk=64, ridge=1.0, o=None,
+                  S_T=None, A_T=None, want_state=True, workspace=None,
+                  stream=None, stage_events=None, train=False):
     """Forward pass on torch device tensors in the ABI layouts of pdn.h.
 
     Returns (o, S_T, A_T); S_T / A_T are None when not requested.  Outputs and
@@ -241,13 +253,13 @@ def pdn_chunk_fwd(q, k, v, beta, *, g=None, gate="none", precond="squash",
     dv = v.shape[-1]
     io = _io_of(q)
     prob = make_problem(B, T, H, dk, dv, io=io, gate=gate, precond=precond,
-                        x=x, scale=scale, chunk=chunk)
+                        x=x, scale=scale, chunk=chunk, ridge=ridge)
     dev = q.device
     if o is None:
         o = torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
     if S_T is None and want_state:
         S_T = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev)
-    if A_T is None and want_state and precond == "squash":
+    if A_T is None and want_state and precond in GRAM_PRECONDS:
         A_T = torch.empty((B, H, dk), dtype=torch.float32, device=dev)
     nbytes = pdn_workspace_size(prob, train)
     if workspace is None:

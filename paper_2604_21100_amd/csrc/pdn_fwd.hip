@@ -177,7 +177,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       *reinterpret_cast<float4*>(sQ + r * LDK + cv * VEC) = qv;
       // identity write key: a copy of the key tile (the key tile's memory is
       // reused by the solve)
-      if (PREC == kIdentity) *reinterpret_cast<float4*>(sKt + r * LDK + cv * VEC) = kv;
+      if (PREC == kIdentity || PREC == kATQ) *reinterpret_cast<float4*>(sKt + r * LDK + cv * VEC) = kv;
       if (PREC == kExternal) *reinterpret_cast<float4*>(sKt + r * LDK + cv * VEC) = xv;
     }
     if (tid < C) {
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       const bool ok = r < n;
       const int64_t sidx = (b * a.T + t0 + r) * a.H + h;
       sBeta[r] = ok ? a.beta[sidx] : 0.f;
-      if (PREC == kSquash) {
+      if (has_gram(PREC)) {
         sBp[r] = ok ? a.beta_p[sidx] : 0.f;
         sEgp[r] = (ok && a.g_p) ? fast_exp(a.g_p[sidx]) : 1.f;
       }
@@ -226,7 +226,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       }
     }
   }
-  if (PREC == kSquash) {
+  if (has_gram(PREC)) {
     // the in-chunk prefix A_r = a_r A_{r-1} + bP_r k_r^2 in NSEG row segments:
     // pass 1 reduces each segment to (prod a, partial sum), the segments are
     // chained from the chunk-start state, pass 2 re-walks its rows
@@ -243,14 +243,63 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     __syncthreads();
     float A = a.Abound[(bh * (a.NT + 1) + i) * DK + c];
     for (int q = 0; q < sg; ++q) A = sSegE[q * DK + c] * A + sSegP[q * DK + c];
-    const float mu = fast_exp(a.log_a_scale[h]);
-    for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-      const float kv = to_f(sK[r * LDK + c]);
-      A = sEgp[r] * A + sBp[r] * kv * kv;
-      sKt[r * LDK + c] = from_f<T>(squash_gain(A, mu, a.lnx) * kv);
+    if (PREC == kSquash) {
+      const float mu = fast_exp(a.log_a_scale[h]);
+      for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
+        const float kv = to_f(sK[r * LDK + c]);
+        A = sEgp[r] * A + sBp[r] * kv * kv;
+        sKt[r * LDK + c] = from_f<T>(squash_gain(A, mu, a.lnx) * kv);
+      }
+    }
+    if (PREC == kATQ) {
+      // preconditioned query q / (A_r + ridge), A_r including token r
+      for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
+        const float kv = to_f(sK[r * LDK + c]);
+        A = sEgp[r] * A + sBp[r] * kv * kv;
+        sQ[r * LDK + c] = from_f<T>(to_f(sQ[r * LDK + c]) / (A + a.ridge));
+      }
+    }
+    if (PREC == kDiagSM) {
+      // Sherman-Morrison write key from the state before token r:
+      //   p = k / (A_{r-1} + ridge),  kt = p / (1 + k . p)
+      // the row sums k . p need every channel: the segment is walked once
+      // for them and again for the exactly recomputed, normalised key
+      const float A_seg = A;
+      float* sNrm = sY;   // free until the solve
+      for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
+        const float kv = to_f(sK[r * LDK + c]);
+        sKt[r * LDK + c] = from_f<T>(kv / (A + a.ridge));
+        A = sEgp[r] * A + sBp[r] * kv * kv;
+      }
+      __syncthreads();
+      {
+        constexpr int PART = DK / 4;
+        const int r = tid >> 2, part = tid & 3;
+        float sum = 0.f;
+        for (int cc = part * PART; cc < (part + 1) * PART; ++cc)
+          sum += to_f(sK[r * LDK + cc]) * to_f(sKt[r * LDK + cc]);
+        sum += __shfl_xor(sum, 1, 64);
+        sum += __shfl_xor(sum, 2, 64);
+        if (part == 0) sNrm[r] = 1.f + sum;
+      }
+      __syncthreads();
+      A = A_seg;
+      for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
+        const float kv = to_f(sK[r * LDK + c]);
+        sKt[r * LDK + c] = from_f<T>(kv / ((A + a.ridge) * sNrm[r]));
+        A = sEgp[r] * A + sBp[r] * kv * kv;
+      }
     }
   }
   __syncthreads();
+  if (PREC == kATQ) {
+    // the preconditioned query rows for the scan's inter-chunk output
+    T* qt = static_cast<T*>(a.Qt) + (bh * a.Tpad + t0) * DK;
+    for (int idx = tid; idx < C * VPR; idx += 256) {
+      const int r = idx / VPR, cv = idx % VPR;
+      *reinterpret_cast<float4*>(qt + r * DK + cv * VEC) = *reinterpret_cast<const float4*>(sQ + r * LDK + cv * VEC);
+    }
+  }
 
   // ---- interaction matrices on MFMA: wave w owns row block w
   floatx4 accA[4], accP[4];
@@ -282,7 +331,8 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
             fb.set(s, fb.get(s) * fast_exp(gref[s] - gt[s]));
           }
         }
-        mma(accA[j], fk, fb);
+        // linear attention (ATQ): no delta-rule interaction, At = 0, T = Diag(beta)
+        if (PREC != kATQ) mma(accA[j], fk, fb);
         mma(accP[j], fq, fb);
       }
     }
@@ -491,8 +541,10 @@ struct ScanCtx {
 // Each chunk's loads are a wave-uniform (scalar) base plus a 32-bit lane
 // byte offset, so the loop does almost no per-lane address arithmetic.
 // OUT = false (state-saving scan of the backward): the query and P tiles are
-// not needed and not loaded.
-template <bool OUT, typename T, int DK, int GATE>
+// not needed and not loaded.  LA (linear attention, ATQ): no read-key tile;
+// the query tile is the preconditioned query the prep kernel left in the
+// workspace.
+template <bool OUT, bool LA, typename T, int DK, int GATE>
 __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdArgs& a, int i,
                                           const ScanCtx& x) {
   constexpr int KK = DK / 32, CT = DK / 64;
@@ -509,10 +561,17 @@ __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdAr
   const T* gb = static_cast<const T*>(a.KtG) + (x.bh * a.NT + i) * (int64_t)(DK * C);
   const uint32_t rr = static_cast<uint32_t>(min(16 * x.w + x.lr, last));
   const uint32_t okq = (rr * static_cast<uint32_t>(HD) + 8 * x.lg) * E;
+  if (LA) {
+    const T* qtb = static_cast<const T*>(a.Qt) + (x.bh * a.Tpad + t0) * DK;
+    const uint32_t oqt = (rr * static_cast<uint32_t>(DK) + 8 * x.lg) * E;
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) {
-    f.K[kk] = ld8(at_bytes(kb, okq + kk * 32 * E));
-    if (OUT) f.Q[kk] = ld8(at_bytes(qb, okq + kk * 32 * E));
+    for (int kk = 0; kk < KK; ++kk) f.Q[kk] = ld8(at_bytes(qtb, oqt + kk * 32 * E));
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      f.K[kk] = ld8(at_bytes(kb, okq + kk * 32 * E));
+      if (OUT) f.Q[kk] = ld8(at_bytes(qb, okq + kk * 32 * E));
+    }
   }
   const int ra = 16 * x.w + x.lr;
   const uint32_t otp = static_cast<uint32_t>(ra * C + 8 * x.lg) * E;
@@ -621,7 +680,7 @@ __device__ __forceinline__ void flush_slab_t(T* dst, int64_t ld, const T* src, i
   }
 }
 
-template <bool FULL, bool SAVE, bool OUT, typename T, int DK, int GATE>
+template <bool FULL, bool SAVE, bool OUT, bool LA, typename T, int DK, int GATE>
 __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float4* vnext,
                                           floatx4 (&st)[DK / 64][2], const FwdArgs& a, int i,
                                           const ScanCtx& x, T* sH, T* sX, T* sE, T* sVt, T* sO) {
@@ -642,7 +701,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
         const float e = fast_exp(f.gk[kk][s]);
-        f.K[kk].set(s, f.K[kk].get(s) * e);
+        if (!LA) f.K[kk].set(s, f.K[kk].get(s) * e);
         if (OUT) f.Q[kk].set(s, f.Q[kk].get(s) * e);
       }
   }
@@ -663,7 +722,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
     accO[vt] = accX[vt];
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      mma(accX[vt], f.K[kk], bH[vt][kk]);
+      if (!LA) mma(accX[vt], f.K[kk], bH[vt][kk]);   // linear attention: X = V
       if (OUT) mma(accO[vt], f.Q[kk], bH[vt][kk]);
     }
 #pragma unroll
@@ -730,7 +789,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
 // SAVE: also write the chunk-start states and the E rows the backward
 // reads.  OUT: compute and write the output (without it, queries and P are
 // neither loaded nor used: the backward's recompute).
-template <typename T, int DK, int GATE, bool SAVE, bool OUT>
+template <typename T, int DK, int GATE, bool SAVE, bool OUT, bool LA = false>
 __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   constexpr int CT = DK / 64;       // state row tiles per wave
   constexpr int LDH = DK + 8, LDE = C + 8;
@@ -787,32 +846,32 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   ScanFrags<T, DK, GATE> f0, f1, f2;
   const int last = a.NT - 1;
   const int NF = static_cast<int>(a.T / C);   // full chunks
-  scan_load<OUT>(f0, a, 0, x);
-  scan_load<OUT>(f1, a, min(1, last), x);
+  scan_load<OUT, LA>(f0, a, 0, x);
+  scan_load<OUT, LA>(f1, a, min(1, last), x);
   stage_values<T>(f0.v, sVt, x.tid);
   __syncthreads();
   int i = 0;
   for (; i + 2 < NF; i += 3) {
-    scan_load<OUT>(f2, a, i + 2, x);
-    scan_step<true, SAVE, OUT>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
-    scan_load<OUT>(f0, a, min(i + 3, last), x);
-    scan_step<true, SAVE, OUT>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
-    scan_load<OUT>(f1, a, min(i + 4, last), x);
-    scan_step<true, SAVE, OUT>(f2, f0.v, st, a, i + 2, x, sH, sX, sE, sVt, sO);
+    scan_load<OUT, LA>(f2, a, i + 2, x);
+    scan_step<true, SAVE, OUT, LA>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_load<OUT, LA>(f0, a, min(i + 3, last), x);
+    scan_step<true, SAVE, OUT, LA>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
+    scan_load<OUT, LA>(f1, a, min(i + 4, last), x);
+    scan_step<true, SAVE, OUT, LA>(f2, f0.v, st, a, i + 2, x, sH, sX, sE, sVt, sO);
   }
   // f0, f1 hold chunks i, i + 1 (clamped to the last chunk)
   if (NF - i == 2) {
-    scan_load<OUT>(f2, a, min(i + 2, last), x);
-    scan_step<true, SAVE, OUT>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
-    scan_step<true, SAVE, OUT>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
+    scan_load<OUT, LA>(f2, a, min(i + 2, last), x);
+    scan_step<true, SAVE, OUT, LA>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE, OUT, LA>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
     i += 2;
-    if (i < a.NT) scan_step<false, SAVE, OUT>(f2, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+    if (i < a.NT) scan_step<false, SAVE, OUT, LA>(f2, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
   } else if (NF - i == 1) {
-    scan_step<true, SAVE, OUT>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE, OUT, LA>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
     i += 1;
-    if (i < a.NT) scan_step<false, SAVE, OUT>(f1, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+    if (i < a.NT) scan_step<false, SAVE, OUT, LA>(f1, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
   } else if (i < a.NT) {
-    scan_step<false, SAVE, OUT>(f0, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<false, SAVE, OUT, LA>(f0, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
   }
   if (OUT) flush_output<T>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
   if (a.S_T) {
@@ -843,7 +902,7 @@ WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precon
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t o = off; off = align256(off + bytes); return o; };
   const size_t bh = static_cast<size_t>(BH), nt = static_cast<size_t>(NT);
-  if (precond == kSquash) {
+  if (has_gram(precond)) {
     L.sumL = take(bh * nt * dk * 4);
     L.sumD = take(bh * nt * 4);
     L.Abound = take(bh * (nt + 1) * dk * 4);
@@ -853,6 +912,7 @@ WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precon
   L.Pm = take(bh * nt * C * C * esz);
   if (gate == kGateScalar) L.G = take(bh * nt * C * 4);
   if (gate == kGateChannel) L.G = take(bh * nt * C * dk * 4);
+  if (precond == kATQ) L.Qt = take(bh * nt * C * dk * esz);
   L.total = off;
   return L;
 }
@@ -869,7 +929,11 @@ static hipError_t launch_k2_prec(const FwdArgs& a, hipStream_t s) {
   switch (a.precond) {
     case kSquash: return launch_k2<T, DK, GATE, kSquash, BWD>(a, s);
     case kIdentity: return launch_k2<T, DK, GATE, kIdentity, BWD>(a, s);
-    default: return launch_k2<T, DK, GATE, kExternal, BWD>(a, s);
+    case kExternal: return launch_k2<T, DK, GATE, kExternal, BWD>(a, s);
+    default:   // forward-only modes (the host rejects them for training)
+      if constexpr (BWD) return hipErrorInvalidValue;
+      else if (a.precond == kDiagSM) return launch_k2<T, DK, GATE, kDiagSM, false>(a, s);
+      else return launch_k2<T, DK, GATE, kATQ, false>(a, s);
   }
 }
 
@@ -880,7 +944,7 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
   hipError_t e;
   auto mark = [&](int i) { return ev ? hipEventRecord(ev[i], s) : hipSuccess; };
   if ((e = mark(0)) != hipSuccess) return e;
-  if (a.precond == kSquash) {
+  if (has_gram(a.precond)) {
     hipLaunchKernelGGL((k1_precond_summary<T, DK>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
                        0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -897,6 +961,23 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
   if ((e = mark(2)) != hipSuccess) return e;
   const int64_t nslab = a.dv / BV;
   const unsigned grid = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
+  if constexpr (!SAVE) {
+    if (a.precond == kATQ) {   // linear attention with the preconditioned query
+      switch (a.gate) {
+        case kGateNone:
+          hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, false, true, true>), dim3(grid), dim3(256), 0, s, a);
+          break;
+        case kGateScalar:
+          hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, false, true, true>), dim3(grid), dim3(256), 0, s, a);
+          break;
+        default:
+          hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, false, true, true>), dim3(grid), dim3(256), 0, s, a);
+          break;
+      }
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      return mark(3);
+    }
+  }
   switch (a.gate) {
     case kGateNone:
       hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, SAVE, true>), dim3(grid), dim3(256), 0, s, a); break;
@@ -917,7 +998,7 @@ static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s, hipEvent_t c
   hipError_t e;
   auto mark = [&](int i) { return ev ? hipEventRecord(ev[i], s) : hipSuccess; };
   if ((e = mark(0)) != hipSuccess) return e;
-  if (a.precond == kSquash) {
+  if (has_gram(a.precond)) {
     hipLaunchKernelGGL((k1_precond_summary<T, DK>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
                        0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;

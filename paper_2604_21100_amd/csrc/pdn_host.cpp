@@ -45,9 +45,13 @@ pdn_status check_problem(const pdn_problem* p, Sizes* sz) {
   if (p->gate != PDN_GATE_NONE && p->gate != PDN_GATE_SCALAR && p->gate != PDN_GATE_CHANNEL)
     return PDN_ERR_VALUE;
   if (p->precond != PDN_PRECOND_SQUASH && p->precond != PDN_PRECOND_IDENTITY &&
-      p->precond != PDN_PRECOND_EXTERNAL)
+      p->precond != PDN_PRECOND_EXTERNAL && p->precond != PDN_PRECOND_DIAG_SM &&
+      p->precond != PDN_PRECOND_ATQ)
     return PDN_ERR_VALUE;
   if (!std::isfinite(p->x) || !(p->x >= 1.0f) || !std::isfinite(p->scale)) return PDN_ERR_VALUE;
+  if ((p->precond == PDN_PRECOND_DIAG_SM || p->precond == PDN_PRECOND_ATQ) &&
+      (!std::isfinite(p->ridge) || !(p->ridge > 0.0f)))
+    return PDN_ERR_VALUE;
   Sizes s{};
   int64_t bt;
   if (!mul_ok(p->B, p->H, &s.BH) || !mul_ok(p->B, p->T, &bt) || !mul_ok(bt, p->H, &s.tok))
@@ -111,7 +115,8 @@ pdn_status check_inputs(const pdn_problem* p, const pdn_inputs* in, const Sizes&
   if (!empty) {
     if (!in->q || !in->k || !in->v || !in->beta) return PDN_ERR_NULL;
     if (p->gate != PDN_GATE_NONE && !in->g) return PDN_ERR_NULL;
-    if (p->precond == PDN_PRECOND_SQUASH && (!in->beta_p || !in->log_a_scale)) return PDN_ERR_NULL;
+    if (pdn::has_gram(p->precond) && !in->beta_p) return PDN_ERR_NULL;
+    if (p->precond == PDN_PRECOND_SQUASH && !in->log_a_scale) return PDN_ERR_NULL;
     if (p->precond == PDN_PRECOND_EXTERNAL && !in->ktilde) return PDN_ERR_NULL;
   }
   if (p->gate == PDN_GATE_NONE && in->g) return PDN_ERR_VALUE;
@@ -120,12 +125,12 @@ pdn_status check_inputs(const pdn_problem* p, const pdn_inputs* in, const Sizes&
       {in->q, s.nq * e}, {in->k, s.nq * e}, {in->v, s.nv * e}, {in->beta, s.nscal * 4},
       {in->g, s.ngate * 4}, {in->S0, s.nS * 4},
   };
-  if (p->precond == PDN_PRECOND_SQUASH) {
+  if (pdn::has_gram(p->precond)) {
     b.push_back({in->beta_p, s.nscal * 4});
     b.push_back({in->g_p, s.nscal * 4});
-    b.push_back({in->log_a_scale, p->H * 4});
     b.push_back({in->A0, s.nA * 4});
   }
+  if (p->precond == PDN_PRECOND_SQUASH) b.push_back({in->log_a_scale, p->H * 4});
   if (p->precond == PDN_PRECOND_EXTERNAL) b.push_back({in->ktilde, s.nq * e});
   for (const Buf& x : b)
     if (x.p && !aligned16(x.p)) return PDN_ERR_ALIGN;
@@ -133,10 +138,11 @@ pdn_status check_inputs(const pdn_problem* p, const pdn_inputs* in, const Sizes&
   return PDN_OK;
 }
 
-// the backward covers the no-gate and scalar-gate forms; fp32 io at head
-// dims 64
+// the backward covers every gate kind and the SQUASH / IDENTITY / EXTERNAL
+// write keys; fp32 io at head dims 64
 pdn_status check_bwd_support(const pdn_problem* p) {
   if (p->io == PDN_F32 && (p->dk != 64 || p->dv != 64)) return PDN_ERR_UNSUPPORTED;
+  if (p->precond == PDN_PRECOND_DIAG_SM || p->precond == PDN_PRECOND_ATQ) return PDN_ERR_UNSUPPORTED;
   return PDN_OK;
 }
 
@@ -182,7 +188,8 @@ pdn_status pdn_workspace_size(const pdn_problem* p, int with_bwd, size_t* bytes)
 // Forward intermediates the backward kernels read: the forward workspace
 // plus the residual arrays of the backward layout.
 static void set_forward_ws(pdn::FwdArgs& a, const pdn::WsLayout& L, const pdn_problem* p, char* w) {
-  if (p->precond == PDN_PRECOND_SQUASH) {
+  if (p->precond == PDN_PRECOND_ATQ) a.Qt = w + L.Qt;
+  if (pdn::has_gram(p->precond)) {
     a.sumL = reinterpret_cast<float*>(w + L.sumL);
     a.sumD = reinterpret_cast<float*>(w + L.sumD);
     a.Abound = reinterpret_cast<float*>(w + L.Abound);
@@ -211,7 +218,7 @@ static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn
   if (train && (st = check_bwd_support(p)) != PDN_OK) return st;
   if (!out) return PDN_ERR_NULL;
   if (s.tok > 0 && !out->o) return PDN_ERR_NULL;
-  if (p->precond != PDN_PRECOND_SQUASH && out->A_T) return PDN_ERR_VALUE;
+  if (!pdn::has_gram(p->precond) && out->A_T) return PDN_ERR_VALUE;
   const std::vector<Buf> outs = {{out->o, s.nv * s.esz}, {out->S_T, s.nS * 4}, {out->A_T, s.nA * 4}};
   for (const Buf& x : outs)
     if (x.p && !aligned16(x.p)) return PDN_ERR_ALIGN;
@@ -236,6 +243,7 @@ static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn
   a.gate = p->gate; a.precond = p->precond;
   a.lnx = std::log(p->x);
   a.scale = p->scale;
+  a.ridge = p->ridge;
   a.q = in->q; a.k = in->k; a.v = in->v; a.ktilde = in->ktilde;
   a.beta = in->beta; a.g = in->g; a.beta_p = in->beta_p; a.g_p = in->g_p;
   a.log_a_scale = in->log_a_scale; a.A0 = in->A0; a.S0 = in->S0;

@@ -10,7 +10,13 @@ namespace pdn {
 constexpr int kChunk = 64;  // chunk length C
 
 enum GateKind { kGateNone = 0, kGateScalar = 1, kGateChannel = 2 };
-enum PrecondKind { kSquash = 0, kIdentity = 1, kExternal = 2 };
+enum PrecondKind { kSquash = 0, kIdentity = 1, kExternal = 2, kDiagSM = 3, kATQ = 4 };
+
+// the write key (or, for ATQ, the query) comes from the diagonal Gram
+// recurrence A_t = exp(gP_t) A_{t-1} + betaP_t k_t^2
+constexpr bool has_gram(int precond) {
+  return precond == kSquash || precond == kDiagSM || precond == kATQ;
+}
 
 // Everything the forward kernels read or write.  Per-token tensors use the
 // ABI layout [B, T, H, d]; workspace tensors are head-major and padded to
@@ -23,6 +29,7 @@ struct FwdArgs {
   int gate, precond;
   float lnx;     // log(x)
   float scale;
+  float ridge;   // DIAG_SM / ATQ: lambda added to A before the inverse
   // inputs
   const void* q;
   const void* k;
@@ -47,6 +54,7 @@ struct FwdArgs {
   void* Tm;       // [BH, NT, C, C]  T = (I + At)^{-1} Diag(beta), io dtype
   void* Pm;       // [BH, NT, C, C]  causal (Q*Lam)(Kt/Lam)^T, io dtype
   float* G;       // [BH, Tpad] or [BH, Tpad, dk] in-chunk log-decay prefix
+  void* Qt;       // [BH, Tpad, dk] io   ATQ: preconditioned query rows q / (A + ridge)
   // backward only (NULL in the forward): forward intermediates kept for the
   // adjoint kernels.  lam_r = exp(G_r), w_r = exp(G_{C-1} - G_r).
   void* Hs;       // [BH, NT, dk, dv] io  chunk-start states S^T
@@ -87,7 +95,7 @@ struct BwdArgs {
 };
 
 struct WsLayout {
-  size_t sumL, sumD, Abound, KtG, Tm, Pm, G, total;
+  size_t sumL, sumD, Abound, KtG, Tm, Pm, G, Qt, total;
 };
 
 WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precond);

@@ -25,12 +25,13 @@ def run_fwd(spec, inp, precond="squash", dev=None, **kw):
     import paper_2604_21100_amd as pdn
     d = dev if dev is not None else to_device(inp, spec.io)
     sq = precond == "squash"
+    gram = precond in ("squash", "diag_sm", "atq")
     o, S_T, A_T = pdn.pdn_chunk_fwd(
         d["q"], d["k"], d["v"], d["beta"], g=d["g"], gate=spec.gate,
-        precond=precond, beta_p=d["beta_p"] if sq else None,
-        g_p=d["g_p"] if sq else None,
+        precond=precond, beta_p=d["beta_p"] if gram else None,
+        g_p=d["g_p"] if gram else None,
         log_a_scale=d["log_a_scale"] if sq else None,
-        A0=d["A0"] if sq else None, S0=d["S0"],
+        A0=d["A0"] if gram else None, S0=d["S0"],
         ktilde=d.get("ktilde") if precond == "external" else None,
         x=spec.x, scale=spec.scale, **kw)
     torch.cuda.synchronize()

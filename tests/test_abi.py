@@ -29,7 +29,9 @@ def test_header_symbols_exported():
     lib = ctypes.CDLL(pdn.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
-    assert pdn.pdn_abi_version() == 1
+    hdr = open(os.path.join(ROOT, "include", "pdn.h")).read()
+    ver = int(re.search(r"#define PDN_ABI_VERSION (\d+)", hdr).group(1))
+    assert pdn.pdn_abi_version() == ver == pdn.ABI_VERSION
 
 
 def test_status_strings():
@@ -64,6 +66,25 @@ def _fwd(prob, inp=None, out=None, ws=A * 64, ws_bytes=None):
         except pdn.PdnError:
             ws_bytes = 0
     return pdn.pdn_chunk_fwd_raw(prob, inp, out, ws, ws_bytes, 0)
+
+
+def test_forward_only_modes_validated():
+    """DIAG_SM and ATQ need a positive finite ridge; their backward is not
+    built (PDN_ERR_UNSUPPORTED, before any HIP call)."""
+    for pc in ("diag_sm", "atq"):
+        assert pdn.pdn_workspace_size(_prob(precond=pc, ridge=0.5)) > 0
+        for bad in (0.0, -1.0, float("nan"), float("inf")):
+            with pytest.raises(pdn.PdnError) as e:
+                pdn.pdn_workspace_size(_prob(precond=pc, ridge=bad))
+            assert e.value.status == pdn.PDN_ERR_VALUE
+        with pytest.raises(pdn.PdnError) as e:
+            pdn.pdn_workspace_size(_prob(precond=pc, ridge=0.5), True)
+        assert e.value.status == pdn.PDN_ERR_UNSUPPORTED
+    # the ridge is ignored by the other modes
+    assert pdn.pdn_workspace_size(_prob(ridge=0.0)) > 0
+    # ATQ keeps the preconditioned query rows in the workspace
+    assert (pdn.pdn_workspace_size(_prob(precond="atq", ridge=1.0))
+            > pdn.pdn_workspace_size(_prob(precond="diag_sm", ridge=1.0)))
 
 
 def test_workspace_size_monotone_and_validated():

@@ -16,14 +16,15 @@ from gpu_util import rel_err, run_fwd, tol
 pytestmark = pytest.mark.gpu
 
 
-def _oracle(spec, inp, precond="squash", heads=None):
+def _oracle(spec, inp, precond="squash", heads=None, ridge=1.0):
     return oabi.forward(inp, gate=spec.gate, precond=precond, x=spec.x,
-                        scale=spec.scale, heads=heads, B=spec.B, H=spec.H)
+                        scale=spec.scale, heads=heads, B=spec.B, H=spec.H,
+                        ridge=ridge)
 
 
-def _check_all_heads(spec, inp, precond="squash", tag=""):
-    o, S_T, A_T = run_fwd(spec, inp, precond)
-    ref = _oracle(spec, inp, precond)
+def _check_all_heads(spec, inp, precond="squash", tag="", ridge=1.0):
+    o, S_T, A_T = run_fwd(spec, inp, precond, ridge=ridge)
+    ref = _oracle(spec, inp, precond, ridge=ridge)
     B, T, H = spec.B, spec.T, spec.H
     ro = np.stack([ref["o"][b * H + h] for b in range(B) for h in range(H)])
     go = np.stack([o[b, :, h] for b in range(B) for h in range(H)])
@@ -33,7 +34,7 @@ def _check_all_heads(spec, inp, precond="squash", tag=""):
     print(msg)
     assert e_o <= tol(spec.io), msg
     assert e_s <= tol(spec.io), msg
-    if precond == "squash":
+    if precond in ("squash", "diag_sm", "atq"):
         e_a = rel_err(A_T.reshape(B * H, spec.dk), ref["A_T"])
         assert e_a <= 1e-4, f"{tag} err(A_T)={e_a:.2e}"
     return o, S_T, A_T
@@ -67,6 +68,42 @@ def test_small_all_heads(io, gate, precond, dk, dv):
         kt = inp["k"] * rng.uniform(1 / 1.5, 1.5, inp["k"].shape)
         inp["ktilde"] = pi.round_bf16(kt) if io == "bf16" else kt.astype(np.float32)
     _check_all_heads(spec, inp, precond, tag=f"{io}/{gate}/{precond}/{dk}x{dv}")
+
+
+MODES = [
+    # (io, gate, precond, dk, dv, ridge): the Sherman-Morrison write key
+    # (unstable ATK) and the apply-to-query linear attention (PLA /
+    # P-Mamba-2 / PGLA), forward only
+    ("bf16", "none", "diag_sm", 128, 128, 0.1),
+    ("bf16", "scalar", "diag_sm", 128, 128, 0.1),
+    ("bf16", "channel", "diag_sm", 64, 128, 0.5),
+    ("f32", "scalar", "diag_sm", 64, 64, 0.1),
+    ("f32", "channel", "diag_sm", 128, 64, 1.0),
+    ("bf16", "none", "atq", 128, 128, 0.1),
+    ("bf16", "scalar", "atq", 128, 128, 0.1),
+    ("bf16", "channel", "atq", 128, 64, 0.5),
+    ("f32", "channel", "atq", 64, 64, 0.1),
+    ("f32", "none", "atq", 128, 128, 1.0),
+]
+
+
+@pytest.mark.parametrize("io,gate,precond,dk,dv,ridge", MODES)
+def test_forward_only_modes(io, gate, precond, dk, dv, ridge):
+    """T = 200 (ragged tail), every head, nonzero S0 and A0, beta^P and g^P
+    as for the squash workloads."""
+    spec = pi.small_spec(io=io, gate=gate, dk=dk, dv=dv, s0="normal",
+                         a0="lognormal")
+    inp = pi.generate(spec, 13)
+    _check_all_heads(spec, inp, precond, ridge=ridge,
+                     tag=f"{io}/{gate}/{precond}/{dk}x{dv}/ridge={ridge}")
+
+
+@pytest.mark.parametrize("precond", ["diag_sm", "atq"])
+@pytest.mark.parametrize("T", [1, 65, 129])
+def test_forward_only_modes_lengths(precond, T):
+    spec = pi.small_spec(T=T, B=1, H=2, gate="scalar", dk=128, dv=128)
+    _check_all_heads(spec, pi.generate(spec, 700 + T), precond, ridge=0.2,
+                     tag=f"{precond} T={T}")
 
 
 @pytest.mark.parametrize("T", [1, 2, 63, 64, 65, 128, 129])

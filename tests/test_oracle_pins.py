@@ -112,6 +112,91 @@ def test_diag_sm_write_key_bounded():
     assert kk.min() >= 0.0 and kk.max() <= 1.0
 
 
+def test_general_modes_on_worked_example():
+    """The end-to-end oracle's Sherman-Morrison (diag_sm) and apply-to-query
+    (atq) modes reproduce the paper's printed values of App. B's worked
+    example (lambda = 1, k_1 = v_1 = [1, 1], beta = beta^P = 1, no decay):
+    kt_1 = 1/3 1, S^APDN_1 = 1/3 11^T and the read-out map 1/2 11^T."""
+    gd = _golden("worked_example.txt")
+    lam = float(gd["lambda"][0])
+    k = gd["k1"][None, None]
+    v = gd["v1"][None, None]
+    one = np.ones((1, 1))
+    for qv in ([1.0, 0.0], [0.0, 1.0]):
+        q = np.array(qv)[None, None]
+        r = recurrent.pdn_forward(q, k, v, one, precond="diag_sm", beta_p=one,
+                                  ridge=lam)
+        assert np.allclose(r["kt"][0, 0], gd["kt1"], atol=1e-15)
+        assert np.allclose(r["S_T"][0].ravel(), gd["S_APDN_1"], atol=1e-15)
+        ra = recurrent.pdn_forward(q, k, v, one, precond="atq", beta_p=one,
+                                   ridge=lam)
+        # o_1 = M_1 q with M_1 = S^APLA_1
+        M = gd["S_APLA_1"].reshape(2, 2)
+        assert np.allclose(ra["o"][0, 0], M @ np.array(qv), atol=1e-15)
+
+
+def _mode_inputs(rng, T, dk, dv, N=2):
+    k = rng.standard_normal((N, T, dk))
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    q = rng.standard_normal((N, T, dk))
+    v = rng.standard_normal((N, T, dv))
+    beta = 1.0 / (1.0 + np.exp(-rng.standard_normal((N, T))))
+    return q, k, v, beta
+
+
+def test_diag_sm_general_matches_single_head_form():
+    """With beta, beta^P, g^P and A0 all drawn at random (no gate), the
+    end-to-end diag_sm mode equals the single-head Sherman-Morrison
+    recurrence pinned above, head by head."""
+    rng = np.random.default_rng(21)
+    q, k, v, beta = _mode_inputs(rng, 40, 5, 3)
+    bp = rng.uniform(0.1, 2.0, (2, 40))
+    gp = -0.2 * rng.uniform(size=(2, 40))
+    A0 = rng.uniform(0.0, 1.0, (2, 5))
+    r = recurrent.pdn_forward(q, k, v, beta, precond="diag_sm", beta_p=bp,
+                              g_p=gp, A0=A0, ridge=0.3)
+    for n in range(2):
+        S_all, kts, o = recurrent.diag_sm_pdn(k[n], v[n], q[n], 0.3,
+                                              beta=beta[n], beta_p=bp[n],
+                                              g_p=gp[n], A0=A0[n])
+        assert np.allclose(r["kt"][n], kts, rtol=1e-13, atol=1e-15)
+        assert np.allclose(r["o"][n], o, rtol=1e-12, atol=1e-13)
+        assert np.allclose(r["S_T"][n], S_all[-1], rtol=1e-12, atol=1e-13)
+    kk = np.einsum("ntd,ntd->nt", k, r["kt"])
+    assert kk.min() >= 0.0 and kk.max() <= 1.0      # App. B stability bound
+
+
+def test_atq_general_matches_pla_form():
+    """With a scalar decay (P-Mamba-2) and beta^P = 1, g^P absent, the
+    end-to-end atq mode equals the single-head preconditioned linear
+    attention read-out pinned above."""
+    rng = np.random.default_rng(22)
+    q, k, v, beta = _mode_inputs(rng, 40, 5, 3)
+    g = -0.1 * np.log1p(np.exp(rng.standard_normal((2, 40))))
+    r = recurrent.pdn_forward(q, k, v, beta, g=g, gate="scalar",
+                              precond="atq", beta_p=np.ones((2, 40)),
+                              ridge=0.7, scale=0.5)
+    for n in range(2):
+        _, o = recurrent.atq_pla(k[n], v[n], q[n], 0.7, beta=beta[n], g=g[n])
+        assert np.allclose(r["o"][n], 0.5 * o, rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("precond", ["diag_sm", "atq"])
+def test_channel_gate_with_equal_channels_is_scalar_gate(precond):
+    """A per-channel decay whose channels all carry the same value is the
+    scalar decay: both general modes agree exactly under the two gates."""
+    rng = np.random.default_rng(23)
+    q, k, v, beta = _mode_inputs(rng, 30, 4, 3)
+    g = -0.2 * rng.uniform(size=(2, 30))
+    gc = np.repeat(g[:, :, None], 4, axis=2)
+    kw = dict(precond=precond, beta_p=rng.uniform(0.1, 1.0, (2, 30)),
+              g_p=-0.1 * rng.uniform(size=(2, 30)), ridge=0.4)
+    a = recurrent.pdn_forward(q, k, v, beta, g=g, gate="scalar", **kw)
+    b = recurrent.pdn_forward(q, k, v, beta, g=gc, gate="channel", **kw)
+    assert np.allclose(a["o"], b["o"], rtol=1e-13, atol=1e-14)
+    assert np.allclose(a["S_T"], b["S_T"], rtol=1e-13, atol=1e-14)
+
+
 # ---------------------------------------------------------------- Sec. 3.5
 def test_squash_range_monotone_and_fixed_points():
     """Eq. precond_end2end: B in [1/x, x], decreasing in A, B = 1 where
