@@ -138,7 +138,8 @@ def _oracle_job(args):
         return time.perf_counter() - t0
 
 
-def cpu_baseline(spec, inp, bwd, target_s=15.0, precond="squash", ridge=1.0):
+def cpu_baseline(spec, inp, bwd, target_s=15.0, precond="squash", ridge=1.0,
+                 knorm="none"):
     """Time the float64 oracle as it stands (token recurrence forward, and
     for bwd its adjoint as well) on a bounded sample: every head of the first
     nb batches over a prefix of Ts tokens, heads spread over worker
@@ -149,6 +150,8 @@ def cpu_baseline(spec, inp, bwd, target_s=15.0, precond="squash", ridge=1.0):
     kw = dict(gate=spec.gate, precond=precond, x=spec.x, scale=spec.scale)
     if precond != "squash":
         kw["ridge"] = ridge
+    if knorm != "none":
+        kw["knorm"] = knorm
 
     def sample_of(nb, Ts):
         s = {}
@@ -349,6 +352,9 @@ def main(argv=None):
                          "the latter two are forward only")
     ap.add_argument("--ridge", type=float, default=0.1,
                     help="ridge lambda of diag_sm / atq")
+    ap.add_argument("--knorm", default="none", choices=("none", "m", "1pm", "beta"),
+                    help="normalisation factor on the squash write key (the "
+                         "paper's ablation; forward only)")
     ap.add_argument("--recompute", action="store_true",
                     help="fwd+bwd with pdn_chunk_fwd + pdn_chunk_bwd (the "
                          "backward recomputes the forward intermediates)")
@@ -373,9 +379,9 @@ def main(argv=None):
     if args.sweep:
         return sweep(args)
     bwd = args.passes == "fwdbwd"
-    if bwd and args.precond != "squash":
-        print(f"bench.py: --precond {args.precond} is forward only; use "
-              "--pass fwd", file=sys.stderr)
+    if bwd and (args.precond != "squash" or args.knorm != "none"):
+        print(f"bench.py: --precond {args.precond} --knorm {args.knorm} is "
+              "forward only; use --pass fwd", file=sys.stderr)
         return 2
     spec = pi.WORKLOADS[args.workload]
     if bwd and not spec.with_do:
@@ -386,7 +392,7 @@ def main(argv=None):
     # the CPU leg runs before the GPU is touched (its worker processes fork)
     sq = args.precond == "squash"
     cpu = None if args.no_cpu_baseline else cpu_baseline(
-        spec, inp, bwd, args.cpu_seconds, args.precond, args.ridge)
+        spec, inp, bwd, args.cpu_seconds, args.precond, args.ridge, args.knorm)
 
     import torch
     import paper_2604_21100_amd as pdn
@@ -406,7 +412,7 @@ def main(argv=None):
     A_T = torch.empty((B, H, dk), dtype=torch.float32, device=dev)
     prob = pdn.make_problem(B, T, H, dk, dv, io=spec.io, gate=spec.gate,
                             precond=args.precond, x=spec.x, scale=spec.scale,
-                            ridge=args.ridge)
+                            ridge=args.ridge, knorm=args.knorm)
     ws = torch.empty(pdn.pdn_workspace_size(prob, with_bwd=bwd),
                      dtype=torch.uint8, device=dev)
     grads = None
@@ -443,7 +449,7 @@ def main(argv=None):
                           beta_p=d["beta_p"], g_p=d["g_p"],
                           log_a_scale=d["log_a_scale"] if sq else None,
                           A0=d["A0"], S0=d["S0"], x=spec.x, scale=spec.scale,
-                          ridge=args.ridge, o=o, S_T=S_T, A_T=A_T,
+                          ridge=args.ridge, knorm=args.knorm, o=o, S_T=S_T, A_T=A_T,
                           workspace=ws, stream=stream, stage_events=fev,
                           train=train)
         if bwd:
@@ -533,6 +539,7 @@ def main(argv=None):
                    "chunk": spec.chunk, "gate": spec.gate,
                    "precond": args.precond, "x": spec.x,
                    **({"ridge": args.ridge} if not sq else {}),
+                   **({"knorm": args.knorm} if args.knorm != "none" else {}),
                    "global_batch": B,
                    "seq_len": T, "parallelism": "none (1 GPU)"},
         "tflops": tflops,

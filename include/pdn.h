@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define PDN_ABI_VERSION 2
+#define PDN_ABI_VERSION 3
 
 typedef enum {
   PDN_OK = 0,
@@ -63,7 +63,8 @@ typedef enum {
   PDN_ERR_ALIAS = 6,       /* an output overlaps an input or another output    */
   PDN_ERR_WORKSPACE = 7,   /* workspace NULL, too small or misaligned          */
   PDN_ERR_VALUE = 8,       /* bad scalar (x < 1, non-finite x/scale, ridge <= 0
-                              for DIAG_SM / ATQ) or enum, or a gate pointer
+                              for DIAG_SM / ATQ) or enum (knorm other than
+                              NONE without SQUASH), or a gate pointer
                               inconsistent with the gate kind               */
   PDN_ERR_HIP = 9          /* a HIP launch failed                              */
 } pdn_status;
@@ -95,6 +96,20 @@ typedef enum {
   PDN_PRECOND_ATQ = 4
 } pdn_precond;
 
+/* Normalisation factor on the SQUASH write key (the ablation of App. E,
+ * "Stable parameterization", table of normalisation factors): with
+ * m_t = k_t^T B_t k_t,
+ *   kt_t = B_t k_t * { 1 | 1 / m_t | 1 / (1 + m_t) | beta_t / (alpha_t + beta_t m_t) }
+ * alpha_t = exp(g_t) for a scalar gate, 1 without a gate.  NONE is the
+ * method; the others are forward only, SQUASH only, and BETA is not
+ * defined for a per-channel gate (PDN_ERR_UNSUPPORTED).                    */
+typedef enum {
+  PDN_KNORM_NONE = 0,
+  PDN_KNORM_M = 1,      /* 1 / m_t                                          */
+  PDN_KNORM_1PM = 2,    /* 1 / (1 + m_t)                                    */
+  PDN_KNORM_BETA = 3    /* beta_t / (alpha_t + beta_t m_t)                  */
+} pdn_knorm;
+
 typedef struct {
   int64_t B, T, H;     /* batch, sequence length, heads; 0 is allowed      */
   int32_t dk, dv;      /* head dims: each 64 or 128                         */
@@ -106,6 +121,7 @@ typedef struct {
   float scale;         /* output scale (paper: 1.0)                         */
   float ridge;         /* DIAG_SM and ATQ: the ridge lambda > 0 added to A
                           before the elementwise inverse; ignored otherwise */
+  pdn_knorm knorm;     /* SQUASH write-key normalisation; NONE otherwise    */
 } pdn_problem;
 
 typedef struct {
@@ -180,7 +196,7 @@ pdn_status pdn_chunk_fwd_events(const pdn_problem* problem, const pdn_inputs* in
  * recomputed; `ws` must hold pdn_workspace_size(problem, 1) bytes.  The
  * output pointers dbeta_p, dg_p, dlog_a_scale, dA0 and dS0 may be NULL to
  * skip them.  SQUASH, IDENTITY and EXTERNAL only (DIAG_SM, ATQ:
- * PDN_ERR_UNSUPPORTED). */
+ * PDN_ERR_UNSUPPORTED), and knorm NONE only. */
 pdn_status pdn_chunk_bwd(const pdn_problem* problem, const pdn_inputs* in,
                          const void* dO, const float* dS_T, pdn_bwd_out* out,
                          void* ws, size_t ws_bytes, void* hip_stream);
@@ -215,7 +231,7 @@ pdn_status pdn_chunk_bwd_events(const pdn_problem* problem, const pdn_inputs* in
  * access stays inside the declared buffers).  pdn_chunk_bwd_train leaves the
  * saved intermediates intact, so it may be called again for another dO.
  * The backward's restrictions apply to both calls (fp32 io only with
- * d_k = d_v = 64; no DIAG_SM or ATQ: PDN_ERR_UNSUPPORTED).
+ * d_k = d_v = 64; no DIAG_SM or ATQ; knorm NONE: PDN_ERR_UNSUPPORTED).
  *
  * stage_events: NULL with n_events = 0, or PDN_FWD_STAGE_EVENTS /
  * PDN_BWD_STAGE_EVENTS caller-created events recorded as in the _events

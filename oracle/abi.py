@@ -55,7 +55,7 @@ def head_inputs(inp, heads, gate, precond):
 
 
 def forward(inp, *, gate, precond="squash", x=1.5, scale=1.0, heads=None,
-            B=None, H=None, ridge=1.0):
+            B=None, H=None, ridge=1.0, knorm="none"):
     """Token-recurrence forward for the selected heads.  Returns dict with
     o (n, T, dv), S_T (n, dk, dv) in ABI orientation, A_T (n, dk), kt."""
     if heads is None:
@@ -64,7 +64,8 @@ def forward(inp, *, gate, precond="squash", x=1.5, scale=1.0, heads=None,
     r = recurrent.pdn_forward(
         d["q"], d["k"], d["v"], d["beta"], g=d["g"], gate=gate,
         precond=precond, beta_p=d["beta_p"], g_p=d["g_p"], mu=d["mu"], x=x,
-        kt_ext=d["kt_ext"], S0=d["S0"], A0=d["A0"], scale=scale, ridge=ridge)
+        kt_ext=d["kt_ext"], S0=d["S0"], A0=d["A0"], scale=scale, ridge=ridge,
+        knorm=knorm)
     r["S_T"] = np.swapaxes(r["S_T"], 1, 2)
     return r
 

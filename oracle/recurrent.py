@@ -175,9 +175,32 @@ def linear_attention(q, k, v, beta, g=None, gate="none", S0=None, scale=1.0):
     return o, S
 
 
+def knorm_factor(k, kt, beta, g, gate, knorm):
+    """Normalisation factor on the squash write key (App. E "Stable
+    parameterization", ablation table), with m_t = k_t^T B_t k_t = k_t . kt_t:
+        "none" 1,  "m" 1/m_t,  "1pm" 1/(1 + m_t),
+        "beta" beta_t / (alpha_t + beta_t m_t)   (alpha_t = exp(g_t), scalar
+               gate; 1 without a gate)
+    Returns the (N, T, 1) factor."""
+    m = np.sum(_f64(k) * _f64(kt), axis=-1, keepdims=True)
+    if knorm == "none":
+        return np.ones_like(m)
+    if knorm == "m":
+        return 1.0 / m
+    if knorm == "1pm":
+        return 1.0 / (1.0 + m)
+    if knorm == "beta":
+        if gate == "channel":
+            raise ValueError("the beta factor needs a scalar decay")
+        al = np.ones_like(m) if gate == "none" else np.exp(_f64(g))[..., None]
+        b = _f64(beta)[..., None]
+        return b / (al + b * m)
+    raise ValueError(knorm)
+
+
 def pdn_forward(q, k, v, beta, *, g=None, gate="none", precond="squash",
                 beta_p=None, g_p=None, mu=None, x=1.5, kt_ext=None, S0=None,
-                A0=None, scale=1.0, ridge=1.0):
+                A0=None, scale=1.0, ridge=1.0, knorm="none"):
     """End-to-end token recurrence for PDN / PGDN / PKDA and the other
     preconditioner realisations.
 
@@ -189,6 +212,7 @@ def pdn_forward(q, k, v, beta, *, g=None, gate="none", precond="squash",
               "atq"       linear attention read through the preconditioned
                           query q_t / (A_t + ridge) (App. D "ATQ
                           preconditioner recurrence"); kt = k
+    knorm (squash only): the normalisation factor of knorm_factor.
     Returns dict(o, S_T, A_T, kt)."""
     k = _f64(k)
     N = k.shape[0]
@@ -197,6 +221,7 @@ def pdn_forward(q, k, v, beta, *, g=None, gate="none", precond="squash",
         if mu is None:
             mu = np.ones(N)
         kt, _, A_T = preconditioner_scan(k, beta_p, g_p, mu, x, A0)
+        kt = kt * knorm_factor(k, kt, beta, g, gate, knorm)
     elif precond == "identity":
         kt = k
     elif precond == "external":

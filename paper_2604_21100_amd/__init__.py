@@ -68,6 +68,8 @@ PRECONDS = {"squash": PDN_PRECOND_SQUASH, "identity": PDN_PRECOND_IDENTITY,
 # modes driven by the diagonal key-Gram recurrence (they take beta_p, g_p,
 # A0 and return A_T)
 GRAM_PRECONDS = ("squash", "diag_sm", "atq")
+# write-key normalisation of the squash mode (pdn_knorm)
+KNORMS = {"none": 0, "m": 1, "1pm": 2, "beta": 3}
 
 _vp = ctypes.c_void_p
 
@@ -78,7 +80,8 @@ class Problem(ctypes.Structure):
                 ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
                 ("io", ctypes.c_int), ("gate", ctypes.c_int),
                 ("precond", ctypes.c_int), ("x", ctypes.c_float),
-                ("scale", ctypes.c_float), ("ridge", ctypes.c_float)]
+                ("scale", ctypes.c_float), ("ridge", ctypes.c_float),
+                ("knorm", ctypes.c_int)]
 
 
 class Inputs(ctypes.Structure):
@@ -131,7 +134,7 @@ _lib.pdn_status_string.restype = ctypes.c_char_p
 _lib.pdn_abi_version.argtypes = []
 _lib.pdn_abi_version.restype = ctypes.c_int
 
-ABI_VERSION = 2   # PDN_ABI_VERSION: the struct layouts mirrored above
+ABI_VERSION = 3   # PDN_ABI_VERSION: the struct layouts mirrored above
 if _lib.pdn_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} implements ABI version "
                       f"{_lib.pdn_abi_version()}, this binding mirrors "
@@ -164,12 +167,13 @@ def pdn_abi_version() -> int:
 
 def make_problem(B, T, H, dk, dv, *, io="bf16", gate="none",
                  precond="squash", x=1.5, scale=1.0, chunk=64,
-                 ridge=1.0) -> Problem:
+                 ridge=1.0, knorm="none") -> Problem:
     return Problem(B, T, H, dk, dv, chunk,
                    PDN_BF16 if io == "bf16" else PDN_F32,
                    GATES[gate] if isinstance(gate, str) else int(gate),
                    PRECONDS[precond] if isinstance(precond, str)
-                   else int(precond), x, scale, ridge)
+                   else int(precond), x, scale, ridge,
+                   KNORMS[knorm] if isinstance(knorm, str) else int(knorm))
 
 
 def pdn_workspace_size(problem: Problem, with_bwd: bool = False) -> int:
@@ -237,9 +241,10 @@ def _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde):
 
 def pdn_chunk_fwd(q, k, v, beta, *, g=None, gate="none", precond="squash",
                   beta_p=None, g_p=None, log_a_scale=None, A0=None, S0=None,
-                  ktilde=None, x=1.5, scale=1.0, chunk=64, ridge=1.0, o=None,
-                  S_T=None, A_T=None, want_state=True, workspace=None,
-                  stream=None, stage_events=None, train=False):
+                  ktilde=None, x=1.5, scale=1.0, chunk=64, ridge=1.0,
+                  knorm="none", o=None, S_T=None, A_T=None, want_state=True,
+                  workspace=None, stream=None, stage_events=None,
+                  train=False):
     """Forward pass on torch device tensors in the ABI layouts of pdn.h.
 
     Returns (o, S_T, A_T); S_T / A_T are None when not requested.  Outputs and
@@ -253,7 +258,8 @@ def pdn_chunk_fwd(q, k, v, beta, *, g=None, gate="none", precond="squash",
     dv = v.shape[-1]
     io = _io_of(q)
     prob = make_problem(B, T, H, dk, dv, io=io, gate=gate, precond=precond,
-                        x=x, scale=scale, chunk=chunk, ridge=ridge)
+                        x=x, scale=scale, chunk=chunk, ridge=ridge,
+                        knorm=knorm)
     dev = q.device
     if o is None:
         o = torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)

@@ -245,10 +245,46 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     for (int q = 0; q < sg; ++q) A = sSegE[q * DK + c] * A + sSegP[q * DK + c];
     if (PREC == kSquash) {
       const float mu = fast_exp(a.log_a_scale[h]);
+      const float A_seg = A;
       for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
         const float kv = to_f(sK[r * LDK + c]);
         A = sEgp[r] * A + sBp[r] * kv * kv;
         sKt[r * LDK + c] = from_f<T>(squash_gain(A, mu, a.lnx) * kv);
+      }
+      if (a.knorm != kKnormNone) {
+        // normalisation ablation: kt = B k * f(m), m = k . (B k) per row;
+        // the rows' m from the stored keys, then the keys recomputed exactly
+        // and scaled once
+        float* sNrm = sY;   // free until the solve
+        __syncthreads();
+        {
+          constexpr int PART = DK / 4;
+          const int r = tid >> 2, part = tid & 3;
+          float m = 0.f;
+          for (int cc = part * PART; cc < (part + 1) * PART; ++cc)
+            m += to_f(sK[r * LDK + cc]) * to_f(sKt[r * LDK + cc]);
+          m += __shfl_xor(m, 1, 64);
+          m += __shfl_xor(m, 2, 64);
+          if (part == 0) {
+            float f = 0.f;   // rows past the sequence end: zero keys
+            if (r < n) {
+              if (a.knorm == kKnormM) f = 1.f / m;
+              else if (a.knorm == kKnorm1pm) f = 1.f / (1.f + m);
+              else {
+                const float al = GATE == kGateScalar ? fast_exp(sGraw[r]) : 1.f;
+                f = sBeta[r] / (al + sBeta[r] * m);
+              }
+            }
+            sNrm[r] = f;
+          }
+        }
+        __syncthreads();
+        A = A_seg;
+        for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
+          const float kv = to_f(sK[r * LDK + c]);
+          A = sEgp[r] * A + sBp[r] * kv * kv;
+          sKt[r * LDK + c] = from_f<T>(squash_gain(A, mu, a.lnx) * kv * sNrm[r]);
+        }
       }
     }
     if (PREC == kATQ) {

@@ -52,6 +52,9 @@ pdn_status check_problem(const pdn_problem* p, Sizes* sz) {
   if ((p->precond == PDN_PRECOND_DIAG_SM || p->precond == PDN_PRECOND_ATQ) &&
       (!std::isfinite(p->ridge) || !(p->ridge > 0.0f)))
     return PDN_ERR_VALUE;
+  if (p->knorm < PDN_KNORM_NONE || p->knorm > PDN_KNORM_BETA) return PDN_ERR_VALUE;
+  if (p->knorm != PDN_KNORM_NONE && p->precond != PDN_PRECOND_SQUASH) return PDN_ERR_VALUE;
+  if (p->knorm == PDN_KNORM_BETA && p->gate == PDN_GATE_CHANNEL) return PDN_ERR_UNSUPPORTED;
   Sizes s{};
   int64_t bt;
   if (!mul_ok(p->B, p->H, &s.BH) || !mul_ok(p->B, p->T, &bt) || !mul_ok(bt, p->H, &s.tok))
@@ -143,6 +146,7 @@ pdn_status check_inputs(const pdn_problem* p, const pdn_inputs* in, const Sizes&
 pdn_status check_bwd_support(const pdn_problem* p) {
   if (p->io == PDN_F32 && (p->dk != 64 || p->dv != 64)) return PDN_ERR_UNSUPPORTED;
   if (p->precond == PDN_PRECOND_DIAG_SM || p->precond == PDN_PRECOND_ATQ) return PDN_ERR_UNSUPPORTED;
+  if (p->knorm != PDN_KNORM_NONE) return PDN_ERR_UNSUPPORTED;
   return PDN_OK;
 }
 
@@ -244,6 +248,7 @@ static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn
   a.lnx = std::log(p->x);
   a.scale = p->scale;
   a.ridge = p->ridge;
+  a.knorm = p->knorm;
   a.q = in->q; a.k = in->k; a.v = in->v; a.ktilde = in->ktilde;
   a.beta = in->beta; a.g = in->g; a.beta_p = in->beta_p; a.g_p = in->g_p;
   a.log_a_scale = in->log_a_scale; a.A0 = in->A0; a.S0 = in->S0;

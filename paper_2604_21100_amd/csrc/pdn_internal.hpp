@@ -11,6 +11,7 @@ constexpr int kChunk = 64;  // chunk length C
 
 enum GateKind { kGateNone = 0, kGateScalar = 1, kGateChannel = 2 };
 enum PrecondKind { kSquash = 0, kIdentity = 1, kExternal = 2, kDiagSM = 3, kATQ = 4 };
+enum KnormKind { kKnormNone = 0, kKnormM = 1, kKnorm1pm = 2, kKnormBeta = 3 };
 
 // the write key (or, for ATQ, the query) comes from the diagonal Gram
 // recurrence A_t = exp(gP_t) A_{t-1} + betaP_t k_t^2
@@ -30,6 +31,7 @@ struct FwdArgs {
   float lnx;     // log(x)
   float scale;
   float ridge;   // DIAG_SM / ATQ: lambda added to A before the inverse
+  int knorm;     // SQUASH write-key normalisation (pdn_knorm)
   // inputs
   const void* q;
   const void* k;

@@ -82,6 +82,22 @@ def test_forward_only_modes_validated():
         assert e.value.status == pdn.PDN_ERR_UNSUPPORTED
     # the ridge is ignored by the other modes
     assert pdn.pdn_workspace_size(_prob(ridge=0.0)) > 0
+    # write-key normalisation: squash only, forward only, and the beta
+    # factor needs a scalar (or no) decay
+    for kn in ("m", "1pm", "beta"):
+        assert pdn.pdn_workspace_size(_prob(knorm=kn)) > 0
+        with pytest.raises(pdn.PdnError) as e:
+            pdn.pdn_workspace_size(_prob(knorm=kn), True)
+        assert e.value.status == pdn.PDN_ERR_UNSUPPORTED
+        with pytest.raises(pdn.PdnError) as e:
+            pdn.pdn_workspace_size(_prob(knorm=kn, precond="identity"))
+        assert e.value.status == pdn.PDN_ERR_VALUE
+    with pytest.raises(pdn.PdnError) as e:
+        pdn.pdn_workspace_size(_prob(knorm="beta", gate="channel"))
+    assert e.value.status == pdn.PDN_ERR_UNSUPPORTED
+    with pytest.raises(pdn.PdnError) as e:
+        pdn.pdn_workspace_size(_prob(knorm=7))
+    assert e.value.status == pdn.PDN_ERR_VALUE
     # ATQ keeps the preconditioned query rows in the workspace
     assert (pdn.pdn_workspace_size(_prob(precond="atq", ridge=1.0))
             > pdn.pdn_workspace_size(_prob(precond="diag_sm", ridge=1.0)))

@@ -98,6 +98,35 @@ def test_forward_only_modes(io, gate, precond, dk, dv, ridge):
                      tag=f"{io}/{gate}/{precond}/{dk}x{dv}/ridge={ridge}")
 
 
+KNORMS = [
+    # (io, gate, knorm, dk, dv): the write-key normalisation ablation
+    ("bf16", "scalar", "m", 128, 128),
+    ("bf16", "none", "1pm", 128, 64),
+    ("bf16", "scalar", "beta", 64, 128),
+    ("bf16", "channel", "1pm", 128, 128),
+    ("f32", "scalar", "beta", 64, 64),
+    ("f32", "channel", "m", 64, 64),
+]
+
+
+@pytest.mark.parametrize("io,gate,knorm,dk,dv", KNORMS)
+def test_squash_write_key_normalisations(io, gate, knorm, dk, dv):
+    import torch
+    spec = pi.small_spec(io=io, gate=gate, dk=dk, dv=dv, s0="normal",
+                         a0="lognormal")
+    inp = pi.generate(spec, 17)
+    o, S_T, A_T = run_fwd(spec, inp, "squash", knorm=knorm)
+    ref = oabi.forward(inp, gate=gate, precond="squash", x=spec.x,
+                       scale=spec.scale, B=spec.B, H=spec.H, knorm=knorm)
+    B, H = spec.B, spec.H
+    go = np.stack([o[b, :, h] for b in range(B) for h in range(H)])
+    e_o = rel_err(go, ref["o"])
+    e_s = rel_err(S_T.reshape(B * H, dk, dv), ref["S_T"])
+    msg = f"{io}/{gate}/knorm={knorm}/{dk}x{dv} err(o)={e_o:.2e} err(S_T)={e_s:.2e}"
+    print(msg)
+    assert e_o <= tol(io) and e_s <= tol(io), msg
+
+
 @pytest.mark.parametrize("precond", ["diag_sm", "atq"])
 @pytest.mark.parametrize("T", [1, 65, 129])
 def test_forward_only_modes_lengths(precond, T):

@@ -197,6 +197,46 @@ def test_channel_gate_with_equal_channels_is_scalar_gate(precond):
     assert np.allclose(a["S_T"], b["S_T"], rtol=1e-13, atol=1e-14)
 
 
+def test_knorm_factors_reduce_at_x_1():
+    """x = 1 makes B = 1, so with unit keys m_t = 1 and the normalisation
+    ablation's factors become constants: 1/m = 1 (the identity write key),
+    1/(1+m) = 1/2 and beta/(alpha + beta m) = beta/(alpha + beta), each an
+    external write key written in closed form."""
+    rng = np.random.default_rng(24)
+    q, k, v, beta = _mode_inputs(rng, 30, 4, 3)
+    g = -0.3 * rng.uniform(size=(2, 30))
+    kw = dict(g=g, gate="scalar", beta_p=rng.uniform(0.1, 1.0, (2, 30)),
+              g_p=-0.1 * rng.uniform(size=(2, 30)), x=1.0)
+    ident = recurrent.pdn_forward(q, k, v, beta, precond="identity", g=g,
+                                  gate="scalar")
+    r = recurrent.pdn_forward(q, k, v, beta, knorm="m", **kw)
+    assert np.allclose(r["o"], ident["o"], rtol=1e-12, atol=1e-13)
+    half = recurrent.pdn_forward(q, k, v, beta, precond="external",
+                                 kt_ext=0.5 * k, g=g, gate="scalar")
+    r = recurrent.pdn_forward(q, k, v, beta, knorm="1pm", **kw)
+    assert np.allclose(r["o"], half["o"], rtol=1e-12, atol=1e-13)
+    fac = (beta / (np.exp(g) + beta))[..., None]
+    ext = recurrent.pdn_forward(q, k, v, beta, precond="external",
+                                kt_ext=fac * k, g=g, gate="scalar")
+    r = recurrent.pdn_forward(q, k, v, beta, knorm="beta", **kw)
+    assert np.allclose(r["o"], ext["o"], rtol=1e-12, atol=1e-13)
+
+
+def test_knorm_invariants():
+    """With the squash gain in force (x = 1.5, keys of varied norm): the 1/m
+    factor makes k^T kt = 1 exactly and the 1/(1+m) factor keeps it in
+    [0, 1)."""
+    rng = np.random.default_rng(25)
+    q, k, v, beta = _mode_inputs(rng, 50, 6, 2)
+    k = k * np.exp(rng.standard_normal((2, 50, 1)))
+    kw = dict(beta_p=rng.uniform(0.01, 2.0, (2, 50)), x=1.5)
+    r = recurrent.pdn_forward(q, k, v, beta, knorm="m", **kw)
+    assert np.allclose(np.sum(k * r["kt"], axis=-1), 1.0, rtol=1e-13)
+    r = recurrent.pdn_forward(q, k, v, beta, knorm="1pm", **kw)
+    kk = np.sum(k * r["kt"], axis=-1)
+    assert kk.min() >= 0.0 and kk.max() < 1.0
+
+
 # ---------------------------------------------------------------- Sec. 3.5
 def test_squash_range_monotone_and_fixed_points():
     """Eq. precond_end2end: B in [1/x, x], decreasing in A, B = 1 where
