@@ -182,8 +182,10 @@ pdn_status pdn_chunk_fwd(const pdn_problem* problem, const pdn_inputs* in,
  *   stage_events[1]  after it / before the per-chunk prep kernel (k2)
  *   stage_events[2]  after k2 / before the inter-chunk scan + output (k3)
  *   stage_events[3]  after k3
- * n_events must be 4 (else PDN_ERR_VALUE).  The events stay owned by the
- * caller; results are identical to pdn_chunk_fwd. */
+ * n_events must be 4 (else PDN_ERR_VALUE); a NULL entry is not recorded
+ * (each record costs a few microseconds of GPU time between kernels, so a
+ * caller timing one stage passes only its two boundaries).  The events stay
+ * owned by the caller; results are identical to pdn_chunk_fwd. */
 #define PDN_FWD_STAGE_EVENTS 4
 pdn_status pdn_chunk_fwd_events(const pdn_problem* problem, const pdn_inputs* in,
                                 pdn_fwd_out* out, void* ws, size_t ws_bytes,
@@ -209,7 +211,7 @@ pdn_status pdn_chunk_bwd(const pdn_problem* problem, const pdn_inputs* in,
  *   [4] after the reverse state-adjoint scan (r1)
  *   [5] after the per-chunk adjoints and gradients (p12)
  *   [6] after the preconditioner's reverse scan (pc_*) or the key combine
- * Results are identical to pdn_chunk_bwd. */
+ * NULL entries are not recorded.  Results are identical to pdn_chunk_bwd. */
 #define PDN_BWD_STAGE_EVENTS 7
 pdn_status pdn_chunk_bwd_events(const pdn_problem* problem, const pdn_inputs* in,
                                 const void* dO, const float* dS_T, pdn_bwd_out* out,

@@ -276,7 +276,8 @@ def pdn_chunk_fwd(q, k, v, beta, *, g=None, gate="none", precond="squash",
     inp = _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde)
     out = FwdOut(_ptr(o), _ptr(S_T), _ptr(A_T))
     if train:
-        evs = [_event_handle(e) for e in (stage_events or [])]
+        evs = [_event_handle(e) if e is not None else None
+               for e in (stage_events or [])]
         arr = (_vp * len(evs))(*evs) if evs else None
         st = _lib.pdn_chunk_fwd_train(
             ctypes.byref(prob), ctypes.byref(inp), ctypes.byref(out),
@@ -288,7 +289,8 @@ def pdn_chunk_fwd(q, k, v, beta, *, g=None, gate="none", precond="squash",
     else:
         st = pdn_chunk_fwd_events_raw(
             prob, inp, out, _ptr(workspace), workspace.numel(),
-            _stream(stream, dev), [_event_handle(e) for e in stage_events])
+            _stream(stream, dev),
+            [_event_handle(e) if e is not None else None for e in stage_events])
     if st != PDN_OK:
         raise PdnError(st, "pdn_chunk_fwd")
     return o, S_T, A_T
@@ -352,7 +354,8 @@ def pdn_chunk_bwd(q, k, v, beta, dO, *, g=None, gate="none", precond="squash",
     inp = _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde)
     bo = BwdOut(*[_ptr(out.get(n)) for n, _ in BwdOut._fields_])
     if saved:
-        evs = [_event_handle(e) for e in (stage_events or [])]
+        evs = [_event_handle(e) if e is not None else None
+               for e in (stage_events or [])]
         arr = (_vp * len(evs))(*evs) if evs else None
         st = _lib.pdn_chunk_bwd_train(
             ctypes.byref(prob), ctypes.byref(inp), _ptr(dO), _ptr(dS_T),
@@ -363,7 +366,8 @@ def pdn_chunk_bwd(q, k, v, beta, dO, *, g=None, gate="none", precond="squash",
                                _ptr(workspace), workspace.numel(),
                                _stream(stream, dev))
     else:
-        evs = [_event_handle(e) for e in stage_events]
+        evs = [_event_handle(e) if e is not None else None
+               for e in stage_events]
         arr = (_vp * len(evs))(*evs)
         st = _lib.pdn_chunk_bwd_events(
             ctypes.byref(prob), ctypes.byref(inp), _ptr(dO), _ptr(dS_T),

@@ -1356,7 +1356,7 @@ template <typename T, int DK, int DV, int GATE>
 static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s, hipEvent_t const* ev) {
   const FwdArgs& a = ba.f;
   hipError_t e;
-  auto mark = [&](int i) { return ev ? hipEventRecord(ev[i], s) : hipSuccess; };
+  auto mark = [&](int i) { return ev && ev[i] ? hipEventRecord(ev[i], s) : hipSuccess; };
   const int64_t nslab = DV / BVB;
   const unsigned grid_scan = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
   const unsigned grid_chunk = static_cast<unsigned>(a.BH * a.NT);
@@ -1418,7 +1418,8 @@ hipError_t launch_backward(const BwdArgs& ba, int io_bf16, hipStream_t s, hipEve
   if (recompute) {
     e = launch_forward_parts(ba.f, io_bf16, s, ev);
   } else if (ev) {   // no recompute: its stages are empty
-    for (int k = 0; k < 4 && e == hipSuccess; ++k) e = hipEventRecord(ev[k], s);
+    for (int k = 0; k < 4 && e == hipSuccess; ++k)
+      if (ev[k]) e = hipEventRecord(ev[k], s);
   }
   if (e != hipSuccess) return e;
   return io_bf16 ? launch_bwd_dims<bf16>(ba, s, ev) : launch_bwd_f32(ba, s, ev);

@@ -978,7 +978,7 @@ static hipError_t launch_k2_prec(const FwdArgs& a, hipStream_t s) {
 template <typename T, int DK, bool SAVE>
 static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* ev) {
   hipError_t e;
-  auto mark = [&](int i) { return ev ? hipEventRecord(ev[i], s) : hipSuccess; };
+  auto mark = [&](int i) { return ev && ev[i] ? hipEventRecord(ev[i], s) : hipSuccess; };
   if ((e = mark(0)) != hipSuccess) return e;
   if (has_gram(a.precond)) {
     hipLaunchKernelGGL((k1_precond_summary<T, DK>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
@@ -1032,7 +1032,7 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
 template <typename T, int DK>
 static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s, hipEvent_t const* ev) {
   hipError_t e;
-  auto mark = [&](int i) { return ev ? hipEventRecord(ev[i], s) : hipSuccess; };
+  auto mark = [&](int i) { return ev && ev[i] ? hipEventRecord(ev[i], s) : hipSuccess; };
   if ((e = mark(0)) != hipSuccess) return e;
   if (has_gram(a.precond)) {
     hipLaunchKernelGGL((k1_precond_summary<T, DK>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
@@ -1073,7 +1073,7 @@ hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent
     // nothing to time: the stage events still mark the (empty) stages
     if (ev)
       for (int i = 0; i < 4; ++i)
-        if (hipEventRecord(ev[i], s) != hipSuccess) return hipErrorInvalidValue;
+        if (ev[i] && hipEventRecord(ev[i], s) != hipSuccess) return hipErrorInvalidValue;
   }
   if (a.BH == 0) return hipSuccess;
   if (a.T == 0) {

@@ -273,8 +273,6 @@ pdn_status pdn_chunk_fwd_events(const pdn_problem* p, const pdn_inputs* in, pdn_
                                 void* const* stage_events, int n_events) {
   if (!stage_events) return PDN_ERR_NULL;
   if (n_events != PDN_FWD_STAGE_EVENTS) return PDN_ERR_VALUE;
-  for (int i = 0; i < n_events; ++i)
-    if (!stage_events[i]) return PDN_ERR_NULL;
   return chunk_fwd_impl(p, in, out, ws, ws_bytes, hip_stream,
                         reinterpret_cast<hipEvent_t const*>(stage_events), false);
 }
@@ -319,7 +317,7 @@ static pdn_status chunk_bwd_impl(const pdn_problem* p, const pdn_inputs* in, con
   if (s.BH == 0 || !tok) {
     if (ev)  // nothing to time: the stage events still mark the empty stages
       for (int k = 0; k < PDN_BWD_STAGE_EVENTS; ++k)
-        if (hipEventRecord(ev[k], stream) != hipSuccess) return PDN_ERR_HIP;
+        if (ev[k] && hipEventRecord(ev[k], stream) != hipSuccess) return PDN_ERR_HIP;
   }
   if (s.BH == 0) return PDN_OK;
   if (!tok) {
@@ -371,18 +369,15 @@ pdn_status pdn_chunk_bwd_events(const pdn_problem* p, const pdn_inputs* in, cons
                                 void* hip_stream, void* const* stage_events, int n_events) {
   if (!stage_events) return PDN_ERR_NULL;
   if (n_events != PDN_BWD_STAGE_EVENTS) return PDN_ERR_VALUE;
-  for (int i = 0; i < n_events; ++i)
-    if (!stage_events[i]) return PDN_ERR_NULL;
   return chunk_bwd_impl(p, in, dO, dS_T, out, ws, ws_bytes, hip_stream,
                         reinterpret_cast<hipEvent_t const*>(stage_events), false);
 }
 
-// stage_events: NULL (n_events 0) or n_events == n events, all non-NULL
+// stage_events: NULL (n_events 0) or an array of n_events == n entries
+// (NULL entries are skipped)
 static pdn_status check_events(void* const* ev, int n_events, int n) {
   if (!ev) return n_events == 0 ? PDN_OK : PDN_ERR_NULL;
   if (n_events != n) return PDN_ERR_VALUE;
-  for (int i = 0; i < n_events; ++i)
-    if (!ev[i]) return PDN_ERR_NULL;
   return PDN_OK;
 }
 

@@ -215,11 +215,17 @@ def test_stage_event_arguments_validated():
     assert lib.pdn_chunk_bwd_events(
         ctypes.byref(p), ctypes.byref(_inputs()), A * 30, None,
         ctypes.byref(bo), A * 64, 0, None, ev_b, 6) == pdn.PDN_ERR_VALUE
+    # NULL entries are allowed (not recorded): validation then goes on to the
+    # problem and reaches the missing workspace
     ev_b[3] = None
+    plain = lib.pdn_chunk_bwd(
+        ctypes.byref(p), ctypes.byref(_inputs()), A * 30, None,
+        ctypes.byref(bo), A * 64, 0, None)
+    assert plain == pdn.PDN_ERR_NULL      # the outputs are missing
     assert lib.pdn_chunk_bwd_events(
         ctypes.byref(p), ctypes.byref(_inputs()), A * 30, None,
         ctypes.byref(bo), A * 64, 0, None, ev_b,
-        pdn.BWD_STAGE_EVENTS) == pdn.PDN_ERR_NULL
+        pdn.BWD_STAGE_EVENTS) == plain
     # with valid event pointers, problem validation still comes first
     ev_b[3] = A * 40
     assert lib.pdn_chunk_bwd_events(
