@@ -1275,10 +1275,25 @@ __global__ __launch_bounds__(DK) void pc_carry(BwdArgs ba) {
   const int64_t bh = blockIdx.x;
   const int c = threadIdx.x;
   float carry = 0.f;
-  ba.pcC[(bh * (a.NT + 1) + a.NT) * DK + c] = 0.f;
-  for (int i = a.NT - 1; i >= 0; --i) {
-    ba.pcC[(bh * (a.NT + 1) + i + 1) * DK + c] = carry;
-    carry = ba.pcL[(bh * a.NT + i) * DK + c] + fast_exp(a.sumD[bh * a.NT + i]) * carry;
+  float* out = ba.pcC + bh * (a.NT + 1) * DK + c;
+  const float* L = ba.pcL + bh * a.NT * DK + c;
+  const float* D = a.sumD + bh * a.NT;
+  out[(int64_t)a.NT * DK] = 0.f;
+  int i = a.NT - 1;
+  // eight chunks' inputs in flight at a time; the chain itself is cheap
+  for (; i >= 7; i -= 8) {
+    float l[8], d[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) { l[u] = L[(int64_t)(i - u) * DK]; d[u] = D[i - u]; }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      out[(int64_t)(i - u + 1) * DK] = carry;
+      carry = l[u] + fast_exp(d[u]) * carry;
+    }
+  }
+  for (; i >= 0; --i) {
+    out[(int64_t)(i + 1) * DK] = carry;
+    carry = L[(int64_t)i * DK] + fast_exp(D[i]) * carry;
   }
   if (ba.dA0) ba.dA0[bh * DK + c] = carry;
 }

@@ -251,3 +251,24 @@ def test_full_workload_sampled_heads(name):
         print(f"{name} head {(b, h)}: err(o)={e_o:.2e} err(S_T)={e_s:.2e} err(A_T)={e_a:.2e}")
         assert e_o <= tol(spec.io) and e_s <= tol(spec.io) and e_a <= 1e-4
     assert np.isfinite(o).all() and np.isfinite(S_T).all()
+
+
+@pytest.mark.parametrize("precond,gate,ridge", [("diag_sm", "scalar", 0.1),
+                                                ("atq", "scalar", 0.1),
+                                                ("atq", "channel", 0.1)])
+def test_forward_only_modes_full_layer(precond, gate, ridge):
+    """The forward-only modes at the 1B layer shape (B=4, T=4096, H=16,
+    d=128; the PGLA case with the PKDA layer's per-channel gate recipe) in
+    the benchmark's launch configuration; two sampled heads end to end."""
+    name = "pgdn_bf16_b4_t4096_h16_d128"
+    spec = pi.WORKLOADS[name].replace(gate=gate)
+    inp = pi.generate(spec, pi.WORKLOAD_SEEDS[name])
+    o, S_T, A_T = run_fwd(spec, inp, precond, ridge=ridge)
+    heads = [(0, 0), (spec.B - 1, spec.H - 1)]
+    ref = _oracle(spec, inp, precond, heads=heads, ridge=ridge)
+    for n, (b, h) in enumerate(heads):
+        e_o = rel_err(o[b, :, h], ref["o"][n])
+        e_s = rel_err(S_T[b, h], ref["S_T"][n])
+        e_a = rel_err(A_T[b, h], ref["A_T"][n])
+        print(f"{precond}/{gate} head {(b, h)}: err(o)={e_o:.2e} err(S_T)={e_s:.2e} err(A_T)={e_a:.2e}")
+        assert e_o <= tol(spec.io) and e_s <= tol(spec.io) and e_a <= 1e-4
