@@ -110,6 +110,19 @@ __global__ __launch_bounds__(DK) void k1_precond_carry(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------- K2
+// k2's tiles are read along rows (MFMA fragments, row staging) and down
+// columns (the transposed outputs, the column-wise scans).  The column index
+// is XOR-permuted in aligned groups (8 elements for the key / query tiles, 4
+// for the fp32 tiles) by the row's 8-row block, so that 8 lanes reading one
+// column from rows 8 apart hit 8 different bank groups while row segments
+// of a group stay contiguous.
+template <typename T>
+__device__ __forceinline__ T* k2sw(T* base, int ld, int row, int col) {
+  return base + row * ld + (col ^ (((row >> 3) & 7) << 3));
+}
+__device__ __forceinline__ float* k2swf(float* base, int ld, int row, int col) {
+  return base + row * ld + (col ^ (((row >> 3) & 7) << 2));
+}
 template <typename T, int DK, int GATE>
 struct K2Smem {
   static constexpr int LDK = DK + 8;          // padded row (elements)
@@ -173,12 +186,12 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         qv = *reinterpret_cast<const float4*>(qp + off);
         if (PREC == kExternal) xv = *reinterpret_cast<const float4*>(xp + off);
       }
-      *reinterpret_cast<float4*>(sK + r * LDK + cv * VEC) = kv;
-      *reinterpret_cast<float4*>(sQ + r * LDK + cv * VEC) = qv;
+      *reinterpret_cast<float4*>(k2sw(sK, LDK, r, cv * VEC)) = kv;
+      *reinterpret_cast<float4*>(k2sw(sQ, LDK, r, cv * VEC)) = qv;
       // identity write key: a copy of the key tile (the key tile's memory is
       // reused by the solve)
-      if (PREC == kIdentity || PREC == kATQ) *reinterpret_cast<float4*>(sKt + r * LDK + cv * VEC) = kv;
-      if (PREC == kExternal) *reinterpret_cast<float4*>(sKt + r * LDK + cv * VEC) = xv;
+      if (PREC == kIdentity || PREC == kATQ) *reinterpret_cast<float4*>(k2sw(sKt, LDK, r, cv * VEC)) = kv;
+      if (PREC == kExternal) *reinterpret_cast<float4*>(k2sw(sKt, LDK, r, cv * VEC)) = xv;
     }
     if (tid < C) {
       const int r = tid;
@@ -197,7 +210,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         float4 gv = make_float4(0.f, 0.f, 0.f, 0.f);
         if (r < n)
           gv = *reinterpret_cast<const float4*>(a.g + ((b * a.T + t0 + r) * a.H + h) * DK + c4 * 4);
-        *reinterpret_cast<float4*>(sGc + r * (DK + 4) + c4 * 4) = gv;
+        *reinterpret_cast<float4*>(k2swf(sGc, DK + 4, r, c4 * 4)) = gv;
       }
     }
   }
@@ -220,8 +233,9 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       float acc = 0.f;
       float* gout = a.G + (bh * a.Tpad + t0) * DK + c;
       for (int r = 0; r < C; ++r) {
-        acc += sGc[r * (DK + 4) + c];
-        sGc[r * (DK + 4) + c] = acc;
+        float* gp = k2swf(sGc, DK + 4, r, c);
+        acc += *gp;
+        *gp = acc;
         gout[(int64_t)r * DK] = acc;
       }
     }
@@ -234,7 +248,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     const int c = tid % DK, sg = tid / DK;
     float E = 1.f, Pp = 0.f;
     for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-      const float kv = to_f(sK[r * LDK + c]);
+      const float kv = to_f(*k2sw(sK, LDK, r, c));
       E *= sEgp[r];
       Pp = sEgp[r] * Pp + sBp[r] * kv * kv;
     }
@@ -247,9 +261,9 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       const float mu = fast_exp(a.log_a_scale[h]);
       const float A_seg = A;
       for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-        const float kv = to_f(sK[r * LDK + c]);
+        const float kv = to_f(*k2sw(sK, LDK, r, c));
         A = sEgp[r] * A + sBp[r] * kv * kv;
-        sKt[r * LDK + c] = from_f<T>(squash_gain(A, mu, a.lnx) * kv);
+        *k2sw(sKt, LDK, r, c) = from_f<T>(squash_gain(A, mu, a.lnx) * kv);
       }
       if (a.knorm != kKnormNone) {
         // normalisation ablation: kt = B k * f(m), m = k . (B k) per row;
@@ -262,7 +276,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
           const int r = tid >> 2, part = tid & 3;
           float m = 0.f;
           for (int cc = part * PART; cc < (part + 1) * PART; ++cc)
-            m += to_f(sK[r * LDK + cc]) * to_f(sKt[r * LDK + cc]);
+            m += to_f(*k2sw(sK, LDK, r, cc)) * to_f(*k2sw(sKt, LDK, r, cc));
           m += __shfl_xor(m, 1, 64);
           m += __shfl_xor(m, 2, 64);
           if (part == 0) {
@@ -281,18 +295,18 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         __syncthreads();
         A = A_seg;
         for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-          const float kv = to_f(sK[r * LDK + c]);
+          const float kv = to_f(*k2sw(sK, LDK, r, c));
           A = sEgp[r] * A + sBp[r] * kv * kv;
-          sKt[r * LDK + c] = from_f<T>(squash_gain(A, mu, a.lnx) * kv * sNrm[r]);
+          *k2sw(sKt, LDK, r, c) = from_f<T>(squash_gain(A, mu, a.lnx) * kv * sNrm[r]);
         }
       }
     }
     if (PREC == kATQ) {
       // preconditioned query q / (A_r + ridge), A_r including token r
       for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-        const float kv = to_f(sK[r * LDK + c]);
+        const float kv = to_f(*k2sw(sK, LDK, r, c));
         A = sEgp[r] * A + sBp[r] * kv * kv;
-        sQ[r * LDK + c] = from_f<T>(to_f(sQ[r * LDK + c]) / (A + a.ridge));
+        *k2sw(sQ, LDK, r, c) = from_f<T>(to_f(*k2sw(sQ, LDK, r, c)) / (A + a.ridge));
       }
     }
     if (PREC == kDiagSM) {
@@ -303,8 +317,8 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       const float A_seg = A;
       float* sNrm = sY;   // free until the solve
       for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-        const float kv = to_f(sK[r * LDK + c]);
-        sKt[r * LDK + c] = from_f<T>(kv / (A + a.ridge));
+        const float kv = to_f(*k2sw(sK, LDK, r, c));
+        *k2sw(sKt, LDK, r, c) = from_f<T>(kv / (A + a.ridge));
         A = sEgp[r] * A + sBp[r] * kv * kv;
       }
       __syncthreads();
@@ -313,7 +327,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         const int r = tid >> 2, part = tid & 3;
         float sum = 0.f;
         for (int cc = part * PART; cc < (part + 1) * PART; ++cc)
-          sum += to_f(sK[r * LDK + cc]) * to_f(sKt[r * LDK + cc]);
+          sum += to_f(*k2sw(sK, LDK, r, cc)) * to_f(*k2sw(sKt, LDK, r, cc));
         sum += __shfl_xor(sum, 1, 64);
         sum += __shfl_xor(sum, 2, 64);
         if (part == 0) sNrm[r] = 1.f + sum;
@@ -321,8 +335,8 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       __syncthreads();
       A = A_seg;
       for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-        const float kv = to_f(sK[r * LDK + c]);
-        sKt[r * LDK + c] = from_f<T>(kv / ((A + a.ridge) * sNrm[r]));
+        const float kv = to_f(*k2sw(sK, LDK, r, c));
+        *k2sw(sKt, LDK, r, c) = from_f<T>(kv / ((A + a.ridge) * sNrm[r]));
         A = sEgp[r] * A + sBp[r] * kv * kv;
       }
     }
@@ -333,7 +347,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     T* qt = static_cast<T*>(a.Qt) + (bh * a.Tpad + t0) * DK;
     for (int idx = tid; idx < C * VPR; idx += 256) {
       const int r = idx / VPR, cv = idx % VPR;
-      *reinterpret_cast<float4*>(qt + r * DK + cv * VEC) = *reinterpret_cast<const float4*>(sQ + r * LDK + cv * VEC);
+      *reinterpret_cast<float4*>(qt + r * DK + cv * VEC) = *reinterpret_cast<const float4*>(k2sw(sQ, LDK, r, cv * VEC));
     }
   }
 
@@ -350,21 +364,19 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
 #pragma unroll
       for (int kk = 0; kk < DK / 32; ++kk) {
         const int c0 = kk * 32 + 8 * lg;
-        Frag8<T> fk = ld8(sK + r * LDK + c0);
-        Frag8<T> fq = ld8(sQ + r * LDK + c0);
-        Frag8<T> fb = ld8(sKt + t * LDK + c0);
+        Frag8<T> fk = ld8(k2sw(sK, LDK, r, c0));
+        Frag8<T> fq = ld8(k2sw(sQ, LDK, r, c0));
+        Frag8<T> fb = ld8(k2sw(sKt, LDK, t, c0));
         if (GATE == kGateChannel) {
           // reference point: first row of the row block keeps both factors
           // bounded for a non-increasing prefix
-          const float* gr = sGc + r * (DK + 4) + c0;
-          const float* gref = sGc + (16 * w) * (DK + 4) + c0;
-          const float* gt = sGc + t * (DK + 4) + c0;
+          const int rref = 16 * w;
 #pragma unroll
           for (int s = 0; s < 8; ++s) {
-            const float fa = fast_exp(gr[s] - gref[s]);
+            const float fa = fast_exp(*k2swf(sGc, DK + 4, r, c0 + s) - *k2swf(sGc, DK + 4, rref, c0 + s));
             fk.set(s, fk.get(s) * fa);
             fq.set(s, fq.get(s) * fa);
-            fb.set(s, fb.get(s) * fast_exp(gref[s] - gt[s]));
+            fb.set(s, fb.get(s) * fast_exp(*k2swf(sGc, DK + 4, rref, c0 + s) - *k2swf(sGc, DK + 4, t, c0 + s)));
           }
         }
         // linear attention (ATQ): no delta-rule interaction, At = 0, T = Diag(beta)
@@ -406,9 +418,9 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         const int r = r0 + s2;
         float lam = 1.f;
         if (GATE == kGateScalar) lam = fast_exp(sG[r]);
-        if (GATE == kGateChannel) lam = fast_exp(sGc[r * (DK + 4) + c]);
-        fq.set(s2, lam * to_f(sQ[r * LDK + c]));
-        fk.set(s2, -lam * to_f(sK[r * LDK + c]));
+        if (GATE == kGateChannel) lam = fast_exp(*k2swf(sGc, DK + 4, r, c));
+        fq.set(s2, lam * to_f(*k2sw(sQ, LDK, r, c)));
+        fk.set(s2, -lam * to_f(*k2sw(sK, LDK, r, c)));
       }
       st8(QlT + c * C + r0, fq);
       st8(KnT + c * C + r0, fk);
@@ -436,7 +448,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       x[r] = s;
     }
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sX[(16 * w + r) * LDA + 16 * w + col] = x[r];
+    for (int r = 0; r < 16; ++r) *k2swf(sX, LDA, 16 * w + r, 16 * w + col) = x[r];
   }
   __syncthreads();
   // off-diagonal blocks, by distance from the diagonal:
@@ -449,7 +461,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     if (active) {
       for (int kb = 0; kb < 4 * d; ++kb) {
         const float av = sA[(16 * ib + lr) * LDA + 16 * j + 4 * kb + lg];
-        const float bv = sX[(16 * j + 4 * kb + lg) * LDA + 16 * j + lr];
+        const float bv = *k2swf(sX, LDA, 16 * j + 4 * kb + lg, 16 * j + lr);
         mma4(y, av, bv);
       }
 #pragma unroll
@@ -460,12 +472,12 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       floatx4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        const float av = sX[(16 * ib + lr) * LDA + 16 * ib + 4 * kb + lg];
+        const float av = *k2swf(sX, LDA, 16 * ib + lr, 16 * ib + 4 * kb + lg);
         const float bv = Yw[(4 * kb + lg) * 17 + lr];
         mma4(z, av, bv);
       }
 #pragma unroll
-      for (int ii = 0; ii < 4; ++ii) sX[(16 * ib + 4 * lg + ii) * LDA + 16 * j + lr] = -z[ii];
+      for (int ii = 0; ii < 4; ++ii) *k2swf(sX, LDA, 16 * ib + 4 * lg + ii, 16 * j + lr) = -z[ii];
     }
     __syncthreads();
   }
@@ -480,7 +492,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       for (int s = 0; s < 8; ++s) {
         const int t = t0v + s;
         const bool lower = (t >> 4) < (r >> 4) || ((t >> 4) == (r >> 4) && t <= r);
-        f.set(s, lower ? sX[r * LDA + t] * sBeta[t] : 0.f);
+        f.set(s, lower ? *k2swf(sX, LDA, r, t) * sBeta[t] : 0.f);
       }
       st8(Tout + r * C + t0v, f);
     }
@@ -496,7 +508,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         const int t = t0v + s2;
         // M^T[r][t] = M[t][r]; M is lower triangular (block-lower in sX)
         const bool upper = (r >> 4) < (t >> 4) || ((r >> 4) == (t >> 4) && r <= t);
-        ft.set(s2, upper ? sX[t * LDA + r] : 0.f);
+        ft.set(s2, upper ? *k2swf(sX, LDA, t, r) : 0.f);
       }
       st8(MtT + r * C + t0v, ft);
     }
@@ -505,13 +517,13 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     T* Kwr = static_cast<T*>(a.Kw) + (bh * a.Tpad + t0) * DK;
     for (int idx = tid; idx < C * (DK / 8); idx += 256) {
       const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
-      const Frag8<T> fk = ld8(sKt + r * LDK + c0);
+      const Frag8<T> fk = ld8(k2sw(sKt, LDK, r, c0));
       Frag8<T> fw;
       const float wr = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[r]) : 1.f;
 #pragma unroll
       for (int s2 = 0; s2 < 8; ++s2) {
         float f = wr;
-        if (GATE == kGateChannel) f = fast_exp(sGc[(C - 1) * (DK + 4) + c0 + s2] - sGc[r * (DK + 4) + c0 + s2]);
+        if (GATE == kGateChannel) f = fast_exp(*k2swf(sGc, DK + 4, C - 1, c0 + s2) - *k2swf(sGc, DK + 4, r, c0 + s2));
         fw.set(s2, f * fk.get(s2));
       }
       st8(Kr + r * DK + c0, fk);
@@ -527,9 +539,9 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
         const int t = tv + s;
-        float val = to_f(sKt[t * LDK + c]);
+        float val = to_f(*k2sw(sKt, LDK, t, c));
         if (GATE == kGateScalar) val *= fast_exp(sG[C - 1] - sG[t]);
-        if (GATE == kGateChannel) val *= fast_exp(sGc[(C - 1) * (DK + 4) + c] - sGc[t * (DK + 4) + c]);
+        if (GATE == kGateChannel) val *= fast_exp(*k2swf(sGc, DK + 4, C - 1, c) - *k2swf(sGc, DK + 4, t, c));
         f.set(s, val);
       }
       st8(Kout + c * C + tv, f);
