@@ -341,20 +341,6 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
 }
 
 // ------------------------------------------------------------ p1
-// rows [C][DD] of src -> dst[DD][C + 8] (transposed; read back through sw())
-template <typename T, int DD>
-__device__ __forceinline__ void load_rows_t(T* dst, const T* src, int64_t lds, int nvalid, int tid) {
-  constexpr int VEC = 16 / sizeof(T), VPR = DD / VEC, LDT = C + 8;
-  for (int idx = tid; idx < C * VPR; idx += 256) {
-    const int r = idx / VPR, cv = idx % VPR;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < nvalid) v = *reinterpret_cast<const float4*>(src + r * lds + cv * VEC);
-    const T* e = reinterpret_cast<const T*>(&v);
-#pragma unroll
-    for (int s2 = 0; s2 < VEC; ++s2) *sw(dst, LDT, cv * VEC + s2, r) = e[s2];
-  }
-}
-
 // Rows [C][DD] of a workspace tensor -> LDS rows [C][DD + 8] (16-byte copies,
 // bank-spread addressing: read back through sw())
 template <typename T, int DD>
@@ -364,6 +350,51 @@ __device__ __forceinline__ void stage_rows(T* dst, const T* src, int tid) {
     const int r = idx / VPR, cv = idx % VPR;
     *reinterpret_cast<float4*>(sw(dst, LD, r, cv * VEC)) = *reinterpret_cast<const float4*>(src + r * DD + cv * VEC);
   }
+}
+
+// Two adjacent HC-column groups of rows [C][.] at once, so each row segment
+// read is a whole 128-byte line: the first group goes to dst[HC][C + 8]
+// (transposed) now, the second comes back in `held` for the next pass.
+// (Named registers, not an array: a private array here is moved to LDS.)
+template <typename T, int HC>
+struct HeldTile {
+  static constexpr int kVec = 16 / static_cast<int>(sizeof(T)), kVpr = HC / kVec;
+  static constexpr int kPer = C * kVpr / 256;
+  static_assert(C * kVpr % 256 == 0 && (kPer == 1 || kPer == 2), "one or two vectors per thread");
+  float4 v0, v1;
+};
+template <typename T, int HC>
+__device__ __forceinline__ void tile_t_put(T* dst, float4 x, int j, int tid) {
+  using HT = HeldTile<T, HC>;
+  constexpr int LDT = C + 8;
+  const int idx = tid + 256 * j, r = idx / HT::kVpr, cv = idx % HT::kVpr;
+  const T* e = reinterpret_cast<const T*>(&x);
+#pragma unroll
+  for (int s2 = 0; s2 < HT::kVec; ++s2) *sw(dst, LDT, cv * HT::kVec + s2, r) = e[s2];
+}
+template <typename T, int HC>
+__device__ __forceinline__ void tile_t_store(T* dst, const HeldTile<T, HC>& held, int tid) {
+  tile_t_put<T, HC>(dst, held.v0, 0, tid);
+  if constexpr (HeldTile<T, HC>::kPer == 2) tile_t_put<T, HC>(dst, held.v1, 1, tid);
+}
+template <typename T, int HC>
+__device__ __forceinline__ void load_pair_t(T* dst, HeldTile<T, HC>& held, const T* src, int64_t lds,
+                                            int nvalid, int tid) {
+  using HT = HeldTile<T, HC>;
+  auto get = [&](int j, float4& now, float4& hold) {
+    const int idx = tid + 256 * j, r = idx / HT::kVpr, cv = idx % HT::kVpr;
+    now = make_float4(0.f, 0.f, 0.f, 0.f);
+    hold = now;
+    if (r < nvalid) {
+      now = *reinterpret_cast<const float4*>(src + r * lds + cv * HT::kVec);
+      hold = *reinterpret_cast<const float4*>(src + r * lds + HC + cv * HT::kVec);
+    }
+  };
+  float4 n0, n1;
+  get(0, n0, held.v0);
+  if constexpr (HT::kPer == 2) get(1, n1, held.v1);
+  tile_t_put<T, HC>(dst, n0, 0, tid);
+  if constexpr (HT::kPer == 2) tile_t_put<T, HC>(dst, n1, 1, tid);
 }
 
 // ------------------------------------------------------------ p12
@@ -594,6 +625,8 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   T* dq = static_cast<T*>(ba.dq) + (b * a.T + t0) * HD + h * DK;
   T* dKm = static_cast<T*>(ba.dKm) + rk;
   T* dKt = static_cast<T*>(ba.dKt) + rk;
+  static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
+  HeldTile<T, HC> hKt, hQ, hK;
 #pragma unroll 1
   for (int p = 0; p < NPASS; ++p) {
     const int c0 = p * HC;
@@ -610,9 +643,17 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
             *reinterpret_cast<const float4*>(dHs + c * DV + cv * VEC);
       }
     }
-    load_rows_t<T, HC>(sKtT, static_cast<const T*>(a.Ktr) + rk + c0, DK, C, tid);
-    load_rows_t<T, HC>(sQT, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
-    load_rows_t<T, HC>(sKT, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
+    // transposed Kt, Q, K tiles: even passes read two column groups (whole
+    // lines) and keep the second for the odd pass
+    if ((p & 1) == 0) {
+      load_pair_t<T, HC>(sKtT, hKt, static_cast<const T*>(a.Ktr) + rk + c0, DK, C, tid);
+      load_pair_t<T, HC>(sQT, hQ, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
+      load_pair_t<T, HC>(sKT, hK, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
+    } else {
+      tile_t_store<T, HC>(sKtT, hKt, tid);
+      tile_t_store<T, HC>(sQT, hQ, tid);
+      tile_t_store<T, HC>(sKT, hK, tid);
+    }
     __syncthreads();
     // sum(dS' o S) over this pass's rows
     for (int idx = tid; idx < HC * DV; idx += 256) {
@@ -879,6 +920,8 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
   T* dKm = static_cast<T*>(ba.dKm) + rk;
   T* dKt = static_cast<T*>(ba.dKt) + rk;
   const float* Gc = a.G + rk;   // in-chunk log-decay prefix rows [t][c]
+  static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
+  HeldTile<T, HC> hKt, hQ, hK;
 #pragma unroll 1
   for (int p = 0; p < NPASS; ++p) {
     const int c0 = p * HC;
@@ -903,9 +946,15 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
         sGT[(c4 + 3) * LDG + t] = gv.w;
       }
     }
-    load_rows_t<T, HC>(sKtT, static_cast<const T*>(a.Ktr) + rk + c0, DK, C, tid);
-    load_rows_t<T, HC>(sQT, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
-    load_rows_t<T, HC>(sKT, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
+    if ((p & 1) == 0) {
+      load_pair_t<T, HC>(sKtT, hKt, static_cast<const T*>(a.Ktr) + rk + c0, DK, C, tid);
+      load_pair_t<T, HC>(sQT, hQ, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
+      load_pair_t<T, HC>(sKT, hK, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
+    } else {
+      tile_t_store<T, HC>(sKtT, hKt, tid);
+      tile_t_store<T, HC>(sQT, hQ, tid);
+      tile_t_store<T, HC>(sKT, hK, tid);
+    }
     __syncthreads();
     {
       // sum_v S dS' per channel of the pass: 8 lanes per channel
