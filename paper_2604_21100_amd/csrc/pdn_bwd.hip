@@ -1101,15 +1101,35 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
 // chains the chunks (adjoint entering each chunk from the right), and
 // pc_chunk<true> recomputes with the carry and writes dk, dbetaP, dgP and the
 // partial d mu.
-// Sum of each of 16 per-row values over the 64 lanes of a wave (butterfly:
-// every lane ends with all 16 totals).  Static indices only: a per-lane
+// Sum of each of 16 per-row values over the 64 lanes of a wave; lane l
+// returns the total of value l >> 2.  Static indices only: a per-lane
 // choice between array elements gets merged into a runtime index by the
 // compiler, which then lowers it to compare / select chains.
-__device__ __forceinline__ void pc_wave_sum16(float (&v)[16]) {
+__device__ __forceinline__ float pc_wave_sum16(const float (&v)[16], int l) {
+  // reduce-scatter: each of the lane bits 5..2 halves the values a lane
+  // keeps (the half named by the bit), bits 1, 0 finish the sum, so lane l
+  // ends with the total of value l >> 2
+  float u[8];
+  const bool b5 = l & 32, b4 = l & 16, b3 = l & 8, b2 = l & 4;
 #pragma unroll
-  for (int off = 1; off < 64; off <<= 1)
+  for (int k = 0; k < 8; ++k) {
+    const float keep = b5 ? v[k + 8] : v[k], send = b5 ? v[k] : v[k + 8];
+    u[k] = keep + __shfl_xor(send, 32, 64);
+  }
 #pragma unroll
-    for (int j = 0; j < 16; ++j) v[j] += __shfl_xor(v[j], off, 64);
+  for (int k = 0; k < 4; ++k) {
+    const float keep = b4 ? u[k + 4] : u[k], send = b4 ? u[k] : u[k + 4];
+    u[k] = keep + __shfl_xor(send, 16, 64);
+  }
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const float keep = b3 ? u[k + 2] : u[k], send = b3 ? u[k] : u[k + 2];
+    u[k] = keep + __shfl_xor(send, 8, 64);
+  }
+  float x = (b2 ? u[1] : u[0]) + __shfl_xor(b2 ? u[0] : u[1], 4, 64);
+  x += __shfl_xor(x, 2, 64);
+  x += __shfl_xor(x, 1, 64);
+  return x;
 }
 
 // One block per (b, h, chunk), one wave per segment of G = 16 tokens; lane l
@@ -1127,7 +1147,7 @@ __device__ __forceinline__ void pc_wave_sum16(float (&v)[16]) {
 // kappa the adjoint entering it from the right, already times aP of the
 // next token).  The per-token products come from the in-chunk prefix of gP.
 // Loop bodies are branch-free.
-constexpr int PCG = 16;   // tokens per segment
+constexpr int PCG = 16;   // tokens per segment (one wave sum of 16 values)
 constexpr int PCS = C / PCG;
 
 template <typename T, int N>
@@ -1225,7 +1245,7 @@ __global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
   }
   // ---- reverse: local adjoint from zero; the gain terms need no D
   const float mu = fast_exp(a.log_a_scale[h]);
-  const float lnx = a.lnx;
+  const float lnx = a.lnx, nlx2 = -lnx * kLog2e;
   float Dh[CPL][PCG];
   float muPart = 0.f, send[CPL];
 #pragma unroll
@@ -1240,7 +1260,7 @@ __global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
       const bool pos = Ar > 0.f;
       const float rr = fast_log(fmaxf(Ar, 1e-30f)) - mu;
       const float qd = fast_rcp(1.f + fabsf(rr));
-      const float Bv = fast_exp(-lnx * (pos ? rr * qd : -1.f));
+      const float Bv = exp2_hw(nlx2 * (pos ? rr * qd : -1.f));
       const float dr = pos ? -lnx * Bv * gk * to_f(kr[j].x[q]) * qd * qd : 0.f;
       D = dr * fast_rcp(fmaxf(Ar, 1e-30f)) + aNext * D;
       aNext = sEgp[s0 + j];
@@ -1289,22 +1309,20 @@ __global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
     }
     if (s0 + j < n) *reinterpret_cast<Pk*>(dko + (s0 + j) * kst) = o;
   }
-  const int64_t sidx = (b * a.T + t0 + s0 + min(l, PCG - 1)) * a.H + h;
-  const bool tok = l < PCG && s0 + l < n;
-  pc_wave_sum16(sr);
-#pragma unroll
-  for (int j = 0; j < PCG; ++j)
-    if (l == j && tok && ba.dbeta_p) ba.dbeta_p[sidx] = sr[j];
+  // lane 4 j carries token s0 + j's sums
+  const int jl = l >> 2;
+  const int64_t sidx = (b * a.T + t0 + s0 + jl) * a.H + h;
+  const bool tok = (l & 3) == 0 && s0 + jl < n;
+  const float sb = pc_wave_sum16(sr, l);
+  if (tok && ba.dbeta_p) ba.dbeta_p[sidx] = sb;
 #pragma unroll
   for (int j = 0; j < PCG; ++j) {
     sr[j] = 0.f;
 #pragma unroll
     for (int q = 0; q < CPL; ++q) sr[j] += Dh[q][j] * (j > 0 ? A[q][j - 1] : A_in[q]);
   }
-  pc_wave_sum16(sr);
-#pragma unroll
-  for (int j = 0; j < PCG; ++j)
-    if (l == j && tok && ba.dg_p) ba.dg_p[sidx] = sEgp[s0 + j] * sr[j];
+  const float sg = pc_wave_sum16(sr, l);
+  if (tok && ba.dg_p) ba.dg_p[sidx] = sEgp[s0 + jl] * sg;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) muPart += __shfl_xor(muPart, off, 64);
   if (l == 0) sMu[w] = muPart;

@@ -166,8 +166,16 @@ __device__ __forceinline__ void st_tile_t(T* out, int ld, const floatx4& acc, in
   st4<T>(out + lr * ld + 4 * lg, scale * acc[0], scale * acc[1], scale * acc[2], scale * acc[3]);
 }
 
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kLog2e = 1.4426950408889634f;
 __device__ __forceinline__ float fast_exp(float x) { return __expf(x); }
-__device__ __forceinline__ float fast_log(float x) { return __logf(x); }
+// 2^x on the hardware exponential (a result below the normal range flushes
+// to zero)
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+// natural log on the hardware base-2 logarithm: ln x = ln 2 * log2 x.  x must
+// be a positive normal number (callers clamp); denormal inputs are not
+// rescaled.
+__device__ __forceinline__ float fast_log(float x) { return kLn2 * __builtin_amdgcn_logf(x); }
 // hardware reciprocal (1 ulp)
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
@@ -177,7 +185,7 @@ __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcp
 __device__ __forceinline__ float squash_gain(float A, float mu, float lnx) {
   const float r = fast_log(fmaxf(A, 1e-30f)) - mu;
   const float s = A > 0.f ? r * fast_rcp(1.f + fabsf(r)) : -1.f;
-  return fast_exp(-lnx * s);
+  return exp2_hw((-lnx * kLog2e) * s);
 }
 
 }  // namespace pdn
