@@ -1172,20 +1172,23 @@ __global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
   const int s0 = PCG * w, c0 = CPL * l;
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
-  const int64_t kst = a.H * static_cast<int64_t>(DK);
-  const T* krow = static_cast<const T*>(a.k) + ((b * a.T + t0) * a.H + h) * DK + c0;
-  const T* grow = static_cast<const T*>(ba.dKt) + (bh * a.Tpad + t0) * DK + c0;
-  const T* mrow = static_cast<const T*>(ba.dKm) + (bh * a.Tpad + t0) * DK + c0;
+  // row bases are wave-uniform; a lane adds a 32-bit byte offset
+  constexpr uint32_t E = sizeof(T);
+  const uint32_t kstb = static_cast<uint32_t>(a.H * DK) * E, lo = static_cast<uint32_t>(c0) * E;
+  const T* kb = static_cast<const T*>(a.k) + ((b * a.T + t0) * a.H + h) * DK;
+  const T* gb = static_cast<const T*>(ba.dKt) + (bh * a.Tpad + t0) * DK;
+  const T* mb = static_cast<const T*>(ba.dKm) + (bh * a.Tpad + t0) * DK;
   // every row of the segment in flight first; rows past the sequence end
   // re-read the last row (keys are zeroed at use, dkt and dkm rows there are
   // zero)
   Pk kr[PCG], gr[PCG], mr[FINAL ? PCG : 1];
 #pragma unroll
   for (int j = 0; j < PCG; ++j) {
-    const int rr = min(s0 + j, n - 1);
-    kr[j] = *reinterpret_cast<const Pk*>(krow + rr * kst);
-    gr[j] = *reinterpret_cast<const Pk*>(grow + (s0 + j) * DK);
-    if (FINAL) mr[j] = *reinterpret_cast<const Pk*>(mrow + (s0 + j) * DK);
+    const uint32_t rr = static_cast<uint32_t>(min(s0 + j, n - 1));
+    const uint32_t ow = static_cast<uint32_t>((s0 + j) * DK) * E + lo;
+    kr[j] = *reinterpret_cast<const Pk*>(at_bytes(kb, rr * kstb + lo));
+    gr[j] = *reinterpret_cast<const Pk*>(at_bytes(gb, ow));
+    if (FINAL) mr[j] = *reinterpret_cast<const Pk*>(at_bytes(mb, ow));
   }
   float A_start[CPL], kap_chunk[CPL];
 #pragma unroll
@@ -1243,9 +1246,12 @@ __global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
 #pragma unroll
     for (int j = 0; j < PCG; ++j) A[q][j] += sFf[s0 + j] * x;
   }
-  // ---- reverse: local adjoint from zero; the gain terms need no D
+  // ---- reverse: local adjoint from zero; the gain terms need no D.  The
+  // adjoint is carried divided by -log x (every injection has that factor
+  // and the recurrence is linear), here, in the chunk summaries and in the
+  // carries; it is applied where values leave: dk, dbetaP, dgP, d mu, dA0.
   const float mu = fast_exp(a.log_a_scale[h]);
-  const float lnx = a.lnx, nlx2 = -lnx * kLog2e;
+  const float nlx = -a.lnx, nlx2 = nlx * kLog2e;
   float Dh[CPL][PCG];
   float muPart = 0.f, send[CPL];
 #pragma unroll
@@ -1261,13 +1267,14 @@ __global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
       const float rr = fast_log(fmaxf(Ar, 1e-30f)) - mu;
       const float qd = fast_rcp(1.f + fabsf(rr));
       const float Bv = exp2_hw(nlx2 * (pos ? rr * qd : -1.f));
-      const float dr = pos ? -lnx * Bv * gk * to_f(kr[j].x[q]) * qd * qd : 0.f;
+      const float bg = Bv * gk;
+      const float dr = pos ? bg * to_f(kr[j].x[q]) * qd * qd : 0.f;   // / (-lnx)
       D = dr * fast_rcp(fmaxf(Ar, 1e-30f)) + aNext * D;
       aNext = sEgp[s0 + j];
       Dh[q][j] = D;
       if (FINAL) {   // dk's terms without D, in place of dKm
         muPart -= dr;
-        mr[j].x[q] = from_f<T>(to_f(mr[j].x[q]) + Bv * gk);
+        mr[j].x[q] = from_f<T>(to_f(mr[j].x[q]) + bg);
       }
     }
     send[q] = aNext * D;   // aP_{s0} Dhat_{s0}: what this segment sends left
@@ -1294,27 +1301,28 @@ __global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
   // ---- outputs: dk = dKm + B dkt + 2 bP k D; per token the sums over
   // channels of D k^2 and D A_{r-1}
   float sr[PCG];
-  T* dko = static_cast<T*>(ba.dk) + ((b * a.T + t0) * a.H + h) * DK + c0;
+  T* dkb = static_cast<T*>(ba.dk) + ((b * a.T + t0) * a.H + h) * DK;
 #pragma unroll
   for (int j = 0; j < PCG; ++j) {
     Pk o;
     sr[j] = 0.f;
+    const float f2 = 2.f * nlx * sBp[s0 + j];
 #pragma unroll
     for (int q = 0; q < CPL; ++q) {
       const float kv = to_f(kr[j].x[q]);
-      const float D = Dh[q][j] + sBf[s0 + j] * kap[q];
-      o.x[q] = from_f<T>(to_f(mr[j].x[q]) + 2.f * sBp[s0 + j] * kv * D);
+      const float D = Dh[q][j] + sBf[s0 + j] * kap[q];   // / (-lnx)
+      o.x[q] = from_f<T>(to_f(mr[j].x[q]) + f2 * kv * D);
       sr[j] += D * kv * kv;
       Dh[q][j] = D;
     }
-    if (s0 + j < n) *reinterpret_cast<Pk*>(dko + (s0 + j) * kst) = o;
+    if (s0 + j < n) *reinterpret_cast<Pk*>(at_bytes(dkb, static_cast<uint32_t>(s0 + j) * kstb + lo)) = o;
   }
   // lane 4 j carries token s0 + j's sums
   const int jl = l >> 2;
   const int64_t sidx = (b * a.T + t0 + s0 + jl) * a.H + h;
   const bool tok = (l & 3) == 0 && s0 + jl < n;
   const float sb = pc_wave_sum16(sr, l);
-  if (tok && ba.dbeta_p) ba.dbeta_p[sidx] = sb;
+  if (tok && ba.dbeta_p) ba.dbeta_p[sidx] = nlx * sb;
 #pragma unroll
   for (int j = 0; j < PCG; ++j) {
     sr[j] = 0.f;
@@ -1322,7 +1330,7 @@ __global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
     for (int q = 0; q < CPL; ++q) sr[j] += Dh[q][j] * (j > 0 ? A[q][j - 1] : A_in[q]);
   }
   const float sg = pc_wave_sum16(sr, l);
-  if (tok && ba.dg_p) ba.dg_p[sidx] = sEgp[s0 + jl] * sg;
+  if (tok && ba.dg_p) ba.dg_p[sidx] = nlx * sEgp[s0 + jl] * sg;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) muPart += __shfl_xor(muPart, off, 64);
   if (l == 0) sMu[w] = muPart;
@@ -1331,11 +1339,12 @@ __global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
     float m = 0.f;
 #pragma unroll
     for (int s = 0; s < PCS; ++s) m += sMu[s];
-    ba.pcMu[bh * a.NT + i] = m;
+    ba.pcMu[bh * a.NT + i] = nlx * m;
   }
 }
 
-// carry_{i-1} = L_i + exp(sumD_i) carry_i, from the last chunk (carry 0)
+// carry_{i-1} = L_i + exp(sumD_i) carry_i, from the last chunk (carry 0);
+// summaries and carries are adjoints divided by -log x, as in pc_chunk
 template <int DK>
 __global__ __launch_bounds__(DK) void pc_carry(BwdArgs ba) {
   const FwdArgs& a = ba.f;
@@ -1362,7 +1371,7 @@ __global__ __launch_bounds__(DK) void pc_carry(BwdArgs ba) {
     out[(int64_t)(i + 1) * DK] = carry;
     carry = L[(int64_t)i * DK] + fast_exp(D[i]) * carry;
   }
-  if (ba.dA0) ba.dA0[bh * DK + c] = carry;
+  if (ba.dA0) ba.dA0[bh * DK + c] = -a.lnx * carry;   // carries are kept divided by -log x
 }
 
 // d logAScale_h = mu_h * sum over batches and chunks of the partial d mu
