@@ -397,6 +397,36 @@ __device__ __forceinline__ void load_pair_t(T* dst, HeldTile<T, HC>& held, const
   if constexpr (HT::kPer == 2) tile_t_put<T, HC>(dst, n1, 1, tid);
 }
 
+// One phase-B pass's rows of the chunk-start state S^T and of its adjoint
+// ([HC][DV] each), loaded a pass ahead into named registers and written to
+// LDS ([HC][DV + 8], bank-spread) when the pass starts.
+template <typename T, int HC, int DV>
+struct StateRows {
+  static constexpr int kVec = 16 / static_cast<int>(sizeof(T)), kVpr = DV / kVec;
+  static constexpr int kPer = HC * kVpr / 256;
+  static_assert(HC * kVpr % 256 == 0 && (kPer == 1 || kPer == 2), "one or two vectors per thread");
+  float4 h0, h1, d0, d1;
+  __device__ __forceinline__ void load(const T* Hs, const T* dHs, int tid) {
+    auto get = [&](int j, float4& h, float4& d) {
+      const int idx = tid + 256 * j, c = idx / kVpr, cv = idx % kVpr;
+      h = *reinterpret_cast<const float4*>(Hs + c * DV + cv * kVec);
+      d = *reinterpret_cast<const float4*>(dHs + c * DV + cv * kVec);
+    };
+    get(0, h0, d0);
+    if constexpr (kPer == 2) get(1, h1, d1);
+  }
+  __device__ __forceinline__ void store(T* sS, T* sdS, int tid) const {
+    constexpr int LDV = DV + 8;
+    auto put = [&](int j, float4 h, float4 d) {
+      const int idx = tid + 256 * j, c = idx / kVpr, cv = idx % kVpr;
+      *reinterpret_cast<float4*>(sw(sS, LDV, c, cv * kVec)) = h;
+      *reinterpret_cast<float4*>(sw(sdS, LDV, c, cv * kVec)) = d;
+    };
+    put(0, h0, d0);
+    if constexpr (kPer == 2) put(1, h1, d1);
+  }
+};
+
 // ------------------------------------------------------------ p12
 // Per chunk, every gradient after the reverse scan except the
 // preconditioner's, in one pass over the chunk's rows:
@@ -591,6 +621,9 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       }
     }
   }
+  // phase B's first state rows: in flight through the rest of phase A
+  StateRows<T, HC, DV> srows;
+  srows.load(static_cast<const T*>(a.Hs) + cs, static_cast<const T*>(ba.dHs) + cs, tid);
   // E rows of this wave (phase B's A operand of A3), from the staged copy
 #pragma unroll
   for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, ra, 32 * kk + 8 * lg));
@@ -631,18 +664,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   for (int p = 0; p < NPASS; ++p) {
     const int c0 = p * HC;
     __syncthreads();   // phase A (or the previous pass) is done with the LDS
-    {
-      constexpr int VEC = 16 / sizeof(T), VPR = DV / VEC;
-      const T* Hs = static_cast<const T*>(a.Hs) + cs + c0 * DV;
-      const T* dHs = static_cast<const T*>(ba.dHs) + cs + c0 * DV;
-      for (int idx = tid; idx < HC * VPR; idx += 256) {
-        const int c = idx / VPR, cv = idx % VPR;
-        *reinterpret_cast<float4*>(sw(sS, LDV, c, cv * VEC)) =
-            *reinterpret_cast<const float4*>(Hs + c * DV + cv * VEC);
-        *reinterpret_cast<float4*>(sw(sdS, LDV, c, cv * VEC)) =
-            *reinterpret_cast<const float4*>(dHs + c * DV + cv * VEC);
-      }
-    }
+    srows.store(sS, sdS, tid);
     // transposed Kt, Q, K tiles: even passes read two column groups (whole
     // lines) and keep the second for the odd pass
     if ((p & 1) == 0) {
@@ -655,6 +677,12 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       tile_t_store<T, HC>(sKT, hK, tid);
     }
     __syncthreads();
+    {
+      // the next pass's state rows load during this pass (the last pass
+      // reloads its own rows, unused)
+      const int cn = min(p + 1, NPASS - 1) * HC;
+      srows.load(static_cast<const T*>(a.Hs) + cs + cn * DV, static_cast<const T*>(ba.dHs) + cs + cn * DV, tid);
+    }
     // sum(dS' o S) over this pass's rows
     for (int idx = tid; idx < HC * DV; idx += 256) {
       const int c = idx / DV, v = idx % DV;
@@ -898,6 +926,9 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
     st4<T>(sw(sSqT, LDT, 16 * j + lr, 16 * w + 4 * lg), dq[0], dq[1], dq[2], dq[3]);
     st4<T>(sw(sSkT, LDT, 16 * j + lr, 16 * w + 4 * lg), dAb[0], dAb[1], dAb[2], dAb[3]);
   }
+  // phase B's first state rows: in flight through the rest of phase A
+  StateRows<T, HC, DV> srows;
+  srows.load(static_cast<const T*>(a.Hs) + cs, static_cast<const T*>(ba.dHs) + cs, tid);
 #pragma unroll
   for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, ra, 32 * kk + 8 * lg));
   __syncthreads();
@@ -926,17 +957,8 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
   for (int p = 0; p < NPASS; ++p) {
     const int c0 = p * HC;
     __syncthreads();   // phase A (or the previous pass) is done with the LDS
+    srows.store(sS, sdS, tid);
     {
-      constexpr int VEC = 16 / sizeof(T), VPR = DV / VEC;
-      const T* Hs = static_cast<const T*>(a.Hs) + cs + c0 * DV;
-      const T* dHs = static_cast<const T*>(ba.dHs) + cs + c0 * DV;
-      for (int idx = tid; idx < HC * VPR; idx += 256) {
-        const int c = idx / VPR, cv = idx % VPR;
-        *reinterpret_cast<float4*>(sw(sS, LDV, c, cv * VEC)) =
-            *reinterpret_cast<const float4*>(Hs + c * DV + cv * VEC);
-        *reinterpret_cast<float4*>(sw(sdS, LDV, c, cv * VEC)) =
-            *reinterpret_cast<const float4*>(dHs + c * DV + cv * VEC);
-      }
       for (int idx = tid; idx < C * (HC / 4); idx += 256) {
         const int t = idx / (HC / 4), c4 = (idx % (HC / 4)) * 4;
         const float4 gv = *reinterpret_cast<const float4*>(Gc + t * DK + c0 + c4);
@@ -956,6 +978,12 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
       tile_t_store<T, HC>(sKT, hK, tid);
     }
     __syncthreads();
+    {
+      // the next pass's state rows load during this pass (the last pass
+      // reloads its own rows, unused)
+      const int cn = min(p + 1, NPASS - 1) * HC;
+      srows.load(static_cast<const T*>(a.Hs) + cs + cn * DV, static_cast<const T*>(ba.dHs) + cs + cn * DV, tid);
+    }
     {
       // sum_v S dS' per channel of the pass: 8 lanes per channel
       const int c = tid >> 3, part = tid & 7;
