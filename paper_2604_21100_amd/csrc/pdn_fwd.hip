@@ -134,7 +134,7 @@ struct K2Smem {
   static constexpr size_t kR3 = kRow;                               // sKt
   static constexpr size_t kGc = GATE == kGateChannel ? sizeof(float) * C * (DK + 4) : 0;
   static constexpr size_t kY = sizeof(float) * 4 * 16 * 17;
-  static constexpr size_t kScal = sizeof(float) * 5 * C;
+  static constexpr size_t kScal = sizeof(float) * 7 * C;
   static constexpr size_t kSeg = sizeof(float) * 2 * 256;   // preconditioner segment carries
   static constexpr size_t kTotal = kR1 + kR2 + kR3 + kGc + kY + kScal + kSeg;
 };
@@ -159,7 +159,9 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   float* sEgp = sBp + C;
   float* sG = sEgp + C;
   float* sGraw = sG + C;
-  float* sSegE = sGraw + C;
+  float* sLam = sGraw + C;   // scalar gate: exp(G_r)
+  float* sWt = sLam + C;     // scalar gate: exp(G_{C-1} - G_r)
+  float* sSegE = sWt + C;
   float* sSegP = sSegE + 256;
 
   const int64_t blk = blockIdx.x;
@@ -226,6 +228,8 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     }
     sG[l] = x;
     a.G[bh * a.Tpad + t0 + l] = x;
+    sLam[l] = fast_exp(x);
+    sWt[l] = fast_exp(__shfl(x, C - 1, 64) - x);
   }
   if (tid < DK) {
     const int c = tid;
@@ -245,12 +249,25 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     // pass 1 reduces each segment to (prod a, partial sum), the segments are
     // chained from the chunk-start state, pass 2 re-walks its rows
     constexpr int NSEG = 256 / DK, SEG = C / NSEG;
-    const int c = tid % DK, sg = tid / DK;
+    static_assert(SEG % 4 == 0, "segment rows come in float4 groups");
+    const int c = tid % DK, sg = tid / DK, r0 = sg * SEG;
+    // this thread's key column over its segment and the rows' decay and
+    // betaP, in registers for every walk below
+    float kreg[SEG], eg[SEG], bpr[SEG];
+#pragma unroll
+    for (int j = 0; j < SEG; ++j) kreg[j] = to_f(*k2sw(sK, LDK, r0 + j, c));
+#pragma unroll
+    for (int j = 0; j < SEG; j += 4) {
+      const float4 e4 = *reinterpret_cast<const float4*>(sEgp + r0 + j);
+      const float4 b4 = *reinterpret_cast<const float4*>(sBp + r0 + j);
+      eg[j] = e4.x; eg[j + 1] = e4.y; eg[j + 2] = e4.z; eg[j + 3] = e4.w;
+      bpr[j] = b4.x; bpr[j + 1] = b4.y; bpr[j + 2] = b4.z; bpr[j + 3] = b4.w;
+    }
     float E = 1.f, Pp = 0.f;
-    for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-      const float kv = to_f(*k2sw(sK, LDK, r, c));
-      E *= sEgp[r];
-      Pp = sEgp[r] * Pp + sBp[r] * kv * kv;
+#pragma unroll
+    for (int j = 0; j < SEG; ++j) {
+      E *= eg[j];
+      Pp = eg[j] * Pp + bpr[j] * kreg[j] * kreg[j];
     }
     sSegE[sg * DK + c] = E;
     sSegP[sg * DK + c] = Pp;
@@ -260,10 +277,11 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     if (PREC == kSquash) {
       const float mu = fast_exp(a.log_a_scale[h]);
       const float A_seg = A;
-      for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-        const float kv = to_f(*k2sw(sK, LDK, r, c));
-        A = sEgp[r] * A + sBp[r] * kv * kv;
-        *k2sw(sKt, LDK, r, c) = from_f<T>(squash_gain(A, mu, a.lnx) * kv);
+#pragma unroll
+      for (int j = 0; j < SEG; ++j) {
+        const float kv = kreg[j];
+        A = eg[j] * A + bpr[j] * kv * kv;
+        *k2sw(sKt, LDK, r0 + j, c) = from_f<T>(squash_gain(A, mu, a.lnx) * kv);
       }
       if (a.knorm != kKnormNone) {
         // normalisation ablation: kt = B k * f(m), m = k . (B k) per row;
@@ -294,19 +312,21 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         }
         __syncthreads();
         A = A_seg;
-        for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-          const float kv = to_f(*k2sw(sK, LDK, r, c));
-          A = sEgp[r] * A + sBp[r] * kv * kv;
-          *k2sw(sKt, LDK, r, c) = from_f<T>(squash_gain(A, mu, a.lnx) * kv * sNrm[r]);
+#pragma unroll
+        for (int j = 0; j < SEG; ++j) {
+          const float kv = kreg[j];
+          A = eg[j] * A + bpr[j] * kv * kv;
+          *k2sw(sKt, LDK, r0 + j, c) = from_f<T>(squash_gain(A, mu, a.lnx) * kv * sNrm[r0 + j]);
         }
       }
     }
     if (PREC == kATQ) {
       // preconditioned query q / (A_r + ridge), A_r including token r
-      for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-        const float kv = to_f(*k2sw(sK, LDK, r, c));
-        A = sEgp[r] * A + sBp[r] * kv * kv;
-        *k2sw(sQ, LDK, r, c) = from_f<T>(to_f(*k2sw(sQ, LDK, r, c)) / (A + a.ridge));
+#pragma unroll
+      for (int j = 0; j < SEG; ++j) {
+        const float kv = kreg[j];
+        A = eg[j] * A + bpr[j] * kv * kv;
+        *k2sw(sQ, LDK, r0 + j, c) = from_f<T>(to_f(*k2sw(sQ, LDK, r0 + j, c)) / (A + a.ridge));
       }
     }
     if (PREC == kDiagSM) {
@@ -316,10 +336,11 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       // for them and again for the exactly recomputed, normalised key
       const float A_seg = A;
       float* sNrm = sY;   // free until the solve
-      for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-        const float kv = to_f(*k2sw(sK, LDK, r, c));
-        *k2sw(sKt, LDK, r, c) = from_f<T>(kv / (A + a.ridge));
-        A = sEgp[r] * A + sBp[r] * kv * kv;
+#pragma unroll
+      for (int j = 0; j < SEG; ++j) {
+        const float kv = kreg[j];
+        *k2sw(sKt, LDK, r0 + j, c) = from_f<T>(kv / (A + a.ridge));
+        A = eg[j] * A + bpr[j] * kv * kv;
       }
       __syncthreads();
       {
@@ -334,10 +355,11 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       }
       __syncthreads();
       A = A_seg;
-      for (int r = sg * SEG; r < (sg + 1) * SEG; ++r) {
-        const float kv = to_f(*k2sw(sK, LDK, r, c));
-        *k2sw(sKt, LDK, r, c) = from_f<T>(kv / ((A + a.ridge) * sNrm[r]));
-        A = sEgp[r] * A + sBp[r] * kv * kv;
+#pragma unroll
+      for (int j = 0; j < SEG; ++j) {
+        const float kv = kreg[j];
+        *k2sw(sKt, LDK, r0 + j, c) = from_f<T>(kv / ((A + a.ridge) * sNrm[r0 + j]));
+        A = eg[j] * A + bpr[j] * kv * kv;
       }
     }
   }
@@ -417,7 +439,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       for (int s2 = 0; s2 < 8; ++s2) {
         const int r = r0 + s2;
         float lam = 1.f;
-        if (GATE == kGateScalar) lam = fast_exp(sG[r]);
+        if (GATE == kGateScalar) lam = sLam[r];
         if (GATE == kGateChannel) lam = fast_exp(*k2swf(sGc, DK + 4, r, c));
         fq.set(s2, lam * to_f(*k2sw(sQ, LDK, r, c)));
         fk.set(s2, -lam * to_f(*k2sw(sK, LDK, r, c)));
@@ -519,7 +541,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
       const Frag8<T> fk = ld8(k2sw(sKt, LDK, r, c0));
       Frag8<T> fw;
-      const float wr = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[r]) : 1.f;
+      const float wr = GATE == kGateScalar ? sWt[r] : 1.f;
 #pragma unroll
       for (int s2 = 0; s2 < 8; ++s2) {
         float f = wr;
@@ -540,7 +562,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       for (int s = 0; s < 8; ++s) {
         const int t = tv + s;
         float val = to_f(*k2sw(sKt, LDK, t, c));
-        if (GATE == kGateScalar) val *= fast_exp(sG[C - 1] - sG[t]);
+        if (GATE == kGateScalar) val *= sWt[t];
         if (GATE == kGateChannel) val *= fast_exp(*k2swf(sGc, DK + 4, C - 1, c) - *k2swf(sGc, DK + 4, t, c));
         f.set(s, val);
       }
