@@ -352,10 +352,9 @@ __device__ __forceinline__ void stage_rows(T* dst, const T* src, int tid) {
   }
 }
 
-// Two adjacent HC-column groups of rows [C][.] at once, so each row segment
-// read is a whole 128-byte line: the first group goes to dst[HC][C + 8]
-// (transposed) now, the second comes back in `held` for the next pass.
-// (Named registers, not an array: a private array here is moved to LDS.)
+// A [C][HC] tile held in registers between its load and its transposed
+// store to dst[HC][C + 8].  (Named registers, not an array: a private array
+// here is moved to LDS.)
 template <typename T, int HC>
 struct HeldTile {
   static constexpr int kVec = 16 / static_cast<int>(sizeof(T)), kVpr = HC / kVec;
@@ -377,24 +376,19 @@ __device__ __forceinline__ void tile_t_store(T* dst, const HeldTile<T, HC>& held
   tile_t_put<T, HC>(dst, held.v0, 0, tid);
   if constexpr (HeldTile<T, HC>::kPer == 2) tile_t_put<T, HC>(dst, held.v1, 1, tid);
 }
+// One pass's tile (rows [C], columns HC from src) into registers, a pass
+// ahead of its transposed LDS store (tile_t_store); rows >= nvalid are zero
 template <typename T, int HC>
-__device__ __forceinline__ void load_pair_t(T* dst, HeldTile<T, HC>& held, const T* src, int64_t lds,
-                                            int nvalid, int tid) {
+__device__ __forceinline__ void load_tile_regs(HeldTile<T, HC>& t, const T* src, int64_t lds, int nvalid,
+                                               int tid) {
   using HT = HeldTile<T, HC>;
-  auto get = [&](int j, float4& now, float4& hold) {
+  auto get = [&](int j, float4& v) {
     const int idx = tid + 256 * j, r = idx / HT::kVpr, cv = idx % HT::kVpr;
-    now = make_float4(0.f, 0.f, 0.f, 0.f);
-    hold = now;
-    if (r < nvalid) {
-      now = *reinterpret_cast<const float4*>(src + r * lds + cv * HT::kVec);
-      hold = *reinterpret_cast<const float4*>(src + r * lds + HC + cv * HT::kVec);
-    }
+    v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < nvalid) v = *reinterpret_cast<const float4*>(src + r * lds + cv * HT::kVec);
   };
-  float4 n0, n1;
-  get(0, n0, held.v0);
-  if constexpr (HT::kPer == 2) get(1, n1, held.v1);
-  tile_t_put<T, HC>(dst, n0, 0, tid);
-  if constexpr (HT::kPer == 2) tile_t_put<T, HC>(dst, n1, 1, tid);
+  get(0, t.v0);
+  if constexpr (HT::kPer == 2) get(1, t.v1);
 }
 
 // One phase-B pass's rows of the chunk-start state S^T and of its adjoint
@@ -624,6 +618,14 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   // phase B's first state rows: in flight through the rest of phase A
   StateRows<T, HC, DV> srows;
   srows.load(static_cast<const T*>(a.Hs) + cs, static_cast<const T*>(ba.dHs) + cs, tid);
+  // and its transposed write-key, query and key tiles
+  const T* qtile = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
+  const T* ktile = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
+  const T* kttile = static_cast<const T*>(a.Ktr) + rk;
+  HeldTile<T, HC> tKt, tQ, tK;
+  load_tile_regs<T, HC>(tKt, kttile, DK, C, tid);
+  load_tile_regs<T, HC>(tQ, qtile, HD, n, tid);
+  load_tile_regs<T, HC>(tK, ktile, HD, n, tid);
   // E rows of this wave (phase B's A operand of A3), from the staged copy
 #pragma unroll
   for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, ra, 32 * kk + 8 * lg));
@@ -658,30 +660,24 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   T* dq = static_cast<T*>(ba.dq) + (b * a.T + t0) * HD + h * DK;
   T* dKm = static_cast<T*>(ba.dKm) + rk;
   T* dKt = static_cast<T*>(ba.dKt) + rk;
-  static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
-  HeldTile<T, HC> hKt, hQ, hK;
 #pragma unroll 1
   for (int p = 0; p < NPASS; ++p) {
     const int c0 = p * HC;
     __syncthreads();   // phase A (or the previous pass) is done with the LDS
     srows.store(sS, sdS, tid);
-    // transposed Kt, Q, K tiles: even passes read two column groups (whole
-    // lines) and keep the second for the odd pass
-    if ((p & 1) == 0) {
-      load_pair_t<T, HC>(sKtT, hKt, static_cast<const T*>(a.Ktr) + rk + c0, DK, C, tid);
-      load_pair_t<T, HC>(sQT, hQ, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
-      load_pair_t<T, HC>(sKT, hK, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
-    } else {
-      tile_t_store<T, HC>(sKtT, hKt, tid);
-      tile_t_store<T, HC>(sQT, hQ, tid);
-      tile_t_store<T, HC>(sKT, hK, tid);
-    }
+    // transposed Kt, Q, K tiles (loaded during the previous pass)
+    tile_t_store<T, HC>(sKtT, tKt, tid);
+    tile_t_store<T, HC>(sQT, tQ, tid);
+    tile_t_store<T, HC>(sKT, tK, tid);
     __syncthreads();
     {
       // the next pass's state rows load during this pass (the last pass
       // reloads its own rows, unused)
       const int cn = min(p + 1, NPASS - 1) * HC;
       srows.load(static_cast<const T*>(a.Hs) + cs + cn * DV, static_cast<const T*>(ba.dHs) + cs + cn * DV, tid);
+      load_tile_regs<T, HC>(tKt, kttile + cn, DK, C, tid);
+      load_tile_regs<T, HC>(tQ, qtile + cn, HD, n, tid);
+      load_tile_regs<T, HC>(tK, ktile + cn, HD, n, tid);
     }
     // sum(dS' o S) over this pass's rows
     for (int idx = tid; idx < HC * DV; idx += 256) {
@@ -929,6 +925,14 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
   // phase B's first state rows: in flight through the rest of phase A
   StateRows<T, HC, DV> srows;
   srows.load(static_cast<const T*>(a.Hs) + cs, static_cast<const T*>(ba.dHs) + cs, tid);
+  // and its transposed write-key, query and key tiles
+  const T* qtile = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
+  const T* ktile = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
+  const T* kttile = static_cast<const T*>(a.Ktr) + rk;
+  HeldTile<T, HC> tKt, tQ, tK;
+  load_tile_regs<T, HC>(tKt, kttile, DK, C, tid);
+  load_tile_regs<T, HC>(tQ, qtile, HD, n, tid);
+  load_tile_regs<T, HC>(tK, ktile, HD, n, tid);
 #pragma unroll
   for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, ra, 32 * kk + 8 * lg));
   __syncthreads();
@@ -951,8 +955,6 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
   T* dKm = static_cast<T*>(ba.dKm) + rk;
   T* dKt = static_cast<T*>(ba.dKt) + rk;
   const float* Gc = a.G + rk;   // in-chunk log-decay prefix rows [t][c]
-  static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
-  HeldTile<T, HC> hKt, hQ, hK;
 #pragma unroll 1
   for (int p = 0; p < NPASS; ++p) {
     const int c0 = p * HC;
@@ -968,21 +970,18 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
         sGT[(c4 + 3) * LDG + t] = gv.w;
       }
     }
-    if ((p & 1) == 0) {
-      load_pair_t<T, HC>(sKtT, hKt, static_cast<const T*>(a.Ktr) + rk + c0, DK, C, tid);
-      load_pair_t<T, HC>(sQT, hQ, static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
-      load_pair_t<T, HC>(sKT, hK, static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK + c0, HD, n, tid);
-    } else {
-      tile_t_store<T, HC>(sKtT, hKt, tid);
-      tile_t_store<T, HC>(sQT, hQ, tid);
-      tile_t_store<T, HC>(sKT, hK, tid);
-    }
+    tile_t_store<T, HC>(sKtT, tKt, tid);
+    tile_t_store<T, HC>(sQT, tQ, tid);
+    tile_t_store<T, HC>(sKT, tK, tid);
     __syncthreads();
     {
       // the next pass's state rows load during this pass (the last pass
       // reloads its own rows, unused)
       const int cn = min(p + 1, NPASS - 1) * HC;
       srows.load(static_cast<const T*>(a.Hs) + cs + cn * DV, static_cast<const T*>(ba.dHs) + cs + cn * DV, tid);
+      load_tile_regs<T, HC>(tKt, kttile + cn, DK, C, tid);
+      load_tile_regs<T, HC>(tQ, qtile + cn, HD, n, tid);
+      load_tile_regs<T, HC>(tK, ktile + cn, HD, n, tid);
     }
     {
       // sum_v S dS' per channel of the pass: 8 lanes per channel
