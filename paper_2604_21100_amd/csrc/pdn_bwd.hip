@@ -391,6 +391,25 @@ __device__ __forceinline__ void load_tile_regs(HeldTile<T, HC>& t, const T* src,
   if constexpr (HT::kPer == 2) get(1, t.v1);
 }
 
+// Dot product of two 16-byte vectors of T, on the packed words (no
+// element-addressed copy, which the compiler would place in memory)
+template <typename T>
+__device__ __forceinline__ float dot16(const float4& a, const float4& b);
+template <>
+__device__ __forceinline__ float dot16<float>(const float4& a, const float4& b) {
+  return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
+}
+template <>
+__device__ __forceinline__ float dot16<bf16>(const float4& a, const float4& b) {
+  // a 32-bit word holds two bf16: the low one is the high half of its float
+  auto w2 = [](float x, float y) {
+    const uint32_t u = __float_as_uint(x), v = __float_as_uint(y);
+    return __uint_as_float(u << 16) * __uint_as_float(v << 16) +
+           __uint_as_float(u & 0xffff0000u) * __uint_as_float(v & 0xffff0000u);
+  };
+  return w2(a.x, b.x) + w2(a.y, b.y) + w2(a.z, b.z) + w2(a.w, b.w);
+}
+
 // One phase-B pass's rows of the chunk-start state S^T and of its adjoint
 // ([HC][DV] each), loaded a pass ahead into named registers and written to
 // LDS ([HC][DV + 8], bank-spread) when the pass starts.
@@ -418,6 +437,11 @@ struct StateRows {
     };
     put(0, h0, d0);
     if constexpr (kPer == 2) put(1, h1, d1);
+  }
+  // sum of S o dS' over vector J's elements (state row (tid + 256 J) / kVpr)
+  template <int J>
+  __device__ __forceinline__ float dot() const {
+    return J == 0 ? dot16<T>(h0, d0) : dot16<T>(h1, d1);
   }
 };
 
@@ -665,6 +689,10 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
     const int c0 = p * HC;
     __syncthreads();   // phase A (or the previous pass) is done with the LDS
     srows.store(sS, sdS, tid);
+    if (GATE == kGateScalar) {   // sum(dS' o S) over this pass's rows
+      red += srows.template dot<0>();
+      if constexpr (StateRows<T, HC, DV>::kPer == 2) red += srows.template dot<1>();
+    }
     // transposed Kt, Q, K tiles (loaded during the previous pass)
     tile_t_store<T, HC>(sKtT, tKt, tid);
     tile_t_store<T, HC>(sQT, tQ, tid);
@@ -678,11 +706,6 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       load_tile_regs<T, HC>(tKt, kttile + cn, DK, C, tid);
       load_tile_regs<T, HC>(tQ, qtile + cn, HD, n, tid);
       load_tile_regs<T, HC>(tK, ktile + cn, HD, n, tid);
-    }
-    // sum(dS' o S) over this pass's rows
-    for (int idx = tid; idx < HC * DV; idx += 256) {
-      const int c = idx / DV, v = idx % DV;
-      red += to_f(*sw(sS, LDV, c, v)) * to_f(*sw(sdS, LDV, c, v));
     }
 #pragma unroll 1
     for (int j = 0; j < HC / 16; ++j) {
@@ -961,6 +984,18 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
     __syncthreads();   // phase A (or the previous pass) is done with the LDS
     srows.store(sS, sdS, tid);
     {
+      // sum_v S dS' per channel of the pass, from the rows just stored: the
+      // kVpr lanes of a channel are adjacent
+      using SR = StateRows<T, HC, DV>;
+      auto chan = [&](float r2, int jj) {
+#pragma unroll
+        for (int off = 1; off < SR::kVpr; off <<= 1) r2 += __shfl_xor(r2, off, 64);
+        if (tid % SR::kVpr == 0) sRedC[(tid + 256 * jj) / SR::kVpr] = r2;
+      };
+      chan(srows.template dot<0>(), 0);
+      if constexpr (SR::kPer == 2) chan(srows.template dot<1>(), 1);
+    }
+    {
       for (int idx = tid; idx < C * (HC / 4); idx += 256) {
         const int t = idx / (HC / 4), c4 = (idx % (HC / 4)) * 4;
         const float4 gv = *reinterpret_cast<const float4*>(Gc + t * DK + c0 + c4);
@@ -982,17 +1017,6 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
       load_tile_regs<T, HC>(tKt, kttile + cn, DK, C, tid);
       load_tile_regs<T, HC>(tQ, qtile + cn, HD, n, tid);
       load_tile_regs<T, HC>(tK, ktile + cn, HD, n, tid);
-    }
-    {
-      // sum_v S dS' per channel of the pass: 8 lanes per channel
-      const int c = tid >> 3, part = tid & 7;
-      float red = 0.f;
-      for (int v = part * (DV / 8); v < (part + 1) * (DV / 8); ++v)
-        red += to_f(*sw(sS, LDV, c, v)) * to_f(*sw(sdS, LDV, c, v));
-      red += __shfl_xor(red, 1, 64);
-      red += __shfl_xor(red, 2, 64);
-      red += __shfl_xor(red, 4, 64);
-      if (part == 0) sRedC[c] = red;
     }
 #pragma unroll 1
     for (int j = 0; j < HC / 16; ++j) {
