@@ -669,17 +669,14 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
     sRs[tid] = GATE == kGateScalar ? sRs[tid] - (sCs[tid] + sCs[C + tid] + sCs[2 * C + tid] + sCs[3 * C + tid])
                                    : 0.f;
   }
-  float lam[4], wr[4], bt[4];
-#pragma unroll
-  for (int ii = 0; ii < 4; ++ii) {
-    const int r = 16 * w + 4 * lg + ii;
-    lam[ii] = GATE == kGateScalar ? fast_exp(sG[r]) : 1.f;
-    wr[ii] = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[r]) : 1.f;
-    bt[ii] = sBeta[r];
-  }
+  // phase B computes its tiles transposed (every product with its operands
+  // swapped), so a lane holds row ra = 16 w + lr at columns 16 j + 4 lg + ii
+  const float lam = GATE == kGateScalar ? fast_exp(sG[ra]) : 1.f;
+  const float wr = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[ra]) : 1.f;
+  const float bt = sBeta[ra];
 
   // ---- phase B
-  float pq[4] = {0.f, 0.f, 0.f, 0.f}, pk[4] = {0.f, 0.f, 0.f, 0.f}, pw[4] = {0.f, 0.f, 0.f, 0.f};
+  float pq = 0.f, pk = 0.f, pw = 0.f;
   float red = 0.f;
   T* dq = static_cast<T*>(ba.dq) + (b * a.T + t0) * HD + h * DK;
   T* dKm = static_cast<T*>(ba.dKm) + rk;
@@ -709,48 +706,45 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
     }
 #pragma unroll 1
     for (int j = 0; j < HC / 16; ++j) {
+      // A1 = dO_s S, A2' = Z S, A3 = E dS' (transposed tiles)
       floatx4 A1 = {0.f, 0.f, 0.f, 0.f}, A2 = A1, A3 = A1;
 #pragma unroll
       for (int kk = 0; kk < KV; ++kk) {
         const Frag8<T> fh = ld8(sw(sS, LDV, 16 * j + lr, 32 * kk + 8 * lg));
         const Frag8<T> fd = ld8(sw(sdS, LDV, 16 * j + lr, 32 * kk + 8 * lg));
-        mma(A1, fO[kk], fh);
-        mma(A2, fZ[kk], fh);
-        mma(A3, fE[kk], fd);
+        mma(A1, fh, fO[kk]);
+        mma(A2, fh, fZ[kk]);
+        mma(A3, fd, fE[kk]);
       }
       // row partials: Q_r . A1_r, K_r . A2'_r (gate and dbeta), Kt_r . A3_r
-      const int c = 16 * j + lr;
+      const int cb = 16 * j + 4 * lg;
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
-        const int r = 16 * w + 4 * lg + ii;
         A1[ii] *= a.scale;
-        pq[ii] += to_f(*sw(sQT, LDT, c, r)) * A1[ii];
-        pk[ii] += to_f(*sw(sKT, LDT, c, r)) * A2[ii];
-        pw[ii] += to_f(*sw(sKtT, LDT, c, r)) * A3[ii];
+        pq += to_f(*sw(sQT, LDT, cb + ii, ra)) * A1[ii];
+        pk += to_f(*sw(sKT, LDT, cb + ii, ra)) * A2[ii];
+        pw += to_f(*sw(sKtT, LDT, cb + ii, ra)) * A3[ii];
       }
       floatx4 aq, ak, at;
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
-        aq[ii] = lam[ii] * A1[ii];
-        ak[ii] = -lam[ii] * bt[ii] * A2[ii];
-        at[ii] = wr[ii] * A3[ii];
+        aq[ii] = lam * A1[ii];
+        ak[ii] = -lam * bt * A2[ii];
+        at[ii] = wr * A3[ii];
       }
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
         const Frag8<T> fk = ld8(sw(sKtT, LDT, 16 * j + lr, 32 * k2 + 8 * lg));
-        mma(aq, fSq[k2], fk);
-        mma(ak, fSk[k2], fk);
-        mma(at, fSqT[k2], ld8(sw(sQT, LDT, 16 * j + lr, 32 * k2 + 8 * lg)));
-        mma(at, fSkT[k2], ld8(sw(sKT, LDT, 16 * j + lr, 32 * k2 + 8 * lg)));
+        mma(aq, fk, fSq[k2]);
+        mma(ak, fk, fSk[k2]);
+        mma(at, ld8(sw(sQT, LDT, 16 * j + lr, 32 * k2 + 8 * lg)), fSqT[k2]);
+        mma(at, ld8(sw(sKT, LDT, 16 * j + lr, 32 * k2 + 8 * lg)), fSkT[k2]);
       }
-      // to this wave's output rows in LDS (rows 4 lg + ii, column c)
-      T* so = sOut + w * 3 * 16 * LDO;
-#pragma unroll
-      for (int ii = 0; ii < 4; ++ii) {
-        so[(4 * lg + ii) * LDO + c] = from_f<T>(aq[ii]);
-        so[(16 + 4 * lg + ii) * LDO + c] = from_f<T>(ak[ii]);
-        so[(32 + 4 * lg + ii) * LDO + c] = from_f<T>(at[ii]);
-      }
+      // to this wave's output rows in LDS: row lr, four adjacent columns
+      T* so = sOut + w * 3 * 16 * LDO + lr * LDO + cb;
+      st4<T>(so, aq[0], aq[1], aq[2], aq[3]);
+      st4<T>(so + 16 * LDO, ak[0], ak[1], ak[2], ak[3]);
+      st4<T>(so + 32 * LDO, at[0], at[1], at[2], at[3]);
     }
     {
       // this wave's 16 rows x HC columns of dq, dK, dKt: 16-byte stores
@@ -769,22 +763,16 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
     }
   }
 #pragma unroll
-  for (int ii = 0; ii < 4; ++ii)
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) {
-      pq[ii] += __shfl_xor(pq[ii], off, 64);
-      pk[ii] += __shfl_xor(pk[ii], off, 64);
-      pw[ii] += __shfl_xor(pw[ii], off, 64);
-    }
-  if (lr == 0) {
-#pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-      const int r = 16 * w + 4 * lg + ii;
-      // dlam_r = Q_r . A1_r - beta_r K_r . A2'_r ;  dw_r = Kt_r . A3_r
-      sDl[r] = r < n ? pq[ii] - sBeta[r] * pk[ii] : 0.f;
-      sDw[r] = r < n ? pw[ii] : 0.f;
-      sKZ[r] = pk[ii];
-    }
+  for (int off = 16; off < 64; off <<= 1) {
+    pq += __shfl_xor(pq, off, 64);
+    pk += __shfl_xor(pk, off, 64);
+    pw += __shfl_xor(pw, off, 64);
+  }
+  if (lg == 0) {
+    // dlam_r = Q_r . A1_r - beta_r K_r . A2'_r ;  dw_r = Kt_r . A3_r
+    sDl[ra] = ra < n ? pq - bt * pk : 0.f;
+    sDw[ra] = ra < n ? pw : 0.f;
+    sKZ[ra] = pk;
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) red += __shfl_xor(red, off, 64);
