@@ -410,6 +410,15 @@ __device__ __forceinline__ float dot16<bf16>(const float4& a, const float4& b) {
   return w2(a.x, b.x) + w2(a.y, b.y) + w2(a.z, b.z) + w2(a.w, b.w);
 }
 
+// Two adjacent passes' tiles at once (columns [0, HC) into `now`, [HC, 2 HC)
+// into `held`), so every row segment fetched is a whole 128-byte line
+template <typename T, int HC>
+__device__ __forceinline__ void load_pair_regs(HeldTile<T, HC>& now, HeldTile<T, HC>& held, const T* src,
+                                               int64_t lds, int nvalid, int tid) {
+  load_tile_regs<T, HC>(now, src, lds, nvalid, tid);
+  load_tile_regs<T, HC>(held, src + HC, lds, nvalid, tid);
+}
+
 // One phase-B pass's rows of the chunk-start state S^T and of its adjoint
 // ([HC][DV] each), loaded a pass ahead into named registers and written to
 // LDS ([HC][DV + 8], bank-spread) when the pass starts.
@@ -646,10 +655,12 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   const T* qtile = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
   const T* ktile = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
   const T* kttile = static_cast<const T*>(a.Ktr) + rk;
-  HeldTile<T, HC> tKt, tQ, tK;
-  load_tile_regs<T, HC>(tKt, kttile, DK, C, tid);
-  load_tile_regs<T, HC>(tQ, qtile, HD, n, tid);
-  load_tile_regs<T, HC>(tK, ktile, HD, n, tid);
+  // (the tiles of two passes at a time: whole lines)
+  static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
+  HeldTile<T, HC> tKt, tQ, tK, hKt, hQ, hK;
+  load_pair_regs<T, HC>(tKt, hKt, kttile, DK, C, tid);
+  load_pair_regs<T, HC>(tQ, hQ, qtile, HD, n, tid);
+  load_pair_regs<T, HC>(tK, hK, ktile, HD, n, tid);
   // E rows of this wave (phase B's A operand of A3), from the staged copy
 #pragma unroll
   for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, ra, 32 * kk + 8 * lg));
@@ -690,19 +701,27 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       red += srows.template dot<0>();
       if constexpr (StateRows<T, HC, DV>::kPer == 2) red += srows.template dot<1>();
     }
-    // transposed Kt, Q, K tiles (loaded during the previous pass)
-    tile_t_store<T, HC>(sKtT, tKt, tid);
-    tile_t_store<T, HC>(sQT, tQ, tid);
-    tile_t_store<T, HC>(sKT, tK, tid);
+    // transposed Kt, Q, K tiles (loaded during an earlier pass)
+    if ((p & 1) == 0) {
+      tile_t_store<T, HC>(sKtT, tKt, tid);
+      tile_t_store<T, HC>(sQT, tQ, tid);
+      tile_t_store<T, HC>(sKT, tK, tid);
+    } else {
+      tile_t_store<T, HC>(sKtT, hKt, tid);
+      tile_t_store<T, HC>(sQT, hQ, tid);
+      tile_t_store<T, HC>(sKT, hK, tid);
+    }
     __syncthreads();
     {
       // the next pass's state rows load during this pass (the last pass
       // reloads its own rows, unused)
       const int cn = min(p + 1, NPASS - 1) * HC;
       srows.load(static_cast<const T*>(a.Hs) + cs + cn * DV, static_cast<const T*>(ba.dHs) + cs + cn * DV, tid);
-      load_tile_regs<T, HC>(tKt, kttile + cn, DK, C, tid);
-      load_tile_regs<T, HC>(tQ, qtile + cn, HD, n, tid);
-      load_tile_regs<T, HC>(tK, ktile + cn, HD, n, tid);
+      if ((p & 1) == 1 && p + 1 < NPASS) {   // the next two passes' tiles
+        load_pair_regs<T, HC>(tKt, hKt, kttile + cn, DK, C, tid);
+        load_pair_regs<T, HC>(tQ, hQ, qtile + cn, HD, n, tid);
+        load_pair_regs<T, HC>(tK, hK, ktile + cn, HD, n, tid);
+      }
     }
 #pragma unroll 1
     for (int j = 0; j < HC / 16; ++j) {
