@@ -959,10 +959,12 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
   const T* qtile = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
   const T* ktile = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
   const T* kttile = static_cast<const T*>(a.Ktr) + rk;
-  HeldTile<T, HC> tKt, tQ, tK;
-  load_tile_regs<T, HC>(tKt, kttile, DK, C, tid);
-  load_tile_regs<T, HC>(tQ, qtile, HD, n, tid);
-  load_tile_regs<T, HC>(tK, ktile, HD, n, tid);
+  // (the tiles of two passes at a time: whole lines)
+  static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
+  HeldTile<T, HC> tKt, tQ, tK, hKt, hQ, hK;
+  load_pair_regs<T, HC>(tKt, hKt, kttile, DK, C, tid);
+  load_pair_regs<T, HC>(tQ, hQ, qtile, HD, n, tid);
+  load_pair_regs<T, HC>(tK, hK, ktile, HD, n, tid);
 #pragma unroll
   for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, ra, 32 * kk + 8 * lg));
   __syncthreads();
@@ -1012,18 +1014,26 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
         sGT[(c4 + 3) * LDG + t] = gv.w;
       }
     }
-    tile_t_store<T, HC>(sKtT, tKt, tid);
-    tile_t_store<T, HC>(sQT, tQ, tid);
-    tile_t_store<T, HC>(sKT, tK, tid);
+    if ((p & 1) == 0) {
+      tile_t_store<T, HC>(sKtT, tKt, tid);
+      tile_t_store<T, HC>(sQT, tQ, tid);
+      tile_t_store<T, HC>(sKT, tK, tid);
+    } else {
+      tile_t_store<T, HC>(sKtT, hKt, tid);
+      tile_t_store<T, HC>(sQT, hQ, tid);
+      tile_t_store<T, HC>(sKT, hK, tid);
+    }
     __syncthreads();
     {
       // the next pass's state rows load during this pass (the last pass
       // reloads its own rows, unused)
       const int cn = min(p + 1, NPASS - 1) * HC;
       srows.load(static_cast<const T*>(a.Hs) + cs + cn * DV, static_cast<const T*>(ba.dHs) + cs + cn * DV, tid);
-      load_tile_regs<T, HC>(tKt, kttile + cn, DK, C, tid);
-      load_tile_regs<T, HC>(tQ, qtile + cn, HD, n, tid);
-      load_tile_regs<T, HC>(tK, ktile + cn, HD, n, tid);
+      if ((p & 1) == 1 && p + 1 < NPASS) {   // the next two passes' tiles
+        load_pair_regs<T, HC>(tKt, hKt, kttile + cn, DK, C, tid);
+        load_pair_regs<T, HC>(tQ, hQ, qtile + cn, HD, n, tid);
+        load_pair_regs<T, HC>(tK, hK, ktile + cn, HD, n, tid);
+      }
     }
 #pragma unroll 1
     for (int j = 0; j < HC / 16; ++j) {
