@@ -80,6 +80,7 @@ struct RevFrags {
   // c = 16 (w CT + ct) + 4 lg + ii this lane holds
   float gC[GATE == kGateChannel ? CT : 1][GATE == kGateChannel ? 4 : 1];
   float beta[4];   // beta of rows 16w + 4lg + ii (raw: past the end masked at use)
+  float gw[GATE == kGateScalar ? 4 : 1];   // scalar gate: G of rows 16w + 4lg + ii
 };
 
 struct RevCtx {
@@ -121,7 +122,9 @@ __device__ __forceinline__ void rev_load(RevFrags<T, DK, GATE>& f, const BwdArgs
   const int64_t ck = (x.bh * a.NT + i) * (int64_t)(DK * C);
   const T* pt = static_cast<const T*>(a.PtT) + cc;
   const T* mt = static_cast<const T*>(a.MtT) + cc;
-  const T* kw = static_cast<const T*>(a.Kw) + (x.bh * a.Tpad + t0) * DK;
+  // decayed write-key rows w_r Kt: stored for the per-channel gate; with a
+  // scalar gate (or none) the plain rows, w_r applied to the product's rows
+  const T* kw = static_cast<const T*>(GATE == kGateChannel ? a.Kw : a.Ktr) + (x.bh * a.Tpad + t0) * DK;
   const T* ql = static_cast<const T*>(a.QlT) + ck;
   const T* kn = static_cast<const T*>(a.KnT) + ck;
   const int ra = 16 * x.w + x.lr;
@@ -145,7 +148,11 @@ __device__ __forceinline__ void rev_load(RevFrags<T, DK, GATE>& f, const BwdArgs
   // the dO slab staged at the end of this chunk's step: that of the chunk
   // before it (reverse order), so it has two steps to arrive
   rev_load_dO<T>(f.dO, ba, max(i - 1, 0), x);
-  if (GATE == kGateScalar) f.gC[0][0] = a.G[x.bh * a.Tpad + t0 + C - 1];
+  if (GATE == kGateScalar) {
+    f.gC[0][0] = a.G[x.bh * a.Tpad + t0 + C - 1];
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) f.gw[ii] = a.G[x.bh * a.Tpad + t0 + 16 * x.w + 4 * x.lg + ii];
+  }
   if (GATE == kGateChannel) {
     const float* gl = a.G + (x.bh * a.Tpad + t0 + C - 1) * DK;
 #pragma unroll
@@ -201,13 +208,18 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE>& f, bool stage_ne
     }
   }
   // ---- dE = P^T dO_s + Diag(w) Kt dS'^T   (rows t of this wave)
+  float wr[4];
+#pragma unroll
+  for (int ii = 0; ii < 4; ++ii) wr[ii] = GATE == kGateScalar ? fast_exp(f.gC[0][0] - f.gw[ii]) : 1.f;
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt) {
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f}, acw = acc;
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Pt[k2], ld8(sw(sDOc, LDE, 16 * vt + lr, k2 * 32 + 8 * lg)));
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) mma(acc, f.Kw[kk], ld8(sw(sH, LDH, 16 * vt + lr, kk * 32 + 8 * lg)));
+    for (int kk = 0; kk < KK; ++kk) mma(acw, f.Kw[kk], ld8(sw(sH, LDH, 16 * vt + lr, kk * 32 + 8 * lg)));
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) acc[ii] += wr[ii] * acw[ii];
     st4<T>(sw(sE, LDE, 16 * vt + lr, 16 * w + 4 * lg), acc[0], acc[1], acc[2], acc[3]);
   }
   lds_barrier_b();
@@ -1495,7 +1507,7 @@ BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate,
   L.PtT = take(bh * nt * C * C * esz);
   L.MtT = take(bh * nt * C * C * esz);
   L.Ktr = take(bh * tp * dk * esz);
-  L.Kw = take(bh * tp * dk * esz);
+  L.Kw = gate == kGateChannel ? take(bh * tp * dk * esz) : 0;   // = w_r Kt rows, per-channel gate only
   L.QlT = take(bh * nt * dk * C * esz);
   L.KnT = take(bh * nt * dk * C * esz);
   L.dHs = take(bh * nt * dk * dv * esz);

@@ -534,22 +534,20 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       }
       st8(MtT + r * C + t0v, ft);
     }
-    // write-key rows and w-scaled write-key rows
+    // write-key rows, and for the per-channel gate the decayed rows
+    // w_r o Kt (with a scalar gate the reverse scan applies w_r itself)
     T* Kr = static_cast<T*>(a.Ktr) + (bh * a.Tpad + t0) * DK;
-    T* Kwr = static_cast<T*>(a.Kw) + (bh * a.Tpad + t0) * DK;
     for (int idx = tid; idx < C * (DK / 8); idx += 256) {
       const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
       const Frag8<T> fk = ld8(k2sw(sKt, LDK, r, c0));
-      Frag8<T> fw;
-      const float wr = GATE == kGateScalar ? sWt[r] : 1.f;
-#pragma unroll
-      for (int s2 = 0; s2 < 8; ++s2) {
-        float f = wr;
-        if (GATE == kGateChannel) f = fast_exp(*k2swf(sGc, DK + 4, C - 1, c0 + s2) - *k2swf(sGc, DK + 4, r, c0 + s2));
-        fw.set(s2, f * fk.get(s2));
-      }
       st8(Kr + r * DK + c0, fk);
-      st8(Kwr + r * DK + c0, fw);
+      if (GATE == kGateChannel) {
+        Frag8<T> fw;
+#pragma unroll
+        for (int s2 = 0; s2 < 8; ++s2)
+          fw.set(s2, fast_exp(*k2swf(sGc, DK + 4, C - 1, c0 + s2) - *k2swf(sGc, DK + 4, r, c0 + s2)) * fk.get(s2));
+        st8(static_cast<T*>(a.Kw) + (bh * a.Tpad + t0 + r) * DK + c0, fw);
+      }
     }
   }
   // ---- decayed write keys, transposed per chunk: (Kt * Lam_C / Lam_t)^T

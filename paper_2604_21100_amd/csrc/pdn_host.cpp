@@ -206,7 +206,7 @@ static void set_forward_ws(pdn::FwdArgs& a, const pdn::WsLayout& L, const pdn_pr
 
 static void set_residuals(pdn::FwdArgs& f, const pdn::BwdWsLayout& L, char* w) {
   f.Hs = w + L.Hs; f.Er = w + L.Er; f.PtT = w + L.PtT; f.MtT = w + L.MtT;
-  f.Ktr = w + L.Ktr; f.Kw = w + L.Kw; f.QlT = w + L.QlT; f.KnT = w + L.KnT;
+  f.Ktr = w + L.Ktr; f.Kw = L.Kw ? w + L.Kw : nullptr; f.QlT = w + L.QlT; f.KnT = w + L.KnT;
 }
 
 // train: the training forward (also leaves the backward's intermediates in

@@ -64,7 +64,7 @@ struct FwdArgs {
   void* PtT;      // [BH, NT, C, C] io    P^T
   void* MtT;      // [BH, NT, C, C] io    M^T, M = (I + At)^{-1} (T = M Diag(beta))
   void* Ktr;      // [BH, Tpad, dk] io    write key rows
-  void* Kw;       // [BH, Tpad, dk] io    w_r * write key rows
+  void* Kw;       // [BH, Tpad, dk] io    w_r o write key rows (per-channel gate; else NULL)
   void* QlT;      // [BH, NT, dk, C] io   (Diag(lam) Q)^T per chunk
   void* KnT;      // [BH, NT, dk, C] io   -(Diag(lam) K)^T per chunk
 };
