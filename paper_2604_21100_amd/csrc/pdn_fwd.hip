@@ -123,20 +123,28 @@ __device__ __forceinline__ T* k2sw(T* base, int ld, int row, int col) {
 __device__ __forceinline__ float* k2swf(float* base, int ld, int row, int col) {
   return base + row * ld + (col ^ (((row >> 3) & 7) << 2));
 }
-template <typename T, int DK, int GATE>
+// NOQ (per-channel gate, query not rewritten): the query tile is not staged
+// (its rows are read from HBM where needed), and the solve's X and Y use the
+// gate-prefix tile's memory, which is dead by then.  That keeps the block
+// under 80 KB, two blocks per CU.
+template <typename T, int DK, int GATE, int PREC>
 struct K2Smem {
   static constexpr int LDK = DK + 8;          // padded row (elements)
   static constexpr int LDA = C + 4;           // fp32 C x C rows
   static constexpr size_t kRow = sizeof(T) * C * LDK;
   static constexpr size_t kFloatCC = sizeof(float) * C * LDA;
   static constexpr size_t kR1 = kRow > kFloatCC ? kRow : kFloatCC;  // sK, later sA
-  static constexpr size_t kR2 = kR1;                                // sQ, later sX
-  static constexpr size_t kR3 = kRow;                               // sKt
-  static constexpr size_t kGc = GATE == kGateChannel ? sizeof(float) * C * (DK + 4) : 0;
   static constexpr size_t kY = sizeof(float) * 4 * 16 * 17;
-  static constexpr size_t kScal = sizeof(float) * 7 * C;
+  static constexpr size_t kGc = GATE == kGateChannel ? sizeof(float) * C * (DK + 4) : 0;  // later sX, sY (NOQ)
+  // (at d_k = 64 the gate tile is too small for X and Y, and the block fits
+  // two per CU anyway)
+  static constexpr bool NOQ = GATE == kGateChannel && PREC != kATQ && kGc >= kFloatCC + kY;
+  static constexpr size_t kR2 = NOQ ? 0 : kR1;                      // sQ, later sX
+  static constexpr size_t kR3 = kRow;                               // sKt
+  static constexpr size_t kYs = NOQ ? 0 : kY;
+  static constexpr size_t kScal = sizeof(float) * 8 * C;    // per-row scalars and the row norms
   static constexpr size_t kSeg = sizeof(float) * 2 * 256;   // preconditioner segment carries
-  static constexpr size_t kTotal = kR1 + kR2 + kR3 + kGc + kY + kScal + kSeg;
+  static constexpr size_t kTotal = kR1 + kR2 + kR3 + kGc + kYs + kScal + kSeg;
 };
 
 // BWD: also write the operand layouts the backward kernels read (P^T, M^T,
@@ -144,24 +152,26 @@ struct K2Smem {
 // -(Lam o K)^T; Lam the scalar or per-channel in-chunk decay).
 template <typename T, int DK, int GATE, int PREC, bool BWD>
 __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
-  using SM = K2Smem<T, DK, GATE>;
+  using SM = K2Smem<T, DK, GATE, PREC>;
+  constexpr bool NOQ = SM::NOQ;
   constexpr int LDK = SM::LDK, LDA = SM::LDA;
   __shared__ __attribute__((aligned(16))) char smem[SM::kTotal];
   T* sK = reinterpret_cast<T*>(smem);
   float* sA = reinterpret_cast<float*>(smem);
-  T* sQ = reinterpret_cast<T*>(smem + SM::kR1);
-  float* sX = reinterpret_cast<float*>(smem + SM::kR1);
+  T* sQ = reinterpret_cast<T*>(smem + SM::kR1);   // (not used with NOQ)
   T* sKt = reinterpret_cast<T*>(smem + SM::kR1 + SM::kR2);
   float* sGc = reinterpret_cast<float*>(smem + SM::kR1 + SM::kR2 + SM::kR3);
-  float* sY = reinterpret_cast<float*>(smem + SM::kR1 + SM::kR2 + SM::kR3 + SM::kGc);
-  float* sBeta = sY + 4 * 16 * 17;
+  float* sX = NOQ ? sGc : reinterpret_cast<float*>(smem + SM::kR1);
+  float* sY = NOQ ? sGc + C * LDA : reinterpret_cast<float*>(smem + SM::kR1 + SM::kR2 + SM::kR3 + SM::kGc);
+  float* sBeta = reinterpret_cast<float*>(smem + SM::kR1 + SM::kR2 + SM::kR3 + SM::kGc + SM::kYs);
+  float* sNrm = sBeta + 7 * C;   // row norms of the normalised write keys
   float* sBp = sBeta + C;
   float* sEgp = sBp + C;
   float* sG = sEgp + C;
   float* sGraw = sG + C;
   float* sLam = sGraw + C;   // scalar gate: exp(G_r)
   float* sWt = sLam + C;     // scalar gate: exp(G_{C-1} - G_r)
-  float* sSegE = sWt + C;
+  float* sSegE = sNrm + C;
   float* sSegP = sSegE + 256;
 
   const int64_t blk = blockIdx.x;
@@ -185,11 +195,11 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       if (r < n) {
         const int64_t off = ((b * a.T + t0 + r) * a.H + h) * DK + cv * VEC;
         kv = *reinterpret_cast<const float4*>(kp + off);
-        qv = *reinterpret_cast<const float4*>(qp + off);
+        if (!NOQ) qv = *reinterpret_cast<const float4*>(qp + off);
         if (PREC == kExternal) xv = *reinterpret_cast<const float4*>(xp + off);
       }
       *reinterpret_cast<float4*>(k2sw(sK, LDK, r, cv * VEC)) = kv;
-      *reinterpret_cast<float4*>(k2sw(sQ, LDK, r, cv * VEC)) = qv;
+      if (!NOQ) *reinterpret_cast<float4*>(k2sw(sQ, LDK, r, cv * VEC)) = qv;
       // identity write key: a copy of the key tile (the key tile's memory is
       // reused by the solve)
       if (PREC == kIdentity || PREC == kATQ) *reinterpret_cast<float4*>(k2sw(sKt, LDK, r, cv * VEC)) = kv;
@@ -287,7 +297,6 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         // normalisation ablation: kt = B k * f(m), m = k . (B k) per row;
         // the rows' m from the stored keys, then the keys recomputed exactly
         // and scaled once
-        float* sNrm = sY;   // free until the solve
         __syncthreads();
         {
           constexpr int PART = DK / 4;
@@ -335,7 +344,6 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       // the row sums k . p need every channel: the segment is walked once
       // for them and again for the exactly recomputed, normalised key
       const float A_seg = A;
-      float* sNrm = sY;   // free until the solve
 #pragma unroll
       for (int j = 0; j < SEG; ++j) {
         const float kv = kreg[j];
@@ -387,7 +395,13 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       for (int kk = 0; kk < DK / 32; ++kk) {
         const int c0 = kk * 32 + 8 * lg;
         Frag8<T> fk = ld8(k2sw(sK, LDK, r, c0));
-        Frag8<T> fq = ld8(k2sw(sQ, LDK, r, c0));
+        Frag8<T> fq;
+        if (NOQ) {
+          fq = frag_zero<T>();
+          if (r < n) fq = ld8(static_cast<const T*>(a.q) + ((b * a.T + t0 + r) * a.H + h) * DK + c0);
+        } else {
+          fq = ld8(k2sw(sQ, LDK, r, c0));
+        }
         Frag8<T> fb = ld8(k2sw(sKt, LDK, t, c0));
         if (GATE == kGateChannel) {
           // reference point: first row of the row block keeps both factors
@@ -441,11 +455,50 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         float lam = 1.f;
         if (GATE == kGateScalar) lam = sLam[r];
         if (GATE == kGateChannel) lam = fast_exp(*k2swf(sGc, DK + 4, r, c));
-        fq.set(s2, lam * to_f(*k2sw(sQ, LDK, r, c)));
+        float qv = 0.f;
+        if (!NOQ) qv = to_f(*k2sw(sQ, LDK, r, c));
+        else if (r < n) qv = to_f(static_cast<const T*>(a.q)[((b * a.T + t0 + r) * a.H + h) * DK + c]);
+        fq.set(s2, lam * qv);
         fk.set(s2, -lam * to_f(*k2sw(sK, LDK, r, c)));
       }
       st8(QlT + c * C + r0, fq);
       st8(KnT + c * C + r0, fk);
+    }
+  }
+  // the write-key outputs (they need only sKt and the gate prefix), before
+  // the solve
+  if (BWD) {
+    // write-key rows, and for the per-channel gate the decayed rows
+    // w_r o Kt (with a scalar gate the reverse scan applies w_r itself)
+    T* Kr = static_cast<T*>(a.Ktr) + (bh * a.Tpad + t0) * DK;
+    for (int idx = tid; idx < C * (DK / 8); idx += 256) {
+      const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
+      const Frag8<T> fk = ld8(k2sw(sKt, LDK, r, c0));
+      st8(Kr + r * DK + c0, fk);
+      if (GATE == kGateChannel) {
+        Frag8<T> fw;
+#pragma unroll
+        for (int s2 = 0; s2 < 8; ++s2)
+          fw.set(s2, fast_exp(*k2swf(sGc, DK + 4, C - 1, c0 + s2) - *k2swf(sGc, DK + 4, r, c0 + s2)) * fk.get(s2));
+        st8(static_cast<T*>(a.Kw) + (bh * a.Tpad + t0 + r) * DK + c0, fw);
+      }
+    }
+  }
+  // ---- decayed write keys, transposed per chunk: (Kt * Lam_C / Lam_t)^T
+  {
+    T* Kout = static_cast<T*>(a.KtG) + (bh * a.NT + i) * (int64_t)(DK * C);
+    for (int idx = tid; idx < DK * C / 8; idx += 256) {
+      const int c = idx / (C / 8), tv = (idx % (C / 8)) * 8;
+      Frag8<T> f;
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const int t = tv + s;
+        float val = to_f(*k2sw(sKt, LDK, t, c));
+        if (GATE == kGateScalar) val *= sWt[t];
+        if (GATE == kGateChannel) val *= fast_exp(*k2swf(sGc, DK + 4, C - 1, c) - *k2swf(sGc, DK + 4, t, c));
+        f.set(s, val);
+      }
+      st8(Kout + c * C + tv, f);
     }
   }
   __syncthreads();  // sK / sQ are free from here on
@@ -533,38 +586,6 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         ft.set(s2, upper ? *k2swf(sX, LDA, t, r) : 0.f);
       }
       st8(MtT + r * C + t0v, ft);
-    }
-    // write-key rows, and for the per-channel gate the decayed rows
-    // w_r o Kt (with a scalar gate the reverse scan applies w_r itself)
-    T* Kr = static_cast<T*>(a.Ktr) + (bh * a.Tpad + t0) * DK;
-    for (int idx = tid; idx < C * (DK / 8); idx += 256) {
-      const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
-      const Frag8<T> fk = ld8(k2sw(sKt, LDK, r, c0));
-      st8(Kr + r * DK + c0, fk);
-      if (GATE == kGateChannel) {
-        Frag8<T> fw;
-#pragma unroll
-        for (int s2 = 0; s2 < 8; ++s2)
-          fw.set(s2, fast_exp(*k2swf(sGc, DK + 4, C - 1, c0 + s2) - *k2swf(sGc, DK + 4, r, c0 + s2)) * fk.get(s2));
-        st8(static_cast<T*>(a.Kw) + (bh * a.Tpad + t0 + r) * DK + c0, fw);
-      }
-    }
-  }
-  // ---- decayed write keys, transposed per chunk: (Kt * Lam_C / Lam_t)^T
-  {
-    T* Kout = static_cast<T*>(a.KtG) + (bh * a.NT + i) * (int64_t)(DK * C);
-    for (int idx = tid; idx < DK * C / 8; idx += 256) {
-      const int c = idx / (C / 8), tv = (idx % (C / 8)) * 8;
-      Frag8<T> f;
-#pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const int t = tv + s;
-        float val = to_f(*k2sw(sKt, LDK, t, c));
-        if (GATE == kGateScalar) val *= sWt[t];
-        if (GATE == kGateChannel) val *= fast_exp(*k2swf(sGc, DK + 4, C - 1, c) - *k2swf(sGc, DK + 4, t, c));
-        f.set(s, val);
-      }
-      st8(Kout + c * C + tv, f);
     }
   }
 }
