@@ -124,9 +124,11 @@ __device__ __forceinline__ float* k2swf(float* base, int ld, int row, int col) {
   return base + row * ld + (col ^ (((row >> 3) & 7) << 2));
 }
 // NOQ (per-channel gate, query not rewritten): the query tile is not staged
-// (its rows are read from HBM where needed), and the solve's X and Y use the
-// gate-prefix tile's memory, which is dead by then.  That keeps the block
-// under 80 KB, two blocks per CU.
+// (its rows are read from HBM where needed), and the solve's X uses the
+// write-key tile's memory, which is dead once the write-key outputs are out.
+// That keeps the block under 80 KB, two per CU.  (For the other gates the
+// HBM reads of the transposed query cost more than a third block per CU
+// gains.)
 template <typename T, int DK, int GATE, int PREC>
 struct K2Smem {
   static constexpr int LDK = DK + 8;          // padded row (elements)
@@ -135,16 +137,15 @@ struct K2Smem {
   static constexpr size_t kFloatCC = sizeof(float) * C * LDA;
   static constexpr size_t kR1 = kRow > kFloatCC ? kRow : kFloatCC;  // sK, later sA
   static constexpr size_t kY = sizeof(float) * 4 * 16 * 17;
-  static constexpr size_t kGc = GATE == kGateChannel ? sizeof(float) * C * (DK + 4) : 0;  // later sX, sY (NOQ)
-  // (at d_k = 64 the gate tile is too small for X and Y, and the block fits
-  // two per CU anyway)
-  static constexpr bool NOQ = GATE == kGateChannel && PREC != kATQ && kGc >= kFloatCC + kY;
+  static constexpr size_t kGc = GATE == kGateChannel ? sizeof(float) * C * (DK + 4) : 0;
+  // (at d_k = 64 in bf16 the write-key tile is too small for X; that block is
+  // small anyway)
+  static constexpr bool NOQ = GATE == kGateChannel && PREC != kATQ && kRow >= kFloatCC;
   static constexpr size_t kR2 = NOQ ? 0 : kR1;                      // sQ, later sX
-  static constexpr size_t kR3 = kRow;                               // sKt
-  static constexpr size_t kYs = NOQ ? 0 : kY;
+  static constexpr size_t kR3 = kRow;                               // sKt, later sX (NOQ)
   static constexpr size_t kScal = sizeof(float) * 8 * C;    // per-row scalars and the row norms
   static constexpr size_t kSeg = sizeof(float) * 2 * 256;   // preconditioner segment carries
-  static constexpr size_t kTotal = kR1 + kR2 + kR3 + kGc + kYs + kScal + kSeg;
+  static constexpr size_t kTotal = kR1 + kR2 + kR3 + kGc + kY + kScal + kSeg;
 };
 
 // BWD: also write the operand layouts the backward kernels read (P^T, M^T,
@@ -161,9 +162,9 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   T* sQ = reinterpret_cast<T*>(smem + SM::kR1);   // (not used with NOQ)
   T* sKt = reinterpret_cast<T*>(smem + SM::kR1 + SM::kR2);
   float* sGc = reinterpret_cast<float*>(smem + SM::kR1 + SM::kR2 + SM::kR3);
-  float* sX = NOQ ? sGc : reinterpret_cast<float*>(smem + SM::kR1);
-  float* sY = NOQ ? sGc + C * LDA : reinterpret_cast<float*>(smem + SM::kR1 + SM::kR2 + SM::kR3 + SM::kGc);
-  float* sBeta = reinterpret_cast<float*>(smem + SM::kR1 + SM::kR2 + SM::kR3 + SM::kGc + SM::kYs);
+  float* sX = reinterpret_cast<float*>(smem + SM::kR1);   // R2, or with NOQ the write-key tile
+  float* sY = reinterpret_cast<float*>(smem + SM::kR1 + SM::kR2 + SM::kR3 + SM::kGc);
+  float* sBeta = sY + 4 * 16 * 17;
   float* sNrm = sBeta + 7 * C;   // row norms of the normalised write keys
   float* sBp = sBeta + C;
   float* sEgp = sBp + C;
@@ -259,10 +260,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     // pass 1 reduces each segment to (prod a, partial sum), the segments are
     // chained from the chunk-start state, pass 2 re-walks its rows
     constexpr int NSEG = 256 / DK, SEG = C / NSEG;
-    static_assert(SEG % 4 == 0, "segment rows come in float4 groups");
     const int c = tid % DK, sg = tid / DK, r0 = sg * SEG;
     // this thread's key column over its segment and the rows' decay and
     // betaP, in registers for every walk below
+    static_assert(SEG % 4 == 0, "segment rows come in float4 groups");
     float kreg[SEG], eg[SEG], bpr[SEG];
 #pragma unroll
     for (int j = 0; j < SEG; ++j) kreg[j] = to_f(*k2sw(sK, LDK, r0 + j, c));
@@ -387,6 +388,16 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   for (int j = 0; j < 4; ++j) { accA[j] = floatx4{0.f, 0.f, 0.f, 0.f}; accP[j] = accA[j]; }
   {
     const int r = 16 * w + lr;  // A-operand row of this lane
+    // NOQ: this row's query fragments straight from HBM, once
+    Frag8<T> fqr[DK / 32];
+    if (NOQ) {
+      const T* qrow = static_cast<const T*>(a.q) + ((b * a.T + t0 + min(r, n - 1)) * a.H + h) * DK;
+#pragma unroll
+      for (int kk = 0; kk < DK / 32; ++kk) {
+        fqr[kk] = ld8(qrow + kk * 32 + 8 * lg);
+        if (r >= n) fqr[kk] = frag_zero<T>();
+      }
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       if (j > w) break;
@@ -395,13 +406,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       for (int kk = 0; kk < DK / 32; ++kk) {
         const int c0 = kk * 32 + 8 * lg;
         Frag8<T> fk = ld8(k2sw(sK, LDK, r, c0));
-        Frag8<T> fq;
-        if (NOQ) {
-          fq = frag_zero<T>();
-          if (r < n) fq = ld8(static_cast<const T*>(a.q) + ((b * a.T + t0 + r) * a.H + h) * DK + c0);
-        } else {
-          fq = ld8(k2sw(sQ, LDK, r, c0));
-        }
+        Frag8<T> fq = NOQ ? fqr[kk] : ld8(k2sw(sQ, LDK, r, c0));
         Frag8<T> fb = ld8(k2sw(sKt, LDK, t, c0));
         if (GATE == kGateChannel) {
           // reference point: first row of the row block keeps both factors
