@@ -381,6 +381,32 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       *reinterpret_cast<float4*>(qt + r * DK + cv * VEC) = *reinterpret_cast<const float4*>(k2sw(sQ, LDK, r, cv * VEC));
     }
   }
+  if (GATE == kGateChannel) {
+    // Lam o Q (the query the scan reads: q, or for ATQ the preconditioned
+    // query) and Lam o K rows for the scan, rounded to io as the scan would
+    // round them, so it needs neither the gate tile nor the exponentials
+    T* ql = static_cast<T*>(a.QL) + (bh * a.Tpad + t0) * DK;
+    T* kl = static_cast<T*>(a.KL) + (bh * a.Tpad + t0) * DK;
+    const T* qg = static_cast<const T*>(a.q) + ((b * a.T + t0) * a.H + h) * DK;
+    for (int idx = tid; idx < C * (DK / 8); idx += 256) {
+      const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
+      Frag8<T> fk = ld8(k2sw(sK, LDK, r, c0)), fq;
+      if (NOQ) {
+        fq = frag_zero<T>();
+        if (r < n) fq = ld8(qg + r * a.H * DK + c0);
+      } else {
+        fq = ld8(k2sw(sQ, LDK, r, c0));
+      }
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) {
+        const float e = fast_exp(*k2swf(sGc, DK + 4, r, c0 + s2));
+        fq.set(s2, fq.get(s2) * e);
+        fk.set(s2, fk.get(s2) * e);
+      }
+      st8(ql + r * DK + c0, fq);
+      st8(kl + r * DK + c0, fk);
+    }
+  }
 
   // ---- interaction matrices on MFMA: wave w owns row block w
   floatx4 accA[4], accP[4];
@@ -610,7 +636,8 @@ struct SlabMap {
 
 // Operands one wave needs for one chunk, loaded two chunks ahead of use.
 // A-operand rows: token 16w + lr of the chunk; decayed write keys: rows
-// c = 16*(w*CT + ct) + lr.  Gate values are kept raw (log-domain) and the
+// c = 16*(w*CT + ct) + lr (per-channel gate: the read key and query rows
+// arrive already decayed).  Gate values are kept raw (log-domain) and the
 // value slab raw: nothing here is consumed at load time, so the loads stay
 // in flight across the compute of the chunks before it.
 //
@@ -624,7 +651,6 @@ struct ScanFrags {
   float4 v[SlabMap<T>::kPer];                      // value slab share
   float g[GATE == kGateScalar ? 4 : 1];            // G of rows 16w + 4lg + ii
   float gC[GATE == kGateChannel ? CT : 1][GATE == kGateNone ? 1 : 4];  // G at the chunk end
-  float gk[GATE == kGateChannel ? KK : 1][GATE == kGateChannel ? 8 : 1];  // G of the A rows
 };
 
 struct ScanCtx {
@@ -647,16 +673,22 @@ __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdAr
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int last = static_cast<int>(min<int64_t>(C, a.T - t0)) - 1;
   const int64_t HD = a.H * (int64_t)DK, HV = a.H * (int64_t)a.dv;
-  const T* kb = static_cast<const T*>(a.k) + (x.b * a.T + t0) * HD + x.h * DK;
-  const T* qb = static_cast<const T*>(a.q) + (x.b * a.T + t0) * HD + x.h * DK;
+  // per-channel gate: the decayed rows Lam o K, Lam o Q the prep kernel left
+  // in the workspace (row stride d_k)
+  constexpr bool CH = GATE == kGateChannel;
+  const int64_t ldk = CH ? DK : HD;
+  const T* kb = CH ? static_cast<const T*>(a.KL) + (x.bh * a.Tpad + t0) * DK
+                   : static_cast<const T*>(a.k) + (x.b * a.T + t0) * HD + x.h * DK;
+  const T* qb = CH ? static_cast<const T*>(a.QL) + (x.bh * a.Tpad + t0) * DK
+                   : static_cast<const T*>(a.q) + (x.b * a.T + t0) * HD + x.h * DK;
   const T* vb = static_cast<const T*>(a.v) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0;
   const T* tb = static_cast<const T*>(a.Tm) + (x.bh * a.NT + i) * (int64_t)(C * C);
   const T* pb = static_cast<const T*>(a.Pm) + (x.bh * a.NT + i) * (int64_t)(C * C);
   const T* gb = static_cast<const T*>(a.KtG) + (x.bh * a.NT + i) * (int64_t)(DK * C);
   const uint32_t rr = static_cast<uint32_t>(min(16 * x.w + x.lr, last));
-  const uint32_t okq = (rr * static_cast<uint32_t>(HD) + 8 * x.lg) * E;
+  const uint32_t okq = (rr * static_cast<uint32_t>(ldk) + 8 * x.lg) * E;
   if (LA) {
-    const T* qtb = static_cast<const T*>(a.Qt) + (x.bh * a.Tpad + t0) * DK;
+    const T* qtb = CH ? qb : static_cast<const T*>(a.Qt) + (x.bh * a.Tpad + t0) * DK;
     const uint32_t oqt = (rr * static_cast<uint32_t>(DK) + 8 * x.lg) * E;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) f.Q[kk] = ld8(at_bytes(qtb, oqt + kk * 32 * E));
@@ -694,11 +726,6 @@ __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdAr
     f.gC[0][0] = gs[C - 1];
   }
   if (GATE == kGateChannel) {
-    const float* gr = a.G + (x.bh * a.Tpad + t0) * DK + static_cast<uint32_t>(ra * DK + 8 * x.lg);
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
-#pragma unroll
-      for (int s = 0; s < 8; ++s) f.gk[kk][s] = gr[kk * 32 + s];
     const float* ge = a.G + (x.bh * a.Tpad + t0 + C - 1) * DK;
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
@@ -788,17 +815,6 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
   float lam[4];
 #pragma unroll
   for (int ii = 0; ii < 4; ++ii) lam[ii] = GATE == kGateScalar ? fast_exp(f.g[ii]) : 1.f;
-  if (GATE == kGateChannel) {
-    // Lam = exp(G) per (token, channel) on the read key and the query
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
-#pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const float e = fast_exp(f.gk[kk][s]);
-        if (!LA) f.K[kk].set(s, f.K[kk].get(s) * e);
-        if (OUT) f.Q[kk].set(s, f.Q[kk].get(s) * e);
-      }
-  }
   // ---- (Lam K) S^T and (Lam Q) S^T;  X = V - (Lam K) S^T
   Frag8<T> bH[2][KK];
 #pragma unroll
@@ -1007,6 +1023,10 @@ WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precon
   if (gate == kGateScalar) L.G = take(bh * nt * C * 4);
   if (gate == kGateChannel) L.G = take(bh * nt * C * dk * 4);
   if (precond == kATQ) L.Qt = take(bh * nt * C * dk * esz);
+  if (gate == kGateChannel) {
+    L.QL = take(bh * nt * C * dk * esz);
+    L.KL = take(bh * nt * C * dk * esz);
+  }
   L.total = off;
   return L;
 }

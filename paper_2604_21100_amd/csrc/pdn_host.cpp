@@ -193,6 +193,10 @@ pdn_status pdn_workspace_size(const pdn_problem* p, int with_bwd, size_t* bytes)
 // plus the residual arrays of the backward layout.
 static void set_forward_ws(pdn::FwdArgs& a, const pdn::WsLayout& L, const pdn_problem* p, char* w) {
   if (p->precond == PDN_PRECOND_ATQ) a.Qt = w + L.Qt;
+  if (p->gate == PDN_GATE_CHANNEL) {
+    a.QL = w + L.QL;
+    a.KL = w + L.KL;
+  }
   if (pdn::has_gram(p->precond)) {
     a.sumL = reinterpret_cast<float*>(w + L.sumL);
     a.sumD = reinterpret_cast<float*>(w + L.sumD);

@@ -57,6 +57,8 @@ struct FwdArgs {
   void* Pm;       // [BH, NT, C, C]  causal (Q*Lam)(Kt/Lam)^T, io dtype
   float* G;       // [BH, Tpad] or [BH, Tpad, dk] in-chunk log-decay prefix
   void* Qt;       // [BH, Tpad, dk] io   ATQ: preconditioned query rows q / (A + ridge)
+  void* QL;       // [BH, Tpad, dk] io   per-channel gate: Lam o (the query the scan reads)
+  void* KL;       // [BH, Tpad, dk] io   per-channel gate: Lam o K
   // backward only (NULL in the forward): forward intermediates kept for the
   // adjoint kernels.  lam_r = exp(G_r), w_r = exp(G_{C-1} - G_r).
   void* Hs;       // [BH, NT, dk, dv] io  chunk-start states S^T
@@ -97,7 +99,7 @@ struct BwdArgs {
 };
 
 struct WsLayout {
-  size_t sumL, sumD, Abound, KtG, Tm, Pm, G, Qt, total;
+  size_t sumL, sumD, Abound, KtG, Tm, Pm, G, Qt, QL, KL, total;
 };
 
 WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precond);
