@@ -353,6 +353,37 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
 }
 
 // ------------------------------------------------------------ p1
+// stage_rows in two halves, so the loads can be issued early and other work
+// done before the LDS store waits for them
+template <typename T, int DD>
+struct RowStage {
+  static constexpr int kVec = 16 / static_cast<int>(sizeof(T)), kVpr = DD / kVec;
+  static constexpr int kPer = C * kVpr / 256;
+  static_assert(C * kVpr % 256 == 0 && kPer >= 1 && kPer <= 4, "one to four vectors per thread");
+  float4 v0, v1, v2, v3;   // named registers: a private array here is placed in memory
+  __device__ __forceinline__ void load(const T* src, int tid) {
+    auto get = [&](int j, float4& x) {
+      const int idx = tid + 256 * j, r = idx / kVpr, cv = idx % kVpr;
+      x = *reinterpret_cast<const float4*>(src + r * DD + cv * kVec);
+    };
+    get(0, v0);
+    if constexpr (kPer > 1) get(1, v1);
+    if constexpr (kPer > 2) get(2, v2);
+    if constexpr (kPer > 3) get(3, v3);
+  }
+  __device__ __forceinline__ void store(T* dst, int tid) const {
+    constexpr int LD = DD + 8;
+    auto put = [&](int j, float4 x) {
+      const int idx = tid + 256 * j, r = idx / kVpr, cv = idx % kVpr;
+      *reinterpret_cast<float4*>(sw(dst, LD, r, cv * kVec)) = x;
+    };
+    put(0, v0);
+    if constexpr (kPer > 1) put(1, v1);
+    if constexpr (kPer > 2) put(2, v2);
+    if constexpr (kPer > 3) put(3, v3);
+  }
+};
+
 // Rows [C][DD] of a workspace tensor -> LDS rows [C][DD + 8] (16-byte copies,
 // bank-spread addressing: read back through sw())
 template <typename T, int DD>
@@ -550,9 +581,12 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   Frag8<T> fV[KV], fQ[KD], fK[KD];    // phase A only
   const T* dob = static_cast<const T*>(ba.dO) + (b * a.T + t0) * HV + h * DV;
   const T* eb = static_cast<const T*>(a.Er) + rv;
+  // phase A's loads in two groups: the Gram products' operands (q, k rows,
+  // the Kt tile) first, then dO, V, Z rows and the E tile, which stay in
+  // flight while the Gram products run
+  RowStage<T, DK> stKt;
+  RowStage<T, DV> stE;
   {
-    const T* vb = static_cast<const T*>(a.v) + (b * a.T + t0) * HV + h * DV;
-    const T* zb = static_cast<const T*>(ba.Zr) + rv;
     const T* qb = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
     const T* kb = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
 #pragma unroll
@@ -561,6 +595,9 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       fQ[kk] = ld8(at_bytes(qb, o));
       fK[kk] = ld8(at_bytes(kb, o));
     }
+    stKt.load(static_cast<const T*>(a.Ktr) + rk, tid);
+    const T* vb = static_cast<const T*>(a.v) + (b * a.T + t0) * HV + h * DV;
+    const T* zb = static_cast<const T*>(ba.Zr) + rv;
 #pragma unroll
     for (int kk = 0; kk < KV; ++kk) {
       const uint32_t o = (rc * static_cast<uint32_t>(HV) + 32 * kk + 8 * lg) * E;
@@ -569,14 +606,32 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       fV[kk] = ld8(at_bytes(vb, o));
       fZ[kk] = ld8(at_bytes(zb, ow));
     }
+    stE.load(eb, tid);
   }
-  // ---- phase A: shared B operands (E, Kt rows) and per-row scalars
-  stage_rows<T, DV>(sE, eb, tid);
-  stage_rows<T, DK>(sKt, static_cast<const T*>(a.Ktr) + rk, tid);
+  // ---- phase A: shared B operands (Kt now, E after the Gram products) and
+  // per-row scalars
+  stKt.store(sKt, tid);
   if (tid < C) {
     sG[tid] = GATE == kGateScalar ? a.G[bh * a.Tpad + t0 + tid] : 0.f;
     sBeta[tid] = tid < n ? a.beta[(b * a.T + t0 + tid) * a.H + h] : 0.f;
   }
+  __syncthreads();
+  // the Gram products (Q and K rows die here)
+  floatx4 Sqk[4], Skk[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    Sqk[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    Skk[j] = Sqk[j];
+    if (j <= w) {
+#pragma unroll
+      for (int kk = 0; kk < KD; ++kk) {
+        const Frag8<T> fk = ld8(sw(sKt, LDK, 16 * j + lr, 32 * kk + 8 * lg));
+        mma(Sqk[j], fQ[kk], fk);
+        mma(Skk[j], fK[kk], fk);
+      }
+    }
+  }
+  stE.store(sE, tid);
   __syncthreads();
   {
     // Z_r . V_r for row ra (Z vanishes on rows past the end)
@@ -590,22 +645,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
     if (lg == 0) sZV[ra] = zv;
   }
   {
-    // the Gram products first (Q and K rows die here), then dP and dL tile
-    // by tile straight into the elementwise algebra
-    floatx4 Sqk[4], Skk[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      Sqk[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-      Skk[j] = Sqk[j];
-      if (j <= w) {
-#pragma unroll
-        for (int kk = 0; kk < KD; ++kk) {
-          const Frag8<T> fk = ld8(sw(sKt, LDK, 16 * j + lr, 32 * kk + 8 * lg));
-          mma(Sqk[j], fQ[kk], fk);
-          mma(Skk[j], fK[kk], fk);
-        }
-      }
-    }
+    // dP and dL tile by tile straight into the elementwise algebra
     float dbA[4] = {0.f, 0.f, 0.f, 0.f}, rs[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
