@@ -631,6 +631,19 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       }
     }
   }
+  // phase B's first state rows: in flight through the rest of phase A
+  StateRows<T, HC, DV> srows;
+  srows.load(static_cast<const T*>(a.Hs) + cs, static_cast<const T*>(ba.dHs) + cs, tid);
+  // and its transposed write-key, query and key tiles
+  const T* qtile = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
+  const T* ktile = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
+  const T* kttile = static_cast<const T*>(a.Ktr) + rk;
+  // (the tiles of two passes at a time: whole lines)
+  static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
+  HeldTile<T, HC> tKt, tQ, tK, hKt, hQ, hK;
+  load_pair_regs<T, HC>(tKt, hKt, kttile, DK, C, tid);
+  load_pair_regs<T, HC>(tQ, hQ, qtile, HD, n, tid);
+  load_pair_regs<T, HC>(tK, hK, ktile, HD, n, tid);
   stE.store(sE, tid);
   __syncthreads();
   {
@@ -700,19 +713,6 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       }
     }
   }
-  // phase B's first state rows: in flight through the rest of phase A
-  StateRows<T, HC, DV> srows;
-  srows.load(static_cast<const T*>(a.Hs) + cs, static_cast<const T*>(ba.dHs) + cs, tid);
-  // and its transposed write-key, query and key tiles
-  const T* qtile = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
-  const T* ktile = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
-  const T* kttile = static_cast<const T*>(a.Ktr) + rk;
-  // (the tiles of two passes at a time: whole lines)
-  static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
-  HeldTile<T, HC> tKt, tQ, tK, hKt, hQ, hK;
-  load_pair_regs<T, HC>(tKt, hKt, kttile, DK, C, tid);
-  load_pair_regs<T, HC>(tQ, hQ, qtile, HD, n, tid);
-  load_pair_regs<T, HC>(tK, hK, ktile, HD, n, tid);
   // E rows of this wave (phase B's A operand of A3), from the staged copy
 #pragma unroll
   for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, ra, 32 * kk + 8 * lg));
