@@ -976,7 +976,22 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
     zv += __shfl_xor(zv, 32, 64);
     if (lg == 0) sZV[ra] = zv;
   }
-  stage_rows<T, DV>(sE, static_cast<const T*>(a.Er) + rv, tid);
+  RowStage<T, DV> stE;
+  stE.load(static_cast<const T*>(a.Er) + rv, tid);
+  // phase B's first state rows: in flight through the rest of phase A
+  StateRows<T, HC, DV> srows;
+  srows.load(static_cast<const T*>(a.Hs) + cs, static_cast<const T*>(ba.dHs) + cs, tid);
+  // and its transposed write-key, query and key tiles
+  const T* qtile = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
+  const T* ktile = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
+  const T* kttile = static_cast<const T*>(a.Ktr) + rk;
+  // (the tiles of two passes at a time: whole lines)
+  static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
+  HeldTile<T, HC> tKt, tQ, tK, hKt, hQ, hK;
+  load_pair_regs<T, HC>(tKt, hKt, kttile, DK, C, tid);
+  load_pair_regs<T, HC>(tQ, hQ, qtile, HD, n, tid);
+  load_pair_regs<T, HC>(tK, hK, ktile, HD, n, tid);
+  stE.store(sE, tid);
   if (tid < C) sBeta[tid] = tid < n ? a.beta[(b * a.T + t0 + tid) * a.H + h] : 0.f;
   __syncthreads();
   // ---- phase A: dSqk = causal(dO_s E^T), dAt = strict_lower(-Z E^T)
@@ -1004,19 +1019,6 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
     st4<T>(sw(sSqT, LDT, 16 * j + lr, 16 * w + 4 * lg), dq[0], dq[1], dq[2], dq[3]);
     st4<T>(sw(sSkT, LDT, 16 * j + lr, 16 * w + 4 * lg), dAb[0], dAb[1], dAb[2], dAb[3]);
   }
-  // phase B's first state rows: in flight through the rest of phase A
-  StateRows<T, HC, DV> srows;
-  srows.load(static_cast<const T*>(a.Hs) + cs, static_cast<const T*>(ba.dHs) + cs, tid);
-  // and its transposed write-key, query and key tiles
-  const T* qtile = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
-  const T* ktile = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
-  const T* kttile = static_cast<const T*>(a.Ktr) + rk;
-  // (the tiles of two passes at a time: whole lines)
-  static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
-  HeldTile<T, HC> tKt, tQ, tK, hKt, hQ, hK;
-  load_pair_regs<T, HC>(tKt, hKt, kttile, DK, C, tid);
-  load_pair_regs<T, HC>(tQ, hQ, qtile, HD, n, tid);
-  load_pair_regs<T, HC>(tK, hK, ktile, HD, n, tid);
 #pragma unroll
   for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, ra, 32 * kk + 8 * lg));
   __syncthreads();
