@@ -1221,8 +1221,8 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
 // inj_t = (dB/dA)(A_t) (dkt_t o k_t).  Chunk-parallel in three passes:
 // pc_chunk<false> computes each chunk's local adjoint (zero carry), pc_carry
 // chains the chunks (adjoint entering each chunk from the right), and
-// pc_chunk<true> recomputes with the carry and writes dk, dbetaP, dgP and the
-// partial d mu.
+// pc_chunk<true> runs the exact recurrences and writes dk, dbetaP, dgP and
+// the partial d mu.
 // Sum of each of 16 per-row values over the 64 lanes of a wave; lane l
 // returns the total of value l >> 2.  Static indices only: a per-lane
 // choice between array elements gets merged into a runtime index by the
@@ -1260,15 +1260,18 @@ __device__ __forceinline__ float pc_wave_sum16(const float (&v)[16], int l) {
 // contiguous wave access (256 bytes for d_k = 128 in bf16) straight from
 // HBM, all of a segment's rows in flight at once, and a token's sums over
 // channels are reductions within one wave.  Both recurrences are
-// first-order linear with a per-token factor aP_r shared by all channels,
-// so each segment scans from zero and a short composition through LDS
-// supplies the exact value entering it:
+// first-order linear with a per-token factor aP_r shared by all channels.
+// The summary pass (FINAL = false) scans each segment from zero and
+// composes the segments through LDS:
 //   forward  A_r = Ahat_r + (prod_{s0 <= j <= r} aP_j) A_in
-//   reverse  D_r = Dhat_r + (prod_{r < j <= s0 + G - 1} aP_j) kappa
-// (s0 the segment's first token, A_in the preconditioner state before it,
-// kappa the adjoint entering it from the right, already times aP of the
-// next token).  The per-token products come from the in-chunk prefix of gP.
-// Loop bodies are branch-free.
+//   reverse  send = aP_{s0} Dhat_{s0}   (what the segment sends left)
+// (s0 the segment's first token, A_in the preconditioner state before it).
+// It stores every segment's A_in and send; the final pass starts each
+// segment from its exact A_in and from the exact adjoint entering it from
+// the right (the chunk carry composed with the later segments' sends), so
+// it runs one forward and one reverse recurrence and writes its outputs as
+// the reverse one goes.  The per-token products come from the in-chunk
+// prefix of gP.  Loop bodies are branch-free.
 constexpr int PCG = 16;   // tokens per segment (one wave sum of 16 values)
 constexpr int PCS = C / PCG;
 
@@ -1277,12 +1280,102 @@ struct alignas(sizeof(T) * N) PcPack {
   T x[N];
 };
 
+// Pins a packed row fragment to this point of the program, so that its
+// unpacking is redone here instead of the unpacked values being kept alive
+// from an earlier use (twice the registers).
+template <typename P>
+__device__ __forceinline__ P pc_pin(P p) {
+  if constexpr (sizeof(P) % 4 == 0) {
+    uint32_t u[sizeof(P) / 4];
+    __builtin_memcpy(u, &p, sizeof(P));
+#pragma unroll
+    for (int i = 0; i < static_cast<int>(sizeof(P) / 4); ++i) asm volatile("" : "+v"(u[i]));
+    __builtin_memcpy(&p, u, sizeof(P));
+  }
+  return p;
+}
+
+// A wave-uniform value (here a per-token factor read from LDS) moved to a
+// scalar register: held in a vector register for every token of a segment
+// it would cost one register per token.
+__device__ __forceinline__ float pc_uni(float x) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
+}
+
+// CPL values rounded to the row type; a bf16 pair is one packed conversion.
+template <typename T, int N>
+__device__ __forceinline__ PcPack<T, N> pc_pack(const float (&x)[N]) {
+  PcPack<T, N> o;
+  if constexpr (sizeof(T) == 2 && N == 2) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef T t16x2 __attribute__((ext_vector_type(2)));
+    const f32x2 f = {x[0], x[1]};
+    const t16x2 v = __builtin_convertvector(f, t16x2);
+    __builtin_memcpy(&o, &v, sizeof(o));
+  } else {
+#pragma unroll
+    for (int q = 0; q < N; ++q) o.x[q] = from_f<T>(x[q]);
+  }
+  return o;
+}
+
+// Stores a 2, 4 or 8 byte row fragment through a raw buffer resource.
+// Offsets at or past the resource's byte range are dropped by the
+// hardware's range check (no branch, so no per-row control flow for the
+// compiler to schedule around).
+template <typename P>
+__device__ __forceinline__ void pc_store(__amdgpu_buffer_rsrc_t r, uint32_t off, const P& v) {
+  if constexpr (sizeof(P) == 2) {
+    unsigned short u;
+    __builtin_memcpy(&u, &v, 2);
+    __builtin_amdgcn_raw_buffer_store_b16(u, r, static_cast<int>(off), 0, 0);
+  } else if constexpr (sizeof(P) == 4) {
+    unsigned u;
+    __builtin_memcpy(&u, &v, 4);
+    __builtin_amdgcn_raw_buffer_store_b32(u, r, static_cast<int>(off), 0, 0);
+  } else {
+    static_assert(sizeof(P) == 8, "row fragment of 2, 4 or 8 bytes");
+    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+    u32x2 u;
+    __builtin_memcpy(&u, &v, 8);
+    __builtin_amdgcn_raw_buffer_store_b64(u, r, static_cast<int>(off), 0, 0);
+  }
+}
+
+// The adjoint injection at one token and channel, divided by -log x:
+//   (dB/dA)(A) (dkt o k) / (-log x) = B(A) / A * s'(rho) dkt k,
+// B(A) = exp(-log x s(rho)), rho = log A - mu, s = rho / (1 + |rho|),
+// s' = 1 / (1 + |rho|)^2; zero where A <= 0 (B = x there, constant).
+// B(A) / A is one exp2 of (-log x log2 e) s - log2 A.  Returns the
+// injection and sets BoA = B(A) / A (finite for A > 0).
+struct PcInj {
+  float inj, BoA;
+};
+__device__ __forceinline__ PcInj pc_injection(float Ar, float gk, float kv, float mu, float nlx2) {
+  // max(A, 1e-30) as an integer max: positive floats order as their bits,
+  // and every A <= 0 (sign bit set, or +0) maps to the bound
+  const float Ac = __int_as_float(max(__float_as_int(Ar), __float_as_int(1e-30f)));
+  const float l2 = __builtin_amdgcn_logf(Ac);
+  const float rr = fmaf(l2, kLn2, -mu);
+  const float qd = fast_rcp(1.f + fabsf(rr));
+  const float BoA = exp2_hw(fmaf(rr * qd, nlx2, -l2));
+  PcInj r;
+  r.inj = Ar > 0.f ? BoA * (gk * kv) * (qd * qd) : 0.f;
+  r.BoA = BoA;
+  return r;
+}
+
 template <typename T, int DK, bool FINAL>
 __global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
   constexpr int CPL = DK / 64;
-  using Pk = PcPack<T, CPL>;
-  __shared__ float sEgp[C], sBp[C], sFf[C], sBf[C];
-  __shared__ float sEnd[PCS][DK];          // per-segment end values (A, then adjoint)
+  using Pk = PcPack<float, CPL>;
+  using Pt = PcPack<T, CPL>;
+  __shared__ float sEgp[C], sBp[C], sFf[C];
+  __shared__ float sEnd[PCS][DK];          // summary pass: per-segment end values (A, then adjoint)
+  // the states A_r of each wave's segment, read back in the reverse
+  // recurrence (a wave reads only its own rows; kept here rather than in
+  // registers, which leaves room for more waves)
+  __shared__ Pk sA[PCS][PCG][64];
   __shared__ float sMu[PCS];
   const FwdArgs& a = ba.f;
   const int64_t blk = blockIdx.x;
@@ -1300,23 +1393,30 @@ __global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
   const T* kb = static_cast<const T*>(a.k) + ((b * a.T + t0) * a.H + h) * DK;
   const T* gb = static_cast<const T*>(ba.dKt) + (bh * a.Tpad + t0) * DK;
   const T* mb = static_cast<const T*>(ba.dKm) + (bh * a.Tpad + t0) * DK;
+  // per-segment values of this chunk: [BH, NT, PCS, DK]
+  const int64_t segb = ((bh * a.NT + i) * PCS) * DK;
   // every row of the segment in flight first; rows past the sequence end
   // re-read the last row (keys are zeroed at use, dkt and dkm rows there are
   // zero)
-  Pk kr[PCG], gr[PCG], mr[FINAL ? PCG : 1];
+  Pt kr[PCG], gr[PCG], mr[FINAL ? PCG : 1];
 #pragma unroll
   for (int j = 0; j < PCG; ++j) {
     const uint32_t rr = static_cast<uint32_t>(min(s0 + j, n - 1));
     const uint32_t ow = static_cast<uint32_t>((s0 + j) * DK) * E + lo;
-    kr[j] = *reinterpret_cast<const Pk*>(at_bytes(kb, rr * kstb + lo));
-    gr[j] = *reinterpret_cast<const Pk*>(at_bytes(gb, ow));
-    if (FINAL) mr[j] = *reinterpret_cast<const Pk*>(at_bytes(mb, ow));
+    kr[j] = *reinterpret_cast<const Pt*>(at_bytes(kb, rr * kstb + lo));
+    gr[j] = *reinterpret_cast<const Pt*>(at_bytes(gb, ow));
   }
-  float A_start[CPL], kap_chunk[CPL];
+  // FINAL: the exact state before the segment and the adjoints the later
+  // segments send (zero carry), then the chunk's carry from the right
+  Pk A_seg, S_seg[PCS - 1], kap_chunk;
+  if (FINAL) {
+    A_seg = *reinterpret_cast<const Pk*>(ba.pcA + segb + w * DK + c0);
 #pragma unroll
-  for (int q = 0; q < CPL; ++q) {
-    A_start[q] = a.Abound[(bh * (a.NT + 1) + i) * DK + c0 + q];
-    kap_chunk[q] = FINAL ? ba.pcC[(bh * (a.NT + 1) + i + 1) * DK + c0 + q] : 0.f;
+    for (int s = 1; s < PCS; ++s)
+      if (s > w) S_seg[s - 1] = *reinterpret_cast<const Pk*>(ba.pcS + segb + s * DK + c0);
+    kap_chunk = *reinterpret_cast<const Pk*>(ba.pcC + (bh * (a.NT + 1) + i + 1) * DK + c0);
+  } else {
+    A_seg = *reinterpret_cast<const Pk*>(a.Abound + (bh * (a.NT + 1) + i) * DK + c0);
   }
   if (tid < C) {
     // per-token factors; padded tokens: aP = 1 (gP = 0), bP = 0; x is the
@@ -1332,127 +1432,155 @@ __global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
       const float y = __shfl_up(x, off, 64);
       if (tid >= off) x += y;
     }
-    // segment composition factors:
-    //   forward  prod_{s0 <= j <= r} aP_j,   reverse  prod_{r < j < s0 + G} aP_j
+    // segment composition factor prod_{s0 <= j <= r} aP_j
     const int q0 = tid & ~(PCG - 1);
-    const float gb = __shfl(x, q0 - 1, 64), ge = __shfl(x, q0 + PCG - 1, 64);
+    const float gb = __shfl(x, q0 - 1, 64);
     sFf[tid] = fast_exp(x - (q0 > 0 ? gb : 0.f));
-    sBf[tid] = fast_exp(ge - x);
   }
+  if (s0 + PCG > n) {   // wave-uniform: only the last chunk's tail segments
 #pragma unroll
-  for (int j = 0; j < PCG; ++j)
+    for (int j = 0; j < PCG; ++j)
 #pragma unroll
-    for (int q = 0; q < CPL; ++q)
-      if (s0 + j >= n) kr[j].x[q] = from_f<T>(0.f);   // keys past the end are zero
+      for (int q = 0; q < CPL; ++q)
+        if (s0 + j >= n) kr[j].x[q] = from_f<T>(0.f);   // keys past the end are zero
+  }
   __syncthreads();
-  // ---- forward: local scan from zero, then the exact state entering
-  float A[CPL][PCG];
+  // ---- forward: the summary pass scans from zero and composes the
+  // segments; the final pass starts from the stored exact state
+  // (summary pass: these are the states from zero, Ahat; the reverse
+  // recurrence adds the composition term as it reads them)
+  float A_in[CPL];
+  {
+    Pk x;
 #pragma unroll
-  for (int q = 0; q < CPL; ++q) {
-    float x = 0.f;
+    for (int q = 0; q < CPL; ++q) x.x[q] = FINAL ? A_seg.x[q] : 0.f;
 #pragma unroll
     for (int j = 0; j < PCG; ++j) {
-      const float kv = to_f(kr[j].x[q]);
-      x = sEgp[s0 + j] * x + sBp[s0 + j] * kv * kv;
-      A[q][j] = x;
-    }
-    sEnd[w][c0 + q] = x;
-  }
-  __syncthreads();
-  float A_in[CPL];
 #pragma unroll
-  for (int q = 0; q < CPL; ++q) {
-    float x = A_start[q];
-    for (int s = 0; s < w; ++s) x = sEnd[s][c0 + q] + sFf[PCG * s + PCG - 1] * x;   // segment product
-    A_in[q] = x;
-#pragma unroll
-    for (int j = 0; j < PCG; ++j) A[q][j] += sFf[s0 + j] * x;
-  }
-  // ---- reverse: local adjoint from zero; the gain terms need no D.  The
-  // adjoint is carried divided by -log x (every injection has that factor
-  // and the recurrence is linear), here, in the chunk summaries and in the
-  // carries; it is applied where values leave: dk, dbetaP, dgP, d mu, dA0.
-  const float mu = fast_exp(a.log_a_scale[h]);
-  const float nlx = -a.lnx, nlx2 = nlx * kLog2e;
-  float Dh[CPL][PCG];
-  float muPart = 0.f, send[CPL];
-#pragma unroll
-  for (int q = 0; q < CPL; ++q) {
-    float D = 0.f, aNext = 1.f;
-#pragma unroll
-    for (int j = PCG - 1; j >= 0; --j) {
-      const float Ar = A[q][j];
-      const float gk = to_f(gr[j].x[q]);
-      // B(A) = exp(-lnx s(rho)), rho = log A - mu, s = rho / (1 + |rho|):
-      // dB/dA = -lnx B / ((1 + |rho|)^2 A); zero where A <= 0 (B = x there)
-      const bool pos = Ar > 0.f;
-      const float rr = fast_log(fmaxf(Ar, 1e-30f)) - mu;
-      const float qd = fast_rcp(1.f + fabsf(rr));
-      const float Bv = exp2_hw(nlx2 * (pos ? rr * qd : -1.f));
-      const float bg = Bv * gk;
-      const float dr = pos ? bg * to_f(kr[j].x[q]) * qd * qd : 0.f;   // / (-lnx)
-      D = dr * fast_rcp(fmaxf(Ar, 1e-30f)) + aNext * D;
-      aNext = sEgp[s0 + j];
-      Dh[q][j] = D;
-      if (FINAL) {   // dk's terms without D, in place of dKm
-        muPart -= dr;
-        mr[j].x[q] = from_f<T>(to_f(mr[j].x[q]) + bg);
+      for (int q = 0; q < CPL; ++q) {
+        const float kv = to_f(kr[j].x[q]);
+        x.x[q] = fmaf(sEgp[s0 + j], x.x[q], sBp[s0 + j] * (kv * kv));
       }
+      sA[w][j][l] = x;
     }
-    send[q] = aNext * D;   // aP_{s0} Dhat_{s0}: what this segment sends left
-  }
-  __syncthreads();   // every wave is done with sEnd (forward)
 #pragma unroll
-  for (int q = 0; q < CPL; ++q) sEnd[w][c0 + q] = send[q];
-  __syncthreads();
-  // adjoint entering this segment from the right
-  float kap[CPL];
-#pragma unroll
-  for (int q = 0; q < CPL; ++q) {
-    float x = kap_chunk[q];
-    for (int s = PCS - 1; s > w; --s) x = sEnd[s][c0 + q] + sFf[PCG * s + PCG - 1] * x;
-    kap[q] = x;
+    for (int q = 0; q < CPL; ++q) {
+      if (!FINAL) sEnd[w][c0 + q] = x.x[q];
+      A_in[q] = A_seg.x[q];
+    }
   }
   if (!FINAL) {
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      float x = A_seg.x[q];
+      for (int s = 0; s < w; ++s) x = sEnd[s][c0 + q] + sFf[PCG * s + PCG - 1] * x;   // segment product
+      A_in[q] = x;
+    }
+    Pk st;
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) st.x[q] = A_in[q];
+    *reinterpret_cast<Pk*>(ba.pcA + segb + w * DK + c0) = st;
+  }
+  // ---- reverse.  The adjoint is carried divided by -log x (every
+  // injection has that factor and the recurrence is linear), here, in the
+  // segment and chunk summaries and in the carries; it is applied where
+  // values leave: dk, dbetaP, dgP, d mu, dA0.
+  const float mu = fast_exp(a.log_a_scale[h]);
+  const float nlx = -a.lnx, nlx2 = nlx * kLog2e;
+  if (!FINAL) {
+    // local adjoint from zero; only what the segment sends left is kept
+    Pk send;
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      float D = 0.f, aNext = 1.f;
+#pragma unroll
+      for (int j = PCG - 1; j >= 0; --j) {
+        const float Ar = fmaf(sFf[s0 + j], A_in[q], sA[w][j][l].x[q]);
+        const PcInj r = pc_injection(Ar, to_f(gr[j].x[q]), to_f(kr[j].x[q]), mu, nlx2);
+        D = fmaf(aNext, D, r.inj);
+        aNext = sEgp[s0 + j];
+      }
+      send.x[q] = aNext * D;   // aP_{s0} Dhat_{s0}
+    }
+    *reinterpret_cast<Pk*>(ba.pcS + segb + w * DK + c0) = send;
+    __syncthreads();   // every wave is done with sEnd (forward)
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) sEnd[w][c0 + q] = send.x[q];
+    __syncthreads();
     // the adjoint this chunk sends to the left, with zero carry: aP_0 D_0
     if (w == 0)
 #pragma unroll
-      for (int q = 0; q < CPL; ++q) ba.pcL[(bh * a.NT + i) * DK + c0 + q] = sEnd[0][c0 + q] + sFf[PCG - 1] * kap[q];
+      for (int q = 0; q < CPL; ++q) {
+        float x = 0.f;
+        for (int s = PCS - 1; s >= 0; --s) x = sEnd[s][c0 + q] + sFf[PCG * s + PCG - 1] * x;
+        ba.pcL[(bh * a.NT + i) * DK + c0 + q] = x;
+      }
     return;
   }
-  // ---- outputs: dk = dKm + B dkt + 2 bP k D; per token the sums over
-  // channels of D k^2 and D A_{r-1}
-  float sr[PCG];
-  T* dkb = static_cast<T*>(ba.dk) + ((b * a.T + t0) * a.H + h) * DK;
+  // ---- final: the exact adjoint entering this segment from the right,
+  // then one reverse recurrence writing dk = dKm + B dkt + 2 bP k D (times
+  // the -log x the adjoint is kept divided by) and, per token, the sums
+  // over channels of D k^2 and D A_{r-1}
+  float D[CPL];
 #pragma unroll
-  for (int j = 0; j < PCG; ++j) {
-    Pk o;
-    sr[j] = 0.f;
-    const float f2 = 2.f * nlx * sBp[s0 + j];
+  for (int q = 0; q < CPL; ++q) {
+    float x = kap_chunk.x[q];
+#pragma unroll
+    for (int s = PCS - 1; s >= 1; --s)
+      if (s > w) x = S_seg[s - 1].x[q] + sFf[PCG * s + PCG - 1] * x;
+    D[q] = x;
+  }
+  // the read-key gradient rows are needed only here (fewer registers held
+  // through the forward recurrence)
+  // (the lane offset is pinned here too, or the compiler forms the sixteen
+  // addresses before the forward recurrence and holds them through it; the
+  // rows are steps of one pointer, so they become immediate offsets)
+  const Pt* mrow = reinterpret_cast<const Pt*>(at_bytes(mb + s0 * DK, pc_pin(lo)));
+#pragma unroll
+  for (int j = 0; j < PCG; ++j) mr[j] = mrow[j * (DK / CPL)];
+  const float xB = exp2_hw(-nlx2);   // B where A <= 0: x
+  float sb[PCG], sg[PCG];
+  float muPart = 0.f;
+  T* dkb = static_cast<T*>(ba.dk) + ((b * a.T + t0) * a.H + h) * DK;
+  // this (b, h, chunk)'s dk rows as a raw buffer ending with row n - 1:
+  // a row r >= n starts at r kstb >= (n - 1) kstb + DK E, past the range
+  const __amdgpu_buffer_rsrc_t dkr = __builtin_amdgcn_make_buffer_rsrc(
+      dkb, 0, static_cast<int>((n - 1) * kstb + DK * E), kBufWord3);
+  Pk Acur = sA[w][PCG - 1][l];
+#pragma unroll
+  for (int j = PCG - 1; j >= 0; --j) {
+    const float f2 = 2.f * nlx * pc_uni(sBp[s0 + j]);
+    const float aNext = j < PCG - 1 ? pc_uni(sEgp[s0 + j + 1]) : 1.f;
+    Pk Aprev;
+    if (j > 0) Aprev = sA[w][j - 1][l];
+    else
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) Aprev.x[q] = A_in[q];
+    float o[CPL];
+    const Pt kj = pc_pin(kr[j]);
 #pragma unroll
     for (int q = 0; q < CPL; ++q) {
-      const float kv = to_f(kr[j].x[q]);
-      const float D = Dh[q][j] + sBf[s0 + j] * kap[q];   // / (-lnx)
-      o.x[q] = from_f<T>(to_f(mr[j].x[q]) + f2 * kv * D);
-      sr[j] += D * kv * kv;
-      Dh[q][j] = D;
+      const float Ar = Acur.x[q], kv = to_f(kj.x[q]), gk = to_f(gr[j].x[q]);
+      const PcInj r = pc_injection(Ar, gk, kv, mu, nlx2);
+      D[q] = fmaf(aNext, D[q], r.inj);
+      const float Bv = Ar > 0.f ? r.BoA * Ar : xB;
+      muPart = fmaf(-r.inj, Ar, muPart);   // -dB/dmu term: -(injection) A
+      o[q] = fmaf(f2 * kv, D[q], fmaf(Bv, gk, to_f(mr[j].x[q])));
+      sb[j] = q == 0 ? D[q] * (kv * kv) : fmaf(D[q], kv * kv, sb[j]);
+      sg[j] = q == 0 ? D[q] * Aprev.x[q] : fmaf(D[q], Aprev.x[q], sg[j]);
     }
-    if (s0 + j < n) *reinterpret_cast<Pk*>(at_bytes(dkb, static_cast<uint32_t>(s0 + j) * kstb + lo)) = o;
+    Acur = Aprev;
+    pc_store(dkr, static_cast<uint32_t>(s0 + j) * kstb + lo, pc_pack<T, CPL>(o));
   }
   // lane 4 j carries token s0 + j's sums
   const int jl = l >> 2;
   const int64_t sidx = (b * a.T + t0 + s0 + jl) * a.H + h;
   const bool tok = (l & 3) == 0 && s0 + jl < n;
-  const float sb = pc_wave_sum16(sr, l);
-  if (tok && ba.dbeta_p) ba.dbeta_p[sidx] = nlx * sb;
-#pragma unroll
-  for (int j = 0; j < PCG; ++j) {
-    sr[j] = 0.f;
-#pragma unroll
-    for (int q = 0; q < CPL; ++q) sr[j] += Dh[q][j] * (j > 0 ? A[q][j - 1] : A_in[q]);
-  }
-  const float sg = pc_wave_sum16(sr, l);
-  if (tok && ba.dg_p) ba.dg_p[sidx] = nlx * sEgp[s0 + jl] * sg;
+  const float tb = pc_wave_sum16(sb, l);
+  const float tg = pc_wave_sum16(sg, l);
+  if (tok && ba.dbeta_p) ba.dbeta_p[sidx] = nlx * tb;
+  if (tok && ba.dg_p) ba.dg_p[sidx] = nlx * sEgp[s0 + jl] * tg;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) muPart += __shfl_xor(muPart, off, 64);
   if (l == 0) sMu[w] = muPart;
@@ -1557,6 +1685,8 @@ BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate,
   L.dKt = take(bh * tp * dk * esz);
   L.dKm = take(bh * tp * dk * esz);
   L.pcL = take(bh * nt * dk * 4);
+  L.pcS = take(bh * nt * PCS * dk * 4);
+  L.pcA = take(bh * nt * PCS * dk * 4);
   L.pcC = take(bh * (nt + 1) * dk * 4);
   L.pcMu = take(bh * nt * 4);
   L.total = off;

@@ -166,6 +166,10 @@ __device__ __forceinline__ void st_tile_t(T* out, int ld, const floatx4& acc, in
   st4<T>(out + lr * ld + 4 * lg, scale * acc[0], scale * acc[1], scale * acc[2], scale * acc[3]);
 }
 
+// Word 3 of a raw (untyped, unswizzled) buffer resource on gfx9-family
+// chips: a 32-bit data format, which untyped accesses need to be non-zero.
+constexpr int kBufWord3 = 0x00020000;
+
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kLog2e = 1.4426950408889634f;
 __device__ __forceinline__ float fast_exp(float x) { return __expf(x); }

@@ -356,6 +356,8 @@ static pdn_status chunk_bwd_impl(const pdn_problem* p, const pdn_inputs* in, con
   a.dKt = w + L.dKt;
   a.dKm = w + L.dKm;
   a.pcL = reinterpret_cast<float*>(w + L.pcL);
+  a.pcS = reinterpret_cast<float*>(w + L.pcS);
+  a.pcA = reinterpret_cast<float*>(w + L.pcA);
   a.pcC = reinterpret_cast<float*>(w + L.pcC);
   a.pcMu = reinterpret_cast<float*>(w + L.pcMu);
   const hipError_t he = pdn::launch_backward(a, p->io == PDN_BF16, stream, ev, !saved);
