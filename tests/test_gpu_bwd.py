@@ -112,11 +112,23 @@ def test_bwd_small_all_heads(io, gate, precond, dk, dv):
     compare(spec, inp, precond, dS_T, tag=f"{io}/{gate}/{precond}/{dk}x{dv}")
 
 
-@pytest.mark.parametrize("T", [1, 64, 65, 130])
+@pytest.mark.parametrize("T", [1, 64, 65, 80, 114, 127, 130])
 def test_bwd_sequence_lengths(T):
+    """Last chunks of 1, 16 (a whole first segment of 16 tokens), 50 (into
+    the fourth segment) and 63 tokens, and whole chunks."""
     spec = pi.small_spec(T=T, B=1, H=2, gate="scalar", dk=128, dv=128,
                          with_do=True)
     compare(spec, pi.generate(spec, 300 + T), tag=f"T={T}")
+
+
+def test_bwd_zero_key_channels():
+    """Key channels that are exactly zero with a zero initial state keep the
+    preconditioner state at A = 0 there: the squash gain is x and has no
+    derivative (the A <= 0 case of the gain), on both sides."""
+    spec = pi.small_spec(gate="scalar", dk=128, dv=128, with_do=True, a0="zero")
+    inp = pi.generate(spec, 41)
+    inp["k"][..., ::7] = 0.0
+    compare(spec, inp, tag="zero key channels")
 
 
 def test_bwd_beta_range_and_squash_coverage():
@@ -125,7 +137,7 @@ def test_bwd_beta_range_and_squash_coverage():
     compare(spec, pi.generate(spec, 31), tag="beta02/aniso")
 
 
-@pytest.mark.parametrize("T", [1, 65, 130])
+@pytest.mark.parametrize("T", [1, 65, 114, 130])
 def test_bwd_channel_gate_sequence_lengths(T):
     spec = pi.small_spec(T=T, B=1, H=2, gate="channel", dk=128, dv=128,
                          with_do=True)
