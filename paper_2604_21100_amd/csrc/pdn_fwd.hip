@@ -685,6 +685,17 @@ __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdAr
   const T* tb = static_cast<const T*>(a.Tm) + (x.bh * a.NT + i) * (int64_t)(C * C);
   const T* pb = static_cast<const T*>(a.Pm) + (x.bh * a.NT + i) * (int64_t)(C * C);
   const T* gb = static_cast<const T*>(a.KtG) + (x.bh * a.NT + i) * (int64_t)(DK * C);
+  // the value slab first: the step before this chunk's stages it into LDS
+  // and so waits for it a step earlier than for the other operands; the
+  // memory counter completes in issue order, so any load issued before it
+  // would be waited for there too
+#pragma unroll
+  for (int j = 0; j < SM::kPer; ++j) {
+    const int idx = x.tid + 256 * j;
+    const uint32_t row = static_cast<uint32_t>(min(idx / SM::kSegs, last));
+    const uint32_t off = (row * static_cast<uint32_t>(HV) + (idx % SM::kSegs) * SM::kVec) * E;
+    f.v[j] = *reinterpret_cast<const float4*>(at_bytes(vb, off));
+  }
   const uint32_t rr = static_cast<uint32_t>(min(16 * x.w + x.lr, last));
   const uint32_t okq = (rr * static_cast<uint32_t>(ldk) + 8 * x.lg) * E;
   if (LA) {
@@ -711,13 +722,6 @@ __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdAr
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2)
       f.G[ct][k2] = ld8(at_bytes(gb, static_cast<uint32_t>((16 * (x.w * CT + ct) + x.lr) * C + 8 * x.lg + k2 * 32) * E));
-#pragma unroll
-  for (int j = 0; j < SM::kPer; ++j) {
-    const int idx = x.tid + 256 * j;
-    const uint32_t row = static_cast<uint32_t>(min(idx / SM::kSegs, last));
-    const uint32_t off = (row * static_cast<uint32_t>(HV) + (idx % SM::kSegs) * SM::kVec) * E;
-    f.v[j] = *reinterpret_cast<const float4*>(at_bytes(vb, off));
-  }
   if (GATE == kGateScalar) {
     const float* gs = a.G + x.bh * a.Tpad + t0;
 #pragma unroll
@@ -758,7 +762,8 @@ __device__ __forceinline__ void stage_values(const float4 (&v)[SlabMap<T>::kPer]
 }
 
 // sO[v][t] -> o rows of chunk i (coalesced 16-byte stores); n valid rows
-template <typename T>
+// (ALL: the whole chunk, no row check around the stores)
+template <bool ALL, typename T>
 __device__ __forceinline__ void flush_output(const FwdArgs& a, int i, int n, const T* sO,
                                              const ScanCtx& x) {
   using SM = SlabMap<T>;
@@ -775,7 +780,7 @@ __device__ __forceinline__ void flush_output(const FwdArgs& a, int i, int n, con
     T* e = reinterpret_cast<T*>(&pk);
 #pragma unroll
     for (int s = 0; s < SM::kVec; ++s) e[s] = *sw(sO, LDE, c0 + s, row);
-    if (row < n)
+    if (ALL || row < n)
       *reinterpret_cast<float4*>(at_bytes(ob, (static_cast<uint32_t>(row) * static_cast<uint32_t>(HV) + c0) *
                                                   static_cast<uint32_t>(sizeof(T)))) = pk;
   }
@@ -786,12 +791,15 @@ __device__ __forceinline__ void flush_output(const FwdArgs& a, int i, int n, con
 // per-row branches (a conditional store would make the compiler wait for the
 // prefetched loads); the ragged last chunk takes FULL = false.
 // [v][t] (or [v][c]) LDS slab -> rows of a [rows][ld] global tensor: columns
-// x.v0 .. x.v0 + BV of rows 0 .. nrows-1, 16-byte stores
-template <typename T>
-__device__ __forceinline__ void flush_slab_t(T* dst, int64_t ld, const T* src, int lds, int nrows,
-                                             int tid) {
+// x.v0 .. x.v0 + BV of rows 0 .. NROWS-1, 16-byte stores (a fixed count per
+// thread: no loop or branch around the stores inside the scan step)
+template <int NROWS, typename T>
+__device__ __forceinline__ void flush_slab_t(T* dst, int64_t ld, const T* src, int lds, int tid) {
   using SM = SlabMap<T>;
-  for (int idx = tid; idx < nrows * SM::kSegs; idx += 256) {
+  static_assert(NROWS * SM::kSegs % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+  for (int j = 0; j < NROWS * SM::kSegs / 256; ++j) {
+    const int idx = tid + 256 * j;
     const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
     float4 pk;
     T* e = reinterpret_cast<T*>(&pk);
@@ -808,10 +816,10 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
   constexpr int KK = DK / 32, CT = DK / 64;
   constexpr int LDH = DK + 8, LDE = C + 8;
   const int w = x.w, lr = x.lr, lg = x.lg;
-  if (OUT && i > 0) flush_output<T>(a, i - 1, C, sO, x);   // only full chunks precede this one
+  if (OUT && i > 0) flush_output<true, T>(a, i - 1, C, sO, x);   // only full chunks precede this one
   if (SAVE)  // chunk-start state S^T of this chunk, rows c, columns of the slab
-    flush_slab_t<T>(static_cast<T*>(a.Hs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv, sH,
-                    LDH, DK, x.tid);
+    flush_slab_t<DK>(static_cast<T*>(a.Hs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv, sH,
+                     LDH, x.tid);
   float lam[4];
 #pragma unroll
   for (int ii = 0; ii < 4; ++ii) lam[ii] = GATE == kGateScalar ? fast_exp(f.g[ii]) : 1.f;
@@ -860,7 +868,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
   lds_barrier();
   if (SAVE) {  // E rows of this chunk (whole chunk: padded rows included)
     const int64_t r0 = (x.bh * a.Tpad + static_cast<int64_t>(i) * C) * a.dv + x.v0;
-    flush_slab_t<T>(static_cast<T*>(a.Er) + r0, a.dv, sE, LDE, C, x.tid);
+    flush_slab_t<C>(static_cast<T*>(a.Er) + r0, a.dv, sE, LDE, x.tid);
   }
   // ---- O = scale [ (Lam Q) S^T + P E ];  S^T <- Diag(gamma_C) S^T + (Kt Gamma)^T E
   Frag8<T> fE[2][2];
@@ -983,7 +991,7 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   } else if (i < a.NT) {
     scan_step<false, SAVE, OUT, LA>(f0, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
   }
-  if (OUT) flush_output<T>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
+  if (OUT) flush_output<false, T>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
   if (a.S_T) {
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
