@@ -55,18 +55,22 @@ __device__ __forceinline__ void lds_barrier_b() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// [v][t] LDS slab -> rows of a [rows][ld] tensor (16-byte stores), rows < n
-template <typename T>
-__device__ __forceinline__ void slab_to_rows(T* dst, int64_t ld, const T* src, int lds, int nrows,
-                                             int n, int tid) {
+// [v][t] (or [v][c]) LDS slab -> rows 0 .. NROWS-1 of a [rows][ld] tensor
+// (16-byte stores), rows < n unless ALL; a fixed count per thread, so no
+// loop or branch around the stores inside the scan step
+template <int NROWS, bool ALL, typename T>
+__device__ __forceinline__ void slab_to_rows(T* dst, int64_t ld, const T* src, int lds, int n, int tid) {
   using SM = Slab<T>;
-  for (int idx = tid; idx < nrows * SM::kSegs; idx += 256) {
+  static_assert(NROWS * SM::kSegs % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+  for (int j = 0; j < NROWS * SM::kSegs / 256; ++j) {
+    const int idx = tid + 256 * j;
     const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
     float4 pk;
     T* e = reinterpret_cast<T*>(&pk);
 #pragma unroll
     for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = *sw(src, lds, c0 + s2, row);
-    if (row < n) *reinterpret_cast<float4*>(dst + row * ld + c0) = pk;
+    if (ALL || row < n) *reinterpret_cast<float4*>(dst + row * ld + c0) = pk;
   }
 }
 
@@ -195,18 +199,8 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE>& f, bool stage_ne
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int n = FULL ? C : static_cast<int>(min<int64_t>(C, a.T - t0));
   // state adjoint entering this chunk from the right, rows c, slab columns
-  {
-    T* dst = static_cast<T*>(ba.dHs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0;
-    using SM = Slab<T>;
-    for (int idx = x.tid; idx < DK * SM::kSegs; idx += 256) {
-      const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
-      float4 pk;
-      T* e = reinterpret_cast<T*>(&pk);
-#pragma unroll
-      for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = *sw(sH, LDH, c0 + s2, row);
-      *reinterpret_cast<float4*>(dst + row * a.dv + c0) = pk;
-    }
-  }
+  slab_to_rows<DK, true>(static_cast<T*>(ba.dHs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv,
+                         sH, LDH, DK, x.tid);
   // ---- dE = P^T dO_s + Diag(w) Kt dS'^T   (rows t of this wave)
   float wr[4];
 #pragma unroll
@@ -239,10 +233,10 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE>& f, bool stage_ne
   lds_barrier_b();
   {
     const int64_t r0 = (x.bh * a.Tpad + t0) * a.dv + x.v0;
-    slab_to_rows<T>(static_cast<T*>(ba.Zr) + r0, a.dv, sZ, LDE, C, C, x.tid);
+    slab_to_rows<C, true>(static_cast<T*>(ba.Zr) + r0, a.dv, sZ, LDE, C, x.tid);
     const int64_t HV = a.H * (int64_t)a.dv;
-    slab_to_rows<T>(static_cast<T*>(ba.dv) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0, HV, sX, LDE, C,
-                    n, x.tid);
+    slab_to_rows<C, FULL>(static_cast<T*>(ba.dv) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0, HV, sX, LDE,
+                          n, x.tid);
   }
   // ---- dS^T <- Diag(lam_C) dS'^T + (Lam o Q)^T dO_s - (Lam o K)^T dX
   const float gam = GATE == kGateScalar ? fast_exp(f.gC[0][0]) : 1.f;
