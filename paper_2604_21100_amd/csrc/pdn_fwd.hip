@@ -816,10 +816,6 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
   constexpr int KK = DK / 32, CT = DK / 64;
   constexpr int LDH = DK + 8, LDE = C + 8;
   const int w = x.w, lr = x.lr, lg = x.lg;
-  if (OUT && i > 0) flush_output<true, T>(a, i - 1, C, sO, x);   // only full chunks precede this one
-  if (SAVE)  // chunk-start state S^T of this chunk, rows c, columns of the slab
-    flush_slab_t<DK>(static_cast<T*>(a.Hs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv, sH,
-                     LDH, x.tid);
   float lam[4];
 #pragma unroll
   for (int ii = 0; ii < 4; ++ii) lam[ii] = GATE == kGateScalar ? fast_exp(f.g[ii]) : 1.f;
@@ -833,6 +829,12 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt)
     vv[vt] = *reinterpret_cast<const typename Vec4<T>::type*>(sw(sVt, LDE, 16 * vt + lr, 16 * w + 4 * lg));
+  // the flushes' LDS reads go after this phase's operand reads (LDS reads
+  // complete in issue order)
+  if (OUT && i > 0) flush_output<true, T>(a, i - 1, C, sO, x);   // only full chunks precede this one
+  if (SAVE)  // chunk-start state S^T of this chunk, rows c, columns of the slab
+    flush_slab_t<DK>(static_cast<T*>(a.Hs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv, sH,
+                     LDH, x.tid);
   floatx4 accX[2], accO[2];
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt) {
@@ -866,16 +868,16 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
     st4<T>(sw(sE, LDE, 16 * vt + lr, 16 * w + 4 * lg), accE[0], accE[1], accE[2], accE[3]);
   }
   lds_barrier();
-  if (SAVE) {  // E rows of this chunk (whole chunk: padded rows included)
-    const int64_t r0 = (x.bh * a.Tpad + static_cast<int64_t>(i) * C) * a.dv + x.v0;
-    flush_slab_t<C>(static_cast<T*>(a.Er) + r0, a.dv, sE, LDE, x.tid);
-  }
   // ---- O = scale [ (Lam Q) S^T + P E ];  S^T <- Diag(gamma_C) S^T + (Kt Gamma)^T E
   Frag8<T> fE[2][2];
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt)
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) fE[vt][k2] = ld8(sw(sE, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
+  if (SAVE) {  // E rows of this chunk (whole chunk: padded rows included)
+    const int64_t r0 = (x.bh * a.Tpad + static_cast<int64_t>(i) * C) * a.dv + x.v0;
+    flush_slab_t<C>(static_cast<T*>(a.Er) + r0, a.dv, sE, LDE, x.tid);
+  }
 #pragma unroll
   for (int vt = 0; vt < 2 && OUT; ++vt) {
     // P is causal: for rows < 32 its second slab is zero
