@@ -198,20 +198,29 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE>& f, bool stage_ne
   const int w = x.w, lr = x.lr, lg = x.lg;
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int n = FULL ? C : static_cast<int>(min<int64_t>(C, a.T - t0));
-  // state adjoint entering this chunk from the right, rows c, slab columns
-  slab_to_rows<DK, true>(static_cast<T*>(ba.dHs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv,
-                         sH, LDH, DK, x.tid);
   // ---- dE = P^T dO_s + Diag(w) Kt dS'^T   (rows t of this wave)
   float wr[4];
 #pragma unroll
   for (int ii = 0; ii < 4; ++ii) wr[ii] = GATE == kGateScalar ? fast_exp(f.gC[0][0] - f.gw[ii]) : 1.f;
+  Frag8<T> bO[2][2], bS[2][KK];
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt) {
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) bO[vt][k2] = ld8(sw(sDOc, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) bS[vt][kk] = ld8(sw(sH, LDH, 16 * vt + lr, kk * 32 + 8 * lg));
+  }
+  // state adjoint entering this chunk from the right, rows c, slab columns
+  // (its LDS reads after the operand reads: LDS reads complete in issue order)
+  slab_to_rows<DK, true>(static_cast<T*>(ba.dHs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv,
+                         sH, LDH, DK, x.tid);
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt) {
     floatx4 acc = {0.f, 0.f, 0.f, 0.f}, acw = acc;
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Pt[k2], ld8(sw(sDOc, LDE, 16 * vt + lr, k2 * 32 + 8 * lg)));
+    for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Pt[k2], bO[vt][k2]);
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) mma(acw, f.Kw[kk], ld8(sw(sH, LDH, 16 * vt + lr, kk * 32 + 8 * lg)));
+    for (int kk = 0; kk < KK; ++kk) mma(acw, f.Kw[kk], bS[vt][kk]);
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) acc[ii] += wr[ii] * acw[ii];
     st4<T>(sw(sE, LDE, 16 * vt + lr, 16 * w + 4 * lg), acc[0], acc[1], acc[2], acc[3]);
@@ -231,23 +240,21 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE>& f, bool stage_ne
            bt[3] * acc[3]);
   }
   lds_barrier_b();
+  // ---- dS^T <- Diag(lam_C) dS'^T + (Lam o Q)^T dO_s - (Lam o K)^T dX
+  const float gam = GATE == kGateScalar ? fast_exp(f.gC[0][0]) : 1.f;
+  Frag8<T> bX[2][2];
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) bX[vt][k2] = ld8(sw(sX, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
   {
+    // Z and dv rows (their LDS reads after the operand reads)
     const int64_t r0 = (x.bh * a.Tpad + t0) * a.dv + x.v0;
     slab_to_rows<C, true>(static_cast<T*>(ba.Zr) + r0, a.dv, sZ, LDE, C, x.tid);
     const int64_t HV = a.H * (int64_t)a.dv;
     slab_to_rows<C, FULL>(static_cast<T*>(ba.dv) + (x.b * a.T + t0) * HV + x.h * a.dv + x.v0, HV, sX, LDE,
                           n, x.tid);
   }
-  // ---- dS^T <- Diag(lam_C) dS'^T + (Lam o Q)^T dO_s - (Lam o K)^T dX
-  const float gam = GATE == kGateScalar ? fast_exp(f.gC[0][0]) : 1.f;
-  Frag8<T> bD[2][2], bX[2][2];
-#pragma unroll
-  for (int vt = 0; vt < 2; ++vt)
-#pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
-      bD[vt][k2] = ld8(sw(sDOc, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
-      bX[vt][k2] = ld8(sw(sX, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
-    }
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
@@ -258,7 +265,7 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE>& f, bool stage_ne
       }
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
-        mma(st[ct][vt], f.Ql[ct][k2], bD[vt][k2]);
+        mma(st[ct][vt], f.Ql[ct][k2], bO[vt][k2]);
         mma(st[ct][vt], f.Kn[ct][k2], bX[vt][k2]);
       }
       st4<T>(sw(sH, LDH, 16 * vt + lr, 16 * (w * CT + ct) + 4 * lg), st[ct][vt][0], st[ct][vt][1],
