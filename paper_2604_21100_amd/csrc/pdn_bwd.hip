@@ -519,6 +519,38 @@ struct StateRows {
 // past the sequence end re-read the last row: their dP rows are masked,
 // their other products meet a zero factor (Z and beta vanish there), and
 // their outputs are not stored.
+// 16-byte store through a raw buffer resource: offsets at or past its byte
+// range are dropped by the hardware's range check (no branch).
+__device__ __forceinline__ void buf_store16(__amdgpu_buffer_rsrc_t r, uint32_t off, float4 v) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 u;
+  __builtin_memcpy(&u, &v, 16);
+  __builtin_amdgcn_raw_buffer_store_b128(u, r, static_cast<int>(off), 0, 0);
+}
+
+// One wave's 16 output rows x HC columns of dq, dK and dKt, from its LDS
+// staging (the wave reads back only what it wrote: no barrier needed):
+// 16-byte stores, a fixed count per lane.  dq is the chunk's rows of the
+// caller's [B,T,H,dk] tensor as a buffer ending with its last valid row, so
+// rows past the sequence end are dropped; dKm / dKt are padded workspace.
+template <typename T, int HC, int LDO, int DK>
+__device__ __forceinline__ void p12_flush_rows(const T* so, __amdgpu_buffer_rsrc_t dqr, int64_t HD,
+                                               int c0, T* dKm, T* dKt, int w, int l) {
+  constexpr int VEC = 16 / sizeof(T), SPR = HC / VEC;
+  static_assert(16 * SPR % 64 == 0, "whole rounds of the wave");
+#pragma unroll
+  for (int u = 0; u < 16 * SPR / 64; ++u) {
+    const int idx = l + 64 * u;
+    const int rr = idx / SPR, sgc = (idx % SPR) * VEC, r = 16 * w + rr;
+    const float4 vq = *reinterpret_cast<const float4*>(so + rr * LDO + sgc);
+    const float4 vk = *reinterpret_cast<const float4*>(so + (16 + rr) * LDO + sgc);
+    const float4 vt = *reinterpret_cast<const float4*>(so + (32 + rr) * LDO + sgc);
+    buf_store16(dqr, static_cast<uint32_t>((r * HD + c0 + sgc) * static_cast<int64_t>(sizeof(T))), vq);
+    *reinterpret_cast<float4*>(dKm + r * DK + c0 + sgc) = vk;
+    *reinterpret_cast<float4*>(dKt + r * DK + c0 + sgc) = vt;
+  }
+}
+
 template <typename T, int DK, int DV>
 struct P12Smem {
   static constexpr int HC = 32;                 // key columns per phase-B pass
@@ -743,6 +775,10 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   float pq = 0.f, pk = 0.f, pw = 0.f;
   float red = 0.f;
   T* dq = static_cast<T*>(ba.dq) + (b * a.T + t0) * HD + h * DK;
+  // the chunk's dq rows as a raw buffer ending with row n - 1: a row r >= n
+  // starts at r HD >= (n - 1) HD + DK elements, past the range
+  const __amdgpu_buffer_rsrc_t dqr = __builtin_amdgcn_make_buffer_rsrc(
+      dq, 0, static_cast<int>(((n - 1) * HD + DK) * static_cast<int64_t>(sizeof(T))), kBufWord3);
   T* dKm = static_cast<T*>(ba.dKm) + rk;
   T* dKt = static_cast<T*>(ba.dKt) + rk;
 #pragma unroll 1
@@ -818,21 +854,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       st4<T>(so + 16 * LDO, ak[0], ak[1], ak[2], ak[3]);
       st4<T>(so + 32 * LDO, at[0], at[1], at[2], at[3]);
     }
-    {
-      // this wave's 16 rows x HC columns of dq, dK, dKt: 16-byte stores
-      // (the wave reads back only what it wrote: no barrier needed)
-      constexpr int VEC = 16 / sizeof(T), SPR = HC / VEC;
-      const T* so = sOut + w * 3 * 16 * LDO;
-      for (int idx = l; idx < 16 * SPR; idx += 64) {
-        const int rr = idx / SPR, sgc = (idx % SPR) * VEC, r = 16 * w + rr;
-        const float4 vq = *reinterpret_cast<const float4*>(so + rr * LDO + sgc);
-        const float4 vk = *reinterpret_cast<const float4*>(so + (16 + rr) * LDO + sgc);
-        const float4 vt = *reinterpret_cast<const float4*>(so + (32 + rr) * LDO + sgc);
-        if (r < n) *reinterpret_cast<float4*>(dq + r * HD + c0 + sgc) = vq;
-        *reinterpret_cast<float4*>(dKm + r * DK + c0 + sgc) = vk;
-        *reinterpret_cast<float4*>(dKt + r * DK + c0 + sgc) = vt;
-      }
-    }
+    p12_flush_rows<T, HC, LDO, DK>(sOut + w * 3 * 16 * LDO, dqr, HD, c0, dKm, dKt, w, l);
   }
 #pragma unroll
   for (int off = 16; off < 64; off <<= 1) {
@@ -1039,6 +1061,10 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
   // ---- phase B
   float pdb[4] = {0.f, 0.f, 0.f, 0.f};
   T* dq = static_cast<T*>(ba.dq) + (b * a.T + t0) * HD + h * DK;
+  // the chunk's dq rows as a raw buffer ending with row n - 1: a row r >= n
+  // starts at r HD >= (n - 1) HD + DK elements, past the range
+  const __amdgpu_buffer_rsrc_t dqr = __builtin_amdgcn_make_buffer_rsrc(
+      dq, 0, static_cast<int>(((n - 1) * HD + DK) * static_cast<int64_t>(sizeof(T))), kBufWord3);
   T* dKm = static_cast<T*>(ba.dKm) + rk;
   T* dKt = static_cast<T*>(ba.dKt) + rk;
   const float* Gc = a.G + rk;   // in-chunk log-decay prefix rows [t][c]
@@ -1165,19 +1191,7 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
         so[(32 + 4 * lg + ii) * LDO + c] = from_f<T>(ot[ii]);
       }
     }
-    {
-      constexpr int VEC = 16 / sizeof(T), SPR = HC / VEC;
-      const T* so = sOut + w * 3 * 16 * LDO;
-      for (int idx = l; idx < 16 * SPR; idx += 64) {
-        const int rr = idx / SPR, sgc = (idx % SPR) * VEC, r = 16 * w + rr;
-        const float4 vq = *reinterpret_cast<const float4*>(so + rr * LDO + sgc);
-        const float4 vk = *reinterpret_cast<const float4*>(so + (16 + rr) * LDO + sgc);
-        const float4 vt = *reinterpret_cast<const float4*>(so + (32 + rr) * LDO + sgc);
-        if (r < n) *reinterpret_cast<float4*>(dq + r * HD + c0 + sgc) = vq;
-        *reinterpret_cast<float4*>(dKm + r * DK + c0 + sgc) = vk;
-        *reinterpret_cast<float4*>(dKt + r * DK + c0 + sgc) = vt;
-      }
-    }
+    p12_flush_rows<T, HC, LDO, DK>(sOut + w * 3 * 16 * LDO, dqr, HD, c0, dKm, dKt, w, l);
     __syncthreads();
     {
       // dg_j = sum_{r >= j} dG_r + the last-row term, per channel: eight
