@@ -190,7 +190,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     const T* kp = static_cast<const T*>(a.k);
     const T* qp = static_cast<const T*>(a.q);
     const T* xp = static_cast<const T*>(a.ktilde);
-    for (int idx = tid; idx < C * VPR; idx += 256) {
+    static_assert((C * VPR) % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+    for (int jj = 0; jj < (C * VPR) / 256; ++jj) {
+      const int idx = tid + 256 * jj;
       const int r = idx / VPR, cv = idx % VPR;
       float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), qv = kv, xv = kv;
       if (r < n) {
@@ -218,7 +221,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       if (GATE == kGateScalar) sGraw[r] = ok ? a.g[sidx] : 0.f;
     }
     if (GATE == kGateChannel) {
-      for (int idx = tid; idx < C * (DK / 4); idx += 256) {
+      static_assert((C * (DK / 4)) % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+      for (int jj = 0; jj < (C * (DK / 4)) / 256; ++jj) {
+        const int idx = tid + 256 * jj;
         const int r = idx / (DK / 4), c4 = idx % (DK / 4);
         float4 gv = make_float4(0.f, 0.f, 0.f, 0.f);
         if (r < n)
@@ -376,7 +382,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   if (PREC == kATQ) {
     // the preconditioned query rows for the scan's inter-chunk output
     T* qt = static_cast<T*>(a.Qt) + (bh * a.Tpad + t0) * DK;
-    for (int idx = tid; idx < C * VPR; idx += 256) {
+    static_assert((C * VPR) % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+    for (int jj = 0; jj < (C * VPR) / 256; ++jj) {
+      const int idx = tid + 256 * jj;
       const int r = idx / VPR, cv = idx % VPR;
       *reinterpret_cast<float4*>(qt + r * DK + cv * VEC) = *reinterpret_cast<const float4*>(k2sw(sQ, LDK, r, cv * VEC));
     }
@@ -388,7 +397,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     T* ql = static_cast<T*>(a.QL) + (bh * a.Tpad + t0) * DK;
     T* kl = static_cast<T*>(a.KL) + (bh * a.Tpad + t0) * DK;
     const T* qg = static_cast<const T*>(a.q) + ((b * a.T + t0) * a.H + h) * DK;
-    for (int idx = tid; idx < C * (DK / 8); idx += 256) {
+    static_assert((C * (DK / 8)) % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+    for (int jj = 0; jj < (C * (DK / 8)) / 256; ++jj) {
+      const int idx = tid + 256 * jj;
       const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
       Frag8<T> fk = ld8(k2sw(sK, LDK, r, c0)), fq;
       if (NOQ) {
@@ -477,7 +489,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     // (Lam o Q)^T and -(Lam o K)^T per chunk, [dk][C]
     T* QlT = static_cast<T*>(a.QlT) + (bh * a.NT + i) * (int64_t)(DK * C);
     T* KnT = static_cast<T*>(a.KnT) + (bh * a.NT + i) * (int64_t)(DK * C);
-    for (int idx = tid; idx < DK * (C / 8); idx += 256) {
+    static_assert((DK * (C / 8)) % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+    for (int jj = 0; jj < (DK * (C / 8)) / 256; ++jj) {
+      const int idx = tid + 256 * jj;
       const int c = idx / (C / 8), r0 = (idx % (C / 8)) * 8;
       Frag8<T> fq, fk;
 #pragma unroll
@@ -502,7 +517,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     // write-key rows, and for the per-channel gate the decayed rows
     // w_r o Kt (with a scalar gate the reverse scan applies w_r itself)
     T* Kr = static_cast<T*>(a.Ktr) + (bh * a.Tpad + t0) * DK;
-    for (int idx = tid; idx < C * (DK / 8); idx += 256) {
+    static_assert((C * (DK / 8)) % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+    for (int jj = 0; jj < (C * (DK / 8)) / 256; ++jj) {
+      const int idx = tid + 256 * jj;
       const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
       const Frag8<T> fk = ld8(k2sw(sKt, LDK, r, c0));
       st8(Kr + r * DK + c0, fk);
@@ -518,7 +536,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   // ---- decayed write keys, transposed per chunk: (Kt * Lam_C / Lam_t)^T
   {
     T* Kout = static_cast<T*>(a.KtG) + (bh * a.NT + i) * (int64_t)(DK * C);
-    for (int idx = tid; idx < DK * C / 8; idx += 256) {
+    static_assert((DK * C / 8) % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+    for (int jj = 0; jj < (DK * C / 8) / 256; ++jj) {
+      const int idx = tid + 256 * jj;
       const int c = idx / (C / 8), tv = (idx % (C / 8)) * 8;
       Frag8<T> f;
 #pragma unroll
@@ -591,7 +612,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   // ---- T = X Diag(beta) (block-lower; upper blocks are zero)
   {
     T* Tout = static_cast<T*>(a.Tm) + (bh * a.NT + i) * (int64_t)(C * C);
-    for (int idx = tid; idx < C * C / 8; idx += 256) {
+    static_assert((C * C / 8) % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+    for (int jj = 0; jj < (C * C / 8) / 256; ++jj) {
+      const int idx = tid + 256 * jj;
       const int r = idx / (C / 8), t0v = (idx % (C / 8)) * 8;
       Frag8<T> f;
 #pragma unroll
@@ -606,7 +630,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   if (BWD) {
     const int64_t cc = (bh * a.NT + i) * (int64_t)(C * C);
     T* MtT = static_cast<T*>(a.MtT) + cc;
-    for (int idx = tid; idx < C * C / 8; idx += 256) {
+    static_assert((C * C / 8) % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+    for (int jj = 0; jj < (C * C / 8) / 256; ++jj) {
+      const int idx = tid + 256 * jj;
       const int r = idx / (C / 8), t0v = (idx % (C / 8)) * 8;
       Frag8<T> ft;
 #pragma unroll
