@@ -354,8 +354,10 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
 }
 
 // ------------------------------------------------------------ p1
-// stage_rows in two halves, so the loads can be issued early and other work
-// done before the LDS store waits for them
+// Rows [C][DD] of a workspace tensor -> LDS rows [C][DD + 8] (16-byte copies,
+// bank-spread addressing: read back through sw()), in two halves, so the
+// loads can be issued early and other work done before the LDS store waits
+// for them
 template <typename T, int DD>
 struct RowStage {
   static constexpr int kVec = 16 / static_cast<int>(sizeof(T)), kVpr = DD / kVec;
@@ -384,17 +386,6 @@ struct RowStage {
     if constexpr (kPer > 3) put(3, v3);
   }
 };
-
-// Rows [C][DD] of a workspace tensor -> LDS rows [C][DD + 8] (16-byte copies,
-// bank-spread addressing: read back through sw())
-template <typename T, int DD>
-__device__ __forceinline__ void stage_rows(T* dst, const T* src, int tid) {
-  constexpr int VEC = 16 / sizeof(T), VPR = DD / VEC, LD = DD + 8;
-  for (int idx = tid; idx < C * VPR; idx += 256) {
-    const int r = idx / VPR, cv = idx % VPR;
-    *reinterpret_cast<float4*>(sw(dst, LD, r, cv * VEC)) = *reinterpret_cast<const float4*>(src + r * DD + cv * VEC);
-  }
-}
 
 // A [C][HC] tile held in registers between its load and its transposed
 // store to dst[HC][C + 8].  (Named registers, not an array: a private array
@@ -1086,7 +1077,10 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
       if constexpr (SR::kPer == 2) chan(srows.template dot<1>(), 1);
     }
     {
-      for (int idx = tid; idx < C * (HC / 4); idx += 256) {
+      static_assert((C * (HC / 4)) % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+      for (int jj = 0; jj < (C * (HC / 4)) / 256; ++jj) {
+        const int idx = tid + 256 * jj;
         const int t = idx / (HC / 4), c4 = (idx % (HC / 4)) * 4;
         const float4 gv = *reinterpret_cast<const float4*>(Gc + t * DK + c0 + c4);
         sGT[(c4 + 0) * LDG + t] = gv.x;
