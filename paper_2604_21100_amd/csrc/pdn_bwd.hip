@@ -548,7 +548,13 @@ struct P12Smem {
   static constexpr int LDE = DV + 8, LDK = DK + 8, LDV = DV + 8, LDT = C + 8;
   static constexpr int LDO = HC + 16;           // output staging rows (bank-spread)
   static constexpr size_t kA = sizeof(T) * (C * LDE + C * LDK + 4 * C * LDT);
-  static constexpr size_t kB = sizeof(T) * (2 * HC * LDV + 3 * HC * LDT + 4 * 3 * 16 * LDO);
+  // phase B: state rows, the pass's Q^T and K^T tiles, output staging, then
+  // the whole transposed write-key tile [DK][C] (written once, after phase A
+  // has read its C x C adjoints, from phase A's row-major copy, which lies
+  // below it)
+  static constexpr size_t kKtT = 2 * HC * LDV + 2 * HC * LDT + 4 * 3 * 16 * LDO;   // elements
+  static constexpr size_t kB = sizeof(T) * (kKtT + DK * LDT);
+  static_assert(kKtT >= static_cast<size_t>(C * LDE + C * LDK), "the K~^T tile lies above phase A's K~ tile");
   static constexpr size_t kMain = kA > kB ? kA : kB;
   static constexpr size_t kTotal = kMain + sizeof(float) * (12 * C + 4);
 };
@@ -571,10 +577,10 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   // phase B (reuses the same memory)
   T* sS = reinterpret_cast<T*>(smem);   // S^T rows c0 .. c0 + HC - 1
   T* sdS = sS + HC * LDV;               // dS'^T rows
-  T* sKtT = sdS + HC * LDV;
-  T* sQT = sKtT + HC * LDT;
+  T* sQT = sdS + HC * LDV;
   T* sKT = sQT + HC * LDT;
   T* sOut = sKT + HC * LDT;             // per wave: dq, dK, dKt rows [3][16][LDO]
+  T* sKtT = reinterpret_cast<T*>(smem) + SM::kKtT;   // K~^T, all DK rows [c][t]
   float* sG = reinterpret_cast<float*>(smem + SM::kMain);
   float* sBeta = sG + C;
   float* sDb = sBeta + C;    // At term of dbeta
@@ -661,11 +667,9 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   // and its transposed write-key, query and key tiles
   const T* qtile = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
   const T* ktile = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
-  const T* kttile = static_cast<const T*>(a.Ktr) + rk;
   // (the tiles of two passes at a time: whole lines)
   static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
-  HeldTile<T, HC> tKt, tQ, tK, hKt, hQ, hK;
-  load_pair_regs<T, HC>(tKt, hKt, kttile, DK, C, tid);
+  HeldTile<T, HC> tQ, tK, hQ, hK;
   load_pair_regs<T, HC>(tQ, hQ, qtile, HD, n, tid);
   load_pair_regs<T, HC>(tK, hK, ktile, HD, n, tid);
   stE.store(sE, tid);
@@ -756,6 +760,21 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
     sRs[tid] = GATE == kGateScalar ? sRs[tid] - (sCs[tid] + sCs[C + tid] + sCs[2 * C + tid] + sCs[3 * C + tid])
                                    : 0.f;
   }
+  __syncthreads();   // every wave holds its adjoint fragments
+  {
+    // K~^T for all of phase B, once, from the row-major tile phase A staged
+    // (so phase B reads no write-key rows from HBM)
+    static_assert(DK * C / 8 % 256 == 0, "whole rounds of 256 threads");
+#pragma unroll
+    for (int jj = 0; jj < DK * C / 8 / 256; ++jj) {
+      const int idx = tid + 256 * jj;
+      const int c = idx / (C / 8), t8 = (idx % (C / 8)) * 8;
+      Frag8<T> f;
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) f.set(s2, to_f(*sw(sKt, LDK, t8 + s2, c)));
+      st8(sw(sKtT, LDT, c, t8), f);
+    }
+  }
   // phase B computes its tiles transposed (every product with its operands
   // swapped), so a lane holds row ra = 16 w + lr at columns 16 j + 4 lg + ii
   const float lam = GATE == kGateScalar ? fast_exp(sG[ra]) : 1.f;
@@ -783,11 +802,9 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
     }
     // transposed Kt, Q, K tiles (loaded during an earlier pass)
     if ((p & 1) == 0) {
-      tile_t_store<T, HC>(sKtT, tKt, tid);
       tile_t_store<T, HC>(sQT, tQ, tid);
       tile_t_store<T, HC>(sKT, tK, tid);
     } else {
-      tile_t_store<T, HC>(sKtT, hKt, tid);
       tile_t_store<T, HC>(sQT, hQ, tid);
       tile_t_store<T, HC>(sKT, hK, tid);
     }
@@ -798,7 +815,6 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       const int cn = min(p + 1, NPASS - 1) * HC;
       srows.load(static_cast<const T*>(a.Hs) + cs + cn * DV, static_cast<const T*>(ba.dHs) + cs + cn * DV, tid);
       if ((p & 1) == 1 && p + 1 < NPASS) {   // the next two passes' tiles
-        load_pair_regs<T, HC>(tKt, hKt, kttile + cn, DK, C, tid);
         load_pair_regs<T, HC>(tQ, hQ, qtile + cn, HD, n, tid);
         load_pair_regs<T, HC>(tK, hK, ktile + cn, HD, n, tid);
       }
@@ -822,7 +838,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
         A1[ii] *= a.scale;
         pq += to_f(*sw(sQT, LDT, cb + ii, ra)) * A1[ii];
         pk += to_f(*sw(sKT, LDT, cb + ii, ra)) * A2[ii];
-        pw += to_f(*sw(sKtT, LDT, cb + ii, ra)) * A3[ii];
+        pw += to_f(*sw(sKtT, LDT, c0 + cb + ii, ra)) * A3[ii];
       }
       floatx4 aq, ak, at;
 #pragma unroll
@@ -833,7 +849,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       }
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
-        const Frag8<T> fk = ld8(sw(sKtT, LDT, 16 * j + lr, 32 * k2 + 8 * lg));
+        const Frag8<T> fk = ld8(sw(sKtT, LDT, c0 + 16 * j + lr, 32 * k2 + 8 * lg));
         mma(aq, fk, fSq[k2]);
         mma(ak, fk, fSk[k2]);
         mma(at, ld8(sw(sQT, LDT, 16 * j + lr, 32 * k2 + 8 * lg)), fSqT[k2]);
