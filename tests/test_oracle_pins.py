@@ -237,6 +237,154 @@ def test_knorm_invariants():
     assert kk.min() >= 0.0 and kk.max() < 1.0
 
 
+@pytest.mark.parametrize("gate", ["none", "scalar"])
+def test_knorm_beta_factor_is_decayed_sherman_morrison(gate):
+    """The beta/(alpha + beta m) factor is the decayed Sherman-Morrison
+    normaliser (App. B, Sherman-Morrison update of the inverse Gram, with a
+    decay alpha and gain beta): for G_t = alpha G_{t-1} + beta k k^T and
+    P = G_{t-1}^{-1},
+        beta G_t^{-1} k = beta / (alpha + beta k^T P k) * P k.
+    The oracle's factor, handed the write key P k for a random dense SPD
+    G_{t-1} (not diagonal), must reproduce the dense inverse on the left."""
+    rng = np.random.default_rng(26)
+    dk, T = 6, 8
+    k = rng.standard_normal((1, T, dk))
+    beta = rng.uniform(0.1, 2.0, (1, T))
+    g = None if gate == "none" else -rng.uniform(0.0, 1.0, (1, T))
+    kt = np.empty_like(k)
+    ref = np.empty_like(k)
+    for t in range(T):
+        Z = rng.standard_normal((dk, dk))
+        G = Z @ Z.T + 0.5 * np.eye(dk)
+        kt[0, t] = np.linalg.inv(G) @ k[0, t]
+        al = 1.0 if g is None else np.exp(g[0, t])
+        Gt = al * G + beta[0, t] * np.outer(k[0, t], k[0, t])
+        ref[0, t] = beta[0, t] * np.linalg.inv(Gt) @ k[0, t]
+    fac = recurrent.knorm_factor(k, kt, beta, g, gate, "beta")
+    assert np.allclose(fac * kt, ref, rtol=1e-10, atol=1e-12)
+
+
+def test_knorm_1pm_factor_is_sherman_morrison():
+    """The 1/(1 + m) factor is the undecayed, unit-gain Sherman-Morrison
+    normaliser (App. B): with P = G^{-1}, (G + k k^T)^{-1} k =
+    P k / (1 + k^T P k), checked against a dense inverse."""
+    rng = np.random.default_rng(27)
+    dk, T = 5, 6
+    k = rng.standard_normal((1, T, dk))
+    kt = np.empty_like(k)
+    ref = np.empty_like(k)
+    for t in range(T):
+        Z = rng.standard_normal((dk, dk))
+        G = Z @ Z.T + 0.3 * np.eye(dk)
+        kt[0, t] = np.linalg.solve(G, k[0, t])
+        ref[0, t] = np.linalg.solve(G + np.outer(k[0, t], k[0, t]), k[0, t])
+    fac = recurrent.knorm_factor(k, kt, np.ones((1, T)), None, "none", "1pm")
+    assert np.allclose(fac * kt, ref, rtol=1e-10, atol=1e-12)
+
+
+# ------------------------------------- App. D linear attention (ATQ family)
+def _la_decays(rng, gate, N, T, dk, strength=0.3):
+    if gate == "none":
+        return None, np.ones((N, T, dk))
+    if gate == "scalar":
+        g = -strength * rng.uniform(size=(N, T))
+        return g, np.repeat(np.exp(g)[..., None], dk, axis=2)
+    g = -strength * rng.uniform(size=(N, T, dk))
+    return g, np.exp(g)
+
+
+@pytest.mark.parametrize("gate", ["none", "scalar", "channel"])
+def test_decayed_linear_attention_unrolled_closed_form(gate):
+    """S_t = alpha_t S_{t-1} + beta_t v_t k_t^T unrolls to
+        S_t = S0 Diag(D_{0,t}) + sum_{j<=t} beta_j v_j (k_j * D_{j,t})^T,
+    D_{j,t} = prod_{j<m<=t} alpha_m (the new term is not decayed by its own
+    alpha_j), and o_t = scale S_t q_t: the quadratic (attention) form of
+    Mamba-2 / GLA.  Brute force over (t, j) with explicit products, against
+    the oracle's token recurrence, on tiny inputs."""
+    rng = np.random.default_rng(61)
+    N, T, dk, dv = 1, 12, 4, 3
+    q = rng.standard_normal((N, T, dk))
+    k = rng.standard_normal((N, T, dk))
+    v = rng.standard_normal((N, T, dv))
+    beta = rng.uniform(0.0, 2.0, (N, T))
+    S0 = rng.standard_normal((N, dv, dk))
+    g, alpha = _la_decays(rng, gate, N, T, dk)
+    o, S_T = recurrent.linear_attention(q, k, v, beta, g, gate, S0, scale=0.7)
+
+    def D(j, t):          # prod of alpha over 1-based tokens j+1..t
+        return np.prod(alpha[0, j:t], axis=0)
+
+    for t in range(1, T + 1):
+        S = S0[0] * D(0, t)[None, :]
+        for j in range(1, t + 1):
+            S = S + beta[0, j - 1] * np.outer(v[0, j - 1], k[0, j - 1] * D(j, t))
+        assert np.allclose(o[0, t - 1], 0.7 * S @ q[0, t - 1], rtol=1e-12,
+                           atol=1e-12)
+    assert np.allclose(S_T[0], S, rtol=1e-12, atol=1e-12)
+
+
+def test_linear_attention_is_causal_masked_product():
+    """No decay, unit gain, zero initial state: the linear-attention outputs
+    are the causal masked product O = (tril(Q K^T)) V (the textbook identity
+    behind App. D's PLA form with the whole sequence as one chunk), with
+    tril from the library."""
+    rng = np.random.default_rng(62)
+    q = rng.standard_normal((2, 20, 5))
+    k = rng.standard_normal((2, 20, 5))
+    v = rng.standard_normal((2, 20, 3))
+    o, _ = recurrent.linear_attention(q, k, v, np.ones((2, 20)))
+    ref = np.tril(q @ np.swapaxes(k, 1, 2)) @ v
+    assert np.allclose(o, ref, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("gate", ["none", "scalar", "channel"])
+@pytest.mark.parametrize("C", [1, 2, 4, 8, 16, 32, 64])
+def test_la_chunkwise_equals_recurrent(gate, C):
+    """App. D's PLA / P-Mamba-2 / PGLA chunkwise forms equal the token
+    recurrence of (decayed) linear attention, with a gain, a ragged last
+    chunk and S0 != 0."""
+    rng = np.random.default_rng(63 + C)
+    N, T, dk, dv = 2, 100, 8, 6
+    q = rng.standard_normal((N, T, dk))
+    k = _unit(rng.standard_normal((N, T, dk)))
+    v = rng.standard_normal((N, T, dv))
+    beta = _sig(rng.standard_normal((N, T)))
+    S0 = 0.1 * rng.standard_normal((N, dv, dk))
+    g, _ = _la_decays(rng, gate, N, T, dk, strength=0.2)
+    o, S_T = recurrent.linear_attention(q, k, v, beta, g, gate, S0, scale=0.8)
+    o2, S2 = chunkwise.la_chunk_forward(q, k, v, beta, g, gate, S0, C, 0.8)
+    assert np.abs(o - o2).max() <= 1e-12 * np.abs(o).max()
+    assert np.abs(S_T - S2).max() <= 1e-12 * np.abs(S_T).max()
+
+
+@pytest.mark.parametrize("gate", ["none", "scalar", "channel"])
+def test_atq_end_to_end_equals_chunkwise_forms(gate):
+    """The apply-to-query mode over many tokens with decays, gains, A0 and
+    S0: the oracle's end-to-end result equals App. D's composition of the
+    chunkwise Gram recurrence (Eq. precond_from_boundary) with the
+    chunkwise P-Mamba-2 / PGLA forms applied to q / (A_t + ridge)."""
+    rng = np.random.default_rng(64)
+    N, T, dk, dv = 2, 90, 6, 5
+    q = _unit(rng.standard_normal((N, T, dk)))
+    k = _unit(rng.standard_normal((N, T, dk)))
+    v = rng.standard_normal((N, T, dv))
+    beta = _sig(rng.standard_normal((N, T)))
+    g, _ = _la_decays(rng, gate, N, T, dk, strength=0.2)
+    bp = rng.uniform(0.1, 2.0, (N, T))
+    gp = -0.1 * rng.uniform(size=(N, T))
+    A0 = rng.uniform(0.0, 1.0, (N, dk))
+    S0 = 0.1 * rng.standard_normal((N, dv, dk))
+    r = recurrent.pdn_forward(q, k, v, beta, g=g, gate=gate, precond="atq",
+                              beta_p=bp, g_p=gp, A0=A0, S0=S0, ridge=0.4,
+                              scale=1.1)
+    A_all, A_bound = chunkwise.gram_chunkwise(k, bp, gp, 16, A0)
+    o2, S2 = chunkwise.la_chunk_forward(q / (A_all + 0.4), k, v, beta, g, gate,
+                                        S0, 16, 1.1)
+    assert np.abs(r["o"] - o2).max() <= 1e-12 * np.abs(r["o"]).max()
+    assert np.abs(r["S_T"] - S2).max() <= 1e-12 * np.abs(r["S_T"]).max()
+    assert np.allclose(r["A_T"], A_bound[:, -1], rtol=1e-12, atol=1e-14)
+
+
 # ---------------------------------------------------------------- Sec. 3.5
 def test_squash_range_monotone_and_fixed_points():
     """Eq. precond_end2end: B in [1/x, x], decreasing in A, B = 1 where
