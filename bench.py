@@ -46,69 +46,101 @@ PEAK_FP32_TFLOPS = 157.3       # dense fp32 matrix
 def algorithmic_per_token_head(spec, train=False, precond="squash"):
     """Algorithmic FLOPs and bytes per token-head (one (b, t, h)).
 
-    Dense per-chunk products as the paper writes them:
+    FLOPs: the dense per-chunk products as the paper writes them,
         forward  FLOP = 6 C dk + 4 C dv + 6 dk dv + C^2 / 3
         backward FLOP = 12 C dk + 8 C dv + 12 dk dv + 4 C^2
     (the backward's recompute of forward intermediates is executed work, not
-    algorithmic, and is not in the totals).  Per kernel stage: the products
-    that kernel performs and its compulsory bytes (what it must read and
-    write, each once).  train: the forward also writes the intermediates the
-    backward reads (training pair).  Returns (flop_fwd, flop_bwd,
-    {stage: (flop, bytes)})."""
+    algorithmic, and is not in the totals).
+
+    Bytes come in two kinds per kernel stage:
+      method bytes  the method's own tensors the stage reads or writes, each
+                    once: q, k, v, beta, g, betaP, gP (and the external write
+                    key) in, o out; dO in, dq, dk, dv and the scalar
+                    gradients out; the per-head states S0/S_T/A0/A_T and their
+                    adjoints amortised over T.  Workspace intermediates are
+                    not method bytes.  These define each stage's roofline
+                    fraction.
+      design bytes  what this design's stage must move as built: the method
+                    bytes plus the intermediates it hands to other kernels
+                    through HBM (solve factors, decayed keys, saved states,
+                    E rows, state adjoints, ...), each once.
+    Returns (flop_fwd, flop_bwd, {stage: (flop, method_bytes, design_bytes)},
+    {"fwd": method bytes of a forward pass, "step": of the timed step}).
+    """
     C, dk, dv = spec.chunk, spec.dk, spec.dv
     e = 2 if spec.io == "bf16" else 4
     gb = {"none": 0, "scalar": 4, "channel": 4 * dk}[spec.gate]
-    st = e * dk * dv / C                       # one chunk-start state, per token
+    gram = precond in ("squash", "diag_sm", "atq")
+    pb = 8 if gram else 0                       # betaP, gP
+    xk = e * dk if precond == "external" else 0  # external write key
+    T = spec.T
+    sh = 4 * dk * dv / T                         # one per-head state, per token
+    ah = (4 * dk / T) if gram else 0.0           # one preconditioner state
+    s0 = sh if spec.s0 != "zero" else 0.0        # S0 read
+    st = e * dk * dv / C                         # one saved chunk-start state
     flop_fwd = 6 * C * dk + 4 * C * dv + 6 * dk * dv + C * C / 3.0
     flop_bwd = 12 * C * dk + 8 * C * dv + 12 * dk * dv + 4 * C * C
-    pre = (3 * dk, e * dk + 8 + 4 * dk / C)
-    # k2: read q, k, beta, g, betaP, gP, chunk-start A; write the decayed
-    # write keys (dk), T and P (C each) and the gate prefix
-    prep = (4 * C * dk + C * C / 3.0,
-            2 * e * dk + 12 + gb + 4 * dk / C + e * (dk + 2 * C) + gb)
+    # method bytes of whole passes
+    fwd_in = e * (2 * dk + dv) + 4 + gb + pb + xk + s0 + ah   # A0 read
+    fwd_m = fwd_in + e * dv + sh + ah                          # o, S_T, A_T
+    bwd_m = (fwd_in + e * dv                                   # inputs, dO
+             + e * (2 * dk + dv) + 4 + gb + pb + xk            # dq dk dv dbeta dg dbetaP dgP (dkt)
+             + sh + ah)                                        # dS0, dA0
+    # per stage: (flop, method bytes, design bytes)
+    pre = (3 * dk, e * dk + pb + 2 * ah, e * dk + pb + 4 * dk / C)
+    # k2: reads q, k, beta, g, betaP, gP and the chunk-start A; writes the
+    # decayed write keys (dk), T and P (C each) and the gate prefix
+    prep_m = e * 2 * dk + 4 + gb + pb + xk
+    prep = (4 * C * dk + C * C / 3.0, prep_m,
+            prep_m + 4 * dk / C + e * (dk + 2 * C) + gb)
     # k2 (backward mode): also P^T and M^T (C each) and the write-key,
     # decayed write-key, decayed query and key rows (dk each)
-    prep_b = (prep[0], prep[1] + 2 * e * C + 4 * e * dk)
-    # k3: read q, k, v, T, P, decayed write keys, gate prefix; write o
-    scan = (6 * dk * dv + 4 * C * dv,
-            e * (2 * dk + dv) + e * (2 * C + dk) + gb + e * dv)
-    # k3 (saving, no output): read k, v, T, decayed write keys, gate prefix;
-    # write the chunk-start states and the E rows
-    save = (4 * dk * dv + 2 * C * dv,
-            e * (dk + dv) + e * (C + dk) + gb + st + e * dv)
+    prep_b = (prep[0], prep_m, prep[2] + 2 * e * C + 4 * e * dk)
+    # k3: reads q, k, v; writes o and S_T (reads T, P, decayed write keys and
+    # the gate prefix from the workspace)
+    scan_m = e * (2 * dk + dv) + e * dv + s0 + sh
+    scan = (6 * dk * dv + 4 * C * dv, scan_m,
+            e * (2 * dk + dv) + e * (2 * C + dk) + gb + e * dv + s0 + sh)
+    # k3 (saving, no output): reads k, v, T, decayed write keys, gate prefix;
+    # writes the chunk-start states and the E rows
+    save = (4 * dk * dv + 2 * C * dv, e * (dk + dv) + s0,
+            e * (dk + dv) + e * (C + dk) + gb + st + e * dv + s0)
     if precond == "atq":
         # linear attention read through the preconditioned query: no
         # interaction matrix or solve; the prep kernel also writes the
         # preconditioned query rows, the scan reads them instead of q and k
         flop_fwd = 2 * C * dk + 2 * C * dv + 4 * dk * dv
-        prep = (2 * C * dk, prep[1] + e * dk)
-        scan = (4 * dk * dv + 2 * C * dv, scan[1] - e * dk)
+        prep = (2 * C * dk, prep[1], prep[2] + e * dk)
+        scan = (4 * dk * dv + 2 * C * dv, scan[1] - e * dk, scan[2] - e * dk)
     stages = {
         "precond": pre,
         "chunk_prep": prep_b if train else prep,
         # training forward: the output, the saved states and E rows
-        "chunk_scan": ((scan[0], scan[1] + st + e * dv) if train
+        "chunk_scan": ((scan[0], scan[1], scan[2] + st + e * dv) if train
                        else scan),
         "bwd_precond_recompute": pre,
         "bwd_chunk_prep": prep_b,
         "bwd_state_save_scan": save,
-        # r1: read P^T, M^T, w*Kt, (lam Q)^T, -(lam K)^T, dO, beta; write the
-        # state adjoints, the Z rows and dv
+        # r1: reads dO and beta, writes dv and dS0 (method); also reads P^T,
+        # M^T, the write keys, (lam Q)^T, -(lam K)^T and writes the state
+        # adjoints and the Z rows
         "bwd_state_adjoint_scan": (4 * C * dv + 6 * dk * dv,
+                                   2 * e * dv + 4 + sh,
                                    2 * e * C + 3 * e * dk + e * dv + 4
-                                   + 4 / C + st + 2 * e * dv),
-        # p12: read dO, Z, V, E, q, k, kt, the chunk-start state and its
-        # adjoint, beta, gate prefix; write dq, dk (read key) and dkt (io),
-        # dbeta, dg
+                                   + 4 / C + st + 2 * e * dv + sh),
+        # p12: reads q, k, v, dO, beta, g; writes dq, dbeta, dg (method);
+        # also reads Z, E, the write keys, the chunk-start states and their
+        # adjoints and writes the key gradients of both keys
         "bwd_chunk_grads": (4 * C * dv + 12 * C * dk + 6 * dk * dv,
+                            e * (2 * dk + 2 * dv) + 4 + gb + e * dk + 4 + gb,
                             4 * e * dv + 3 * e * dk + 2 * st + 4 + gb
                             + 3 * e * dk + 8),
-        # pc: read k, dk (read key), dkt, betaP, gP, chunk-start A; write dk,
-        # dbetaP, dgP
-        "bwd_precond_reverse": (10 * dk,
+        # pc: reads k, betaP, gP; writes dk, dbetaP, dgP, dA0 (method); also
+        # reads both key gradients and the chunk-start A
+        "bwd_precond_reverse": (10 * dk, e * dk + pb + e * dk + pb + ah,
                                 3 * e * dk + 8 + 4 * dk / C + e * dk + 8),
     }
-    return flop_fwd, flop_bwd, stages
+    return flop_fwd, flop_bwd, stages, {"fwd": fwd_m, "bwd": bwd_m}
 
 
 KERNELS = {
@@ -174,7 +206,15 @@ def cpu_baseline(spec, inp, bwd, target_s=15.0, precond="squash", ridge=1.0,
         list(ex.map(_oracle_job, [(smp, kw, g, bwd) for g in groups]))
         return time.perf_counter() - t0, len(heads) * Ts
 
-    workers = max(1, min(16, ncpu, spec.B * spec.H))
+    # every core of the affinity set, unless the host declares a smaller CPU
+    # share for this job through OMP_NUM_THREADS (the GPU hosts do: 16 per
+    # GPU); never more workers than heads in the sample
+    share = ncpu
+    try:
+        share = max(1, int(os.environ.get("OMP_NUM_THREADS", ncpu)))
+    except ValueError:
+        pass
+    workers = max(1, min(ncpu, share, spec.B * spec.H))
     with ProcessPoolExecutor(max_workers=workers) as ex:
         run(ex, workers, 1, min(spec.T, 8))               # start the workers
         Tc = min(spec.T, 128)
@@ -194,7 +234,8 @@ def cpu_baseline(spec, inp, bwd, target_s=15.0, precond="squash", ridge=1.0,
         "sample": (f"float64 token-recurrence oracle, {what}, batches "
                    f"0..{nb - 1} x all {spec.H} heads, first {Ts} of {spec.T} "
                    f"tokens ({token_heads} token-heads in {wall:.1f} s on "
-                   f"{workers} worker processes x 1 thread); value = "
+                   f"{workers} worker processes x 1 thread; affinity set "
+                   f"{ncpu} cores, declared CPU share {share}); value = "
                    f"token-heads/s / H"),
     }
 
@@ -229,15 +270,20 @@ def measured_traffic(workload, mode, stage):
 
 
 def roofline_of(stage, ms, stages, token_heads, train=False):
-    """Roofline object for one kernel stage from its measured average time."""
-    dflop, dbytes = stages[stage]
+    """Roofline object for one kernel stage from its measured average time:
+    `achieved` = the stage's method bytes (or FLOPs, when its method
+    intensity is above the bf16 ridge) per launch / its time; the design's
+    own compulsory bytes are reported beside it (design_bytes_per_launch,
+    design_frac), and the counter traffic, when known, with its ratio to
+    the method bytes."""
+    dflop, mbytes, dbytes = stages[stage]
     sec = ms / 1e3
-    if dflop / dbytes >= PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
+    if dflop / mbytes >= PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
         ach = dflop * token_heads / sec / 1e12
         roof = {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s"}
     else:
-        ach = dbytes * token_heads / sec / 1e9
+        ach = mbytes * token_heads / sec / 1e9
         roof = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS,
                 "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
@@ -246,8 +292,12 @@ def roofline_of(stage, ms, stages, token_heads, train=False):
                                      ("chunk_prep", "chunk_scan") else "")]
     roof["stage"] = stage
     roof["avg_ms"] = ms
-    roof["alg_bytes_per_launch"] = dbytes * token_heads
+    roof["alg_bytes_per_launch"] = mbytes * token_heads
+    roof["alg_bytes_per_token_head"] = mbytes
     roof["alg_flop_per_launch"] = dflop * token_heads
+    roof["mfma_frac"] = dflop * token_heads / sec / 1e12 / PEAK_BF16_TFLOPS
+    roof["design_bytes_per_launch"] = dbytes * token_heads
+    roof["design_frac"] = dbytes * token_heads / sec / 1e9 / PEAK_HBM_GBS
     return roof
 
 
@@ -366,6 +416,9 @@ def main(argv=None):
                          "the preconditioner, with a given write key and "
                          "with k~ = k (one JSON line per point)")
     ap.add_argument("--sweep-t", default="1024,2048,4096,8192,16384,32768")
+    ap.add_argument("--rotate", type=int, default=2,
+                    help="input/output sets for the rotated (cold-MALL) "
+                         "timing reported next to the hot one; 1 skips it")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also launch one device copy of this many MiB per "
                          "step (reference kernel for HBM counter scaling)")
@@ -407,31 +460,42 @@ def main(argv=None):
         t = torch.from_numpy(np.ascontiguousarray(a))
         d[key] = (t.to(io_dt) if key in ("q", "k", "v", "dO") else t).to(dev)
     B, T, H, dk, dv = spec.B, spec.T, spec.H, spec.dk, spec.dv
-    o = torch.empty((B, T, H, dv), dtype=io_dt, device=dev)
-    S_T = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev)
-    A_T = torch.empty((B, H, dk), dtype=torch.float32, device=dev)
     prob = pdn.make_problem(B, T, H, dk, dv, io=spec.io, gate=spec.gate,
                             precond=args.precond, x=spec.x, scale=spec.scale,
                             ridge=args.ridge, knorm=args.knorm)
     ws = torch.empty(pdn.pdn_workspace_size(prob, with_bwd=bwd),
                      dtype=torch.uint8, device=dev)
-    grads = None
-    if bwd:
+
+    def outputs():
         f32 = dict(dtype=torch.float32, device=dev)
-        grads = {
-            "dq": torch.empty((B, T, H, dk), dtype=io_dt, device=dev),
-            "dk": torch.empty((B, T, H, dk), dtype=io_dt, device=dev),
-            "dv": torch.empty((B, T, H, dv), dtype=io_dt, device=dev),
-            "dbeta": torch.empty((B, T, H), **f32),
-            "dg": (torch.empty((B, T, H), **f32) if spec.gate == "scalar"
-                   else torch.empty((B, T, H, dk), **f32)
-                   if spec.gate == "channel" else None),
-            "dS0": torch.empty((B, H, dk, dv), **f32),
-            "dbeta_p": torch.empty((B, T, H), **f32),
-            "dg_p": torch.empty((B, T, H), **f32),
-            "dlog_a_scale": torch.empty((H,), **f32),
-            "dA0": torch.empty((B, H, dk), **f32),
-        }
+        out = {"o": torch.empty((B, T, H, dv), dtype=io_dt, device=dev),
+               "S_T": torch.empty((B, H, dk, dv), **f32),
+               "A_T": torch.empty((B, H, dk), **f32), "grads": None}
+        if bwd:
+            out["grads"] = {
+                "dq": torch.empty((B, T, H, dk), dtype=io_dt, device=dev),
+                "dk": torch.empty((B, T, H, dk), dtype=io_dt, device=dev),
+                "dv": torch.empty((B, T, H, dv), dtype=io_dt, device=dev),
+                "dbeta": torch.empty((B, T, H), **f32),
+                "dg": (torch.empty((B, T, H), **f32) if spec.gate == "scalar"
+                       else torch.empty((B, T, H, dk), **f32)
+                       if spec.gate == "channel" else None),
+                "dS0": torch.empty((B, H, dk, dv), **f32),
+                "dbeta_p": torch.empty((B, T, H), **f32),
+                "dg_p": torch.empty((B, T, H), **f32),
+                "dlog_a_scale": torch.empty((H,), **f32),
+                "dA0": torch.empty((B, H, dk), **f32),
+            }
+        return out
+
+    # set 0 is the hot-cache set; the rotated timing alternates it with
+    # independent copies at other addresses (inputs and outputs), so that no
+    # step finds its inputs in the 256 MB MALL the previous step left warm
+    nrot = max(1, args.rotate)
+    sets = [(d, outputs())]
+    for _ in range(1, nrot):
+        sets.append(({k: (None if v is None else v.clone()) for k, v in d.items()},
+                     outputs()))
     calib = None
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20) // 4
@@ -443,22 +507,25 @@ def main(argv=None):
 
     train = bwd and not args.recompute
 
-    def step(fev=None, bev=None):
-        pdn.pdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], g=d["g"],
+    def step(fev=None, bev=None, which=0):
+        x, out = sets[which]
+        pdn.pdn_chunk_fwd(x["q"], x["k"], x["v"], x["beta"], g=x["g"],
                           gate=spec.gate, precond=args.precond,
-                          beta_p=d["beta_p"], g_p=d["g_p"],
-                          log_a_scale=d["log_a_scale"] if sq else None,
-                          A0=d["A0"], S0=d["S0"], x=spec.x, scale=spec.scale,
-                          ridge=args.ridge, knorm=args.knorm, o=o, S_T=S_T, A_T=A_T,
+                          beta_p=x["beta_p"], g_p=x["g_p"],
+                          log_a_scale=x["log_a_scale"] if sq else None,
+                          A0=x["A0"], S0=x["S0"], x=spec.x, scale=spec.scale,
+                          ridge=args.ridge, knorm=args.knorm, o=out["o"],
+                          S_T=out["S_T"], A_T=out["A_T"],
                           workspace=ws, stream=stream, stage_events=fev,
                           train=train)
         if bwd:
-            pdn.pdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], d["dO"],
-                              g=d["g"], gate=spec.gate, beta_p=d["beta_p"],
-                              g_p=d["g_p"], log_a_scale=d["log_a_scale"],
-                              A0=d["A0"], S0=d["S0"], x=spec.x,
-                              scale=spec.scale, outputs=grads, workspace=ws,
-                              stream=stream, stage_events=bev, saved=train)
+            pdn.pdn_chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["dO"],
+                              g=x["g"], gate=spec.gate, beta_p=x["beta_p"],
+                              g_p=x["g_p"], log_a_scale=x["log_a_scale"],
+                              A0=x["A0"], S0=x["S0"], x=spec.x,
+                              scale=spec.scale, outputs=out["grads"],
+                              workspace=ws, stream=stream, stage_events=bev,
+                              saved=train)
         if calib is not None:
             calib[1].copy_(calib[0])
 
@@ -504,40 +571,65 @@ def main(argv=None):
         return [events[j] if j in (si, si + 1) else None
                 for j in range(len(stages_list) + 1)]
 
-    fev = [only_dom(fwd_stages, fwd_stages, mk(len(fwd_stages) + 1)) for _ in range(K)]
-    bev = ([only_dom(bwd_stages, bwd_stages, mk(len(bwd_stages) + 1)) for _ in range(K)]
-           if bwd else [None] * K)
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    start.record(stream)
-    for i in range(K):
-        step(fev[i], bev[i])
-    end.record(stream)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    total_ms = start.elapsed_time(end)
+    def timed(rotate):
+        """K steps between synchronisations, an event at every step
+        boundary (for the median) and at the dominant stage's boundaries.
+        Returns (total ms, per-step ms list, dominant stage ms, wall s)."""
+        fev = [only_dom(fwd_stages, fwd_stages, mk(len(fwd_stages) + 1))
+               for _ in range(K)]
+        bev = ([only_dom(bwd_stages, bwd_stages, mk(len(bwd_stages) + 1))
+                for _ in range(K)] if bwd else [None] * K)
+        marks = mk(K + 1)
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter()
+        for i in range(K):
+            marks[i].record(stream)
+            step(fev[i], bev[i], i % nrot if rotate else 0)
+        marks[K].record(stream)
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter() - t_wall
+        per = [marks[i].elapsed_time(marks[i + 1]) for i in range(K)]
+        return (marks[0].elapsed_time(marks[K]), per,
+                stage_times(fev, bev, K)[dom], t_wall)
+
+    total_ms, per_step, dom_ms, t_wall = timed(False)
     ms_per_step = total_ms / K
-    dom_ms = stage_times(fev, bev, K)[dom]
+    rot = None
+    if nrot > 1:
+        for i in range(nrot):          # touch every set once
+            step(which=i)
+        rtot, rper, rdom, _ = timed(True)
+        rot = {"sets": nrot, "ms_per_step": rtot / K,
+               "median_ms_per_step": float(np.median(rper)),
+               "value": B * T / (rtot / K / 1e3),
+               "dominant_stage_ms": rdom}
 
     tokens = B * T
     token_heads = B * T * H
-    flop_fwd, flop_bwd, stages = algorithmic_per_token_head(spec, train,
-                                                            args.precond)
+    flop_fwd, flop_bwd, stages, passes = algorithmic_per_token_head(
+        spec, train, args.precond)
     roof = roofline_of(dom, dom_ms, stages, token_heads, train)
     mode = "train" if train else ("recompute" if bwd else "forward")
     roof["traffic"] = (measured_traffic(args.workload, mode, dom) if sq
                        else None)
+    roof["traffic_over_alg"] = (None if roof["traffic"] is None else
+                                roof["traffic"] / roof["alg_bytes_per_launch"])
+    roof["traffic_over_design"] = (
+        None if roof["traffic"] is None else
+        roof["traffic"] / roof["design_bytes_per_launch"])
     if spec.gate == "channel":
         roof["kernel"] = roof["kernel"].replace("p12_", "p12c_")
-    kernels = {k: roofline_of(k, v, stages, token_heads, train)["frac"]
-               for k, v in stage_ms.items()}
+    kernels = {}
+    for k, v in stage_ms.items():
+        r = roofline_of(k, v, stages, token_heads, train)
+        kernels[k] = {"frac": r["frac"], "design_frac": r["design_frac"],
+                      "mfma_frac": r["mfma_frac"]}
 
     flop_step = flop_fwd + (flop_bwd if bwd else 0.0)
     step_s = ms_per_step / 1e3
     tflops = flop_step * token_heads / step_s / 1e12
     peak_tf = PEAK_BF16_TFLOPS if spec.io == "bf16" else PEAK_FP32_TFLOPS
+    step_bytes = passes["fwd"] + (passes["bwd"] if bwd else 0.0)
     variant = {"scalar": "PGDN", "channel": "PKDA"}.get(spec.gate, "PDN")
     if args.precond == "atq":
         variant = {"scalar": "P-Mamba-2", "channel": "PGLA"}.get(spec.gate,
@@ -553,6 +645,7 @@ def main(argv=None):
         "steps": K,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "median_ms_per_step": float(np.median(per_step)),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -572,6 +665,8 @@ def main(argv=None):
         "tflops": tflops,
         "mfma_frac": tflops / peak_tf,
         "alg_flop_per_token_head": flop_step,
+        "alg_bytes_per_token_head": step_bytes,
+        "hbm_frac": step_bytes * token_heads / step_s / 1e9 / PEAK_HBM_GBS,
         "fwd_ms": fwd_ms,
         "fwd_tokens_per_s": tokens / (fwd_ms / 1e3),
         "bwd_ms": bwd_ms,
@@ -579,8 +674,9 @@ def main(argv=None):
         "stage_ms_source": (f"{NC} untimed steps with an event at every stage "
                             "boundary; fwd_ms / bwd_ms likewise; the timed "
                             "steps record only the dominant stage"),
-        "stage_roofline_frac": kernels,
+        "stage_roofline": kernels,
         "wall_s_timed": t_wall,
+        "rotated": rot,
         "roofline": roof,
         "cpu_baseline": cpu,
     }

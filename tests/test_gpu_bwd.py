@@ -69,7 +69,7 @@ def compare(spec, inp, precond="squash", dS_T=None, heads=None, tag=""):
         else:
             gs = np.stack([g[b, :, h] for b, h in heads])
         errs[name] = rel_err(gs, r)
-    msg = f"{tag} " + " ".join(f"{k}={v:.1e}" for k, v in errs.items())
+    msg = f"{tag} " + " ".join(f"{k}={v:.2e}" for k, v in errs.items())
     print(msg)
     bad = {k: v for k, v in errs.items() if v > tol(spec.io)}
     assert not bad, msg

@@ -80,3 +80,59 @@ def test_training_pair_matches(io, gate, precond, dk, dv, T):
     for name in ref_b:
         assert torch.equal(ref_b[name], got_b[name]), name
         assert torch.equal(got_b[name], again[name]), name
+
+
+def test_training_pair_bench_workload_sampled_heads():
+    """The exact step bench.py times: the 1B PGDN layer (B=4, T=4096, H=16,
+    d=128, bf16, scalar gate, squash, x=1.5) with the bench's seed and its
+    dO ~ N(0, 1), through pdn_chunk_fwd_train + pdn_chunk_bwd_train.  At
+    B*H = 64 the scans map 8 XCD groups x 4 value slabs; heads (0,0), (1,7)
+    and (3,15) sit in different groups and batches.  Forward outputs, final
+    states and every gradient of those heads are compared with the oracle's
+    token recurrence and adjoint at the bf16 bar."""
+    import dataclasses
+    import torch
+    import paper_2604_21100_amd as pdn
+    from oracle import abi as oabi
+    from gpu_util import rel_err, tol
+
+    name = "pgdn_bf16_b4_t4096_h16_d128"
+    spec = dataclasses.replace(pi.WORKLOADS[name], with_do=True)
+    inp = pi.generate(spec, pi.WORKLOAD_SEEDS[name])
+    d = to_device(inp, spec.io)
+    kw = dict(g=d["g"], gate=spec.gate, beta_p=d["beta_p"], g_p=d["g_p"],
+              log_a_scale=d["log_a_scale"], A0=d["A0"], S0=d["S0"], x=spec.x,
+              scale=spec.scale)
+    B, T, H = spec.B, spec.T, spec.H
+    prob = pdn.make_problem(B, T, H, spec.dk, spec.dv, io=spec.io,
+                            gate=spec.gate, x=spec.x, scale=spec.scale)
+    ws = torch.empty(pdn.pdn_workspace_size(prob, True), dtype=torch.uint8,
+                     device="cuda")
+    o, S_T, A_T = pdn.pdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"],
+                                    workspace=ws, train=True, **kw)
+    grads = pdn.pdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], d["dO"],
+                              workspace=ws, saved=True, **kw)
+    torch.cuda.synchronize()
+    heads = [(0, 0), (1, 7), (3, 15)]
+    cv = lambda t: t.float().cpu().numpy().astype(np.float64)  # noqa: E731
+    rf = oabi.forward(inp, gate=spec.gate, x=spec.x, scale=spec.scale,
+                      heads=heads)
+    rb = oabi.backward(inp, gate=spec.gate, x=spec.x, scale=spec.scale,
+                       heads=heads)
+    o, S_T, A_T = cv(o), cv(S_T), cv(A_T)
+    errs = {
+        "o": rel_err(np.stack([o[b, :, h] for b, h in heads]), rf["o"]),
+        "S_T": rel_err(np.stack([S_T[b, h] for b, h in heads]), rf["S_T"]),
+        "A_T": rel_err(np.stack([A_T[b, h] for b, h in heads]), rf["A_T"]),
+    }
+    for key in ("dq", "dk", "dv", "dbeta", "dg", "dS0", "dbeta_p", "dg_p",
+                "dA0"):
+        g = cv(grads[key])
+        gs = (np.stack([g[b, h] for b, h in heads]) if key in ("dS0", "dA0")
+              else np.stack([g[b, :, h] for b, h in heads]))
+        errs[key] = rel_err(gs, rb[key])
+    msg = name + " train pair, heads (0,0) (1,7) (3,15): " + " ".join(
+        f"{k}={v:.2e}" for k, v in errs.items())
+    print(msg)
+    assert errs["A_T"] < 1e-4, msg
+    assert max(errs.values()) <= tol(spec.io), msg
