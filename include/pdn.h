@@ -22,7 +22,8 @@
  * Conventions
  *   - Every tensor argument is a DEVICE pointer to dense row-major memory owned
  *     by the caller.  The library never allocates or frees device memory; all
- *     scratch lives in a caller-provided workspace (pdn_workspace_size).
+ *     scratch lives in a caller-provided workspace (pdn_workspace_size), except
+ *     for pdn_chunk_fwd_noalloc's fixed per-device array (see there).
  *   - Layouts: q, k, ktilde, dq, dk: [B, T, H, dk];  v, o, dO, dv: [B, T, H, dv];
  *     beta, betaP, gP and a scalar gate g: [B, T, H];  a per-channel gate g:
  *     [B, T, H, dk];  logAScale: [H];  A0, A_T: [B, H, dk];
@@ -38,8 +39,10 @@
  *     and writes nothing.  A failed kernel launch returns PDN_ERR_HIP and
  *     leaves the outputs undefined.  Values are not inspected: NaN / Inf in
  *     the inputs propagate.  No exception, abort or printf crosses the ABI.
- *   - The library keeps no mutable global state: calls are re-entrant and may
- *     run concurrently on different streams with distinct workspaces.
+ *   - Apart from pdn_chunk_fwd_noalloc (which shares one fixed scratch array
+ *     per device), the library keeps no mutable global state: calls are
+ *     re-entrant and may run concurrently on different streams with
+ *     distinct workspaces.
  */
 #ifndef PDN_H
 #define PDN_H
@@ -51,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PDN_ABI_VERSION 3
+#define PDN_ABI_VERSION 4
 
 typedef enum {
   PDN_OK = 0,
@@ -66,7 +69,9 @@ typedef enum {
                               for DIAG_SM / ATQ) or enum (knorm other than
                               NONE without SQUASH), or a gate pointer
                               inconsistent with the gate kind               */
-  PDN_ERR_HIP = 9          /* a HIP launch failed                              */
+  PDN_ERR_HIP = 9,         /* a HIP launch failed                              */
+  PDN_ERR_SCRATCH = 10     /* pdn_chunk_fwd_noalloc: the problem's workspace
+                              exceeds PDN_NOALLOC_SCRATCH_BYTES              */
 } pdn_status;
 
 typedef enum { PDN_F32 = 0, PDN_BF16 = 1 } pdn_dtype;
@@ -173,6 +178,35 @@ pdn_status pdn_workspace_size(const pdn_problem* problem, int with_bwd,
 pdn_status pdn_chunk_fwd(const pdn_problem* problem, const pdn_inputs* in,
                          pdn_fwd_out* out, void* ws, size_t ws_bytes,
                          void* hip_stream);
+
+/* pdn_chunk_fwd without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  It computes exactly what pdn_chunk_fwd
+ * computes, with the same kernels, using as its workspace a fixed scratch
+ * array of PDN_NOALLOC_SCRATCH_BYTES (64 MiB) that the library holds in
+ * every device it runs on, from the library's loading on that device until
+ * the process ends.  It calls no hipMalloc / hipFree or other allocating
+ * routine; its first call on a device looks up that device's array once.
+ *
+ * Limit: pdn_workspace_size(problem, 0, &n) must give n <=
+ * PDN_NOALLOC_SCRATCH_BYTES, else PDN_ERR_SCRATCH (returned, like every
+ * other validation failure, before any HIP call).  For example, bf16 with
+ * d_k = d_v = 128 and a scalar gate needs about 0.53 KB per token-head:
+ * B*T*H up to about 120k (B=1, T=8192, H=14).
+ *
+ * Sharing: every call on one device uses that device's single array, which
+ * keeps the last call's contents (the forward overwrites every byte it reads
+ * before reading it, so nothing needs clearing).  Calls that overlap in time
+ * on one device -- on different streams, or from different host threads
+ * without ordering -- race on the array and give undefined results; order
+ * them on one stream.  Arguments, outputs and errors otherwise as
+ * pdn_chunk_fwd. */
+#define PDN_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+pdn_status pdn_chunk_fwd_noalloc(const pdn_problem* problem, const pdn_inputs* in,
+                                 pdn_fwd_out* out, void* hip_stream);
+
+/* PDN_NOALLOC_SCRATCH_BYTES of the built library. */
+size_t pdn_noalloc_scratch_bytes(void);
 
 /* pdn_chunk_fwd that also records caller-created HIP events (hipEvent_t
  * handles passed as void*) on `hip_stream` at the stage boundaries, for

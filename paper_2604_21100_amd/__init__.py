@@ -54,7 +54,7 @@ if len(loaded_hip_runtimes()) > 1:
 # ---------------------------------------------------------------- enums
 PDN_OK, PDN_ERR_NULL, PDN_ERR_SHAPE, PDN_ERR_DTYPE, PDN_ERR_UNSUPPORTED, \
     PDN_ERR_ALIGN, PDN_ERR_ALIAS, PDN_ERR_WORKSPACE, PDN_ERR_VALUE, \
-    PDN_ERR_HIP = range(10)
+    PDN_ERR_HIP, PDN_ERR_SCRATCH = range(11)
 PDN_F32, PDN_BF16 = 0, 1
 PDN_GATE_NONE, PDN_GATE_SCALAR, PDN_GATE_CHANNEL = 0, 1, 2
 PDN_PRECOND_SQUASH, PDN_PRECOND_IDENTITY, PDN_PRECOND_EXTERNAL, \
@@ -129,12 +129,18 @@ _lib.pdn_chunk_bwd_train.argtypes = [
     ctypes.POINTER(BwdOut), _vp, ctypes.c_size_t, _vp, ctypes.POINTER(_vp),
     ctypes.c_int]
 _lib.pdn_chunk_bwd_train.restype = ctypes.c_int
+_lib.pdn_chunk_fwd_noalloc.argtypes = [
+    ctypes.POINTER(Problem), ctypes.POINTER(Inputs), ctypes.POINTER(FwdOut),
+    _vp]
+_lib.pdn_chunk_fwd_noalloc.restype = ctypes.c_int
+_lib.pdn_noalloc_scratch_bytes.argtypes = []
+_lib.pdn_noalloc_scratch_bytes.restype = ctypes.c_size_t
 _lib.pdn_status_string.argtypes = [ctypes.c_int]
 _lib.pdn_status_string.restype = ctypes.c_char_p
 _lib.pdn_abi_version.argtypes = []
 _lib.pdn_abi_version.restype = ctypes.c_int
 
-ABI_VERSION = 3   # PDN_ABI_VERSION: the struct layouts mirrored above
+ABI_VERSION = 4   # PDN_ABI_VERSION: the struct layouts mirrored above
 if _lib.pdn_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} implements ABI version "
                       f"{_lib.pdn_abi_version()}, this binding mirrors "
@@ -142,7 +148,9 @@ if _lib.pdn_abi_version() != ABI_VERSION:
 
 EXPORTED = ("pdn_workspace_size", "pdn_chunk_fwd", "pdn_chunk_fwd_events",
             "pdn_chunk_bwd", "pdn_chunk_bwd_events", "pdn_chunk_fwd_train",
-            "pdn_chunk_bwd_train", "pdn_status_string", "pdn_abi_version")
+            "pdn_chunk_bwd_train", "pdn_chunk_fwd_noalloc",
+            "pdn_noalloc_scratch_bytes", "pdn_status_string",
+            "pdn_abi_version")
 FWD_STAGE_EVENTS = 4   # PDN_FWD_STAGE_EVENTS
 BWD_STAGE_EVENTS = 7   # PDN_BWD_STAGE_EVENTS
 FWD_STAGES = ("precond", "chunk_prep", "chunk_scan")
@@ -201,6 +209,18 @@ def pdn_chunk_fwd_events_raw(problem: Problem, inputs: Inputs, out: FwdOut,
     return _lib.pdn_chunk_fwd_events(ctypes.byref(problem),
                                      ctypes.byref(inputs), ctypes.byref(out),
                                      ws, ws_bytes, stream, arr, len(events))
+
+
+def pdn_chunk_fwd_noalloc_raw(problem: Problem, inputs: Inputs, out: FwdOut,
+                              stream: int) -> int:
+    """pdn_chunk_fwd_noalloc with raw pointers; returns the status code."""
+    return _lib.pdn_chunk_fwd_noalloc(ctypes.byref(problem),
+                                      ctypes.byref(inputs), ctypes.byref(out),
+                                      stream)
+
+
+def pdn_noalloc_scratch_bytes() -> int:
+    return _lib.pdn_noalloc_scratch_bytes()
 
 
 def pdn_chunk_bwd_raw(problem: Problem, inputs: Inputs, dO: int, dS_T: int,
@@ -293,6 +313,27 @@ def pdn_chunk_fwd(q, k, v, beta, *, g=None, gate="none", precond="squash",
             [_event_handle(e) if e is not None else None for e in stage_events])
     if st != PDN_OK:
         raise PdnError(st, "pdn_chunk_fwd")
+    return o, S_T, A_T
+
+
+def pdn_chunk_fwd_noalloc(q, k, v, beta, *, o, g=None, gate="none",
+                          precond="squash", beta_p=None, g_p=None,
+                          log_a_scale=None, A0=None, S0=None, ktilde=None,
+                          x=1.5, scale=1.0, chunk=64, ridge=1.0,
+                          knorm="none", S_T=None, A_T=None, stream=None):
+    """pdn_chunk_fwd through the no-allocation entry point: the caller passes
+    every output (o required, S_T / A_T optional) and no workspace; the
+    library uses its fixed per-device scratch.  Returns (o, S_T, A_T)."""
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    prob = make_problem(B, T, H, dk, dv, io=_io_of(q), gate=gate,
+                        precond=precond, x=x, scale=scale, chunk=chunk,
+                        ridge=ridge, knorm=knorm)
+    inp = _inputs(q, k, v, beta, g, beta_p, g_p, log_a_scale, A0, S0, ktilde)
+    out = FwdOut(_ptr(o), _ptr(S_T), _ptr(A_T))
+    st = pdn_chunk_fwd_noalloc_raw(prob, inp, out, _stream(stream, q.device))
+    if st != PDN_OK:
+        raise PdnError(st, "pdn_chunk_fwd_noalloc")
     return o, S_T, A_T
 
 

@@ -16,6 +16,8 @@
 //                       inter-chunk state scan with the chunk output fused in
 //                       (Eq. chunkwise_atk_form; decayed forms of App. D),
 //                       using E = U - W S^T = T (V - (Lam*K) S^T)
+#include <mutex>
+
 #include "pdn_device.hpp"
 #include "pdn_internal.hpp"
 
@@ -1181,6 +1183,30 @@ static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s, hipEvent_t c
 hipError_t launch_forward_parts(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev) {
   if (io_bf16) return a.dk == 64 ? launch_recompute<bf16, 64>(a, s, ev) : launch_recompute<bf16, 128>(a, s, ev);
   return launch_recompute<float, 64>(a, s, ev);
+}
+
+// The workspace of pdn_chunk_fwd_noalloc.  Host code never uses this name
+// as an address (on the host it is only a registration handle): kernels get
+// the device address that noalloc_scratch looks up.
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+hipError_t noalloc_scratch(void** ptr) {
+  static std::mutex mu;
+  static void* addr[kNoallocMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kNoallocMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev, bool train) {

@@ -14,6 +14,9 @@ namespace {
 
 using pdn::kChunk;
 
+static_assert(PDN_NOALLOC_SCRATCH_BYTES == pdn::kNoallocScratchBytes,
+              "the header's scratch size and the library's must agree");
+
 struct Range {
   uintptr_t lo, hi;  // [lo, hi)
 };
@@ -166,6 +169,9 @@ const char* pdn_status_string(pdn_status st) {
     case PDN_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case PDN_ERR_VALUE: return "invalid scalar, enum or gate pointer";
     case PDN_ERR_HIP: return "HIP launch failed";
+    case PDN_ERR_SCRATCH:
+      return "problem needs more workspace than the no-allocation entry point's fixed scratch "
+             "(pdn_noalloc_scratch_bytes(), 64 MiB per device)";
   }
   return "unknown status";
 }
@@ -214,10 +220,12 @@ static void set_residuals(pdn::FwdArgs& f, const pdn::BwdWsLayout& L, char* w) {
 }
 
 // train: the training forward (also leaves the backward's intermediates in
-// the workspace, which then has the backward's size)
+// the workspace, which then has the backward's size).  noalloc: ws and
+// ws_bytes are ignored; the workspace is the device's fixed scratch array,
+// looked up only after every argument has been validated.
 static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out* out,
                                  void* ws, size_t ws_bytes, void* hip_stream,
-                                 hipEvent_t const* ev, bool train) {
+                                 hipEvent_t const* ev, bool train, bool noalloc = false) {
   Sizes s;
   pdn_status st = check_problem(p, &s);
   if (st != PDN_OK) return st;
@@ -236,10 +244,21 @@ static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn
       pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond);
   const size_t need_bytes = train ? LB.total : L.total;
   const bool need_ws = s.tok > 0;
+  if (noalloc) {
+    ws = nullptr;
+    ws_bytes = 0;
+    if (need_ws && need_bytes > pdn::kNoallocScratchBytes) return PDN_ERR_SCRATCH;
+  }
   // the whole declared workspace range must be disjoint from inputs/outputs;
   // its size is checked last
   if ((st = check_aliasing(ins, outs, Buf{ws, need_ws ? static_cast<int64_t>(ws_bytes) : 0})) != PDN_OK)
     return st;
+  if (noalloc && need_ws) {
+    // every argument is valid: the first HIP call of this entry point (the
+    // scratch array belongs to the library, so it overlaps no caller buffer)
+    if (pdn::noalloc_scratch(&ws) != hipSuccess) return PDN_ERR_HIP;
+    ws_bytes = pdn::kNoallocScratchBytes;
+  }
   if (need_ws && (!ws || ws_bytes < need_bytes || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0))
     return PDN_ERR_WORKSPACE;
 
@@ -271,6 +290,13 @@ pdn_status pdn_chunk_fwd(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out
                          size_t ws_bytes, void* hip_stream) {
   return chunk_fwd_impl(p, in, out, ws, ws_bytes, hip_stream, nullptr, false);
 }
+
+pdn_status pdn_chunk_fwd_noalloc(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out* out,
+                                 void* hip_stream) {
+  return chunk_fwd_impl(p, in, out, nullptr, 0, hip_stream, nullptr, false, true);
+}
+
+size_t pdn_noalloc_scratch_bytes(void) { return pdn::kNoallocScratchBytes; }
 
 pdn_status pdn_chunk_fwd_events(const pdn_problem* p, const pdn_inputs* in, pdn_fwd_out* out,
                                 void* ws, size_t ws_bytes, void* hip_stream,

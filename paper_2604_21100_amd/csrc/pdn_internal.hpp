@@ -120,6 +120,16 @@ BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate,
 hipError_t launch_backward(const BwdArgs& a, int io_bf16, hipStream_t stream,
                            hipEvent_t const* ev = nullptr, bool recompute = true);
 
+// Fixed scratch of pdn_chunk_fwd_noalloc (PDN_NOALLOC_SCRATCH_BYTES): a
+// static device array in pdn_fwd.hip, one copy per device.
+constexpr size_t kNoallocScratchBytes = static_cast<size_t>(64) << 20;
+constexpr int kNoallocMaxDevices = 64;
+
+// Device address of the current device's scratch array, looked up with
+// hipGetSymbolAddress on the first call made with that device current and
+// cached per device (thread-safe).  Fails for device ids >= 64.
+hipError_t noalloc_scratch(void** ptr);
+
 // ev: NULL or 4 events recorded at the stage boundaries (see
 // pdn_chunk_fwd_events).  train: also leave the backward's intermediates in
 // the workspace (a's backward fields set).

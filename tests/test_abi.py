@@ -35,7 +35,7 @@ def test_header_symbols_exported():
 
 
 def test_status_strings():
-    for st in range(10):
+    for st in range(11):
         assert pdn.pdn_status_string(st)
     assert pdn.pdn_status_string(0) == "ok"
 
@@ -289,3 +289,46 @@ def test_training_pair_validation():
     assert lib.pdn_chunk_bwd_train(
         ctypes.byref(pf), ctypes.byref(_inputs()), A * 30, None,
         ctypes.byref(bo), A * 64, 0, None, None, 0) == pdn.PDN_ERR_UNSUPPORTED
+
+
+def _fwd_noalloc(prob, inp=None, out=None):
+    if inp is None:
+        inp = _inputs()
+    if out is None:
+        out = pdn.FwdOut(A * 20, A * 21, A * 22)
+    return pdn.pdn_chunk_fwd_noalloc_raw(prob, inp, out, 0)
+
+
+def test_noalloc_rejects_problems_beyond_its_scratch():
+    """The no-allocation forward holds a fixed 64 MiB scratch per device: a
+    problem whose forward workspace is larger is refused with
+    PDN_ERR_SCRATCH before any HIP call (the 1B layer, B=4 T=4096 H=16,
+    needs about 136 MB)."""
+    assert pdn.pdn_noalloc_scratch_bytes() == 64 << 20
+    big = pdn.make_problem(4, 4096, 16, 128, 128, gate="scalar")
+    assert pdn.pdn_workspace_size(big) > pdn.pdn_noalloc_scratch_bytes()
+    assert _fwd_noalloc(big) == pdn.PDN_ERR_SCRATCH
+    assert "scratch" in pdn.pdn_status_string(pdn.PDN_ERR_SCRATCH)
+    # the largest T that fits, and one chunk more, at B=1 H=14 d=128
+    fits = [T for T in range(64, 20000, 64)
+            if pdn.pdn_workspace_size(pdn.make_problem(1, T, 14, 128, 128,
+                                                       gate="scalar"))
+            <= pdn.pdn_noalloc_scratch_bytes()]
+    tmax = max(fits)
+    assert tmax >= 8192
+    over = pdn.make_problem(1, tmax + 64, 14, 128, 128, gate="scalar")
+    assert _fwd_noalloc(over) == pdn.PDN_ERR_SCRATCH
+
+
+def test_noalloc_validates_like_the_forward():
+    """Every argument check of pdn_chunk_fwd runs first, with its codes."""
+    p = _prob()
+    assert _fwd_noalloc(pdn.make_problem(2, 130, 3, 96, 64)) == \
+        pdn.PDN_ERR_UNSUPPORTED
+    assert _fwd_noalloc(p, _inputs(q=None)) == pdn.PDN_ERR_NULL
+    assert _fwd_noalloc(p, _inputs(q=A + 2)) == pdn.PDN_ERR_ALIGN
+    assert _fwd_noalloc(p, out=pdn.FwdOut(None, None, None)) == pdn.PDN_ERR_NULL
+    assert _fwd_noalloc(p, out=pdn.FwdOut(A * 3 + 256, None, None)) == \
+        pdn.PDN_ERR_ALIAS
+    assert _fwd_noalloc(_prob(precond="identity"), _inputs(beta_p=None)) == \
+        pdn.PDN_ERR_VALUE
