@@ -693,7 +693,16 @@ struct ScanCtx {
 // not needed and not loaded.  LA (linear attention, ATQ): no read-key tile;
 // the query tile is the preconditioned query the prep kernel left in the
 // workspace.
-template <bool OUT, bool LA, typename T, int DK, int GATE>
+//
+// PARTS selects which loads to issue (bit mask, 7 = all): 1 the value slab and
+// the read-key rows (for LA the query rows), 2 the query rows and T, 4 P, the
+// decayed write keys and the gate values.  A step issues the loads of the
+// chunk two ahead in these three parts, each right after one of its phases has
+// issued its MFMAs: the per-CU vector memory path accepts one chunk's loads
+// (about 90 KB per workgroup) only about as fast as the step's dependency
+// chain runs, so loads issued as one block stall the wave in front of the
+// chain instead of beside it.
+template <int PARTS, bool OUT, bool LA, typename T, int DK, int GATE>
 __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdArgs& a, int i,
                                           const ScanCtx& x) {
   constexpr int KK = DK / 32, CT = DK / 64;
@@ -718,33 +727,44 @@ __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdAr
   // and so waits for it a step earlier than for the other operands; the
   // memory counter completes in issue order, so any load issued before it
   // would be waited for there too
+  if (PARTS & 1) {
 #pragma unroll
-  for (int j = 0; j < SM::kPer; ++j) {
-    const int idx = x.tid + 256 * j;
-    const uint32_t row = static_cast<uint32_t>(min(idx / SM::kSegs, last));
-    const uint32_t off = (row * static_cast<uint32_t>(HV) + (idx % SM::kSegs) * SM::kVec) * E;
-    f.v[j] = *reinterpret_cast<const float4*>(at_bytes(vb, off));
+    for (int j = 0; j < SM::kPer; ++j) {
+      const int idx = x.tid + 256 * j;
+      const uint32_t row = static_cast<uint32_t>(min(idx / SM::kSegs, last));
+      const uint32_t off = (row * static_cast<uint32_t>(HV) + (idx % SM::kSegs) * SM::kVec) * E;
+      f.v[j] = *reinterpret_cast<const float4*>(at_bytes(vb, off));
+    }
   }
   const uint32_t rr = static_cast<uint32_t>(min(16 * x.w + x.lr, last));
   const uint32_t okq = (rr * static_cast<uint32_t>(ldk) + 8 * x.lg) * E;
   if (LA) {
-    const T* qtb = CH ? qb : static_cast<const T*>(a.Qt) + (x.bh * a.Tpad + t0) * DK;
-    const uint32_t oqt = (rr * static_cast<uint32_t>(DK) + 8 * x.lg) * E;
+    if (PARTS & 1) {
+      const T* qtb = CH ? qb : static_cast<const T*>(a.Qt) + (x.bh * a.Tpad + t0) * DK;
+      const uint32_t oqt = (rr * static_cast<uint32_t>(DK) + 8 * x.lg) * E;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) f.Q[kk] = ld8(at_bytes(qtb, oqt + kk * 32 * E));
+      for (int kk = 0; kk < KK; ++kk) f.Q[kk] = ld8(at_bytes(qtb, oqt + kk * 32 * E));
+    }
   } else {
+    if (PARTS & 1) {
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      f.K[kk] = ld8(at_bytes(kb, okq + kk * 32 * E));
-      if (OUT) f.Q[kk] = ld8(at_bytes(qb, okq + kk * 32 * E));
+      for (int kk = 0; kk < KK; ++kk) f.K[kk] = ld8(at_bytes(kb, okq + kk * 32 * E));
+    }
+    if (OUT && (PARTS & 2)) {
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) f.Q[kk] = ld8(at_bytes(qb, okq + kk * 32 * E));
     }
   }
   const int ra = 16 * x.w + x.lr;
   const uint32_t otp = static_cast<uint32_t>(ra * C + 8 * x.lg) * E;
+  if (PARTS & 2) {
 #pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) {
-    f.Tm[k2] = ld8(at_bytes(tb, otp + k2 * 32 * E));
-    if (OUT) f.P[k2] = ld8(at_bytes(pb, otp + k2 * 32 * E));
+    for (int k2 = 0; k2 < 2; ++k2) f.Tm[k2] = ld8(at_bytes(tb, otp + k2 * 32 * E));
+  }
+  if (!(PARTS & 4)) return;
+  if (OUT) {
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) f.P[k2] = ld8(at_bytes(pb, otp + k2 * 32 * E));
   }
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
@@ -838,8 +858,11 @@ __device__ __forceinline__ void flush_slab_t(T* dst, int64_t ld, const T* src, i
   }
 }
 
-template <bool FULL, bool SAVE, bool OUT, bool LA, typename T, int DK, int GATE>
+// NEXT: also issue the loads of chunk `in` into `fn`, in three parts placed
+// after the MFMAs of each phase (see scan_load).
+template <bool FULL, bool SAVE, bool OUT, bool LA, bool NEXT, typename T, int DK, int GATE>
 __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float4* vnext,
+                                          ScanFrags<T, DK, GATE>& fn, int in,
                                           floatx4 (&st)[DK / 64][2], const FwdArgs& a, int i,
                                           const ScanCtx& x, T* sH, T* sX, T* sE, T* sVt, T* sO) {
   constexpr int KK = DK / 32, CT = DK / 64;
@@ -874,6 +897,10 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
       if (!LA) mma(accX[vt], f.K[kk], bH[vt][kk]);   // linear attention: X = V
       if (OUT) mma(accO[vt], f.Q[kk], bH[vt][kk]);
     }
+  }
+  if (NEXT) scan_load<1, OUT, LA>(fn, a, in, x);
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt) {
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
       accX[vt][ii] = to_f(vv[vt][ii]) - lam[ii] * accX[vt][ii];
@@ -889,13 +916,18 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
   for (int vt = 0; vt < 2; ++vt)
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) bX[vt][k2] = ld8(sw(sX, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
+  floatx4 accE[2];
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt) {
-    floatx4 accE = {0.f, 0.f, 0.f, 0.f};
+    accE[vt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) mma(accE, f.Tm[k2], bX[vt][k2]);
-    st4<T>(sw(sE, LDE, 16 * vt + lr, 16 * w + 4 * lg), accE[0], accE[1], accE[2], accE[3]);
+    for (int k2 = 0; k2 < 2; ++k2) mma(accE[vt], f.Tm[k2], bX[vt][k2]);
   }
+  if (NEXT) scan_load<2, OUT, LA>(fn, a, in, x);
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt)
+    st4<T>(sw(sE, LDE, 16 * vt + lr, 16 * w + 4 * lg), accE[vt][0], accE[vt][1], accE[vt][2],
+           accE[vt][3]);
   lds_barrier();
   // ---- O = scale [ (Lam Q) S^T + P E ];  S^T <- Diag(gamma_C) S^T + (Kt Gamma)^T E
   Frag8<T> fE[2][2];
@@ -912,8 +944,6 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
     // P is causal: for rows < 32 its second slab is zero
     mma(accO[vt], f.P[0], fE[vt][0]);
     mma(accO[vt], f.P[1], fE[vt][1]);
-    st4<T>(sw(sO, LDE, 16 * vt + lr, 16 * w + 4 * lg), a.scale * accO[vt][0], a.scale * accO[vt][1],
-           a.scale * accO[vt][2], a.scale * accO[vt][3]);
   }
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
@@ -928,9 +958,18 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
       }
       mma(st[ct][vt], f.G[ct][0], fE[vt][0]);
       mma(st[ct][vt], f.G[ct][1], fE[vt][1]);
+    }
+  if (NEXT) scan_load<4, OUT, LA>(fn, a, in, x);
+#pragma unroll
+  for (int vt = 0; vt < 2 && OUT; ++vt)
+    st4<T>(sw(sO, LDE, 16 * vt + lr, 16 * w + 4 * lg), a.scale * accO[vt][0], a.scale * accO[vt][1],
+           a.scale * accO[vt][2], a.scale * accO[vt][3]);
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int vt = 0; vt < 2; ++vt)
       st4<T>(sw(sH, LDH, 16 * vt + lr, 16 * (w * CT + ct) + 4 * lg), st[ct][vt][0], st[ct][vt][1],
              st[ct][vt][2], st[ct][vt][3]);
-    }
   if (vnext) stage_values<T>(*reinterpret_cast<const float4(*)[SlabMap<T>::kPer]>(vnext), sVt, x.tid);
   lds_barrier();
 }
@@ -995,32 +1034,28 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   ScanFrags<T, DK, GATE> f0, f1, f2;
   const int last = a.NT - 1;
   const int NF = static_cast<int>(a.T / C);   // full chunks
-  scan_load<OUT, LA>(f0, a, 0, x);
-  scan_load<OUT, LA>(f1, a, min(1, last), x);
+  scan_load<7, OUT, LA>(f0, a, 0, x);
+  scan_load<7, OUT, LA>(f1, a, min(1, last), x);
   stage_values<T>(f0.v, sVt, x.tid);
   __syncthreads();
   int i = 0;
   for (; i + 2 < NF; i += 3) {
-    scan_load<OUT, LA>(f2, a, i + 2, x);
-    scan_step<true, SAVE, OUT, LA>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
-    scan_load<OUT, LA>(f0, a, min(i + 3, last), x);
-    scan_step<true, SAVE, OUT, LA>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
-    scan_load<OUT, LA>(f1, a, min(i + 4, last), x);
-    scan_step<true, SAVE, OUT, LA>(f2, f0.v, st, a, i + 2, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE, OUT, LA, true>(f0, f1.v, f2, i + 2, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE, OUT, LA, true>(f1, f2.v, f0, min(i + 3, last), st, a, i + 1, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE, OUT, LA, true>(f2, f0.v, f1, min(i + 4, last), st, a, i + 2, x, sH, sX, sE, sVt, sO);
   }
   // f0, f1 hold chunks i, i + 1 (clamped to the last chunk)
   if (NF - i == 2) {
-    scan_load<OUT, LA>(f2, a, min(i + 2, last), x);
-    scan_step<true, SAVE, OUT, LA>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
-    scan_step<true, SAVE, OUT, LA>(f1, f2.v, st, a, i + 1, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE, OUT, LA, true>(f0, f1.v, f2, min(i + 2, last), st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE, OUT, LA, false>(f1, f2.v, f0, 0, st, a, i + 1, x, sH, sX, sE, sVt, sO);
     i += 2;
-    if (i < a.NT) scan_step<false, SAVE, OUT, LA>(f2, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+    if (i < a.NT) scan_step<false, SAVE, OUT, LA, false>(f2, nullptr, f0, 0, st, a, i, x, sH, sX, sE, sVt, sO);
   } else if (NF - i == 1) {
-    scan_step<true, SAVE, OUT, LA>(f0, f1.v, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<true, SAVE, OUT, LA, false>(f0, f1.v, f2, 0, st, a, i, x, sH, sX, sE, sVt, sO);
     i += 1;
-    if (i < a.NT) scan_step<false, SAVE, OUT, LA>(f1, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+    if (i < a.NT) scan_step<false, SAVE, OUT, LA, false>(f1, nullptr, f2, 0, st, a, i, x, sH, sX, sE, sVt, sO);
   } else if (i < a.NT) {
-    scan_step<false, SAVE, OUT, LA>(f0, nullptr, st, a, i, x, sH, sX, sE, sVt, sO);
+    scan_step<false, SAVE, OUT, LA, false>(f0, nullptr, f1, 0, st, a, i, x, sH, sX, sE, sVt, sO);
   }
   if (OUT) flush_output<false, T>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
   if (a.S_T) {
