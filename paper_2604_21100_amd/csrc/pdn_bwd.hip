@@ -41,7 +41,7 @@
 
 namespace pdn {
 
-constexpr int C = kChunk;
+constexpr int C = 64;  // the backward kernels are built for 64-token chunks
 constexpr int BVB = 32;  // value columns per workgroup in the reverse scan
 
 template <typename T>
@@ -1693,7 +1693,7 @@ static size_t align256b(size_t x) { return (x + 255) & ~static_cast<size_t>(255)
 
 BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond) {
   BwdWsLayout L{};
-  L.f = fwd_ws_layout(BH, NT, dk, esz, gate, precond);
+  L.f = fwd_ws_layout(BH, NT, dk, esz, gate, precond, C);
   size_t off = L.f.total;
   auto take = [&](size_t bytes) { const size_t o = off; off = align256b(off + bytes); return o; };
   const size_t bh = static_cast<size_t>(BH), nt = static_cast<size_t>(NT), tp = nt * C;

@@ -23,13 +23,12 @@
 
 namespace pdn {
 
-constexpr int C = kChunk;
 
 // ---------------------------------------------------------------- K1
 // The chunk's affine summary: A_end = exp(sum gP) A_start + L with
 // L = sum_r betaP_r exp(GP_end - GP_r) k_r^2, GP the in-chunk prefix of gP.
 // Rows are weighted in parallel, then reduced per channel.
-template <typename T, int DK>
+template <typename T, int DK, int C>
 __global__ __launch_bounds__(256) void k1_precond_summary(FwdArgs a) {
   constexpr int VEC = 16 / sizeof(T);
   constexpr int VPR = DK / VEC;       // 16-byte vectors per row
@@ -53,7 +52,7 @@ __global__ __launch_bounds__(256) void k1_precond_summary(FwdArgs a) {
       if (r >= off) gp += y;
     }
     const float gend = __shfl(gp, 63, 64);
-    sW[r] = r < n ? a.beta_p[sidx] * fast_exp(gend - gp) : 0.f;
+    if (r < C) sW[r] = r < n ? a.beta_p[sidx] * fast_exp(gend - gp) : 0.f;
     if (r == 0) a.sumD[bh * a.NT + i] = gend;
   }
   __syncthreads();
@@ -131,7 +130,7 @@ __device__ __forceinline__ float* k2swf(float* base, int ld, int row, int col) {
 // That keeps the block under 80 KB, two per CU.  (For the other gates the
 // HBM reads of the transposed query cost more than a third block per CU
 // gains.)
-template <typename T, int DK, int GATE, int PREC>
+template <typename T, int DK, int GATE, int PREC, int C>
 struct K2Smem {
   static constexpr int LDK = DK + 8;          // padded row (elements)
   static constexpr int LDA = C + 4;           // fp32 C x C rows
@@ -153,9 +152,13 @@ struct K2Smem {
 // BWD: also write the operand layouts the backward kernels read (P^T, M^T,
 // write-key rows, write-key rows decayed to the chunk end, (Lam o Q)^T and
 // -(Lam o K)^T; Lam the scalar or per-channel in-chunk decay).
-template <typename T, int DK, int GATE, int PREC, bool BWD>
+template <typename T, int DK, int GATE, int PREC, bool BWD, int C>
 __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
-  using SM = K2Smem<T, DK, GATE, PREC>;
+  using SM = K2Smem<T, DK, GATE, PREC, C>;
+  // row blocks of 16 tokens: wave w owns block w (C = 32: waves 2, 3 only
+  // take part in the column-wise phases)
+  constexpr int NB = C / 16;
+  static_assert(NB == 2 || NB == 4, "chunk of 32 or 64 tokens");
   constexpr bool NOQ = SM::NOQ;
   constexpr int LDK = SM::LDK, LDA = SM::LDA;
   __shared__ __attribute__((aligned(16))) char smem[SM::kTotal];
@@ -239,16 +242,19 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
 
   // ---- gate prefix and preconditioner prefix
   if (GATE == kGateScalar && w == 0) {
-    float x = sGraw[l];
+    float x = l < C ? sGraw[l] : 0.f;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
       const float y = __shfl_up(x, off, 64);
       if (l >= off) x += y;
     }
-    sG[l] = x;
-    a.G[bh * a.Tpad + t0 + l] = x;
-    sLam[l] = fast_exp(x);
-    sWt[l] = fast_exp(__shfl(x, C - 1, 64) - x);
+    const float xC = __shfl(x, C - 1, 64);
+    if (l < C) {
+      sG[l] = x;
+      a.G[bh * a.Tpad + t0 + l] = x;
+      sLam[l] = fast_exp(x);
+      sWt[l] = fast_exp(xC - x);
+    }
   }
   if (tid < DK) {
     const int c = tid;
@@ -307,7 +313,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         // the rows' m from the stored keys, then the keys recomputed exactly
         // and scaled once
         __syncthreads();
-        {
+        if ((tid >> 2) < C) {
           constexpr int PART = DK / 4;
           const int r = tid >> 2, part = tid & 3;
           float m = 0.f;
@@ -360,7 +366,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         A = eg[j] * A + bpr[j] * kv * kv;
       }
       __syncthreads();
-      {
+      if ((tid >> 2) < C) {
         constexpr int PART = DK / 4;
         const int r = tid >> 2, part = tid & 3;
         float sum = 0.f;
@@ -423,10 +429,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   }
 
   // ---- interaction matrices on MFMA: wave w owns row block w
-  floatx4 accA[4], accP[4];
+  floatx4 accA[NB], accP[NB];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) { accA[j] = floatx4{0.f, 0.f, 0.f, 0.f}; accP[j] = accA[j]; }
-  {
+  for (int j = 0; j < NB; ++j) { accA[j] = floatx4{0.f, 0.f, 0.f, 0.f}; accP[j] = accA[j]; }
+  if (NB == 4 || w < NB) {
     const int r = 16 * w + lr;  // A-operand row of this lane
     // NOQ: this row's query fragments straight from HBM, once
     Frag8<T> fqr[DK / 32];
@@ -439,7 +445,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       }
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < NB; ++j) {
       if (j > w) break;
       const int t = 16 * j + lr;  // B-operand column of this lane
 #pragma unroll
@@ -467,10 +473,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     }
   }
   // masks, beta and scalar decay; P goes straight to the workspace
-  {
+  if (NB == 4 || w < NB) {
     T* P = static_cast<T*>(a.Pm) + (bh * a.NT + i) * (int64_t)(C * C);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < NB; ++j) {
       const int t = 16 * j + lr;
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
@@ -557,15 +563,15 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   }
   __syncthreads();  // sK / sQ are free from here on
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (j > w) break;
+  for (int j = 0; j < NB; ++j) {
+    if (j > w || !(NB == 4 || w < NB)) break;
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) sA[(16 * w + 4 * lg + ii) * LDA + 16 * j + lr] = accA[j][ii];
   }
   __syncthreads();
 
   // ---- X = (I + At)^{-1}: diagonal 16x16 blocks by forward substitution
-  if (lg == 0) {
+  if ((NB == 4 || w < NB) && lg == 0) {
     const int col = lr;
     const float* Ab = sA + (16 * w) * LDA + 16 * w;
     float x[16];
@@ -583,9 +589,9 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   // off-diagonal blocks, by distance from the diagonal:
   //   X_ij = -X_ii * sum_{j <= m < i} At_im X_mj
   float* Yw = sY + w * 16 * 17;
-  for (int d = 1; d < 4; ++d) {
+  for (int d = 1; d < NB; ++d) {
     const int j = w, ib = w + d;
-    const bool active = ib < 4;
+    const bool active = ib < NB;
     floatx4 y = {0.f, 0.f, 0.f, 0.f};
     if (active) {
       for (int kb = 0; kb < 4 * d; ++kb) {
@@ -614,10 +620,11 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   // ---- T = X Diag(beta) (block-lower; upper blocks are zero)
   {
     T* Tout = static_cast<T*>(a.Tm) + (bh * a.NT + i) * (int64_t)(C * C);
-    static_assert((C * C / 8) % 256 == 0, "whole rounds of 256 threads");
+    constexpr int NV = C * C / 8;
 #pragma unroll
-    for (int jj = 0; jj < (C * C / 8) / 256; ++jj) {
+    for (int jj = 0; jj < (NV + 255) / 256; ++jj) {
       const int idx = tid + 256 * jj;
+      if (NV % 256 != 0 && idx >= NV) break;
       const int r = idx / (C / 8), t0v = (idx % (C / 8)) * 8;
       Frag8<T> f;
 #pragma unroll
@@ -632,10 +639,11 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   if (BWD) {
     const int64_t cc = (bh * a.NT + i) * (int64_t)(C * C);
     T* MtT = static_cast<T*>(a.MtT) + cc;
-    static_assert((C * C / 8) % 256 == 0, "whole rounds of 256 threads");
+    constexpr int NV = C * C / 8;
 #pragma unroll
-    for (int jj = 0; jj < (C * C / 8) / 256; ++jj) {
+    for (int jj = 0; jj < (NV + 255) / 256; ++jj) {
       const int idx = tid + 256 * jj;
+      if (NV % 256 != 0 && idx >= NV) break;
       const int r = idx / (C / 8), t0v = (idx % (C / 8)) * 8;
       Frag8<T> ft;
 #pragma unroll
@@ -655,13 +663,23 @@ constexpr int BV = 32;  // value columns per workgroup
 
 // One thread's share of a chunk's C x BV value (or output) slab, as 16-byte
 // vectors: vector j of thread tid covers row idx / kSegs, elements
-// [(idx % kSegs) * kVec, + kVec) with idx = tid + 256 j.
-template <typename T>
+// [(idx % kSegs) * kVec, + kVec) with idx = tid + 256 j, for idx < kN (at
+// C = 32 in bf16 only the first half of the threads have a vector).
+template <typename T, int C>
 struct SlabMap {
   static constexpr int kVec = 16 / static_cast<int>(sizeof(T));
   static constexpr int kSegs = BV / kVec;
-  static constexpr int kPer = C * kSegs / 256;
+  static constexpr int kN = C * kSegs;
+  static constexpr int kPer = (kN + 255) / 256;
+  static constexpr bool kWhole = kN % 256 == 0;
 };
+
+// sw() for the [v][t] slabs of C token columns: the XOR keeps the column
+// inside the C columns of a row (C = 64: the same permutation as sw())
+template <int COLS, typename T>
+__device__ __forceinline__ T* swv(T* base, int ld, int row, int col) {
+  return base + row * ld + (col ^ (((row >> 3) & (COLS / 16 - 1) & 3) << 4));
+}
 
 // Operands one wave needs for one chunk, loaded two chunks ahead of use.
 // A-operand rows: token 16w + lr of the chunk; decayed write keys: rows
@@ -673,11 +691,11 @@ struct SlabMap {
 // Rows past the end of the sequence (last chunk only) are loaded from the
 // last valid row instead of being zeroed: their T columns and rows are zero
 // (beta = 0 on padded rows), so they cannot reach any stored output.
-template <typename T, int DK, int GATE>
+template <typename T, int DK, int GATE, int C>
 struct ScanFrags {
-  static constexpr int KK = DK / 32, CT = DK / 64;
-  Frag8<T> K[KK], Q[KK], Tm[2], P[2], G[CT][2];
-  float4 v[SlabMap<T>::kPer];                      // value slab share
+  static constexpr int KK = DK / 32, CT = DK / 64, KC = C / 32;
+  Frag8<T> K[KK], Q[KK], Tm[KC], P[KC], G[CT][KC];
+  float4 v[SlabMap<T, C>::kPer];                   // value slab share
   float g[GATE == kGateScalar ? 4 : 1];            // G of rows 16w + 4lg + ii
   float gC[GATE == kGateChannel ? CT : 1][GATE == kGateNone ? 1 : 4];  // G at the chunk end
 };
@@ -702,12 +720,14 @@ struct ScanCtx {
 // (about 90 KB per workgroup) only about as fast as the step's dependency
 // chain runs, so loads issued as one block stall the wave in front of the
 // chain instead of beside it.
-template <int PARTS, bool OUT, bool LA, typename T, int DK, int GATE>
-__device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdArgs& a, int i,
+template <int PARTS, bool OUT, bool LA, typename T, int DK, int GATE, int C>
+__device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE, C>& f, const FwdArgs& a, int i,
                                           const ScanCtx& x) {
-  constexpr int KK = DK / 32, CT = DK / 64;
+  constexpr int KK = DK / 32, CT = DK / 64, KC = C / 32, NB = C / 16;
   constexpr uint32_t E = sizeof(T);
-  using SM = SlabMap<T>;
+  using SM = SlabMap<T, C>;
+  // waves past the chunk's row blocks (C = 32: waves 2, 3) load no rows
+  const bool rows = NB == 4 || x.w < NB;
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int last = static_cast<int>(min<int64_t>(C, a.T - t0)) - 1;
   const int64_t HD = a.H * (int64_t)DK, HV = a.H * (int64_t)a.dv;
@@ -731,6 +751,7 @@ __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdAr
 #pragma unroll
     for (int j = 0; j < SM::kPer; ++j) {
       const int idx = x.tid + 256 * j;
+      if (!SM::kWhole && idx >= SM::kN) break;
       const uint32_t row = static_cast<uint32_t>(min(idx / SM::kSegs, last));
       const uint32_t off = (row * static_cast<uint32_t>(HV) + (idx % SM::kSegs) * SM::kVec) * E;
       f.v[j] = *reinterpret_cast<const float4*>(at_bytes(vb, off));
@@ -738,7 +759,10 @@ __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdAr
   }
   const uint32_t rr = static_cast<uint32_t>(min(16 * x.w + x.lr, last));
   const uint32_t okq = (rr * static_cast<uint32_t>(ldk) + 8 * x.lg) * E;
-  if (LA) {
+  if (!rows) {
+    // no rows of this chunk: only the decayed write keys and the chunk-end
+    // gate values below
+  } else if (LA) {
     if (PARTS & 1) {
       const T* qtb = CH ? qb : static_cast<const T*>(a.Qt) + (x.bh * a.Tpad + t0) * DK;
       const uint32_t oqt = (rr * static_cast<uint32_t>(DK) + 8 * x.lg) * E;
@@ -757,25 +781,25 @@ __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE>& f, const FwdAr
   }
   const int ra = 16 * x.w + x.lr;
   const uint32_t otp = static_cast<uint32_t>(ra * C + 8 * x.lg) * E;
-  if (PARTS & 2) {
+  if ((PARTS & 2) && rows) {
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) f.Tm[k2] = ld8(at_bytes(tb, otp + k2 * 32 * E));
+    for (int k2 = 0; k2 < KC; ++k2) f.Tm[k2] = ld8(at_bytes(tb, otp + k2 * 32 * E));
   }
   if (!(PARTS & 4)) return;
-  if (OUT) {
+  if (OUT && rows) {
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) f.P[k2] = ld8(at_bytes(pb, otp + k2 * 32 * E));
+    for (int k2 = 0; k2 < KC; ++k2) f.P[k2] = ld8(at_bytes(pb, otp + k2 * 32 * E));
   }
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2)
+    for (int k2 = 0; k2 < KC; ++k2)
       f.G[ct][k2] = ld8(at_bytes(gb, static_cast<uint32_t>((16 * (x.w * CT + ct) + x.lr) * C + 8 * x.lg + k2 * 32) * E));
   if (GATE == kGateScalar) {
     const float* gs = a.G + x.bh * a.Tpad + t0;
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii)
-      f.g[ii] = *at_bytes(gs, static_cast<uint32_t>(16 * x.w + 4 * x.lg + ii) * 4u);
+      f.g[ii] = rows ? *at_bytes(gs, static_cast<uint32_t>(16 * x.w + 4 * x.lg + ii) * 4u) : 0.f;
     f.gC[0][0] = gs[C - 1];
   }
   if (GATE == kGateChannel) {
@@ -794,28 +818,29 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // value slab share -> sVt[v][t] (transposed)
-template <typename T>
-__device__ __forceinline__ void stage_values(const float4 (&v)[SlabMap<T>::kPer], T* sVt,
+template <typename T, int C>
+__device__ __forceinline__ void stage_values(const float4 (&v)[SlabMap<T, C>::kPer], T* sVt,
                                              int tid) {
-  using SM = SlabMap<T>;
+  using SM = SlabMap<T, C>;
   constexpr int LDE = C + 8;
 #pragma unroll
   for (int j = 0; j < SM::kPer; ++j) {
     const int idx = tid + 256 * j;
+    if (!SM::kWhole && idx >= SM::kN) break;
     const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
     const float4 raw = pin_here(v[j]);
     const T* e = reinterpret_cast<const T*>(&raw);
 #pragma unroll
-    for (int s = 0; s < SM::kVec; ++s) *sw(sVt, LDE, c0 + s, row) = e[s];
+    for (int s = 0; s < SM::kVec; ++s) *swv<C>(sVt, LDE, c0 + s, row) = e[s];
   }
 }
 
 // sO[v][t] -> o rows of chunk i (coalesced 16-byte stores); n valid rows
 // (ALL: the whole chunk, no row check around the stores)
-template <bool ALL, typename T>
+template <bool ALL, typename T, int C>
 __device__ __forceinline__ void flush_output(const FwdArgs& a, int i, int n, const T* sO,
                                              const ScanCtx& x) {
-  using SM = SlabMap<T>;
+  using SM = SlabMap<T, C>;
   constexpr int LDE = C + 8;
   if (!a.o) return;
   const int64_t t0 = static_cast<int64_t>(i) * C;
@@ -824,11 +849,12 @@ __device__ __forceinline__ void flush_output(const FwdArgs& a, int i, int n, con
 #pragma unroll
   for (int j = 0; j < SM::kPer; ++j) {
     const int idx = x.tid + 256 * j;
+    if (!SM::kWhole && idx >= SM::kN) break;
     const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
     float4 pk;
     T* e = reinterpret_cast<T*>(&pk);
 #pragma unroll
-    for (int s = 0; s < SM::kVec; ++s) e[s] = *sw(sO, LDE, c0 + s, row);
+    for (int s = 0; s < SM::kVec; ++s) e[s] = *swv<C>(sO, LDE, c0 + s, row);
     if (ALL || row < n)
       *reinterpret_cast<float4*>(at_bytes(ob, (static_cast<uint32_t>(row) * static_cast<uint32_t>(HV) + c0) *
                                                   static_cast<uint32_t>(sizeof(T)))) = pk;
@@ -844,30 +870,33 @@ __device__ __forceinline__ void flush_output(const FwdArgs& a, int i, int n, con
 // thread: no loop or branch around the stores inside the scan step)
 template <int NROWS, typename T>
 __device__ __forceinline__ void flush_slab_t(T* dst, int64_t ld, const T* src, int lds, int tid) {
-  using SM = SlabMap<T>;
-  static_assert(NROWS * SM::kSegs % 256 == 0, "whole rounds of 256 threads");
+  using SM = SlabMap<T, NROWS>;
 #pragma unroll
-  for (int j = 0; j < NROWS * SM::kSegs / 256; ++j) {
+  for (int j = 0; j < SM::kPer; ++j) {
     const int idx = tid + 256 * j;
+    if (!SM::kWhole && idx >= SM::kN) break;
     const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
     float4 pk;
     T* e = reinterpret_cast<T*>(&pk);
 #pragma unroll
-    for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = *sw(src, lds, c0 + s2, row);
+    for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = *swv<NROWS>(src, lds, c0 + s2, row);
     *reinterpret_cast<float4*>(dst + row * ld + c0) = pk;
   }
 }
 
 // NEXT: also issue the loads of chunk `in` into `fn`, in three parts placed
-// after the MFMAs of each phase (see scan_load).
-template <bool FULL, bool SAVE, bool OUT, bool LA, bool NEXT, typename T, int DK, int GATE>
-__device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float4* vnext,
-                                          ScanFrags<T, DK, GATE>& fn, int in,
+// after the MFMAs of each phase (see scan_load).  Waves past the chunk's row
+// blocks (C = 32: waves 2, 3) skip the row phases and take part in the state
+// update only.
+template <bool FULL, bool SAVE, bool OUT, bool LA, bool NEXT, typename T, int DK, int GATE, int C>
+__device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE, C>& f, const float4* vnext,
+                                          ScanFrags<T, DK, GATE, C>& fn, int in,
                                           floatx4 (&st)[DK / 64][2], const FwdArgs& a, int i,
                                           const ScanCtx& x, T* sH, T* sX, T* sE, T* sVt, T* sO) {
-  constexpr int KK = DK / 32, CT = DK / 64;
+  constexpr int KK = DK / 32, CT = DK / 64, KC = C / 32, NB = C / 16;
   constexpr int LDH = DK + 8, LDE = C + 8;
   const int w = x.w, lr = x.lr, lg = x.lg;
+  const bool rows = NB == 4 || w < NB;
   float lam[4];
 #pragma unroll
   for (int ii = 0; ii < 4; ++ii) lam[ii] = GATE == kGateScalar ? fast_exp(f.g[ii]) : 1.f;
@@ -878,12 +907,14 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) bH[vt][kk] = ld8(sw(sH, LDH, 16 * vt + lr, kk * 32 + 8 * lg));
   typename Vec4<T>::type vv[2];
+  if (rows) {
 #pragma unroll
-  for (int vt = 0; vt < 2; ++vt)
-    vv[vt] = *reinterpret_cast<const typename Vec4<T>::type*>(sw(sVt, LDE, 16 * vt + lr, 16 * w + 4 * lg));
+    for (int vt = 0; vt < 2; ++vt)
+      vv[vt] = *reinterpret_cast<const typename Vec4<T>::type*>(swv<C>(sVt, LDE, 16 * vt + lr, 16 * w + 4 * lg));
+  }
   // the flushes' LDS reads go after this phase's operand reads (LDS reads
   // complete in issue order)
-  if (OUT && i > 0) flush_output<true, T>(a, i - 1, C, sO, x);   // only full chunks precede this one
+  if (OUT && i > 0) flush_output<true, T, C>(a, i - 1, C, sO, x);   // only full chunks precede this one
   if (SAVE)  // chunk-start state S^T of this chunk, rows c, columns of the slab
     flush_slab_t<DK>(static_cast<T*>(a.Hs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv, sH,
                      LDH, x.tid);
@@ -892,6 +923,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
   for (int vt = 0; vt < 2; ++vt) {
     accX[vt] = floatx4{0.f, 0.f, 0.f, 0.f};
     accO[vt] = accX[vt];
+    if (!rows) continue;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       if (!LA) mma(accX[vt], f.K[kk], bH[vt][kk]);   // linear attention: X = V
@@ -899,51 +931,57 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
     }
   }
   if (NEXT) scan_load<1, OUT, LA>(fn, a, in, x);
+  if (rows) {
 #pragma unroll
-  for (int vt = 0; vt < 2; ++vt) {
+    for (int vt = 0; vt < 2; ++vt) {
 #pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-      accX[vt][ii] = to_f(vv[vt][ii]) - lam[ii] * accX[vt][ii];
-      if (OUT) accO[vt][ii] *= lam[ii];
+      for (int ii = 0; ii < 4; ++ii) {
+        accX[vt][ii] = to_f(vv[vt][ii]) - lam[ii] * accX[vt][ii];
+        if (OUT) accO[vt][ii] *= lam[ii];
+      }
+      st4<T>(swv<C>(sX, LDE, 16 * vt + lr, 16 * w + 4 * lg), accX[vt][0], accX[vt][1], accX[vt][2],
+             accX[vt][3]);
     }
-    st4<T>(sw(sX, LDE, 16 * vt + lr, 16 * w + 4 * lg), accX[vt][0], accX[vt][1], accX[vt][2],
-           accX[vt][3]);
   }
   lds_barrier();
   // ---- E = T X
-  Frag8<T> bX[2][2];
-#pragma unroll
-  for (int vt = 0; vt < 2; ++vt)
-#pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) bX[vt][k2] = ld8(sw(sX, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
   floatx4 accE[2];
 #pragma unroll
-  for (int vt = 0; vt < 2; ++vt) {
-    accE[vt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int vt = 0; vt < 2; ++vt) accE[vt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  if (rows) {
+    Frag8<T> bX[2][KC];
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) mma(accE[vt], f.Tm[k2], bX[vt][k2]);
+    for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+      for (int k2 = 0; k2 < KC; ++k2) bX[vt][k2] = ld8(swv<C>(sX, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
+#pragma unroll
+    for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+      for (int k2 = 0; k2 < KC; ++k2) mma(accE[vt], f.Tm[k2], bX[vt][k2]);
   }
   if (NEXT) scan_load<2, OUT, LA>(fn, a, in, x);
+  if (rows) {
 #pragma unroll
-  for (int vt = 0; vt < 2; ++vt)
-    st4<T>(sw(sE, LDE, 16 * vt + lr, 16 * w + 4 * lg), accE[vt][0], accE[vt][1], accE[vt][2],
-           accE[vt][3]);
+    for (int vt = 0; vt < 2; ++vt)
+      st4<T>(swv<C>(sE, LDE, 16 * vt + lr, 16 * w + 4 * lg), accE[vt][0], accE[vt][1], accE[vt][2],
+             accE[vt][3]);
+  }
   lds_barrier();
   // ---- O = scale [ (Lam Q) S^T + P E ];  S^T <- Diag(gamma_C) S^T + (Kt Gamma)^T E
-  Frag8<T> fE[2][2];
+  Frag8<T> fE[2][KC];
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt)
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) fE[vt][k2] = ld8(sw(sE, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
+    for (int k2 = 0; k2 < KC; ++k2) fE[vt][k2] = ld8(swv<C>(sE, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
   if (SAVE) {  // E rows of this chunk (whole chunk: padded rows included)
     const int64_t r0 = (x.bh * a.Tpad + static_cast<int64_t>(i) * C) * a.dv + x.v0;
     flush_slab_t<C>(static_cast<T*>(a.Er) + r0, a.dv, sE, LDE, x.tid);
   }
+  if (OUT && rows) {
 #pragma unroll
-  for (int vt = 0; vt < 2 && OUT; ++vt) {
-    // P is causal: for rows < 32 its second slab is zero
-    mma(accO[vt], f.P[0], fE[vt][0]);
-    mma(accO[vt], f.P[1], fE[vt][1]);
+    for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+      for (int k2 = 0; k2 < KC; ++k2) mma(accO[vt], f.P[k2], fE[vt][k2]);   // P is causal
   }
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
@@ -956,32 +994,34 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE>& f, const float
         if (GATE == kGateChannel) gam = fast_exp(f.gC[ct][ii]);
         st[ct][vt][ii] *= gam;
       }
-      mma(st[ct][vt], f.G[ct][0], fE[vt][0]);
-      mma(st[ct][vt], f.G[ct][1], fE[vt][1]);
+#pragma unroll
+      for (int k2 = 0; k2 < KC; ++k2) mma(st[ct][vt], f.G[ct][k2], fE[vt][k2]);
     }
   if (NEXT) scan_load<4, OUT, LA>(fn, a, in, x);
+  if (OUT && rows) {
 #pragma unroll
-  for (int vt = 0; vt < 2 && OUT; ++vt)
-    st4<T>(sw(sO, LDE, 16 * vt + lr, 16 * w + 4 * lg), a.scale * accO[vt][0], a.scale * accO[vt][1],
-           a.scale * accO[vt][2], a.scale * accO[vt][3]);
+    for (int vt = 0; vt < 2; ++vt)
+      st4<T>(swv<C>(sO, LDE, 16 * vt + lr, 16 * w + 4 * lg), a.scale * accO[vt][0], a.scale * accO[vt][1],
+             a.scale * accO[vt][2], a.scale * accO[vt][3]);
+  }
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
     for (int vt = 0; vt < 2; ++vt)
       st4<T>(sw(sH, LDH, 16 * vt + lr, 16 * (w * CT + ct) + 4 * lg), st[ct][vt][0], st[ct][vt][1],
              st[ct][vt][2], st[ct][vt][3]);
-  if (vnext) stage_values<T>(*reinterpret_cast<const float4(*)[SlabMap<T>::kPer]>(vnext), sVt, x.tid);
+  if (vnext) stage_values<T, C>(*reinterpret_cast<const float4(*)[SlabMap<T, C>::kPer]>(vnext), sVt, x.tid);
   lds_barrier();
 }
 
 // SAVE: also write the chunk-start states and the E rows the backward
 // reads.  OUT: compute and write the output (without it, queries and P are
 // neither loaded nor used: the backward's recompute).
-template <typename T, int DK, int GATE, bool SAVE, bool OUT, bool LA = false>
+template <typename T, int DK, int GATE, bool SAVE, bool OUT, bool LA, int C>
 __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   constexpr int CT = DK / 64;       // state row tiles per wave
   constexpr int LDH = DK + 8, LDE = C + 8;
-  // [v][.] slabs, addressed through sw() (bank-spread)
+  // [v][.] slabs, addressed through sw() / swv() (bank-spread)
   __shared__ __attribute__((aligned(16))) T sH[BV * LDH];   // io copy of the S^T slab, [v][c]
   __shared__ __attribute__((aligned(16))) T sX[BV * LDE];   // X = V - Lam K S^T, [v][t]
   __shared__ __attribute__((aligned(16))) T sE[BV * LDE];   // E = T X, [v][t]
@@ -1031,12 +1071,12 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   // the last chunk), so every path into the loop header has the same loads
   // in flight and the compiler's wait counts stay exact.  A ragged last chunk
   // runs after it.
-  ScanFrags<T, DK, GATE> f0, f1, f2;
+  ScanFrags<T, DK, GATE, C> f0, f1, f2;
   const int last = a.NT - 1;
   const int NF = static_cast<int>(a.T / C);   // full chunks
   scan_load<7, OUT, LA>(f0, a, 0, x);
   scan_load<7, OUT, LA>(f1, a, min(1, last), x);
-  stage_values<T>(f0.v, sVt, x.tid);
+  stage_values<T, C>(f0.v, sVt, x.tid);
   __syncthreads();
   int i = 0;
   for (; i + 2 < NF; i += 3) {
@@ -1057,7 +1097,7 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   } else if (i < a.NT) {
     scan_step<false, SAVE, OUT, LA, false>(f0, nullptr, f1, 0, st, a, i, x, sH, sX, sE, sVt, sO);
   }
-  if (OUT) flush_output<false, T>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
+  if (OUT) flush_output<false, T, C>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
   if (a.S_T) {
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
@@ -1081,7 +1121,7 @@ __global__ void k0_copy_states(FwdArgs a, int64_t nS, int64_t nA) {
 // ---------------------------------------------------------------- host side
 static size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
-WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precond) {
+WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precond, int C) {
   WsLayout L{};
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t o = off; off = align256(off + bytes); return o; };
@@ -1105,35 +1145,35 @@ WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precon
   return L;
 }
 
-template <typename T, int DK, int GATE, int PREC, bool BWD>
+template <typename T, int DK, int GATE, int PREC, bool BWD, int C>
 static hipError_t launch_k2(const FwdArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((k2_chunk_prep<T, DK, GATE, PREC, BWD>), dim3(static_cast<unsigned>(a.BH * a.NT)),
+  hipLaunchKernelGGL((k2_chunk_prep<T, DK, GATE, PREC, BWD, C>), dim3(static_cast<unsigned>(a.BH * a.NT)),
                      dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
-template <typename T, int DK, int GATE, bool BWD = false>
+template <typename T, int DK, int GATE, bool BWD, int C>
 static hipError_t launch_k2_prec(const FwdArgs& a, hipStream_t s) {
   switch (a.precond) {
-    case kSquash: return launch_k2<T, DK, GATE, kSquash, BWD>(a, s);
-    case kIdentity: return launch_k2<T, DK, GATE, kIdentity, BWD>(a, s);
-    case kExternal: return launch_k2<T, DK, GATE, kExternal, BWD>(a, s);
+    case kSquash: return launch_k2<T, DK, GATE, kSquash, BWD, C>(a, s);
+    case kIdentity: return launch_k2<T, DK, GATE, kIdentity, BWD, C>(a, s);
+    case kExternal: return launch_k2<T, DK, GATE, kExternal, BWD, C>(a, s);
     default:   // forward-only modes (the host rejects them for training)
       if constexpr (BWD) return hipErrorInvalidValue;
-      else if (a.precond == kDiagSM) return launch_k2<T, DK, GATE, kDiagSM, false>(a, s);
-      else return launch_k2<T, DK, GATE, kATQ, false>(a, s);
+      else if (a.precond == kDiagSM) return launch_k2<T, DK, GATE, kDiagSM, false, C>(a, s);
+      else return launch_k2<T, DK, GATE, kATQ, false, C>(a, s);
   }
 }
 
 // SAVE: the training forward (k2 in backward mode, k3 also saving the
 // chunk states and E rows)
-template <typename T, int DK, bool SAVE>
+template <typename T, int DK, bool SAVE, int C>
 static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* ev) {
   hipError_t e;
   auto mark = [&](int i) { return ev && ev[i] ? hipEventRecord(ev[i], s) : hipSuccess; };
   if ((e = mark(0)) != hipSuccess) return e;
   if (has_gram(a.precond)) {
-    hipLaunchKernelGGL((k1_precond_summary<T, DK>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
+    hipLaunchKernelGGL((k1_precond_summary<T, DK, C>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
                        0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((k1_precond_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, a);
@@ -1141,9 +1181,9 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
   }
   if ((e = mark(1)) != hipSuccess) return e;
   switch (a.gate) {
-    case kGateNone: e = launch_k2_prec<T, DK, kGateNone, SAVE>(a, s); break;
-    case kGateScalar: e = launch_k2_prec<T, DK, kGateScalar, SAVE>(a, s); break;
-    default: e = launch_k2_prec<T, DK, kGateChannel, SAVE>(a, s); break;
+    case kGateNone: e = launch_k2_prec<T, DK, kGateNone, SAVE, C>(a, s); break;
+    case kGateScalar: e = launch_k2_prec<T, DK, kGateScalar, SAVE, C>(a, s); break;
+    default: e = launch_k2_prec<T, DK, kGateChannel, SAVE, C>(a, s); break;
   }
   if (e != hipSuccess) return e;
   if ((e = mark(2)) != hipSuccess) return e;
@@ -1153,13 +1193,13 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
     if (a.precond == kATQ) {   // linear attention with the preconditioned query
       switch (a.gate) {
         case kGateNone:
-          hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, false, true, true>), dim3(grid), dim3(256), 0, s, a);
+          hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, false, true, true, C>), dim3(grid), dim3(256), 0, s, a);
           break;
         case kGateScalar:
-          hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, false, true, true>), dim3(grid), dim3(256), 0, s, a);
+          hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, false, true, true, C>), dim3(grid), dim3(256), 0, s, a);
           break;
         default:
-          hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, false, true, true>), dim3(grid), dim3(256), 0, s, a);
+          hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, false, true, true, C>), dim3(grid), dim3(256), 0, s, a);
           break;
       }
       if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1168,11 +1208,11 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
   }
   switch (a.gate) {
     case kGateNone:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, SAVE, true>), dim3(grid), dim3(256), 0, s, a); break;
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, SAVE, true, false, C>), dim3(grid), dim3(256), 0, s, a); break;
     case kGateScalar:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, SAVE, true>), dim3(grid), dim3(256), 0, s, a); break;
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, SAVE, true, false, C>), dim3(grid), dim3(256), 0, s, a); break;
     default:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, SAVE, true>), dim3(grid), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, SAVE, true, false, C>), dim3(grid), dim3(256), 0, s, a);
       break;
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1181,13 +1221,13 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
 
 // the backward's forward recompute: k1 (squash), k2 in backward mode and k3
 // saving chunk states and E rows (no output)
-template <typename T, int DK>
+template <typename T, int DK, int C>
 static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s, hipEvent_t const* ev) {
   hipError_t e;
   auto mark = [&](int i) { return ev && ev[i] ? hipEventRecord(ev[i], s) : hipSuccess; };
   if ((e = mark(0)) != hipSuccess) return e;
   if (has_gram(a.precond)) {
-    hipLaunchKernelGGL((k1_precond_summary<T, DK>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
+    hipLaunchKernelGGL((k1_precond_summary<T, DK, C>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
                        0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((k1_precond_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, a);
@@ -1195,9 +1235,9 @@ static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s, hipEvent_t c
   }
   if ((e = mark(1)) != hipSuccess) return e;
   switch (a.gate) {
-    case kGateNone: e = launch_k2_prec<T, DK, kGateNone, true>(a, s); break;
-    case kGateScalar: e = launch_k2_prec<T, DK, kGateScalar, true>(a, s); break;
-    default: e = launch_k2_prec<T, DK, kGateChannel, true>(a, s); break;
+    case kGateNone: e = launch_k2_prec<T, DK, kGateNone, true, C>(a, s); break;
+    case kGateScalar: e = launch_k2_prec<T, DK, kGateScalar, true, C>(a, s); break;
+    default: e = launch_k2_prec<T, DK, kGateChannel, true, C>(a, s); break;
   }
   if (e != hipSuccess) return e;
   if ((e = mark(2)) != hipSuccess) return e;
@@ -1205,19 +1245,25 @@ static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s, hipEvent_t c
   const unsigned grid = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
   switch (a.gate) {
     case kGateNone:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, true, false>), dim3(grid), dim3(256), 0, s, a); break;
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, true, false, false, C>), dim3(grid), dim3(256), 0, s, a); break;
     case kGateScalar:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, true, false>), dim3(grid), dim3(256), 0, s, a); break;
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, true, false, false, C>), dim3(grid), dim3(256), 0, s, a); break;
     default:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, true, false>), dim3(grid), dim3(256), 0, s, a); break;
+      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, true, false, false, C>), dim3(grid), dim3(256), 0, s, a); break;
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return mark(3);
 }
 
+template <int C>
+static hipError_t launch_forward_parts_c(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev) {
+  if (io_bf16) return a.dk == 64 ? launch_recompute<bf16, 64, C>(a, s, ev) : launch_recompute<bf16, 128, C>(a, s, ev);
+  return launch_recompute<float, 64, C>(a, s, ev);
+}
+
 hipError_t launch_forward_parts(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev) {
-  if (io_bf16) return a.dk == 64 ? launch_recompute<bf16, 64>(a, s, ev) : launch_recompute<bf16, 128>(a, s, ev);
-  return launch_recompute<float, 64>(a, s, ev);
+  return a.chunk == 32 ? launch_forward_parts_c<32>(a, io_bf16, s, ev)
+                       : launch_forward_parts_c<64>(a, io_bf16, s, ev);
 }
 
 // The workspace of pdn_chunk_fwd_noalloc.  Host code never uses this name
@@ -1244,6 +1290,18 @@ hipError_t noalloc_scratch(void** ptr) {
   return hipSuccess;
 }
 
+template <int C>
+static hipError_t launch_chunks(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev, bool train) {
+  if (train) {   // the host admits fp32 io only with d_k = d_v = 64 here
+    if (io_bf16) return a.dk == 64 ? launch_all<bf16, 64, true, C>(a, s, ev) : launch_all<bf16, 128, true, C>(a, s, ev);
+    return launch_all<float, 64, true, C>(a, s, ev);
+  }
+  if (io_bf16) {
+    return a.dk == 64 ? launch_all<bf16, 64, false, C>(a, s, ev) : launch_all<bf16, 128, false, C>(a, s, ev);
+  }
+  return a.dk == 64 ? launch_all<float, 64, false, C>(a, s, ev) : launch_all<float, 128, false, C>(a, s, ev);
+}
+
 hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev, bool train) {
   if (a.BH == 0 || a.T == 0) {
     // nothing to time: the stage events still mark the (empty) stages
@@ -1259,14 +1317,8 @@ hipError_t launch_forward(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent
                        a, nS, nA);
     return hipGetLastError();
   }
-  if (train) {   // the host admits fp32 io only with d_k = d_v = 64 here
-    if (io_bf16) return a.dk == 64 ? launch_all<bf16, 64, true>(a, s, ev) : launch_all<bf16, 128, true>(a, s, ev);
-    return launch_all<float, 64, true>(a, s, ev);
-  }
-  if (io_bf16) {
-    return a.dk == 64 ? launch_all<bf16, 64, false>(a, s, ev) : launch_all<bf16, 128, false>(a, s, ev);
-  }
-  return a.dk == 64 ? launch_all<float, 64, false>(a, s, ev) : launch_all<float, 128, false>(a, s, ev);
+  return a.chunk == 32 ? launch_chunks<32>(a, io_bf16, s, ev, train)
+                       : launch_chunks<64>(a, io_bf16, s, ev, train);
 }
 
 }  // namespace pdn

@@ -12,7 +12,6 @@
 
 namespace {
 
-using pdn::kChunk;
 
 static_assert(PDN_NOALLOC_SCRATCH_BYTES == pdn::kNoallocScratchBytes,
               "the header's scratch size and the library's must agree");
@@ -44,7 +43,7 @@ pdn_status check_problem(const pdn_problem* p, Sizes* sz) {
   if (p->B < 0 || p->T < 0 || p->H < 0) return PDN_ERR_SHAPE;
   if (p->io != PDN_F32 && p->io != PDN_BF16) return PDN_ERR_DTYPE;
   if ((p->dk != 64 && p->dk != 128) || (p->dv != 64 && p->dv != 128)) return PDN_ERR_UNSUPPORTED;
-  if (p->chunk != kChunk) return PDN_ERR_UNSUPPORTED;
+  if (!pdn::chunk_supported(p->chunk)) return PDN_ERR_UNSUPPORTED;
   if (p->gate != PDN_GATE_NONE && p->gate != PDN_GATE_SCALAR && p->gate != PDN_GATE_CHANNEL)
     return PDN_ERR_VALUE;
   if (p->precond != PDN_PRECOND_SQUASH && p->precond != PDN_PRECOND_IDENTITY &&
@@ -62,9 +61,9 @@ pdn_status check_problem(const pdn_problem* p, Sizes* sz) {
   int64_t bt;
   if (!mul_ok(p->B, p->H, &s.BH) || !mul_ok(p->B, p->T, &bt) || !mul_ok(bt, p->H, &s.tok))
     return PDN_ERR_SHAPE;
-  s.NT = (p->T + kChunk - 1) / kChunk;
+  s.NT = (p->T + p->chunk - 1) / p->chunk;
   int64_t tpad;
-  if (!mul_ok(s.NT, kChunk, &tpad)) return PDN_ERR_SHAPE;
+  if (!mul_ok(s.NT, p->chunk, &tpad)) return PDN_ERR_SHAPE;
   // every element count used below must fit in int64 (with a generous margin
   // for the workspace's byte counts)
   int64_t tmp;
@@ -147,6 +146,7 @@ pdn_status check_inputs(const pdn_problem* p, const pdn_inputs* in, const Sizes&
 // the backward covers every gate kind and the SQUASH / IDENTITY / EXTERNAL
 // write keys; fp32 io at head dims 64
 pdn_status check_bwd_support(const pdn_problem* p) {
+  if (p->chunk != 64) return PDN_ERR_UNSUPPORTED;
   if (p->io == PDN_F32 && (p->dk != 64 || p->dv != 64)) return PDN_ERR_UNSUPPORTED;
   if (p->precond == PDN_PRECOND_DIAG_SM || p->precond == PDN_PRECOND_ATQ) return PDN_ERR_UNSUPPORTED;
   if (p->knorm != PDN_KNORM_NONE) return PDN_ERR_UNSUPPORTED;
@@ -163,7 +163,7 @@ const char* pdn_status_string(pdn_status st) {
     case PDN_ERR_NULL: return "a required pointer is NULL";
     case PDN_ERR_SHAPE: return "invalid or overflowing shape";
     case PDN_ERR_DTYPE: return "unknown io dtype";
-    case PDN_ERR_UNSUPPORTED: return "head dimension or chunk size not supported (dk, dv in {64, 128}; chunk 64)";
+    case PDN_ERR_UNSUPPORTED: return "head dimension, chunk size or mode not supported (dk, dv in {64, 128}; chunk 32 or 64, the backward and training pair 64)";
     case PDN_ERR_ALIGN: return "a tensor is not 16-byte aligned";
     case PDN_ERR_ALIAS: return "an output overlaps an input, another output or the workspace";
     case PDN_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
@@ -190,7 +190,7 @@ pdn_status pdn_workspace_size(const pdn_problem* p, int with_bwd, size_t* bytes)
     return PDN_OK;
   }
   const pdn::WsLayout L = pdn::fwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, s.esz, p->gate,
-                                             p->precond);
+                                             p->precond, p->chunk);
   *bytes = L.total;
   return PDN_OK;
 }
@@ -239,7 +239,7 @@ static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn
   for (const Buf& x : outs)
     if (x.p && !aligned16(x.p)) return PDN_ERR_ALIGN;
   const pdn::WsLayout L = pdn::fwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, s.esz, p->gate,
-                                             p->precond);
+                                             p->precond, p->chunk);
   const pdn::BwdWsLayout LB =
       pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond);
   const size_t need_bytes = train ? LB.total : L.total;
@@ -264,8 +264,9 @@ static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn
 
   pdn::FwdArgs a{};
   a.B = p->B; a.T = p->T; a.H = p->H; a.BH = s.BH;
+  a.chunk = p->chunk;
   a.NT = static_cast<int>(s.NT);
-  a.Tpad = s.NT * kChunk;
+  a.Tpad = s.NT * p->chunk;
   a.dk = p->dk; a.dv = p->dv;
   a.gate = p->gate; a.precond = p->precond;
   a.lnx = std::log(p->x);
@@ -361,8 +362,9 @@ static pdn_status chunk_bwd_impl(const pdn_problem* p, const pdn_inputs* in, con
   pdn::BwdArgs a{};
   pdn::FwdArgs& f = a.f;
   f.B = p->B; f.T = p->T; f.H = p->H; f.BH = s.BH;
+  f.chunk = p->chunk;
   f.NT = static_cast<int>(s.NT);
-  f.Tpad = s.NT * kChunk;
+  f.Tpad = s.NT * p->chunk;
   f.dk = p->dk; f.dv = p->dv;
   f.gate = p->gate; f.precond = p->precond;
   f.lnx = std::log(p->x);

@@ -7,7 +7,8 @@
 
 namespace pdn {
 
-constexpr int kChunk = 64;  // chunk length C
+// chunk lengths C the kernels are built for
+constexpr bool chunk_supported(int c) { return c == 32 || c == 64; }
 
 enum GateKind { kGateNone = 0, kGateScalar = 1, kGateChannel = 2 };
 enum PrecondKind { kSquash = 0, kIdentity = 1, kExternal = 2, kDiagSM = 3, kATQ = 4 };
@@ -24,6 +25,7 @@ constexpr bool has_gram(int precond) {
 // whole chunks (T_pad = NT * C rows).
 struct FwdArgs {
   int64_t B, T, H, BH;
+  int chunk;     // chunk length C (32 or 64)
   int NT;        // number of chunks, ceil(T / C)
   int64_t Tpad;  // NT * C
   int dk, dv;
@@ -104,7 +106,7 @@ struct WsLayout {
   size_t sumL, sumD, Abound, KtG, Tm, Pm, G, Qt, QL, KL, total;
 };
 
-WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precond);
+WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precond, int C);
 
 struct BwdWsLayout {
   WsLayout f;

@@ -117,7 +117,9 @@ def test_workspace_size_monotone_and_validated():
 @pytest.mark.parametrize("kw,code", [
     (dict(dk=96), pdn.PDN_ERR_UNSUPPORTED),
     (dict(dv=256), pdn.PDN_ERR_UNSUPPORTED),
-    (dict(chunk=32), pdn.PDN_ERR_UNSUPPORTED),
+    (dict(chunk=16), pdn.PDN_ERR_UNSUPPORTED),
+    (dict(chunk=48), pdn.PDN_ERR_UNSUPPORTED),
+    (dict(chunk=128), pdn.PDN_ERR_UNSUPPORTED),
     (dict(B=-1), pdn.PDN_ERR_SHAPE),
     (dict(T=-5), pdn.PDN_ERR_SHAPE),
     (dict(B=1 << 40, T=1 << 30), pdn.PDN_ERR_SHAPE),
@@ -332,3 +334,20 @@ def test_noalloc_validates_like_the_forward():
         pdn.PDN_ERR_ALIAS
     assert _fwd_noalloc(_prob(precond="identity"), _inputs(beta_p=None)) == \
         pdn.PDN_ERR_VALUE
+
+
+def test_chunk_sizes():
+    """Chunks of 32 and 64 tokens run the forward; the backward and the
+    training pair are built for 64 only (PDN_ERR_UNSUPPORTED, before any HIP
+    call).  The 32-token workspace holds twice the chunks."""
+    p32, p64 = _prob(chunk=32), _prob(chunk=64)
+    n32, n64 = pdn.pdn_workspace_size(p32), pdn.pdn_workspace_size(p64)
+    assert n32 > 0 and n64 > 0
+    with pytest.raises(pdn.PdnError) as e:
+        pdn.pdn_workspace_size(p32, True)
+    assert e.value.status == pdn.PDN_ERR_UNSUPPORTED
+    st = pdn.pdn_chunk_bwd_raw(p32, _inputs(), A * 30, None,
+                               pdn.BwdOut(*([None] * 11)), A * 64, 0, 0)
+    assert st == pdn.PDN_ERR_UNSUPPORTED
+    # forward validation still runs for chunk 32 (a one-byte-short workspace)
+    assert _fwd(p32) == pdn.PDN_ERR_WORKSPACE

@@ -272,3 +272,79 @@ def test_forward_only_modes_full_layer(precond, gate, ridge):
         e_a = rel_err(A_T[b, h], ref["A_T"][n])
         print(f"{precond}/{gate} head {(b, h)}: err(o)={e_o:.2e} err(S_T)={e_s:.2e} err(A_T)={e_a:.2e}")
         assert e_o <= tol(spec.io) and e_s <= tol(spec.io) and e_a <= 1e-4
+
+
+CHUNK32 = [
+    # (io, gate, precond, dk, dv, ridge): 32-token chunks (two 16-row blocks
+    # per chunk) across gates, write keys and the forward-only modes
+    ("bf16", "none", "squash", 128, 128, 1.0),
+    ("bf16", "scalar", "squash", 128, 128, 1.0),
+    ("bf16", "channel", "squash", 128, 128, 1.0),
+    ("bf16", "scalar", "identity", 64, 128, 1.0),
+    ("bf16", "channel", "external", 128, 64, 1.0),
+    ("f32", "scalar", "squash", 64, 64, 1.0),
+    ("f32", "channel", "identity", 64, 64, 1.0),
+    ("f32", "none", "squash", 128, 128, 1.0),
+    ("bf16", "scalar", "diag_sm", 128, 128, 0.1),
+    ("bf16", "channel", "atq", 128, 64, 0.5),
+    ("f32", "scalar", "atq", 64, 64, 0.1),
+]
+
+
+@pytest.mark.parametrize("io,gate,precond,dk,dv,ridge", CHUNK32)
+def test_chunk32_all_heads(io, gate, precond, dk, dv, ridge):
+    """chunk = 32: T = 200 = 6*32 + 8 (ragged tail), every head, nonzero S0
+    and A0, against the token recurrence (which has no chunk)."""
+    spec = pi.small_spec(io=io, gate=gate, dk=dk, dv=dv, s0="normal",
+                         a0="lognormal" if precond != "identity" and
+                         precond != "external" else "zero")
+    inp = pi.generate(spec, 19)
+    if precond == "external":
+        rng = np.random.default_rng(5)
+        kt = inp["k"] * rng.uniform(1 / 1.5, 1.5, inp["k"].shape)
+        inp["ktilde"] = pi.round_bf16(kt) if io == "bf16" else kt.astype(np.float32)
+    o, S_T, A_T = run_fwd(spec, inp, precond, ridge=ridge, chunk=32)
+    ref = _oracle(spec, inp, precond, ridge=ridge)
+    B, H = spec.B, spec.H
+    go = np.stack([o[b, :, h] for b in range(B) for h in range(H)])
+    e_o = rel_err(go, ref["o"])
+    e_s = rel_err(S_T.reshape(B * H, dk, dv), ref["S_T"])
+    msg = f"chunk32 {io}/{gate}/{precond}/{dk}x{dv} err(o)={e_o:.2e} err(S_T)={e_s:.2e}"
+    print(msg)
+    assert e_o <= tol(io) and e_s <= tol(io), msg
+    if A_T is not None:
+        assert rel_err(A_T.reshape(B * H, dk), ref["A_T"]) <= 1e-4
+
+
+@pytest.mark.parametrize("T", [1, 31, 32, 33, 64, 95, 97])
+@pytest.mark.parametrize("gate", ["scalar", "channel"])
+def test_chunk32_sequence_lengths(T, gate):
+    spec = pi.small_spec(T=T, B=1, H=2, gate=gate, dk=128, dv=128, s0="normal")
+    inp = pi.generate(spec, 900 + T)
+    o, S_T, A_T = run_fwd(spec, inp, chunk=32)
+    ref = _oracle(spec, inp)
+    go = np.stack([o[0, :, h] for h in range(2)])
+    e_o, e_s = rel_err(go, ref["o"]), rel_err(S_T.reshape(2, 128, 128), ref["S_T"])
+    print(f"chunk32 {gate} T={T} err(o)={e_o:.2e} err(S_T)={e_s:.2e}")
+    assert e_o <= 2e-2 and e_s <= 2e-2
+    assert rel_err(A_T.reshape(2, 128), ref["A_T"]) <= 1e-4
+
+
+def test_chunk32_full_layer_sampled_heads():
+    """The 1B PGDN layer (B=4, T=4096, H=16, d=128) with 32-token chunks:
+    two sampled heads against the oracle, and the result close to the
+    64-token chunking of the same inputs."""
+    name = "pgdn_bf16_b4_t4096_h16_d128"
+    spec = pi.WORKLOADS[name]
+    inp = pi.generate(spec, pi.WORKLOAD_SEEDS[name])
+    o, S_T, A_T = run_fwd(spec, inp, chunk=32)
+    heads = [(0, 0), (spec.B - 1, spec.H - 1)]
+    ref = _oracle(spec, inp, heads=heads)
+    for n, (b, h) in enumerate(heads):
+        e_o = rel_err(o[b, :, h], ref["o"][n])
+        e_s = rel_err(S_T[b, h], ref["S_T"][n])
+        print(f"chunk32 {name} head {(b, h)}: err(o)={e_o:.2e} err(S_T)={e_s:.2e}")
+        assert e_o <= 2e-2 and e_s <= 2e-2
+        assert rel_err(A_T[b, h], ref["A_T"][n]) <= 1e-4
+    o64, S64, _ = run_fwd(spec, inp, chunk=64)
+    assert rel_err(o, o64) <= 2e-2 and rel_err(S_T, S64) <= 2e-2
