@@ -61,7 +61,9 @@ typedef enum {
   PDN_ERR_NULL = 1,        /* a required pointer is NULL                       */
   PDN_ERR_SHAPE = 2,       /* B, T, H negative or sizes overflow               */
   PDN_ERR_DTYPE = 3,       /* unknown io dtype                                 */
-  PDN_ERR_UNSUPPORTED = 4, /* dk, dv or chunk outside the built kernels        */
+  PDN_ERR_UNSUPPORTED = 4, /* dk, dv or chunk outside the built kernels (dk, dv
+                              in {64, 128}, chunk in {32, 64}), or a mode
+                              the entry point does not cover                 */
   PDN_ERR_ALIGN = 5,       /* a tensor is not 16-byte aligned                  */
   PDN_ERR_ALIAS = 6,       /* an output overlaps an input or another output    */
   PDN_ERR_WORKSPACE = 7,   /* workspace NULL, too small or misaligned          */
@@ -118,7 +120,8 @@ typedef enum {
 typedef struct {
   int64_t B, T, H;     /* batch, sequence length, heads; 0 is allowed      */
   int32_t dk, dv;      /* head dims: each 64 or 128                         */
-  int32_t chunk;       /* chunk length C: 64                                */
+  int32_t chunk;       /* chunk length C: 32 or 64 (the paper's form for
+                          any C; results differ only by rounding)        */
   pdn_dtype io;        /* dtype of q, k, v, o, ktilde and their gradients   */
   pdn_gate gate;
   pdn_precond precond;

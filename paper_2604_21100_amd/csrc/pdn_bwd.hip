@@ -41,15 +41,35 @@
 
 namespace pdn {
 
-constexpr int C = 64;  // the backward kernels are built for 64-token chunks
 constexpr int BVB = 32;  // value columns per workgroup in the reverse scan
 
-template <typename T>
+// Every kernel here takes the chunk length C (32 or 64) as a template
+// parameter.  Wave w owns the chunk's row block w (16 tokens); at C = 32
+// waves 2 and 3 skip the row work and take part in the column-wise and
+// cooperative work only.  Guards written (NB == 4 || ...) are compile-time
+// true at C = 64.
+
+// A thread's share of a [NR rows] x BVB slab in 16-byte vectors: vector j
+// of thread tid is idx = tid + 256 j (idx < kN), row idx / kSegs
+template <typename T, int NR>
 struct Slab {
   static constexpr int kVec = 16 / static_cast<int>(sizeof(T));
   static constexpr int kSegs = BVB / kVec;
-  static constexpr int kPer = C * kSegs / 256;
+  static constexpr int kN = NR * kSegs;
+  static constexpr int kPer = (kN + 255) / 256;
+  static constexpr bool kWhole = kN % 256 == 0;
 };
+
+// sw() for LDS slabs whose rows hold COLS token columns: the XOR stays
+// inside the COLS columns (COLS = 64: the same permutation as sw())
+template <int COLS, typename T>
+__device__ __forceinline__ T* swc(T* base, int ld, int row, int col) {
+  return base + row * ld + (col ^ (((row >> 3) & (COLS / 16 - 1) & 3) << 4));
+}
+template <int COLS, typename T>
+__device__ __forceinline__ const T* swc(const T* base, int ld, int row, int col) {
+  return base + row * ld + (col ^ (((row >> 3) & (COLS / 16 - 1) & 3) << 4));
+}
 
 __device__ __forceinline__ void lds_barrier_b() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
@@ -60,26 +80,26 @@ __device__ __forceinline__ void lds_barrier_b() {
 // loop or branch around the stores inside the scan step
 template <int NROWS, bool ALL, typename T>
 __device__ __forceinline__ void slab_to_rows(T* dst, int64_t ld, const T* src, int lds, int n, int tid) {
-  using SM = Slab<T>;
-  static_assert(NROWS * SM::kSegs % 256 == 0, "whole rounds of 256 threads");
+  using SM = Slab<T, NROWS>;
 #pragma unroll
-  for (int j = 0; j < NROWS * SM::kSegs / 256; ++j) {
+  for (int j = 0; j < SM::kPer; ++j) {
     const int idx = tid + 256 * j;
+    if (!SM::kWhole && idx >= SM::kN) break;
     const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
     float4 pk;
     T* e = reinterpret_cast<T*>(&pk);
 #pragma unroll
-    for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = *sw(src, lds, c0 + s2, row);
+    for (int s2 = 0; s2 < SM::kVec; ++s2) e[s2] = *swc<NROWS>(src, lds, c0 + s2, row);
     if (ALL || row < n) *reinterpret_cast<float4*>(dst + row * ld + c0) = pk;
   }
 }
 
 // ------------------------------------------------------------ r1
-template <typename T, int DK, int GATE>
+template <typename T, int DK, int GATE, int C>
 struct RevFrags {
-  static constexpr int KK = DK / 32, CT = DK / 64;
-  Frag8<T> Pt[2], Kw[KK], Mt[2], Ql[CT][2], Kn[CT][2];
-  float4 dO[Slab<T>::kPer];   // dO slab of the chunk before this one
+  static constexpr int KK = DK / 32, CT = DK / 64, KC = C / 32;
+  Frag8<T> Pt[KC], Kw[KK], Mt[KC], Ql[CT][KC], Kn[CT][KC];
+  float4 dO[Slab<T, C>::kPer];   // dO slab of the chunk before this one
   // log decay at the chunk end: scalar, or per channel of the state rows
   // c = 16 (w CT + ct) + 4 lg + ii this lane holds
   float gC[GATE == kGateChannel ? CT : 1][GATE == kGateChannel ? 4 : 1];
@@ -94,10 +114,10 @@ struct RevCtx {
 
 // dO slab of chunk i (rows past the sequence end re-read its last row; the
 // staging zeroes them)
-template <typename T>
-__device__ __forceinline__ void rev_load_dO(float4 (&d)[Slab<T>::kPer], const BwdArgs& ba, int i,
+template <typename T, int C, int NPER = Slab<T, C>::kPer>
+__device__ __forceinline__ void rev_load_dO(float4 (&d)[NPER], const BwdArgs& ba, int i,
                                             const RevCtx& x) {
-  using SM = Slab<T>;
+  using SM = Slab<T, C>;
   constexpr uint32_t E = sizeof(T);
   const FwdArgs& a = ba.f;
   const int64_t t0 = static_cast<int64_t>(i) * C;
@@ -107,18 +127,19 @@ __device__ __forceinline__ void rev_load_dO(float4 (&d)[Slab<T>::kPer], const Bw
 #pragma unroll
   for (int j = 0; j < SM::kPer; ++j) {
     const int idx = x.tid + 256 * j;
+    if (!SM::kWhole && idx >= SM::kN) break;
     const uint32_t row = static_cast<uint32_t>(min(idx / SM::kSegs, last));
     const uint32_t off = (row * static_cast<uint32_t>(HV) + (idx % SM::kSegs) * SM::kVec) * E;
     d[j] = *reinterpret_cast<const float4*>(at_bytes(dob, off));
   }
 }
 
-template <typename T, int DK, int GATE>
-__device__ __forceinline__ void rev_load(RevFrags<T, DK, GATE>& f, const BwdArgs& ba, int i,
+template <typename T, int DK, int GATE, int C>
+__device__ __forceinline__ void rev_load(RevFrags<T, DK, GATE, C>& f, const BwdArgs& ba, int i,
                                          const RevCtx& x) {
-  constexpr int KK = DK / 32, CT = DK / 64;
+  constexpr int KK = DK / 32, CT = DK / 64, KC = C / 32, NB = C / 16;
   constexpr uint32_t E = sizeof(T);
-  using SM = Slab<T>;
+  const bool rows = NB == 4 || x.w < NB;
   const FwdArgs& a = ba.f;
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int last = static_cast<int>(min<int64_t>(C, a.T - t0)) - 1;
@@ -132,30 +153,32 @@ __device__ __forceinline__ void rev_load(RevFrags<T, DK, GATE>& f, const BwdArgs
   const T* ql = static_cast<const T*>(a.QlT) + ck;
   const T* kn = static_cast<const T*>(a.KnT) + ck;
   const int ra = 16 * x.w + x.lr;
-  const uint32_t ocr = static_cast<uint32_t>(ra * C + 8 * x.lg) * E;
+  if (rows) {
+    const uint32_t ocr = static_cast<uint32_t>(ra * C + 8 * x.lg) * E;
 #pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) {
-    f.Pt[k2] = ld8(at_bytes(pt, ocr + k2 * 32 * E));
-    f.Mt[k2] = ld8(at_bytes(mt, ocr + k2 * 32 * E));
+    for (int k2 = 0; k2 < KC; ++k2) {
+      f.Pt[k2] = ld8(at_bytes(pt, ocr + k2 * 32 * E));
+      f.Mt[k2] = ld8(at_bytes(mt, ocr + k2 * 32 * E));
+    }
+    const uint32_t okw = static_cast<uint32_t>(ra * DK + 8 * x.lg) * E;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) f.Kw[kk] = ld8(at_bytes(kw, okw + kk * 32 * E));
   }
-  const uint32_t okw = static_cast<uint32_t>(ra * DK + 8 * x.lg) * E;
-#pragma unroll
-  for (int kk = 0; kk < KK; ++kk) f.Kw[kk] = ld8(at_bytes(kw, okw + kk * 32 * E));
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
+    for (int k2 = 0; k2 < KC; ++k2) {
       const uint32_t o = static_cast<uint32_t>((16 * (x.w * CT + ct) + x.lr) * C + 8 * x.lg + k2 * 32) * E;
       f.Ql[ct][k2] = ld8(at_bytes(ql, o));
       f.Kn[ct][k2] = ld8(at_bytes(kn, o));
     }
   // the dO slab staged at the end of this chunk's step: that of the chunk
   // before it (reverse order), so it has two steps to arrive
-  rev_load_dO<T>(f.dO, ba, max(i - 1, 0), x);
+  rev_load_dO<T, C>(f.dO, ba, max(i - 1, 0), x);
   if (GATE == kGateScalar) {
     f.gC[0][0] = a.G[x.bh * a.Tpad + t0 + C - 1];
 #pragma unroll
-    for (int ii = 0; ii < 4; ++ii) f.gw[ii] = a.G[x.bh * a.Tpad + t0 + 16 * x.w + 4 * x.lg + ii];
+    for (int ii = 0; ii < 4; ++ii) f.gw[ii] = rows ? a.G[x.bh * a.Tpad + t0 + 16 * x.w + 4 * x.lg + ii] : 0.f;
   }
   if (GATE == kGateChannel) {
     const float* gl = a.G + (x.bh * a.Tpad + t0 + C - 1) * DK;
@@ -170,43 +193,45 @@ __device__ __forceinline__ void rev_load(RevFrags<T, DK, GATE>& f, const BwdArgs
 }
 
 // scale * dO of one chunk -> sDO[v][r]; rows past the sequence end are zero
-template <typename T>
-__device__ __forceinline__ void rev_stage_dO(const float4 (&v)[Slab<T>::kPer], T* sDO, int n,
+template <typename T, int C>
+__device__ __forceinline__ void rev_stage_dO(const float4 (&v)[Slab<T, C>::kPer], T* sDO, int n,
                                              float scale, int tid) {
-  using SM = Slab<T>;
+  using SM = Slab<T, C>;
   constexpr int LDE = C + 8;
 #pragma unroll
   for (int j = 0; j < SM::kPer; ++j) {
     const int idx = tid + 256 * j;
+    if (!SM::kWhole && idx >= SM::kN) break;
     const int row = idx / SM::kSegs, c0 = (idx % SM::kSegs) * SM::kVec;
     const float4 raw = pin_here(v[j]);
     const T* e = reinterpret_cast<const T*>(&raw);
 #pragma unroll
     for (int s2 = 0; s2 < SM::kVec; ++s2)
-      *sw(sDO, LDE, c0 + s2, row) = from_f<T>(row < n ? scale * to_f(e[s2]) : 0.f);
+      *swc<C>(sDO, LDE, c0 + s2, row) = from_f<T>(row < n ? scale * to_f(e[s2]) : 0.f);
   }
 }
 
-template <bool FULL, typename T, int DK, int GATE>
-__device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE>& f, bool stage_next,
+template <bool FULL, typename T, int DK, int GATE, int C>
+__device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE, C>& f, bool stage_next,
                                          floatx4 (&st)[DK / 64][2], const BwdArgs& ba, int i,
                                          const RevCtx& x, T* sH, T* sDOc, T* sDOn, T* sE, T* sX,
                                          T* sZ) {
-  constexpr int KK = DK / 32, CT = DK / 64;
+  constexpr int KK = DK / 32, CT = DK / 64, KC = C / 32, NB = C / 16;
   constexpr int LDH = DK + 8, LDE = C + 8;
   const FwdArgs& a = ba.f;
   const int w = x.w, lr = x.lr, lg = x.lg;
+  const bool rows = NB == 4 || w < NB;
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int n = FULL ? C : static_cast<int>(min<int64_t>(C, a.T - t0));
   // ---- dE = P^T dO_s + Diag(w) Kt dS'^T   (rows t of this wave)
   float wr[4];
 #pragma unroll
   for (int ii = 0; ii < 4; ++ii) wr[ii] = GATE == kGateScalar ? fast_exp(f.gC[0][0] - f.gw[ii]) : 1.f;
-  Frag8<T> bO[2][2], bS[2][KK];
+  Frag8<T> bO[2][KC], bS[2][KK];
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt) {
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) bO[vt][k2] = ld8(sw(sDOc, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
+    for (int k2 = 0; k2 < KC; ++k2) bO[vt][k2] = ld8(swc<C>(sDOc, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) bS[vt][kk] = ld8(sw(sH, LDH, 16 * vt + lr, kk * 32 + 8 * lg));
   }
@@ -214,39 +239,43 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE>& f, bool stage_ne
   // (its LDS reads after the operand reads: LDS reads complete in issue order)
   slab_to_rows<DK, true>(static_cast<T*>(ba.dHs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv,
                          sH, LDH, DK, x.tid);
+  if (rows) {
 #pragma unroll
-  for (int vt = 0; vt < 2; ++vt) {
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f}, acw = acc;
+    for (int vt = 0; vt < 2; ++vt) {
+      floatx4 acc = {0.f, 0.f, 0.f, 0.f}, acw = acc;
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Pt[k2], bO[vt][k2]);
+      for (int k2 = 0; k2 < KC; ++k2) mma(acc, f.Pt[k2], bO[vt][k2]);
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) mma(acw, f.Kw[kk], bS[vt][kk]);
+      for (int kk = 0; kk < KK; ++kk) mma(acw, f.Kw[kk], bS[vt][kk]);
 #pragma unroll
-    for (int ii = 0; ii < 4; ++ii) acc[ii] += wr[ii] * acw[ii];
-    st4<T>(sw(sE, LDE, 16 * vt + lr, 16 * w + 4 * lg), acc[0], acc[1], acc[2], acc[3]);
+      for (int ii = 0; ii < 4; ++ii) acc[ii] += wr[ii] * acw[ii];
+      st4<T>(swc<C>(sE, LDE, 16 * vt + lr, 16 * w + 4 * lg), acc[0], acc[1], acc[2], acc[3]);
+    }
   }
   lds_barrier_b();
   // ---- Z = M^T dE;  dX = Diag(beta) Z   (rows t = 16w + 4lg + ii)
-  float bt[4];
+  if (rows) {
+    float bt[4];
 #pragma unroll
-  for (int ii = 0; ii < 4; ++ii) bt[ii] = (FULL || 16 * w + 4 * lg + ii < n) ? f.beta[ii] : 0.f;
+    for (int ii = 0; ii < 4; ++ii) bt[ii] = (FULL || 16 * w + 4 * lg + ii < n) ? f.beta[ii] : 0.f;
 #pragma unroll
-  for (int vt = 0; vt < 2; ++vt) {
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int vt = 0; vt < 2; ++vt) {
+      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) mma(acc, f.Mt[k2], ld8(sw(sE, LDE, 16 * vt + lr, k2 * 32 + 8 * lg)));
-    st4<T>(sw(sZ, LDE, 16 * vt + lr, 16 * w + 4 * lg), acc[0], acc[1], acc[2], acc[3]);
-    st4<T>(sw(sX, LDE, 16 * vt + lr, 16 * w + 4 * lg), bt[0] * acc[0], bt[1] * acc[1], bt[2] * acc[2],
-           bt[3] * acc[3]);
+      for (int k2 = 0; k2 < KC; ++k2) mma(acc, f.Mt[k2], ld8(swc<C>(sE, LDE, 16 * vt + lr, k2 * 32 + 8 * lg)));
+      st4<T>(swc<C>(sZ, LDE, 16 * vt + lr, 16 * w + 4 * lg), acc[0], acc[1], acc[2], acc[3]);
+      st4<T>(swc<C>(sX, LDE, 16 * vt + lr, 16 * w + 4 * lg), bt[0] * acc[0], bt[1] * acc[1],
+             bt[2] * acc[2], bt[3] * acc[3]);
+    }
   }
   lds_barrier_b();
   // ---- dS^T <- Diag(lam_C) dS'^T + (Lam o Q)^T dO_s - (Lam o K)^T dX
   const float gam = GATE == kGateScalar ? fast_exp(f.gC[0][0]) : 1.f;
-  Frag8<T> bX[2][2];
+  Frag8<T> bX[2][KC];
 #pragma unroll
   for (int vt = 0; vt < 2; ++vt)
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) bX[vt][k2] = ld8(sw(sX, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
+    for (int k2 = 0; k2 < KC; ++k2) bX[vt][k2] = ld8(swc<C>(sX, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
   {
     // Z and dv rows (their LDS reads after the operand reads)
     const int64_t r0 = (x.bh * a.Tpad + t0) * a.dv + x.v0;
@@ -264,18 +293,18 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE>& f, bool stage_ne
         st[ct][vt][ii] *= GATE == kGateChannel ? fast_exp(f.gC[ct][ii]) : gam;
       }
 #pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
+      for (int k2 = 0; k2 < KC; ++k2) {
         mma(st[ct][vt], f.Ql[ct][k2], bO[vt][k2]);
         mma(st[ct][vt], f.Kn[ct][k2], bX[vt][k2]);
       }
       st4<T>(sw(sH, LDH, 16 * vt + lr, 16 * (w * CT + ct) + 4 * lg), st[ct][vt][0], st[ct][vt][1],
              st[ct][vt][2], st[ct][vt][3]);
     }
-  if (stage_next) rev_stage_dO<T>(f.dO, sDOn, C, a.scale, x.tid);  // earlier chunks are full
+  if (stage_next) rev_stage_dO<T, C>(f.dO, sDOn, C, a.scale, x.tid);  // earlier chunks are full
   lds_barrier_b();
 }
 
-template <typename T, int DK, int GATE>
+template <typename T, int DK, int GATE, int C>
 __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
   constexpr int CT = DK / 64;
   constexpr int LDH = DK + 8, LDE = C + 8;
@@ -322,24 +351,24 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
   // reverse order: the (possibly ragged) last chunk first, then the full
   // chunks two per trip with a branch-free body; dO slabs double-buffered
   const int NT = a.NT;
-  RevFrags<T, DK, GATE> fA, fB;
-  float4 dlast[Slab<T>::kPer];
-  rev_load_dO<T>(dlast, ba, NT - 1, x);
-  rev_load<T, DK, GATE>(fA, ba, NT - 1, x);
-  rev_load<T, DK, GATE>(fB, ba, max(NT - 2, 0), x);
-  rev_stage_dO<T>(dlast, sDO[0], static_cast<int>(a.T - static_cast<int64_t>(NT - 1) * C), a.scale, x.tid);
+  RevFrags<T, DK, GATE, C> fA, fB;
+  float4 dlast[Slab<T, C>::kPer];
+  rev_load_dO<T, C>(dlast, ba, NT - 1, x);
+  rev_load<T, DK, GATE, C>(fA, ba, NT - 1, x);
+  rev_load<T, DK, GATE, C>(fB, ba, max(NT - 2, 0), x);
+  rev_stage_dO<T, C>(dlast, sDO[0], static_cast<int>(a.T - static_cast<int64_t>(NT - 1) * C), a.scale, x.tid);
   __syncthreads();
-  rev_step<false, T, DK, GATE>(fA, NT > 1, st, ba, NT - 1, x, sH, sDO[0], sDO[1], sE, sX, sZ);
+  rev_step<false, T, DK, GATE, C>(fA, NT > 1, st, ba, NT - 1, x, sH, sDO[0], sDO[1], sE, sX, sZ);
   int i = NT - 2, buf = 1;
   for (; i >= 1; i -= 2) {
-    rev_load<T, DK, GATE>(fA, ba, i - 1, x);
-    rev_step<true, T, DK, GATE>(fB, true, st, ba, i, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
+    rev_load<T, DK, GATE, C>(fA, ba, i - 1, x);
+    rev_step<true, T, DK, GATE, C>(fB, true, st, ba, i, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
     buf ^= 1;
-    rev_load<T, DK, GATE>(fB, ba, max(i - 2, 0), x);
-    rev_step<true, T, DK, GATE>(fA, true, st, ba, i - 1, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
+    rev_load<T, DK, GATE, C>(fB, ba, max(i - 2, 0), x);
+    rev_step<true, T, DK, GATE, C>(fA, true, st, ba, i - 1, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
     buf ^= 1;
   }
-  if (i == 0) rev_step<true, T, DK, GATE>(fB, false, st, ba, 0, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
+  if (i == 0) rev_step<true, T, DK, GATE, C>(fB, false, st, ba, 0, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
   if (ba.dS0) {
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
@@ -358,7 +387,7 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
 // bank-spread addressing: read back through sw()), in two halves, so the
 // loads can be issued early and other work done before the LDS store waits
 // for them
-template <typename T, int DD>
+template <typename T, int DD, int C>
 struct RowStage {
   static constexpr int kVec = 16 / static_cast<int>(sizeof(T)), kVpr = DD / kVec;
   static constexpr int kPer = C * kVpr / 256;
@@ -390,37 +419,41 @@ struct RowStage {
 // A [C][HC] tile held in registers between its load and its transposed
 // store to dst[HC][C + 8].  (Named registers, not an array: a private array
 // here is moved to LDS.)
-template <typename T, int HC>
+// (C = 32 in bf16: 128 vectors, so half the threads hold one: kN guards)
+template <typename T, int HC, int C>
 struct HeldTile {
   static constexpr int kVec = 16 / static_cast<int>(sizeof(T)), kVpr = HC / kVec;
-  static constexpr int kPer = C * kVpr / 256;
-  static_assert(C * kVpr % 256 == 0 && (kPer == 1 || kPer == 2), "one or two vectors per thread");
+  static constexpr int kN = C * kVpr;
+  static constexpr int kPer = (kN + 255) / 256;
+  static_assert(kPer == 1 || kPer == 2, "one or two vectors per thread");
   float4 v0, v1;
 };
-template <typename T, int HC>
+template <typename T, int HC, int C>
 __device__ __forceinline__ void tile_t_put(T* dst, float4 x, int j, int tid) {
-  using HT = HeldTile<T, HC>;
+  using HT = HeldTile<T, HC, C>;
   constexpr int LDT = C + 8;
   const int idx = tid + 256 * j, r = idx / HT::kVpr, cv = idx % HT::kVpr;
+  if (HT::kN % 256 != 0 && idx >= HT::kN) return;
   const T* e = reinterpret_cast<const T*>(&x);
 #pragma unroll
-  for (int s2 = 0; s2 < HT::kVec; ++s2) *sw(dst, LDT, cv * HT::kVec + s2, r) = e[s2];
+  for (int s2 = 0; s2 < HT::kVec; ++s2) *swc<C>(dst, LDT, cv * HT::kVec + s2, r) = e[s2];
 }
-template <typename T, int HC>
-__device__ __forceinline__ void tile_t_store(T* dst, const HeldTile<T, HC>& held, int tid) {
-  tile_t_put<T, HC>(dst, held.v0, 0, tid);
-  if constexpr (HeldTile<T, HC>::kPer == 2) tile_t_put<T, HC>(dst, held.v1, 1, tid);
+template <typename T, int HC, int C>
+__device__ __forceinline__ void tile_t_store(T* dst, const HeldTile<T, HC, C>& held, int tid) {
+  tile_t_put<T, HC, C>(dst, held.v0, 0, tid);
+  if constexpr (HeldTile<T, HC, C>::kPer == 2) tile_t_put<T, HC, C>(dst, held.v1, 1, tid);
 }
 // One pass's tile (rows [C], columns HC from src) into registers, a pass
 // ahead of its transposed LDS store (tile_t_store); rows >= nvalid are zero
-template <typename T, int HC>
-__device__ __forceinline__ void load_tile_regs(HeldTile<T, HC>& t, const T* src, int64_t lds, int nvalid,
+template <typename T, int HC, int C>
+__device__ __forceinline__ void load_tile_regs(HeldTile<T, HC, C>& t, const T* src, int64_t lds, int nvalid,
                                                int tid) {
-  using HT = HeldTile<T, HC>;
+  using HT = HeldTile<T, HC, C>;
   auto get = [&](int j, float4& v) {
     const int idx = tid + 256 * j, r = idx / HT::kVpr, cv = idx % HT::kVpr;
     v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < nvalid) v = *reinterpret_cast<const float4*>(src + r * lds + cv * HT::kVec);
+    if (r < nvalid && (HT::kN % 256 == 0 || idx < HT::kN))
+      v = *reinterpret_cast<const float4*>(src + r * lds + cv * HT::kVec);
   };
   get(0, t.v0);
   if constexpr (HT::kPer == 2) get(1, t.v1);
@@ -447,11 +480,11 @@ __device__ __forceinline__ float dot16<bf16>(const float4& a, const float4& b) {
 
 // Two adjacent passes' tiles at once (columns [0, HC) into `now`, [HC, 2 HC)
 // into `held`), so every row segment fetched is a whole 128-byte line
-template <typename T, int HC>
-__device__ __forceinline__ void load_pair_regs(HeldTile<T, HC>& now, HeldTile<T, HC>& held, const T* src,
+template <typename T, int HC, int C>
+__device__ __forceinline__ void load_pair_regs(HeldTile<T, HC, C>& now, HeldTile<T, HC, C>& held, const T* src,
                                                int64_t lds, int nvalid, int tid) {
-  load_tile_regs<T, HC>(now, src, lds, nvalid, tid);
-  load_tile_regs<T, HC>(held, src + HC, lds, nvalid, tid);
+  load_tile_regs<T, HC, C>(now, src, lds, nvalid, tid);
+  load_tile_regs<T, HC, C>(held, src + HC, lds, nvalid, tid);
 }
 
 // One phase-B pass's rows of the chunk-start state S^T and of its adjoint
@@ -542,7 +575,7 @@ __device__ __forceinline__ void p12_flush_rows(const T* so, __amdgpu_buffer_rsrc
   }
 }
 
-template <typename T, int DK, int DV>
+template <typename T, int DK, int DV, int C>
 struct P12Smem {
   static constexpr int HC = 32;                 // key columns per phase-B pass
   static constexpr int LDE = DV + 8, LDK = DK + 8, LDV = DV + 8, LDT = C + 8;
@@ -559,9 +592,10 @@ struct P12Smem {
   static constexpr size_t kTotal = kMain + sizeof(float) * (12 * C + 4);
 };
 
-template <typename T, int DK, int DV, int GATE>
+template <typename T, int DK, int DV, int GATE, int C>
 __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
-  using SM = P12Smem<T, DK, DV>;
+  using SM = P12Smem<T, DK, DV, C>;
+  constexpr int NB = C / 16, KC = C / 32;
   constexpr int HC = SM::HC, LDE = SM::LDE, LDK = SM::LDK, LDV = SM::LDV, LDT = SM::LDT;
   constexpr int LDO = SM::LDO;
   constexpr int KV = DV / 32, KD = DK / 32, NPASS = DK / HC;
@@ -598,6 +632,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   const int i = static_cast<int>(blk % a.NT);
   const int64_t b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 15, lg = l >> 4;
+  const bool rows = NB == 4 || w < NB;   // this wave owns rows of the chunk
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
   const int64_t HV = a.H * (int64_t)DV, HD = a.H * (int64_t)DK;
@@ -614,8 +649,8 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   // phase A's loads in two groups: the Gram products' operands (q, k rows,
   // the Kt tile) first, then dO, V, Z rows and the E tile, which stay in
   // flight while the Gram products run
-  RowStage<T, DK> stKt;
-  RowStage<T, DV> stE;
+  RowStage<T, DK, C> stKt;
+  RowStage<T, DV, C> stE;
   {
     const T* qb = static_cast<const T*>(a.q) + (b * a.T + t0) * HD + h * DK;
     const T* kb = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
@@ -631,7 +666,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
 #pragma unroll
     for (int kk = 0; kk < KV; ++kk) {
       const uint32_t o = (rc * static_cast<uint32_t>(HV) + 32 * kk + 8 * lg) * E;
-      const uint32_t ow = (static_cast<uint32_t>(ra * DV) + 32 * kk + 8 * lg) * E;
+      const uint32_t ow = (static_cast<uint32_t>((rows ? ra : 0) * DV) + 32 * kk + 8 * lg) * E;
       fO[kk] = ld8(at_bytes(dob, o));
       fV[kk] = ld8(at_bytes(vb, o));
       fZ[kk] = ld8(at_bytes(zb, ow));
@@ -647,12 +682,12 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   }
   __syncthreads();
   // the Gram products (Q and K rows die here)
-  floatx4 Sqk[4], Skk[4];
+  floatx4 Sqk[NB], Skk[NB];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < NB; ++j) {
     Sqk[j] = floatx4{0.f, 0.f, 0.f, 0.f};
     Skk[j] = Sqk[j];
-    if (j <= w) {
+    if (rows && j <= w) {
 #pragma unroll
       for (int kk = 0; kk < KD; ++kk) {
         const Frag8<T> fk = ld8(sw(sKt, LDK, 16 * j + lr, 32 * kk + 8 * lg));
@@ -669,9 +704,9 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   const T* ktile = static_cast<const T*>(a.k) + (b * a.T + t0) * HD + h * DK;
   // (the tiles of two passes at a time: whole lines)
   static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
-  HeldTile<T, HC> tQ, tK, hQ, hK;
-  load_pair_regs<T, HC>(tQ, hQ, qtile, HD, n, tid);
-  load_pair_regs<T, HC>(tK, hK, ktile, HD, n, tid);
+  HeldTile<T, HC, C> tQ, tK, hQ, hK;
+  load_pair_regs<T, HC, C>(tQ, hQ, qtile, HD, n, tid);
+  load_pair_regs<T, HC, C>(tK, hK, ktile, HD, n, tid);
   stE.store(sE, tid);
   __syncthreads();
   {
@@ -683,13 +718,13 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       for (int s2 = 0; s2 < 8; ++s2) zv += fZ[kk].get(s2) * fV[kk].get(s2);
     zv += __shfl_xor(zv, 16, 64);
     zv += __shfl_xor(zv, 32, 64);
-    if (lg == 0) sZV[ra] = zv;
+    if (lg == 0 && rows) sZV[ra] = zv;
   }
-  {
+  if (rows) {
     // dP and dL tile by tile straight into the elementwise algebra
     float dbA[4] = {0.f, 0.f, 0.f, 0.f}, rs[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < NB; ++j) {
       floatx4 dP = {0.f, 0.f, 0.f, 0.f}, dL = dP;
       if (j <= w) {
 #pragma unroll
@@ -717,11 +752,11 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       }
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
-        *sw(sSq, LDT, 16 * w + 4 * lg + ii, 16 * j + lr) = from_f<T>(dq[ii]);
-        *sw(sSk, LDT, 16 * w + 4 * lg + ii, 16 * j + lr) = from_f<T>(dk[ii]);
+        *swc<C>(sSq, LDT, 16 * w + 4 * lg + ii, 16 * j + lr) = from_f<T>(dq[ii]);
+        *swc<C>(sSk, LDT, 16 * w + 4 * lg + ii, 16 * j + lr) = from_f<T>(dk[ii]);
       }
-      st4<T>(sw(sSqT, LDT, 16 * j + lr, 16 * w + 4 * lg), dq[0], dq[1], dq[2], dq[3]);
-      st4<T>(sw(sSkT, LDT, 16 * j + lr, 16 * w + 4 * lg), dk[0], dk[1], dk[2], dk[3]);
+      st4<T>(swc<C>(sSqT, LDT, 16 * j + lr, 16 * w + 4 * lg), dq[0], dq[1], dq[2], dq[3]);
+      st4<T>(swc<C>(sSkT, LDT, 16 * j + lr, 16 * w + 4 * lg), dk[0], dk[1], dk[2], dk[3]);
       csum += __shfl_xor(csum, 16, 64);
       csum += __shfl_xor(csum, 32, 64);
       if (lg == 0) sCs[w * C + 16 * j + lr] = csum;
@@ -742,23 +777,27 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
     }
   }
   // E rows of this wave (phase B's A operand of A3), from the staged copy
+  // (a wave without rows of the chunk reads row 0: its results are unused)
+  const int rw = rows ? ra : 0;
 #pragma unroll
-  for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, ra, 32 * kk + 8 * lg));
+  for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, rw, 32 * kk + 8 * lg));
   __syncthreads();
   // the C x C adjoints as A fragments of this wave's rows (k = 32 k2 + 8 lg)
-  Frag8<T> fSq[2], fSk[2], fSqT[2], fSkT[2];
+  Frag8<T> fSq[KC], fSk[KC], fSqT[KC], fSkT[KC];
 #pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) {
+  for (int k2 = 0; k2 < KC; ++k2) {
     const int o = 32 * k2 + 8 * lg;
-    fSq[k2] = ld8(sw(sSq, LDT, ra, o));
-    fSk[k2] = ld8(sw(sSk, LDT, ra, o));
-    fSqT[k2] = ld8(sw(sSqT, LDT, ra, o));
-    fSkT[k2] = ld8(sw(sSkT, LDT, ra, o));
+    fSq[k2] = ld8(swc<C>(sSq, LDT, rw, o));
+    fSk[k2] = ld8(swc<C>(sSk, LDT, rw, o));
+    fSqT[k2] = ld8(swc<C>(sSqT, LDT, rw, o));
+    fSkT[k2] = ld8(swc<C>(sSkT, LDT, rw, o));
   }
   if (tid < C) {
     // Gam_rt = exp(G_r - G_t): d/dG_r of sum R_rt = row sum, d/dG_t = -column sum
-    sRs[tid] = GATE == kGateScalar ? sRs[tid] - (sCs[tid] + sCs[C + tid] + sCs[2 * C + tid] + sCs[3 * C + tid])
-                                   : 0.f;
+    float cs4 = 0.f;
+#pragma unroll
+    for (int q = 0; q < NB; ++q) cs4 += sCs[q * C + tid];
+    sRs[tid] = GATE == kGateScalar ? sRs[tid] - cs4 : 0.f;
   }
   __syncthreads();   // every wave holds its adjoint fragments
   {
@@ -772,14 +811,14 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       Frag8<T> f;
 #pragma unroll
       for (int s2 = 0; s2 < 8; ++s2) f.set(s2, to_f(*sw(sKt, LDK, t8 + s2, c)));
-      st8(sw(sKtT, LDT, c, t8), f);
+      st8(swc<C>(sKtT, LDT, c, t8), f);
     }
   }
   // phase B computes its tiles transposed (every product with its operands
   // swapped), so a lane holds row ra = 16 w + lr at columns 16 j + 4 lg + ii
-  const float lam = GATE == kGateScalar ? fast_exp(sG[ra]) : 1.f;
-  const float wr = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[ra]) : 1.f;
-  const float bt = sBeta[ra];
+  const float lam = GATE == kGateScalar ? fast_exp(sG[rw]) : 1.f;
+  const float wr = GATE == kGateScalar ? fast_exp(sG[C - 1] - sG[rw]) : 1.f;
+  const float bt = sBeta[rw];
 
   // ---- phase B
   float pq = 0.f, pk = 0.f, pw = 0.f;
@@ -802,11 +841,11 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
     }
     // transposed Kt, Q, K tiles (loaded during an earlier pass)
     if ((p & 1) == 0) {
-      tile_t_store<T, HC>(sQT, tQ, tid);
-      tile_t_store<T, HC>(sKT, tK, tid);
+      tile_t_store<T, HC, C>(sQT, tQ, tid);
+      tile_t_store<T, HC, C>(sKT, tK, tid);
     } else {
-      tile_t_store<T, HC>(sQT, hQ, tid);
-      tile_t_store<T, HC>(sKT, hK, tid);
+      tile_t_store<T, HC, C>(sQT, hQ, tid);
+      tile_t_store<T, HC, C>(sKT, hK, tid);
     }
     __syncthreads();
     {
@@ -815,12 +854,12 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       const int cn = min(p + 1, NPASS - 1) * HC;
       srows.load(static_cast<const T*>(a.Hs) + cs + cn * DV, static_cast<const T*>(ba.dHs) + cs + cn * DV, tid);
       if ((p & 1) == 1 && p + 1 < NPASS) {   // the next two passes' tiles
-        load_pair_regs<T, HC>(tQ, hQ, qtile + cn, HD, n, tid);
-        load_pair_regs<T, HC>(tK, hK, ktile + cn, HD, n, tid);
+        load_pair_regs<T, HC, C>(tQ, hQ, qtile + cn, HD, n, tid);
+        load_pair_regs<T, HC, C>(tK, hK, ktile + cn, HD, n, tid);
       }
     }
 #pragma unroll 1
-    for (int j = 0; j < HC / 16; ++j) {
+    for (int j = 0; j < HC / 16 && rows; ++j) {
       // A1 = dO_s S, A2' = Z S, A3 = E dS' (transposed tiles)
       floatx4 A1 = {0.f, 0.f, 0.f, 0.f}, A2 = A1, A3 = A1;
 #pragma unroll
@@ -836,9 +875,9 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
         A1[ii] *= a.scale;
-        pq += to_f(*sw(sQT, LDT, cb + ii, ra)) * A1[ii];
-        pk += to_f(*sw(sKT, LDT, cb + ii, ra)) * A2[ii];
-        pw += to_f(*sw(sKtT, LDT, c0 + cb + ii, ra)) * A3[ii];
+        pq += to_f(*swc<C>(sQT, LDT, cb + ii, ra)) * A1[ii];
+        pk += to_f(*swc<C>(sKT, LDT, cb + ii, ra)) * A2[ii];
+        pw += to_f(*swc<C>(sKtT, LDT, c0 + cb + ii, ra)) * A3[ii];
       }
       floatx4 aq, ak, at;
 #pragma unroll
@@ -848,12 +887,12 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
         at[ii] = wr * A3[ii];
       }
 #pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        const Frag8<T> fk = ld8(sw(sKtT, LDT, c0 + 16 * j + lr, 32 * k2 + 8 * lg));
+      for (int k2 = 0; k2 < KC; ++k2) {
+        const Frag8<T> fk = ld8(swc<C>(sKtT, LDT, c0 + 16 * j + lr, 32 * k2 + 8 * lg));
         mma(aq, fk, fSq[k2]);
         mma(ak, fk, fSk[k2]);
-        mma(at, ld8(sw(sQT, LDT, 16 * j + lr, 32 * k2 + 8 * lg)), fSqT[k2]);
-        mma(at, ld8(sw(sKT, LDT, 16 * j + lr, 32 * k2 + 8 * lg)), fSkT[k2]);
+        mma(at, ld8(swc<C>(sQT, LDT, 16 * j + lr, 32 * k2 + 8 * lg)), fSqT[k2]);
+        mma(at, ld8(swc<C>(sKT, LDT, 16 * j + lr, 32 * k2 + 8 * lg)), fSkT[k2]);
       }
       // to this wave's output rows in LDS: row lr, four adjacent columns
       T* so = sOut + w * 3 * 16 * LDO + lr * LDO + cb;
@@ -861,7 +900,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
       st4<T>(so + 16 * LDO, ak[0], ak[1], ak[2], ak[3]);
       st4<T>(so + 32 * LDO, at[0], at[1], at[2], at[3]);
     }
-    p12_flush_rows<T, HC, LDO, DK>(sOut + w * 3 * 16 * LDO, dqr, HD, c0, dKm, dKt, w, l);
+    if (rows) p12_flush_rows<T, HC, LDO, DK>(sOut + w * 3 * 16 * LDO, dqr, HD, c0, dKm, dKt, w, l);
   }
 #pragma unroll
   for (int off = 16; off < 64; off <<= 1) {
@@ -869,7 +908,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
     pk += __shfl_xor(pk, off, 64);
     pw += __shfl_xor(pw, off, 64);
   }
-  if (lg == 0) {
+  if (lg == 0 && rows) {
     // dlam_r = Q_r . A1_r - beta_r K_r . A2'_r ;  dw_r = Kt_r . A3_r
     sDl[ra] = ra < n ? pq - bt * pk : 0.f;
     sDw[ra] = ra < n ? pw : 0.f;
@@ -886,11 +925,13 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
   }
   // ---- gate: dG_r, then the reverse in-chunk cumsum -> dg
   if (GATE == kGateScalar && w == 0) {
-    const int r = l;
-    const float lamr = fast_exp(sG[r]);
-    const float wrr = fast_exp(sG[C - 1] - sG[r]);
-    float wdw = wrr * sDw[r];
-    float dG = sRs[r] + lamr * sDl[r] - wdw;
+    // lanes r >= C (C = 32) carry zeros through the sums
+    const int r = l, rr = min(l, C - 1);
+    const bool in = r < C;
+    const float lamr = fast_exp(sG[rr]);
+    const float wrr = fast_exp(sG[C - 1] - sG[rr]);
+    float wdw = in ? wrr * sDw[rr] : 0.f;
+    float dG = in ? sRs[rr] + lamr * sDl[rr] - wdw : 0.f;
     // lam_C and the w_r all depend on G_{C-1}
     float tot = wdw;
 #pragma unroll
@@ -928,7 +969,7 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
 //                         + Lam_C sum_v S dS')
 // and dg is its reverse in-chunk cumsum.  dbeta_r = Z_r . V_r +
 // sum_c k_rc (dK_rc / beta_r) takes the bracket before the beta factor.
-template <typename T, int DK, int DV>
+template <typename T, int DK, int DV, int C>
 struct P12cSmem {
   static constexpr int HC = 32;
   static constexpr int LDE = DV + 8, LDV = DV + 8, LDT = C + 8, LDO = HC + 16, LDG = C + 4;
@@ -939,9 +980,10 @@ struct P12cSmem {
   static constexpr size_t kTotal = kMain + sizeof(float) * (3 * C + 4 * HC + HC + 8 * HC);
 };
 
-template <typename T, int DK, int DV>
+template <typename T, int DK, int DV, int C>
 __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
-  using SM = P12cSmem<T, DK, DV>;
+  using SM = P12cSmem<T, DK, DV, C>;
+  constexpr int NB = C / 16, KC = C / 32;
   constexpr int HC = SM::HC, LDE = SM::LDE, LDV = SM::LDV, LDT = SM::LDT, LDO = SM::LDO, LDG = SM::LDG;
   constexpr int KV = DV / 32, NPASS = DK / HC;
   constexpr uint32_t E = sizeof(T);
@@ -974,6 +1016,7 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
   const int i = static_cast<int>(blk % a.NT);
   const int64_t b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 15, lg = l >> 4;
+  const bool rows = NB == 4 || w < NB;   // this wave owns rows of the chunk
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
   const int64_t HV = a.H * (int64_t)DV, HD = a.H * (int64_t)DK;
@@ -991,7 +1034,7 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
 #pragma unroll
     for (int kk = 0; kk < KV; ++kk) {
       const uint32_t o = (rc * static_cast<uint32_t>(HV) + 32 * kk + 8 * lg) * E;
-      const uint32_t ow = (static_cast<uint32_t>(ra * DV) + 32 * kk + 8 * lg) * E;
+      const uint32_t ow = (static_cast<uint32_t>((rows ? ra : 0) * DV) + 32 * kk + 8 * lg) * E;
       fO[kk] = ld8(at_bytes(dob, o));
       fV[kk] = ld8(at_bytes(vb, o));
       fZ[kk] = ld8(at_bytes(zb, ow));
@@ -1004,9 +1047,9 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
       for (int s2 = 0; s2 < 8; ++s2) zv += fZ[kk].get(s2) * fV[kk].get(s2);
     zv += __shfl_xor(zv, 16, 64);
     zv += __shfl_xor(zv, 32, 64);
-    if (lg == 0) sZV[ra] = zv;
+    if (lg == 0 && rows) sZV[ra] = zv;
   }
-  RowStage<T, DV> stE;
+  RowStage<T, DV, C> stE;
   stE.load(static_cast<const T*>(a.Er) + rv, tid);
   // phase B's first state rows: in flight through the rest of phase A
   StateRows<T, HC, DV> srows;
@@ -1017,16 +1060,16 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
   const T* kttile = static_cast<const T*>(a.Ktr) + rk;
   // (the tiles of two passes at a time: whole lines)
   static_assert(NPASS % 2 == 0, "phase B passes come in pairs");
-  HeldTile<T, HC> tKt, tQ, tK, hKt, hQ, hK;
-  load_pair_regs<T, HC>(tKt, hKt, kttile, DK, C, tid);
-  load_pair_regs<T, HC>(tQ, hQ, qtile, HD, n, tid);
-  load_pair_regs<T, HC>(tK, hK, ktile, HD, n, tid);
+  HeldTile<T, HC, C> tKt, tQ, tK, hKt, hQ, hK;
+  load_pair_regs<T, HC, C>(tKt, hKt, kttile, DK, C, tid);
+  load_pair_regs<T, HC, C>(tQ, hQ, qtile, HD, n, tid);
+  load_pair_regs<T, HC, C>(tK, hK, ktile, HD, n, tid);
   stE.store(sE, tid);
   if (tid < C) sBeta[tid] = tid < n ? a.beta[(b * a.T + t0 + tid) * a.H + h] : 0.f;
   __syncthreads();
   // ---- phase A: dSqk = causal(dO_s E^T), dAt = strict_lower(-Z E^T)
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < NB && rows; ++j) {
     floatx4 dP = {0.f, 0.f, 0.f, 0.f}, dL = dP;
     if (j <= w) {
 #pragma unroll
@@ -1043,27 +1086,29 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
       dq[ii] = (r >= t && r < n) ? a.scale * dP[ii] : 0.f;
       dA[ii] = r > t ? -dL[ii] : 0.f;
       dAb[ii] = sBeta[r] * dA[ii];
-      *sw(sSq, LDT, r, t) = from_f<T>(dq[ii]);
-      *sw(sSk, LDT, r, t) = from_f<T>(dA[ii]);
+      *swc<C>(sSq, LDT, r, t) = from_f<T>(dq[ii]);
+      *swc<C>(sSk, LDT, r, t) = from_f<T>(dA[ii]);
     }
-    st4<T>(sw(sSqT, LDT, 16 * j + lr, 16 * w + 4 * lg), dq[0], dq[1], dq[2], dq[3]);
-    st4<T>(sw(sSkT, LDT, 16 * j + lr, 16 * w + 4 * lg), dAb[0], dAb[1], dAb[2], dAb[3]);
+    st4<T>(swc<C>(sSqT, LDT, 16 * j + lr, 16 * w + 4 * lg), dq[0], dq[1], dq[2], dq[3]);
+    st4<T>(swc<C>(sSkT, LDT, 16 * j + lr, 16 * w + 4 * lg), dAb[0], dAb[1], dAb[2], dAb[3]);
   }
+  // (a wave without rows of the chunk reads row 0: its results are unused)
+  const int rw = rows ? ra : 0;
 #pragma unroll
-  for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, ra, 32 * kk + 8 * lg));
+  for (int kk = 0; kk < KV; ++kk) fE[kk] = ld8(sw(sE, LDE, rw, 32 * kk + 8 * lg));
   __syncthreads();
-  Frag8<T> fSq[2], fSk[2], fSqT[2], fSkT[2];
+  Frag8<T> fSq[KC], fSk[KC], fSqT[KC], fSkT[KC];
 #pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) {
+  for (int k2 = 0; k2 < KC; ++k2) {
     const int o = 32 * k2 + 8 * lg;
-    fSq[k2] = ld8(sw(sSq, LDT, ra, o));
-    fSk[k2] = ld8(sw(sSk, LDT, ra, o));
-    fSqT[k2] = ld8(sw(sSqT, LDT, ra, o));
-    fSkT[k2] = ld8(sw(sSkT, LDT, ra, o));
+    fSq[k2] = ld8(swc<C>(sSq, LDT, rw, o));
+    fSk[k2] = ld8(swc<C>(sSk, LDT, rw, o));
+    fSqT[k2] = ld8(swc<C>(sSqT, LDT, rw, o));
+    fSkT[k2] = ld8(swc<C>(sSkT, LDT, rw, o));
   }
   float bt[4];
 #pragma unroll
-  for (int ii = 0; ii < 4; ++ii) bt[ii] = sBeta[16 * w + 4 * lg + ii];
+  for (int ii = 0; ii < 4; ++ii) bt[ii] = rows ? sBeta[16 * w + 4 * lg + ii] : 0.f;
 
   // ---- phase B
   float pdb[4] = {0.f, 0.f, 0.f, 0.f};
@@ -1106,13 +1151,13 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
       }
     }
     if ((p & 1) == 0) {
-      tile_t_store<T, HC>(sKtT, tKt, tid);
-      tile_t_store<T, HC>(sQT, tQ, tid);
-      tile_t_store<T, HC>(sKT, tK, tid);
+      tile_t_store<T, HC, C>(sKtT, tKt, tid);
+      tile_t_store<T, HC, C>(sQT, tQ, tid);
+      tile_t_store<T, HC, C>(sKT, tK, tid);
     } else {
-      tile_t_store<T, HC>(sKtT, hKt, tid);
-      tile_t_store<T, HC>(sQT, hQ, tid);
-      tile_t_store<T, HC>(sKT, hK, tid);
+      tile_t_store<T, HC, C>(sKtT, hKt, tid);
+      tile_t_store<T, HC, C>(sQT, hQ, tid);
+      tile_t_store<T, HC, C>(sKT, hK, tid);
     }
     __syncthreads();
     {
@@ -1121,13 +1166,13 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
       const int cn = min(p + 1, NPASS - 1) * HC;
       srows.load(static_cast<const T*>(a.Hs) + cs + cn * DV, static_cast<const T*>(ba.dHs) + cs + cn * DV, tid);
       if ((p & 1) == 1 && p + 1 < NPASS) {   // the next two passes' tiles
-        load_pair_regs<T, HC>(tKt, hKt, kttile + cn, DK, C, tid);
-        load_pair_regs<T, HC>(tQ, hQ, qtile + cn, HD, n, tid);
-        load_pair_regs<T, HC>(tK, hK, ktile + cn, HD, n, tid);
+        load_pair_regs<T, HC, C>(tKt, hKt, kttile + cn, DK, C, tid);
+        load_pair_regs<T, HC, C>(tQ, hQ, qtile + cn, HD, n, tid);
+        load_pair_regs<T, HC, C>(tK, hK, ktile + cn, HD, n, tid);
       }
     }
 #pragma unroll 1
-    for (int j = 0; j < HC / 16; ++j) {
+    for (int j = 0; j < HC / 16 && rows; ++j) {
       const int c = 16 * j + lr;
       const float* gcol = sGT + c * LDG;
       floatx4 A1 = {0.f, 0.f, 0.f, 0.f}, A2 = A1, A3 = A1;
@@ -1143,14 +1188,14 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
       const float gref = gcol[16 * w], gref2 = gcol[16 * w + 15];
       floatx4 aqi = {0.f, 0.f, 0.f, 0.f}, aki = aqi, ati = aqi;
 #pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
+      for (int k2 = 0; k2 < KC; ++k2) {
         const int tb = 32 * k2 + 8 * lg;
         const float4 g0 = *reinterpret_cast<const float4*>(gcol + tb);
         const float4 g1 = *reinterpret_cast<const float4*>(gcol + tb + 4);
         const float gt[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-        Frag8<T> fk = ld8(sw(sKtT, LDT, c, tb));
-        Frag8<T> fq = ld8(sw(sQT, LDT, c, tb));
-        Frag8<T> fr = ld8(sw(sKT, LDT, c, tb));
+        Frag8<T> fk = ld8(swc<C>(sKtT, LDT, c, tb));
+        Frag8<T> fq = ld8(swc<C>(sQT, LDT, c, tb));
+        Frag8<T> fr = ld8(swc<C>(sKT, LDT, c, tb));
 #pragma unroll
         for (int s2 = 0; s2 < 8; ++s2) {
           const int t = tb + s2;
@@ -1170,9 +1215,9 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
       const float gend = gcol[C - 1];
       const float4 g4 = *reinterpret_cast<const float4*>(gcol + 16 * w + 4 * lg);
       const float gr4[4] = {g4.x, g4.y, g4.z, g4.w};
-      const typename Vec4<T>::type q4 = *reinterpret_cast<const typename Vec4<T>::type*>(sw(sQT, LDT, c, 16 * w + 4 * lg));
-      const typename Vec4<T>::type k4 = *reinterpret_cast<const typename Vec4<T>::type*>(sw(sKT, LDT, c, 16 * w + 4 * lg));
-      const typename Vec4<T>::type t4 = *reinterpret_cast<const typename Vec4<T>::type*>(sw(sKtT, LDT, c, 16 * w + 4 * lg));
+      const typename Vec4<T>::type q4 = *reinterpret_cast<const typename Vec4<T>::type*>(swc<C>(sQT, LDT, c, 16 * w + 4 * lg));
+      const typename Vec4<T>::type k4 = *reinterpret_cast<const typename Vec4<T>::type*>(swc<C>(sKT, LDT, c, 16 * w + 4 * lg));
+      const typename Vec4<T>::type t4 = *reinterpret_cast<const typename Vec4<T>::type*>(swc<C>(sKtT, LDT, c, 16 * w + 4 * lg));
       floatx4 oq, ok, ot;
       float xk = 0.f;
 #pragma unroll
@@ -1201,30 +1246,34 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
         so[(32 + 4 * lg + ii) * LDO + c] = from_f<T>(ot[ii]);
       }
     }
-    p12_flush_rows<T, HC, LDO, DK>(sOut + w * 3 * 16 * LDO, dqr, HD, c0, dKm, dKt, w, l);
+    if (rows) p12_flush_rows<T, HC, LDO, DK>(sOut + w * 3 * 16 * LDO, dqr, HD, c0, dKm, dKt, w, l);
     __syncthreads();
     {
-      // dg_j = sum_{r >= j} dG_r + the last-row term, per channel: eight
+      // dg_j = sum_{r >= j} dG_r + the last-row term, per channel: C / 8
       // segments of 8 rows, then the totals of the later segments
+      constexpr int NSG = C / 8;
       const int c = tid & (HC - 1), sg = tid / HC;
+      const bool seg = NSG == 8 || sg < NSG;
       float x = 0.f;
       float v[8];
 #pragma unroll
       for (int q = 7; q >= 0; --q) {
-        x += sDG[(8 * sg + q) * (HC + 1) + c];
+        if (seg) x += sDG[(8 * sg + q) * (HC + 1) + c];
         v[q] = x;
       }
-      sSeg[sg * HC + c] = x;
+      if (seg) sSeg[sg * HC + c] = x;
       __syncthreads();
-      float add = fast_exp(sGT[c * LDG + C - 1]) * sRedC[c];
+      if (seg) {
+        float add = fast_exp(sGT[c * LDG + C - 1]) * sRedC[c];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) add += sXc[q * HC + c];
-      for (int q = sg + 1; q < 8; ++q) add += sSeg[q * HC + c];
-      float* dg = ba.dg + ((b * a.T + t0) * a.H + h) * DK + c0 + c;
+        for (int q = 0; q < NB; ++q) add += sXc[q * HC + c];
+        for (int q = sg + 1; q < NSG; ++q) add += sSeg[q * HC + c];
+        float* dg = ba.dg + ((b * a.T + t0) * a.H + h) * DK + c0 + c;
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int r = 8 * sg + q;
-        if (r < n) dg[r * HD] = v[q] + add;
+        for (int q = 0; q < 8; ++q) {
+          const int r = 8 * sg + q;
+          if (r < n) dg[r * HD] = v[q] + add;
+        }
       }
     }
   }
@@ -1232,7 +1281,7 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
   for (int ii = 0; ii < 4; ++ii)
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) pdb[ii] += __shfl_xor(pdb[ii], off, 64);
-  if (lr == 0) {
+  if (lr == 0 && rows) {
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) sDb[16 * w + 4 * lg + ii] = pdb[ii];
   }
@@ -1298,7 +1347,6 @@ __device__ __forceinline__ float pc_wave_sum16(const float (&v)[16], int l) {
 // the reverse one goes.  The per-token products come from the in-chunk
 // prefix of gP.  Loop bodies are branch-free.
 constexpr int PCG = 16;   // tokens per segment (one wave sum of 16 values)
-constexpr int PCS = C / PCG;
 
 template <typename T, int N>
 struct alignas(sizeof(T) * N) PcPack {
@@ -1390,8 +1438,9 @@ __device__ __forceinline__ PcInj pc_injection(float Ar, float gk, float kv, floa
   return r;
 }
 
-template <typename T, int DK, bool FINAL>
-__global__ __launch_bounds__(64 * PCS) void pc_chunk(BwdArgs ba) {
+template <typename T, int DK, bool FINAL, int C>
+__global__ __launch_bounds__(64 * (C / PCG)) void pc_chunk(BwdArgs ba) {
+  constexpr int PCS = C / PCG;   // segments (waves) per chunk
   constexpr int CPL = DK / 64;
   using Pk = PcPack<float, CPL>;
   using Pt = PcPack<T, CPL>;
@@ -1691,7 +1740,8 @@ __global__ __launch_bounds__(256) void combine_dk(BwdArgs ba) {
 // ------------------------------------------------------------ host side
 static size_t align256b(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
-BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond) {
+BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond, int C) {
+  const int PCS = C / PCG;
   BwdWsLayout L{};
   L.f = fwd_ws_layout(BH, NT, dk, esz, gate, precond, C);
   size_t off = L.f.total;
@@ -1720,29 +1770,30 @@ BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate,
 
 hipError_t launch_forward_parts(const FwdArgs& a, int io_bf16, hipStream_t s, hipEvent_t const* ev);
 
-template <typename T, int DK, int DV, int GATE>
+template <typename T, int DK, int DV, int GATE, int C>
 static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s, hipEvent_t const* ev) {
+  constexpr int PCS = C / PCG;
   const FwdArgs& a = ba.f;
   hipError_t e;
   auto mark = [&](int i) { return ev && ev[i] ? hipEventRecord(ev[i], s) : hipSuccess; };
   const int64_t nslab = DV / BVB;
   const unsigned grid_scan = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
   const unsigned grid_chunk = static_cast<unsigned>(a.BH * a.NT);
-  hipLaunchKernelGGL((r1_state_adjoint<T, DK, GATE>), dim3(grid_scan), dim3(256), 0, s, ba);
+  hipLaunchKernelGGL((r1_state_adjoint<T, DK, GATE, C>), dim3(grid_scan), dim3(256), 0, s, ba);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = mark(4)) != hipSuccess) return e;
   if constexpr (GATE == kGateChannel)
-    hipLaunchKernelGGL((p12c_chunk_grads<T, DK, DV>), dim3(grid_chunk), dim3(256), 0, s, ba);
+    hipLaunchKernelGGL((p12c_chunk_grads<T, DK, DV, C>), dim3(grid_chunk), dim3(256), 0, s, ba);
   else
-    hipLaunchKernelGGL((p12_chunk_grads<T, DK, DV, GATE>), dim3(grid_chunk), dim3(256), 0, s, ba);
+    hipLaunchKernelGGL((p12_chunk_grads<T, DK, DV, GATE, C>), dim3(grid_chunk), dim3(256), 0, s, ba);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = mark(5)) != hipSuccess) return e;
   if (a.precond == kSquash) {
-    hipLaunchKernelGGL((pc_chunk<T, DK, false>), dim3(grid_chunk), dim3(64 * PCS), 0, s, ba);
+    hipLaunchKernelGGL((pc_chunk<T, DK, false, C>), dim3(grid_chunk), dim3(64 * PCS), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((pc_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((pc_chunk<T, DK, true>), dim3(grid_chunk), dim3(64 * PCS), 0, s, ba);
+    hipLaunchKernelGGL((pc_chunk<T, DK, true, C>), dim3(grid_chunk), dim3(64 * PCS), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ba.dlog_a_scale) {
       hipLaunchKernelGGL(pc_mu, dim3(static_cast<unsigned>(a.H)), dim3(256), 0, s, ba);
@@ -1757,13 +1808,19 @@ static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s, hipEvent_t 
   return mark(6);
 }
 
+template <typename T, int DK, int DV, int C>
+static hipError_t launch_bwd_gate_c(const BwdArgs& ba, hipStream_t s, hipEvent_t const* ev) {
+  switch (ba.f.gate) {
+    case kGateNone: return launch_bwd_typed<T, DK, DV, kGateNone, C>(ba, s, ev);
+    case kGateScalar: return launch_bwd_typed<T, DK, DV, kGateScalar, C>(ba, s, ev);
+    default: return launch_bwd_typed<T, DK, DV, kGateChannel, C>(ba, s, ev);
+  }
+}
+
 template <typename T, int DK, int DV>
 static hipError_t launch_bwd_gate(const BwdArgs& ba, hipStream_t s, hipEvent_t const* ev) {
-  switch (ba.f.gate) {
-    case kGateNone: return launch_bwd_typed<T, DK, DV, kGateNone>(ba, s, ev);
-    case kGateScalar: return launch_bwd_typed<T, DK, DV, kGateScalar>(ba, s, ev);
-    default: return launch_bwd_typed<T, DK, DV, kGateChannel>(ba, s, ev);
-  }
+  return ba.f.chunk == 32 ? launch_bwd_gate_c<T, DK, DV, 32>(ba, s, ev)
+                          : launch_bwd_gate_c<T, DK, DV, 64>(ba, s, ev);
 }
 
 // fp32 io: head dims 64 only (LDS); the host validates this

@@ -146,7 +146,6 @@ pdn_status check_inputs(const pdn_problem* p, const pdn_inputs* in, const Sizes&
 // the backward covers every gate kind and the SQUASH / IDENTITY / EXTERNAL
 // write keys; fp32 io at head dims 64
 pdn_status check_bwd_support(const pdn_problem* p) {
-  if (p->chunk != 64) return PDN_ERR_UNSUPPORTED;
   if (p->io == PDN_F32 && (p->dk != 64 || p->dv != 64)) return PDN_ERR_UNSUPPORTED;
   if (p->precond == PDN_PRECOND_DIAG_SM || p->precond == PDN_PRECOND_ATQ) return PDN_ERR_UNSUPPORTED;
   if (p->knorm != PDN_KNORM_NONE) return PDN_ERR_UNSUPPORTED;
@@ -163,7 +162,7 @@ const char* pdn_status_string(pdn_status st) {
     case PDN_ERR_NULL: return "a required pointer is NULL";
     case PDN_ERR_SHAPE: return "invalid or overflowing shape";
     case PDN_ERR_DTYPE: return "unknown io dtype";
-    case PDN_ERR_UNSUPPORTED: return "head dimension, chunk size or mode not supported (dk, dv in {64, 128}; chunk 32 or 64, the backward and training pair 64)";
+    case PDN_ERR_UNSUPPORTED: return "head dimension, chunk size or mode not supported (dk, dv in {64, 128}; chunk 32 or 64)";
     case PDN_ERR_ALIGN: return "a tensor is not 16-byte aligned";
     case PDN_ERR_ALIAS: return "an output overlaps an input, another output or the workspace";
     case PDN_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
@@ -186,7 +185,7 @@ pdn_status pdn_workspace_size(const pdn_problem* p, int with_bwd, size_t* bytes)
   if (with_bwd) {
     const pdn_status sb = check_bwd_support(p);
     if (sb != PDN_OK) return sb;
-    *bytes = pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond).total;
+    *bytes = pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond, p->chunk).total;
     return PDN_OK;
   }
   const pdn::WsLayout L = pdn::fwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, s.esz, p->gate,
@@ -241,7 +240,7 @@ static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn
   const pdn::WsLayout L = pdn::fwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, s.esz, p->gate,
                                              p->precond, p->chunk);
   const pdn::BwdWsLayout LB =
-      pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond);
+      pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond, p->chunk);
   const size_t need_bytes = train ? LB.total : L.total;
   const bool need_ws = s.tok > 0;
   if (noalloc) {
@@ -339,7 +338,7 @@ static pdn_status chunk_bwd_impl(const pdn_problem* p, const pdn_inputs* in, con
   for (const Buf& x : ins)
     if (x.p && !aligned16(x.p)) return PDN_ERR_ALIGN;
   const pdn::BwdWsLayout L =
-      pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond);
+      pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond, p->chunk);
   if ((st = check_aliasing(ins, outs, Buf{ws, tok ? static_cast<int64_t>(ws_bytes) : 0})) != PDN_OK)
     return st;
   if (tok && (!ws || ws_bytes < L.total || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0))

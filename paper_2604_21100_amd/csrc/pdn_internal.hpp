@@ -96,8 +96,8 @@ struct BwdArgs {
   void* dKt;      // [BH, Tpad, dk] io    gradient of the write key
   void* dKm;      // [BH, Tpad, dk] io    gradient of the read key (main recurrence)
   float* pcL;     // [BH, NT, dk]         preconditioner: in-chunk adjoint at chunk start
-  float* pcS;     // [BH, NT, 4, dk]      preconditioner: per 16-token segment, the in-segment adjoint it sends left
-  float* pcA;     // [BH, NT, 4, dk]      preconditioner: per 16-token segment, the state before it
+  float* pcS;     // [BH, NT, C/16, dk]   preconditioner: per 16-token segment, the in-segment adjoint it sends left
+  float* pcA;     // [BH, NT, C/16, dk]   preconditioner: per 16-token segment, the state before it
   float* pcC;     // [BH, NT + 1, dk]     preconditioner: adjoint carried into each chunk
   float* pcMu;    // [BH, NT]             preconditioner: partial d mu
 };
@@ -114,7 +114,7 @@ struct BwdWsLayout {
   size_t dHs, Zr, dKt, dKm, pcL, pcS, pcA, pcC, pcMu, total;
 };
 
-BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond);
+BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond, int C);
 
 // ev: NULL or 8 events recorded at the stage boundaries (see
 // pdn_chunk_bwd_events).  recompute = false: the forward intermediates are

@@ -337,17 +337,17 @@ def test_noalloc_validates_like_the_forward():
 
 
 def test_chunk_sizes():
-    """Chunks of 32 and 64 tokens run the forward; the backward and the
-    training pair are built for 64 only (PDN_ERR_UNSUPPORTED, before any HIP
-    call).  The 32-token workspace holds twice the chunks."""
+    """Chunks of 32 and 64 tokens: forward, backward and training-pair
+    workspaces size, and argument checks run for both (a one-byte-short
+    workspace fails before any HIP call)."""
     p32, p64 = _prob(chunk=32), _prob(chunk=64)
-    n32, n64 = pdn.pdn_workspace_size(p32), pdn.pdn_workspace_size(p64)
-    assert n32 > 0 and n64 > 0
-    with pytest.raises(pdn.PdnError) as e:
-        pdn.pdn_workspace_size(p32, True)
-    assert e.value.status == pdn.PDN_ERR_UNSUPPORTED
-    st = pdn.pdn_chunk_bwd_raw(p32, _inputs(), A * 30, None,
-                               pdn.BwdOut(*([None] * 11)), A * 64, 0, 0)
-    assert st == pdn.PDN_ERR_UNSUPPORTED
-    # forward validation still runs for chunk 32 (a one-byte-short workspace)
+    for with_bwd in (False, True):
+        n32 = pdn.pdn_workspace_size(p32, with_bwd)
+        n64 = pdn.pdn_workspace_size(p64, with_bwd)
+        assert n32 > 0 and n64 > 0
     assert _fwd(p32) == pdn.PDN_ERR_WORKSPACE
+    st = pdn.pdn_chunk_bwd_raw(p32, _inputs(), A * 30, None,
+                               pdn.BwdOut(A * 40, A * 41, A * 42, A * 43, A * 44,
+                                          None, None, None, None, None, None),
+                               A * 64, 1, 0)
+    assert st == pdn.PDN_ERR_WORKSPACE

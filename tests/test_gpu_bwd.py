@@ -24,7 +24,7 @@ def _heads(x, B, H):
     return np.stack([x[b, :, h] for b in range(B) for h in range(H)])
 
 
-def run_bwd(spec, inp, precond="squash", dS_T=None):
+def run_bwd(spec, inp, precond="squash", dS_T=None, chunk=64):
     import torch
     import paper_2604_21100_amd as pdn
     d = to_device(inp, spec.io)
@@ -37,13 +37,13 @@ def run_bwd(spec, inp, precond="squash", dS_T=None):
         log_a_scale=d["log_a_scale"] if sq else None,
         A0=d["A0"] if sq else None, S0=d["S0"],
         ktilde=d.get("ktilde") if precond == "external" else None,
-        dS_T=dST, x=spec.x, scale=spec.scale)
+        dS_T=dST, x=spec.x, scale=spec.scale, chunk=chunk)
     torch.cuda.synchronize()
     return {k: v.float().cpu().numpy().astype(np.float64) for k, v in out.items()}
 
 
-def compare(spec, inp, precond="squash", dS_T=None, heads=None, tag=""):
-    got = run_bwd(spec, inp, precond, dS_T)
+def compare(spec, inp, precond="squash", dS_T=None, heads=None, tag="", chunk=64):
+    got = run_bwd(spec, inp, precond, dS_T, chunk)
     B, H = spec.B, spec.H
     if heads is None:
         heads = oabi.all_heads(B, H)
@@ -179,3 +179,51 @@ def test_bwd_full_workload_sampled_heads():
     spec = pi.WORKLOADS[name]
     inp = pi.generate(spec, pi.WORKLOAD_SEEDS[name])
     compare(spec, inp, heads=[(0, 0), (0, 15)], tag=name)
+
+
+CHUNK32 = [
+    # (io, gate, precond, dk, dv): the backward with 32-token chunks
+    ("bf16", "scalar", "squash", 128, 128),
+    ("bf16", "none", "squash", 128, 64),
+    ("bf16", "channel", "squash", 128, 128),
+    ("bf16", "scalar", "identity", 64, 128),
+    ("bf16", "channel", "external", 128, 64),
+    ("f32", "scalar", "squash", 64, 64),
+    ("f32", "channel", "identity", 64, 64),
+    ("f32", "none", "external", 64, 64),
+]
+
+
+@pytest.mark.parametrize("io,gate,precond,dk,dv", CHUNK32)
+def test_bwd_chunk32_all_heads(io, gate, precond, dk, dv):
+    """chunk = 32: T = 200 (six chunks and a ragged tail of 8), every head,
+    nonzero S0, A0 and dS_T, every gradient against the oracle adjoint."""
+    spec = pi.small_spec(io=io, gate=gate, dk=dk, dv=dv, s0="normal",
+                         a0="lognormal" if precond == "squash" else "zero",
+                         with_do=True)
+    inp = pi.generate(spec, 23)
+    if precond == "external":
+        rng = np.random.default_rng(6)
+        kt = inp["k"] * rng.uniform(1 / 1.5, 1.5, inp["k"].shape)
+        inp["ktilde"] = pi.round_bf16(kt) if io == "bf16" else kt.astype(np.float32)
+    dS_T = (0.1 * np.random.default_rng(8).standard_normal(
+        (spec.B, spec.H, dk, dv))).astype(np.float32)
+    compare(spec, inp, precond, dS_T, tag=f"chunk32 {io}/{gate}/{precond}/{dk}x{dv}",
+            chunk=32)
+
+
+@pytest.mark.parametrize("T", [1, 16, 17, 31, 32, 33, 65, 100])
+@pytest.mark.parametrize("gate", ["scalar", "channel"])
+def test_bwd_chunk32_sequence_lengths(T, gate):
+    """Last chunks of 1, 16 (one whole 16-token segment), 17 and 31 tokens,
+    and whole chunks."""
+    spec = pi.small_spec(T=T, B=1, H=2, gate=gate, dk=128, dv=128, with_do=True)
+    compare(spec, pi.generate(spec, 600 + T), tag=f"chunk32 {gate} T={T}",
+            chunk=32)
+
+
+def test_bwd_chunk32_coverage():
+    """beta in [0, 2], anisotropic keys, beta^P over decades, chunk = 32."""
+    spec = pi.small_spec(gate="scalar", dk=128, dv=128, with_do=True,
+                         beta_max=2.0, key_aniso=1.0, betap_logspan=2.0)
+    compare(spec, pi.generate(spec, 31), tag="chunk32 beta02/aniso", chunk=32)

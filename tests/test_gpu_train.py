@@ -26,7 +26,7 @@ CASES = [
 ]
 
 
-def _run(spec, inp, precond):
+def _run(spec, inp, precond, chunk=64):
     import torch
     import paper_2604_21100_amd as pdn
     d = to_device(inp, spec.io)
@@ -36,11 +36,11 @@ def _run(spec, inp, precond):
               log_a_scale=d["log_a_scale"] if sq else None,
               A0=d["A0"] if sq else None, S0=d["S0"],
               ktilde=d.get("ktilde") if precond == "external" else None,
-              x=spec.x, scale=spec.scale)
+              x=spec.x, scale=spec.scale, chunk=chunk)
     B, T, H = spec.B, spec.T, spec.H
     prob = pdn.make_problem(B, T, H, spec.dk, spec.dv, io=spec.io,
                             gate=spec.gate, precond=precond, x=spec.x,
-                            scale=spec.scale)
+                            scale=spec.scale, chunk=chunk)
     ws = torch.zeros(max(pdn.pdn_workspace_size(prob, True), 1),
                      dtype=torch.uint8, device="cuda")
     dST = torch.from_numpy((0.1 * np.random.default_rng(3).standard_normal(
@@ -58,8 +58,9 @@ def _run(spec, inp, precond):
     return ref_f, ref_b, got_f, got_b, again
 
 
+@pytest.mark.parametrize("chunk", [64, 32])
 @pytest.mark.parametrize("io,gate,precond,dk,dv,T", CASES)
-def test_training_pair_matches(io, gate, precond, dk, dv, T):
+def test_training_pair_matches(io, gate, precond, dk, dv, T, chunk):
     import torch
     spec = pi.small_spec(io=io, gate=gate, dk=dk, dv=dv, T=T, s0="normal",
                          a0="lognormal" if precond == "squash" else "zero",
@@ -69,8 +70,8 @@ def test_training_pair_matches(io, gate, precond, dk, dv, T):
         rng = np.random.default_rng(5)
         kt = inp["k"] * rng.uniform(1 / 1.5, 1.5, inp["k"].shape)
         inp["ktilde"] = pi.round_bf16(kt) if io == "bf16" else kt.astype(np.float32)
-    ref_f, ref_b, got_f, got_b, again = _run(spec, inp, precond)
-    print(f"{io}/{gate}/{precond}/{dk}x{dv}/T={T}")
+    ref_f, ref_b, got_f, got_b, again = _run(spec, inp, precond, chunk)
+    print(f"{io}/{gate}/{precond}/{dk}x{dv}/T={T}/chunk={chunk}")
     for a, b in zip(ref_f, got_f):
         if a is None:
             assert b is None
