@@ -673,13 +673,16 @@ __global__ __launch_bounds__(256, 2) void p12_chunk_grads(BwdArgs ba) {
     }
     stE.load(eb, tid);
   }
+  // per-row scalars, with the tiles: every wave loads the chunk's rows and
+  // stores the same values (no branch, so the loads issue with the rest)
+  const int rs = tid % C;
+  const float vG = GATE == kGateScalar ? a.G[bh * a.Tpad + t0 + rs] : 0.f;
+  const float vB = a.beta[(b * a.T + t0 + min(rs, n - 1)) * a.H + h];
   // ---- phase A: shared B operands (Kt now, E after the Gram products) and
   // per-row scalars
   stKt.store(sKt, tid);
-  if (tid < C) {
-    sG[tid] = GATE == kGateScalar ? a.G[bh * a.Tpad + t0 + tid] : 0.f;
-    sBeta[tid] = tid < n ? a.beta[(b * a.T + t0 + tid) * a.H + h] : 0.f;
-  }
+  sG[rs] = vG;
+  sBeta[rs] = rs < n ? vB : 0.f;
   __syncthreads();
   // the Gram products (Q and K rows die here)
   floatx4 Sqk[NB], Skk[NB];
@@ -1064,8 +1067,10 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
   load_pair_regs<T, HC, C>(tKt, hKt, kttile, DK, C, tid);
   load_pair_regs<T, HC, C>(tQ, hQ, qtile, HD, n, tid);
   load_pair_regs<T, HC, C>(tK, hK, ktile, HD, n, tid);
+  const int rs = tid % C;
+  const float vB = a.beta[(b * a.T + t0 + min(rs, n - 1)) * a.H + h];
   stE.store(sE, tid);
-  if (tid < C) sBeta[tid] = tid < n ? a.beta[(b * a.T + t0 + tid) * a.H + h] : 0.f;
+  sBeta[rs] = rs < n ? vB : 0.f;   // every wave stores the same values
   __syncthreads();
   // ---- phase A: dSqk = causal(dO_s E^T), dAt = strict_lower(-Z E^T)
 #pragma unroll
@@ -1444,7 +1449,8 @@ __global__ __launch_bounds__(64 * (C / PCG)) void pc_chunk(BwdArgs ba) {
   constexpr int CPL = DK / 64;
   using Pk = PcPack<float, CPL>;
   using Pt = PcPack<T, CPL>;
-  __shared__ float sEgp[C], sBp[C], sFf[C];
+  // per-token factors, one entry per lane (entries from C on unused)
+  __shared__ float sEgp[64], sBp[64], sFf[64];
   __shared__ float sEnd[PCS][DK];          // summary pass: per-segment end values (A, then adjoint)
   // the states A_r of each wave's segment, read back in the reverse
   // recurrence (a wave reads only its own rows; kept here rather than in
@@ -1469,17 +1475,13 @@ __global__ __launch_bounds__(64 * (C / PCG)) void pc_chunk(BwdArgs ba) {
   const T* mb = static_cast<const T*>(ba.dKm) + (bh * a.Tpad + t0) * DK;
   // per-segment values of this chunk: [BH, NT, PCS, DK]
   const int64_t segb = ((bh * a.NT + i) * PCS) * DK;
-  // every row of the segment in flight first; rows past the sequence end
-  // re-read the last row (keys are zeroed at use, dkt and dkm rows there are
-  // zero)
-  Pt kr[PCG], gr[PCG], mr[FINAL ? PCG : 1];
-#pragma unroll
-  for (int j = 0; j < PCG; ++j) {
-    const uint32_t rr = static_cast<uint32_t>(min(s0 + j, n - 1));
-    const uint32_t ow = static_cast<uint32_t>((s0 + j) * DK) * E + lo;
-    kr[j] = *reinterpret_cast<const Pt*>(at_bytes(kb, rr * kstb + lo));
-    gr[j] = *reinterpret_cast<const Pt*>(at_bytes(gb, ow));
-  }
+  // the per-token inputs first (lane = token; every wave loads them, so no
+  // branch holds them back), then every row of the segment; rows past the
+  // sequence end re-read the last row (keys are zeroed at use, dkt and dkm
+  // rows there are zero)
+  const int64_t lidx = (b * a.T + t0 + min(l, n - 1)) * a.H + h;
+  const float vgp = a.g_p ? a.g_p[lidx] : 0.f;
+  const float vbp = a.beta_p[lidx];
   // FINAL: the exact state before the segment and the adjoints the later
   // segments send (zero carry), then the chunk's carry from the right
   Pk A_seg, S_seg[PCS - 1], kap_chunk;
@@ -1492,24 +1494,33 @@ __global__ __launch_bounds__(64 * (C / PCG)) void pc_chunk(BwdArgs ba) {
   } else {
     A_seg = *reinterpret_cast<const Pk*>(a.Abound + (bh * (a.NT + 1) + i) * DK + c0);
   }
-  if (tid < C) {
+  Pt kr[PCG], gr[PCG], mr[FINAL ? PCG : 1];
+#pragma unroll
+  for (int j = 0; j < PCG; ++j) {
+    const uint32_t rr = static_cast<uint32_t>(min(s0 + j, n - 1));
+    const uint32_t ow = static_cast<uint32_t>((s0 + j) * DK) * E + lo;
+    kr[j] = *reinterpret_cast<const Pt*>(at_bytes(kb, rr * kstb + lo));
+    gr[j] = *reinterpret_cast<const Pt*>(at_bytes(gb, ow));
+  }
+  {
     // per-token factors; padded tokens: aP = 1 (gP = 0), bP = 0; x is the
-    // in-chunk inclusive prefix of gP (one wave, shuffle scan)
-    const bool ok = tid < n;
-    const int64_t sidx = (b * a.T + t0 + min(tid, n - 1)) * a.H + h;
-    const float gp = (ok && a.g_p) ? a.g_p[sidx] : 0.f;
-    sEgp[tid] = fast_exp(gp);
-    sBp[tid] = ok ? a.beta_p[sidx] : 0.f;
+    // in-chunk inclusive prefix of gP (shuffle scan over the lanes).  Every
+    // wave computes and stores the same values: without a branch the
+    // compiler keeps their loads ahead of the segment rows'
+    const bool ok = l < n;
+    const float gp = ok ? vgp : 0.f;
     float x = gp;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
       const float y = __shfl_up(x, off, 64);
-      if (tid >= off) x += y;
+      if (l >= off) x += y;
     }
     // segment composition factor prod_{s0 <= j <= r} aP_j
-    const int q0 = tid & ~(PCG - 1);
+    const int q0 = l & ~(PCG - 1);
     const float gb = __shfl(x, q0 - 1, 64);
-    sFf[tid] = fast_exp(x - (q0 > 0 ? gb : 0.f));
+    sEgp[l] = fast_exp(gp);
+    sBp[l] = ok ? vbp : 0.f;
+    sFf[l] = fast_exp(x - (q0 > 0 ? gb : 0.f));
   }
   if (s0 + PCG > n) {   // wave-uniform: only the last chunk's tail segments
 #pragma unroll

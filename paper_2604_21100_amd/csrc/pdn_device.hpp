@@ -172,6 +172,10 @@ constexpr int kBufWord3 = 0x00020000;
 
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kLog2e = 1.4426950408889634f;
+// v where ok, else zeros (per component, so the value stays in registers)
+__device__ __forceinline__ float4 keep_if(float4 v, bool ok) {
+  return make_float4(ok ? v.x : 0.f, ok ? v.y : 0.f, ok ? v.z : 0.f, ok ? v.w : 0.f);
+}
 __device__ __forceinline__ float fast_exp(float x) { return __expf(x); }
 // 2^x on the hardware exponential (a result below the normal range flushes
 // to zero)

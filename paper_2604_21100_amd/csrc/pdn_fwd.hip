@@ -42,30 +42,40 @@ __global__ __launch_bounds__(256) void k1_precond_summary(FwdArgs a) {
   const int tid = threadIdx.x;
   const int64_t t0 = static_cast<int64_t>(i) * C;
   const int n = static_cast<int>(min<int64_t>(C, a.T - t0));
+  // this thread's key vectors, issued first (rows past the sequence end
+  // read the last valid row; their weight below is zero)
+  const T* k = static_cast<const T*>(a.k);
+  const int cg = tid % VPR, r0 = tid / VPR;
+  static_assert(C % RPP == 0, "whole passes of rows");
+  float4 raw[C / RPP];
+#pragma unroll
+  for (int j = 0; j < C / RPP; ++j) {
+    const int r = min(r0 + j * RPP, n - 1);
+    raw[j] = *reinterpret_cast<const float4*>(k + ((b * a.T + t0 + r) * a.H + h) * DK + cg * VEC);
+  }
   if (tid < 64) {
     const int r = tid;
-    const int64_t sidx = (b * a.T + t0 + r) * a.H + h;
-    float gp = (r < n && a.g_p) ? a.g_p[sidx] : 0.f;
+    const int64_t sidx = (b * a.T + t0 + min(r, n - 1)) * a.H + h;
+    const float bp = a.beta_p[sidx];
+    float gp = a.g_p ? a.g_p[sidx] : 0.f;
+    if (r >= n) gp = 0.f;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
       const float y = __shfl_up(gp, off, 64);
       if (r >= off) gp += y;
     }
     const float gend = __shfl(gp, 63, 64);
-    if (r < C) sW[r] = r < n ? a.beta_p[sidx] * fast_exp(gend - gp) : 0.f;
+    if (r < C) sW[r] = r < n ? bp * fast_exp(gend - gp) : 0.f;
     if (r == 0) a.sumD[bh * a.NT + i] = gend;
   }
   __syncthreads();
-  const T* k = static_cast<const T*>(a.k);
-  const int cg = tid % VPR, r0 = tid / VPR;
   float acc[VEC];
 #pragma unroll
   for (int s = 0; s < VEC; ++s) acc[s] = 0.f;
-  for (int r = r0; r < n; r += RPP) {
-    const T* src = k + ((b * a.T + t0 + r) * a.H + h) * DK + cg * VEC;
-    float4 raw = *reinterpret_cast<const float4*>(src);
-    const T* e = reinterpret_cast<const T*>(&raw);
-    const float wr = sW[r];
+#pragma unroll
+  for (int j = 0; j < C / RPP; ++j) {
+    const T* e = reinterpret_cast<const T*>(&raw[j]);
+    const float wr = sW[r0 + j * RPP];
 #pragma unroll
     for (int s = 0; s < VEC; ++s) {
       const float kv = to_f(e[s]);
@@ -92,20 +102,31 @@ __global__ __launch_bounds__(DK) void k1_precond_carry(FwdArgs a) {
   const float* L = a.sumL + bh * a.NT * DK + c;
   const float* D = a.sumD + bh * a.NT;
   out[0] = A;
-  int i = 0;
-  for (; i + 8 <= a.NT; i += 8) {
-    float d[8], l[8];
+  // batches of 8 chunks; the next batch's loads are issued before the
+  // current batch is chained
+  constexpr int U = 8;
+  float d[U], l[U], dn[U], ln[U];
+  const int NT = a.NT;
 #pragma unroll
-    for (int u = 0; u < 8; ++u) { d[u] = D[i + u]; l[u] = L[(int64_t)(i + u) * DK]; }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      A = fast_exp(d[u]) * A + l[u];
-      out[(int64_t)(i + u + 1) * DK] = A;
-    }
+  for (int u = 0; u < U; ++u) {
+    const int j = min(u, NT - 1);
+    d[u] = D[j]; l[u] = L[(int64_t)j * DK];
   }
-  for (; i < a.NT; ++i) {
-    A = fast_exp(D[i]) * A + L[(int64_t)i * DK];
-    out[(int64_t)(i + 1) * DK] = A;
+  for (int i = 0; i < NT; i += U) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = min(i + U + u, NT - 1);
+      dn[u] = D[j]; ln[u] = L[(int64_t)j * DK];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (i + u < NT) {
+        A = fast_exp(d[u]) * A + l[u];
+        out[(int64_t)(i + u + 1) * DK] = A;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) { d[u] = dn[u]; l[u] = ln[u]; }
   }
   if (a.A_T) a.A_T[bh * DK + c] = A;
 }
@@ -190,52 +211,81 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   constexpr int VEC = 16 / sizeof(T);
   constexpr int VPR = DK / VEC;  // vectors per row
 
-  // ---- load key, query (and external write key) tiles, zero-padded
+  // ---- load key, query (and external write key) tiles, zero-padded.
+  // Every global load of the phase is issued before the first is used (rows
+  // past the sequence end read the last valid row and are zeroed after), so
+  // the block waits for one memory round trip rather than one per vector.
+  float Ab = 0.f;    // preconditioner state before this chunk, one channel per thread
+  float lmu = 0.f;   // log of the squash scale
   {
     const T* kp = static_cast<const T*>(a.k);
     const T* qp = static_cast<const T*>(a.q);
     const T* xp = static_cast<const T*>(a.ktilde);
     static_assert((C * VPR) % 256 == 0, "whole rounds of 256 threads");
+    constexpr int NJ = (C * VPR) / 256;
+    constexpr int NG = GATE == kGateChannel ? (C * (DK / 4)) / 256 : 0;
+    float4 kv[NJ], qv[NJ], xv[NJ], gv[NG > 0 ? NG : 1];
 #pragma unroll
-    for (int jj = 0; jj < (C * VPR) / 256; ++jj) {
+    for (int jj = 0; jj < NJ; ++jj) {
       const int idx = tid + 256 * jj;
-      const int r = idx / VPR, cv = idx % VPR;
-      float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), qv = kv, xv = kv;
-      if (r < n) {
-        const int64_t off = ((b * a.T + t0 + r) * a.H + h) * DK + cv * VEC;
-        kv = *reinterpret_cast<const float4*>(kp + off);
-        if (!NOQ) qv = *reinterpret_cast<const float4*>(qp + off);
-        if (PREC == kExternal) xv = *reinterpret_cast<const float4*>(xp + off);
-      }
-      *reinterpret_cast<float4*>(k2sw(sK, LDK, r, cv * VEC)) = kv;
-      if (!NOQ) *reinterpret_cast<float4*>(k2sw(sQ, LDK, r, cv * VEC)) = qv;
-      // identity write key: a copy of the key tile (the key tile's memory is
-      // reused by the solve)
-      if (PREC == kIdentity || PREC == kATQ) *reinterpret_cast<float4*>(k2sw(sKt, LDK, r, cv * VEC)) = kv;
-      if (PREC == kExternal) *reinterpret_cast<float4*>(k2sw(sKt, LDK, r, cv * VEC)) = xv;
-    }
-    if (tid < C) {
-      const int r = tid;
-      const bool ok = r < n;
-      const int64_t sidx = (b * a.T + t0 + r) * a.H + h;
-      sBeta[r] = ok ? a.beta[sidx] : 0.f;
-      if (has_gram(PREC)) {
-        sBp[r] = ok ? a.beta_p[sidx] : 0.f;
-        sEgp[r] = (ok && a.g_p) ? fast_exp(a.g_p[sidx]) : 1.f;
-      }
-      if (GATE == kGateScalar) sGraw[r] = ok ? a.g[sidx] : 0.f;
+      const int r = min(idx / VPR, n - 1), cv = idx % VPR;
+      const int64_t off = ((b * a.T + t0 + r) * a.H + h) * DK + cv * VEC;
+      kv[jj] = *reinterpret_cast<const float4*>(kp + off);
+      if (!NOQ) qv[jj] = *reinterpret_cast<const float4*>(qp + off);
+      if (PREC == kExternal) xv[jj] = *reinterpret_cast<const float4*>(xp + off);
     }
     if (GATE == kGateChannel) {
       static_assert((C * (DK / 4)) % 256 == 0, "whole rounds of 256 threads");
 #pragma unroll
-      for (int jj = 0; jj < (C * (DK / 4)) / 256; ++jj) {
+      for (int jj = 0; jj < NG; ++jj) {
+        const int idx = tid + 256 * jj;
+        const int r = min(idx / (DK / 4), n - 1), c4 = idx % (DK / 4);
+        gv[jj] = *reinterpret_cast<const float4*>(a.g + ((b * a.T + t0 + r) * a.H + h) * DK + c4 * 4);
+      }
+    }
+    // per-row scalars: every wave loads the chunk's rows (branch-free, so
+    // the loads issue with the tiles'); the first C threads keep them
+    const int64_t sidx = (b * a.T + t0 + min(tid % C, n - 1)) * a.H + h;
+    const float vb = a.beta[sidx];
+    float vbp = 0.f, vgp = 0.f, vg = 0.f;
+    if (has_gram(PREC)) {
+      vbp = a.beta_p[sidx];
+      vgp = (a.g_p ? a.g_p : a.beta_p)[sidx];   // (unused without g_p)
+      Ab = a.Abound[(bh * (a.NT + 1) + i) * DK + tid % DK];
+      if (PREC == kSquash) lmu = a.log_a_scale[h];
+    }
+    if (GATE == kGateScalar) vg = a.g[sidx];
+#pragma unroll
+    for (int jj = 0; jj < NJ; ++jj) {
+      const int idx = tid + 256 * jj;
+      const int r = idx / VPR, cv = idx % VPR;
+      const bool ok = r < n;
+      *reinterpret_cast<float4*>(k2sw(sK, LDK, r, cv * VEC)) = keep_if(kv[jj], ok);
+      if (!NOQ) *reinterpret_cast<float4*>(k2sw(sQ, LDK, r, cv * VEC)) = keep_if(qv[jj], ok);
+      // identity write key: a copy of the key tile (the key tile's memory is
+      // reused by the solve)
+      if (PREC == kIdentity || PREC == kATQ) *reinterpret_cast<float4*>(k2sw(sKt, LDK, r, cv * VEC)) = keep_if(kv[jj], ok);
+      if (PREC == kExternal) *reinterpret_cast<float4*>(k2sw(sKt, LDK, r, cv * VEC)) = keep_if(xv[jj], ok);
+    }
+    if (GATE == kGateChannel) {
+#pragma unroll
+      for (int jj = 0; jj < NG; ++jj) {
         const int idx = tid + 256 * jj;
         const int r = idx / (DK / 4), c4 = idx % (DK / 4);
-        float4 gv = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (r < n)
-          gv = *reinterpret_cast<const float4*>(a.g + ((b * a.T + t0 + r) * a.H + h) * DK + c4 * 4);
-        *reinterpret_cast<float4*>(k2swf(sGc, DK + 4, r, c4 * 4)) = gv;
+        *reinterpret_cast<float4*>(k2swf(sGc, DK + 4, r, c4 * 4)) = keep_if(gv[jj], r < n);
       }
+    }
+    // every wave stores the same row scalars (identical values): no branch,
+    // so the compiler keeps their loads with the tiles'
+    {
+      const int r = tid % C;
+      const bool ok = r < n;
+      sBeta[r] = ok ? vb : 0.f;
+      if (has_gram(PREC)) {
+        sBp[r] = ok ? vbp : 0.f;
+        sEgp[r] = (ok && a.g_p) ? fast_exp(vgp) : 1.f;
+      }
+      if (GATE == kGateScalar) sGraw[r] = ok ? vg : 0.f;
     }
   }
   __syncthreads();
@@ -297,10 +347,10 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     sSegE[sg * DK + c] = E;
     sSegP[sg * DK + c] = Pp;
     __syncthreads();
-    float A = a.Abound[(bh * (a.NT + 1) + i) * DK + c];
+    float A = Ab;
     for (int q = 0; q < sg; ++q) A = sSegE[q * DK + c] * A + sSegP[q * DK + c];
     if (PREC == kSquash) {
-      const float mu = fast_exp(a.log_a_scale[h]);
+      const float mu = fast_exp(lmu);
       const float A_seg = A;
 #pragma unroll
       for (int j = 0; j < SEG; ++j) {
