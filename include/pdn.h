@@ -84,6 +84,17 @@ typedef enum {
   PDN_GATE_CHANNEL = 2  /* PKDA: alpha_t = exp(g_t), g [B,T,H,dk]   */
 } pdn_gate;
 
+/* Admissible per-channel decay (PDN_GATE_CHANNEL).  Inside a chunk the
+ * decay between tokens t <= r of one channel, exp(G_r - G_t) with G the
+ * in-chunk prefix sum of that channel's g, is applied as the product of two
+ * fp32 factors split at a reference row of each 16-token block (forward
+ * interaction matrices and the backward's intra-chunk products).  One of
+ * the two is the exponential of up to 15 consecutive log-decays with the
+ * sign flipped, so every run of 15 consecutive g of a channel must sum to
+ * more than -87 (a mean log-decay above -5.8 per token, alpha above 0.003);
+ * below that the factor overflows and outputs and gradients hold Inf / NaN.
+ * Nothing checks the range.  The scalar gate has no such limit.           */
+
 typedef enum {
   PDN_PRECOND_SQUASH = 0,   /* write key of Eq. precond_end2end (the method) */
   PDN_PRECOND_IDENTITY = 1, /* kt = k: plain DeltaNet / GDN / KDA            */

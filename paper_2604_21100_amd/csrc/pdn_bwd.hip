@@ -181,7 +181,7 @@ __device__ __forceinline__ void rev_load(RevFrags<T, DK, GATE, C>& f, const BwdA
     for (int ii = 0; ii < 4; ++ii) f.gw[ii] = rows ? a.G[x.bh * a.Tpad + t0 + 16 * x.w + 4 * x.lg + ii] : 0.f;
   }
   if (GATE == kGateChannel) {
-    const float* gl = a.G + (x.bh * a.Tpad + t0 + C - 1) * DK;
+    const float* gl = a.G + (x.bh * a.NT + i) * DK;   // G at the chunk end
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
@@ -1124,11 +1124,26 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
       dq, 0, static_cast<int>(((n - 1) * HD + DK) * static_cast<int64_t>(sizeof(T))), kBufWord3);
   T* dKm = static_cast<T*>(ba.dKm) + rk;
   T* dKt = static_cast<T*>(ba.dKt) + rk;
-  const float* Gc = a.G + rk;   // in-chunk log-decay prefix rows [t][c]
+  // the per-channel log-decays g of the pass's channels: C / 8 segments of
+  // 8 rows, one thread per (channel, segment)
+  constexpr int NSG = C / 8;
+  const int gc = tid & (HC - 1), gsg = tid / HC;
+  const bool gseg = NSG == 8 || gsg < NSG;
+  const float* gin = a.g + ((b * a.T + t0) * a.H + h) * DK;   // row stride HD
 #pragma unroll 1
   for (int p = 0; p < NPASS; ++p) {
     const int c0 = p * HC;
     __syncthreads();   // phase A (or the previous pass) is done with the LDS
+    if (gseg) {
+      // raw g of the pass's channels, transposed (rows past the end: 0);
+      // the in-chunk prefix is rebuilt from it below rather than read back
+      float gr[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        gr[q] = *at_bytes(gin, static_cast<uint32_t>(min(8 * gsg + q, n - 1) * HD + c0 + gc) * 4u);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) sGT[gc * LDG + 8 * gsg + q] = 8 * gsg + q < n ? gr[q] : 0.f;
+    }
     srows.store(sS, sdS, tid);
     {
       // sum_v S dS' per channel of the pass, from the rows just stored: the
@@ -1142,17 +1157,24 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
       chan(srows.template dot<0>(), 0);
       if constexpr (SR::kPer == 2) chan(srows.template dot<1>(), 1);
     }
-    {
-      static_assert((C * (HC / 4)) % 256 == 0, "whole rounds of 256 threads");
+    // the in-chunk prefix G, in place: each segment is summed, then re-walked
+    // from the total of the segments before it
+    __syncthreads();
+    if (gseg) {
+      float x = 0.f;
 #pragma unroll
-      for (int jj = 0; jj < (C * (HC / 4)) / 256; ++jj) {
-        const int idx = tid + 256 * jj;
-        const int t = idx / (HC / 4), c4 = (idx % (HC / 4)) * 4;
-        const float4 gv = *reinterpret_cast<const float4*>(Gc + t * DK + c0 + c4);
-        sGT[(c4 + 0) * LDG + t] = gv.x;
-        sGT[(c4 + 1) * LDG + t] = gv.y;
-        sGT[(c4 + 2) * LDG + t] = gv.z;
-        sGT[(c4 + 3) * LDG + t] = gv.w;
+      for (int q = 0; q < 8; ++q) x += sGT[gc * LDG + 8 * gsg + q];
+      sSeg[gsg * HC + gc] = x;
+    }
+    __syncthreads();
+    if (gseg) {
+      float x = 0.f;
+      for (int q = 0; q < gsg; ++q) x += sSeg[q * HC + gc];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        float* gp = sGT + gc * LDG + 8 * gsg + q;
+        x += *gp;
+        *gp = x;
       }
     }
     if ((p & 1) == 0) {
@@ -1256,7 +1278,6 @@ __global__ __launch_bounds__(256, 2) void p12c_chunk_grads(BwdArgs ba) {
     {
       // dg_j = sum_{r >= j} dG_r + the last-row term, per channel: C / 8
       // segments of 8 rows, then the totals of the later segments
-      constexpr int NSG = C / 8;
       const int c = tid & (HC - 1), sg = tid / HC;
       const bool seg = NSG == 8 || sg < NSG;
       float x = 0.f;

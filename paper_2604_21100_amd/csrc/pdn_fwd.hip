@@ -306,18 +306,39 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       sWt[l] = fast_exp(xC - x);
     }
   }
-  if (tid < DK) {
-    const int c = tid;
-    if (GATE == kGateChannel) {
-      float acc = 0.f;
-      float* gout = a.G + (bh * a.Tpad + t0) * DK + c;
-      for (int r = 0; r < C; ++r) {
-        float* gp = k2swf(sGc, DK + 4, r, c);
-        acc += *gp;
-        *gp = acc;
-        gout[(int64_t)r * DK] = acc;
+  if (GATE == kGateChannel) {
+    // per-channel in-chunk prefix G of g (rows past the end hold g = 0) over
+    // 8-row segments: each segment is summed, then re-walked from the total
+    // of the segments before it (the backward rebuilds G from g with the
+    // same sums in the same order).  Only the chunk-end row leaves the
+    // kernel.
+    constexpr int NS8 = C / 8, NSG = 256 / DK, SPT = NS8 / NSG;
+    static_assert(NS8 % NSG == 0, "whole segments per thread");
+    const int c = tid % DK, sg = tid / DK;
+    float* sTot = sY;   // [NS8][DK] segment totals (sY is idle until the solve)
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) {
+      const int sgm = sg * SPT + u;
+      float x = 0.f;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) x += *k2swf(sGc, DK + 4, 8 * sgm + q, c);
+      sTot[sgm * DK + c] = x;
+    }
+    __syncthreads();
+    float x = 0.f;
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) {
+      const int sgm = sg * SPT + u;
+      x = 0.f;
+      for (int q = 0; q < sgm; ++q) x += sTot[q * DK + c];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        float* gp = k2swf(sGc, DK + 4, 8 * sgm + q, c);
+        x += *gp;
+        *gp = x;
       }
     }
+    if (sg == NSG - 1) a.G[(bh * a.NT + i) * DK + c] = x;   // row C - 1
   }
   if (has_gram(PREC)) {
     // the in-chunk prefix A_r = a_r A_{r-1} + bP_r k_r^2 in NSEG row segments:
@@ -449,32 +470,58 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     }
   }
   if (GATE == kGateChannel) {
-    // Lam o Q (the query the scan reads: q, or for ATQ the preconditioned
-    // query) and Lam o K rows for the scan, rounded to io as the scan would
-    // round them, so it needs neither the gate tile nor the exponentials
+    // Lam o Q and Lam o K (Lam_r = exp(G_r) per channel; Q the query the
+    // scan reads: q, or for ATQ the preconditioned query): the rows the
+    // scan reads, rounded to io as the scan would round them, and for the
+    // backward their transposes (Lam o Q)^T and -(Lam o K)^T, [dk][C].  A
+    // thread takes 8 rows x 4 channels, so each exponential serves all four
+    // outputs.
     T* ql = static_cast<T*>(a.QL) + (bh * a.Tpad + t0) * DK;
     T* kl = static_cast<T*>(a.KL) + (bh * a.Tpad + t0) * DK;
     const T* qg = static_cast<const T*>(a.q) + ((b * a.T + t0) * a.H + h) * DK;
-    static_assert((C * (DK / 8)) % 256 == 0, "whole rounds of 256 threads");
+    using V4 = typename Vec4<T>::type;
+    constexpr int RB = C / 8, NTILE = RB * (DK / 4);
 #pragma unroll
-    for (int jj = 0; jj < (C * (DK / 8)) / 256; ++jj) {
+    for (int jj = 0; jj < (NTILE + 255) / 256; ++jj) {
       const int idx = tid + 256 * jj;
-      const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
-      Frag8<T> fk = ld8(k2sw(sK, LDK, r, c0)), fq;
-      if (NOQ) {
-        fq = frag_zero<T>();
-        if (r < n) fq = ld8(qg + r * a.H * DK + c0);
-      } else {
-        fq = ld8(k2sw(sQ, LDK, r, c0));
-      }
+      if (NTILE % 256 != 0 && idx >= NTILE) break;
+      const int r0 = (idx % RB) * 8, c0 = (idx / RB) * 4;
+      V4 q4[8], k4[8];
+      float4 g4[8];
 #pragma unroll
       for (int s2 = 0; s2 < 8; ++s2) {
-        const float e = fast_exp(*k2swf(sGc, DK + 4, r, c0 + s2));
-        fq.set(s2, fq.get(s2) * e);
-        fk.set(s2, fk.get(s2) * e);
+        const int r = r0 + s2;
+        if (NOQ) q4[s2] = *reinterpret_cast<const V4*>(qg + static_cast<int64_t>(min(r, n - 1)) * a.H * DK + c0);
+        else q4[s2] = *reinterpret_cast<const V4*>(k2sw(sQ, LDK, r, c0));
+        k4[s2] = *reinterpret_cast<const V4*>(k2sw(sK, LDK, r, c0));
+        g4[s2] = *reinterpret_cast<const float4*>(k2swf(sGc, DK + 4, r, c0));
       }
-      st8(ql + r * DK + c0, fq);
-      st8(kl + r * DK + c0, fk);
+      Frag8<T> fq[4], fk[4];
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) {
+        const int r = r0 + s2;
+        const float gv[4] = {g4[s2].x, g4[s2].y, g4[s2].z, g4[s2].w};
+        float qo[4], ko[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float lam = fast_exp(gv[e]);
+          qo[e] = lam * ((NOQ && r >= n) ? 0.f : to_f(q4[s2][e]));
+          ko[e] = lam * to_f(k4[s2][e]);
+          fq[e].set(s2, qo[e]);
+          fk[e].set(s2, -ko[e]);
+        }
+        st4<T>(ql + r * DK + c0, qo[0], qo[1], qo[2], qo[3]);
+        st4<T>(kl + r * DK + c0, ko[0], ko[1], ko[2], ko[3]);
+      }
+      if (BWD) {
+        T* QlT = static_cast<T*>(a.QlT) + (bh * a.NT + i) * (int64_t)(DK * C);
+        T* KnT = static_cast<T*>(a.KnT) + (bh * a.NT + i) * (int64_t)(DK * C);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          st8(QlT + (c0 + e) * C + r0, fq[e]);
+          st8(KnT + (c0 + e) * C + r0, fk[e]);
+        }
+      }
     }
   }
 
@@ -494,31 +541,52 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         if (r >= n) fqr[kk] = frag_zero<T>();
       }
     }
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      if (j > w) break;
-      const int t = 16 * j + lr;  // B-operand column of this lane
+    if (GATE == kGateChannel) {
+      // the decay ratio e^{G_r - G_t} inside the contraction, split at a
+      // reference row (the row block's first): the A operands take
+      // e^{G_r - G_ref} (once per 32 channels, shared by every column
+      // block), the B operands e^{G_ref - G_t}
+      const int rref = 16 * w;
 #pragma unroll
       for (int kk = 0; kk < DK / 32; ++kk) {
         const int c0 = kk * 32 + 8 * lg;
         Frag8<T> fk = ld8(k2sw(sK, LDK, r, c0));
         Frag8<T> fq = NOQ ? fqr[kk] : ld8(k2sw(sQ, LDK, r, c0));
-        Frag8<T> fb = ld8(k2sw(sKt, LDK, t, c0));
-        if (GATE == kGateChannel) {
-          // reference point: first row of the row block keeps both factors
-          // bounded for a non-increasing prefix
-          const int rref = 16 * w;
+        float gref[8];
 #pragma unroll
-          for (int s = 0; s < 8; ++s) {
-            const float fa = fast_exp(*k2swf(sGc, DK + 4, r, c0 + s) - *k2swf(sGc, DK + 4, rref, c0 + s));
-            fk.set(s, fk.get(s) * fa);
-            fq.set(s, fq.get(s) * fa);
-            fb.set(s, fb.get(s) * fast_exp(*k2swf(sGc, DK + 4, rref, c0 + s) - *k2swf(sGc, DK + 4, t, c0 + s)));
-          }
+        for (int s = 0; s < 8; ++s) {
+          gref[s] = *k2swf(sGc, DK + 4, rref, c0 + s);
+          const float fa = fast_exp(*k2swf(sGc, DK + 4, r, c0 + s) - gref[s]);
+          fk.set(s, fk.get(s) * fa);
+          fq.set(s, fq.get(s) * fa);
         }
-        // linear attention (ATQ): no delta-rule interaction, At = 0, T = Diag(beta)
-        if (PREC != kATQ) mma(accA[j], fk, fb);
-        mma(accP[j], fq, fb);
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          if (j > w) break;
+          const int t = 16 * j + lr;  // B-operand column of this lane
+          Frag8<T> fb = ld8(k2sw(sKt, LDK, t, c0));
+#pragma unroll
+          for (int s = 0; s < 8; ++s)
+            fb.set(s, fb.get(s) * fast_exp(gref[s] - *k2swf(sGc, DK + 4, t, c0 + s)));
+          if (PREC != kATQ) mma(accA[j], fk, fb);
+          mma(accP[j], fq, fb);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        if (j > w) break;
+        const int t = 16 * j + lr;  // B-operand column of this lane
+#pragma unroll
+        for (int kk = 0; kk < DK / 32; ++kk) {
+          const int c0 = kk * 32 + 8 * lg;
+          const Frag8<T> fk = ld8(k2sw(sK, LDK, r, c0));
+          const Frag8<T> fq = NOQ ? fqr[kk] : ld8(k2sw(sQ, LDK, r, c0));
+          const Frag8<T> fb = ld8(k2sw(sKt, LDK, t, c0));
+          // linear attention (ATQ): no delta-rule interaction, At = 0, T = Diag(beta)
+          if (PREC != kATQ) mma(accA[j], fk, fb);
+          mma(accP[j], fq, fb);
+        }
       }
     }
   }
@@ -543,8 +611,9 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       }
     }
   }
-  if (BWD) {
-    // (Lam o Q)^T and -(Lam o K)^T per chunk, [dk][C]
+  if (BWD && GATE != kGateChannel) {
+    // (Lam o Q)^T and -(Lam o K)^T per chunk, [dk][C] (per-channel gate:
+    // written with the Lam o Q / Lam o K rows above)
     T* QlT = static_cast<T*>(a.QlT) + (bh * a.NT + i) * (int64_t)(DK * C);
     T* KnT = static_cast<T*>(a.KnT) + (bh * a.NT + i) * (int64_t)(DK * C);
     static_assert((DK * (C / 8)) % 256 == 0, "whole rounds of 256 threads");
@@ -556,13 +625,8 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
 #pragma unroll
       for (int s2 = 0; s2 < 8; ++s2) {
         const int r = r0 + s2;
-        float lam = 1.f;
-        if (GATE == kGateScalar) lam = sLam[r];
-        if (GATE == kGateChannel) lam = fast_exp(*k2swf(sGc, DK + 4, r, c));
-        float qv = 0.f;
-        if (!NOQ) qv = to_f(*k2sw(sQ, LDK, r, c));
-        else if (r < n) qv = to_f(static_cast<const T*>(a.q)[((b * a.T + t0 + r) * a.H + h) * DK + c]);
-        fq.set(s2, lam * qv);
+        const float lam = GATE == kGateScalar ? sLam[r] : 1.f;
+        fq.set(s2, lam * to_f(*k2sw(sQ, LDK, r, c)));
         fk.set(s2, -lam * to_f(*k2sw(sK, LDK, r, c)));
       }
       st8(QlT + c * C + r0, fq);
@@ -572,27 +636,53 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   // the write-key outputs (they need only sKt and the gate prefix), before
   // the solve
   if (BWD) {
-    // write-key rows, and for the per-channel gate the decayed rows
-    // w_r o Kt (with a scalar gate the reverse scan applies w_r itself)
+    // write-key rows (the per-channel gate's decayed rows w_r o Kt go out
+    // with the transposed decayed write keys below; with a scalar gate the
+    // reverse scan applies w_r itself)
     T* Kr = static_cast<T*>(a.Ktr) + (bh * a.Tpad + t0) * DK;
     static_assert((C * (DK / 8)) % 256 == 0, "whole rounds of 256 threads");
 #pragma unroll
     for (int jj = 0; jj < (C * (DK / 8)) / 256; ++jj) {
       const int idx = tid + 256 * jj;
       const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
-      const Frag8<T> fk = ld8(k2sw(sKt, LDK, r, c0));
-      st8(Kr + r * DK + c0, fk);
-      if (GATE == kGateChannel) {
-        Frag8<T> fw;
-#pragma unroll
-        for (int s2 = 0; s2 < 8; ++s2)
-          fw.set(s2, fast_exp(*k2swf(sGc, DK + 4, C - 1, c0 + s2) - *k2swf(sGc, DK + 4, r, c0 + s2)) * fk.get(s2));
-        st8(static_cast<T*>(a.Kw) + (bh * a.Tpad + t0 + r) * DK + c0, fw);
-      }
+      st8(Kr + r * DK + c0, ld8(k2sw(sKt, LDK, r, c0)));
     }
   }
   // ---- decayed write keys, transposed per chunk: (Kt * Lam_C / Lam_t)^T
-  {
+  if (GATE == kGateChannel) {
+    // w_t = exp(G_{C-1} - G_t) per channel, 8 rows x 4 channels a thread:
+    // each factor serves the transposed tile for the scan and, for the
+    // backward, the row-major w o Kt
+    T* Kout = static_cast<T*>(a.KtG) + (bh * a.NT + i) * (int64_t)(DK * C);
+    T* Kw = static_cast<T*>(a.Kw) + (bh * a.Tpad + t0) * DK;
+    using V4 = typename Vec4<T>::type;
+    constexpr int RB = C / 8, NTILE = RB * (DK / 4);
+#pragma unroll
+    for (int jj = 0; jj < (NTILE + 255) / 256; ++jj) {
+      const int idx = tid + 256 * jj;
+      if (NTILE % 256 != 0 && idx >= NTILE) break;
+      const int r0 = (idx % RB) * 8, c0 = (idx / RB) * 4;
+      const float4 ge = *reinterpret_cast<const float4*>(k2swf(sGc, DK + 4, C - 1, c0));
+      const float gend[4] = {ge.x, ge.y, ge.z, ge.w};
+      Frag8<T> f[4];
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) {
+        const int t = r0 + s2;
+        const V4 kt4 = *reinterpret_cast<const V4*>(k2sw(sKt, LDK, t, c0));
+        const float4 g4 = *reinterpret_cast<const float4*>(k2swf(sGc, DK + 4, t, c0));
+        const float gv[4] = {g4.x, g4.y, g4.z, g4.w};
+        float wv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          wv[e] = fast_exp(gend[e] - gv[e]) * to_f(kt4[e]);
+          f[e].set(s2, wv[e]);
+        }
+        if (BWD) st4<T>(Kw + t * DK + c0, wv[0], wv[1], wv[2], wv[3]);
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) st8(Kout + (c0 + e) * C + r0, f[e]);
+    }
+  } else {
     T* Kout = static_cast<T*>(a.KtG) + (bh * a.NT + i) * (int64_t)(DK * C);
     static_assert((DK * C / 8) % 256 == 0, "whole rounds of 256 threads");
 #pragma unroll
@@ -605,7 +695,6 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         const int t = tv + s;
         float val = to_f(*k2sw(sKt, LDK, t, c));
         if (GATE == kGateScalar) val *= sWt[t];
-        if (GATE == kGateChannel) val *= fast_exp(*k2swf(sGc, DK + 4, C - 1, c) - *k2swf(sGc, DK + 4, t, c));
         f.set(s, val);
       }
       st8(Kout + c * C + tv, f);
@@ -853,7 +942,7 @@ __device__ __forceinline__ void scan_load(ScanFrags<T, DK, GATE, C>& f, const Fw
     f.gC[0][0] = gs[C - 1];
   }
   if (GATE == kGateChannel) {
-    const float* ge = a.G + (x.bh * a.Tpad + t0 + C - 1) * DK;
+    const float* ge = a.G + (x.bh * a.NT + i) * DK;   // G at the chunk end
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
@@ -1185,7 +1274,7 @@ WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precon
   L.Tm = take(bh * nt * C * C * esz);
   L.Pm = take(bh * nt * C * C * esz);
   if (gate == kGateScalar) L.G = take(bh * nt * C * 4);
-  if (gate == kGateChannel) L.G = take(bh * nt * C * dk * 4);
+  if (gate == kGateChannel) L.G = take(bh * nt * dk * 4);   // chunk-end rows only
   if (precond == kATQ) L.Qt = take(bh * nt * C * dk * esz);
   if (gate == kGateChannel) {
     L.QL = take(bh * nt * C * dk * esz);

@@ -57,7 +57,8 @@ struct FwdArgs {
   void* KtG;      // [BH, NT, dk, C] (Kt * Gamma)^T per chunk, io dtype
   void* Tm;       // [BH, NT, C, C]  T = (I + At)^{-1} Diag(beta), io dtype
   void* Pm;       // [BH, NT, C, C]  causal (Q*Lam)(Kt/Lam)^T, io dtype
-  float* G;       // [BH, Tpad] or [BH, Tpad, dk] in-chunk log-decay prefix
+  float* G;       // scalar gate: [BH, Tpad] in-chunk log-decay prefix; per-channel
+                  // gate: [BH, NT, dk], its chunk-end row only
   void* Qt;       // [BH, Tpad, dk] io   ATQ: preconditioned query rows q / (A + ridge)
   void* QL;       // [BH, Tpad, dk] io   per-channel gate: Lam o (the query the scan reads)
   void* KL;       // [BH, Tpad, dk] io   per-channel gate: Lam o K
