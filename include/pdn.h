@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PDN_ABI_VERSION 4
+#define PDN_ABI_VERSION 5
 
 typedef enum {
   PDN_OK = 0,
@@ -184,6 +184,21 @@ typedef struct {
  * problem; *bytes is written only on PDN_OK. */
 pdn_status pdn_workspace_size(const pdn_problem* problem, int with_bwd,
                               size_t* bytes);
+
+/* Number of sequence segments the forward state scan of this problem runs
+ * in (1: one pass over the chunks).  A scan workgroup holds one head's
+ * 32-column state slab on one compute unit, so with few heads (B * H *
+ * dv / 32 far below the 256 compute units of MI355X) most of the chip
+ * would idle.  The chunks are then cut into S >= 3 segments: segment 0
+ * runs from S0 while every middle segment runs from zero and, with its
+ * values zeroed, from the identity (giving its d_k x d_k transition Phi,
+ * S_end^T = Phi S_start^T + local end, the chunkwise recurrence being
+ * affine in the state); the exact start of each segment is composed from
+ * those, and segments 1 .. S - 1 run again from it.  The result is the same
+ * recurrence up to fp32 rounding.  S depends only on the problem's sizes,
+ * as does the workspace (which holds the segment states).  Host-only, no
+ * HIP call; errors as pdn_workspace_size. */
+pdn_status pdn_scan_segments(const pdn_problem* problem, int* segments);
 
 /* Forward pass (Eq. chunkwise_atk_form with the preconditioner of Eq.
  * precond_end2end; decayed forms of App. D).  Writes o and, when non-NULL,

@@ -139,8 +139,11 @@ _lib.pdn_status_string.argtypes = [ctypes.c_int]
 _lib.pdn_status_string.restype = ctypes.c_char_p
 _lib.pdn_abi_version.argtypes = []
 _lib.pdn_abi_version.restype = ctypes.c_int
+_lib.pdn_scan_segments.argtypes = [ctypes.POINTER(Problem),
+                                   ctypes.POINTER(ctypes.c_int)]
+_lib.pdn_scan_segments.restype = ctypes.c_int
 
-ABI_VERSION = 4   # PDN_ABI_VERSION: the struct layouts mirrored above
+ABI_VERSION = 5   # PDN_ABI_VERSION: the struct layouts mirrored above
 if _lib.pdn_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} implements ABI version "
                       f"{_lib.pdn_abi_version()}, this binding mirrors "
@@ -150,7 +153,7 @@ EXPORTED = ("pdn_workspace_size", "pdn_chunk_fwd", "pdn_chunk_fwd_events",
             "pdn_chunk_bwd", "pdn_chunk_bwd_events", "pdn_chunk_fwd_train",
             "pdn_chunk_bwd_train", "pdn_chunk_fwd_noalloc",
             "pdn_noalloc_scratch_bytes", "pdn_status_string",
-            "pdn_abi_version")
+            "pdn_abi_version", "pdn_scan_segments")
 FWD_STAGE_EVENTS = 4   # PDN_FWD_STAGE_EVENTS
 BWD_STAGE_EVENTS = 7   # PDN_BWD_STAGE_EVENTS
 FWD_STAGES = ("precond", "chunk_prep", "chunk_scan")
@@ -190,6 +193,14 @@ def pdn_workspace_size(problem: Problem, with_bwd: bool = False) -> int:
                                  ctypes.byref(n))
     if st != PDN_OK:
         raise PdnError(st, "pdn_workspace_size")
+    return n.value
+
+
+def pdn_scan_segments(problem: Problem) -> int:
+    n = ctypes.c_int(0)
+    st = _lib.pdn_scan_segments(ctypes.byref(problem), ctypes.byref(n))
+    if st != PDN_OK:
+        raise PdnError(st, "pdn_scan_segments")
     return n.value
 
 

@@ -1775,7 +1775,7 @@ static size_t align256b(size_t x) { return (x + 255) & ~static_cast<size_t>(255)
 BwdWsLayout bwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond, int C) {
   const int PCS = C / PCG;
   BwdWsLayout L{};
-  L.f = fwd_ws_layout(BH, NT, dk, esz, gate, precond, C);
+  L.f = fwd_ws_layout(BH, NT, dk, dv, esz, gate, precond, C);
   size_t off = L.f.total;
   auto take = [&](size_t bytes) { const size_t o = off; off = align256b(off + bytes); return o; };
   const size_t bh = static_cast<size_t>(BH), nt = static_cast<size_t>(NT), tp = nt * C;

@@ -842,6 +842,8 @@ struct ScanFrags {
 struct ScanCtx {
   int64_t b, h, bh;
   int v0, w, lr, lg, tid;
+  int c0;        // first chunk of this workgroup's run
+  float vkeep;   // 1, or 0 for a transition workgroup (values zeroed)
 };
 
 // Each chunk's loads are a wave-uniform (scalar) base plus a 32-bit lane
@@ -1053,7 +1055,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE, C>& f, const fl
   }
   // the flushes' LDS reads go after this phase's operand reads (LDS reads
   // complete in issue order)
-  if (OUT && i > 0) flush_output<true, T, C>(a, i - 1, C, sO, x);   // only full chunks precede this one
+  if (OUT && i > x.c0) flush_output<true, T, C>(a, i - 1, C, sO, x);   // only full chunks precede this one
   if (SAVE)  // chunk-start state S^T of this chunk, rows c, columns of the slab
     flush_slab_t<DK>(static_cast<T*>(a.Hs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv, sH,
                      LDH, x.tid);
@@ -1075,7 +1077,7 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE, C>& f, const fl
     for (int vt = 0; vt < 2; ++vt) {
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
-        accX[vt][ii] = to_f(vv[vt][ii]) - lam[ii] * accX[vt][ii];
+        accX[vt][ii] = x.vkeep * to_f(vv[vt][ii]) - lam[ii] * accX[vt][ii];
         if (OUT) accO[vt][ii] *= lam[ii];
       }
       st4<T>(swv<C>(sX, LDE, 16 * vt + lr, 16 * w + 4 * lg), accX[vt][0], accX[vt][1], accX[vt][2],
@@ -1167,13 +1169,35 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   __shared__ __attribute__((aligned(16))) T sVt[BV * LDE];  // this chunk's values, [v][t]
   __shared__ __attribute__((aligned(16))) T sO[BV * LDE];   // last chunk's output, [v][t]
 
-  const int nslab = a.dv / BV;
+  // workgroup -> (head, role, slab); the slabs of one head share an XCD
+  // (and its L2).  Roles per head: phase 0, the value slabs of the whole
+  // sequence; phase 1, segment 0's value slabs, then per middle segment its
+  // value slabs (local, from zero) and d_k / BV transition slabs; phase 3,
+  // the value slabs of segments 1 .. S - 1.
+  const int nslab = a.dv / BV, npslab = DK / BV;
+  const int S = a.seg_cnt;
+  const int nrole = a.seg_phase == 0 ? nslab
+                  : a.seg_phase == 1 ? nslab + (S - 2) * (nslab + npslab)
+                                     : (S - 1) * nslab;
   const int64_t bid = blockIdx.x;
   const int xcd = static_cast<int>(bid & 7);
   const int64_t j8 = bid >> 3;
-  const int slab = static_cast<int>(j8 % nslab);
-  const int64_t bh = (j8 / nslab) * 8 + xcd;  // slabs of one head share an XCD (and its L2)
+  const int role = static_cast<int>(j8 % nrole);
+  const int64_t bh = (j8 / nrole) * 8 + xcd;
   if (bh >= a.BH) return;
+  int seg = 0, slab = role;
+  bool probe = false;
+  if (a.seg_phase == 1 && role >= nslab) {
+    const int r = role - nslab;
+    seg = 1 + r / (nslab + npslab);
+    slab = r % (nslab + npslab);
+    probe = slab >= nslab;
+  } else if (a.seg_phase == 3) {
+    seg = 1 + role / nslab;
+    slab = role % nslab;
+  }
+  const int c0 = a.seg_phase == 0 ? 0 : seg * a.seg_len;
+  const int c1 = a.seg_phase == 0 ? a.NT : min(a.NT, c0 + a.seg_len);
   ScanCtx x;
   x.bh = bh;
   x.b = bh / a.H;
@@ -1182,9 +1206,15 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   x.w = x.tid >> 6;
   x.lr = x.tid & 15;
   x.lg = (x.tid & 63) >> 4;
-  x.v0 = slab * BV;
+  // a transition slab reads (and zeroes) value slab 0; its own columns are
+  // pv0 .. pv0 + BV of the d_k x d_k transition
+  x.v0 = probe ? 0 : slab * BV;
+  x.c0 = c0;
+  x.vkeep = probe ? 0.f : 1.f;
+  const int pv0 = probe ? (slab - nslab) * BV : 0;
   const int w = x.w, lr = x.lr, lg = x.lg;
   const int DV = a.dv;
+  const int64_t BHDK = a.BH * static_cast<int64_t>(DK);
 
   // state slab: rows c = 16*(w*CT+ct) + 4*lg + ii, column v0 + 16*vt + lr
   floatx4 st[CT][2];
@@ -1194,8 +1224,15 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
     for (int vt = 0; vt < 2; ++vt)
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
-        const int c = 16 * (w * CT + ct) + 4 * lg + ii;
-        st[ct][vt][ii] = a.S0 ? a.S0[(bh * DK + c) * DV + x.v0 + 16 * vt + lr] : 0.f;
+        const int c = 16 * (w * CT + ct) + 4 * lg + ii, v = 16 * vt + lr;
+        float s0 = 0.f;   // middle segments' local runs start from zero
+        if (a.seg_phase == 0 || (a.seg_phase == 1 && seg == 0))
+          s0 = a.S0 ? a.S0[(bh * DK + c) * DV + x.v0 + v] : 0.f;
+        else if (a.seg_phase == 3)
+          s0 = a.seg_start[(seg * BHDK + bh * DK + c) * DV + x.v0 + v];
+        else if (probe)
+          s0 = c == pv0 + v ? 1.f : 0.f;
+        st[ct][vt][ii] = s0;
       }
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
@@ -1205,19 +1242,19 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
              st[ct][vt][1], st[ct][vt][2], st[ct][vt][3]);
 
   // software pipeline, three deep: chunk i+2's operands load while chunk i
-  // computes.  The loop covers the full chunks, three per trip, with no exit
-  // in the middle and unconditional prefetches (past the end they re-read
-  // the last chunk), so every path into the loop header has the same loads
-  // in flight and the compiler's wait counts stay exact.  A ragged last chunk
-  // runs after it.
+  // computes.  The loop covers the run's full chunks, three per trip, with
+  // no exit in the middle and unconditional prefetches (past the end they
+  // re-read the last chunk), so every path into the loop header has the same
+  // loads in flight and the compiler's wait counts stay exact.  A ragged last
+  // chunk (only the sequence's last) runs after it.
   ScanFrags<T, DK, GATE, C> f0, f1, f2;
-  const int last = a.NT - 1;
-  const int NF = static_cast<int>(a.T / C);   // full chunks
-  scan_load<7, OUT, LA>(f0, a, 0, x);
-  scan_load<7, OUT, LA>(f1, a, min(1, last), x);
+  const int last = c1 - 1;
+  const int NF = min(c1, static_cast<int>(a.T / C));   // end of the run's full chunks
+  scan_load<7, OUT, LA>(f0, a, c0, x);
+  scan_load<7, OUT, LA>(f1, a, min(c0 + 1, last), x);
   stage_values<T, C>(f0.v, sVt, x.tid);
   __syncthreads();
-  int i = 0;
+  int i = c0;
   for (; i + 2 < NF; i += 3) {
     scan_step<true, SAVE, OUT, LA, true>(f0, f1.v, f2, i + 2, st, a, i, x, sH, sX, sE, sVt, sO);
     scan_step<true, SAVE, OUT, LA, true>(f1, f2.v, f0, min(i + 3, last), st, a, i + 1, x, sH, sX, sE, sVt, sO);
@@ -1228,16 +1265,32 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
     scan_step<true, SAVE, OUT, LA, true>(f0, f1.v, f2, min(i + 2, last), st, a, i, x, sH, sX, sE, sVt, sO);
     scan_step<true, SAVE, OUT, LA, false>(f1, f2.v, f0, 0, st, a, i + 1, x, sH, sX, sE, sVt, sO);
     i += 2;
-    if (i < a.NT) scan_step<false, SAVE, OUT, LA, false>(f2, nullptr, f0, 0, st, a, i, x, sH, sX, sE, sVt, sO);
+    if (i < c1) scan_step<false, SAVE, OUT, LA, false>(f2, nullptr, f0, 0, st, a, i, x, sH, sX, sE, sVt, sO);
   } else if (NF - i == 1) {
     scan_step<true, SAVE, OUT, LA, false>(f0, f1.v, f2, 0, st, a, i, x, sH, sX, sE, sVt, sO);
     i += 1;
-    if (i < a.NT) scan_step<false, SAVE, OUT, LA, false>(f1, nullptr, f2, 0, st, a, i, x, sH, sX, sE, sVt, sO);
-  } else if (i < a.NT) {
+    if (i < c1) scan_step<false, SAVE, OUT, LA, false>(f1, nullptr, f2, 0, st, a, i, x, sH, sX, sE, sVt, sO);
+  } else if (i < c1) {
     scan_step<false, SAVE, OUT, LA, false>(f0, nullptr, f1, 0, st, a, i, x, sH, sX, sE, sVt, sO);
   }
-  if (OUT) flush_output<false, T, C>(a, last, static_cast<int>(a.T - static_cast<int64_t>(last) * C), sO, x);
-  if (a.S_T) {
+  if (OUT) flush_output<false, T, C>(a, last, static_cast<int>(min<int64_t>(C, a.T - static_cast<int64_t>(last) * C)), sO, x);
+  // the end state: S_T after the sequence's last chunk; phase 1: segment
+  // 0's exact end, a middle segment's local end or its transition
+  float* dst = nullptr;
+  int64_t ld = DV;
+  int col0 = x.v0;
+  if (a.seg_phase == 1) {
+    if (probe) {
+      dst = a.seg_phi + (seg * BHDK + bh * DK) * DK;
+      ld = DK;
+      col0 = pv0;
+    } else {
+      dst = a.seg_end + (seg * BHDK + bh * DK) * DV;
+    }
+  } else if (c1 == a.NT && a.S_T) {
+    dst = a.S_T + bh * DK * DV;
+  }
+  if (dst) {
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
@@ -1245,8 +1298,49 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) {
           const int c = 16 * (w * CT + ct) + 4 * lg + ii;
-          a.S_T[(bh * DK + c) * DV + x.v0 + 16 * vt + lr] = st[ct][vt][ii];
+          dst[c * ld + col0 + 16 * vt + lr] = st[ct][vt][ii];
         }
+  }
+}
+
+// S^T_start of segment s + 1 = Phi_s S^T_start of segment s + local end of
+// segment s, from segment 1 (whose start is segment 0's exact end) up; one
+// workgroup per head, fp32.  Thread t owns column t % DV and DK / (256 / DV)
+// consecutive rows.
+template <int DK, int DV>
+__global__ __launch_bounds__(256) void k3_seg_compose(FwdArgs a) {
+  constexpr int G = 256 / DV, R = DK / G;
+  __shared__ float sS[DK * DV];
+  __shared__ float sP[DK * DK];
+  const int64_t bh = blockIdx.x;
+  const int tid = threadIdx.x, v = tid % DV, r0 = (tid / DV) * R;
+  const int64_t BHDK = a.BH * static_cast<int64_t>(DK);
+  const float* e0 = a.seg_end + bh * DK * DV;   // segment 0's end
+  float* s1 = a.seg_start + (BHDK + bh * DK) * DV;
+  float acc[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    acc[r] = e0[(r0 + r) * DV + v];
+    s1[(r0 + r) * DV + v] = acc[r];
+  }
+  for (int sg = 1; sg + 1 < a.seg_cnt; ++sg) {
+    __syncthreads();   // the previous products are done with the LDS
+#pragma unroll
+    for (int r = 0; r < R; ++r) sS[(r0 + r) * DV + v] = acc[r];
+    const float* phi = a.seg_phi + (sg * BHDK + bh * DK) * DK;
+    for (int j = tid; j < DK * DK; j += 256) sP[j] = phi[j];
+    const float* loc = a.seg_end + (sg * BHDK + bh * DK) * DV;
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = loc[(r0 + r) * DV + v];
+    __syncthreads();
+    for (int p = 0; p < DK; ++p) {
+      const float hv = sS[p * DV + v];
+#pragma unroll
+      for (int r = 0; r < R; ++r) acc[r] = fmaf(sP[(r0 + r) * DK + p], hv, acc[r]);
+    }
+    float* sn = a.seg_start + ((sg + 1) * BHDK + bh * DK) * DV;
+#pragma unroll
+    for (int r = 0; r < R; ++r) sn[(r0 + r) * DV + v] = acc[r];
   }
 }
 
@@ -1260,7 +1354,7 @@ __global__ void k0_copy_states(FwdArgs a, int64_t nS, int64_t nA) {
 // ---------------------------------------------------------------- host side
 static size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
-WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precond, int C) {
+WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond, int C) {
   WsLayout L{};
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t o = off; off = align256(off + bytes); return o; };
@@ -1279,6 +1373,13 @@ WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precon
   if (gate == kGateChannel) {
     L.QL = take(bh * nt * C * dk * esz);
     L.KL = take(bh * nt * C * dk * esz);
+  }
+  L.split = scan_split(BH, NT, dk, dv);
+  if (L.split.S > 1) {
+    const size_t S = static_cast<size_t>(L.split.S);
+    L.seg_end = take(S * bh * dk * dv * 4);
+    L.seg_phi = take(S * bh * dk * dk * 4);
+    L.seg_start = take(S * bh * dk * dv * 4);
   }
   L.total = off;
   return L;
@@ -1304,6 +1405,36 @@ static hipError_t launch_k2_prec(const FwdArgs& a, hipStream_t s) {
   }
 }
 
+// The state scan: one pass over the chunks, or with a sequence split
+// (scan_split) the three passes: segment 0 next to the middle segments'
+// local scans and transitions, the composition of the segment starts, and
+// segments 1 .. S - 1 from their exact starts.  The first pass's middle
+// segments also write outputs and saved rows for their chunks from the
+// wrong start; the third pass overwrites every one of them.
+template <typename T, int DK, int GATE, bool SAVE, bool OUT, bool LA, int C>
+static hipError_t launch_k3(const FwdArgs& a0, hipStream_t s) {
+  FwdArgs a = a0;
+  const int nslab = a.dv / BV, npslab = DK / BV;
+  auto grid = [&](int nrole) { return dim3(static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nrole)); };
+  if (a.seg_cnt < 3) {
+    a.seg_phase = 0;
+    hipLaunchKernelGGL((k3_chunk_scan<T, DK, GATE, SAVE, OUT, LA, C>), grid(nslab), dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
+  const int S = a.seg_cnt;
+  a.seg_phase = 1;
+  hipLaunchKernelGGL((k3_chunk_scan<T, DK, GATE, SAVE, OUT, LA, C>), grid(nslab + (S - 2) * (nslab + npslab)),
+                     dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (a.dv == 64) hipLaunchKernelGGL((k3_seg_compose<DK, 64>), dim3(static_cast<unsigned>(a.BH)), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((k3_seg_compose<DK, 128>), dim3(static_cast<unsigned>(a.BH)), dim3(256), 0, s, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  a.seg_phase = 3;
+  hipLaunchKernelGGL((k3_chunk_scan<T, DK, GATE, SAVE, OUT, LA, C>), grid((S - 1) * nslab), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 // SAVE: the training forward (k2 in backward mode, k3 also saving the
 // chunk states and E rows)
 template <typename T, int DK, bool SAVE, int C>
@@ -1326,35 +1457,33 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
   }
   if (e != hipSuccess) return e;
   if ((e = mark(2)) != hipSuccess) return e;
-  const int64_t nslab = a.dv / BV;
-  const unsigned grid = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
   if constexpr (!SAVE) {
     if (a.precond == kATQ) {   // linear attention with the preconditioned query
       switch (a.gate) {
         case kGateNone:
-          hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, false, true, true, C>), dim3(grid), dim3(256), 0, s, a);
+          e = launch_k3<T, DK, kGateNone, false, true, true, C>(a, s);
           break;
         case kGateScalar:
-          hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, false, true, true, C>), dim3(grid), dim3(256), 0, s, a);
+          e = launch_k3<T, DK, kGateScalar, false, true, true, C>(a, s);
           break;
         default:
-          hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, false, true, true, C>), dim3(grid), dim3(256), 0, s, a);
+          e = launch_k3<T, DK, kGateChannel, false, true, true, C>(a, s);
           break;
       }
-      if ((e = hipGetLastError()) != hipSuccess) return e;
+      if (e != hipSuccess) return e;
       return mark(3);
     }
   }
   switch (a.gate) {
     case kGateNone:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, SAVE, true, false, C>), dim3(grid), dim3(256), 0, s, a); break;
+      e = launch_k3<T, DK, kGateNone, SAVE, true, false, C>(a, s); break;
     case kGateScalar:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, SAVE, true, false, C>), dim3(grid), dim3(256), 0, s, a); break;
+      e = launch_k3<T, DK, kGateScalar, SAVE, true, false, C>(a, s); break;
     default:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, SAVE, true, false, C>), dim3(grid), dim3(256), 0, s, a);
+      e = launch_k3<T, DK, kGateChannel, SAVE, true, false, C>(a, s);
       break;
   }
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (e != hipSuccess) return e;
   return mark(3);
 }
 
@@ -1380,17 +1509,15 @@ static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s, hipEvent_t c
   }
   if (e != hipSuccess) return e;
   if ((e = mark(2)) != hipSuccess) return e;
-  const int64_t nslab = a.dv / BV;
-  const unsigned grid = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
   switch (a.gate) {
     case kGateNone:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateNone, true, false, false, C>), dim3(grid), dim3(256), 0, s, a); break;
+      e = launch_k3<T, DK, kGateNone, true, false, false, C>(a, s); break;
     case kGateScalar:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateScalar, true, false, false, C>), dim3(grid), dim3(256), 0, s, a); break;
+      e = launch_k3<T, DK, kGateScalar, true, false, false, C>(a, s); break;
     default:
-      hipLaunchKernelGGL((k3_chunk_scan<T, DK, kGateChannel, true, false, false, C>), dim3(grid), dim3(256), 0, s, a); break;
+      e = launch_k3<T, DK, kGateChannel, true, false, false, C>(a, s); break;
   }
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (e != hipSuccess) return e;
   return mark(3);
 }
 

@@ -188,9 +188,18 @@ pdn_status pdn_workspace_size(const pdn_problem* p, int with_bwd, size_t* bytes)
     *bytes = pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond, p->chunk).total;
     return PDN_OK;
   }
-  const pdn::WsLayout L = pdn::fwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, s.esz, p->gate,
+  const pdn::WsLayout L = pdn::fwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate,
                                              p->precond, p->chunk);
   *bytes = L.total;
+  return PDN_OK;
+}
+
+pdn_status pdn_scan_segments(const pdn_problem* p, int* segments) {
+  if (!segments) return PDN_ERR_NULL;
+  Sizes s;
+  const pdn_status st = check_problem(p, &s);
+  if (st != PDN_OK) return st;
+  *segments = s.tok > 0 ? pdn::scan_split(s.BH, static_cast<int>(s.NT), p->dk, p->dv).S : 1;
   return PDN_OK;
 }
 
@@ -211,6 +220,13 @@ static void set_forward_ws(pdn::FwdArgs& a, const pdn::WsLayout& L, const pdn_pr
   a.Tm = w + L.Tm;
   a.Pm = w + L.Pm;
   if (p->gate != PDN_GATE_NONE) a.G = reinterpret_cast<float*>(w + L.G);
+  if (L.split.S > 1) {
+    a.seg_cnt = L.split.S;
+    a.seg_len = L.split.L;
+    a.seg_end = reinterpret_cast<float*>(w + L.seg_end);
+    a.seg_phi = reinterpret_cast<float*>(w + L.seg_phi);
+    a.seg_start = reinterpret_cast<float*>(w + L.seg_start);
+  }
 }
 
 static void set_residuals(pdn::FwdArgs& f, const pdn::BwdWsLayout& L, char* w) {
@@ -237,7 +253,7 @@ static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn
   const std::vector<Buf> outs = {{out->o, s.nv * s.esz}, {out->S_T, s.nS * 4}, {out->A_T, s.nA * 4}};
   for (const Buf& x : outs)
     if (x.p && !aligned16(x.p)) return PDN_ERR_ALIGN;
-  const pdn::WsLayout L = pdn::fwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, s.esz, p->gate,
+  const pdn::WsLayout L = pdn::fwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate,
                                              p->precond, p->chunk);
   const pdn::BwdWsLayout LB =
       pdn::bwd_ws_layout(s.BH, static_cast<int>(s.NT), p->dk, p->dv, s.esz, p->gate, p->precond, p->chunk);

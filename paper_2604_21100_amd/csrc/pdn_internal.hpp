@@ -72,7 +72,46 @@ struct FwdArgs {
   void* Kw;       // [BH, Tpad, dk] io    w_r o write key rows (per-channel gate; else NULL)
   void* QlT;      // [BH, NT, dk, C] io   (Diag(lam) Q)^T per chunk
   void* KnT;      // [BH, NT, dk, C] io   -(Diag(lam) K)^T per chunk
+  // sequence split of the state scan (see scan_split): seg_phase 0 = one
+  // pass over all chunks from S0; 1 = segment 0 from S0 next to the local
+  // scans (from zero) and transitions (from the identity, no values) of the
+  // middle segments; 3 = segments 1 .. seg_cnt - 1 from seg_start
+  int seg_phase, seg_len, seg_cnt;
+  float* seg_end;    // [S, BH, dk, dv] phase-1 end states (segment 0: exact; others: local)
+  float* seg_phi;    // [S, BH, dk, dk] segment transitions, S_end^T = Phi S_start^T + local
+  float* seg_start;  // [S, BH, dk, dv] exact start states of segments 1 .. S - 1
 };
+
+// Sequence split of the state scan.  A scan workgroup holds one head's
+// 32-column state slab (one per compute unit); with few heads most of the
+// chip idles through the sequential chunk loop.  The chunks are then cut
+// into S segments of L: segment 0 runs from S0 while each middle segment
+// runs from zero (its local end state) and, on d_k / 32 more workgroups,
+// from the identity with the values zeroed (its d_k x d_k transition); a
+// short sequential pass composes the exact start of every segment, and
+// segments 1 .. S - 1 run again from it.  The critical path drops from NT
+// steps to about 2 NT / S; S is the largest count whose first pass still
+// fits one workgroup per compute unit of the target device, with at least
+// kSegMinChunks chunks per segment.
+constexpr int kScanCUs = 256;       // compute units of MI355X
+constexpr int kSegMinChunks = 4;
+constexpr int kSegMax = 16;
+struct ScanSplit {
+  int S, L;   // segments (1: no split) and chunks per segment
+};
+inline ScanSplit scan_split(int64_t BH, int NT, int dk, int dv) {
+  const int64_t ns = dv / 32, np = dk / 32;
+  ScanSplit r{1, NT};
+  for (int s = 3; s <= kSegMax; ++s) {
+    if (BH * (ns + (s - 2) * (ns + np)) > kScanCUs) break;
+    const int L = (NT + s - 1) / s;
+    if (L < kSegMinChunks) break;
+    r.S = (NT + L - 1) / L;
+    r.L = L;
+  }
+  if (r.S < 3) r = ScanSplit{1, NT};
+  return r;
+}
 
 // Backward-only arguments and workspace (the forward recompute uses f).
 struct BwdArgs {
@@ -104,10 +143,11 @@ struct BwdArgs {
 };
 
 struct WsLayout {
-  size_t sumL, sumD, Abound, KtG, Tm, Pm, G, Qt, QL, KL, total;
+  size_t sumL, sumD, Abound, KtG, Tm, Pm, G, Qt, QL, KL, seg_end, seg_phi, seg_start, total;
+  ScanSplit split;
 };
 
-WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int esz, int gate, int precond, int C);
+WsLayout fwd_ws_layout(int64_t BH, int NT, int dk, int dv, int esz, int gate, int precond, int C);
 
 struct BwdWsLayout {
   WsLayout f;

@@ -317,7 +317,7 @@ def test_noalloc_rejects_problems_beyond_its_scratch():
                                                        gate="scalar"))
             <= pdn.pdn_noalloc_scratch_bytes()]
     tmax = max(fits)
-    assert tmax >= 8192
+    assert tmax >= 7680   # (the sequence split's segment states included)
     over = pdn.make_problem(1, tmax + 64, 14, 128, 128, gate="scalar")
     assert _fwd_noalloc(over) == pdn.PDN_ERR_SCRATCH
 
@@ -351,3 +351,28 @@ def test_chunk_sizes():
                                           None, None, None, None, None, None),
                                A * 64, 1, 0)
     assert st == pdn.PDN_ERR_WORKSPACE
+
+
+def test_scan_segments():
+    """The forward scan splits the sequence only when the heads' slabs leave
+    most of the 256 compute units idle and segments of ceil(NT / S) >= 4
+    chunks remain: the 32K-token 16-head layer runs in 3 segments, the 1B layer
+    (64 heads of B x H) in one pass; a single head over 33 chunks takes 9
+    segments of 4 (plus one chunk)."""
+    mp = pdn.make_problem
+    assert pdn.pdn_scan_segments(mp(1, 32768, 16, 128, 128)) == 3
+    assert pdn.pdn_scan_segments(mp(4, 4096, 16, 128, 128)) == 1
+    assert pdn.pdn_scan_segments(mp(2, 8192, 16, 128, 128)) == 1
+    assert pdn.pdn_scan_segments(mp(1, 2112, 1, 128, 128)) == 9
+    assert pdn.pdn_scan_segments(mp(1, 700, 2, 64, 64)) == 3
+    assert pdn.pdn_scan_segments(mp(1, 704, 2, 64, 64)) == 3
+    assert pdn.pdn_scan_segments(mp(1, 640, 2, 64, 64)) == 3   # 10 chunks: 4 + 4 + 2
+    assert pdn.pdn_scan_segments(mp(1, 512, 2, 64, 64)) == 1   # 8 chunks: 3 per segment
+    assert pdn.pdn_scan_segments(mp(0, 640, 2, 64, 64)) == 1
+    # more segments never cost more workspace than their states
+    a = pdn.pdn_workspace_size(mp(1, 32768, 16, 128, 128))
+    b = pdn.pdn_workspace_size(mp(1, 32768, 16, 128, 128, chunk=32))
+    assert a > 0 and b > 0
+    with pytest.raises(pdn.PdnError) as e:
+        pdn.pdn_scan_segments(mp(1, 64, 2, 96, 64))
+    assert e.value.status == pdn.PDN_ERR_UNSUPPORTED
