@@ -110,6 +110,7 @@ struct RevFrags {
 struct RevCtx {
   int64_t b, h, bh;
   int v0, w, lr, lg, tid;
+  float dscale;   // scale, or 0 for a transition workgroup (dO zeroed)
 };
 
 // dO slab of chunk i (rows past the sequence end re-read its last row; the
@@ -300,7 +301,7 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE, C>& f, bool stage
       st4<T>(sw(sH, LDH, 16 * vt + lr, 16 * (w * CT + ct) + 4 * lg), st[ct][vt][0], st[ct][vt][1],
              st[ct][vt][2], st[ct][vt][3]);
     }
-  if (stage_next) rev_stage_dO<T, C>(f.dO, sDOn, C, a.scale, x.tid);  // earlier chunks are full
+  if (stage_next) rev_stage_dO<T, C>(f.dO, sDOn, C, x.dscale, x.tid);  // earlier chunks are full
   lds_barrier_b();
 }
 
@@ -314,13 +315,34 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
   __shared__ __attribute__((aligned(16))) T sX[BVB * LDE];
   __shared__ __attribute__((aligned(16))) T sZ[BVB * LDE];
   const FwdArgs& a = ba.f;
-  const int nslab = a.dv / BVB;
+  // workgroup -> (head, role, slab) as in the forward scan, mirrored: phase
+  // 1 runs the last segment from dS_T beside the middle segments' local
+  // runs (from zero) and transitions (from the identity, dO zeroed); phase
+  // 3 runs segments 0 .. S - 2 from their composed starts
+  const int nslab = a.dv / BVB, npslab = DK / BVB;
+  const int S = a.seg_cnt;
+  const int nrole = a.seg_phase == 0 ? nslab
+                  : a.seg_phase == 1 ? nslab + (S - 2) * (nslab + npslab)
+                                     : (S - 1) * nslab;
   const int64_t bid = blockIdx.x;
   const int xcd = static_cast<int>(bid & 7);
   const int64_t j8 = bid >> 3;
-  const int slab = static_cast<int>(j8 % nslab);
-  const int64_t bh = (j8 / nslab) * 8 + xcd;
+  const int role = static_cast<int>(j8 % nrole);
+  const int64_t bh = (j8 / nrole) * 8 + xcd;
   if (bh >= a.BH) return;
+  int seg = S - 1, slab = role;
+  bool probe = false;
+  if (a.seg_phase == 1 && role >= nslab) {
+    const int r = role - nslab;
+    seg = 1 + r / (nslab + npslab);
+    slab = r % (nslab + npslab);
+    probe = slab >= nslab;
+  } else if (a.seg_phase == 3) {
+    seg = role / nslab;
+    slab = role % nslab;
+  }
+  const int c0 = a.seg_phase == 0 ? 0 : seg * a.seg_len;
+  const int c1 = a.seg_phase == 0 ? a.NT : min(a.NT, c0 + a.seg_len);
   RevCtx x;
   x.bh = bh;
   x.b = bh / a.H;
@@ -329,9 +351,12 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
   x.w = x.tid >> 6;
   x.lr = x.tid & 15;
   x.lg = (x.tid & 63) >> 4;
-  x.v0 = slab * BVB;
+  x.v0 = probe ? 0 : slab * BVB;
+  x.dscale = probe ? 0.f : a.scale;
+  const int pv0 = probe ? (slab - nslab) * BVB : 0;
   const int w = x.w, lr = x.lr, lg = x.lg;
   const int DV = a.dv;
+  const int64_t BHDK = a.BH * static_cast<int64_t>(DK);
   floatx4 st[CT][2];
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
@@ -339,8 +364,15 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
     for (int vt = 0; vt < 2; ++vt)
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
-        const int c = 16 * (w * CT + ct) + 4 * lg + ii;
-        st[ct][vt][ii] = ba.dS_T ? ba.dS_T[(bh * DK + c) * DV + x.v0 + 16 * vt + lr] : 0.f;
+        const int c = 16 * (w * CT + ct) + 4 * lg + ii, v = 16 * vt + lr;
+        float s0 = 0.f;   // middle segments' local runs start from zero
+        if (a.seg_phase == 0 || (a.seg_phase == 1 && seg == S - 1))
+          s0 = ba.dS_T ? ba.dS_T[(bh * DK + c) * DV + x.v0 + v] : 0.f;
+        else if (a.seg_phase == 3)
+          s0 = a.seg_start[(seg * BHDK + bh * DK + c) * DV + x.v0 + v];
+        else if (probe)
+          s0 = c == pv0 + v ? 1.f : 0.f;
+        st[ct][vt][ii] = s0;
       }
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
@@ -348,28 +380,46 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
     for (int vt = 0; vt < 2; ++vt)
       st4<T>(sw(sH, LDH, 16 * vt + lr, 16 * (w * CT + ct) + 4 * lg), st[ct][vt][0], st[ct][vt][1],
              st[ct][vt][2], st[ct][vt][3]);
-  // reverse order: the (possibly ragged) last chunk first, then the full
-  // chunks two per trip with a branch-free body; dO slabs double-buffered
-  const int NT = a.NT;
+  // reverse order over the run [c0, c1): its top chunk first (the ragged
+  // last chunk of the sequence, if the run ends there), then full chunks two
+  // per trip with a branch-free body; dO slabs double-buffered
+  const int top = c1 - 1;
   RevFrags<T, DK, GATE, C> fA, fB;
   float4 dlast[Slab<T, C>::kPer];
-  rev_load_dO<T, C>(dlast, ba, NT - 1, x);
-  rev_load<T, DK, GATE, C>(fA, ba, NT - 1, x);
-  rev_load<T, DK, GATE, C>(fB, ba, max(NT - 2, 0), x);
-  rev_stage_dO<T, C>(dlast, sDO[0], static_cast<int>(a.T - static_cast<int64_t>(NT - 1) * C), a.scale, x.tid);
+  rev_load_dO<T, C>(dlast, ba, top, x);
+  rev_load<T, DK, GATE, C>(fA, ba, top, x);
+  rev_load<T, DK, GATE, C>(fB, ba, max(top - 1, c0), x);
+  rev_stage_dO<T, C>(dlast, sDO[0], static_cast<int>(min<int64_t>(C, a.T - static_cast<int64_t>(top) * C)),
+                     x.dscale, x.tid);
   __syncthreads();
-  rev_step<false, T, DK, GATE, C>(fA, NT > 1, st, ba, NT - 1, x, sH, sDO[0], sDO[1], sE, sX, sZ);
-  int i = NT - 2, buf = 1;
-  for (; i >= 1; i -= 2) {
+  rev_step<false, T, DK, GATE, C>(fA, top > c0, st, ba, top, x, sH, sDO[0], sDO[1], sE, sX, sZ);
+  int i = top - 1, buf = 1;
+  for (; i >= c0 + 1; i -= 2) {
     rev_load<T, DK, GATE, C>(fA, ba, i - 1, x);
     rev_step<true, T, DK, GATE, C>(fB, true, st, ba, i, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
     buf ^= 1;
-    rev_load<T, DK, GATE, C>(fB, ba, max(i - 2, 0), x);
+    rev_load<T, DK, GATE, C>(fB, ba, max(i - 2, c0), x);
     rev_step<true, T, DK, GATE, C>(fA, true, st, ba, i - 1, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
     buf ^= 1;
   }
-  if (i == 0) rev_step<true, T, DK, GATE, C>(fB, false, st, ba, 0, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
-  if (ba.dS0) {
+  if (i == c0) rev_step<true, T, DK, GATE, C>(fB, false, st, ba, c0, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
+  // the end state: dS0 after chunk 0; phase 1: the last segment's exact
+  // end, a middle segment's local end or its transition
+  float* dst = nullptr;
+  int64_t ld = DV;
+  int col0 = x.v0;
+  if (a.seg_phase == 1) {
+    if (probe) {
+      dst = a.seg_phi + (seg * BHDK + bh * DK) * DK;
+      ld = DK;
+      col0 = pv0;
+    } else {
+      dst = a.seg_end + (seg * BHDK + bh * DK) * DV;
+    }
+  } else if (c0 == 0 && ba.dS0) {
+    dst = ba.dS0 + bh * DK * DV;
+  }
+  if (dst) {
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
@@ -377,7 +427,7 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) {
           const int c = 16 * (w * CT + ct) + 4 * lg + ii;
-          ba.dS0[(bh * DK + c) * DV + x.v0 + 16 * vt + lr] = st[ct][vt][ii];
+          dst[c * ld + col0 + 16 * vt + lr] = st[ct][vt][ii];
         }
   }
 }
@@ -1808,11 +1858,30 @@ static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s, hipEvent_t 
   const FwdArgs& a = ba.f;
   hipError_t e;
   auto mark = [&](int i) { return ev && ev[i] ? hipEventRecord(ev[i], s) : hipSuccess; };
-  const int64_t nslab = DV / BVB;
-  const unsigned grid_scan = static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nslab);
+  const int nslab = DV / BVB, npslab = DK / BVB;
+  auto grid_scan = [&](int nrole) { return dim3(static_cast<unsigned>(((a.BH + 7) / 8) * 8 * nrole)); };
   const unsigned grid_chunk = static_cast<unsigned>(a.BH * a.NT);
-  hipLaunchKernelGGL((r1_state_adjoint<T, DK, GATE, C>), dim3(grid_scan), dim3(256), 0, s, ba);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (a.seg_cnt < 3) {
+    BwdArgs b0 = ba;
+    b0.f.seg_phase = 0;
+    hipLaunchKernelGGL((r1_state_adjoint<T, DK, GATE, C>), grid_scan(nslab), dim3(256), 0, s, b0);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  } else {
+    // split reverse scan: the last segment beside the middle segments'
+    // local runs and transitions, the composed starts, then segments
+    // 0 .. S - 2 (the first pass's middle runs also write dHs, Z and dv rows
+    // for their chunks from the wrong start; the third pass overwrites them)
+    const int S = a.seg_cnt;
+    BwdArgs b1 = ba;
+    b1.f.seg_phase = 1;
+    hipLaunchKernelGGL((r1_state_adjoint<T, DK, GATE, C>), grid_scan(nslab + (S - 2) * (nslab + npslab)),
+                       dim3(256), 0, s, b1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_seg_compose(b1.f, true, s)) != hipSuccess) return e;
+    b1.f.seg_phase = 3;
+    hipLaunchKernelGGL((r1_state_adjoint<T, DK, GATE, C>), grid_scan((S - 1) * nslab), dim3(256), 0, s, b1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   if ((e = mark(4)) != hipSuccess) return e;
   if constexpr (GATE == kGateChannel)
     hipLaunchKernelGGL((p12c_chunk_grads<T, DK, DV, C>), dim3(grid_chunk), dim3(256), 0, s, ba);

@@ -1303,33 +1303,40 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
   }
 }
 
-// S^T_start of segment s + 1 = Phi_s S^T_start of segment s + local end of
-// segment s, from segment 1 (whose start is segment 0's exact end) up; one
-// workgroup per head, fp32.  Thread t owns column t % DV and DK / (256 / DV)
+// Exact start states of the segments from the first pass: forward (REV =
+// false), start(1) = end(0) and start(s + 1) = Phi_s start(s) + end(s) up to
+// s = S - 2; reverse (the state-adjoint scan, REV = true), start(S - 2) =
+// end(S - 1) and start(s - 1) = Phi_s start(s) + end(s) down to s = 1 (end:
+// the exact end of the first segment run, a local end otherwise).  One
+// workgroup per head, fp32; thread t owns column t % DV and DK / (256 / DV)
 // consecutive rows.
-template <int DK, int DV>
-__global__ __launch_bounds__(256) void k3_seg_compose(FwdArgs a) {
+template <int DK, int DV, bool REV>
+__global__ __launch_bounds__(256) void seg_compose(FwdArgs a) {
   constexpr int G = 256 / DV, R = DK / G;
   __shared__ float sS[DK * DV];
   __shared__ float sP[DK * DK];
   const int64_t bh = blockIdx.x;
   const int tid = threadIdx.x, v = tid % DV, r0 = (tid / DV) * R;
   const int64_t BHDK = a.BH * static_cast<int64_t>(DK);
-  const float* e0 = a.seg_end + bh * DK * DV;   // segment 0's end
-  float* s1 = a.seg_start + (BHDK + bh * DK) * DV;
+  const int S = a.seg_cnt;
+  auto state = [&](float* base, int sg) { return base + (sg * BHDK + bh * DK) * DV; };
+  const int first = REV ? S - 1 : 0, step = REV ? -1 : 1;
+  const float* e0 = state(a.seg_end, first);
+  float* s1 = state(a.seg_start, first + step);
   float acc[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     acc[r] = e0[(r0 + r) * DV + v];
     s1[(r0 + r) * DV + v] = acc[r];
   }
-  for (int sg = 1; sg + 1 < a.seg_cnt; ++sg) {
-    __syncthreads();   // the previous products are done with the LDS
+  for (int k = 1; k + 1 < S; ++k) {
+    const int sg = first + step * k;   // the middle segment crossed
+    __syncthreads();   // the previous product is done with the LDS
 #pragma unroll
     for (int r = 0; r < R; ++r) sS[(r0 + r) * DV + v] = acc[r];
     const float* phi = a.seg_phi + (sg * BHDK + bh * DK) * DK;
     for (int j = tid; j < DK * DK; j += 256) sP[j] = phi[j];
-    const float* loc = a.seg_end + (sg * BHDK + bh * DK) * DV;
+    const float* loc = state(a.seg_end, sg);
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = loc[(r0 + r) * DV + v];
     __syncthreads();
@@ -1338,10 +1345,24 @@ __global__ __launch_bounds__(256) void k3_seg_compose(FwdArgs a) {
 #pragma unroll
       for (int r = 0; r < R; ++r) acc[r] = fmaf(sP[(r0 + r) * DK + p], hv, acc[r]);
     }
-    float* sn = a.seg_start + ((sg + 1) * BHDK + bh * DK) * DV;
+    float* sn = state(a.seg_start, sg + step);
 #pragma unroll
     for (int r = 0; r < R; ++r) sn[(r0 + r) * DV + v] = acc[r];
   }
+}
+
+template <bool REV>
+static hipError_t launch_compose(const FwdArgs& a, hipStream_t s) {
+  const dim3 grid(static_cast<unsigned>(a.BH));
+  if (a.dk == 64 && a.dv == 64) hipLaunchKernelGGL((seg_compose<64, 64, REV>), grid, dim3(256), 0, s, a);
+  else if (a.dk == 64) hipLaunchKernelGGL((seg_compose<64, 128, REV>), grid, dim3(256), 0, s, a);
+  else if (a.dv == 64) hipLaunchKernelGGL((seg_compose<128, 64, REV>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((seg_compose<128, 128, REV>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_seg_compose(const FwdArgs& a, bool rev, hipStream_t s) {
+  return rev ? launch_compose<true>(a, s) : launch_compose<false>(a, s);
 }
 
 // ---------------------------------------------------------------- T == 0
@@ -1427,9 +1448,7 @@ static hipError_t launch_k3(const FwdArgs& a0, hipStream_t s) {
                      dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (a.dv == 64) hipLaunchKernelGGL((k3_seg_compose<DK, 64>), dim3(static_cast<unsigned>(a.BH)), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((k3_seg_compose<DK, 128>), dim3(static_cast<unsigned>(a.BH)), dim3(256), 0, s, a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = launch_compose<false>(a, s)) != hipSuccess) return e;
   a.seg_phase = 3;
   hipLaunchKernelGGL((k3_chunk_scan<T, DK, GATE, SAVE, OUT, LA, C>), grid((S - 1) * nslab), dim3(256), 0, s, a);
   return hipGetLastError();

@@ -142,6 +142,11 @@ struct BwdArgs {
   float* pcMu;    // [BH, NT]             preconditioner: partial d mu
 };
 
+// The composition pass of a split scan (seg_compose): the exact segment
+// starts from the first pass's end states and transitions, forward or (rev)
+// for the reverse state-adjoint scan.
+hipError_t launch_seg_compose(const FwdArgs& a, bool rev, hipStream_t s);
+
 struct WsLayout {
   size_t sumL, sumD, Abound, KtG, Tm, Pm, G, Qt, QL, KL, seg_end, seg_phi, seg_start, total;
   ScanSplit split;
