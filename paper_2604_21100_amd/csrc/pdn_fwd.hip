@@ -1308,46 +1308,66 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
 // s = S - 2; reverse (the state-adjoint scan, REV = true), start(S - 2) =
 // end(S - 1) and start(s - 1) = Phi_s start(s) + end(s) down to s = 1 (end:
 // the exact end of the first segment run, a local end otherwise).  One
-// workgroup per head, fp32; thread t owns column t % DV and DK / (256 / DV)
-// consecutive rows.
+// workgroup per head, fp32 on MFMA (16x16x4): wave w owns rows
+// [w DK/4, (w+1) DK/4) of every product, all DV columns.
 template <int DK, int DV, bool REV>
 __global__ __launch_bounds__(256) void seg_compose(FwdArgs a) {
-  constexpr int G = 256 / DV, R = DK / G;
-  __shared__ float sS[DK * DV];
-  __shared__ float sP[DK * DK];
+  constexpr int RW = DK / 4, RT = RW / 16, CV = DV / 16;
+  constexpr int LS = DV + 4, LP = DK + 4;   // padded rows
+  __shared__ __attribute__((aligned(16))) float sS[DK * LS];
+  __shared__ __attribute__((aligned(16))) float sP[DK * LP];
   const int64_t bh = blockIdx.x;
-  const int tid = threadIdx.x, v = tid % DV, r0 = (tid / DV) * R;
+  const int tid = threadIdx.x, w = tid >> 6, lr = tid & 15, lg = (tid & 63) >> 4;
   const int64_t BHDK = a.BH * static_cast<int64_t>(DK);
   const int S = a.seg_cnt;
   auto state = [&](float* base, int sg) { return base + (sg * BHDK + bh * DK) * DV; };
   const int first = REV ? S - 1 : 0, step = REV ? -1 : 1;
-  const float* e0 = state(a.seg_end, first);
-  float* s1 = state(a.seg_start, first + step);
-  float acc[R];
+  // acc[rt][cv][ii]: row w RW + 16 rt + 4 lg + ii, column 16 cv + lr
+  floatx4 acc[RT][CV];
+  auto load_acc = [&](const float* src) {
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    acc[r] = e0[(r0 + r) * DV + v];
-    s1[(r0 + r) * DV + v] = acc[r];
-  }
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int cv = 0; cv < CV; ++cv)
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii)
+          acc[rt][cv][ii] = src[(w * RW + 16 * rt + 4 * lg + ii) * DV + 16 * cv + lr];
+  };
+  auto store_acc = [&](float* dst, int ld) {
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int cv = 0; cv < CV; ++cv)
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii)
+          dst[(w * RW + 16 * rt + 4 * lg + ii) * ld + 16 * cv + lr] = acc[rt][cv][ii];
+  };
+  load_acc(state(a.seg_end, first));
+  store_acc(state(a.seg_start, first + step), DV);
   for (int k = 1; k + 1 < S; ++k) {
     const int sg = first + step * k;   // the middle segment crossed
     __syncthreads();   // the previous product is done with the LDS
-#pragma unroll
-    for (int r = 0; r < R; ++r) sS[(r0 + r) * DV + v] = acc[r];
+    store_acc(sS, LS);
     const float* phi = a.seg_phi + (sg * BHDK + bh * DK) * DK;
-    for (int j = tid; j < DK * DK; j += 256) sP[j] = phi[j];
-    const float* loc = state(a.seg_end, sg);
-#pragma unroll
-    for (int r = 0; r < R; ++r) acc[r] = loc[(r0 + r) * DV + v];
-    __syncthreads();
-    for (int p = 0; p < DK; ++p) {
-      const float hv = sS[p * DV + v];
-#pragma unroll
-      for (int r = 0; r < R; ++r) acc[r] = fmaf(sP[(r0 + r) * DK + p], hv, acc[r]);
+    for (int j = tid * 4; j < DK * DK; j += 1024) {
+      const float4 v = *reinterpret_cast<const float4*>(phi + j);
+      *reinterpret_cast<float4*>(sP + (j / DK) * LP + j % DK) = v;
     }
-    float* sn = state(a.seg_start, sg + step);
+    load_acc(state(a.seg_end, sg));
+    __syncthreads();
+#pragma unroll 4
+    for (int kk = 0; kk < DK; kk += 4) {
+      float fa[RT], fb[CV];
 #pragma unroll
-    for (int r = 0; r < R; ++r) sn[(r0 + r) * DV + v] = acc[r];
+      for (int rt = 0; rt < RT; ++rt) fa[rt] = sP[(w * RW + 16 * rt + lr) * LP + kk + lg];
+#pragma unroll
+      for (int cv = 0; cv < CV; ++cv) fb[cv] = sS[(kk + lg) * LS + 16 * cv + lr];
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int cv = 0; cv < CV; ++cv) mma4(acc[rt][cv], fa[rt], fb[cv]);
+    }
+    store_acc(state(a.seg_start, sg + step), DV);
   }
 }
 
