@@ -1751,33 +1751,45 @@ __global__ __launch_bounds__(64 * (C / PCG)) void pc_chunk(BwdArgs ba) {
 
 // carry_{i-1} = L_i + exp(sumD_i) carry_i, from the last chunk (carry 0);
 // summaries and carries are adjoints divided by -log x, as in pc_chunk
+// The chunks' local adjoints chained from the right, carry_i = L_i +
+// exp(D_i) carry_{i+1} (zero past the last chunk); pcC[i + 1] holds the
+// carry entering chunk i.  16 channels x 16 chunk segments a workgroup:
+// each segment reduces to its affine map, a segment's entering carry chains
+// the maps of the segments to its right, and each segment re-walks its
+// chunks writing the carries.
+constexpr int kPcCh = 16, kPcSeg = 16;
 template <int DK>
-__global__ __launch_bounds__(DK) void pc_carry(BwdArgs ba) {
+__global__ __launch_bounds__(256) void pc_carry(BwdArgs ba) {
+  __shared__ float sE[kPcSeg][kPcCh], sP[kPcSeg][kPcCh];
   const FwdArgs& a = ba.f;
-  const int64_t bh = blockIdx.x;
-  const int c = threadIdx.x;
-  float carry = 0.f;
-  float* out = ba.pcC + bh * (a.NT + 1) * DK + c;
-  const float* L = ba.pcL + bh * a.NT * DK + c;
-  const float* D = a.sumD + bh * a.NT;
-  out[(int64_t)a.NT * DK] = 0.f;
-  int i = a.NT - 1;
-  // eight chunks' inputs in flight at a time; the chain itself is cheap
-  for (; i >= 7; i -= 8) {
-    float l[8], d[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) { l[u] = L[(int64_t)(i - u) * DK]; d[u] = D[i - u]; }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      out[(int64_t)(i - u + 1) * DK] = carry;
-      carry = l[u] + fast_exp(d[u]) * carry;
-    }
+  const int64_t bh = blockIdx.x / (DK / kPcCh);
+  const int ch = threadIdx.x % kPcCh, sg = threadIdx.x / kPcCh;
+  const int c = static_cast<int>(blockIdx.x % (DK / kPcCh)) * kPcCh + ch;
+  const int NT = a.NT, Ls = (NT + kPcSeg - 1) / kPcSeg;
+  const int i0 = min(NT, sg * Ls), i1 = min(NT, i0 + Ls);
+  float* out = ba.pcC + bh * (NT + 1) * DK + c;
+  const float* L = ba.pcL + bh * NT * DK + c;
+  const float* D = a.sumD + bh * NT;
+  float E = 1.f, P = 0.f;
+#pragma unroll 8
+  for (int i = i1 - 1; i >= i0; --i) {
+    const float e = fast_exp(D[i]);
+    E *= e;
+    P = L[(int64_t)i * DK] + e * P;
   }
-  for (; i >= 0; --i) {
+  sE[sg][ch] = E;
+  sP[sg][ch] = P;
+  __syncthreads();
+  float carry = 0.f;
+  if (sg == kPcSeg - 1) out[(int64_t)NT * DK] = 0.f;
+  for (int q = kPcSeg - 1; q > sg; --q) carry = sP[q][ch] + sE[q][ch] * carry;
+#pragma unroll 8
+  for (int i = i1 - 1; i >= i0; --i) {
     out[(int64_t)(i + 1) * DK] = carry;
     carry = L[(int64_t)i * DK] + fast_exp(D[i]) * carry;
   }
-  if (ba.dA0) ba.dA0[bh * DK + c] = -a.lnx * carry;   // carries are kept divided by -log x
+  // carries are kept divided by -log x
+  if (ba.dA0 && sg == 0) ba.dA0[bh * DK + c] = -a.lnx * carry;
 }
 
 // d logAScale_h = mu_h * sum over batches and chunks of the partial d mu
@@ -1892,7 +1904,7 @@ static hipError_t launch_bwd_typed(const BwdArgs& ba, hipStream_t s, hipEvent_t 
   if (a.precond == kSquash) {
     hipLaunchKernelGGL((pc_chunk<T, DK, false, C>), dim3(grid_chunk), dim3(64 * PCS), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((pc_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, ba);
+    hipLaunchKernelGGL((pc_carry<DK>), dim3(static_cast<unsigned>(a.BH * (DK / kPcCh))), dim3(256), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((pc_chunk<T, DK, true, C>), dim3(grid_chunk), dim3(64 * PCS), 0, s, ba);
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -93,42 +93,42 @@ __global__ __launch_bounds__(256) void k1_precond_summary(FwdArgs a) {
   }
 }
 
+// The chunk summaries chained into the state before every chunk, A_{i+1} =
+// exp(D_i) A_i + L_i per channel: 16 channels x 16 chunk segments a
+// workgroup.  Each segment reduces to its affine map (prod exp D, partial
+// sum from zero), a segment's start state chains the maps before it from
+// A0, and each segment re-walks its chunks writing the states.
+constexpr int kCarryCh = 16, kCarrySeg = 16;
 template <int DK>
-__global__ __launch_bounds__(DK) void k1_precond_carry(FwdArgs a) {
-  const int64_t bh = blockIdx.x;
-  const int c = threadIdx.x;
+__global__ __launch_bounds__(256) void k1_precond_carry(FwdArgs a) {
+  __shared__ float sE[kCarrySeg][kCarryCh], sP[kCarrySeg][kCarryCh];
+  const int64_t bh = blockIdx.x / (DK / kCarryCh);
+  const int ch = threadIdx.x % kCarryCh, sg = threadIdx.x / kCarryCh;
+  const int c = static_cast<int>(blockIdx.x % (DK / kCarryCh)) * kCarryCh + ch;
+  const int NT = a.NT, Ls = (NT + kCarrySeg - 1) / kCarrySeg;
+  const int i0 = min(NT, sg * Ls), i1 = min(NT, i0 + Ls);
+  float* out = a.Abound + bh * (NT + 1) * DK + c;
+  const float* L = a.sumL + bh * NT * DK + c;
+  const float* D = a.sumD + bh * NT;
+  float E = 1.f, P = 0.f;
+#pragma unroll 8
+  for (int i = i0; i < i1; ++i) {
+    const float e = fast_exp(D[i]);
+    E *= e;
+    P = e * P + L[(int64_t)i * DK];
+  }
+  sE[sg][ch] = E;
+  sP[sg][ch] = P;
+  __syncthreads();
   float A = a.A0 ? a.A0[bh * DK + c] : 0.f;
-  float* out = a.Abound + bh * (a.NT + 1) * DK + c;
-  const float* L = a.sumL + bh * a.NT * DK + c;
-  const float* D = a.sumD + bh * a.NT;
-  out[0] = A;
-  // batches of 8 chunks; the next batch's loads are issued before the
-  // current batch is chained
-  constexpr int U = 8;
-  float d[U], l[U], dn[U], ln[U];
-  const int NT = a.NT;
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int j = min(u, NT - 1);
-    d[u] = D[j]; l[u] = L[(int64_t)j * DK];
+  if (sg == 0) out[0] = A;
+  for (int q = 0; q < sg; ++q) A = sE[q][ch] * A + sP[q][ch];
+#pragma unroll 8
+  for (int i = i0; i < i1; ++i) {
+    A = fast_exp(D[i]) * A + L[(int64_t)i * DK];
+    out[(int64_t)(i + 1) * DK] = A;
   }
-  for (int i = 0; i < NT; i += U) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int j = min(i + U + u, NT - 1);
-      dn[u] = D[j]; ln[u] = L[(int64_t)j * DK];
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (i + u < NT) {
-        A = fast_exp(d[u]) * A + l[u];
-        out[(int64_t)(i + u + 1) * DK] = A;
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) { d[u] = dn[u]; l[u] = ln[u]; }
-  }
-  if (a.A_T) a.A_T[bh * DK + c] = A;
+  if (a.A_T && i0 < i1 && i1 == NT) a.A_T[bh * DK + c] = A;
 }
 
 // ---------------------------------------------------------------- K2
@@ -1485,7 +1485,7 @@ static hipError_t launch_all(const FwdArgs& a, hipStream_t s, hipEvent_t const* 
     hipLaunchKernelGGL((k1_precond_summary<T, DK, C>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
                        0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((k1_precond_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, a);
+    hipLaunchKernelGGL((k1_precond_carry<DK>), dim3(static_cast<unsigned>(a.BH * (DK / kCarryCh))), dim3(256), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if ((e = mark(1)) != hipSuccess) return e;
@@ -1537,7 +1537,7 @@ static hipError_t launch_recompute(const FwdArgs& a, hipStream_t s, hipEvent_t c
     hipLaunchKernelGGL((k1_precond_summary<T, DK, C>), dim3(static_cast<unsigned>(a.BH * a.NT)), dim3(256),
                        0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((k1_precond_carry<DK>), dim3(static_cast<unsigned>(a.BH)), dim3(DK), 0, s, a);
+    hipLaunchKernelGGL((k1_precond_carry<DK>), dim3(static_cast<unsigned>(a.BH * (DK / kCarryCh))), dim3(256), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if ((e = mark(1)) != hipSuccess) return e;
