@@ -1158,60 +1158,17 @@ __device__ __forceinline__ void scan_step(ScanFrags<T, DK, GATE, C>& f, const fl
 // SAVE: also write the chunk-start states and the E rows the backward
 // reads.  OUT: compute and write the output (without it, queries and P are
 // neither loaded nor used: the backward's recompute).
+// One workgroup's run of the scan: chunks [x.c0, c1) of head x.bh, from the
+// start state its role gives (S0, a composed segment start, zero, or for a
+// transition slab the identity columns pv0 ..), ending with the end state
+// written where its role sends it.
 template <typename T, int DK, int GATE, bool SAVE, bool OUT, bool LA, int C>
-__global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
-  constexpr int CT = DK / 64;       // state row tiles per wave
-  constexpr int LDH = DK + 8, LDE = C + 8;
-  // [v][.] slabs, addressed through sw() / swv() (bank-spread)
-  __shared__ __attribute__((aligned(16))) T sH[BV * LDH];   // io copy of the S^T slab, [v][c]
-  __shared__ __attribute__((aligned(16))) T sX[BV * LDE];   // X = V - Lam K S^T, [v][t]
-  __shared__ __attribute__((aligned(16))) T sE[BV * LDE];   // E = T X, [v][t]
-  __shared__ __attribute__((aligned(16))) T sVt[BV * LDE];  // this chunk's values, [v][t]
-  __shared__ __attribute__((aligned(16))) T sO[BV * LDE];   // last chunk's output, [v][t]
-
-  // workgroup -> (head, role, slab); the slabs of one head share an XCD
-  // (and its L2).  Roles per head: phase 0, the value slabs of the whole
-  // sequence; phase 1, segment 0's value slabs, then per middle segment its
-  // value slabs (local, from zero) and d_k / BV transition slabs; phase 3,
-  // the value slabs of segments 1 .. S - 1.
-  const int nslab = a.dv / BV, npslab = DK / BV;
-  const int S = a.seg_cnt;
-  const int nrole = a.seg_phase == 0 ? nslab
-                  : a.seg_phase == 1 ? nslab + (S - 2) * (nslab + npslab)
-                                     : (S - 1) * nslab;
-  const int64_t bid = blockIdx.x;
-  const int xcd = static_cast<int>(bid & 7);
-  const int64_t j8 = bid >> 3;
-  const int role = static_cast<int>(j8 % nrole);
-  const int64_t bh = (j8 / nrole) * 8 + xcd;
-  if (bh >= a.BH) return;
-  int seg = 0, slab = role;
-  bool probe = false;
-  if (a.seg_phase == 1 && role >= nslab) {
-    const int r = role - nslab;
-    seg = 1 + r / (nslab + npslab);
-    slab = r % (nslab + npslab);
-    probe = slab >= nslab;
-  } else if (a.seg_phase == 3) {
-    seg = 1 + role / nslab;
-    slab = role % nslab;
-  }
-  const int c0 = a.seg_phase == 0 ? 0 : seg * a.seg_len;
-  const int c1 = a.seg_phase == 0 ? a.NT : min(a.NT, c0 + a.seg_len);
-  ScanCtx x;
-  x.bh = bh;
-  x.b = bh / a.H;
-  x.h = bh % a.H;
-  x.tid = threadIdx.x;
-  x.w = x.tid >> 6;
-  x.lr = x.tid & 15;
-  x.lg = (x.tid & 63) >> 4;
-  // a transition slab reads (and zeroes) value slab 0; its own columns are
-  // pv0 .. pv0 + BV of the d_k x d_k transition
-  x.v0 = probe ? 0 : slab * BV;
-  x.c0 = c0;
-  x.vkeep = probe ? 0.f : 1.f;
-  const int pv0 = probe ? (slab - nslab) * BV : 0;
+__device__ __forceinline__ void k3_body(const FwdArgs& a, const ScanCtx& x, int seg, bool probe, int pv0,
+                                        int c1, T* sH, T* sX, T* sE, T* sVt, T* sO) {
+  constexpr int CT = DK / 64;
+  constexpr int LDH = DK + 8;
+  const int64_t bh = x.bh;
+  const int c0 = x.c0;
   const int w = x.w, lr = x.lr, lg = x.lg;
   const int DV = a.dv;
   const int64_t BHDK = a.BH * static_cast<int64_t>(DK);
@@ -1301,6 +1258,71 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
           dst[c * ld + col0 + 16 * vt + lr] = st[ct][vt][ii];
         }
   }
+}
+
+template <typename T, int DK, int GATE, bool SAVE, bool OUT, bool LA, int C>
+__global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
+  constexpr int CT = DK / 64;       // state row tiles per wave
+  constexpr int LDH = DK + 8, LDE = C + 8;
+  // [v][.] slabs, addressed through sw() / swv() (bank-spread)
+  __shared__ __attribute__((aligned(16))) T sH[BV * LDH];   // io copy of the S^T slab, [v][c]
+  __shared__ __attribute__((aligned(16))) T sX[BV * LDE];   // X = V - Lam K S^T, [v][t]
+  __shared__ __attribute__((aligned(16))) T sE[BV * LDE];   // E = T X, [v][t]
+  __shared__ __attribute__((aligned(16))) T sVt[BV * LDE];  // this chunk's values, [v][t]
+  __shared__ __attribute__((aligned(16))) T sO[BV * LDE];   // last chunk's output, [v][t]
+
+  // workgroup -> (head, role, slab); the slabs of one head share an XCD
+  // (and its L2).  Roles per head: phase 0, the value slabs of the whole
+  // sequence; phase 1, segment 0's value slabs, then per middle segment its
+  // value slabs (local, from zero) and d_k / BV transition slabs; phase 3,
+  // the value slabs of segments 1 .. S - 1.
+  const int nslab = a.dv / BV, npslab = DK / BV;
+  const int S = a.seg_cnt;
+  const int nrole = a.seg_phase == 0 ? nslab
+                  : a.seg_phase == 1 ? nslab + (S - 2) * (nslab + npslab)
+                                     : (S - 1) * nslab;
+  const int64_t bid = blockIdx.x;
+  const int xcd = static_cast<int>(bid & 7);
+  const int64_t j8 = bid >> 3;
+  const int role = static_cast<int>(j8 % nrole);
+  const int64_t bh = (j8 / nrole) * 8 + xcd;
+  if (bh >= a.BH) return;
+  int seg = 0, slab = role;
+  bool probe = false;
+  if (a.seg_phase == 1 && role >= nslab) {
+    const int r = role - nslab;
+    seg = 1 + r / (nslab + npslab);
+    slab = r % (nslab + npslab);
+    probe = slab >= nslab;
+  } else if (a.seg_phase == 3) {
+    seg = 1 + role / nslab;
+    slab = role % nslab;
+  }
+  const int c0 = a.seg_phase == 0 ? 0 : seg * a.seg_len;
+  const int c1 = a.seg_phase == 0 ? a.NT : min(a.NT, c0 + a.seg_len);
+  ScanCtx x;
+  x.bh = bh;
+  x.b = bh / a.H;
+  x.h = bh % a.H;
+  x.tid = threadIdx.x;
+  x.w = x.tid >> 6;
+  x.lr = x.tid & 15;
+  x.lg = (x.tid & 63) >> 4;
+  // a transition slab reads (and zeroes) value slab 0; its own columns are
+  // pv0 .. pv0 + BV of the d_k x d_k transition
+  x.v0 = probe ? 0 : slab * BV;
+  x.c0 = c0;
+  x.vkeep = probe ? 0.f : 1.f;
+  const int pv0 = probe ? (slab - nslab) * BV : 0;
+  // middle segments of the first pass need only their end states: their
+  // run skips the output and the saved rows (the third pass writes those)
+  if constexpr (SAVE || OUT) {
+    if (a.seg_phase == 1 && seg > 0) {
+      k3_body<T, DK, GATE, false, false, LA, C>(a, x, seg, probe, pv0, c1, sH, sX, sE, sVt, sO);
+      return;
+    }
+  }
+  k3_body<T, DK, GATE, SAVE, OUT, LA, C>(a, x, seg, probe, pv0, c1, sH, sX, sE, sVt, sO);
 }
 
 // Exact start states of the segments from the first pass: forward (REV =
