@@ -212,7 +212,9 @@ __device__ __forceinline__ void rev_stage_dO(const float4 (&v)[Slab<T, C>::kPer]
   }
 }
 
-template <bool FULL, typename T, int DK, int GATE, int C>
+// WR = false: the step leaves no rows behind (dHs, Z and dv are not
+// written): a run that only needs its end state
+template <bool FULL, typename T, int DK, int GATE, int C, bool WR = true>
 __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE, C>& f, bool stage_next,
                                          floatx4 (&st)[DK / 64][2], const BwdArgs& ba, int i,
                                          const RevCtx& x, T* sH, T* sDOc, T* sDOn, T* sE, T* sX,
@@ -238,8 +240,9 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE, C>& f, bool stage
   }
   // state adjoint entering this chunk from the right, rows c, slab columns
   // (its LDS reads after the operand reads: LDS reads complete in issue order)
-  slab_to_rows<DK, true>(static_cast<T*>(ba.dHs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv,
-                         sH, LDH, DK, x.tid);
+  if (WR)
+    slab_to_rows<DK, true>(static_cast<T*>(ba.dHs) + (x.bh * a.NT + i) * (int64_t)DK * a.dv + x.v0, a.dv,
+                           sH, LDH, DK, x.tid);
   if (rows) {
 #pragma unroll
     for (int vt = 0; vt < 2; ++vt) {
@@ -277,7 +280,7 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE, C>& f, bool stage
   for (int vt = 0; vt < 2; ++vt)
 #pragma unroll
     for (int k2 = 0; k2 < KC; ++k2) bX[vt][k2] = ld8(swc<C>(sX, LDE, 16 * vt + lr, k2 * 32 + 8 * lg));
-  {
+  if (WR) {
     // Z and dv rows (their LDS reads after the operand reads)
     const int64_t r0 = (x.bh * a.Tpad + t0) * a.dv + x.v0;
     slab_to_rows<C, true>(static_cast<T*>(ba.Zr) + r0, a.dv, sZ, LDE, C, x.tid);
@@ -303,6 +306,97 @@ __device__ __forceinline__ void rev_step(RevFrags<T, DK, GATE, C>& f, bool stage
     }
   if (stage_next) rev_stage_dO<T, C>(f.dO, sDOn, C, x.dscale, x.tid);  // earlier chunks are full
   lds_barrier_b();
+}
+
+// One workgroup's run of the reverse scan: chunks [c0, c1) of head x.bh
+// from the top down, from the start state its role gives (dS_T, a composed
+// segment start, zero, or for a transition slab the identity columns
+// pv0 ..), ending with the end state written where its role sends it.
+template <typename T, int DK, int GATE, int C, bool WR>
+__device__ __forceinline__ void r1_body(const BwdArgs& ba, const RevCtx& x, int seg, bool probe, int pv0,
+                                        int c0, int c1, T* sH, T* sDO0, T* sDO1, T* sE, T* sX, T* sZ) {
+  constexpr int CT = DK / 64;
+  constexpr int LDH = DK + 8;
+  const FwdArgs& a = ba.f;
+  const int S = a.seg_cnt;
+  const int64_t bh = x.bh;
+  T* sDO[2] = {sDO0, sDO1};
+  const int w = x.w, lr = x.lr, lg = x.lg;
+  const int DV = a.dv;
+  const int64_t BHDK = a.BH * static_cast<int64_t>(DK);
+  floatx4 st[CT][2];
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int c = 16 * (w * CT + ct) + 4 * lg + ii, v = 16 * vt + lr;
+        float s0 = 0.f;   // middle segments' local runs start from zero
+        if (a.seg_phase == 0 || (a.seg_phase == 1 && seg == S - 1))
+          s0 = ba.dS_T ? ba.dS_T[(bh * DK + c) * DV + x.v0 + v] : 0.f;
+        else if (a.seg_phase == 3)
+          s0 = a.seg_start[(seg * BHDK + bh * DK + c) * DV + x.v0 + v];
+        else if (probe)
+          s0 = c == pv0 + v ? 1.f : 0.f;
+        st[ct][vt][ii] = s0;
+      }
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int vt = 0; vt < 2; ++vt)
+      st4<T>(sw(sH, LDH, 16 * vt + lr, 16 * (w * CT + ct) + 4 * lg), st[ct][vt][0], st[ct][vt][1],
+             st[ct][vt][2], st[ct][vt][3]);
+  // reverse order over the run [c0, c1): its top chunk first (the ragged
+  // last chunk of the sequence, if the run ends there), then full chunks two
+  // per trip with a branch-free body; dO slabs double-buffered
+  const int top = c1 - 1;
+  RevFrags<T, DK, GATE, C> fA, fB;
+  float4 dlast[Slab<T, C>::kPer];
+  rev_load_dO<T, C>(dlast, ba, top, x);
+  rev_load<T, DK, GATE, C>(fA, ba, top, x);
+  rev_load<T, DK, GATE, C>(fB, ba, max(top - 1, c0), x);
+  rev_stage_dO<T, C>(dlast, sDO[0], static_cast<int>(min<int64_t>(C, a.T - static_cast<int64_t>(top) * C)),
+                     x.dscale, x.tid);
+  __syncthreads();
+  rev_step<false, T, DK, GATE, C, WR>(fA, top > c0, st, ba, top, x, sH, sDO[0], sDO[1], sE, sX, sZ);
+  int i = top - 1, buf = 1;
+  for (; i >= c0 + 1; i -= 2) {
+    rev_load<T, DK, GATE, C>(fA, ba, i - 1, x);
+    rev_step<true, T, DK, GATE, C, WR>(fB, true, st, ba, i, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
+    buf ^= 1;
+    rev_load<T, DK, GATE, C>(fB, ba, max(i - 2, c0), x);
+    rev_step<true, T, DK, GATE, C, WR>(fA, true, st, ba, i - 1, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
+    buf ^= 1;
+  }
+  if (i == c0) rev_step<true, T, DK, GATE, C, WR>(fB, false, st, ba, c0, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
+  // the end state: dS0 after chunk 0; phase 1: the last segment's exact
+  // end, a middle segment's local end or its transition
+  float* dst = nullptr;
+  int64_t ld = DV;
+  int col0 = x.v0;
+  if (a.seg_phase == 1) {
+    if (probe) {
+      dst = a.seg_phi + (seg * BHDK + bh * DK) * DK;
+      ld = DK;
+      col0 = pv0;
+    } else {
+      dst = a.seg_end + (seg * BHDK + bh * DK) * DV;
+    }
+  } else if (c0 == 0 && ba.dS0) {
+    dst = ba.dS0 + bh * DK * DV;
+  }
+  if (dst) {
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) {
+          const int c = 16 * (w * CT + ct) + 4 * lg + ii;
+          dst[c * ld + col0 + 16 * vt + lr] = st[ct][vt][ii];
+        }
+  }
 }
 
 template <typename T, int DK, int GATE, int C>
@@ -354,82 +448,12 @@ __global__ __launch_bounds__(256) void r1_state_adjoint(BwdArgs ba) {
   x.v0 = probe ? 0 : slab * BVB;
   x.dscale = probe ? 0.f : a.scale;
   const int pv0 = probe ? (slab - nslab) * BVB : 0;
-  const int w = x.w, lr = x.lr, lg = x.lg;
-  const int DV = a.dv;
-  const int64_t BHDK = a.BH * static_cast<int64_t>(DK);
-  floatx4 st[CT][2];
-#pragma unroll
-  for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-    for (int vt = 0; vt < 2; ++vt)
-#pragma unroll
-      for (int ii = 0; ii < 4; ++ii) {
-        const int c = 16 * (w * CT + ct) + 4 * lg + ii, v = 16 * vt + lr;
-        float s0 = 0.f;   // middle segments' local runs start from zero
-        if (a.seg_phase == 0 || (a.seg_phase == 1 && seg == S - 1))
-          s0 = ba.dS_T ? ba.dS_T[(bh * DK + c) * DV + x.v0 + v] : 0.f;
-        else if (a.seg_phase == 3)
-          s0 = a.seg_start[(seg * BHDK + bh * DK + c) * DV + x.v0 + v];
-        else if (probe)
-          s0 = c == pv0 + v ? 1.f : 0.f;
-        st[ct][vt][ii] = s0;
-      }
-#pragma unroll
-  for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-    for (int vt = 0; vt < 2; ++vt)
-      st4<T>(sw(sH, LDH, 16 * vt + lr, 16 * (w * CT + ct) + 4 * lg), st[ct][vt][0], st[ct][vt][1],
-             st[ct][vt][2], st[ct][vt][3]);
-  // reverse order over the run [c0, c1): its top chunk first (the ragged
-  // last chunk of the sequence, if the run ends there), then full chunks two
-  // per trip with a branch-free body; dO slabs double-buffered
-  const int top = c1 - 1;
-  RevFrags<T, DK, GATE, C> fA, fB;
-  float4 dlast[Slab<T, C>::kPer];
-  rev_load_dO<T, C>(dlast, ba, top, x);
-  rev_load<T, DK, GATE, C>(fA, ba, top, x);
-  rev_load<T, DK, GATE, C>(fB, ba, max(top - 1, c0), x);
-  rev_stage_dO<T, C>(dlast, sDO[0], static_cast<int>(min<int64_t>(C, a.T - static_cast<int64_t>(top) * C)),
-                     x.dscale, x.tid);
-  __syncthreads();
-  rev_step<false, T, DK, GATE, C>(fA, top > c0, st, ba, top, x, sH, sDO[0], sDO[1], sE, sX, sZ);
-  int i = top - 1, buf = 1;
-  for (; i >= c0 + 1; i -= 2) {
-    rev_load<T, DK, GATE, C>(fA, ba, i - 1, x);
-    rev_step<true, T, DK, GATE, C>(fB, true, st, ba, i, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
-    buf ^= 1;
-    rev_load<T, DK, GATE, C>(fB, ba, max(i - 2, c0), x);
-    rev_step<true, T, DK, GATE, C>(fA, true, st, ba, i - 1, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
-    buf ^= 1;
+  // middle segments of the first pass need only their end states
+  if (a.seg_phase == 1 && seg < S - 1) {
+    r1_body<T, DK, GATE, C, false>(ba, x, seg, probe, pv0, c0, c1, sH, sDO[0], sDO[1], sE, sX, sZ);
+    return;
   }
-  if (i == c0) rev_step<true, T, DK, GATE, C>(fB, false, st, ba, c0, x, sH, sDO[buf], sDO[buf ^ 1], sE, sX, sZ);
-  // the end state: dS0 after chunk 0; phase 1: the last segment's exact
-  // end, a middle segment's local end or its transition
-  float* dst = nullptr;
-  int64_t ld = DV;
-  int col0 = x.v0;
-  if (a.seg_phase == 1) {
-    if (probe) {
-      dst = a.seg_phi + (seg * BHDK + bh * DK) * DK;
-      ld = DK;
-      col0 = pv0;
-    } else {
-      dst = a.seg_end + (seg * BHDK + bh * DK) * DV;
-    }
-  } else if (c0 == 0 && ba.dS0) {
-    dst = ba.dS0 + bh * DK * DV;
-  }
-  if (dst) {
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-      for (int vt = 0; vt < 2; ++vt)
-#pragma unroll
-        for (int ii = 0; ii < 4; ++ii) {
-          const int c = 16 * (w * CT + ct) + 4 * lg + ii;
-          dst[c * ld + col0 + 16 * vt + lr] = st[ct][vt][ii];
-        }
-  }
+  r1_body<T, DK, GATE, C, true>(ba, x, seg, probe, pv0, c0, c1, sH, sDO[0], sDO[1], sE, sX, sZ);
 }
 
 // ------------------------------------------------------------ p1
