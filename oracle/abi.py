@@ -108,6 +108,7 @@ def backward(inp, *, gate, precond="squash", x=1.5, scale=1.0, heads=None,
     r["dS0"] = np.swapaxes(r["dS0"], 1, 2)
     if "dmu" in r:
         r["dlog_a_scale"] = d["mu"] * r["dmu"]
+        r["dlog_a_scale_abs"] = d["mu"] * r["dmu_abs"]
     return r
 
 

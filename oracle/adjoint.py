@@ -29,7 +29,8 @@ def pdn_backward(q, k, v, beta, do, *, g=None, gate="none",
     """Gradients of sum_t <do_t, o_t> + <dS_T, S_T> with respect to every
     input.  Shapes as in `recurrent` (per-head layout).  Returns a dict with
     dq, dk, dv (N,T,d); dbeta, dg (N,T) or dg (N,T,dk); dS0 (N,dv,dk);
-    and for precond="squash": dbeta_p, dg_p (N,T), dmu (N,), dA0 (N,dk);
+    and for precond="squash": dbeta_p, dg_p (N,T), dmu (N,), dA0 (N,dk),
+    and dmu_abs (N,), the sum of the absolute values of dmu's terms;
     for precond="external": dkt (N,T,dk)."""
     q, k, v, beta, do = map(_f64, (q, k, v, beta, do))
     g = _f64(g)
@@ -112,6 +113,7 @@ def pdn_backward(q, k, v, beta, do, *, g=None, gate="none",
         lnx = np.log(x)
         dA = np.zeros((N, dk))
         dmu = np.zeros(N)
+        dmu_abs = np.zeros(N)   # sum of |terms| of dmu: the scale of its rounding error
         dbeta_p = np.zeros((N, T))
         dg_p = np.zeros((N, T))
         m = mu.reshape(N, 1)
@@ -128,11 +130,12 @@ def pdn_backward(q, k, v, beta, do, *, g=None, gate="none",
                 dr = np.where(pos, ds / (1.0 + np.abs(r)) ** 2, 0.0)
                 dA_tot = dA + np.where(pos, dr / A_t, 0.0)
             dmu -= dr.sum(axis=1)
+            dmu_abs += np.abs(dr).sum(axis=1)
             dbeta_p[:, t] = np.einsum("nk,nk->n", dA_tot, k[:, t] ** 2)
             dkk[:, t] += 2.0 * beta_p[:, t, None] * k[:, t] * dA_tot
             a_p = np.ones(N) if g_p is None else np.exp(_f64(g_p)[:, t])
             dg_p[:, t] = a_p * np.einsum("nk,nk->n", dA_tot, A_prev)
             dA = a_p[:, None] * dA_tot
-        out.update(dbeta_p=dbeta_p, dg_p=dg_p, dmu=dmu, dA0=dA)
+        out.update(dbeta_p=dbeta_p, dg_p=dg_p, dmu=dmu, dmu_abs=dmu_abs, dA0=dA)
     out["dk"] = dkk
     return out

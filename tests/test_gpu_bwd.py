@@ -3,7 +3,11 @@ the float64 oracle adjoint on the same seeded inputs.
 
 Every gradient is compared with max|x - r| / max|r|: <= 1e-4 for fp32 io and
 <= 2e-2 for bf16 io (the bar the forward outputs meet, applied to each
-gradient)."""
+gradient).  The one exception is d logAScale, a sum over every token and
+key channel of terms of both signs (the squash gain depends on mu through
+r_t = log A_t - mu): its sum cancels to 0.1 - 0.7 % of the sum of its
+terms' magnitudes, so its error is measured against that magnitude, the
+scale of the standard bound for a rounded sum (error <= n u sum |x_i|)."""
 import numpy as np
 import pytest
 
@@ -56,11 +60,13 @@ def compare(spec, inp, precond="squash", dS_T=None, heads=None, tag="", chunk=64
         g = got[name]
         if name == "dlog_a_scale":
             r = np.zeros(H)
+            scale = np.zeros(H)
             for n, (b, h) in enumerate(heads):
                 r[h] += ref["dlog_a_scale"][n]
+                scale[h] += ref["dlog_a_scale_abs"][n]
             if len(heads) != B * H:
                 continue
-            errs[name] = rel_err(g, r)
+            errs[name] = float(np.abs(np.asarray(g, np.float64) - r).max() / scale.max())
             continue
         key = {"dktilde": "dkt"}.get(name, name)
         r = ref[key]
