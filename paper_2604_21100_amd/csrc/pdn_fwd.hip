@@ -469,6 +469,15 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       *reinterpret_cast<float4*>(qt + r * DK + cv * VEC) = *reinterpret_cast<const float4*>(k2sw(sQ, LDK, r, cv * VEC));
     }
   }
+  // NOQ: the query fragments of this lane's A-operand row, straight from
+  // HBM, issued here so they arrive during the decayed-row outputs
+  Frag8<T> fqr[DK / 32];
+  if (NOQ && (NB == 4 || w < NB)) {
+    const int r = 16 * w + lr;
+    const T* qrow = static_cast<const T*>(a.q) + ((b * a.T + t0 + min(r, n - 1)) * a.H + h) * DK;
+#pragma unroll
+    for (int kk = 0; kk < DK / 32; ++kk) fqr[kk] = ld8(qrow + kk * 32 + 8 * lg);
+  }
   if (GATE == kGateChannel) {
     // Lam o Q and Lam o K (Lam_r = exp(G_r) per channel; Q the query the
     // scan reads: q, or for ATQ the preconditioned query): the rows the
@@ -531,15 +540,9 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   for (int j = 0; j < NB; ++j) { accA[j] = floatx4{0.f, 0.f, 0.f, 0.f}; accP[j] = accA[j]; }
   if (NB == 4 || w < NB) {
     const int r = 16 * w + lr;  // A-operand row of this lane
-    // NOQ: this row's query fragments straight from HBM, once
-    Frag8<T> fqr[DK / 32];
-    if (NOQ) {
-      const T* qrow = static_cast<const T*>(a.q) + ((b * a.T + t0 + min(r, n - 1)) * a.H + h) * DK;
+    if (NOQ && r >= n) {   // rows past the sequence end: zero queries
 #pragma unroll
-      for (int kk = 0; kk < DK / 32; ++kk) {
-        fqr[kk] = ld8(qrow + kk * 32 + 8 * lg);
-        if (r >= n) fqr[kk] = frag_zero<T>();
-      }
+      for (int kk = 0; kk < DK / 32; ++kk) fqr[kk] = frag_zero<T>();
     }
     if (GATE == kGateChannel) {
       // the decay ratio e^{G_r - G_t} inside the contraction, split at a
@@ -1262,7 +1265,6 @@ __device__ __forceinline__ void k3_body(const FwdArgs& a, const ScanCtx& x, int 
 
 template <typename T, int DK, int GATE, bool SAVE, bool OUT, bool LA, int C>
 __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
-  constexpr int CT = DK / 64;       // state row tiles per wave
   constexpr int LDH = DK + 8, LDE = C + 8;
   // [v][.] slabs, addressed through sw() / swv() (bank-spread)
   __shared__ __attribute__((aligned(16))) T sH[BV * LDH];   // io copy of the S^T slab, [v][c]
