@@ -133,15 +133,22 @@ __global__ __launch_bounds__(256) void k1_precond_carry(FwdArgs a) {
 
 // ---------------------------------------------------------------- K2
 // k2's tiles are read along rows (MFMA fragments, row staging) and down
-// columns (the transposed outputs, the column-wise scans).  The column index
-// is XOR-permuted in aligned groups (8 elements for the key / query tiles, 4
-// for the fp32 tiles) by the row's 8-row block, so that 8 lanes reading one
-// column from rows 8 apart hit 8 different bank groups while row segments
-// of a group stay contiguous.
+// columns (the transposed outputs, the column-wise scans), with unpadded
+// rows.  The column index is XOR-permuted in aligned groups (8 elements for
+// the key / query tiles, 4 for the fp32 C x C tiles) by
+// v(row) = (row mod G) ^ ((row / 8) mod 8), G the groups per row: the 16
+// consecutive rows of an MFMA fragment read and the 8 rows 8 apart of a
+// column read each land on distinct groups, while a group stays contiguous.
 template <typename T>
 __device__ __forceinline__ T* k2sw(T* base, int ld, int row, int col) {
-  return base + row * ld + (col ^ (((row >> 3) & 7) << 3));
+  const int g = ld >> 3;
+  return base + row * ld + (col ^ ((((row & (g - 1)) ^ ((row >> 3) & 7)) & (g - 1)) << 3));
 }
+__device__ __forceinline__ float* k2swc(float* base, int ld, int row, int col) {
+  const int g = ld >> 2;
+  return base + row * ld + (col ^ ((((row & (g - 1)) ^ ((row >> 3) & 7)) & (g - 1)) << 2));
+}
+// the per-channel gate tile (padded rows of d_k + 4 floats)
 __device__ __forceinline__ float* k2swf(float* base, int ld, int row, int col) {
   return base + row * ld + (col ^ (((row >> 3) & 7) << 2));
 }
@@ -153,8 +160,8 @@ __device__ __forceinline__ float* k2swf(float* base, int ld, int row, int col) {
 // gains.)
 template <typename T, int DK, int GATE, int PREC, int C>
 struct K2Smem {
-  static constexpr int LDK = DK + 8;          // padded row (elements)
-  static constexpr int LDA = C + 4;           // fp32 C x C rows
+  static constexpr int LDK = DK;              // row (elements; swizzled, unpadded)
+  static constexpr int LDA = C;               // fp32 C x C rows (swizzled, unpadded)
   static constexpr size_t kRow = sizeof(T) * C * LDK;
   static constexpr size_t kFloatCC = sizeof(float) * C * LDA;
   static constexpr size_t kR1 = kRow > kFloatCC ? kRow : kFloatCC;  // sK, later sA
@@ -167,14 +174,19 @@ struct K2Smem {
   static constexpr size_t kR3 = kRow;                               // sKt, later sX (NOQ)
   static constexpr size_t kScal = sizeof(float) * 8 * C;    // per-row scalars and the row norms
   static constexpr size_t kSeg = sizeof(float) * 2 * 256;   // preconditioner segment carries
-  static constexpr size_t kTotal = kR1 + kR2 + kR3 + kGc + kY + kScal + kSeg;
+  // the solve's partial products (sY) sit in the write-key tile, dead by the
+  // solve, unless the per-channel gate needs them while that tile is live
+  // (its gate prefix) or the tile is too small
+  static constexpr bool YSEP = GATE == kGateChannel || kR3 < kY;
+  static constexpr size_t kYs = YSEP ? kY : 0;
+  static constexpr size_t kTotal = kR1 + kR2 + kR3 + kGc + kYs + kScal + kSeg;
 };
 
 // BWD: also write the operand layouts the backward kernels read (P^T, M^T,
 // write-key rows, write-key rows decayed to the chunk end, (Lam o Q)^T and
 // -(Lam o K)^T; Lam the scalar or per-channel in-chunk decay).
 template <typename T, int DK, int GATE, int PREC, bool BWD, int C>
-__global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
+__global__ __launch_bounds__(256, 3) void k2_chunk_prep(FwdArgs a) {
   using SM = K2Smem<T, DK, GATE, PREC, C>;
   // row blocks of 16 tokens: wave w owns block w (C = 32: waves 2, 3 only
   // take part in the column-wise phases)
@@ -189,8 +201,8 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   T* sKt = reinterpret_cast<T*>(smem + SM::kR1 + SM::kR2);
   float* sGc = reinterpret_cast<float*>(smem + SM::kR1 + SM::kR2 + SM::kR3);
   float* sX = reinterpret_cast<float*>(smem + SM::kR1);   // R2, or with NOQ the write-key tile
-  float* sY = reinterpret_cast<float*>(smem + SM::kR1 + SM::kR2 + SM::kR3 + SM::kGc);
-  float* sBeta = sY + 4 * 16 * 17;
+  float* sY = reinterpret_cast<float*>(smem + SM::kR1 + SM::kR2 + (SM::YSEP ? SM::kR3 + SM::kGc : 0));
+  float* sBeta = reinterpret_cast<float*>(smem + SM::kR1 + SM::kR2 + SM::kR3 + SM::kGc + SM::kYs);
   float* sNrm = sBeta + 7 * C;   // row norms of the normalised write keys
   float* sBp = sBeta + C;
   float* sEgp = sBp + C;
@@ -347,23 +359,30 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     constexpr int NSEG = 256 / DK, SEG = C / NSEG;
     const int c = tid % DK, sg = tid / DK, r0 = sg * SEG;
     // this thread's key column over its segment and the rows' decay and
-    // betaP, in registers for every walk below
+    // betaP: held in registers for every walk below, or (backward mode,
+    // whose peak is elsewhere and tighter) read from LDS at each walk
+    constexpr bool SEGREG = !BWD;
     static_assert(SEG % 4 == 0, "segment rows come in float4 groups");
-    float kreg[SEG], eg[SEG], bpr[SEG];
+    float kreg[SEGREG ? SEG : 1], egr[SEGREG ? SEG : 1], bpr[SEGREG ? SEG : 1];
+    if constexpr (SEGREG) {
 #pragma unroll
-    for (int j = 0; j < SEG; ++j) kreg[j] = to_f(*k2sw(sK, LDK, r0 + j, c));
+      for (int j = 0; j < SEG; ++j) kreg[j] = to_f(*k2sw(sK, LDK, r0 + j, c));
 #pragma unroll
-    for (int j = 0; j < SEG; j += 4) {
-      const float4 e4 = *reinterpret_cast<const float4*>(sEgp + r0 + j);
-      const float4 b4 = *reinterpret_cast<const float4*>(sBp + r0 + j);
-      eg[j] = e4.x; eg[j + 1] = e4.y; eg[j + 2] = e4.z; eg[j + 3] = e4.w;
-      bpr[j] = b4.x; bpr[j + 1] = b4.y; bpr[j + 2] = b4.z; bpr[j + 3] = b4.w;
+      for (int j = 0; j < SEG; j += 4) {
+        const float4 e4 = *reinterpret_cast<const float4*>(sEgp + r0 + j);
+        const float4 b4 = *reinterpret_cast<const float4*>(sBp + r0 + j);
+        egr[j] = e4.x; egr[j + 1] = e4.y; egr[j + 2] = e4.z; egr[j + 3] = e4.w;
+        bpr[j] = b4.x; bpr[j + 1] = b4.y; bpr[j + 2] = b4.z; bpr[j + 3] = b4.w;
+      }
     }
+    auto kv_at = [&](int j) { return SEGREG ? kreg[SEGREG ? j : 0] : to_f(*k2sw(sK, LDK, r0 + j, c)); };
+    auto eg_at = [&](int j) { return SEGREG ? egr[SEGREG ? j : 0] : sEgp[r0 + j]; };
+    auto bp_at = [&](int j) { return SEGREG ? bpr[SEGREG ? j : 0] : sBp[r0 + j]; };
     float E = 1.f, Pp = 0.f;
 #pragma unroll
     for (int j = 0; j < SEG; ++j) {
-      E *= eg[j];
-      Pp = eg[j] * Pp + bpr[j] * kreg[j] * kreg[j];
+      E *= eg_at(j);
+      Pp = eg_at(j) * Pp + bp_at(j) * kv_at(j) * kv_at(j);
     }
     sSegE[sg * DK + c] = E;
     sSegP[sg * DK + c] = Pp;
@@ -375,8 +394,8 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       const float A_seg = A;
 #pragma unroll
       for (int j = 0; j < SEG; ++j) {
-        const float kv = kreg[j];
-        A = eg[j] * A + bpr[j] * kv * kv;
+        const float kv = kv_at(j);
+        A = eg_at(j) * A + bp_at(j) * kv * kv;
         *k2sw(sKt, LDK, r0 + j, c) = from_f<T>(squash_gain(A, mu, a.lnx) * kv);
       }
       if (a.knorm != kKnormNone) {
@@ -409,8 +428,8 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         A = A_seg;
 #pragma unroll
         for (int j = 0; j < SEG; ++j) {
-          const float kv = kreg[j];
-          A = eg[j] * A + bpr[j] * kv * kv;
+          const float kv = kv_at(j);
+          A = eg_at(j) * A + bp_at(j) * kv * kv;
           *k2sw(sKt, LDK, r0 + j, c) = from_f<T>(squash_gain(A, mu, a.lnx) * kv * sNrm[r0 + j]);
         }
       }
@@ -419,8 +438,8 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       // preconditioned query q / (A_r + ridge), A_r including token r
 #pragma unroll
       for (int j = 0; j < SEG; ++j) {
-        const float kv = kreg[j];
-        A = eg[j] * A + bpr[j] * kv * kv;
+        const float kv = kv_at(j);
+        A = eg_at(j) * A + bp_at(j) * kv * kv;
         *k2sw(sQ, LDK, r0 + j, c) = from_f<T>(to_f(*k2sw(sQ, LDK, r0 + j, c)) / (A + a.ridge));
       }
     }
@@ -432,9 +451,9 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       const float A_seg = A;
 #pragma unroll
       for (int j = 0; j < SEG; ++j) {
-        const float kv = kreg[j];
+        const float kv = kv_at(j);
         *k2sw(sKt, LDK, r0 + j, c) = from_f<T>(kv / (A + a.ridge));
-        A = eg[j] * A + bpr[j] * kv * kv;
+        A = eg_at(j) * A + bp_at(j) * kv * kv;
       }
       __syncthreads();
       if ((tid >> 2) < C) {
@@ -451,9 +470,9 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       A = A_seg;
 #pragma unroll
       for (int j = 0; j < SEG; ++j) {
-        const float kv = kreg[j];
+        const float kv = kv_at(j);
         *k2sw(sKt, LDK, r0 + j, c) = from_f<T>(kv / ((A + a.ridge) * sNrm[r0 + j]));
-        A = eg[j] * A + bpr[j] * kv * kv;
+        A = eg_at(j) * A + bp_at(j) * kv * kv;
       }
     }
   }
@@ -708,24 +727,23 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
   for (int j = 0; j < NB; ++j) {
     if (j > w || !(NB == 4 || w < NB)) break;
 #pragma unroll
-    for (int ii = 0; ii < 4; ++ii) sA[(16 * w + 4 * lg + ii) * LDA + 16 * j + lr] = accA[j][ii];
+    for (int ii = 0; ii < 4; ++ii) *k2swc(sA, LDA, 16 * w + 4 * lg + ii, 16 * j + lr) = accA[j][ii];
   }
   __syncthreads();
 
   // ---- X = (I + At)^{-1}: diagonal 16x16 blocks by forward substitution
   if ((NB == 4 || w < NB) && lg == 0) {
     const int col = lr;
-    const float* Ab = sA + (16 * w) * LDA + 16 * w;
     float x[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       float s = (r == col) ? 1.f : 0.f;
 #pragma unroll
-      for (int t = 0; t < r; ++t) s -= Ab[r * LDA + t] * x[t];
+      for (int t = 0; t < r; ++t) s -= *k2swc(sA, LDA, 16 * w + r, 16 * w + t) * x[t];
       x[r] = s;
     }
 #pragma unroll
-    for (int r = 0; r < 16; ++r) *k2swf(sX, LDA, 16 * w + r, 16 * w + col) = x[r];
+    for (int r = 0; r < 16; ++r) *k2swc(sX, LDA, 16 * w + r, 16 * w + col) = x[r];
   }
   __syncthreads();
   // off-diagonal blocks, by distance from the diagonal:
@@ -737,8 +755,8 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
     floatx4 y = {0.f, 0.f, 0.f, 0.f};
     if (active) {
       for (int kb = 0; kb < 4 * d; ++kb) {
-        const float av = sA[(16 * ib + lr) * LDA + 16 * j + 4 * kb + lg];
-        const float bv = *k2swf(sX, LDA, 16 * j + 4 * kb + lg, 16 * j + lr);
+        const float av = *k2swc(sA, LDA, 16 * ib + lr, 16 * j + 4 * kb + lg);
+        const float bv = *k2swc(sX, LDA, 16 * j + 4 * kb + lg, 16 * j + lr);
         mma4(y, av, bv);
       }
 #pragma unroll
@@ -749,12 +767,12 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       floatx4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        const float av = *k2swf(sX, LDA, 16 * ib + lr, 16 * ib + 4 * kb + lg);
+        const float av = *k2swc(sX, LDA, 16 * ib + lr, 16 * ib + 4 * kb + lg);
         const float bv = Yw[(4 * kb + lg) * 17 + lr];
         mma4(z, av, bv);
       }
 #pragma unroll
-      for (int ii = 0; ii < 4; ++ii) *k2swf(sX, LDA, 16 * ib + 4 * lg + ii, 16 * j + lr) = -z[ii];
+      for (int ii = 0; ii < 4; ++ii) *k2swc(sX, LDA, 16 * ib + 4 * lg + ii, 16 * j + lr) = -z[ii];
     }
     __syncthreads();
   }
@@ -773,7 +791,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
       for (int s = 0; s < 8; ++s) {
         const int t = t0v + s;
         const bool lower = (t >> 4) < (r >> 4) || ((t >> 4) == (r >> 4) && t <= r);
-        f.set(s, lower ? *k2swf(sX, LDA, r, t) * sBeta[t] : 0.f);
+        f.set(s, lower ? *k2swc(sX, LDA, r, t) * sBeta[t] : 0.f);
       }
       st8(Tout + r * C + t0v, f);
     }
@@ -793,7 +811,7 @@ __global__ __launch_bounds__(256) void k2_chunk_prep(FwdArgs a) {
         const int t = t0v + s2;
         // M^T[r][t] = M[t][r]; M is lower triangular (block-lower in sX)
         const bool upper = (r >> 4) < (t >> 4) || ((r >> 4) == (t >> 4) && r <= t);
-        ft.set(s2, upper ? *k2swf(sX, LDA, t, r) : 0.f);
+        ft.set(s2, upper ? *k2swc(sX, LDA, t, r) : 0.f);
       }
       st8(MtT + r * C + t0v, ft);
     }
