@@ -143,6 +143,8 @@ def algorithmic_per_token_head(spec, train=False, precond="squash"):
     return flop_fwd, flop_bwd, stages, {"fwd": fwd_m, "bwd": bwd_m}
 
 
+SCAN_STAGES = ("chunk_scan", "bwd_state_save_scan", "bwd_state_adjoint_scan")
+
 KERNELS = {
     "precond": "k1_precond_summary+k1_precond_carry",
     "chunk_prep": "k2_chunk_prep",
@@ -269,13 +271,15 @@ def measured_traffic(workload, mode, stage):
     return int(m.group(1)) if m else None
 
 
-def roofline_of(stage, ms, stages, token_heads, train=False):
+def roofline_of(stage, ms, stages, token_heads, train=False, segs=1):
     """Roofline object for one kernel stage from its measured average time:
     `achieved` = the stage's method bytes (or FLOPs, when its method
     intensity is above the bf16 ridge) per launch / its time; the design's
     own compulsory bytes are reported beside it (design_bytes_per_launch,
     design_frac), and the counter traffic, when known, with its ratio to
-    the method bytes."""
+    the method bytes.  When the scans are split along the sequence (`segs`
+    > 1), a scan stage is two launches of its kernel with the segment
+    composition between them, and its figures are per stage."""
     dflop, mbytes, dbytes = stages[stage]
     sec = ms / 1e3
     if dflop / mbytes >= PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
@@ -291,6 +295,11 @@ def roofline_of(stage, ms, stages, token_heads, train=False):
     roof["kernel"] = KERNELS[stage + ("_train" if train and stage in
                                      ("chunk_prep", "chunk_scan") else "")]
     roof["stage"] = stage
+    roof["launches_in_stage"] = 1
+    if segs > 1 and stage in SCAN_STAGES:
+        roof["kernel"] = (f"{roof['kernel']} x2 + seg_compose (sequence "
+                          f"split into {segs} segments)")
+        roof["launches_in_stage"] = 3
     roof["avg_ms"] = ms
     roof["alg_bytes_per_launch"] = mbytes * token_heads
     roof["alg_bytes_per_token_head"] = mbytes
@@ -608,7 +617,8 @@ def main(argv=None):
     token_heads = B * T * H
     flop_fwd, flop_bwd, stages, passes = algorithmic_per_token_head(
         spec, train, args.precond)
-    roof = roofline_of(dom, dom_ms, stages, token_heads, train)
+    segs = pdn.pdn_scan_segments(prob)
+    roof = roofline_of(dom, dom_ms, stages, token_heads, train, segs)
     mode = "train" if train else ("recompute" if bwd else "forward")
     roof["traffic"] = (measured_traffic(args.workload, mode, dom) if sq
                        else None)
@@ -621,7 +631,7 @@ def main(argv=None):
         roof["kernel"] = roof["kernel"].replace("p12_", "p12c_")
     kernels = {}
     for k, v in stage_ms.items():
-        r = roofline_of(k, v, stages, token_heads, train)
+        r = roofline_of(k, v, stages, token_heads, train, segs)
         kernels[k] = {"frac": r["frac"], "design_frac": r["design_frac"],
                       "mfma_frac": r["mfma_frac"]}
 
@@ -657,6 +667,7 @@ def main(argv=None):
                             if bwd else "forward"),
                    "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
                    "chunk": spec.chunk, "gate": spec.gate,
+                   "scan_segments": segs,
                    "precond": args.precond, "x": spec.x,
                    **({"ridge": args.ridge} if not sq else {}),
                    **({"knorm": args.knorm} if args.knorm != "none" else {}),
