@@ -1349,22 +1349,25 @@ __global__ __launch_bounds__(256) void k3_chunk_scan(FwdArgs a) {
 // false), start(1) = end(0) and start(s + 1) = Phi_s start(s) + end(s) up to
 // s = S - 2; reverse (the state-adjoint scan, REV = true), start(S - 2) =
 // end(S - 1) and start(s - 1) = Phi_s start(s) + end(s) down to s = 1 (end:
-// the exact end of the first segment run, a local end otherwise).  One
-// workgroup per head, fp32 on MFMA (16x16x4): wave w owns rows
-// [w DK/4, (w+1) DK/4) of every product, all DV columns.
+// the exact end of the first segment run, a local end otherwise).  The
+// columns of a state are independent in these products, so each workgroup
+// takes one head and 32 of its d_v columns; fp32 on MFMA (16x16x4): wave w
+// owns rows [w DK/4, (w+1) DK/4) of every product.
 template <int DK, int DV, bool REV>
 __global__ __launch_bounds__(256) void seg_compose(FwdArgs a) {
-  constexpr int RW = DK / 4, RT = RW / 16, CV = DV / 16;
-  constexpr int LS = DV + 4, LP = DK + 4;   // padded rows
+  constexpr int NSL = DV / 32;              // column slabs per head
+  constexpr int RW = DK / 4, RT = RW / 16, CV = 2;
+  constexpr int LS = 48, LP = DK + 4;       // padded rows: conflict-free fragment reads
   __shared__ __attribute__((aligned(16))) float sS[DK * LS];
   __shared__ __attribute__((aligned(16))) float sP[DK * LP];
-  const int64_t bh = blockIdx.x;
+  const int64_t bh = blockIdx.x / NSL;
+  const int col0 = static_cast<int>(blockIdx.x % NSL) * 32;
   const int tid = threadIdx.x, w = tid >> 6, lr = tid & 15, lg = (tid & 63) >> 4;
   const int64_t BHDK = a.BH * static_cast<int64_t>(DK);
   const int S = a.seg_cnt;
-  auto state = [&](float* base, int sg) { return base + (sg * BHDK + bh * DK) * DV; };
+  auto state = [&](float* base, int sg) { return base + (sg * BHDK + bh * DK) * DV + col0; };
   const int first = REV ? S - 1 : 0, step = REV ? -1 : 1;
-  // acc[rt][cv][ii]: row w RW + 16 rt + 4 lg + ii, column 16 cv + lr
+  // acc[rt][cv][ii]: row w RW + 16 rt + 4 lg + ii, column col0 + 16 cv + lr
   floatx4 acc[RT][CV];
   auto load_acc = [&](const float* src) {
 #pragma unroll
@@ -1390,12 +1393,18 @@ __global__ __launch_bounds__(256) void seg_compose(FwdArgs a) {
     const int sg = first + step * k;   // the middle segment crossed
     __syncthreads();   // the previous product is done with the LDS
     store_acc(sS, LS);
+    // every global load of the step is issued before the first LDS store
     const float* phi = a.seg_phi + (sg * BHDK + bh * DK) * DK;
-    for (int j = tid * 4; j < DK * DK; j += 1024) {
-      const float4 v = *reinterpret_cast<const float4*>(phi + j);
-      *reinterpret_cast<float4*>(sP + (j / DK) * LP + j % DK) = v;
-    }
+    constexpr int NPV = DK * DK / 1024;   // float4 per thread
+    float4 pv[NPV];
+#pragma unroll
+    for (int u = 0; u < NPV; ++u) pv[u] = *reinterpret_cast<const float4*>(phi + tid * 4 + u * 1024);
     load_acc(state(a.seg_end, sg));
+#pragma unroll
+    for (int u = 0; u < NPV; ++u) {
+      const int j = tid * 4 + u * 1024;
+      *reinterpret_cast<float4*>(sP + (j / DK) * LP + j % DK) = pv[u];
+    }
     __syncthreads();
 #pragma unroll 4
     for (int kk = 0; kk < DK; kk += 4) {
@@ -1415,11 +1424,11 @@ __global__ __launch_bounds__(256) void seg_compose(FwdArgs a) {
 
 template <bool REV>
 static hipError_t launch_compose(const FwdArgs& a, hipStream_t s) {
-  const dim3 grid(static_cast<unsigned>(a.BH));
-  if (a.dk == 64 && a.dv == 64) hipLaunchKernelGGL((seg_compose<64, 64, REV>), grid, dim3(256), 0, s, a);
-  else if (a.dk == 64) hipLaunchKernelGGL((seg_compose<64, 128, REV>), grid, dim3(256), 0, s, a);
-  else if (a.dv == 64) hipLaunchKernelGGL((seg_compose<128, 64, REV>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((seg_compose<128, 128, REV>), grid, dim3(256), 0, s, a);
+  const unsigned n = static_cast<unsigned>(a.BH * (a.dv / 32));
+  if (a.dk == 64 && a.dv == 64) hipLaunchKernelGGL((seg_compose<64, 64, REV>), dim3(n), dim3(256), 0, s, a);
+  else if (a.dk == 64) hipLaunchKernelGGL((seg_compose<64, 128, REV>), dim3(n), dim3(256), 0, s, a);
+  else if (a.dv == 64) hipLaunchKernelGGL((seg_compose<128, 64, REV>), dim3(n), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((seg_compose<128, 128, REV>), dim3(n), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -294,7 +294,7 @@ static pdn_status chunk_fwd_impl(const pdn_problem* p, const pdn_inputs* in, pdn
   a.o = out->o; a.S_T = out->S_T; a.A_T = out->A_T;
   char* w = static_cast<char*>(ws);
   if (need_ws) {
-    set_forward_ws(a, L, p, w);
+    set_forward_ws(a, train ? LB.f : L, p, w);
     if (train) set_residuals(a, LB, w);
   }
   const hipError_t e =
