@@ -433,9 +433,9 @@ def main(argv=None):
                          "step (reference kernel for HBM counter scaling)")
     args = ap.parse_args(argv)
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is "
-              "not supported (the (b, h) sharding across GPUs is described "
-              "in DESIGN.md but not built)", file=sys.stderr)
+        print(f"bench.py: one GPU only; --gpus {args.gpus} is not supported "
+              "(sharding the (batch, head) pairs over several GPUs is not "
+              "implemented)", file=sys.stderr)
         return 2
 
     if args.sweep:
